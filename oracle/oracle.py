@@ -1,0 +1,299 @@
+"""Python face of the CPU oracle (ctypes over liboracle.so, numpy host arrays).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg, never by the GPU library or its binding.
+
+Each function follows one step of the paper's quantized dataflow (arXiv
+2011.14504, Sec. 3) and says which equation; the composition of a layer
+(integer sum, then the quantizer) is written out here in the order the paper
+applies it.  Quantized tensors are (codes, exponent) pairs: value = code*2^exp.
+"""
+import ctypes as C
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+# L1BN bit-widths, Sec. 5 implementation details (DeepLabv3 row):
+# k_mu = k_sigma = k_xhat = 16, k_gamma = k_beta = 8, k_A = k_E1 = 8, k_E2 = 16.
+BN_DEFAULT = dict(k_mu=16, k_sigma=16, k_xhat=16, k_gamma=8, k_beta=8,
+                  k_A=8, k_E1=8, k_E2=16, eps_code=0, relu=1)
+_BN_KEYS = ["k_mu", "k_sigma", "k_xhat", "k_gamma", "k_beta", "k_A", "k_E1",
+            "k_E2", "eps_code", "relu"]
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        path = _build.LIB
+        if not os.path.exists(path):
+            _build.build()
+        L = C.CDLL(path)
+        P = C.c_void_p
+        i64, i32, u64, u32 = C.c_int64, C.c_int32, C.c_uint64, C.c_uint32
+        L.orc_philox4x32_10.argtypes = [P, P, P]
+        L.orc_draw_u64.argtypes = [u64, u32, u32, u64]
+        L.orc_draw_u64.restype = u64
+        L.orc_uq_code_f64.argtypes = [C.c_double, C.c_int]
+        L.orc_uq_code_f64.restype = i64
+        L.orc_quantize_f32.argtypes = [P, i64, C.c_int, C.c_int, P, P]
+        L.orc_requant.argtypes = [P, i64, i32, C.c_int, C.c_int, C.c_int, u64, u32, u32, P, P]
+        for f in ("orc_conv_fwd_raw", "orc_conv_bwd_data_raw", "orc_conv_bwd_weight_raw"):
+            getattr(L, f).argtypes = [P, P, P, P]
+            getattr(L, f).restype = None
+        L.orc_bn_fwd.argtypes = [P, i32, i64, i64, P, P, P, P, P, P, P, P, P]
+        L.orc_bn_bwd.argtypes = [P, i32, P, i32, i64, i64, P, P, P, P, P, P, P, P, P, P, P]
+        L.orc_weight_update.argtypes = [P, i64, P, i32, C.c_int, C.c_int, C.c_int, C.c_int, P]
+        L.orc_weight_quant.argtypes = [P, i64, C.c_int, C.c_int, P]
+        L.orc_maxpool_fwd.argtypes = [P, i64, i64, i64, i64, i64, i64, i64, P]
+        L.orc_maxpool_fwd.restype = None
+        L.orc_maxpool_bwd_raw.argtypes = [P, P, i64, i64, i64, i64, i64, i64, i64, P]
+        L.orc_maxpool_bwd_raw.restype = None
+        L.orc_num_threads.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise OracleError(f"{what}: oracle returned {rc}")
+
+
+def num_threads():
+    return lib().orc_num_threads()
+
+
+# --------------------------------------------------------------------------
+# random numbers for stochastic rounding
+# --------------------------------------------------------------------------
+def philox4x32_10(ctr, key):
+    c = np.asarray(ctr, dtype=np.uint32)
+    k = np.asarray(key, dtype=np.uint32)
+    o = np.zeros(4, dtype=np.uint32)
+    lib().orc_philox4x32_10(_p(c), _p(k), _p(o))
+    return o
+
+
+def draw_u64(seed, tensor_id, step, idx):
+    return int(lib().orc_draw_u64(seed, tensor_id, step, idx))
+
+
+# --------------------------------------------------------------------------
+# quantizers (Sec. 3.1)
+# --------------------------------------------------------------------------
+def uq_code(x, k):
+    """Eq. 2 on one real number (exact for float32/float64 input)."""
+    return int(lib().orc_uq_code_f64(float(x), int(k)))
+
+
+def quantize_f32(x, k, mode="sq"):
+    """float32 tensor -> (int64 codes, exponent); mode 'uq' (Eq. 2) or 'sq' (Eq. 4)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.zeros(x.shape, dtype=np.int64)
+    e = np.zeros(1, dtype=np.int32)
+    rc = lib().orc_quantize_f32(_p(x), x.size, int(k), {"uq": 0, "sq": 1}[mode], _p(codes), _p(e))
+    _check(rc, "quantize_f32")
+    return codes, int(e[0])
+
+
+def requant(acc, in_exp, k, stochastic=False, keep_scale=True, seed=0, tensor_id=0, step=0):
+    """SQ (Eq. 4) or RQ (Eq. 5-6) of an integer tensor -> (int64 codes, exponent).
+    keep_scale=False drops the magnitude (Eq. 18)."""
+    a = np.ascontiguousarray(acc, dtype=np.int64)
+    codes = np.zeros(a.shape, dtype=np.int64)
+    e = np.zeros(1, dtype=np.int32)
+    rc = lib().orc_requant(_p(a), a.size, int(in_exp), int(k), int(bool(stochastic)),
+                           int(bool(keep_scale)), int(seed), int(tensor_id), int(step),
+                           _p(codes), _p(e))
+    _check(rc, "requant")
+    return codes, int(e[0])
+
+
+# --------------------------------------------------------------------------
+# convolutions
+# --------------------------------------------------------------------------
+def conv_out_hw(geom):
+    N, H, W, Cc, K, R, S, sh, sw, ph, pw, dh, dw = geom
+    P = (H + 2 * ph - dh * (R - 1) - 1) // sh + 1
+    Q = (W + 2 * pw - dw * (S - 1) - 1) // sw + 1
+    return P, Q
+
+
+def _geom(geom):
+    return np.asarray(geom, dtype=np.int64)
+
+
+def conv_fwd_raw(x, w, geom):
+    """Exact integer forward sums (NHWC x, KRSC w) -> int64 NPQK."""
+    N, H, W, Cc, K, R, S = geom[:7]
+    P, Q = conv_out_hw(geom)
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    w = np.ascontiguousarray(w, dtype=np.int8)
+    out = np.zeros((N, P, Q, K), dtype=np.int64)
+    lib().orc_conv_fwd_raw(_p(x), _p(w), _p(_geom(geom)), _p(out))
+    return out
+
+
+def conv_bwd_data_raw(dy, w, geom):
+    N, H, W, Cc = geom[:4]
+    dy = np.ascontiguousarray(dy, dtype=np.int8)
+    w = np.ascontiguousarray(w, dtype=np.int8)
+    out = np.zeros((N, H, W, Cc), dtype=np.int64)
+    lib().orc_conv_bwd_data_raw(_p(dy), _p(w), _p(_geom(geom)), _p(out))
+    return out
+
+
+def conv_bwd_weight_raw(dy, x, geom):
+    K, R, S, Cc = geom[4], geom[5], geom[6], geom[3]
+    dy = np.ascontiguousarray(dy, dtype=np.int8)
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    out = np.zeros((K, R, S, Cc), dtype=np.int64)
+    lib().orc_conv_bwd_weight_raw(_p(dy), _p(x), _p(_geom(geom)), _p(out))
+    return out
+
+
+def conv_fwd(x, x_exp, w, w_exp, geom, k_A=8):
+    """Conv forward then SQ to k_A bits (activation quantizer on the MAC output)."""
+    acc = conv_fwd_raw(x, w, geom)
+    return requant(acc, x_exp + w_exp, k_A)
+
+
+def conv_bwd_data(dy, dy_exp, w, w_exp, geom, k_E1=8):
+    """Backward-data sums then Q_E = SQ(., k_E1) (Eq. 16)."""
+    acc = conv_bwd_data_raw(dy, w, geom)
+    return requant(acc, dy_exp + w_exp, k_E1)
+
+
+def conv_bwd_weight(dy, dy_exp, x, x_exp, geom, k_G=8, keep_scale=True, seed=0,
+                    tensor_id=0, step=0):
+    """Backward-weight sums then Q_G: stochastic RQ (Eq. 17, or Eq. 18 when
+    keep_scale=False)."""
+    acc = conv_bwd_weight_raw(dy, x, geom)
+    return requant(acc, dy_exp + x_exp, k_G, stochastic=True, keep_scale=keep_scale,
+                   seed=seed, tensor_id=tensor_id, step=step)
+
+
+# --------------------------------------------------------------------------
+# L1 batch normalization (Eq. 12-15) and its backward
+# --------------------------------------------------------------------------
+def _bn_cfg(cfg):
+    d = dict(BN_DEFAULT)
+    if cfg:
+        d.update(cfg)
+    return np.asarray([d[k] for k in _BN_KEYS], dtype=np.int32)
+
+
+def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None):
+    """x: int8 [..., C] (NHWC).  Returns dict with A codes (int8), exponent,
+    n_mu, n_sigma (per channel), b (exponent of Q_xhat's scale) and the
+    per-element xhat codes."""
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    Cc = x.shape[-1]
+    M = x.size // Cc
+    g = np.ascontiguousarray(gamma_q, dtype=np.int8)
+    b = np.ascontiguousarray(beta_q, dtype=np.int8)
+    out = np.zeros(x.shape, dtype=np.int8)
+    e = np.zeros(1, dtype=np.int32)
+    n_mu = np.zeros(Cc, dtype=np.int32)
+    n_sig = np.zeros(Cc, dtype=np.int32)
+    bx = np.zeros(1, dtype=np.int32)
+    nxh = np.zeros(x.shape, dtype=np.int16)
+    rc = lib().orc_bn_fwd(_p(x), int(x_exp), M, Cc, _p(g), _p(b), _p(_bn_cfg(cfg)),
+                          _p(out), _p(e), _p(n_mu), _p(n_sig), _p(bx), _p(nxh))
+    _check(rc, "bn_fwd")
+    return dict(y=out, y_exp=int(e[0]), n_mu=n_mu, n_sigma=n_sig, b=int(bx[0]), xhat=nxh)
+
+
+def bn_bwd(dA, dA_exp, x, x_exp, gamma_q, beta_q, cfg=None, want_pre=False):
+    """Backward of L1BN (+ReLU).  Returns dict with dx codes, exponent, raw
+    dgamma/dbeta sums and their exponents; dx_pre (float64 value of dx before
+    its quantizer) and the count of channels whose pre-quantizer dx does not
+    sum to exactly zero."""
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    dA = np.ascontiguousarray(dA, dtype=np.int8)
+    Cc = x.shape[-1]
+    M = x.size // Cc
+    g = np.ascontiguousarray(gamma_q, dtype=np.int8)
+    b = np.ascontiguousarray(beta_q, dtype=np.int8)
+    dx = np.zeros(x.shape, dtype=np.int8)
+    e = np.zeros(1, dtype=np.int32)
+    dg = np.zeros(Cc, dtype=np.int64)
+    db = np.zeros(Cc, dtype=np.int64)
+    dge = np.zeros(1, dtype=np.int32)
+    dbe = np.zeros(1, dtype=np.int32)
+    pre = np.zeros(x.shape, dtype=np.float64) if want_pre else None
+    zf = np.zeros(1, dtype=np.int64)
+    rc = lib().orc_bn_bwd(_p(dA), int(dA_exp), _p(x), int(x_exp), M, Cc, _p(g), _p(b),
+                          _p(_bn_cfg(cfg)), _p(dx), _p(e), _p(dg), _p(db), _p(dge), _p(dbe),
+                          _p(pre) if want_pre else None, _p(zf))
+    _check(rc, "bn_bwd")
+    return dict(dx=dx, dx_exp=int(e[0]), dgamma=dg, dbeta=db, dgamma_exp=int(dge[0]),
+                dbeta_exp=int(dbe[0]), dx_pre=pre, zero_sum_failures=int(zf[0]))
+
+
+# --------------------------------------------------------------------------
+# update (Eq. 19) and weight quantizer (Eq. 8)
+# --------------------------------------------------------------------------
+def weight_update(master, g_codes, g_exp, lr_shift, master_exp=-23, k_U=24, k_W=8):
+    """Returns (new master codes int32, new W_q codes int8); master is not modified."""
+    m = np.array(master, dtype=np.int32, copy=True).ravel()
+    g = np.ascontiguousarray(g_codes, dtype=np.int8).ravel()
+    wq = np.zeros(m.shape, dtype=np.int8)
+    rc = lib().orc_weight_update(_p(m), m.size, _p(g), int(g_exp), int(lr_shift),
+                                 int(master_exp), int(k_U), int(k_W), _p(wq))
+    _check(rc, "weight_update")
+    shape = np.shape(master)
+    return m.reshape(shape), wq.reshape(shape)
+
+
+def weight_quant(master, k_U=24, k_W=8):
+    m = np.ascontiguousarray(master, dtype=np.int32)
+    wq = np.zeros(m.shape, dtype=np.int8)
+    rc = lib().orc_weight_quant(_p(m), m.size, int(k_U), int(k_W), _p(wq))
+    _check(rc, "weight_quant")
+    return wq
+
+
+def master_init(w_float, k_U=24):
+    """Eq. 7: W_m = UQ(W, k_U) -> int32 codes with exponent 1-k_U."""
+    codes, e = quantize_f32(w_float, k_U, mode="uq")
+    return codes.astype(np.int32), e
+
+
+# --------------------------------------------------------------------------
+# max pooling
+# --------------------------------------------------------------------------
+def maxpool_fwd(x, k, stride, pad):
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    N, H, W, Cc = x.shape
+    P = (H + 2 * pad - k) // stride + 1
+    Q = (W + 2 * pad - k) // stride + 1
+    y = np.zeros((N, P, Q, Cc), dtype=np.int8)
+    lib().orc_maxpool_fwd(_p(x), N, H, W, Cc, k, stride, pad, _p(y))
+    return y
+
+
+def maxpool_bwd_raw(dy, x, k, stride, pad):
+    """Routes each output error to its forward maximum; overlaps add exactly."""
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    dy = np.ascontiguousarray(dy, dtype=np.int8)
+    N, H, W, Cc = x.shape
+    raw = np.zeros(x.shape, dtype=np.int64)
+    lib().orc_maxpool_bwd_raw(_p(dy), _p(x), N, H, W, Cc, k, stride, pad, _p(raw))
+    return raw
+
+
+def maxpool_bwd(dy, dy_exp, x, k, stride, pad, k_E1=8):
+    """Routed errors, then Q_E (Eq. 16)."""
+    return requant(maxpool_bwd_raw(dy, x, k, stride, pad), dy_exp, k_E1)

@@ -1,0 +1,171 @@
+"""Pins of the oracle's L1 batch normalization (Eq. 12-15) and its backward:
+the hand-worked example, the exact-rational brute force of the real-valued
+formulas, finite differences of Eq. 12-13, the zero-sum property of the
+backward and the Gaussian L1/L2 deviation ratio."""
+import json
+import math
+import os
+from fractions import Fraction as Fr
+
+import numpy as np
+import pytest
+
+import bruteforce as bf
+from paper_2011_14504_amd import synth
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")))
+CFG = dict(k_mu=16, k_sigma=16, k_xhat=16, k_gamma=8, k_beta=8, k_A=8, k_E1=8,
+           k_E2=16, eps_code=0, relu=1)
+
+
+def _cols(codes, e):
+    """[M, C] codes -> per-channel lists of rational values."""
+    a = np.asarray(codes).reshape(-1, np.asarray(codes).shape[-1])
+    return [[Fr(int(v)) * Fr(2) ** e for v in a[:, c]] for c in range(a.shape[1])]
+
+
+def test_l1bn_hand_example(orc):
+    g = GOLD["l1bn_fwd"]
+    x = np.array(g["x_codes"], np.int8).reshape(4, 1)
+    r = orc.bn_fwd(x, g["x_exp"], [g["gamma_code"]], [g["beta_code"]], CFG)
+    assert int(r["n_mu"][0]) == g["n_mu"] and int(r["n_sigma"][0]) == g["n_sigma"]
+    assert r["b"] == g["b"]
+    assert r["xhat"].ravel().tolist() == g["xhat_codes"]
+    assert r["y"].ravel().tolist() == g["A_codes"] and r["y_exp"] == g["A_exp"]
+
+
+def _bn_case(seed, M, C, x_exp, cfg, rand_affine=True, const_chan=False):
+    x = synth.int_codes(seed, (M, C))
+    if const_chan:
+        x[:, 0] = 17
+    if rand_affine:
+        gq = synth.int_codes(seed + 1, (C,))
+        bq = synth.int_codes(seed + 2, (C,))
+    else:
+        gq = np.full(C, 64, np.int8)
+        bq = np.zeros(C, np.int8)
+    return x, gq, bq
+
+
+CASES = [
+    dict(seed=1, M=6, C=3, x_exp=-7, cfg={}),
+    dict(seed=2, M=5, C=2, x_exp=-2, cfg=dict(relu=0)),
+    dict(seed=3, M=7, C=2, x_exp=-16, cfg=dict(eps_code=1)),
+    dict(seed=4, M=4, C=3, x_exp=3, cfg=dict(k_E2=8)),
+    dict(seed=5, M=8, C=2, x_exp=-9, cfg=dict(relu=0, k_E2=8), const_chan=True),
+    dict(seed=6, M=3, C=4, x_exp=-20, cfg={}),
+    dict(seed=7, M=9, C=1, x_exp=-7, cfg=dict(k_xhat=8, k_mu=8, k_sigma=8)),
+    dict(seed=8, M=6, C=2, x_exp=-7, cfg={}, rand_affine=False),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"seed{c['seed']}")
+def test_l1bn_fwd_vs_bruteforce(orc, case):
+    cfg = dict(CFG, **case["cfg"])
+    x, gq, bq = _bn_case(case["seed"], case["M"], case["C"], case["x_exp"], cfg,
+                         case.get("rand_affine", True), case.get("const_chan", False))
+    r = orc.bn_fwd(x, case["x_exp"], gq, bq, cfg)
+    gam = [Fr(int(v)) * Fr(2) ** (2 - cfg["k_gamma"]) for v in gq]
+    bet = [Fr(int(v)) * Fr(2) ** (2 - cfg["k_beta"]) for v in bq]
+    ref = bf.l1bn_forward(_cols(x, case["x_exp"]), gam, bet, cfg)
+    e_mu = 2 - cfg["k_mu"]
+    assert [Fr(int(v)) * Fr(2) ** e_mu for v in r["n_mu"]] == ref["mu_q"]
+    assert [Fr(int(v)) * Fr(2) ** (2 - cfg["k_sigma"]) for v in r["n_sigma"]] == ref["sigma_q"]
+    e_xh = r["b"] - (cfg["k_xhat"] - 1)
+    assert _cols(r["xhat"], e_xh) == ref["xhat_q"]
+    assert _cols(r["y"], r["y_exp"]) == ref["A"]
+    lim = 2 ** (cfg["k_A"] - 1) - 1
+    assert r["y"].max() <= lim and r["y"].min() >= -lim
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"seed{c['seed']}")
+def test_l1bn_bwd_vs_bruteforce(orc, case):
+    cfg = dict(CFG, **case["cfg"])
+    x, gq, bq = _bn_case(case["seed"], case["M"], case["C"], case["x_exp"], cfg,
+                         case.get("rand_affine", True), case.get("const_chan", False))
+    dA = synth.int_codes(case["seed"] + 50, x.shape)
+    dA_exp = -20
+    r = orc.bn_bwd(dA, dA_exp, x, case["x_exp"], gq, bq, cfg, want_pre=True)
+    gam = [Fr(int(v)) * Fr(2) ** (2 - cfg["k_gamma"]) for v in gq]
+    bet = [Fr(int(v)) * Fr(2) ** (2 - cfg["k_beta"]) for v in bq]
+    ref = bf.l1bn_backward(_cols(x, case["x_exp"]), _cols(dA, dA_exp), gam, bet, cfg)
+    assert [Fr(int(v)) * Fr(2) ** r["dbeta_exp"] for v in r["dbeta"]] == ref["dbeta"]
+    assert [Fr(int(v)) * Fr(2) ** r["dgamma_exp"] for v in r["dgamma"]] == ref["dgamma"]
+    assert _cols(r["dx"], r["dx_exp"]) == ref["E1"]
+    pre = r["dx_pre"]
+    for c in range(x.shape[1]):
+        for i in range(x.shape[0]):
+            assert abs(pre[i, c] - float(ref["dx_pre"][c][i])) <= 1e-12 * max(1e-300, abs(float(ref["dx_pre"][c][i]))) + 1e-300
+    assert r["zero_sum_failures"] == 0
+
+
+def _l1bn_float(x):
+    mu = x.mean(axis=0)
+    sig = np.abs(x - mu).mean(axis=0)
+    return (x - mu) / sig
+
+
+def test_l1bn_bwd_finite_differences(orc):
+    # the oracle's dx before E1's quantizer against central differences of the
+    # unquantized Eq. 12-13 (eps = 0); E2 exact (k_E2 = 16) and no ReLU, so the
+    # upstream gradient is exactly gamma_q * dA.  The quantized statistics
+    # (mu_q, sigma_q, xhat_q) leave a ~1e-4 relative gap; dropping the
+    # mean-of-sign term of d sigma/dx would leave a gap of order 1e-1.
+    M, C = 41, 3
+    x_exp = -7
+    x = synth.int_codes(61, (M, C))
+    gq = np.array([64, -90, 37], np.int8)
+    bq = np.zeros(C, np.int8)
+    dA = synth.int_codes(62, (M, C))
+    cfg = dict(CFG, relu=0)
+    r = orc.bn_bwd(dA, -20, x, x_exp, gq, bq, cfg, want_pre=True)
+    xf = x.astype(np.float64) * 2.0 ** x_exp
+    gup = (gq.astype(np.float64) * 2.0 ** -6) * dA.astype(np.float64) * 2.0 ** -20
+    mu = xf.mean(axis=0)
+    assert np.all(np.abs(xf - mu) > 1e-9)      # no element at the kink of |x - mu|
+    h = 1e-7
+    fd = np.zeros_like(xf)
+    for i in range(M):
+        for c in range(C):
+            xp = xf.copy(); xp[i, c] += h
+            xm = xf.copy(); xm[i, c] -= h
+            fd[i, c] = ((gup * _l1bn_float(xp)).sum() - (gup * _l1bn_float(xm)).sum()) / (2 * h)
+    scale = np.abs(fd).max()
+    err = np.abs(r["dx_pre"] - fd).max() / scale
+    assert err < 2e-3, err
+    # without the mean-of-sign term the derivative would be visibly different
+    s = np.sign(xf - mu)
+    xh = _l1bn_float(xf)
+    sig = np.abs(xf - mu).mean(axis=0)
+    no_sign_mean = (gup - gup.mean(0) - (gup * xh).mean(0) * s) / sig
+    assert np.abs(no_sign_mean - fd).max() / scale > 20 * err
+
+
+def test_l1bn_bwd_zero_sum_large(orc):
+    x = synth.int_codes(71, (3000, 8))
+    dA = synth.int_codes(72, (3000, 8))
+    gq = synth.int_codes(73, (8,))
+    bq = synth.int_codes(74, (8,))
+    for kE2 in (8, 16):
+        r = orc.bn_bwd(dA, -20, x, -7, gq, bq, dict(CFG, k_E2=kE2))
+        assert r["zero_sum_failures"] == 0
+
+
+def test_l1_deviation_ratio_gaussian(orc):
+    # Sec. 1 relies on L1BN being equivalent to L2BN: for Gaussian data the
+    # mean absolute deviation is sqrt(2/pi) times the standard deviation.
+    M = 200000
+    x = synth.gaussian_codes(81, (M, 1), std=20.0)
+    r = orc.bn_fwd(x, -7, [64], [0], CFG)
+    sigma_l1 = int(r["n_sigma"][0]) * 2.0 ** -14
+    xf = x.astype(np.float64) * 2.0 ** -7
+    ratio = sigma_l1 / xf.std()
+    assert abs(ratio - math.sqrt(2 / math.pi)) < 5e-3
+
+
+def test_l1bn_range_preconditions(orc):
+    x = synth.int_codes(91, (4, 2))
+    with pytest.raises(orc.OracleError):
+        orc.bn_fwd(x, 21, [64, 64], [0, 0], CFG)
+    with pytest.raises(orc.OracleError):
+        orc.bn_fwd(x, -41, [64, 64], [0, 0], CFG)
