@@ -1,0 +1,274 @@
+/*
+ * iseg.h -- C ABI of libiseg.so, the MI355X (gfx950) kernels of the integer
+ * training dataflow of "Training and Inference for Integer-Based Semantic
+ * Segmentation Network" (arXiv 2011.14504, Sec. 3).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Quantized tensor.  A tensor of integer codes n plus ONE int32 exponent e per
+ * tensor; the value of an element is n * 2^e.  Codes of a k-bit object lie in
+ * [-(2^(k-1)-1), 2^(k-1)-1] (the clip range of Eq. 2); -128 never appears in
+ * an int8 code tensor.  Exponents live in DEVICE memory (one int32 each) so
+ * that a producer's data-dependent scale reaches its consumer without a host
+ * round trip.
+ *
+ * Layouts.  Activations and errors: NHWC, contiguous, int8.  Conv weights:
+ * KRSC (out-channel, kernel row, kernel column, in-channel), int8 codes;
+ * masters int32.  Per-channel vectors: C.
+ *
+ * Pointers.  Every data pointer is a device pointer unless said otherwise;
+ * geometry/config structs are HOST pointers read during the call.  The caller
+ * owns all memory.  The library never allocates: scratch space comes from a
+ * caller workspace `ws` of at least the size returned by the matching
+ * iseg_*_ws() query (256-byte aligned).  Inputs and outputs must not alias.
+ *
+ * Streams.  Every compute call only enqueues work on `stream` (0 = the null
+ * stream) and returns; results are ready when the stream reaches that point.
+ *
+ * Errors.  Return values are synchronous host checks: ISEG_OK, or
+ * ISEG_ERR_ARG / _SHAPE / _UNSUPPORTED / _WORKSPACE before anything is
+ * enqueued, or ISEG_ERR_DEVICE if a launch failed.  Conditions only the device
+ * can see (an exponent outside a documented range, a non-finite float) are
+ * OR-ed as ISEG_DEV_* bits into the caller's sticky int32 `dev_status` word (device
+ * memory, may be NULL); outputs are then unspecified.
+ *
+ * Scale rule.  Scale(x) = max|x| (Eq. 3) is realized as the smallest power of
+ * two strictly greater than max|x|, so every scale is an exponent shift and
+ * requantizing a tensor that already holds k-bit codes is value-exact.
+ * Rounding is half-up (floor(x/Delta + 1/2), Eq. 2) unless stochastic
+ * (Eq. 5-6).  A tensor whose maximum is 0 gets codes 0 and keeps its input
+ * exponent.
+ *
+ * Stochastic rounding draws come from Philox4x32-10 with key (seed mod 2^32,
+ * tensor_id) and counter (idx mod 2^32, idx >> 32, step, 0), idx the element's
+ * linear index in the output layout; the draw is w0 | w1 << 32 and the top r
+ * bits decide a rounding of r fractional bits.
+ */
+#ifndef ISEG_H
+#define ISEG_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum iseg_status {
+    ISEG_OK = 0,
+    ISEG_ERR_ARG = 1,          /* bad pointer, bit-width or mode */
+    ISEG_ERR_SHAPE = 2,        /* inconsistent or empty-but-invalid geometry */
+    ISEG_ERR_UNSUPPORTED = 3,  /* valid but outside what the kernels cover */
+    ISEG_ERR_WORKSPACE = 4,    /* ws NULL or smaller than the query says */
+    ISEG_ERR_DEVICE = 5        /* a HIP launch failed */
+};
+
+/* bits OR-ed into *dev_status by kernels */
+enum iseg_dev_status {
+    ISEG_DEV_RANGE = 1,        /* an exponent outside its documented range */
+    ISEG_DEV_NONFINITE = 4     /* a NaN or infinity in a float input */
+};
+
+enum iseg_dtype { ISEG_I8 = 0, ISEG_I16 = 1, ISEG_I32 = 2, ISEG_I64 = 3 };
+
+enum iseg_qmode { ISEG_Q_UQ = 0, ISEG_Q_SQ = 1 };
+
+/* conv output: SQ to 8 bits (int8 codes), or the raw exact int32 sums */
+enum iseg_out_mode { ISEG_OUT_Q8 = 0, ISEG_OUT_RAW = 1 };
+
+/* weight-gradient quantizer: Eq. 17 keeps Scale(G), Eq. 18 drops it; RAW
+ * returns the exact int64 sums */
+enum iseg_g_mode { ISEG_G_KEEP = 0, ISEG_G_DROP = 1, ISEG_G_RAW = 2 };
+
+/* Convolution geometry.  Input NHWC [N,H,W,C]; weights KRSC [K,R,S,C];
+ * output [N,P,Q,K] with P = floor((H + 2 pad_h - dil_h (R-1) - 1)/stride_h)+1
+ * (Q likewise).  Zero padding, cross-correlation, no bias. */
+typedef struct iseg_conv_geom {
+    int64_t N, H, W, C;
+    int64_t K, R, S;
+    int32_t stride_h, stride_w, pad_h, pad_w, dil_h, dil_w;
+} iseg_conv_geom;
+
+/* L1BN bit-widths (Sec. 3.2.2, Eq. 14; defaults from Sec. 5: 16,16,16,8,8)
+ * plus the activation/error widths around it and two readings the paper
+ * leaves open: eps_code (epsilon in LSBs of the sigma grid) and relu (apply a
+ * ReLU between the affine step and Q_A). */
+typedef struct iseg_bn_cfg {
+    int32_t k_mu, k_sigma, k_xhat, k_gamma, k_beta;
+    int32_t k_A, k_E1, k_E2;
+    int32_t eps_code, relu;
+} iseg_bn_cfg;
+
+/* ------------------------------------------------------------------------ */
+/* Quantizers                                                                */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_quantize -- float32 tensor to integer codes (Eq. 2 UQ, or Eq. 3-4 SQ
+ * with the power-of-two Scale).  UQ: code = clamp(floor(x 2^(bits-1) + 1/2)),
+ * exponent 1-bits.  SQ: b = exponent of the smallest power of two strictly
+ * above max|x| (0 for an all-zero tensor), code = clamp(floor(x 2^(bits-1-b) +
+ * 1/2)), exponent b+1-bits.
+ *   x [n] float32 (device); bits in [2, 31]; out_dtype ISEG_I8 (bits <= 8),
+ *   ISEG_I16 (bits <= 16) or ISEG_I32; out [n]; out_exp: one device int32.
+ *   Non-finite input sets ISEG_DEV_NONFINITE. */
+size_t iseg_quantize_ws(int64_t n);
+int iseg_quantize(const float* x, int64_t n, int32_t bits, int32_t mode,
+                  int32_t out_dtype, void* out, int32_t* out_exp,
+                  void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_requant -- SQ (Eq. 4) or stochastic RQ (Eq. 5-6) of an integer tensor.
+ * With M = max|in| and r = bitlen(M) - (bits-1): code = clamp(floor(in/2^r +
+ * 1/2)) (half-up) or clamp(floor(in/2^r) + [u_r < in mod 2^r]) (stochastic,
+ * u_r the top r bits of the element's Philox draw); for r <= 0 code =
+ * in * 2^-r exactly.  Exponent in_exp + r (keep_scale = 1, Eq. 4 / Eq. 17) or
+ * 1-bits (keep_scale = 0, Eq. 18).
+ *   in [n] of in_dtype ISEG_I32 or ISEG_I64; in_exp device int32 (ignored
+ *   when keep_scale = 0); bits in [2, 16]; out_dtype ISEG_I8 (bits <= 8) or
+ *   ISEG_I16. */
+size_t iseg_requant_ws(int64_t n);
+int iseg_requant(const void* in, int32_t in_dtype, int64_t n, const int32_t* in_exp,
+                 int32_t bits, int32_t stochastic, int32_t keep_scale,
+                 uint64_t seed, uint32_t tensor_id, uint32_t step,
+                 int32_t out_dtype, void* out, int32_t* out_exp,
+                 void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Convolutions (int8 x int8 -> exact int32 sums on MFMA, then a quantizer)  */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_conv_fwd -- y[n,p,q,k] = sum_{r,s,c} x[n, p st_h - pad_h + r dil_h,
+ * q st_w - pad_w + s dil_w, c] * w[k,r,s,c]; then Q_A = SQ(., 8) (Eq. 15) for
+ * ISEG_OUT_Q8 (y int8, y_exp = x_exp + w_exp + r) or the raw sums for
+ * ISEG_OUT_RAW (y int32, y_exp = x_exp + w_exp).  The weights are W_q of
+ * Eq. 8.  Requires C*R*S <= 131071 so the exact sums fit int32. */
+size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode);
+int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
+                  const iseg_conv_geom* g, int32_t out_mode, void* y, int32_t* y_exp,
+                  void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_conv_bwd_data -- the adjoint of iseg_conv_fwd: dx[n,h,w,c] = sum of
+ * dy[n,p,q,k] * w[k,r,s,c] over h = p st_h - pad_h + r dil_h, w = q st_w -
+ * pad_w + s dil_w; then Q_E = SQ(., 8) (Eq. 16) for ISEG_OUT_Q8 (dx int8,
+ * dx_exp = dy_exp + w_exp + r) or the raw int32 sums.  dy is [N,P,Q,K];
+ * dx is [N,H,W,C].  Requires K*R*S <= 131071. */
+size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mode);
+int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
+                       const iseg_conv_geom* g, int32_t out_mode, void* dx, int32_t* dx_exp,
+                       void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_conv_bwd_weight -- G[k,r,s,c] = sum_{n,p,q} dy[n,p,q,k] * x[n, p st_h -
+ * pad_h + r dil_h, q st_w - pad_w + s dil_w, c] exactly (int32 partial sums of
+ * at most 131008 pixels, added in int64); then Q_G: stochastic RQ to `bits`
+ * (Eq. 5-6) keeping the scale (ISEG_G_KEEP, Eq. 17: dw_exp = dy_exp + x_exp +
+ * r) or dropping it (ISEG_G_DROP, Eq. 18: dw_exp = 1-bits); dw int8 [K,R,S,C].
+ * ISEG_G_RAW writes the int64 sums (dw_exp = dy_exp + x_exp).  Philox index =
+ * the KRSC linear index. */
+size_t iseg_conv_bwd_weight_ws(const iseg_conv_geom* g, int32_t g_mode);
+int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, const int8_t* x, const int32_t* x_exp,
+                         const iseg_conv_geom* g, int32_t g_mode, int32_t bits,
+                         uint64_t seed, uint32_t tensor_id, uint32_t step,
+                         void* dw, int32_t* dw_exp,
+                         void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* L1 batch normalization (Eq. 12-15) and its backward                       */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_bn_fwd -- per channel c of x [M, C] (M = N*H*W, codes with exponent
+ * s_x in [-40, 16], M <= 2^22, C % 4 == 0):
+ *   mu_q  = 2 UQ(mu/2, k_mu), mu the batch mean            (Eq. 10, 14)
+ *   sigma = mean |x - mu_q|; sigma_q = 2 UQ(sigma/2, k_sigma) (Eq. 13, 14)
+ *   xhat  = (x - mu_q) / (sigma_q + eps)                    (Eq. 12)
+ *           with the denominator code max(n_sigma + eps_code, 1)
+ *   xhat_q= SQ(xhat, k_xhat), one scale for the tensor      (Eq. 14)
+ *   y     = gamma_q xhat_q + beta_q, ReLU if cfg->relu      (Eq. 12)
+ *   A     = SQ(y, k_A) -> y_out int8, y_exp                 (Eq. 15)
+ * gamma_q / beta_q: [C] int8 codes of Q_gamma / Q_beta (value n 2^(2-k)).
+ * An all-zero xhat takes b = 0.  s_x outside its range sets ISEG_DEV_RANGE.
+ * `saved` (iseg_bn_saved_bytes(C) bytes, device) receives what the backward
+ * needs; its layout is:
+ *   int32 hdr[16]: [0] b (xhat_q exponent is b+1-k_xhat), [1] y grid exponent,
+ *                  [2] A exponent, [3] s_x;
+ *   then, each 256-byte aligned: int32 n_mu[C], n_sigma[C], den[C], qmin[C],
+ *   qmax[C]; int16 xhat_code[C][256] (by input code + 128); uint8 flags[C][256]
+ *   (bit0: y > 0, bits1-2: sgn(x - mu_q) + 1); int8 a_code[C][256]. */
+size_t iseg_bn_saved_bytes(int64_t C);
+size_t iseg_bn_fwd_ws(int64_t M, int64_t C);
+int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
+                const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
+                int8_t* y_out, int32_t* y_exp, void* saved,
+                void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_bn_bwd -- exact derivative of Eq. 12-13 with straight-through
+ * quantizers (the paper prints no backward formula), for the forward that
+ * filled `saved` from the same x:
+ *   delta  = dy * [y > 0] (ReLU mask only if cfg->relu)
+ *   dbeta  = sum delta      -> dbeta[C] int64,  *dbeta_exp  = dy_exp
+ *   dgamma = sum delta xhat_q -> dgamma[C] int64, *dgamma_exp = dy_exp + exp(xhat_q)
+ *   E2     = SQ(gamma_q delta, k_E2)                         (Eq. 16)
+ *   dx     = [E2 - mean E2 - mean(E2 xhat_q) (s - mean s)] / (sigma_q + eps),
+ *            s = sgn(x - mu_q), means over the channel's M values
+ *   E1     = SQ(dx, k_E1) -> dx_out int8, dx_exp                (Eq. 16)
+ * dy [M, C] int8 with exponent in [-60, 16]. */
+size_t iseg_bn_bwd_ws(int64_t M, int64_t C);
+int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
+                int64_t M, int64_t C, const int8_t* gamma_q, const iseg_bn_cfg* cfg,
+                const void* saved, int8_t* dx_out, int32_t* dx_exp,
+                int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
+                void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Update (Eq. 19) and weight quantizer (Eq. 7-8)                            */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_weight_update -- Delta W = UQ(G_q * 2^-lr_shift, k_U) (Eq. 19),
+ * master <- clamp(master - Delta W, +-(2^(k_U-1)-1)), w_q = UQ(master, k_W)
+ * (Eq. 8).  master [n] int32 codes with exponent master_exp (1-k_U for conv
+ * weights; 2-k_U for gamma/beta, whose quantizers carry the x2 fold); g [n]
+ * int8 codes with device exponent g_exp; w_q [n] int8 with exponent
+ * master_exp + k_U - k_W.  k_U in [9, 31], k_W in [2, 8]. */
+int iseg_weight_update(int32_t* master, int64_t n, const int8_t* g, const int32_t* g_exp,
+                       int32_t lr_shift, int32_t master_exp, int32_t k_U, int32_t k_W,
+                       int8_t* w_q, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_weight_quant -- Eq. 8 alone: w_q = UQ(master, k_W) from k_U-bit masters. */
+int iseg_weight_quant(const int32_t* master, int64_t n, int32_t k_U, int32_t k_W,
+                      int8_t* w_q, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Max pooling on codes (encoder glue)                                       */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_maxpool_fwd -- window k x k, stride, zero-size padding never picked;
+ * y [N,P,Q,C] with P = floor((H + 2 pad - k)/stride) + 1; y_exp = x_exp. */
+int iseg_maxpool_fwd(const int8_t* x, const int32_t* x_exp, int64_t N, int64_t H, int64_t W,
+                     int64_t C, int32_t k, int32_t stride, int32_t pad,
+                     int8_t* y, int32_t* y_exp, hipStream_t stream);
+
+/* iseg_maxpool_bwd -- each dy element goes to its window's first maximum in
+ * row-major order; overlapping windows add exactly; then Q_E = SQ(., bits)
+ * (Eq. 16).  dx [N,H,W,C] int8, dx_exp. */
+size_t iseg_maxpool_bwd_ws(int64_t N, int64_t H, int64_t W, int64_t C);
+int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
+                     int64_t N, int64_t H, int64_t W, int64_t C,
+                     int32_t k, int32_t stride, int32_t pad, int32_t bits,
+                     int8_t* dx, int32_t* dx_exp,
+                     void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Host-side utilities                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Philox4x32-10 block on the host, the same function the kernels use
+ * (exposed for known-answer tests; no GPU needed). */
+void iseg_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Library version string (static storage). */
+const char* iseg_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISEG_H */

@@ -344,7 +344,7 @@ void orc_conv_bwd_weight_raw(const int8_t* dy, const int8_t* x, const int64_t* g
 /* sigma grid and the denominator code is max(n_sigma + eps_code, 1); ReLU    */
 /* sits between the affine step and Q_A; SQ uses the power-of-two scale; an   */
 /* all-zero xhat takes b = 0 (exponent 1-k_xhat).                             */
-/* Preconditions (else ORC_ERR_RANGE): s_x in [-40, 20], 1 <= m <= 2^22.      */
+/* Preconditions (else ORC_ERR_RANGE): s_x in [-40, 16], 1 <= m <= 2^22.      */
 /* ------------------------------------------------------------------------ */
 typedef struct {
     int k_mu, k_sigma, k_xhat, k_gamma, k_beta, k_A, k_E1, k_E2, eps_code, relu;
@@ -396,7 +396,7 @@ static int bn_fwd_core(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
                        orc_bn_chan* st, int* b_out, int16_t* nxh /* M*C */,
                        i128* Y /* M*C, pre-ReLU y on grid 2^e_y */, int* e_y_out)
 {
-    if (s_x < -40 || s_x > 20 || M < 1 || M > ((int64_t)1 << 22)) return ORC_ERR_RANGE;
+    if (s_x < -40 || s_x > 16 || M < 1 || M > ((int64_t)1 << 22)) return ORC_ERR_RANGE;
     int e_mu = 2 - cf->k_mu, e_sig = 2 - cf->k_sigma;
     for (int64_t c = 0; c < C; c++) bn_channel_stats(x, s_x, M, C, c, cf, &st[c]);
     /* b = smallest integer with |xhat_i| < 2^b for all i */

@@ -1,0 +1,141 @@
+// pool.hip -- max pooling on int8 codes (encoder glue of the VGG16 / ResNet-50
+// encoders) and its backward.  The forward picks the first maximum in
+// row-major window order (padding is never picked) and keeps the exponent;
+// the backward routes each error code to that position, adds overlapping
+// windows exactly in int32 and applies Q_E (SQ, Eq. 16) to the sums.
+#include "iseg_common.h"
+
+namespace {
+
+struct PoolGeom {
+    int64_t N, H, W, C, P, Q;
+    int32_t k, st, pad;
+};
+
+__device__ __forceinline__ int64_t pool_argmax(const int8_t* __restrict__ x, const PoolGeom& g,
+                                               int64_t n, int p, int q, int64_t c)
+{
+    int64_t best = -1;
+    int bv = -1000;
+    for (int r = 0; r < g.k; r++) {
+        int h = p * g.st - g.pad + r;
+        if (h < 0 || h >= g.H) continue;
+        for (int s = 0; s < g.k; s++) {
+            int w = q * g.st - g.pad + s;
+            if (w < 0 || w >= g.W) continue;
+            int64_t idx = ((n * g.H + h) * g.W + w) * g.C + c;
+            int v = x[idx];
+            if (v > bv) { bv = v; best = idx; }
+        }
+    }
+    return best;
+}
+
+__global__ __launch_bounds__(256) void k_maxpool_fwd(const int8_t* __restrict__ x, int8_t* __restrict__ y,
+                                                     PoolGeom g, const int32_t* x_exp, int32_t* y_exp)
+{
+    if (blockIdx.x == 0 && threadIdx.x == 0) *y_exp = *x_exp;
+    int64_t total = g.N * g.P * g.Q * g.C;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t c = i % g.C;
+        int64_t t = i / g.C;
+        int q = (int)(t % g.Q);
+        t /= g.Q;
+        int p = (int)(t % g.P);
+        int64_t n = t / g.P;
+        int64_t a = pool_argmax(x, g, n, p, q, c);
+        y[i] = a >= 0 ? x[a] : 0;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_maxpool_bwd(const int8_t* __restrict__ dy,
+                                                     const int8_t* __restrict__ x,
+                                                     int32_t* __restrict__ acc, PoolGeom g,
+                                                     unsigned long long* maxp)
+{
+    int64_t total = g.N * g.H * g.W * g.C;
+    uint64_t mx = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t c = i % g.C;
+        int64_t t = i / g.C;
+        int w = (int)(t % g.W);
+        t /= g.W;
+        int h = (int)(t % g.H);
+        int64_t n = t / g.H;
+        // windows p with p*st - pad <= h <= p*st - pad + k - 1
+        int plo = h + g.pad - g.k + 1;
+        plo = plo <= 0 ? 0 : (plo + g.st - 1) / g.st;
+        int phi = (h + g.pad) / g.st;
+        int qlo = w + g.pad - g.k + 1;
+        qlo = qlo <= 0 ? 0 : (qlo + g.st - 1) / g.st;
+        int qhi = (w + g.pad) / g.st;
+        int32_t sum = 0;
+        for (int p = plo; p <= phi && p < g.P; p++)
+            for (int q = qlo; q <= qhi && q < g.Q; q++)
+                if (pool_argmax(x, g, n, p, q, c) == i)
+                    sum += dy[((n * g.P + p) * g.Q + q) * g.C + c];
+        acc[i] = sum;
+        uint64_t a = sum < 0 ? (uint64_t)(-(int64_t)sum) : (uint64_t)sum;
+        mx = a > mx ? a : mx;
+    }
+    block_atomic_max_u64(mx, maxp);
+}
+
+bool pool_geom(int64_t N, int64_t H, int64_t W, int64_t C, int32_t k, int32_t st, int32_t pad,
+               PoolGeom* g)
+{
+    if (N < 0 || H < 1 || W < 1 || C < 1 || k < 1 || st < 1 || pad < 0 || pad >= k) return false;
+    if (H + 2 * pad < k || W + 2 * pad < k) return false;
+    g->N = N; g->H = H; g->W = W; g->C = C; g->k = k; g->st = st; g->pad = pad;
+    g->P = (H + 2 * pad - k) / st + 1;
+    g->Q = (W + 2 * pad - k) / st + 1;
+    return true;
+}
+
+}  // namespace
+
+extern "C" int iseg_maxpool_fwd(const int8_t* x, const int32_t* x_exp, int64_t N, int64_t H, int64_t W,
+                                int64_t C, int32_t k, int32_t stride, int32_t pad,
+                                int8_t* y, int32_t* y_exp, hipStream_t stream)
+{
+    PoolGeom g;
+    if (!pool_geom(N, H, W, C, k, stride, pad, &g)) return ISEG_ERR_SHAPE;
+    if (!x_exp || !y_exp || (N > 0 && (!x || !y))) return ISEG_ERR_ARG;
+    int64_t total = g.N * g.P * g.Q * g.C;
+    hipLaunchKernelGGL(k_maxpool_fwd, dim3(grid_for(total, 256, 8192)), dim3(256), 0, stream,
+                       x, y, g, x_exp, y_exp);
+    return launch_ok();
+}
+
+extern "C" size_t iseg_maxpool_bwd_ws(int64_t N, int64_t H, int64_t W, int64_t C)
+{
+    return 256 + align256((size_t)(N * H * W * C) * 4);
+}
+
+extern "C" int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
+                                int64_t N, int64_t H, int64_t W, int64_t C,
+                                int32_t k, int32_t stride, int32_t pad, int32_t bits,
+                                int8_t* dx, int32_t* dx_exp,
+                                void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    PoolGeom g;
+    if (!pool_geom(N, H, W, C, k, stride, pad, &g)) return ISEG_ERR_SHAPE;
+    if (!dy_exp || !dx_exp || bits < 2 || bits > 8 || (N > 0 && (!dy || !x || !dx)))
+        return ISEG_ERR_ARG;
+    if (!ws || ws_bytes < iseg_maxpool_bwd_ws(N, H, W, C)) return ISEG_ERR_WORKSPACE;
+    unsigned long long* maxp = (unsigned long long*)ws;
+    int32_t* acc = (int32_t*)((char*)ws + 256);
+    int rc = launch_fill_u32(maxp, 2, 0, stream);
+    if (rc) return rc;
+    int64_t total = N * H * W * C;
+    if (total > 0) {
+        hipLaunchKernelGGL(k_maxpool_bwd, dim3(grid_for(total, 256, 8192)), dim3(256), 0, stream,
+                           dy, x, acc, g, maxp);
+        if ((rc = launch_ok())) return rc;
+    }
+    (void)dev_status;
+    return launch_requant_apply(acc, ISEG_I32, total, dy_exp, nullptr, 0, bits, 0, 1, 0, 0, 0,
+                                ISEG_I8, dx, dx_exp, maxp, stream);
+}

@@ -1,0 +1,389 @@
+// quant.hip -- the quantizers (Eq. 2 UQ, Eq. 3-4 SQ, Eq. 5-6 RQ), the update
+// and weight quantizers (Eq. 19, Eq. 8) and the shared requant machinery.
+//
+// All of these are bandwidth-bound streams: one pass computes max|x| with a
+// wave reduction and one atomicMax per block, a second pass turns elements
+// into codes with 16-byte vector loads where the dtype allows.
+#include "iseg_common.h"
+
+// ---------------------------------------------------------------------------
+// fill / absmax
+// ---------------------------------------------------------------------------
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v)
+{
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+int launch_fill_u32(void* p, int64_t n_words, uint32_t v, hipStream_t s)
+{
+    if (n_words <= 0) return ISEG_OK;
+    hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(n_words, 256, 1024)), dim3(256), 0, s,
+                       (uint32_t*)p, n_words, v);
+    return launch_ok();
+}
+
+__device__ __forceinline__ uint64_t uabs64(int64_t v)
+{
+    return v < 0 ? (uint64_t)0 - (uint64_t)v : (uint64_t)v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_absmax_scalar(const T* __restrict__ in, int64_t n,
+                                                       unsigned long long* maxp)
+{
+    uint64_t m = 0;
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < n;
+         j += (int64_t)gridDim.x * blockDim.x) {
+        uint64_t a = uabs64((int64_t)in[j]);
+        m = a > m ? a : m;
+    }
+    block_atomic_max_u64(m, maxp);
+}
+
+// int32 input, 16-byte aligned
+template <typename T>
+__global__ __launch_bounds__(256) void k_absmax(const T* __restrict__ in, int64_t n,
+                                                unsigned long long* maxp)
+{
+    uint64_t m = 0;
+    int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (sizeof(T) == 4) {
+        // 4 elements per step through int4 loads on the aligned body
+        const int4* v4 = (const int4*)in;
+        int64_t n4 = n >> 2;
+        for (int64_t j = i; j < n4; j += stride) {
+            int4 v = v4[j];
+            uint64_t a = uabs64(v.x), b = uabs64(v.y), c = uabs64(v.z), d = uabs64(v.w);
+            a = a > b ? a : b;
+            c = c > d ? c : d;
+            a = a > c ? a : c;
+            m = a > m ? a : m;
+        }
+        for (int64_t j = (n4 << 2) + i; j < n; j += stride) {
+            uint64_t a = uabs64((int64_t)in[j]);
+            m = a > m ? a : m;
+        }
+    } else {
+        for (int64_t j = i; j < n; j += stride) {
+            uint64_t a = uabs64((int64_t)in[j]);
+            m = a > m ? a : m;
+        }
+    }
+    block_atomic_max_u64(m, maxp);
+}
+
+int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* maxp,
+                  int32_t*, hipStream_t s)
+{
+    if (n <= 0) return ISEG_OK;
+    if (in_dtype == ISEG_I32 && ((uintptr_t)in & 15) == 0)
+        hipLaunchKernelGGL(k_absmax<int32_t>, dim3(grid_for(n, 256 * 16, 2048)), dim3(256), 0, s,
+                           (const int32_t*)in, n, maxp);
+    else if (in_dtype == ISEG_I32)
+        hipLaunchKernelGGL(k_absmax_scalar<int32_t>, dim3(grid_for(n, 256 * 8, 2048)), dim3(256), 0, s,
+                           (const int32_t*)in, n, maxp);
+    else
+        hipLaunchKernelGGL(k_absmax_scalar<int64_t>, dim3(grid_for(n, 256 * 8, 2048)), dim3(256), 0, s,
+                           (const int64_t*)in, n, maxp);
+    return launch_ok();
+}
+
+// ---------------------------------------------------------------------------
+// requant apply: SQ half-up or RQ stochastic with r = bitlen(max) - (bits-1)
+// ---------------------------------------------------------------------------
+struct RqArgs {
+    int64_t n;
+    const int32_t* exp_a;
+    const int32_t* exp_b;
+    int32_t exp_add;
+    int32_t bits, stochastic, keep_scale;
+    uint64_t seed;
+    uint32_t tensor_id, step;
+    int32_t* out_exp;
+    const unsigned long long* maxp;
+};
+
+__device__ __forceinline__ int rq_shift(const RqArgs& a, uint64_t M)
+{
+    return M ? bitlen_u64(M) - (a.bits - 1) : 0;
+}
+
+__device__ __forceinline__ void rq_write_exp(const RqArgs& a, uint64_t M, int r)
+{
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.out_exp) {
+        int32_t e = (a.exp_a ? *a.exp_a : 0) + (a.exp_b ? *a.exp_b : 0) + a.exp_add;
+        *a.out_exp = a.keep_scale ? e + r : 1 - a.bits;
+        (void)M;
+    }
+}
+
+__device__ __forceinline__ int64_t rq_one(const RqArgs& a, int64_t q, int r, int64_t idx)
+{
+    if (a.stochastic && r > 0)
+        return rq_code(q, r, a.bits, philox_draw(a.seed, a.tensor_id, a.step, (uint64_t)idx));
+    return sq_code(q, r, a.bits);
+}
+
+// int32 -> int8, 16 elements per vector step
+__global__ __launch_bounds__(256) void k_requant_i32_i8(const int32_t* __restrict__ in,
+                                                        int8_t* __restrict__ out, RqArgs a)
+{
+    uint64_t M = *a.maxp;
+    int r = rq_shift(a, M);
+    rq_write_exp(a, M, r);
+    int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    int64_t n16 = a.n >> 4;
+    const int4* in4 = (const int4*)in;
+    int4* out16 = (int4*)out;
+    for (int64_t j = i0; j < n16; j += stride) {
+        uint32_t w[4];
+#pragma unroll
+        for (int v = 0; v < 4; v++) {
+            int4 q = in4[j * 4 + v];
+            int64_t base = j * 16 + v * 4;
+            uint32_t b0 = (uint8_t)rq_one(a, q.x, r, base + 0);
+            uint32_t b1 = (uint8_t)rq_one(a, q.y, r, base + 1);
+            uint32_t b2 = (uint8_t)rq_one(a, q.z, r, base + 2);
+            uint32_t b3 = (uint8_t)rq_one(a, q.w, r, base + 3);
+            w[v] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+        }
+        out16[j] = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
+    }
+    for (int64_t j = (n16 << 4) + i0; j < a.n; j += stride)
+        out[j] = (int8_t)rq_one(a, in[j], r, j);
+}
+
+template <typename TIn, typename TOut>
+__global__ __launch_bounds__(256) void k_requant_generic(const TIn* __restrict__ in,
+                                                         TOut* __restrict__ out, RqArgs a)
+{
+    uint64_t M = *a.maxp;
+    int r = rq_shift(a, M);
+    rq_write_exp(a, M, r);
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.n;
+         j += (int64_t)gridDim.x * blockDim.x)
+        out[j] = (TOut)rq_one(a, (int64_t)in[j], r, j);
+}
+
+int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t* exp_a,
+                         const int32_t* exp_b, int32_t exp_add, int bits, int stochastic,
+                         int keep_scale, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                         int out_dtype, void* out, int32_t* out_exp,
+                         const unsigned long long* maxp, hipStream_t s)
+{
+    RqArgs a;
+    a.n = n; a.exp_a = exp_a; a.exp_b = exp_b; a.exp_add = exp_add;
+    a.bits = bits; a.stochastic = stochastic; a.keep_scale = keep_scale;
+    a.seed = seed; a.tensor_id = tensor_id; a.step = step;
+    a.out_exp = out_exp; a.maxp = maxp;
+    bool aligned = (((uintptr_t)in | (uintptr_t)out) & 15) == 0;
+    if (in_dtype == ISEG_I32 && out_dtype == ISEG_I8 && aligned)
+        hipLaunchKernelGGL(k_requant_i32_i8, dim3(grid_for(n, 256 * 16, 4096)), dim3(256), 0, s,
+                           (const int32_t*)in, (int8_t*)out, a);
+    else if (in_dtype == ISEG_I32 && out_dtype == ISEG_I8)
+        hipLaunchKernelGGL((k_requant_generic<int32_t, int8_t>), dim3(grid_for(n, 256, 4096)),
+                           dim3(256), 0, s, (const int32_t*)in, (int8_t*)out, a);
+    else if (in_dtype == ISEG_I32 && out_dtype == ISEG_I16)
+        hipLaunchKernelGGL((k_requant_generic<int32_t, int16_t>), dim3(grid_for(n, 256, 4096)),
+                           dim3(256), 0, s, (const int32_t*)in, (int16_t*)out, a);
+    else if (in_dtype == ISEG_I64 && out_dtype == ISEG_I8)
+        hipLaunchKernelGGL((k_requant_generic<int64_t, int8_t>), dim3(grid_for(n, 256, 4096)),
+                           dim3(256), 0, s, (const int64_t*)in, (int8_t*)out, a);
+    else if (in_dtype == ISEG_I64 && out_dtype == ISEG_I16)
+        hipLaunchKernelGGL((k_requant_generic<int64_t, int16_t>), dim3(grid_for(n, 256, 4096)),
+                           dim3(256), 0, s, (const int64_t*)in, (int16_t*)out, a);
+    else
+        return ISEG_ERR_ARG;
+    return launch_ok();
+}
+
+// ---------------------------------------------------------------------------
+// iseg_requant
+// ---------------------------------------------------------------------------
+extern "C" size_t iseg_requant_ws(int64_t) { return 256; }
+
+extern "C" int iseg_requant(const void* in, int32_t in_dtype, int64_t n, const int32_t* in_exp,
+                            int32_t bits, int32_t stochastic, int32_t keep_scale,
+                            uint64_t seed, uint32_t tensor_id, uint32_t step,
+                            int32_t out_dtype, void* out, int32_t* out_exp,
+                            void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    if (n < 0 || !out_exp || (n > 0 && (!in || !out))) return ISEG_ERR_ARG;
+    if (in_dtype != ISEG_I32 && in_dtype != ISEG_I64) return ISEG_ERR_ARG;
+    if (out_dtype == ISEG_I8 ? (bits < 2 || bits > 8)
+                             : (out_dtype != ISEG_I16 || bits < 2 || bits > 16))
+        return ISEG_ERR_ARG;
+    if (keep_scale && !in_exp) return ISEG_ERR_ARG;
+    if (!ws || ws_bytes < iseg_requant_ws(n)) return ISEG_ERR_WORKSPACE;
+    unsigned long long* maxp = (unsigned long long*)ws;
+    int rc = launch_fill_u32(maxp, 2, 0, stream);
+    if (rc == ISEG_OK) rc = launch_absmax(in, in_dtype, n, maxp, dev_status, stream);
+    if (rc == ISEG_OK)
+        rc = launch_requant_apply(in, in_dtype, n, keep_scale ? in_exp : nullptr, nullptr, 0,
+                                  bits, stochastic, keep_scale, seed, tensor_id, step,
+                                  out_dtype, out, out_exp, maxp, stream);
+    return rc;
+}
+
+// ---------------------------------------------------------------------------
+// iseg_quantize: float32 -> codes
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_fabsmax(const float* __restrict__ x, int64_t n,
+                                                 unsigned long long* maxp, int32_t* dev_status)
+{
+    uint32_t m = 0;
+    bool bad = false;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t b = __float_as_uint(x[i]) & 0x7fffffffu;
+        bad |= b >= 0x7f800000u;
+        m = b > m ? b : m;
+    }
+    if (bad) set_status(dev_status, ISEG_DEV_NONFINITE);
+    block_atomic_max_u64(m, maxp);
+}
+
+// exponent e of the smallest power of two strictly greater than the positive
+// float with bits `mb` (frexp's exponent)
+__device__ __forceinline__ int frexp_exp_bits(uint32_t mb)
+{
+    uint32_t E = mb >> 23, man = mb & 0x7fffffu;
+    if (E == 0) return bitlen_u64(man) - 149;
+    return (int)E - 126;
+}
+
+struct QzArgs {
+    int64_t n;
+    int32_t bits, mode;
+    int32_t* out_exp;
+    const unsigned long long* maxp;
+};
+
+template <typename TOut>
+__global__ __launch_bounds__(256) void k_quantize_apply(const float* __restrict__ x,
+                                                        TOut* __restrict__ out, QzArgs a)
+{
+    int b = 0;
+    if (a.mode == ISEG_Q_SQ) {
+        uint32_t mb = (uint32_t)*a.maxp;
+        b = mb ? frexp_exp_bits(mb) : 0;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.out_exp = b + 1 - a.bits;
+    int sh = a.bits - 1 - b;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < a.n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        float v = ldexpf(x[i], sh);         // x / (S Delta), a power-of-two scale
+        float fl = floorf(v);
+        float fr = v - fl;                  // decides the half-up rounding exactly
+        float nf = fl + (fr >= 0.5f ? 1.0f : 0.0f);
+        int64_t n;
+        if (!(nf == nf)) n = 0;
+        else if (nf >= 4.6e18f) n = INT64_MAX / 2;
+        else if (nf <= -4.6e18f) n = -(INT64_MAX / 2);
+        else n = (int64_t)nf;
+        out[i] = (TOut)clamp_k(n, a.bits);
+    }
+}
+
+extern "C" size_t iseg_quantize_ws(int64_t) { return 256; }
+
+extern "C" int iseg_quantize(const float* x, int64_t n, int32_t bits, int32_t mode,
+                             int32_t out_dtype, void* out, int32_t* out_exp,
+                             void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    if (n < 0 || !out_exp || (n > 0 && (!x || !out))) return ISEG_ERR_ARG;
+    if (mode != ISEG_Q_UQ && mode != ISEG_Q_SQ) return ISEG_ERR_ARG;
+    int maxbits = out_dtype == ISEG_I8 ? 8 : out_dtype == ISEG_I16 ? 16 : out_dtype == ISEG_I32 ? 31 : 0;
+    if (bits < 2 || bits > maxbits) return ISEG_ERR_ARG;
+    if (!ws || ws_bytes < iseg_quantize_ws(n)) return ISEG_ERR_WORKSPACE;
+    unsigned long long* maxp = (unsigned long long*)ws;
+    int rc = launch_fill_u32(maxp, 2, 0, stream);
+    if (rc != ISEG_OK) return rc;
+    if (n > 0) {
+        hipLaunchKernelGGL(k_fabsmax, dim3(grid_for(n, 256 * 8, 2048)), dim3(256), 0, stream,
+                           x, n, maxp, dev_status);
+        if ((rc = launch_ok()) != ISEG_OK) return rc;
+    }
+    QzArgs a;
+    a.n = n; a.bits = bits; a.mode = mode; a.out_exp = out_exp; a.maxp = maxp;
+    dim3 g(grid_for(n, 256 * 4, 4096));
+    if (out_dtype == ISEG_I8)
+        hipLaunchKernelGGL(k_quantize_apply<int8_t>, g, dim3(256), 0, stream, x, (int8_t*)out, a);
+    else if (out_dtype == ISEG_I16)
+        hipLaunchKernelGGL(k_quantize_apply<int16_t>, g, dim3(256), 0, stream, x, (int16_t*)out, a);
+    else
+        hipLaunchKernelGGL(k_quantize_apply<int32_t>, g, dim3(256), 0, stream, x, (int32_t*)out, a);
+    return launch_ok();
+}
+
+// ---------------------------------------------------------------------------
+// Eq. 19 update and Eq. 8 weight quantizer
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_weight_update(int32_t* __restrict__ master, int64_t n,
+                                                       const int8_t* __restrict__ g,
+                                                       const int32_t* g_exp, int32_t lr_shift,
+                                                       int32_t master_exp, int32_t k_U,
+                                                       int32_t k_W, int8_t* __restrict__ w_q)
+{
+    int sh = *g_exp - lr_shift - master_exp;     // Delta W code = g 2^sh, rounded
+    int dq = k_U - k_W;
+    int64_t lim = ((int64_t)1 << (k_U - 1)) - 1;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t gv = g[i];
+        int64_t dW;
+        if (gv == 0 || sh < -40) dW = 0;
+        else if (sh > 40) dW = gv > 0 ? lim : -lim;
+        else if (sh >= 0) dW = clamp_k(gv * ((int64_t)1 << sh), k_U);
+        else dW = clamp_k(shr_rhu(gv, -sh), k_U);
+        int64_t m = clamp_k((int64_t)master[i] - dW, k_U);
+        master[i] = (int32_t)m;
+        w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), k_W);
+    }
+}
+
+extern "C" int iseg_weight_update(int32_t* master, int64_t n, const int8_t* g, const int32_t* g_exp,
+                                  int32_t lr_shift, int32_t master_exp, int32_t k_U, int32_t k_W,
+                                  int8_t* w_q, int32_t*, hipStream_t stream)
+{
+    if (n < 0 || (n > 0 && (!master || !g || !g_exp || !w_q))) return ISEG_ERR_ARG;
+    if (k_U < 9 || k_U > 31 || k_W < 2 || k_W > 8) return ISEG_ERR_ARG;
+    if (n == 0) return ISEG_OK;
+    hipLaunchKernelGGL(k_weight_update, dim3(grid_for(n, 256, 4096)), dim3(256), 0, stream,
+                       master, n, g, g_exp, lr_shift, master_exp, k_U, k_W, w_q);
+    return launch_ok();
+}
+
+__global__ __launch_bounds__(256) void k_weight_quant(const int32_t* __restrict__ master, int64_t n,
+                                                      int32_t dq, int32_t k_W, int8_t* __restrict__ w_q)
+{
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        w_q[i] = (int8_t)clamp_k(shr_rhu(master[i], dq), k_W);
+}
+
+extern "C" int iseg_weight_quant(const int32_t* master, int64_t n, int32_t k_U, int32_t k_W,
+                                 int8_t* w_q, hipStream_t stream)
+{
+    if (n < 0 || (n > 0 && (!master || !w_q))) return ISEG_ERR_ARG;
+    if (k_U < 9 || k_U > 31 || k_W < 2 || k_W > 8) return ISEG_ERR_ARG;
+    if (n == 0) return ISEG_OK;
+    hipLaunchKernelGGL(k_weight_quant, dim3(grid_for(n, 256, 4096)), dim3(256), 0, stream,
+                       master, n, k_U - k_W, k_W, w_q);
+    return launch_ok();
+}
+
+// ---------------------------------------------------------------------------
+// host utilities
+// ---------------------------------------------------------------------------
+extern "C" void iseg_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    philox_out o = philox4x32_10(ctr[0], ctr[1], ctr[2], ctr[3], key[0], key[1]);
+    for (int i = 0; i < 4; i++) out[i] = o.v[i];
+}
+
+extern "C" const char* iseg_version(void) { return "iseg 0.1 gfx950"; }

@@ -1,0 +1,394 @@
+"""Python binding of libiseg.so (ctypes).
+
+The `iseg_*` functions here carry the C ABI's names and arguments one to one:
+they only turn torch tensors into device pointers, pass the current HIP
+stream, and raise on a non-zero status.  Every computation runs in the HIP
+kernels; there is no fallback.  The helpers below them (conv_fwd, bn_fwd, ...)
+allocate outputs and workspaces with torch and call those entry points.
+
+A quantized tensor is a pair (codes, exp): integer codes and a 1-element int32
+device tensor holding the power-of-two exponent (value = code * 2^exp).
+"""
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libiseg.so")
+
+ISEG_OK, ISEG_ERR_ARG, ISEG_ERR_SHAPE, ISEG_ERR_UNSUPPORTED, ISEG_ERR_WORKSPACE, ISEG_ERR_DEVICE = range(6)
+ISEG_DEV_RANGE, ISEG_DEV_NONFINITE = 1, 4
+ISEG_I8, ISEG_I16, ISEG_I32, ISEG_I64 = range(4)
+ISEG_Q_UQ, ISEG_Q_SQ = 0, 1
+ISEG_OUT_Q8, ISEG_OUT_RAW = 0, 1
+ISEG_G_KEEP, ISEG_G_DROP, ISEG_G_RAW = 0, 1, 2
+
+_ERRS = {1: "ISEG_ERR_ARG", 2: "ISEG_ERR_SHAPE", 3: "ISEG_ERR_UNSUPPORTED",
+         4: "ISEG_ERR_WORKSPACE", 5: "ISEG_ERR_DEVICE"}
+
+
+class IsegError(RuntimeError):
+    pass
+
+
+class ConvGeom(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in ("N", "H", "W", "C", "K", "R", "S")] + \
+               [(n, C.c_int32) for n in ("stride_h", "stride_w", "pad_h", "pad_w", "dil_h", "dil_w")]
+
+
+class BnCfg(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in ("k_mu", "k_sigma", "k_xhat", "k_gamma", "k_beta",
+                                         "k_A", "k_E1", "k_E2", "eps_code", "relu")]
+
+
+BN_DEFAULT = dict(k_mu=16, k_sigma=16, k_xhat=16, k_gamma=8, k_beta=8, k_A=8, k_E1=8, k_E2=16,
+                  eps_code=0, relu=1)
+
+_lib = None
+_P, _I64, _I32, _U64, _U32, _SZ = C.c_void_p, C.c_int64, C.c_int32, C.c_uint64, C.c_uint32, C.c_size_t
+
+_SIGS = {
+    "iseg_quantize_ws": ([_I64], _SZ),
+    "iseg_quantize": ([_P, _I64, _I32, _I32, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_requant_ws": ([_I64], _SZ),
+    "iseg_requant": ([_P, _I32, _I64, _P, _I32, _I32, _I32, _U64, _U32, _U32, _I32, _P, _P, _P, _SZ,
+                      _P, _P], C.c_int),
+    "iseg_conv_fwd_ws": ([_P, _I32], _SZ),
+    "iseg_conv_fwd": ([_P, _P, _P, _P, _P, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_conv_bwd_data_ws": ([_P, _I32], _SZ),
+    "iseg_conv_bwd_data": ([_P, _P, _P, _P, _P, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_conv_bwd_weight_ws": ([_P, _I32], _SZ),
+    "iseg_conv_bwd_weight": ([_P, _P, _P, _P, _P, _I32, _I32, _U64, _U32, _U32, _P, _P, _P, _SZ,
+                              _P, _P], C.c_int),
+    "iseg_bn_saved_bytes": ([_I64], _SZ),
+    "iseg_bn_fwd_ws": ([_I64, _I64], _SZ),
+    "iseg_bn_fwd": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_bn_bwd_ws": ([_I64, _I64], _SZ),
+    "iseg_bn_bwd": ([_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P],
+                    C.c_int),
+    "iseg_weight_update": ([_P, _I64, _P, _P, _I32, _I32, _I32, _I32, _P, _P, _P], C.c_int),
+    "iseg_weight_quant": ([_P, _I64, _I32, _I32, _P, _P], C.c_int),
+    "iseg_maxpool_fwd": ([_P, _P, _I64, _I64, _I64, _I64, _I32, _I32, _I32, _P, _P, _P], C.c_int),
+    "iseg_maxpool_bwd_ws": ([_I64, _I64, _I64, _I64], _SZ),
+    "iseg_maxpool_bwd": ([_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32, _I32, _I32, _P, _P, _P,
+                          _SZ, _P, _P], C.c_int),
+    "iseg_philox4x32_10": ([_P, _P, _P], None),
+    "iseg_version": ([], C.c_char_p),
+}
+
+
+def lib():
+    """Load libiseg.so; raises if it has not been built (no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"libiseg.so not built at {LIB_PATH}; run __graft_entry__.build()")
+        L = C.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _check(rc, name):
+    if rc != ISEG_OK:
+        raise IsegError(f"{name} returned {_ERRS.get(rc, rc)}")
+
+
+def _ws_tuple(ws):
+    return (_ptr(ws), C.c_size_t(ws.numel() if ws is not None else 0))
+
+
+# --------------------------------------------------------------------------
+# entry points, one to one with include/iseg.h
+# --------------------------------------------------------------------------
+def iseg_quantize(x, bits, mode, out_dtype, out, out_exp, ws, status=None):
+    rc = lib().iseg_quantize(_ptr(x), x.numel(), bits, mode, out_dtype, _ptr(out), _ptr(out_exp),
+                             *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_quantize")
+
+
+def iseg_requant(inp, in_dtype, in_exp, bits, stochastic, keep_scale, seed, tensor_id, step,
+                 out_dtype, out, out_exp, ws, status=None):
+    rc = lib().iseg_requant(_ptr(inp), in_dtype, inp.numel(), _ptr(in_exp), bits, stochastic,
+                            keep_scale, seed, tensor_id, step, out_dtype, _ptr(out), _ptr(out_exp),
+                            *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_requant")
+
+
+def iseg_conv_fwd(x, x_exp, w, w_exp, geom, out_mode, y, y_exp, ws, status=None):
+    rc = lib().iseg_conv_fwd(_ptr(x), _ptr(x_exp), _ptr(w), _ptr(w_exp), C.byref(geom), out_mode,
+                             _ptr(y), _ptr(y_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_conv_fwd")
+
+
+def iseg_conv_bwd_data(dy, dy_exp, w, w_exp, geom, out_mode, dx, dx_exp, ws, status=None):
+    rc = lib().iseg_conv_bwd_data(_ptr(dy), _ptr(dy_exp), _ptr(w), _ptr(w_exp), C.byref(geom),
+                                  out_mode, _ptr(dx), _ptr(dx_exp), *_ws_tuple(ws), _ptr(status),
+                                  _stream())
+    _check(rc, "iseg_conv_bwd_data")
+
+
+def iseg_conv_bwd_weight(dy, dy_exp, x, x_exp, geom, g_mode, bits, seed, tensor_id, step, dw,
+                         dw_exp, ws, status=None):
+    rc = lib().iseg_conv_bwd_weight(_ptr(dy), _ptr(dy_exp), _ptr(x), _ptr(x_exp), C.byref(geom),
+                                    g_mode, bits, seed, tensor_id, step, _ptr(dw), _ptr(dw_exp),
+                                    *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_conv_bwd_weight")
+
+
+def iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, ws, status=None):
+    rc = lib().iseg_bn_fwd(_ptr(x), _ptr(x_exp), M, Cc, _ptr(gamma_q), _ptr(beta_q), C.byref(cfg),
+                           _ptr(y), _ptr(y_exp), _ptr(saved), *_ws_tuple(ws), _ptr(status),
+                           _stream())
+    _check(rc, "iseg_bn_fwd")
+
+
+def iseg_bn_bwd(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, dx_exp, dgamma, dbeta, dgamma_exp,
+                dbeta_exp, ws, status=None):
+    rc = lib().iseg_bn_bwd(_ptr(dy), _ptr(dy_exp), _ptr(x), M, Cc, _ptr(gamma_q), C.byref(cfg),
+                           _ptr(saved), _ptr(dx), _ptr(dx_exp), _ptr(dgamma), _ptr(dbeta),
+                           _ptr(dgamma_exp), _ptr(dbeta_exp), *_ws_tuple(ws), _ptr(status),
+                           _stream())
+    _check(rc, "iseg_bn_bwd")
+
+
+def iseg_weight_update(master, g, g_exp, lr_shift, master_exp, k_U, k_W, w_q, status=None):
+    rc = lib().iseg_weight_update(_ptr(master), master.numel(), _ptr(g), _ptr(g_exp), lr_shift,
+                                  master_exp, k_U, k_W, _ptr(w_q), _ptr(status), _stream())
+    _check(rc, "iseg_weight_update")
+
+
+def iseg_weight_quant(master, k_U, k_W, w_q):
+    rc = lib().iseg_weight_quant(_ptr(master), master.numel(), k_U, k_W, _ptr(w_q), _stream())
+    _check(rc, "iseg_weight_quant")
+
+
+def iseg_maxpool_fwd(x, x_exp, k, stride, pad, y, y_exp):
+    N, H, W, Cc = x.shape
+    rc = lib().iseg_maxpool_fwd(_ptr(x), _ptr(x_exp), N, H, W, Cc, k, stride, pad, _ptr(y),
+                                _ptr(y_exp), _stream())
+    _check(rc, "iseg_maxpool_fwd")
+
+
+def iseg_maxpool_bwd(dy, dy_exp, x, k, stride, pad, bits, dx, dx_exp, ws, status=None):
+    N, H, W, Cc = x.shape
+    rc = lib().iseg_maxpool_bwd(_ptr(dy), _ptr(dy_exp), _ptr(x), N, H, W, Cc, k, stride, pad, bits,
+                                _ptr(dx), _ptr(dx_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_maxpool_bwd")
+
+
+def iseg_philox4x32_10(ctr, key):
+    c = (C.c_uint32 * 4)(*ctr)
+    k = (C.c_uint32 * 2)(*key)
+    o = (C.c_uint32 * 4)()
+    lib().iseg_philox4x32_10(c, k, o)
+    return list(o)
+
+
+def iseg_version():
+    return lib().iseg_version().decode()
+
+
+# --------------------------------------------------------------------------
+# workspace and helpers (allocation with torch; compute in the entry points)
+# --------------------------------------------------------------------------
+class Workspace:
+    """A growable device scratch buffer shared by consecutive calls on one
+    stream (stream order keeps the uses apart)."""
+
+    def __init__(self, device="cuda"):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes):
+        nbytes = max(int(nbytes), 256)
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self.buf[:nbytes]
+
+
+_WS = {}
+
+
+def workspace(device):
+    d = torch.device(device)
+    if d.type == "cuda" and d.index is None:
+        d = torch.device("cuda", torch.cuda.current_device())
+    key = str(d)
+    if key not in _WS:
+        _WS[key] = Workspace(d)
+    return _WS[key]
+
+
+def new_exp(device="cuda", value=0):
+    return torch.full((1,), int(value), dtype=torch.int32, device=device)
+
+
+def geom(N, H, W, Cc, K, R, S, stride=1, pad=0, dil=1):
+    st = stride if isinstance(stride, (tuple, list)) else (stride, stride)
+    pd = pad if isinstance(pad, (tuple, list)) else (pad, pad)
+    dl = dil if isinstance(dil, (tuple, list)) else (dil, dil)
+    return ConvGeom(N, H, W, Cc, K, R, S, st[0], st[1], pd[0], pd[1], dl[0], dl[1])
+
+
+def conv_out_hw(g):
+    P = (g.H + 2 * g.pad_h - g.dil_h * (g.R - 1) - 1) // g.stride_h + 1
+    Q = (g.W + 2 * g.pad_w - g.dil_w * (g.S - 1) - 1) // g.stride_w + 1
+    return P, Q
+
+
+def bn_cfg(**kw):
+    d = dict(BN_DEFAULT)
+    d.update(kw)
+    return BnCfg(*[d[k] for k in ("k_mu", "k_sigma", "k_xhat", "k_gamma", "k_beta", "k_A", "k_E1",
+                                  "k_E2", "eps_code", "relu")])
+
+
+def quantize(x, bits, mode=ISEG_Q_SQ, status=None):
+    dt = {8: (torch.int8, ISEG_I8), 16: (torch.int16, ISEG_I16)}.get(
+        8 if bits <= 8 else 16 if bits <= 16 else 32, (torch.int32, ISEG_I32))
+    out = torch.empty(x.shape, dtype=dt[0], device=x.device)
+    e = new_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_quantize_ws(x.numel()))
+    iseg_quantize(x.contiguous(), bits, mode, dt[1], out, e, ws, status)
+    return out, e
+
+
+def requant(acc, acc_exp, bits=8, stochastic=False, keep_scale=True, seed=0, tensor_id=0, step=0,
+            status=None):
+    in_dt = {torch.int32: ISEG_I32, torch.int64: ISEG_I64}[acc.dtype]
+    od, odt = (torch.int8, ISEG_I8) if bits <= 8 else (torch.int16, ISEG_I16)
+    out = torch.empty(acc.shape, dtype=od, device=acc.device)
+    e = new_exp(acc.device)
+    ws = workspace(acc.device).get(lib().iseg_requant_ws(acc.numel()))
+    iseg_requant(acc.contiguous(), in_dt, acc_exp, bits, int(stochastic), int(keep_scale), seed,
+                 tensor_id, step, odt, out, e, ws, status)
+    return out, e
+
+
+def conv_fwd(x, x_exp, w, w_exp, stride=1, pad=0, dil=1, out_mode=ISEG_OUT_Q8, status=None):
+    N, H, W, Cc = x.shape
+    K, R, S, _ = w.shape
+    g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
+    P, Q = conv_out_hw(g)
+    y = torch.empty((N, P, Q, K), dtype=torch.int8 if out_mode == ISEG_OUT_Q8 else torch.int32,
+                    device=x.device)
+    e = new_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_conv_fwd_ws(C.byref(g), out_mode))
+    iseg_conv_fwd(x, x_exp, w, w_exp, g, out_mode, y, e, ws, status)
+    return y, e
+
+
+def conv_bwd_data(dy, dy_exp, w, w_exp, x_shape, stride=1, pad=0, dil=1, out_mode=ISEG_OUT_Q8,
+                  status=None):
+    N, H, W, Cc = x_shape
+    K, R, S, _ = w.shape
+    g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
+    dx = torch.empty((N, H, W, Cc), dtype=torch.int8 if out_mode == ISEG_OUT_Q8 else torch.int32,
+                     device=dy.device)
+    e = new_exp(dy.device)
+    ws = workspace(dy.device).get(lib().iseg_conv_bwd_data_ws(C.byref(g), out_mode))
+    iseg_conv_bwd_data(dy, dy_exp, w, w_exp, g, out_mode, dx, e, ws, status)
+    return dx, e
+
+
+def conv_bwd_weight(dy, dy_exp, x, x_exp, w_shape, stride=1, pad=0, dil=1, g_mode=ISEG_G_KEEP,
+                    bits=8, seed=0, tensor_id=0, step=0, status=None):
+    N, H, W, Cc = x.shape
+    K, R, S, _ = w_shape
+    g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
+    dw = torch.empty((K, R, S, Cc), dtype=torch.int64 if g_mode == ISEG_G_RAW else torch.int8,
+                     device=x.device)
+    e = new_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_conv_bwd_weight_ws(C.byref(g), g_mode))
+    iseg_conv_bwd_weight(dy, dy_exp, x, x_exp, g, g_mode, bits, seed, tensor_id, step, dw, e, ws,
+                         status)
+    return dw, e
+
+
+def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None, saved=None, status=None):
+    Cc = x.shape[-1]
+    M = x.numel() // Cc
+    cfg = cfg or bn_cfg()
+    y = torch.empty_like(x)
+    e = new_exp(x.device)
+    if saved is None:
+        saved = torch.empty(lib().iseg_bn_saved_bytes(Cc), dtype=torch.uint8, device=x.device)
+    ws = workspace(x.device).get(lib().iseg_bn_fwd_ws(M, Cc))
+    iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, e, saved, ws, status)
+    return y, e, saved
+
+
+def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None):
+    Cc = x.shape[-1]
+    M = x.numel() // Cc
+    cfg = cfg or bn_cfg()
+    dx = torch.empty_like(x)
+    e = new_exp(x.device)
+    dg = torch.empty(Cc, dtype=torch.int64, device=x.device)
+    db = torch.empty(Cc, dtype=torch.int64, device=x.device)
+    dge, dbe = new_exp(x.device), new_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_bn_bwd_ws(M, Cc))
+    iseg_bn_bwd(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, e, dg, db, dge, dbe, ws, status)
+    return dx, e, dg, db, dge, dbe
+
+
+def bn_saved_view(saved, Cc):
+    """Named views of the saved-state buffer (layout of iseg.h)."""
+    def al(v):
+        return (v + 255) // 256 * 256
+    off = 256
+    out = {"hdr": saved[:64].view(torch.int32)}
+    for name in ("n_mu", "n_sigma", "den", "qmin", "qmax"):
+        out[name] = saved[off:off + 4 * Cc].view(torch.int32)
+        off += al(4 * Cc)
+    out["xcode"] = saved[off:off + 512 * Cc].view(torch.int16).view(Cc, 256)
+    off += al(512 * Cc)
+    out["flags"] = saved[off:off + 256 * Cc].view(Cc, 256)
+    off += al(256 * Cc)
+    out["acode"] = saved[off:off + 256 * Cc].view(torch.int8).view(Cc, 256)
+    return out
+
+
+def weight_update(master, g, g_exp, lr_shift, master_exp=-23, k_U=24, k_W=8, w_q=None, status=None):
+    if w_q is None:
+        w_q = torch.empty(master.shape, dtype=torch.int8, device=master.device)
+    iseg_weight_update(master, g, g_exp, lr_shift, master_exp, k_U, k_W, w_q, status)
+    return w_q
+
+
+def weight_quant(master, k_U=24, k_W=8):
+    w_q = torch.empty(master.shape, dtype=torch.int8, device=master.device)
+    iseg_weight_quant(master, k_U, k_W, w_q)
+    return w_q
+
+
+def maxpool_fwd(x, x_exp, k, stride, pad=0):
+    N, H, W, Cc = x.shape
+    P = (H + 2 * pad - k) // stride + 1
+    Q = (W + 2 * pad - k) // stride + 1
+    y = torch.empty((N, P, Q, Cc), dtype=torch.int8, device=x.device)
+    e = new_exp(x.device)
+    iseg_maxpool_fwd(x, x_exp, k, stride, pad, y, e)
+    return y, e
+
+
+def maxpool_bwd(dy, dy_exp, x, k, stride, pad=0, bits=8, status=None):
+    N, H, W, Cc = x.shape
+    dx = torch.empty_like(x)
+    e = new_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_maxpool_bwd_ws(N, H, W, Cc))
+    iseg_maxpool_bwd(dy, dy_exp, x, k, stride, pad, bits, dx, e, ws, status)
+    return dx, e

@@ -53,3 +53,53 @@ def labels(seed, shape, classes):
 
 def uniform_f32(seed, shape, lo=-1.0, hi=1.0):
     return rng(seed).uniform(lo, hi, size=shape).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# workload shapes (shapes and seeds only)
+# ---------------------------------------------------------------------------
+# A layer is ("conv", C_in, C_out, R, stride, pad, dilation) -- each conv is
+# followed by L1BN + ReLU -- or ("maxpool", k, stride, pad).
+
+# Single 3x3 conv 16 -> 16, stride 1, pad 1, on a 1x32x32 map, then L1BN over
+# 16 channels; the input gradient is computed too.
+SINGLE_CONV = dict(id=1, name="single-conv3x3-16ch-32x32-n1", N=1, H=32, W=32, C=16,
+                   input_grad=True,
+                   layers=[("conv", 16, 16, 3, 1, 1, 1)])
+
+# FCN-VGG16 encoder slice: conv1_1, conv1_2, maxpool 2x2/2, conv2_1, conv2_2,
+# batch 8 of 3x224x224 images; no gradient is taken w.r.t. the image.
+VGG16_BLOCKS12 = dict(id=2, name="fcn-vgg16-blocks1-2-n8-224", N=8, H=224, W=224, C=3,
+                      input_grad=False,
+                      layers=[("conv", 3, 64, 3, 1, 1, 1),
+                              ("conv", 64, 64, 3, 1, 1, 1),
+                              ("maxpool", 2, 2, 0),
+                              ("conv", 64, 128, 3, 1, 1, 1),
+                              ("conv", 128, 128, 3, 1, 1, 1)])
+
+WORKLOADS = {1: SINGLE_CONV, 2: VGG16_BLOCKS12}
+
+
+def workload_inputs(wl, N=None):
+    """Seeded inputs of a workload: image/activation codes, float weights per
+    conv (He-normal), and the error arriving at the last activation."""
+    N = wl["N"] if N is None else N
+    x = int_codes(seed_for(wl["id"], 0), (N, wl["H"], wl["W"], wl["C"]))
+    weights = []
+    Hh, W = wl["H"], wl["W"]
+    ordinal = 1
+    for layer in wl["layers"]:
+        if layer[0] == "conv":
+            _, cin, cout, R, st, pad, dil = layer
+            weights.append(he_normal(seed_for(wl["id"], ordinal), (cout, R, R, cin), cin * R * R))
+            ordinal += 1
+            Hh = (Hh + 2 * pad - dil * (R - 1) - 1) // st + 1
+            W = (W + 2 * pad - dil * (R - 1) - 1) // st + 1
+            cl = cout
+        else:
+            _, k, st, pad = layer
+            Hh = (Hh + 2 * pad - k) // st + 1
+            W = (W + 2 * pad - k) // st + 1
+    dy = int_codes(seed_for(wl["id"], 50), (N, Hh, W, cl))
+    return dict(x=x, x_exp=ACT_EXP, weights=weights, dy=dy, dy_exp=ERR_EXP,
+                seed=seed_for(wl["id"], 0))

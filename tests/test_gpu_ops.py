@@ -1,0 +1,300 @@
+"""GPU parity: every libiseg entry point against the CPU oracle, bit-exact on
+codes and exponents, on seeded inputs that span several tiles and ragged
+tails, plus the degenerate cases (all-zero tensors, a single element, padding
+-only taps, constant BN channels)."""
+import numpy as np
+import pytest
+
+from paper_2011_14504_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2011_14504_amd import iseg
+    iseg.lib()
+    return torch.device("cuda", 0)
+
+
+def T(a, dev):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def E(v, dev):
+    import torch
+    return torch.tensor([int(v)], dtype=torch.int32, device=dev)
+
+
+def H(t):
+    return t.cpu().numpy()
+
+
+def ev(t):
+    return int(t.item())
+
+
+# ---------------------------------------------------------------------------
+# quantizers
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("n", [1, 17, 4096 + 5, 300001])
+@pytest.mark.parametrize("bits,mode", [(8, "sq"), (16, "sq"), (8, "uq"), (24, "uq")])
+def test_quantize_f32(orc, dev, n, bits, mode):
+    from paper_2011_14504_amd import iseg
+    x = synth.uniform_f32(n + bits, (n,), -3.0, 3.0) * np.float32(2.0 ** (n % 5 - 2))
+    if n > 4:
+        x[3] = np.float32(0.5) / np.float32(2 ** (bits - 1))      # an exact tie
+        x[4] = -x[3]
+    codes, e = iseg.quantize(T(x, dev), bits, iseg.ISEG_Q_SQ if mode == "sq" else iseg.ISEG_Q_UQ)
+    rc, re = orc.quantize_f32(x, bits, mode)
+    assert np.array_equal(H(codes).astype(np.int64), rc) and ev(e) == re
+
+
+def test_quantize_zero_tensor(orc, dev):
+    from paper_2011_14504_amd import iseg
+    x = np.zeros(1000, np.float32)
+    codes, e = iseg.quantize(T(x, dev), 8)
+    assert not H(codes).any() and ev(e) == -7
+
+
+@pytest.mark.parametrize("dtype", [np.int32, np.int64])
+@pytest.mark.parametrize("n", [1, 15, 16, 1000003])
+@pytest.mark.parametrize("stochastic,keep", [(0, 1), (1, 1), (1, 0)])
+def test_requant(orc, dev, dtype, n, stochastic, keep):
+    from paper_2011_14504_amd import iseg
+    mag = 30 if dtype == np.int32 else 50
+    a = synth.rng(n + mag).integers(-(2 ** mag), 2 ** mag, size=n, dtype=np.int64).astype(dtype)
+    codes, e = iseg.requant(T(a, dev), E(-11, dev), 8, stochastic=stochastic, keep_scale=keep,
+                            seed=77, tensor_id=5, step=3)
+    rc, re = orc.requant(a, -11, 8, stochastic=bool(stochastic), keep_scale=bool(keep), seed=77,
+                         tensor_id=5, step=3)
+    assert np.array_equal(H(codes).astype(np.int64), rc) and ev(e) == re
+
+
+def test_requant_small_and_zero(orc, dev):
+    from paper_2011_14504_amd import iseg
+    for a in (np.zeros(37, np.int32), synth.int_codes(3, (999,), -20, 20, np.int32)):
+        codes, e = iseg.requant(T(a, dev), E(-4, dev), 8)
+        rc, re = orc.requant(a, -4, 8)
+        assert np.array_equal(H(codes).astype(np.int64), rc) and ev(e) == re
+
+
+def test_philox_host_hook_matches_oracle(orc):
+    from paper_2011_14504_amd import iseg
+    for ctr, key in [([1, 2, 3, 4], [5, 6]), ([0xffffffff, 0, 7, 9], [123, 456])]:
+        assert iseg.iseg_philox4x32_10(ctr, key) == list(orc.philox4x32_10(ctr, key))
+
+
+# ---------------------------------------------------------------------------
+# convolutions
+# ---------------------------------------------------------------------------
+# (N, H, W, C, K, R, stride, pad, dil)
+CONV_SHAPES = [
+    (1, 32, 32, 16, 16, 3, 1, 1, 1),      # single-conv workload
+    (2, 23, 19, 3, 64, 3, 1, 1, 1),       # C = 3 stem, ragged
+    (1, 37, 29, 64, 64, 3, 1, 1, 1),
+    (2, 17, 18, 64, 128, 3, 2, 1, 1),     # stride 2
+    (1, 20, 21, 32, 48, 3, 1, 2, 2),      # dilation 2
+    (1, 26, 26, 16, 24, 3, 1, 6, 6),      # atrous, many padding-only taps
+    (2, 14, 15, 64, 256, 1, 1, 0, 1),     # 1x1
+    (1, 30, 30, 3, 64, 7, 2, 3, 1),       # 7x7/2 stem
+    (1, 9, 11, 128, 130, 3, 1, 1, 1),     # K not a multiple of the tile
+    (1, 5, 5, 20, 21, 1, 1, 0, 1),        # C % 16 != 0, K = 21
+]
+
+
+def _geom(s):
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    return (N, Hh, W, Cc, K, R, R, st, st, pad, pad, d, d)
+
+
+@pytest.mark.parametrize("s", CONV_SHAPES, ids=str)
+def test_conv_fwd(orc, dev, s):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    x = synth.int_codes(11, (N, Hh, W, Cc))
+    w = synth.int_codes(12, (K, R, R, Cc))
+    raw, re = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d,
+                            out_mode=iseg.ISEG_OUT_RAW)
+    ref = orc.conv_fwd_raw(x, w, _geom(s))
+    assert np.array_equal(H(raw).astype(np.int64), ref) and ev(re) == -14
+    y, ye = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d)
+    rc, rce = orc.requant(ref, -14, 8)
+    assert np.array_equal(H(y).astype(np.int64), rc) and ev(ye) == rce
+
+
+@pytest.mark.parametrize("s", CONV_SHAPES, ids=str)
+def test_conv_bwd_data(orc, dev, s):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    P, Q = orc.conv_out_hw(_geom(s))
+    dy = synth.int_codes(21, (N, P, Q, K))
+    w = synth.int_codes(22, (K, R, R, Cc))
+    raw, re = iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc),
+                                 st, pad, d, out_mode=iseg.ISEG_OUT_RAW)
+    ref = orc.conv_bwd_data_raw(dy, w, _geom(s))
+    assert np.array_equal(H(raw).astype(np.int64), ref) and ev(re) == -27
+    dx, dxe = iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc),
+                                 st, pad, d)
+    rc, rce = orc.requant(ref, -27, 8)
+    assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
+
+
+@pytest.mark.parametrize("s", CONV_SHAPES, ids=str)
+def test_conv_bwd_weight(orc, dev, s):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    P, Q = orc.conv_out_hw(_geom(s))
+    dy = synth.int_codes(31, (N, P, Q, K))
+    x = synth.int_codes(32, (N, Hh, W, Cc))
+    raw, re = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (K, R, R, Cc),
+                                   st, pad, d, g_mode=iseg.ISEG_G_RAW)
+    ref = orc.conv_bwd_weight_raw(dy, x, _geom(s))
+    assert np.array_equal(H(raw), ref) and ev(re) == -27
+    for mode, keep in ((iseg.ISEG_G_KEEP, True), (iseg.ISEG_G_DROP, False)):
+        g, ge = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (K, R, R, Cc),
+                                     st, pad, d, g_mode=mode, seed=1450401, tensor_id=16, step=2)
+        rc, rce = orc.requant(ref, -27, 8, stochastic=True, keep_scale=keep, seed=1450401,
+                              tensor_id=16, step=2)
+        assert np.array_equal(H(g).astype(np.int64), rc) and ev(ge) == rce
+
+
+def test_conv_bwd_weight_long_reduction(orc, dev):
+    # more output pixels than one int32 partial may hold (131008): the split
+    # reduction must still be exact
+    x = synth.int_codes(41, (3, 220, 220, 4))
+    dy = synth.int_codes(42, (3, 220, 220, 4))
+    from paper_2011_14504_amd import iseg
+    raw, _ = iseg.conv_bwd_weight(T(dy, dev), E(0, dev), T(x, dev), E(0, dev), (4, 1, 1, 4),
+                                  1, 0, 1, g_mode=iseg.ISEG_G_RAW)
+    ref = orc.conv_bwd_weight_raw(dy, x, (3, 220, 220, 4, 4, 1, 1, 1, 1, 0, 0, 1, 1))
+    assert np.array_equal(H(raw), ref)
+
+
+def test_conv_zero_input(orc, dev):
+    from paper_2011_14504_amd import iseg
+    x = np.zeros((1, 8, 8, 16), np.int8)
+    w = synth.int_codes(5, (16, 3, 3, 16))
+    y, ye = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), 1, 1, 1)
+    assert not H(y).any() and ev(ye) == -14
+
+
+def test_conv_deterministic(dev):
+    from paper_2011_14504_amd import iseg
+    x = synth.int_codes(51, (2, 40, 40, 64))
+    dy = synth.int_codes(52, (2, 40, 40, 64))
+    a, ae = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (64, 3, 3, 64),
+                                 1, 1, 1, seed=9)
+    b, be = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (64, 3, 3, 64),
+                                 1, 1, 1, seed=9)
+    assert np.array_equal(H(a), H(b)) and ev(ae) == ev(be)
+
+
+# ---------------------------------------------------------------------------
+# L1 batch normalization
+# ---------------------------------------------------------------------------
+BN_CASES = [
+    dict(M=1024, C=16, x_exp=-9, cfg={}),
+    dict(M=4099, C=64, x_exp=-7, cfg=dict(relu=0)),
+    dict(M=777, C=128, x_exp=-14, cfg=dict(eps_code=1)),
+    dict(M=300, C=256, x_exp=2, cfg=dict(k_E2=8)),
+    dict(M=5, C=4, x_exp=-30, cfg={}),
+    dict(M=2000, C=48, x_exp=-11, cfg=dict(k_E2=8, relu=0), const=True),
+    dict(M=1500, C=20, x_exp=-7, cfg=dict(k_xhat=8, k_mu=8, k_sigma=8)),
+]
+
+
+def _bn_inputs(i, case):
+    x = synth.int_codes(100 + i, (case["M"], case["C"]))
+    if case.get("const"):
+        x[:, 1] = 17
+        x[:, 2] = 0
+    gq = synth.int_codes(200 + i, (case["C"],))
+    bq = synth.int_codes(300 + i, (case["C"],))
+    dA = synth.int_codes(400 + i, (case["M"], case["C"]))
+    return x, gq, bq, dA
+
+
+@pytest.mark.parametrize("i", range(len(BN_CASES)))
+def test_bn_fwd(orc, dev, i):
+    from paper_2011_14504_amd import iseg
+    case = BN_CASES[i]
+    x, gq, bq, _ = _bn_inputs(i, case)
+    cfg = dict(orc.BN_DEFAULT, **case["cfg"])
+    y, ye, saved = iseg.bn_fwd(T(x, dev), E(case["x_exp"], dev), T(gq, dev), T(bq, dev),
+                               iseg.bn_cfg(**cfg))
+    r = orc.bn_fwd(x, case["x_exp"], gq, bq, cfg)
+    sv = iseg.bn_saved_view(saved, case["C"])
+    assert np.array_equal(H(sv["n_mu"]), r["n_mu"])
+    assert np.array_equal(H(sv["n_sigma"]), r["n_sigma"])
+    assert int(H(sv["hdr"])[0]) == r["b"]
+    xc = H(sv["xcode"])
+    cols = np.arange(case["C"])[None, :]
+    assert np.array_equal(xc[cols, x.astype(np.int64) + 128], r["xhat"])
+    assert np.array_equal(H(y), r["y"]) and ev(ye) == r["y_exp"]
+
+
+@pytest.mark.parametrize("i", range(len(BN_CASES)))
+def test_bn_bwd(orc, dev, i):
+    from paper_2011_14504_amd import iseg
+    case = BN_CASES[i]
+    x, gq, bq, dA = _bn_inputs(i, case)
+    cfg = dict(orc.BN_DEFAULT, **case["cfg"])
+    c = iseg.bn_cfg(**cfg)
+    y, ye, saved = iseg.bn_fwd(T(x, dev), E(case["x_exp"], dev), T(gq, dev), T(bq, dev), c)
+    dx, dxe, dg, db, dge, dbe = iseg.bn_bwd(T(dA, dev), E(-20, dev), T(x, dev), T(gq, dev), saved, c)
+    r = orc.bn_bwd(dA, -20, x, case["x_exp"], gq, bq, cfg)
+    assert np.array_equal(H(db), r["dbeta"]) and ev(dbe) == r["dbeta_exp"]
+    assert np.array_equal(H(dg), r["dgamma"]) and ev(dge) == r["dgamma_exp"]
+    assert np.array_equal(H(dx), r["dx"]) and ev(dxe) == r["dx_exp"]
+
+
+def test_bn_exponent_out_of_range_flags_status(dev):
+    import torch
+    from paper_2011_14504_amd import iseg
+    x = synth.int_codes(9, (64, 16))
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    iseg.bn_fwd(T(x, dev), E(30, dev), T(np.full(16, 64, np.int8), dev),
+                T(np.zeros(16, np.int8), dev), status=st)
+    assert ev(st) & iseg.ISEG_DEV_RANGE
+
+
+# ---------------------------------------------------------------------------
+# update, weight quantizer, max pooling
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("g_exp,lr,mexp", [(-20, 10, -23), (-3, 4, -23), (-30, 0, -22), (5, 2, -23)])
+def test_weight_update(orc, dev, g_exp, lr, mexp):
+    from paper_2011_14504_amd import iseg
+    n = 100003
+    master = synth.int_codes(61, (n,), -(2 ** 23) + 1, 2 ** 23 - 1, np.int32)
+    g = synth.int_codes(62, (n,))
+    m_t = T(master, dev)
+    wq = iseg.weight_update(m_t, T(g, dev), E(g_exp, dev), lr, mexp)
+    rm, rw = orc.weight_update(master, g, g_exp, lr, mexp)
+    assert np.array_equal(H(m_t), rm) and np.array_equal(H(wq), rw)
+
+
+def test_weight_quant_and_master_init(orc, dev):
+    from paper_2011_14504_amd import iseg
+    w = synth.he_normal(63, (64, 3, 3, 64), 576)
+    m, me = iseg.quantize(T(w, dev), 24, iseg.ISEG_Q_UQ)
+    rm, rme = orc.master_init(w)
+    assert np.array_equal(H(m), rm) and ev(me) == rme == -23
+    assert np.array_equal(H(iseg.weight_quant(m)), orc.weight_quant(rm))
+
+
+@pytest.mark.parametrize("k,st,pad", [(2, 2, 0), (3, 2, 1), (3, 1, 1)])
+def test_maxpool(orc, dev, k, st, pad):
+    from paper_2011_14504_amd import iseg
+    x = synth.int_codes(71, (2, 29, 31, 24))
+    x[0, :4, :4, :] = 5                       # ties
+    y, ye = iseg.maxpool_fwd(T(x, dev), E(-6, dev), k, st, pad)
+    assert np.array_equal(H(y), orc.maxpool_fwd(x, k, st, pad)) and ev(ye) == -6
+    dy = synth.int_codes(72, H(y).shape)
+    dx, dxe = iseg.maxpool_bwd(T(dy, dev), E(-20, dev), T(x, dev), k, st, pad)
+    rc, rce = orc.maxpool_bwd(dy, -20, x, k, st, pad)
+    assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce

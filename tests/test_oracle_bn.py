@@ -166,6 +166,6 @@ def test_l1_deviation_ratio_gaussian(orc):
 def test_l1bn_range_preconditions(orc):
     x = synth.int_codes(91, (4, 2))
     with pytest.raises(orc.OracleError):
-        orc.bn_fwd(x, 21, [64, 64], [0, 0], CFG)
+        orc.bn_fwd(x, 17, [64, 64], [0, 0], CFG)
     with pytest.raises(orc.OracleError):
         orc.bn_fwd(x, -41, [64, 64], [0, 0], CFG)
