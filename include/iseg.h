@@ -190,9 +190,12 @@ int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, const int8_t* 
  * needs; its layout is:
  *   int32 hdr[16]: [0] b (xhat_q exponent is b+1-k_xhat), [1] y grid exponent,
  *                  [2] A exponent, [3] s_x;
- *   then, each 256-byte aligned: int32 n_mu[C], n_sigma[C], den[C], qmin[C],
- *   qmax[C]; int16 xhat_code[C][256] (by input code + 128); uint8 flags[C][256]
- *   (bit0: y > 0, bits1-2: sgn(x - mu_q) + 1); int8 a_code[C][256]. */
+ *   then, each 256-byte aligned: int32 n_mu[C], n_sigma[C], den[C] (the
+ *   denominator code), qmin[C], qmax[C] (occupied input-code range), t0[C]
+ *   (least code with x >= mu_q), p0[C] (least code with x > mu_q), mlo[C],
+ *   mhi[C] (codes with y > 0 form [mlo, mhi]); int16 xhat_code[C][256] (by
+ *   input code + 128); uint8 flags[C][256] (bit0: y > 0, bits1-2: sgn(x -
+ *   mu_q) + 1); int8 a_code[C][256]. */
 size_t iseg_bn_saved_bytes(int64_t C);
 size_t iseg_bn_fwd_ws(int64_t M, int64_t C);
 int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
@@ -232,6 +235,24 @@ int iseg_weight_update(int32_t* master, int64_t n, const int8_t* g, const int32_
                        int32_t lr_shift, int32_t master_exp, int32_t k_U, int32_t k_W,
                        int8_t* w_q, int32_t* dev_status, hipStream_t stream);
 
+/* iseg_bn_param_update -- Q_G and Q_U of one L1BN layer's gamma and beta in
+ * one launch: G = RQ(d, bits) keeping the scale (Eq. 5-6, 17) for d = dgamma
+ * (Philox tensor id tid_gamma) and d = dbeta (tid_beta), Philox index = the
+ * channel; then Delta = UQ(G 2^-lr_shift, k_U) (Eq. 19), master <- clamp(
+ * master - Delta), and the quantized parameter UQ(master, k_W) (Eq. 14's
+ * Q_gamma / Q_beta with the fixed x2 fold when master_exp = 2-k_U).  Equal to
+ * iseg_requant (stochastic, keep_scale) followed by iseg_weight_update.
+ *   dgamma, dbeta [C] int64 raw sums with device exponents; masters [C] int32
+ *   (updated in place); gamma_q, beta_q [C] int8 out; g_gamma, g_beta [C] int8
+ *   and g_*_exp (the quantized gradients) are optional outputs (NULL to skip). */
+int iseg_bn_param_update(const int64_t* dgamma, const int32_t* dgamma_exp,
+                         const int64_t* dbeta, const int32_t* dbeta_exp, int64_t C, int32_t bits,
+                         uint64_t seed, uint32_t tid_gamma, uint32_t tid_beta, uint32_t step,
+                         int32_t lr_shift, int32_t master_exp, int32_t k_U, int32_t k_W,
+                         int32_t* gamma_m, int32_t* beta_m, int8_t* gamma_q, int8_t* beta_q,
+                         int8_t* g_gamma, int8_t* g_beta, int32_t* g_gamma_exp, int32_t* g_beta_exp,
+                         int32_t* dev_status, hipStream_t stream);
+
 /* iseg_weight_quant -- Eq. 8 alone: w_q = UQ(master, k_W) from k_U-bit masters. */
 int iseg_weight_quant(const int32_t* master, int64_t n, int32_t k_U, int32_t k_W,
                       int8_t* w_q, hipStream_t stream);
@@ -263,6 +284,28 @@ int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
 /* Philox4x32-10 block on the host, the same function the kernels use
  * (exposed for known-answer tests; no GPU needed). */
 void iseg_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Measurement hook.  Kernel families that can be timed in place: */
+enum iseg_kernel_id {
+    ISEG_KID_NONE = 0,
+    ISEG_KID_CONV_FWD = 1,       /* implicit GEMM of iseg_conv_fwd */
+    ISEG_KID_CONV_BWD_DATA = 2,  /* implicit GEMM of iseg_conv_bwd_data */
+    ISEG_KID_CONV_WGRAD = 3,     /* implicit GEMM of iseg_conv_bwd_weight */
+    ISEG_KID_REQUANT = 4,        /* SQ/RQ code pass of any requantization */
+    ISEG_KID_BN_FWD_APPLY = 5,   /* output pass of iseg_bn_fwd */
+    ISEG_KID_BN_BWD_APPLY = 6,   /* output pass of iseg_bn_bwd */
+    ISEG_KID_BN_FWD_STATS1 = 7,  /* first statistics pass of iseg_bn_fwd */
+    ISEG_KID_BN_FWD_STATS2 = 8,  /* second statistics pass of iseg_bn_fwd */
+    ISEG_KID_BN_BWD_STATS = 9,   /* statistics pass of iseg_bn_bwd */
+    ISEG_KID_MAXPOOL_BWD = 10    /* routing pass of iseg_maxpool_bwd */
+};
+
+/* iseg_profile_arm -- the next launch of kernel family `kernel_id` (by any
+ * entry point, on any stream) records `start` immediately before and `stop`
+ * immediately after itself on its own stream, then the hook disarms.  The
+ * events are the caller's (hipEventCreate).  Process-global and not
+ * thread-safe: meant for benchmarks.  kernel_id ISEG_KID_NONE disarms. */
+int iseg_profile_arm(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 
 /* Library version string (static storage). */
 const char* iseg_version(void);

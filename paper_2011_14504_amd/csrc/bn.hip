@@ -3,23 +3,32 @@
 // Because the input of BN is an int8 code tensor, every per-element quantity
 // of the forward (xhat_q, y, the ReLU mask, sgn(x - mu_q), the output code A)
 // is a function of (channel, input code) only, and the backward's dx code is
-// a function of (channel, sgn class, masked error code).  So the work splits
-// into bandwidth-bound streaming passes over [M, C] (coalesced dword loads,
-// four channels per lane, per-channel sums reduced through LDS and one global
-// atomic per block and channel) and tiny finalize kernels that do the exact
-// rational arithmetic (__int128) once per channel or per table entry.
+// a function of (channel, sgn class, masked error code).  The work therefore
+// splits into
+//   * streaming passes over [M, C]: coalesced dword loads (four channels per
+//     lane), four rows in flight per lane, per-channel sums reduced in LDS and
+//     written as one partial per block and channel (no global atomics, so no
+//     same-address serialization across blocks);
+//   * per-channel finalize kernels (one block per channel) that reduce the
+//     partials and do the exact rational arithmetic in __int128, once per
+//     channel or per table entry.
+// sgn(x - mu_q) and the ReLU mask are monotone in the input code, so the
+// streaming passes get them from two thresholds per channel instead of a
+// table.
 //
-// Forward:  stats1 (sum q, min q, max q) -> stats2 (sum |x - mu_q|) ->
-//           fin1 (n_sigma, den, tensor max of |xhat|) -> fin2 (xhat codes,
-//           y, max |y|) -> fin3 (A codes) -> apply (table gather).
+// Forward:  stats1 (sum q, min q, max q) -> finmu -> stats2 (sum |x - mu_q|)
+//           -> finsig (n_sigma, den, max|xhat| exponent) -> fin2 (xhat codes,
+//           y, thresholds, max|y|) -> fin3 (A codes) -> apply (table gather).
 // Backward: stats (sum delta, sum delta*xhat, sum sgn, per-class extremes of
-//           delta) -> fin1 (dgamma, dbeta, max |gamma delta|) -> [stats2 for
-//           k_E2 < 15] -> fin2 (max |dx|) -> table -> apply (gather).
+//           delta) -> fin1 (dgamma, dbeta, max|gamma delta|) -> [stats2 for
+//           k_E2 < 15] -> fin2 (max|dx| exponent) -> table -> apply (gather).
 #include "iseg_common.h"
 
 namespace {
 
 constexpr int kSentinelLo = -(1 << 30);
+constexpr int kUnroll = 4;          // rows in flight per lane
+constexpr int kMaxBlocks = 1024;    // streaming blocks per call (all slices)
 
 // ---------------------------------------------------------------------------
 // saved-state layout (documented in iseg.h)
@@ -27,14 +36,15 @@ constexpr int kSentinelLo = -(1 << 30);
 struct Saved {
     int32_t* hdr;
     int32_t *n_mu, *n_sigma, *den, *qmin, *qmax;
-    int16_t* xcode;    // [C][256]
-    uint8_t* flags;    // [C][256]
-    int8_t* acode;     // [C][256]
+    int32_t *t0, *p0, *mlo, *mhi;   // sgn/mask thresholds
+    int16_t* xcode;                  // [C][256]
+    uint8_t* flags;                  // [C][256]
+    int8_t* acode;                   // [C][256]
 };
 
 size_t saved_bytes(int64_t C)
 {
-    return 256 + 5 * align256((size_t)C * 4) + align256((size_t)C * 512) +
+    return 256 + 9 * align256((size_t)C * 4) + align256((size_t)C * 512) +
            2 * align256((size_t)C * 256);
 }
 
@@ -42,76 +52,114 @@ Saved saved_map(void* base, int64_t C)
 {
     char* p = (char*)base;
     Saved s;
+    size_t v = align256((size_t)C * 4);
     s.hdr = (int32_t*)p; p += 256;
-    s.n_mu = (int32_t*)p; p += align256((size_t)C * 4);
-    s.n_sigma = (int32_t*)p; p += align256((size_t)C * 4);
-    s.den = (int32_t*)p; p += align256((size_t)C * 4);
-    s.qmin = (int32_t*)p; p += align256((size_t)C * 4);
-    s.qmax = (int32_t*)p; p += align256((size_t)C * 4);
+    s.n_mu = (int32_t*)p; p += v;
+    s.n_sigma = (int32_t*)p; p += v;
+    s.den = (int32_t*)p; p += v;
+    s.qmin = (int32_t*)p; p += v;
+    s.qmax = (int32_t*)p; p += v;
+    s.t0 = (int32_t*)p; p += v;
+    s.p0 = (int32_t*)p; p += v;
+    s.mlo = (int32_t*)p; p += v;
+    s.mhi = (int32_t*)p; p += v;
     s.xcode = (int16_t*)p; p += align256((size_t)C * 512);
     s.flags = (uint8_t*)p; p += align256((size_t)C * 256);
     s.acode = (int8_t*)p;
     return s;
 }
 
-// forward workspace
-struct FwdWs {
-    long long* S1;         // [C]
-    long long* sumabs;     // [C]
-    long long* Y;          // [C][256] y on the grid 2^e_y (before ReLU)
-    int32_t* b_glob;       // tensor exponent of Q_xhat's scale (atomicMax)
-    unsigned long long* maxY;
+// ---------------------------------------------------------------------------
+// streaming geometry: a block covers one channel slice of CS channels (CS % 4
+// == 0, CS divides C); lane g of a row handles channels 4g..4g+3 of the slice;
+// rpi rows are in flight per block step.
+// ---------------------------------------------------------------------------
+struct Stream {
+    int64_t M;
+    int32_t C, CS, G, rpi, gx;
 };
 
-size_t fwd_ws_bytes(int64_t C)
+int pick_cs(int64_t C, int csmax)
 {
-    return 256 + 2 * align256((size_t)C * 8) + align256((size_t)C * 256 * 8);
+    for (int cs = csmax; cs >= 4; cs -= 4)
+        if (C % cs == 0) return cs;
+    return 0;
 }
 
-FwdWs fwd_ws_map(void* base, int64_t C)
+Stream make_stream(int64_t M, int64_t C, int cs)
 {
-    char* p = (char*)base;
-    FwdWs w;
-    w.b_glob = (int32_t*)p;
-    w.maxY = (unsigned long long*)(p + 64);
-    p += 256;
-    w.S1 = (long long*)p; p += align256((size_t)C * 8);
-    w.sumabs = (long long*)p; p += align256((size_t)C * 8);
-    w.Y = (long long*)p;
-    return w;
+    Stream s;
+    s.M = M; s.C = (int32_t)C; s.CS = cs; s.G = cs / 4; s.rpi = 256 / s.G;
+    int nsl = (int)(C / cs);
+    int64_t want = kMaxBlocks / nsl;
+    if (want < 1) want = 1;
+    int64_t rows = ceil_div64(M, (int64_t)s.rpi * kUnroll);
+    s.gx = (int32_t)(rows < want ? rows : want);
+    if (s.gx < 1) s.gx = 1;
+    return s;
 }
 
-// backward workspace
-struct BwdWs {
-    long long *sd, *sdn, *sf, *sfn;   // [C] sums of delta, delta*n_xhat, f, f*n_xhat
-    int32_t* Z;                      // [C] sum of sgn(x - mu_q)
-    int32_t* mm;                     // [C][6]: (min, max) delta for sgn = -1, 0, +1
-    int8_t* lut;                     // [C][3][256] dx codes
-    int32_t* bdx;                    // tensor exponent of E1's scale (atomicMax)
-    unsigned long long* maxF;
-};
+dim3 stream_grid(const Stream& s) { return dim3((unsigned)s.gx, (unsigned)(s.C / s.CS)); }
 
-size_t bwd_ws_bytes(int64_t C)
+__device__ __forceinline__ bool stream_lane(const Stream& st, int& g, int& rsub)
 {
-    return 256 + 4 * align256((size_t)C * 8) + align256((size_t)C * 4) +
-           align256((size_t)C * 24) + align256((size_t)C * 768);
+    g = threadIdx.x % st.G;
+    rsub = threadIdx.x / st.G;
+    return rsub < st.rpi;
 }
 
-BwdWs bwd_ws_map(void* base, int64_t C)
+// Iterate the rows of this lane, kUnroll loads in flight: f(row, dword).
+template <typename F>
+__device__ __forceinline__ void stream_rows(const Stream& st, const int8_t* __restrict__ a, int c0,
+                                            int rsub, F f)
 {
-    char* p = (char*)base;
-    BwdWs w;
-    w.bdx = (int32_t*)p;
-    w.maxF = (unsigned long long*)(p + 64);
-    p += 256;
-    w.sd = (long long*)p; p += align256((size_t)C * 8);
-    w.sdn = (long long*)p; p += align256((size_t)C * 8);
-    w.sf = (long long*)p; p += align256((size_t)C * 8);
-    w.sfn = (long long*)p; p += align256((size_t)C * 8);
-    w.Z = (int32_t*)p; p += align256((size_t)C * 4);
-    w.mm = (int32_t*)p; p += align256((size_t)C * 24);
-    w.lut = (int8_t*)p;
-    return w;
+    const int64_t step = (int64_t)gridDim.x * st.rpi;
+    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += step * kUnroll) {
+        uint32_t v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; u++) {
+            int64_t rr = r + u * step;
+            v[u] = rr < st.M ? *(const uint32_t*)(a + rr * st.C + c0) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; u++) {
+            int64_t rr = r + u * step;
+            if (rr < st.M) f(rr, v[u]);
+        }
+    }
+}
+
+// two-input variant
+template <typename F>
+__device__ __forceinline__ void stream_rows2(const Stream& st, const int8_t* __restrict__ a,
+                                             const int8_t* __restrict__ b, int c0, int rsub, F f)
+{
+    const int64_t step = (int64_t)gridDim.x * st.rpi;
+    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += step * kUnroll) {
+        uint32_t va[kUnroll], vb[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; u++) {
+            int64_t rr = r + u * step;
+            va[u] = rr < st.M ? *(const uint32_t*)(a + rr * st.C + c0) : 0u;
+            vb[u] = rr < st.M ? *(const uint32_t*)(b + rr * st.C + c0) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; u++) {
+            int64_t rr = r + u * step;
+            if (rr < st.M) f(rr, va[u], vb[u]);
+        }
+    }
+}
+
+__device__ __forceinline__ int sbyte(uint32_t w, int i) { return (int)(int8_t)(w >> (8 * i)); }
+
+__device__ __forceinline__ bool sx_ok(int32_t s_x) { return s_x >= -40 && s_x <= 16; }
+
+// D = (x - mu_q) / 2^g for code q; g = min(s_x, e_mu)
+__device__ __forceinline__ int64_t bn_D(int q, int32_t s_x, int32_t n_mu, int e_mu)
+{
+    int g = s_x < e_mu ? s_x : e_mu;
+    return (int64_t)q * ((int64_t)1 << (s_x - g)) - (int64_t)n_mu * ((int64_t)1 << (e_mu - g));
 }
 
 struct BnCfg {
@@ -127,87 +175,71 @@ BnCfg to_cfg(const iseg_bn_cfg* c)
     return b;
 }
 
+// block-wide reductions of one value per thread (256 threads)
+template <typename T, typename Op>
+__device__ __forceinline__ T block_reduce(T v, Op op, T* sh)
+{
+    sh[threadIdx.x] = v;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sh[threadIdx.x] = op(sh[threadIdx.x], sh[threadIdx.x + o]);
+        __syncthreads();
+    }
+    T r = sh[0];
+    __syncthreads();
+    return r;
+}
+
+struct OpAdd { template <typename T> __device__ T operator()(T a, T b) const { return a + b; } };
+struct OpMin { template <typename T> __device__ T operator()(T a, T b) const { return a < b ? a : b; } };
+struct OpMax { template <typename T> __device__ T operator()(T a, T b) const { return a > b ? a : b; } };
+
 // ---------------------------------------------------------------------------
-// streaming geometry: a block covers one channel slice of CS channels (CS % 4
-// == 0, CS divides C); lane g of a row handles channels 4g..4g+3 of the
-// slice; rows_per_iter rows are in flight per block iteration.
+// forward workspace
 // ---------------------------------------------------------------------------
-struct Stream {
-    int64_t M;
-    int32_t C, CS, G, rpi;
+struct FwdWs {
+    int32_t* b_glob;                 // exponent of Q_xhat's scale (atomicMax)
+    unsigned long long* maxY;
+    int32_t *p_s1, *p_min, *p_max;   // [gx][C] partials
+    long long* p_abs;                // [gx][C]
+    long long* Y;                    // [C][256] y on the grid 2^e_y (before ReLU)
 };
 
-__device__ __forceinline__ bool stream_lane(const Stream& st, int& g, int& rsub)
+size_t fwd_ws_bytes(const Stream& st)
 {
-    g = threadIdx.x % st.G;
-    rsub = threadIdx.x / st.G;
-    return rsub < st.rpi;
+    size_t pc = (size_t)st.gx * st.C;
+    return 256 + 3 * align256(pc * 4) + align256(pc * 8) + align256((size_t)st.C * 256 * 8);
 }
 
-int pick_cs(int64_t C, int csmax)
+FwdWs fwd_ws_map(void* base, const Stream& st)
 {
-    for (int cs = csmax; cs >= 4; cs -= 4)
-        if (C % cs == 0) return cs;
-    return 0;
-}
-
-Stream make_stream(int64_t M, int64_t C, int cs)
-{
-    Stream s;
-    s.M = M; s.C = (int32_t)C; s.CS = cs; s.G = cs / 4; s.rpi = 256 / s.G;
-    return s;
-}
-
-dim3 stream_grid(const Stream& s)
-{
-    int nsl = s.C / s.CS;
-    int64_t want = 2048 / nsl;
-    if (want < 1) want = 1;
-    int64_t rows = ceil_div64(s.M, s.rpi);
-    int64_t gx = rows < want ? rows : want;
-    if (gx < 1) gx = 1;
-    return dim3((unsigned)gx, (unsigned)nsl);
-}
-
-__device__ __forceinline__ int sbyte(uint32_t w, int i) { return (int)(int8_t)(w >> (8 * i)); }
-
-__device__ __forceinline__ bool sx_ok(int32_t s_x) { return s_x >= -40 && s_x <= 16; }
-
-// D = (x - mu_q) / 2^g for code q; g = min(s_x, e_mu)
-__device__ __forceinline__ int64_t bn_D(int q, int32_t s_x, int32_t n_mu, int e_mu)
-{
-    int g = s_x < e_mu ? s_x : e_mu;
-    return (int64_t)q * ((int64_t)1 << (s_x - g)) - (int64_t)n_mu * ((int64_t)1 << (e_mu - g));
-}
-
-// n_mu from the channel sum (Eq. 14: mu_q = 2 UQ(mu/2, k_mu))
-__device__ __forceinline__ int32_t bn_n_mu(long long S1, int32_t s_x, int64_t M, const BnCfg& cf)
-{
-    return (int32_t)clamp_k128(rhu128((i128)S1, s_x - 1 + (cf.k_mu - 1), (i128)M), cf.k_mu);
+    char* p = (char*)base;
+    size_t pc = (size_t)st.gx * st.C;
+    FwdWs w;
+    w.b_glob = (int32_t*)p;
+    w.maxY = (unsigned long long*)(p + 64);
+    p += 256;
+    w.p_s1 = (int32_t*)p; p += align256(pc * 4);
+    w.p_min = (int32_t*)p; p += align256(pc * 4);
+    w.p_max = (int32_t*)p; p += align256(pc * 4);
+    w.p_abs = (long long*)p; p += align256(pc * 8);
+    w.Y = (long long*)p;
+    return w;
 }
 
 // ---------------------------------------------------------------------------
 // forward kernels
 // ---------------------------------------------------------------------------
-__global__ void k_bnf_init(FwdWs w, Saved sv, int32_t C)
-{
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c == 0) { *w.b_glob = kSentinelLo; *w.maxY = 0; }
-    if (c < C) { w.S1[c] = 0; w.sumabs[c] = 0; sv.qmin[c] = 1000; sv.qmax[c] = -1000; }
-}
-
-__global__ __launch_bounds__(256) void k_bnf_stats1(const int8_t* __restrict__ x, Stream st, FwdWs w,
-                                                    Saved sv)
+__global__ __launch_bounds__(256) void k_bnf_stats1(const int8_t* __restrict__ x, Stream st, FwdWs w)
 {
     __shared__ int32_t sS[128], sMin[128], sMax[128];
-    if (threadIdx.x < st.CS) { sS[threadIdx.x] = 0; sMin[threadIdx.x] = 1000; sMax[threadIdx.x] = -1000; }
+    if ((int)threadIdx.x < st.CS) { sS[threadIdx.x] = 0; sMin[threadIdx.x] = 1000; sMax[threadIdx.x] = -1000; }
     __syncthreads();
     int g, rsub;
     if (stream_lane(st, g, rsub)) {
         int s[4] = {0, 0, 0, 0}, mn[4] = {1000, 1000, 1000, 1000}, mx[4] = {-1000, -1000, -1000, -1000};
         int c0 = blockIdx.y * st.CS + g * 4;
-        for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += (int64_t)gridDim.x * st.rpi) {
-            uint32_t v = *(const uint32_t*)(x + r * st.C + c0);
+        stream_rows(st, x, c0, rsub, [&](int64_t, uint32_t v) {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 int q = sbyte(v, i);
@@ -215,7 +247,7 @@ __global__ __launch_bounds__(256) void k_bnf_stats1(const int8_t* __restrict__ x
                 mn[i] = q < mn[i] ? q : mn[i];
                 mx[i] = q > mx[i] ? q : mx[i];
             }
-        }
+        });
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             atomicAdd(&sS[g * 4 + i], s[i]);
@@ -224,11 +256,42 @@ __global__ __launch_bounds__(256) void k_bnf_stats1(const int8_t* __restrict__ x
         }
     }
     __syncthreads();
-    if (threadIdx.x < st.CS) {
-        int c = blockIdx.y * st.CS + threadIdx.x;
-        atomicAdd((unsigned long long*)&w.S1[c], (unsigned long long)(long long)sS[threadIdx.x]);
-        atomicMin(&sv.qmin[c], sMin[threadIdx.x]);
-        atomicMax(&sv.qmax[c], sMax[threadIdx.x]);
+    if ((int)threadIdx.x < st.CS) {
+        int64_t o = (int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x;
+        w.p_s1[o] = sS[threadIdx.x];
+        w.p_min[o] = sMin[threadIdx.x];
+        w.p_max[o] = sMax[threadIdx.x];
+    }
+}
+
+// per channel: reduce the stats1 partials, n_mu (Eq. 14), occupancy range
+__global__ __launch_bounds__(256) void k_bnf_finmu(const int32_t* x_exp, Stream st, FwdWs w, Saved sv,
+                                                   BnCfg cf)
+{
+    __shared__ long long sh64[256];
+    __shared__ int32_t sh32[256];
+    const int c = blockIdx.x;
+    long long s = 0;
+    int mn = 1000, mx = -1000;
+    for (int b = threadIdx.x; b < st.gx; b += 256) {
+        int64_t o = (int64_t)b * st.C + c;
+        s += w.p_s1[o];
+        mn = w.p_min[o] < mn ? w.p_min[o] : mn;
+        mx = w.p_max[o] > mx ? w.p_max[o] : mx;
+    }
+    s = block_reduce(s, OpAdd(), sh64);
+    mn = block_reduce(mn, OpMin(), sh32);
+    mx = block_reduce(mx, OpMax(), sh32);
+    if (threadIdx.x == 0) {
+        int32_t s_x = *x_exp;
+        int32_t nm = 0;
+        if (sx_ok(s_x))   // mu/2 = S1 2^(s_x - 1) / M, code floor(mu/2 2^(k_mu-1) + 1/2)
+            nm = (int32_t)clamp_k128(rhu128((i128)s, s_x - 1 + (cf.k_mu - 1), (i128)st.M), cf.k_mu);
+        sv.n_mu[c] = nm;
+        sv.qmin[c] = mn;
+        sv.qmax[c] = mx;
+        sv.t0[c] = 128; sv.p0[c] = 128; sv.mlo[c] = 128; sv.mhi[c] = -129;
+        if (c == 0) { *w.b_glob = kSentinelLo; *w.maxY = 0; }
     }
 }
 
@@ -236,60 +299,55 @@ __global__ __launch_bounds__(256) void k_bnf_stats2(const int8_t* __restrict__ x
                                                     Stream st, FwdWs w, Saved sv, BnCfg cf,
                                                     int32_t* dev_status)
 {
-    __shared__ int32_t sMu[128];
     __shared__ unsigned long long sA[128];
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) {
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) set_status(dev_status, ISEG_DEV_RANGE);
-        return;
+        s_x = -14;     // keep shifts defined; outputs are unspecified
     }
-    int e_mu = 2 - cf.k_mu;
-    if (threadIdx.x < st.CS) {
-        int c = blockIdx.y * st.CS + threadIdx.x;
-        int32_t nm = bn_n_mu(w.S1[c], s_x, st.M, cf);
-        sMu[threadIdx.x] = nm;
-        sA[threadIdx.x] = 0;
-        if (blockIdx.x == 0) sv.n_mu[c] = nm;
-    }
+    if ((int)threadIdx.x < st.CS) sA[threadIdx.x] = 0;
     __syncthreads();
+    const int e_mu = 2 - cf.k_mu;
     int g, rsub;
     if (stream_lane(st, g, rsub)) {
         int c0 = blockIdx.y * st.CS + g * 4;
         int64_t a[4] = {0, 0, 0, 0};
-        int gg = s_x < e_mu ? s_x : e_mu;
-        int64_t mulq = (int64_t)1 << (s_x - gg);
+        const int gg = s_x < e_mu ? s_x : e_mu;
+        const int64_t mulq = (int64_t)1 << (s_x - gg);
         int64_t off[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++) off[i] = (int64_t)sMu[g * 4 + i] * ((int64_t)1 << (e_mu - gg));
-        for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += (int64_t)gridDim.x * st.rpi) {
-            uint32_t v = *(const uint32_t*)(x + r * st.C + c0);
+        for (int i = 0; i < 4; i++) off[i] = (int64_t)sv.n_mu[c0 + i] * ((int64_t)1 << (e_mu - gg));
+        stream_rows(st, x, c0, rsub, [&](int64_t, uint32_t v) {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 int64_t D = (int64_t)sbyte(v, i) * mulq - off[i];
                 a[i] += D < 0 ? -D : D;
             }
-        }
+        });
 #pragma unroll
         for (int i = 0; i < 4; i++) atomicAdd(&sA[g * 4 + i], (unsigned long long)a[i]);
     }
     __syncthreads();
-    if (threadIdx.x < st.CS) {
-        int c = blockIdx.y * st.CS + threadIdx.x;
-        atomicAdd((unsigned long long*)&w.sumabs[c], sA[threadIdx.x]);
-    }
+    if ((int)threadIdx.x < st.CS)
+        w.p_abs[(int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x] = (long long)sA[threadIdx.x];
 }
 
-// per channel: n_sigma, den, and this channel's bound on max|xhat|
-__global__ void k_bnf_fin1(const int32_t* x_exp, int64_t M, int32_t C, FwdWs w, Saved sv, BnCfg cf)
+// per channel: sigma (Eq. 13-14), denominator, this channel's bound on max|xhat|
+__global__ __launch_bounds__(256) void k_bnf_finsig(const int32_t* x_exp, Stream st, FwdWs w, Saved sv,
+                                                    BnCfg cf)
 {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
+    __shared__ long long sh64[256];
+    const int c = blockIdx.x;
+    long long a = 0;
+    for (int b = threadIdx.x; b < st.gx; b += 256) a += w.p_abs[(int64_t)b * st.C + c];
+    a = block_reduce(a, OpAdd(), sh64);
+    if (threadIdx.x != 0) return;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
-    int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
-    int gg = s_x < e_mu ? s_x : e_mu;
+    const int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
+    const int gg = s_x < e_mu ? s_x : e_mu;
     // sigma/2 = sumabs 2^(g-1) / M ; n_sigma = floor(sigma/2 2^(k_sigma-1) + 1/2)
-    int32_t ns = (int32_t)clamp_k128(rhu128((i128)w.sumabs[c], gg - 1 + (cf.k_sigma - 1), (i128)M), cf.k_sigma);
+    int32_t ns = (int32_t)clamp_k128(rhu128((i128)a, gg - 1 + (cf.k_sigma - 1), (i128)st.M), cf.k_sigma);
     int32_t den = ns + cf.eps_code;
     if (den < 1) den = 1;
     sv.n_sigma[c] = ns;
@@ -297,7 +355,7 @@ __global__ void k_bnf_fin1(const int32_t* x_exp, int64_t M, int32_t C, FwdWs w, 
     int32_t nm = sv.n_mu[c];
     int best = kSentinelLo;
     int qs[2] = {sv.qmin[c], sv.qmax[c]};
-    for (int t = 0; t < 2; t++) {
+    for (int t = 0; t < 2; t++) {          // xhat is linear in q: extremes at qmin / qmax
         int64_t D = bn_D(qs[t], s_x, nm, e_mu);
         if (D == 0) continue;
         int e = ceil_pow2_exp128(abs128((i128)D), (i128)den) + gg - e_sig;
@@ -306,21 +364,22 @@ __global__ void k_bnf_fin1(const int32_t* x_exp, int64_t M, int32_t C, FwdWs w, 
     if (best > kSentinelLo) atomicMax(w.b_glob, best);
 }
 
-// per (channel, code): xhat code, y, flags; max |ReLU(y)| over the occurring codes
+// per (channel, code): xhat code, y, flags, thresholds; max |ReLU(y)| over the
+// occurring codes (y is monotone in q, so over qmin and qmax)
 __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w, Saved sv, BnCfg cf,
                                                   const int8_t* gamma_q, const int8_t* beta_q)
 {
-    int c = blockIdx.x;
-    int q = (int)threadIdx.x - 128;
+    const int c = blockIdx.x;
+    const int q = (int)threadIdx.x - 128;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
     int b = *w.b_glob;
     if (b == kSentinelLo) b = 0;
-    int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
-    int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
-    int e_xh = b - (cf.k_xhat - 1);
-    int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
-    int gg = s_x < e_mu ? s_x : e_mu;
+    const int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
+    const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
+    const int e_xh = b - (cf.k_xhat - 1);
+    const int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
+    const int gg = s_x < e_mu ? s_x : e_mu;
     int64_t D = bn_D(q, s_x, sv.n_mu[c], e_mu);
     int32_t den = sv.den[c];
     i128 nx = clamp_k128(rhu128((i128)D, gg - e_sig + (cf.k_xhat - 1) - b, (i128)den), cf.k_xhat);
@@ -330,6 +389,9 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w,
     int sg = (D > 0) - (D < 0);
     sv.flags[idx] = (uint8_t)((Y > 0 ? 1 : 0) | ((sg + 1) << 1));
     w.Y[idx] = (long long)Y;
+    if (D >= 0) atomicMin(&sv.t0[c], q);
+    if (D > 0) atomicMin(&sv.p0[c], q);
+    if (Y > 0) { atomicMin(&sv.mlo[c], q); atomicMax(&sv.mhi[c], q); }
     if (q == sv.qmin[c] || q == sv.qmax[c]) {
         i128 Yr = cf.relu && Y < 0 ? 0 : Y;
         atomicMax(w.maxY, (unsigned long long)abs128(Yr));
@@ -339,14 +401,14 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w,
 __global__ __launch_bounds__(256) void k_bnf_fin3(const int32_t* x_exp, FwdWs w, Saved sv, BnCfg cf,
                                                   int32_t* y_exp)
 {
-    int c = blockIdx.x;
+    const int c = blockIdx.x;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
     int b = *w.b_glob;
     if (b == kSentinelLo) b = 0;
-    int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
-    int e_xh = b - (cf.k_xhat - 1);
-    int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
+    const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
+    const int e_xh = b - (cf.k_xhat - 1);
+    const int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
     uint64_t M = *w.maxY;
     int r = M ? bitlen_u64(M) - (cf.k_A - 1) : 0;
     int idx = c * 256 + threadIdx.x;
@@ -366,89 +428,130 @@ __global__ __launch_bounds__(256) void k_bnf_apply(const int8_t* __restrict__ x,
                                                    Stream st, Saved sv)
 {
     __shared__ int8_t lut[128 * 256];
-    for (int i = threadIdx.x; i < st.CS * 64; i += blockDim.x)
-        ((uint32_t*)lut)[i] = ((const uint32_t*)(sv.acode + (int64_t)blockIdx.y * st.CS * 256))[i];
+    const uint32_t* src = (const uint32_t*)(sv.acode + (int64_t)blockIdx.y * st.CS * 256);
+    for (int i = threadIdx.x; i < st.CS * 64; i += blockDim.x) ((uint32_t*)lut)[i] = src[i];
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
-    int c0 = blockIdx.y * st.CS + g * 4;
+    const int c0 = blockIdx.y * st.CS + g * 4;
     const int8_t* l = lut + g * 4 * 256 + 128;
-    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += (int64_t)gridDim.x * st.rpi) {
-        uint32_t v = *(const uint32_t*)(x + r * st.C + c0);
+    stream_rows(st, x, c0, rsub, [&](int64_t r, uint32_t v) {
         uint32_t o = 0;
 #pragma unroll
         for (int i = 0; i < 4; i++) o |= (uint32_t)(uint8_t)l[i * 256 + sbyte(v, i)] << (8 * i);
         *(uint32_t*)(y + r * st.C + c0) = o;
-    }
+    });
 }
 
 // ---------------------------------------------------------------------------
-// backward kernels
+// backward workspace
 // ---------------------------------------------------------------------------
-__global__ void k_bnb_init(BwdWs w, int32_t C)
+struct BwdWs {
+    int32_t* bdx;                    // exponent of E1's scale (atomicMax)
+    unsigned long long* maxF;        // max |gamma delta|
+    int32_t *p_sd, *p_z;             // [gx][C] partials
+    long long *p_sdn, *p_sf, *p_sfn; // [gx][C]
+    int32_t* p_mm;                   // [6][gx][C]: (min, max) delta for sgn = -1, 0, +1
+    long long *sd, *sdn, *sf, *sfn;  // [C] reduced
+    int32_t *Z, *mm;                 // [C], [C][6]
+    int8_t* lut;                     // [C][3][256] dx codes
+};
+
+size_t bwd_ws_bytes(const Stream& st)
 {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c == 0) { *w.bdx = kSentinelLo; *w.maxF = 0; }
-    if (c < C) {
-        w.sd[c] = 0; w.sdn[c] = 0; w.sf[c] = 0; w.sfn[c] = 0; w.Z[c] = 0;
-        for (int i = 0; i < 3; i++) { w.mm[c * 6 + 2 * i] = 1000; w.mm[c * 6 + 2 * i + 1] = -1000; }
-    }
+    size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
+    return 256 + 2 * align256(pc * 4) + 3 * align256(pc * 8) + align256(pc * 24) +
+           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768);
 }
+
+BwdWs bwd_ws_map(void* base, const Stream& st)
+{
+    char* p = (char*)base;
+    size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
+    BwdWs w;
+    w.bdx = (int32_t*)p;
+    w.maxF = (unsigned long long*)(p + 64);
+    p += 256;
+    w.p_sd = (int32_t*)p; p += align256(pc * 4);
+    w.p_z = (int32_t*)p; p += align256(pc * 4);
+    w.p_sdn = (long long*)p; p += align256(pc * 8);
+    w.p_sf = (long long*)p; p += align256(pc * 8);
+    w.p_sfn = (long long*)p; p += align256(pc * 8);
+    w.p_mm = (int32_t*)p; p += align256(pc * 24);
+    w.sd = (long long*)p; p += align256(C * 8);
+    w.sdn = (long long*)p; p += align256(C * 8);
+    w.sf = (long long*)p; p += align256(C * 8);
+    w.sfn = (long long*)p; p += align256(C * 8);
+    w.Z = (int32_t*)p; p += align256(C * 4);
+    w.mm = (int32_t*)p; p += align256(C * 24);
+    w.lut = (int8_t*)p;
+    return w;
+}
+
+// sgn class (sgn + 1) and ReLU mask of an input code from the thresholds
+struct Thr {
+    int t0, p0, mlo, mhi;
+};
+
+__device__ __forceinline__ int thr_cls(const Thr& t, int q) { return 1 + (q >= t.p0) - (q < t.t0); }
+__device__ __forceinline__ bool thr_mask(const Thr& t, int q) { return q >= t.mlo && q <= t.mhi; }
 
 // pass 1: sum delta, sum delta*n_xhat, sum sgn, per-class min/max of delta
 __global__ __launch_bounds__(256) void k_bnb_stats(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                    Saved sv, int32_t relu)
 {
-    __shared__ uint8_t fl[64 * 256];
     __shared__ int16_t xc[64 * 256];
-    __shared__ unsigned long long sSd[64], sSdn[64];
-    __shared__ int32_t sZ[64], sMM[64 * 6];
-    int64_t cbase = (int64_t)blockIdx.y * st.CS;
-    for (int i = threadIdx.x; i < st.CS * 256; i += blockDim.x) {
-        fl[i] = sv.flags[cbase * 256 + i];
-        xc[i] = sv.xcode[cbase * 256 + i];
+    __shared__ Thr thr[64];
+    __shared__ unsigned long long sSdn[64];
+    __shared__ int32_t sSd[64], sZ[64], sMM[64 * 6];
+    const int64_t cbase = (int64_t)blockIdx.y * st.CS;
+    {
+        const uint32_t* src = (const uint32_t*)(sv.xcode + cbase * 256);
+        for (int i = threadIdx.x; i < st.CS * 128; i += blockDim.x) ((uint32_t*)xc)[i] = src[i];
     }
-    if (threadIdx.x < st.CS) {
-        sSd[threadIdx.x] = 0; sSdn[threadIdx.x] = 0; sZ[threadIdx.x] = 0;
-        for (int i = 0; i < 3; i++) { sMM[threadIdx.x * 6 + 2 * i] = 1000; sMM[threadIdx.x * 6 + 2 * i + 1] = -1000; }
+    if ((int)threadIdx.x < st.CS) {
+        int c = (int)cbase + threadIdx.x;
+        thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], relu ? sv.mlo[c] : -1000, relu ? sv.mhi[c] : 1000};
+        sSdn[threadIdx.x] = 0; sSd[threadIdx.x] = 0; sZ[threadIdx.x] = 0;
+        for (int k = 0; k < 3; k++) { sMM[threadIdx.x * 6 + 2 * k] = 1000; sMM[threadIdx.x * 6 + 2 * k + 1] = -1000; }
     }
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) { *w.maxF = 0; *w.bdx = kSentinelLo; }
     __syncthreads();
     int g, rsub;
     if (stream_lane(st, g, rsub)) {
-        int c0 = (int)cbase + g * 4;
+        const int c0 = (int)cbase + g * 4;
         int32_t sd[4] = {0, 0, 0, 0}, z[4] = {0, 0, 0, 0};
         int64_t sdn[4] = {0, 0, 0, 0};
         int32_t mm[4][6];
+        Thr t[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++)
+        for (int i = 0; i < 4; i++) {
+            t[i] = thr[g * 4 + i];
 #pragma unroll
             for (int k = 0; k < 3; k++) { mm[i][2 * k] = 1000; mm[i][2 * k + 1] = -1000; }
-        for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += (int64_t)gridDim.x * st.rpi) {
-            uint32_t vx = *(const uint32_t*)(x + r * st.C + c0);
-            uint32_t vd = *(const uint32_t*)(dy + r * st.C + c0);
+        }
+        stream_rows2(st, x, dy, c0, rsub, [&](int64_t, uint32_t vx, uint32_t vd) {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                int li = (g * 4 + i) * 256 + sbyte(vx, i) + 128;
-                int f = fl[li];
-                int d = sbyte(vd, i);
-                if (relu && !(f & 1)) d = 0;
-                int cls = (f >> 1) & 3;           // sgn + 1
+                int q = sbyte(vx, i);
+                int d = thr_mask(t[i], q) ? sbyte(vd, i) : 0;
+                int cls = thr_cls(t[i], q);
                 sd[i] += d;
-                sdn[i] += (int64_t)d * xc[li];
+                sdn[i] += (int64_t)d * xc[(g * 4 + i) * 256 + q + 128];
                 z[i] += cls - 1;
 #pragma unroll
-                for (int k = 0; k < 3; k++)
-                    if (cls == k) {
-                        mm[i][2 * k] = d < mm[i][2 * k] ? d : mm[i][2 * k];
-                        mm[i][2 * k + 1] = d > mm[i][2 * k + 1] ? d : mm[i][2 * k + 1];
-                    }
+                for (int k = 0; k < 3; k++) {
+                    bool hit = cls == k;
+                    mm[i][2 * k] = hit && d < mm[i][2 * k] ? d : mm[i][2 * k];
+                    mm[i][2 * k + 1] = hit && d > mm[i][2 * k + 1] ? d : mm[i][2 * k + 1];
+                }
             }
-        }
+        });
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             int cl = g * 4 + i;
-            atomicAdd(&sSd[cl], (unsigned long long)(long long)sd[i]);
+            atomicAdd(&sSd[cl], sd[i]);
             atomicAdd(&sSdn[cl], (unsigned long long)sdn[i]);
             atomicAdd(&sZ[cl], z[i]);
 #pragma unroll
@@ -459,38 +562,62 @@ __global__ __launch_bounds__(256) void k_bnb_stats(const int8_t* __restrict__ dy
         }
     }
     __syncthreads();
-    if (threadIdx.x < st.CS) {
-        int c = (int)cbase + threadIdx.x;
-        atomicAdd((unsigned long long*)&w.sd[c], sSd[threadIdx.x]);
-        atomicAdd((unsigned long long*)&w.sdn[c], sSdn[threadIdx.x]);
-        atomicAdd(&w.Z[c], sZ[threadIdx.x]);
-        for (int k = 0; k < 3; k++) {
-            atomicMin(&w.mm[c * 6 + 2 * k], sMM[threadIdx.x * 6 + 2 * k]);
-            atomicMax(&w.mm[c * 6 + 2 * k + 1], sMM[threadIdx.x * 6 + 2 * k + 1]);
-        }
+    if ((int)threadIdx.x < st.CS) {
+        const size_t pc = (size_t)st.gx * st.C;
+        int64_t o = (int64_t)blockIdx.x * st.C + cbase + threadIdx.x;
+        w.p_sd[o] = sSd[threadIdx.x];
+        w.p_sdn[o] = (long long)sSdn[threadIdx.x];
+        w.p_z[o] = sZ[threadIdx.x];
+        for (int k = 0; k < 6; k++) w.p_mm[k * pc + o] = sMM[threadIdx.x * 6 + k];
     }
 }
 
-__global__ void k_bnb_fin1(const int32_t* dy_exp, int32_t C, BwdWs w, Saved sv, BnCfg cf,
-                           const int8_t* gamma_q, int64_t* dgamma, int64_t* dbeta,
-                           int32_t* dgamma_exp, int32_t* dbeta_exp, int32_t* dev_status)
+// per channel: reduce pass-1 partials; dgamma, dbeta; max |gamma delta|
+__global__ __launch_bounds__(256) void k_bnb_fin1(const int32_t* dy_exp, Stream st, BwdWs w, Saved sv,
+                                                  BnCfg cf, const int8_t* gamma_q, int64_t* dgamma,
+                                                  int64_t* dbeta, int32_t* dgamma_exp,
+                                                  int32_t* dbeta_exp, int32_t* dev_status)
 {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
+    __shared__ long long sh64[256];
+    __shared__ int32_t sh32[256];
+    const int c = blockIdx.x;
+    const size_t pc = (size_t)st.gx * st.C;
+    long long sd = 0, sdn = 0;
+    int z = 0;
+    int mm[6] = {1000, -1000, 1000, -1000, 1000, -1000};
+    for (int b = threadIdx.x; b < st.gx; b += 256) {
+        int64_t o = (int64_t)b * st.C + c;
+        sd += w.p_sd[o];
+        sdn += w.p_sdn[o];
+        z += w.p_z[o];
+        for (int k = 0; k < 6; k++) {
+            int v = w.p_mm[k * pc + o];
+            mm[k] = (k & 1) ? (v > mm[k] ? v : mm[k]) : (v < mm[k] ? v : mm[k]);
+        }
+    }
+    sd = block_reduce(sd, OpAdd(), sh64);
+    sdn = block_reduce(sdn, OpAdd(), sh64);
+    z = block_reduce(z, OpAdd(), sh32);
+    for (int k = 0; k < 6; k++)
+        mm[k] = (k & 1) ? block_reduce(mm[k], OpMax(), sh32) : block_reduce(mm[k], OpMin(), sh32);
+    if (threadIdx.x != 0) return;
     int32_t s_d = *dy_exp;
     if (c == 0) {
         if (s_d < -60 || s_d > 16) set_status(dev_status, ISEG_DEV_RANGE);
         *dbeta_exp = s_d;
         *dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
     }
-    if (c >= C) return;
-    dbeta[c] = w.sd[c];
-    dgamma[c] = w.sdn[c];
+    w.sd[c] = sd; w.sdn[c] = sdn; w.Z[c] = z;
+    for (int k = 0; k < 6; k++) w.mm[c * 6 + k] = mm[k];
+    dbeta[c] = sd;
+    dgamma[c] = sdn;
     int amax = 0;
     for (int k = 0; k < 3; k++) {
-        int lo = w.mm[c * 6 + 2 * k], hi = w.mm[c * 6 + 2 * k + 1];
+        int lo = mm[2 * k], hi = mm[2 * k + 1];
         if (lo > hi) continue;
-        amax = (lo < 0 ? -lo : lo) > amax ? (lo < 0 ? -lo : lo) : amax;
-        amax = (hi < 0 ? -hi : hi) > amax ? (hi < 0 ? -hi : hi) : amax;
+        int a = lo < 0 ? -lo : lo, bb = hi < 0 ? -hi : hi;
+        amax = a > amax ? a : amax;
+        amax = bb > amax ? bb : amax;
     }
     int gq = gamma_q[c];
     uint64_t F = (uint64_t)(gq < 0 ? -gq : gq) * (uint64_t)amax;
@@ -508,37 +635,39 @@ __global__ __launch_bounds__(256) void k_bnb_stats2(const int8_t* __restrict__ d
                                                     const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                     Saved sv, BnCfg cf, const int8_t* gamma_q)
 {
-    __shared__ uint8_t fl[64 * 256];
     __shared__ int16_t xc[64 * 256];
+    __shared__ Thr thr[64];
     __shared__ unsigned long long sF[64], sFn[64];
-    int64_t cbase = (int64_t)blockIdx.y * st.CS;
-    for (int i = threadIdx.x; i < st.CS * 256; i += blockDim.x) {
-        fl[i] = sv.flags[cbase * 256 + i];
-        xc[i] = sv.xcode[cbase * 256 + i];
+    const int64_t cbase = (int64_t)blockIdx.y * st.CS;
+    {
+        const uint32_t* src = (const uint32_t*)(sv.xcode + cbase * 256);
+        for (int i = threadIdx.x; i < st.CS * 128; i += blockDim.x) ((uint32_t*)xc)[i] = src[i];
     }
-    if (threadIdx.x < st.CS) { sF[threadIdx.x] = 0; sFn[threadIdx.x] = 0; }
+    if ((int)threadIdx.x < st.CS) {
+        int c = (int)cbase + threadIdx.x;
+        thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], cf.relu ? sv.mlo[c] : -1000, cf.relu ? sv.mhi[c] : 1000};
+        sF[threadIdx.x] = 0; sFn[threadIdx.x] = 0;
+    }
     __syncthreads();
-    int r2 = bnb_r2(w, cf);
+    const int r2 = bnb_r2(w, cf);
     int g, rsub;
     if (stream_lane(st, g, rsub)) {
-        int c0 = (int)cbase + g * 4;
+        const int c0 = (int)cbase + g * 4;
         int gq[4];
+        Thr t[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++) gq[i] = gamma_q[c0 + i];
+        for (int i = 0; i < 4; i++) { gq[i] = gamma_q[c0 + i]; t[i] = thr[g * 4 + i]; }
         int64_t sf[4] = {0, 0, 0, 0}, sfn[4] = {0, 0, 0, 0};
-        for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += (int64_t)gridDim.x * st.rpi) {
-            uint32_t vx = *(const uint32_t*)(x + r * st.C + c0);
-            uint32_t vd = *(const uint32_t*)(dy + r * st.C + c0);
+        stream_rows2(st, x, dy, c0, rsub, [&](int64_t, uint32_t vx, uint32_t vd) {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                int li = (g * 4 + i) * 256 + sbyte(vx, i) + 128;
-                int d = sbyte(vd, i);
-                if (cf.relu && !(fl[li] & 1)) d = 0;
+                int q = sbyte(vx, i);
+                int d = thr_mask(t[i], q) ? sbyte(vd, i) : 0;
                 int64_t f = sq_code((int64_t)gq[i] * d, r2, cf.k_E2);
                 sf[i] += f;
-                sfn[i] += f * xc[li];
+                sfn[i] += f * xc[(g * 4 + i) * 256 + q + 128];
             }
-        }
+        });
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             atomicAdd(&sF[g * 4 + i], (unsigned long long)sf[i]);
@@ -546,10 +675,10 @@ __global__ __launch_bounds__(256) void k_bnb_stats2(const int8_t* __restrict__ d
         }
     }
     __syncthreads();
-    if (threadIdx.x < st.CS) {
-        int c = (int)cbase + threadIdx.x;
-        atomicAdd((unsigned long long*)&w.sf[c], sF[threadIdx.x]);
-        atomicAdd((unsigned long long*)&w.sfn[c], sFn[threadIdx.x]);
+    if ((int)threadIdx.x < st.CS) {
+        int64_t o = (int64_t)blockIdx.x * st.C + cbase + threadIdx.x;
+        w.p_sf[o] = (long long)sF[threadIdx.x];
+        w.p_sfn[o] = (long long)sFn[threadIdx.x];
     }
 }
 
@@ -566,15 +695,15 @@ struct BnbChan {
     int e_xh, Ebase, r2;
 };
 
-__device__ __forceinline__ BnbChan bnb_chan(int c, const int32_t* dy_exp, int64_t M, const BwdWs& w,
+__device__ __forceinline__ BnbChan bnb_chan(int c, const int32_t* dy_exp, const BwdWs& w,
                                             const Saved& sv, const BnCfg& cf, int gq, bool exact_e2)
 {
     BnbChan ch;
     ch.r2 = bnb_r2(w, cf);
-    int b = sv.hdr[0];
+    const int b = sv.hdr[0];
     ch.e_xh = b - (cf.k_xhat - 1);
-    int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
-    int s2 = *dy_exp + e_g + ch.r2;
+    const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
+    const int s2 = *dy_exp + e_g + ch.r2;
     ch.Ebase = s2 - e_sig + (ch.e_xh < 0 ? ch.e_xh : 0);
     if (exact_e2) {
         // E2 exact: f = gamma_q delta 2^-r2 with r2 <= 0
@@ -585,26 +714,39 @@ __device__ __forceinline__ BnbChan bnb_chan(int c, const int32_t* dy_exp, int64_
         ch.T = (i128)w.sfn[c];
     }
     ch.Z = (i128)w.Z[c];
-    (void)M;
     return ch;
 }
 
-__global__ void k_bnb_fin2(const int32_t* dy_exp, int64_t M, int32_t C, BwdWs w, Saved sv, BnCfg cf,
-                           const int8_t* gamma_q, int exact_e2)
+// per channel: (reduce pass-2 partials,) exponent bound of max|dx|
+__global__ __launch_bounds__(256) void k_bnb_fin2(const int32_t* dy_exp, Stream st, BwdWs w, Saved sv,
+                                                  BnCfg cf, const int8_t* gamma_q, int exact_e2)
 {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    int gq = gamma_q[c];
-    BnbChan ch = bnb_chan(c, dy_exp, M, w, sv, cf, gq, exact_e2);
-    i128 Dd = (i128)sv.den[c] * (i128)M * (i128)M;
+    __shared__ long long sh64[256];
+    const int c = blockIdx.x;
+    if (!exact_e2) {
+        long long sf = 0, sfn = 0;
+        for (int b = threadIdx.x; b < st.gx; b += 256) {
+            int64_t o = (int64_t)b * st.C + c;
+            sf += w.p_sf[o];
+            sfn += w.p_sfn[o];
+        }
+        sf = block_reduce(sf, OpAdd(), sh64);
+        sfn = block_reduce(sfn, OpAdd(), sh64);
+        if (threadIdx.x == 0) { w.sf[c] = sf; w.sfn[c] = sfn; }
+    }
+    if (threadIdx.x != 0) return;
+    const int gq = gamma_q[c];
+    BnbChan ch = bnb_chan(c, dy_exp, w, sv, cf, gq, exact_e2);
+    const i128 M = st.M;
+    const i128 Dd = (i128)sv.den[c] * M * M;
     int best = kSentinelLo;
     for (int k = 0; k < 3; k++) {
         int lo = w.mm[c * 6 + 2 * k], hi = w.mm[c * 6 + 2 * k + 1];
         if (lo > hi) continue;
         int ds[2] = {lo, hi};
-        for (int t = 0; t < 2; t++) {
+        for (int t = 0; t < 2; t++) {      // |dx| is extreme at the class's extreme deltas
             int64_t f = sq_code((int64_t)gq * ds[t], ch.r2, cf.k_E2);
-            i128 B = bnb_bracket(f, k - 1, (i128)M, ch.Sf, ch.T, ch.Z, ch.e_xh);
+            i128 B = bnb_bracket(f, k - 1, M, ch.Sf, ch.T, ch.Z, ch.e_xh);
             if (B == 0) continue;
             int e = ceil_pow2_exp128(abs128(B), Dd) + ch.Ebase;
             best = e > best ? e : best;
@@ -614,23 +756,24 @@ __global__ void k_bnb_fin2(const int32_t* dy_exp, int64_t M, int32_t C, BwdWs w,
 }
 
 // dx code table for every (sgn class, masked error code) of a channel
-__global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t M, BwdWs w, Saved sv,
+__global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t Mrows, BwdWs w, Saved sv,
                                                  BnCfg cf, const int8_t* gamma_q, int exact_e2,
                                                  int32_t* dx_exp)
 {
-    int c = blockIdx.x;
-    int d = (int)threadIdx.x - 128;
-    int gq = gamma_q[c];
-    BnbChan ch = bnb_chan(c, dy_exp, M, w, sv, cf, gq, exact_e2);
+    const int c = blockIdx.x;
+    const int d = (int)threadIdx.x - 128;
+    const int gq = gamma_q[c];
+    BnbChan ch = bnb_chan(c, dy_exp, w, sv, cf, gq, exact_e2);
     int bdx = *w.bdx;
     if (bdx == kSentinelLo) bdx = 0;
     if (c == 0 && threadIdx.x == 0) *dx_exp = bdx - (cf.k_E1 - 1);
-    i128 Dd = (i128)sv.den[c] * (i128)M * (i128)M;
-    int64_t f = d < -127 ? 0 : sq_code((int64_t)gq * d, ch.r2, cf.k_E2);
+    const i128 M = Mrows;
+    const i128 Dd = (i128)sv.den[c] * M * M;
+    const int64_t f = d < -127 ? 0 : sq_code((int64_t)gq * d, ch.r2, cf.k_E2);
     for (int k = 0; k < 3; k++) {
         int8_t code = 0;
         if (d >= -127) {
-            i128 B = bnb_bracket(f, k - 1, (i128)M, ch.Sf, ch.T, ch.Z, ch.e_xh);
+            i128 B = bnb_bracket(f, k - 1, M, ch.Sf, ch.T, ch.Z, ch.e_xh);
             code = (int8_t)clamp_k128(rhu128(B, ch.Ebase + (cf.k_E1 - 1) - bdx, Dd), cf.k_E1);
         }
         w.lut[((int64_t)c * 3 + k) * 256 + threadIdx.x] = code;
@@ -642,32 +785,35 @@ __global__ __launch_bounds__(256) void k_bnb_apply(const int8_t* __restrict__ dy
                                                    int8_t* __restrict__ dx, Stream st, BwdWs w,
                                                    Saved sv, int32_t relu)
 {
-    __shared__ uint8_t fl[64 * 256];
     __shared__ int8_t lut[64 * 768];
-    int64_t cbase = (int64_t)blockIdx.y * st.CS;
-    for (int i = threadIdx.x; i < st.CS * 64; i += blockDim.x)
-        ((uint32_t*)fl)[i] = ((const uint32_t*)(sv.flags + cbase * 256))[i];
-    for (int i = threadIdx.x; i < st.CS * 192; i += blockDim.x)
-        ((uint32_t*)lut)[i] = ((const uint32_t*)(w.lut + cbase * 768))[i];
+    __shared__ Thr thr[64];
+    const int64_t cbase = (int64_t)blockIdx.y * st.CS;
+    {
+        const uint32_t* src = (const uint32_t*)(w.lut + cbase * 768);
+        for (int i = threadIdx.x; i < st.CS * 192; i += blockDim.x) ((uint32_t*)lut)[i] = src[i];
+    }
+    if ((int)threadIdx.x < st.CS) {
+        int c = (int)cbase + threadIdx.x;
+        thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], relu ? sv.mlo[c] : -1000, relu ? sv.mhi[c] : 1000};
+    }
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
-    int c0 = (int)cbase + g * 4;
-    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += (int64_t)gridDim.x * st.rpi) {
-        uint32_t vx = *(const uint32_t*)(x + r * st.C + c0);
-        uint32_t vd = *(const uint32_t*)(dy + r * st.C + c0);
+    const int c0 = (int)cbase + g * 4;
+    Thr t[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) t[i] = thr[g * 4 + i];
+    stream_rows2(st, x, dy, c0, rsub, [&](int64_t r, uint32_t vx, uint32_t vd) {
         uint32_t o = 0;
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            int cl = g * 4 + i;
-            int f = fl[cl * 256 + sbyte(vx, i) + 128];
-            int d = sbyte(vd, i);
-            if (relu && !(f & 1)) d = 0;
-            int cls = (f >> 1) & 3;
-            o |= (uint32_t)(uint8_t)lut[(cl * 3 + cls) * 256 + d + 128] << (8 * i);
+            int q = sbyte(vx, i);
+            int d = thr_mask(t[i], q) ? sbyte(vd, i) : 0;
+            int cls = thr_cls(t[i], q);
+            o |= (uint32_t)(uint8_t)lut[((g * 4 + i) * 3 + cls) * 256 + d + 128] << (8 * i);
         }
         *(uint32_t*)(dx + r * st.C + c0) = o;
-    }
+    });
 }
 
 bool cfg_ok(const iseg_bn_cfg* c)
@@ -679,14 +825,28 @@ bool cfg_ok(const iseg_bn_cfg* c)
            in(c->k_E2, 2, 16) && in(c->eps_code, 0, 1 << 15) && (c->relu == 0 || c->relu == 1);
 }
 
+bool shape_ok(int64_t M, int64_t C) { return M >= 1 && C >= 4 && M <= ((int64_t)1 << 22) && C <= (1 << 16); }
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // C ABI
 // ---------------------------------------------------------------------------
 extern "C" size_t iseg_bn_saved_bytes(int64_t C) { return C > 0 ? saved_bytes(C) : 0; }
-extern "C" size_t iseg_bn_fwd_ws(int64_t, int64_t C) { return C > 0 ? fwd_ws_bytes(C) : 0; }
-extern "C" size_t iseg_bn_bwd_ws(int64_t, int64_t C) { return C > 0 ? bwd_ws_bytes(C) : 0; }
+
+extern "C" size_t iseg_bn_fwd_ws(int64_t M, int64_t C)
+{
+    int cs = pick_cs(C, 128);
+    if (!shape_ok(M, C) || !cs) return 0;
+    return fwd_ws_bytes(make_stream(M, C, cs));
+}
+
+extern "C" size_t iseg_bn_bwd_ws(int64_t M, int64_t C)
+{
+    int cs = pick_cs(C, 64);
+    if (!shape_ok(M, C) || !cs) return 0;
+    return bwd_ws_bytes(make_stream(M, C, cs));
+}
 
 extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
                            const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
@@ -694,25 +854,25 @@ extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int
                            void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
 {
     if (M < 1 || C < 4) return ISEG_ERR_SHAPE;
-    if (M > ((int64_t)1 << 22) || C > (1 << 16)) return ISEG_ERR_UNSUPPORTED;
+    if (!shape_ok(M, C)) return ISEG_ERR_UNSUPPORTED;
     if (!x || !x_exp || !gamma_q || !beta_q || !y_out || !y_exp || !saved || !cfg_ok(cfg))
         return ISEG_ERR_ARG;
     int cs = pick_cs(C, 128);
     if (!cs || (((uintptr_t)x | (uintptr_t)y_out) & 3)) return ISEG_ERR_UNSUPPORTED;
-    if (!ws || ws_bytes < fwd_ws_bytes(C)) return ISEG_ERR_WORKSPACE;
+    Stream st = make_stream(M, C, cs);
+    if (!ws || ws_bytes < fwd_ws_bytes(st)) return ISEG_ERR_WORKSPACE;
     BnCfg cf = to_cfg(cfg);
     Saved sv = saved_map(saved, C);
-    FwdWs w = fwd_ws_map(ws, C);
-    Stream st = make_stream(M, C, cs);
+    FwdWs w = fwd_ws_map(ws, st);
     dim3 sg = stream_grid(st);
-    unsigned cg = (unsigned)ceil_div64(C, 256);
-    hipLaunchKernelGGL(k_bnf_init, dim3(cg), dim3(256), 0, stream, w, sv, (int32_t)C);
-    hipLaunchKernelGGL(k_bnf_stats1, sg, dim3(256), 0, stream, x, st, w, sv);
-    hipLaunchKernelGGL(k_bnf_stats2, sg, dim3(256), 0, stream, x, x_exp, st, w, sv, cf, dev_status);
-    hipLaunchKernelGGL(k_bnf_fin1, dim3(cg), dim3(256), 0, stream, x_exp, M, (int32_t)C, w, sv, cf);
-    hipLaunchKernelGGL(k_bnf_fin2, dim3((unsigned)C), dim3(256), 0, stream, x_exp, w, sv, cf, gamma_q, beta_q);
-    hipLaunchKernelGGL(k_bnf_fin3, dim3((unsigned)C), dim3(256), 0, stream, x_exp, w, sv, cf, y_exp);
-    hipLaunchKernelGGL(k_bnf_apply, sg, dim3(256), 0, stream, x, y_out, st, sv);
+    dim3 cb((unsigned)C);
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1, sg, dim3(256), 0, stream, x, st, w);
+    hipLaunchKernelGGL(k_bnf_finmu, cb, dim3(256), 0, stream, x_exp, st, w, sv, cf);
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2, sg, dim3(256), 0, stream, x, x_exp, st, w, sv, cf, dev_status);
+    hipLaunchKernelGGL(k_bnf_finsig, cb, dim3(256), 0, stream, x_exp, st, w, sv, cf);
+    hipLaunchKernelGGL(k_bnf_fin2, cb, dim3(256), 0, stream, x_exp, w, sv, cf, gamma_q, beta_q);
+    hipLaunchKernelGGL(k_bnf_fin3, cb, dim3(256), 0, stream, x_exp, w, sv, cf, y_exp);
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply, sg, dim3(256), 0, stream, x, y_out, st, sv);
     return launch_ok();
 }
 
@@ -723,31 +883,30 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
                            void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
 {
     if (M < 1 || C < 4) return ISEG_ERR_SHAPE;
-    if (M > ((int64_t)1 << 22) || C > (1 << 16)) return ISEG_ERR_UNSUPPORTED;
+    if (!shape_ok(M, C)) return ISEG_ERR_UNSUPPORTED;
     if (!dy || !dy_exp || !x || !gamma_q || !saved || !dx_out || !dx_exp || !dgamma || !dbeta ||
         !dgamma_exp || !dbeta_exp || !cfg_ok(cfg))
         return ISEG_ERR_ARG;
     int cs = pick_cs(C, 64);
     if (!cs || (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx_out) & 3)) return ISEG_ERR_UNSUPPORTED;
-    if (!ws || ws_bytes < bwd_ws_bytes(C)) return ISEG_ERR_WORKSPACE;
+    Stream st = make_stream(M, C, cs);
+    if (!ws || ws_bytes < bwd_ws_bytes(st)) return ISEG_ERR_WORKSPACE;
     BnCfg cf = to_cfg(cfg);
     Saved sv = saved_map((void*)saved, C);
-    BwdWs w = bwd_ws_map(ws, C);
-    Stream st = make_stream(M, C, cs);
+    BwdWs w = bwd_ws_map(ws, st);
     dim3 sg = stream_grid(st);
-    unsigned cg = (unsigned)ceil_div64(C, 256);
+    dim3 cb((unsigned)C);
     // E2 = SQ(gamma delta, k_E2) is exact when |gamma delta| <= 127^2 < 2^(k_E2-1)
-    int exact_e2 = cf.k_E2 >= 15;
-    hipLaunchKernelGGL(k_bnb_init, dim3(cg), dim3(256), 0, stream, w, (int32_t)C);
-    hipLaunchKernelGGL(k_bnb_stats, sg, dim3(256), 0, stream, dy, x, st, w, sv, cf.relu);
-    hipLaunchKernelGGL(k_bnb_fin1, dim3(cg), dim3(256), 0, stream, dy_exp, (int32_t)C, w, sv, cf,
-                       gamma_q, dgamma, dbeta, dgamma_exp, dbeta_exp, dev_status);
+    const int exact_e2 = cf.k_E2 >= 15;
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats, sg, dim3(256), 0, stream, dy, x, st, w, sv, cf.relu);
+    hipLaunchKernelGGL(k_bnb_fin1, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma,
+                       dbeta, dgamma_exp, dbeta_exp, dev_status);
     if (!exact_e2)
         hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(256), 0, stream, dy, x, st, w, sv, cf, gamma_q);
-    hipLaunchKernelGGL(k_bnb_fin2, dim3(cg), dim3(256), 0, stream, dy_exp, M, (int32_t)C, w, sv, cf,
-                       gamma_q, exact_e2);
-    hipLaunchKernelGGL(k_bnb_lut, dim3((unsigned)C), dim3(256), 0, stream, dy_exp, M, w, sv, cf,
-                       gamma_q, exact_e2, dx_exp);
-    hipLaunchKernelGGL(k_bnb_apply, sg, dim3(256), 0, stream, dy, x, dx_out, st, w, sv, cf.relu);
+    hipLaunchKernelGGL(k_bnb_fin2, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, exact_e2);
+    hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2,
+                       dx_exp);
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, sg, dim3(256), 0, stream, dy, x, dx_out,
+                      st, w, sv, cf.relu);
     return launch_ok();
 }

@@ -212,14 +212,15 @@ int launch_igemm(const IgemmArgs& a, hipStream_t s)
     bool vec = (a.Ci % 16) == 0 && (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0;
     dim3 block(256);
     unsigned gx = (unsigned)ceil_div64(a.Mrows, 128);
+    const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
     if (a.Nout > 64) {
         dim3 grid(gx, (unsigned)ceil_div64(a.Nout, 128));
-        if (vec) hipLaunchKernelGGL((k_conv_igemm<MODE, true, 128, 128>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_conv_igemm<MODE, false, 128, 128>), grid, block, 0, s, a);
+        if (vec) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, true, 128, 128>), grid, block, 0, s, a);
+        else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, false, 128, 128>), grid, block, 0, s, a);
     } else {
         dim3 grid(gx, 1);
-        if (vec) hipLaunchKernelGGL((k_conv_igemm<MODE, true, 128, 64>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_conv_igemm<MODE, false, 128, 64>), grid, block, 0, s, a);
+        if (vec) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, true, 128, 64>), grid, block, 0, s, a);
+        else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, false, 128, 64>), grid, block, 0, s, a);
     }
     return launch_ok();
 }
@@ -414,8 +415,8 @@ int launch_wgrad(WgradArgs a, hipStream_t s)
     a.pix_per_split = pps;
     splits = ceil_div64(a.NPQ, pps);
     dim3 grid((unsigned)ceil_div64(a.RSC, BN), (unsigned)ceil_div64(a.K, BM), (unsigned)splits);
-    if (vec) hipLaunchKernelGGL((k_conv_wgrad<true, BM, BN>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_conv_wgrad<false, BM, BN>), grid, dim3(256), 0, s, a);
+    if (vec) ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, (k_conv_wgrad<true, BM, BN>), grid, dim3(256), 0, s, a);
+    else ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, (k_conv_wgrad<false, BM, BN>), grid, dim3(256), 0, s, a);
     return launch_ok();
 }
 

@@ -207,3 +207,14 @@ int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* m
                   int32_t* dev_status, hipStream_t s);
 
 int launch_fill_u32(void* p, int64_t n_words, uint32_t v, hipStream_t s);
+
+// measurement hook (iseg_profile_arm): wrap one kernel launch
+bool prof_begin(int kid, hipStream_t s);
+void prof_end(int kid, hipStream_t s);
+
+#define ISEG_TIMED_LAUNCH(kid, stream, ...)            \
+    do {                                               \
+        bool iseg_timed_ = prof_begin((kid), (stream)); \
+        hipLaunchKernelGGL(__VA_ARGS__);               \
+        if (iseg_timed_) prof_end((kid), (stream));    \
+    } while (0)

@@ -83,6 +83,108 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd(const int8_t* __restrict__ 
     block_atomic_max_u64(mx, maxp);
 }
 
+// forward, four channels (one dword) per lane
+__global__ __launch_bounds__(256) void k_maxpool_fwd4(const int8_t* __restrict__ x, int8_t* __restrict__ y,
+                                                      PoolGeom g, const int32_t* x_exp, int32_t* y_exp)
+{
+    if (blockIdx.x == 0 && threadIdx.x == 0) *y_exp = *x_exp;
+    const int64_t C4 = g.C / 4;
+    const int64_t total = g.N * g.P * g.Q * C4;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t c4 = i % C4;
+        int64_t t = i / C4;
+        int q = (int)(t % g.Q);
+        t /= g.Q;
+        int p = (int)(t % g.P);
+        int64_t n = t / g.P;
+        int best[4] = {-1000, -1000, -1000, -1000};
+        for (int r = 0; r < g.k; r++) {
+            int h = p * g.st - g.pad + r;
+            if (h < 0 || h >= g.H) continue;
+            for (int s = 0; s < g.k; s++) {
+                int w = q * g.st - g.pad + s;
+                if (w < 0 || w >= g.W) continue;
+                uint32_t v = *(const uint32_t*)(x + ((n * g.H + h) * g.W + w) * g.C + c4 * 4);
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    int b = (int)(int8_t)(v >> (8 * j));
+                    best[j] = b > best[j] ? b : best[j];
+                }
+            }
+        }
+        uint32_t o = 0;
+#pragma unroll
+        for (int j = 0; j < 4; j++) o |= (uint32_t)(uint8_t)best[j] << (8 * j);
+        *(uint32_t*)(y + i * 4) = o;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_absmax_i8x4(const int8_t* __restrict__ p, int64_t n4,
+                                                     unsigned long long* maxp)
+{
+    uint64_t m = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t v = ((const uint32_t*)p)[i];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            int b = (int)(int8_t)(v >> (8 * j));
+            uint64_t a = (uint64_t)(b < 0 ? -b : b);
+            m = a > m ? a : m;
+        }
+    }
+    block_atomic_max_u64(m, maxp);
+}
+
+// backward for non-overlapping windows (k == stride, no padding), one lane per
+// input pixel and four channels: each input receives at most one error, so
+// max|routed| = max|dy| and the SQ codes are written directly.
+__global__ __launch_bounds__(256) void k_maxpool_bwd_disjoint(const int8_t* __restrict__ dy,
+                                                              const int8_t* __restrict__ x,
+                                                              int8_t* __restrict__ dx, PoolGeom g,
+                                                              const unsigned long long* maxp,
+                                                              const int32_t* dy_exp, int32_t* dx_exp,
+                                                              int bits)
+{
+    const uint64_t M = *maxp;
+    const int r = M ? bitlen_u64(M) - (bits - 1) : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *dx_exp = *dy_exp + r;
+    const int64_t C4 = g.C / 4;
+    const int64_t total = g.N * g.H * g.W * C4;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t c4 = i % C4;
+        int64_t t = i / C4;
+        int w = (int)(t % g.W);
+        t /= g.W;
+        int h = (int)(t % g.H);
+        int64_t n = t / g.H;
+        int p = h / g.k, q = w / g.k;
+        uint32_t o = 0;
+        if (p < g.P && q < g.Q) {
+            // first maximum of the window in row-major order, per channel
+            int best[4] = {-1000, -1000, -1000, -1000}, bpos[4] = {0, 0, 0, 0};
+            for (int rr = 0; rr < g.k; rr++)
+                for (int s = 0; s < g.k; s++) {
+                    uint32_t v = *(const uint32_t*)(x + ((n * g.H + p * g.k + rr) * g.W + q * g.k + s) * g.C + c4 * 4);
+#pragma unroll
+                    for (int j = 0; j < 4; j++) {
+                        int b = (int)(int8_t)(v >> (8 * j));
+                        if (b > best[j]) { best[j] = b; bpos[j] = rr * g.k + s; }
+                    }
+                }
+            uint32_t e = *(const uint32_t*)(dy + ((n * g.P + p) * g.Q + q) * g.C + c4 * 4);
+            int me = (h - p * g.k) * g.k + (w - q * g.k);
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                if (bpos[j] == me)
+                    o |= (uint32_t)(uint8_t)sq_code((int8_t)(e >> (8 * j)), r, bits) << (8 * j);
+        }
+        *(uint32_t*)(dx + i * 4) = o;
+    }
+}
+
 bool pool_geom(int64_t N, int64_t H, int64_t W, int64_t C, int32_t k, int32_t st, int32_t pad,
                PoolGeom* g)
 {
@@ -104,8 +206,12 @@ extern "C" int iseg_maxpool_fwd(const int8_t* x, const int32_t* x_exp, int64_t N
     if (!pool_geom(N, H, W, C, k, stride, pad, &g)) return ISEG_ERR_SHAPE;
     if (!x_exp || !y_exp || (N > 0 && (!x || !y))) return ISEG_ERR_ARG;
     int64_t total = g.N * g.P * g.Q * g.C;
-    hipLaunchKernelGGL(k_maxpool_fwd, dim3(grid_for(total, 256, 8192)), dim3(256), 0, stream,
-                       x, y, g, x_exp, y_exp);
+    if (C % 4 == 0 && (((uintptr_t)x | (uintptr_t)y) & 3) == 0)
+        hipLaunchKernelGGL(k_maxpool_fwd4, dim3(grid_for(total / 4, 256, 8192)), dim3(256), 0, stream,
+                           x, y, g, x_exp, y_exp);
+    else
+        hipLaunchKernelGGL(k_maxpool_fwd, dim3(grid_for(total, 256, 8192)), dim3(256), 0, stream,
+                           x, y, g, x_exp, y_exp);
     return launch_ok();
 }
 
@@ -130,9 +236,21 @@ extern "C" int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const i
     int rc = launch_fill_u32(maxp, 2, 0, stream);
     if (rc) return rc;
     int64_t total = N * H * W * C;
+    if (k == stride && pad == 0 && C % 4 == 0 &&
+        (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx) & 3) == 0) {
+        int64_t ndy = g.N * g.P * g.Q * C;
+        if (ndy > 0)
+            hipLaunchKernelGGL(k_absmax_i8x4, dim3(grid_for(ndy / 4, 256 * 4, 2048)), dim3(256), 0,
+                               stream, dy, ndy / 4, maxp);
+        if ((rc = launch_ok())) return rc;
+        ISEG_TIMED_LAUNCH(ISEG_KID_MAXPOOL_BWD, stream, k_maxpool_bwd_disjoint,
+                          dim3(grid_for(total / 4, 256, 8192)), dim3(256), 0, stream, dy, x, dx, g,
+                          maxp, dy_exp, dx_exp, bits);
+        return launch_ok();
+    }
     if (total > 0) {
-        hipLaunchKernelGGL(k_maxpool_bwd, dim3(grid_for(total, 256, 8192)), dim3(256), 0, stream,
-                           dy, x, acc, g, maxp);
+        ISEG_TIMED_LAUNCH(ISEG_KID_MAXPOOL_BWD, stream, k_maxpool_bwd, dim3(grid_for(total, 256, 8192)),
+                          dim3(256), 0, stream, dy, x, acc, g, maxp);
         if ((rc = launch_ok())) return rc;
     }
     (void)dev_status;

@@ -182,19 +182,19 @@ int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t*
     a.out_exp = out_exp; a.maxp = maxp;
     bool aligned = (((uintptr_t)in | (uintptr_t)out) & 15) == 0;
     if (in_dtype == ISEG_I32 && out_dtype == ISEG_I8 && aligned)
-        hipLaunchKernelGGL(k_requant_i32_i8, dim3(grid_for(n, 256 * 16, 4096)), dim3(256), 0, s,
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_i32_i8, dim3(grid_for(n, 256 * 16, 4096)), dim3(256), 0, s,
                            (const int32_t*)in, (int8_t*)out, a);
     else if (in_dtype == ISEG_I32 && out_dtype == ISEG_I8)
-        hipLaunchKernelGGL((k_requant_generic<int32_t, int8_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int32_t, int8_t>), dim3(grid_for(n, 256, 4096)),
                            dim3(256), 0, s, (const int32_t*)in, (int8_t*)out, a);
     else if (in_dtype == ISEG_I32 && out_dtype == ISEG_I16)
-        hipLaunchKernelGGL((k_requant_generic<int32_t, int16_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int32_t, int16_t>), dim3(grid_for(n, 256, 4096)),
                            dim3(256), 0, s, (const int32_t*)in, (int16_t*)out, a);
     else if (in_dtype == ISEG_I64 && out_dtype == ISEG_I8)
-        hipLaunchKernelGGL((k_requant_generic<int64_t, int8_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int64_t, int8_t>), dim3(grid_for(n, 256, 4096)),
                            dim3(256), 0, s, (const int64_t*)in, (int8_t*)out, a);
     else if (in_dtype == ISEG_I64 && out_dtype == ISEG_I16)
-        hipLaunchKernelGGL((k_requant_generic<int64_t, int16_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int64_t, int16_t>), dim3(grid_for(n, 256, 4096)),
                            dim3(256), 0, s, (const int64_t*)in, (int16_t*)out, a);
     else
         return ISEG_ERR_ARG;
@@ -355,6 +355,84 @@ extern "C" int iseg_weight_update(int32_t* master, int64_t n, const int8_t* g, c
     if (n == 0) return ISEG_OK;
     hipLaunchKernelGGL(k_weight_update, dim3(grid_for(n, 256, 4096)), dim3(256), 0, stream,
                        master, n, g, g_exp, lr_shift, master_exp, k_U, k_W, w_q);
+    return launch_ok();
+}
+
+// Q_G + Q_U of gamma (block 0) and beta (block 1) of one L1BN layer
+struct BnpArgs {
+    const int64_t* d[2];
+    const int32_t* dexp[2];
+    int32_t* master[2];
+    int8_t* wq[2];
+    int8_t* gout[2];
+    int32_t* gexp[2];
+    uint32_t tid[2];
+    int64_t C;
+    uint64_t seed;
+    uint32_t step;
+    int32_t bits, lr_shift, master_exp, k_U, k_W;
+};
+
+__global__ __launch_bounds__(256) void k_bn_param_update(BnpArgs a)
+{
+    __shared__ uint64_t red[4];
+    const int which = blockIdx.x;
+    const int64_t* d = a.d[which];
+    uint64_t m = 0;
+    for (int64_t c = threadIdx.x; c < a.C; c += blockDim.x) {
+        uint64_t v = uabs64(d[c]);
+        m = v > m ? v : m;
+    }
+    m = wave_max_u64(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = red[0];
+    for (int i = 1; i < 4; i++) m = red[i] > m ? red[i] : m;
+    const int r = m ? bitlen_u64(m) - (a.bits - 1) : 0;
+    const int32_t gexp = *a.dexp[which] + r;                   // Eq. 17 keeps the scale
+    if (threadIdx.x == 0 && a.gexp[which]) *a.gexp[which] = gexp;
+    const int sh = gexp - a.lr_shift - a.master_exp;
+    const int dq = a.k_U - a.k_W;
+    const int64_t lim = ((int64_t)1 << (a.k_U - 1)) - 1;
+    for (int64_t c = threadIdx.x; c < a.C; c += blockDim.x) {
+        int64_t g = r > 0 ? rq_code(d[c], r, a.bits, philox_draw(a.seed, a.tid[which], a.step, (uint64_t)c))
+                          : sq_code(d[c], r, a.bits);
+        if (a.gout[which]) a.gout[which][c] = (int8_t)g;
+        int64_t dW;
+        if (g == 0 || sh < -40) dW = 0;
+        else if (sh > 40) dW = g > 0 ? lim : -lim;
+        else if (sh >= 0) dW = clamp_k(g * ((int64_t)1 << sh), a.k_U);
+        else dW = clamp_k(shr_rhu(g, -sh), a.k_U);
+        int64_t mm = clamp_k((int64_t)a.master[which][c] - dW, a.k_U);
+        a.master[which][c] = (int32_t)mm;
+        a.wq[which][c] = (int8_t)clamp_k(shr_rhu(mm, dq), a.k_W);
+    }
+}
+
+extern "C" int iseg_bn_param_update(const int64_t* dgamma, const int32_t* dgamma_exp,
+                                    const int64_t* dbeta, const int32_t* dbeta_exp, int64_t C,
+                                    int32_t bits, uint64_t seed, uint32_t tid_gamma, uint32_t tid_beta,
+                                    uint32_t step, int32_t lr_shift, int32_t master_exp, int32_t k_U,
+                                    int32_t k_W, int32_t* gamma_m, int32_t* beta_m, int8_t* gamma_q,
+                                    int8_t* beta_q, int8_t* g_gamma, int8_t* g_beta,
+                                    int32_t* g_gamma_exp, int32_t* g_beta_exp, int32_t*,
+                                    hipStream_t stream)
+{
+    if (C < 1 || !dgamma || !dgamma_exp || !dbeta || !dbeta_exp || !gamma_m || !beta_m ||
+        !gamma_q || !beta_q)
+        return ISEG_ERR_ARG;
+    if (bits < 2 || bits > 8 || k_U < 9 || k_U > 31 || k_W < 2 || k_W > 8) return ISEG_ERR_ARG;
+    BnpArgs a;
+    a.d[0] = dgamma; a.d[1] = dbeta;
+    a.dexp[0] = dgamma_exp; a.dexp[1] = dbeta_exp;
+    a.master[0] = gamma_m; a.master[1] = beta_m;
+    a.wq[0] = gamma_q; a.wq[1] = beta_q;
+    a.gout[0] = g_gamma; a.gout[1] = g_beta;
+    a.gexp[0] = g_gamma_exp; a.gexp[1] = g_beta_exp;
+    a.tid[0] = tid_gamma; a.tid[1] = tid_beta;
+    a.C = C; a.seed = seed; a.step = step;
+    a.bits = bits; a.lr_shift = lr_shift; a.master_exp = master_exp; a.k_U = k_U; a.k_W = k_W;
+    hipLaunchKernelGGL(k_bn_param_update, dim3(2), dim3(256), 0, stream, a);
     return launch_ok();
 }
 

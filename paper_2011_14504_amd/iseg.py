@@ -23,6 +23,9 @@ ISEG_I8, ISEG_I16, ISEG_I32, ISEG_I64 = range(4)
 ISEG_Q_UQ, ISEG_Q_SQ = 0, 1
 ISEG_OUT_Q8, ISEG_OUT_RAW = 0, 1
 ISEG_G_KEEP, ISEG_G_DROP, ISEG_G_RAW = 0, 1, 2
+(ISEG_KID_NONE, ISEG_KID_CONV_FWD, ISEG_KID_CONV_BWD_DATA, ISEG_KID_CONV_WGRAD, ISEG_KID_REQUANT,
+ ISEG_KID_BN_FWD_APPLY, ISEG_KID_BN_BWD_APPLY, ISEG_KID_BN_FWD_STATS1, ISEG_KID_BN_FWD_STATS2,
+ ISEG_KID_BN_BWD_STATS, ISEG_KID_MAXPOOL_BWD) = range(11)
 
 _ERRS = {1: "ISEG_ERR_ARG", 2: "ISEG_ERR_SHAPE", 3: "ISEG_ERR_UNSUPPORTED",
          4: "ISEG_ERR_WORKSPACE", 5: "ISEG_ERR_DEVICE"}
@@ -73,7 +76,10 @@ _SIGS = {
     "iseg_maxpool_bwd_ws": ([_I64, _I64, _I64, _I64], _SZ),
     "iseg_maxpool_bwd": ([_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32, _I32, _I32, _P, _P, _P,
                           _SZ, _P, _P], C.c_int),
+    "iseg_bn_param_update": ([_P, _P, _P, _P, _I64, _I32, _U64, _U32, _U32, _U32, _I32, _I32, _I32,
+                              _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "iseg_philox4x32_10": ([_P, _P, _P], None),
+    "iseg_profile_arm": ([_I32, _P, _P], C.c_int),
     "iseg_version": ([], C.c_char_p),
 }
 
@@ -170,6 +176,17 @@ def iseg_weight_update(master, g, g_exp, lr_shift, master_exp, k_U, k_W, w_q, st
     _check(rc, "iseg_weight_update")
 
 
+def iseg_bn_param_update(dgamma, dgamma_exp, dbeta, dbeta_exp, bits, seed, tid_gamma, tid_beta, step,
+                         lr_shift, master_exp, k_U, k_W, gamma_m, beta_m, gamma_q, beta_q,
+                         g_gamma=None, g_beta=None, g_gamma_exp=None, g_beta_exp=None, status=None):
+    rc = lib().iseg_bn_param_update(_ptr(dgamma), _ptr(dgamma_exp), _ptr(dbeta), _ptr(dbeta_exp),
+                                    dgamma.numel(), bits, seed, tid_gamma, tid_beta, step, lr_shift,
+                                    master_exp, k_U, k_W, _ptr(gamma_m), _ptr(beta_m), _ptr(gamma_q),
+                                    _ptr(beta_q), _ptr(g_gamma), _ptr(g_beta), _ptr(g_gamma_exp),
+                                    _ptr(g_beta_exp), _ptr(status), _stream())
+    _check(rc, "iseg_bn_param_update")
+
+
 def iseg_weight_quant(master, k_U, k_W, w_q):
     rc = lib().iseg_weight_quant(_ptr(master), master.numel(), k_U, k_W, _ptr(w_q), _stream())
     _check(rc, "iseg_weight_quant")
@@ -199,6 +216,90 @@ def iseg_philox4x32_10(ctr, key):
 
 def iseg_version():
     return lib().iseg_version().decode()
+
+
+def iseg_profile_arm(kernel_id, start_event, stop_event):
+    _check(lib().iseg_profile_arm(kernel_id, start_event, stop_event), "iseg_profile_arm")
+
+
+# --------------------------------------------------------------------------
+# in-place kernel timing (HIP events recorded around one kernel launch)
+# --------------------------------------------------------------------------
+_hip = None
+
+
+def _hiprt():
+    global _hip
+    if _hip is None:
+        h = C.CDLL("libamdhip64.so")
+        h.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        h.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        h.hipEventSynchronize.argtypes = [C.c_void_p]
+        h.hipEventDestroy.argtypes = [C.c_void_p]
+        _hip = h
+    return _hip
+
+
+class KernelTimer:
+    """Times every launch of one kernel family whose layer key matches, with a
+    pair of HIP events that the library records around the launch on its own
+    stream (iseg_profile_arm)."""
+
+    def __init__(self, kernel_id, layer_match=None):
+        self.kid = kernel_id
+        self.match = tuple(layer_match) if layer_match is not None else None
+        self.pairs = []
+
+    def wants(self, kid, key):
+        return kid == self.kid and (self.match is None or tuple(key) == self.match)
+
+    def arm(self):
+        h = _hiprt()
+        a, b = C.c_void_p(), C.c_void_p()
+        if h.hipEventCreate(C.byref(a)) or h.hipEventCreate(C.byref(b)):
+            raise IsegError("hipEventCreate failed")
+        self.pairs.append((a, b))
+        iseg_profile_arm(self.kid, a, b)
+
+    def times_ms(self):
+        h = _hiprt()
+        out = []
+        for a, b in self.pairs:
+            h.hipEventSynchronize(b)
+            ms = C.c_float()
+            if h.hipEventElapsedTime(C.byref(ms), a, b) == 0:
+                out.append(ms.value)
+        return out
+
+    def mean_ms(self):
+        t = self.times_ms()
+        return sum(t) / len(t) if t else None
+
+    def count(self):
+        return len(self.pairs)
+
+    def close(self):
+        h = _hiprt()
+        for a, b in self.pairs:
+            h.hipEventDestroy(a)
+            h.hipEventDestroy(b)
+        self.pairs = []
+
+
+_TIMER = None
+
+
+def set_kernel_timer(timer):
+    """Install (or remove, with None) the timer consulted by the helpers below."""
+    global _TIMER
+    if timer is None:
+        iseg_profile_arm(ISEG_KID_NONE, None, None)
+    _TIMER = timer
+
+
+def _maybe_arm(kid, key):
+    if _TIMER is not None and _TIMER.wants(kid, key):
+        _TIMER.arm()
 
 
 # --------------------------------------------------------------------------
@@ -232,6 +333,11 @@ def workspace(device):
     return _WS[key]
 
 
+def _out_exp(device):
+    """Exponent slot for a kernel to write (no initialization kernel)."""
+    return torch.empty(1, dtype=torch.int32, device=device)
+
+
 def new_exp(device="cuda", value=0):
     return torch.full((1,), int(value), dtype=torch.int32, device=device)
 
@@ -260,7 +366,7 @@ def quantize(x, bits, mode=ISEG_Q_SQ, status=None):
     dt = {8: (torch.int8, ISEG_I8), 16: (torch.int16, ISEG_I16)}.get(
         8 if bits <= 8 else 16 if bits <= 16 else 32, (torch.int32, ISEG_I32))
     out = torch.empty(x.shape, dtype=dt[0], device=x.device)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_quantize_ws(x.numel()))
     iseg_quantize(x.contiguous(), bits, mode, dt[1], out, e, ws, status)
     return out, e
@@ -271,7 +377,7 @@ def requant(acc, acc_exp, bits=8, stochastic=False, keep_scale=True, seed=0, ten
     in_dt = {torch.int32: ISEG_I32, torch.int64: ISEG_I64}[acc.dtype]
     od, odt = (torch.int8, ISEG_I8) if bits <= 8 else (torch.int16, ISEG_I16)
     out = torch.empty(acc.shape, dtype=od, device=acc.device)
-    e = new_exp(acc.device)
+    e = _out_exp(acc.device)
     ws = workspace(acc.device).get(lib().iseg_requant_ws(acc.numel()))
     iseg_requant(acc.contiguous(), in_dt, acc_exp, bits, int(stochastic), int(keep_scale), seed,
                  tensor_id, step, odt, out, e, ws, status)
@@ -285,8 +391,9 @@ def conv_fwd(x, x_exp, w, w_exp, stride=1, pad=0, dil=1, out_mode=ISEG_OUT_Q8, s
     P, Q = conv_out_hw(g)
     y = torch.empty((N, P, Q, K), dtype=torch.int8 if out_mode == ISEG_OUT_Q8 else torch.int32,
                     device=x.device)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_conv_fwd_ws(C.byref(g), out_mode))
+    _maybe_arm(ISEG_KID_CONV_FWD, (N, H, W, Cc, K))
     iseg_conv_fwd(x, x_exp, w, w_exp, g, out_mode, y, e, ws, status)
     return y, e
 
@@ -298,8 +405,9 @@ def conv_bwd_data(dy, dy_exp, w, w_exp, x_shape, stride=1, pad=0, dil=1, out_mod
     g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
     dx = torch.empty((N, H, W, Cc), dtype=torch.int8 if out_mode == ISEG_OUT_Q8 else torch.int32,
                      device=dy.device)
-    e = new_exp(dy.device)
+    e = _out_exp(dy.device)
     ws = workspace(dy.device).get(lib().iseg_conv_bwd_data_ws(C.byref(g), out_mode))
+    _maybe_arm(ISEG_KID_CONV_BWD_DATA, (N, H, W, Cc, K))
     iseg_conv_bwd_data(dy, dy_exp, w, w_exp, g, out_mode, dx, e, ws, status)
     return dx, e
 
@@ -311,8 +419,9 @@ def conv_bwd_weight(dy, dy_exp, x, x_exp, w_shape, stride=1, pad=0, dil=1, g_mod
     g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
     dw = torch.empty((K, R, S, Cc), dtype=torch.int64 if g_mode == ISEG_G_RAW else torch.int8,
                      device=x.device)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_conv_bwd_weight_ws(C.byref(g), g_mode))
+    _maybe_arm(ISEG_KID_CONV_WGRAD, (N, H, W, Cc, K))
     iseg_conv_bwd_weight(dy, dy_exp, x, x_exp, g, g_mode, bits, seed, tensor_id, step, dw, e, ws,
                          status)
     return dw, e
@@ -323,10 +432,12 @@ def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None, saved=None, status=None):
     M = x.numel() // Cc
     cfg = cfg or bn_cfg()
     y = torch.empty_like(x)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     if saved is None:
         saved = torch.empty(lib().iseg_bn_saved_bytes(Cc), dtype=torch.uint8, device=x.device)
     ws = workspace(x.device).get(lib().iseg_bn_fwd_ws(M, Cc))
+    for kid in (ISEG_KID_BN_FWD_APPLY, ISEG_KID_BN_FWD_STATS1, ISEG_KID_BN_FWD_STATS2):
+        _maybe_arm(kid, (M, Cc))
     iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, e, saved, ws, status)
     return y, e, saved
 
@@ -336,11 +447,13 @@ def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None):
     M = x.numel() // Cc
     cfg = cfg or bn_cfg()
     dx = torch.empty_like(x)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     dg = torch.empty(Cc, dtype=torch.int64, device=x.device)
     db = torch.empty(Cc, dtype=torch.int64, device=x.device)
-    dge, dbe = new_exp(x.device), new_exp(x.device)
+    dge, dbe = _out_exp(x.device), _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_bn_bwd_ws(M, Cc))
+    for kid in (ISEG_KID_BN_BWD_APPLY, ISEG_KID_BN_BWD_STATS):
+        _maybe_arm(kid, (M, Cc))
     iseg_bn_bwd(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, e, dg, db, dge, dbe, ws, status)
     return dx, e, dg, db, dge, dbe
 
@@ -351,7 +464,7 @@ def bn_saved_view(saved, Cc):
         return (v + 255) // 256 * 256
     off = 256
     out = {"hdr": saved[:64].view(torch.int32)}
-    for name in ("n_mu", "n_sigma", "den", "qmin", "qmax"):
+    for name in ("n_mu", "n_sigma", "den", "qmin", "qmax", "t0", "p0", "mlo", "mhi"):
         out[name] = saved[off:off + 4 * Cc].view(torch.int32)
         off += al(4 * Cc)
     out["xcode"] = saved[off:off + 512 * Cc].view(torch.int16).view(Cc, 256)
@@ -380,7 +493,7 @@ def maxpool_fwd(x, x_exp, k, stride, pad=0):
     P = (H + 2 * pad - k) // stride + 1
     Q = (W + 2 * pad - k) // stride + 1
     y = torch.empty((N, P, Q, Cc), dtype=torch.int8, device=x.device)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     iseg_maxpool_fwd(x, x_exp, k, stride, pad, y, e)
     return y, e
 
@@ -388,7 +501,8 @@ def maxpool_fwd(x, x_exp, k, stride, pad=0):
 def maxpool_bwd(dy, dy_exp, x, k, stride, pad=0, bits=8, status=None):
     N, H, W, Cc = x.shape
     dx = torch.empty_like(x)
-    e = new_exp(x.device)
+    e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_maxpool_bwd_ws(N, H, W, Cc))
+    _maybe_arm(ISEG_KID_MAXPOOL_BWD, (N, H, W, Cc))
     iseg_maxpool_bwd(dy, dy_exp, x, k, stride, pad, bits, dx, e, ws, status)
     return dx, e

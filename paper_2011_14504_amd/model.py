@@ -90,13 +90,9 @@ class IntNet:
             G, Ge = iseg.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape,
                                          L["st"], L["pad"], L["dil"], iseg.ISEG_G_KEEP, 8,
                                          self.seed, 16 * li, self.step_no)
-            Gg, Gge = iseg.requant(dg, dge, 8, stochastic=True, keep_scale=True, seed=self.seed,
-                                   tensor_id=16 * li + 1, step=self.step_no)
-            Gb, Gbe = iseg.requant(db, dbe, 8, stochastic=True, keep_scale=True, seed=self.seed,
-                                   tensor_id=16 * li + 2, step=self.step_no)
-            r.update(dz=dz, dz_exp=dze, dgamma=dg, dbeta=db, G=G, G_exp=Ge, Gg=Gg, Gg_exp=Gge,
-                     Gb=Gb, Gb_exp=Gbe)
-            grads.append((L, G, Ge, Gg, Gge, Gb, Gbe))
+            r.update(dz=dz, dz_exp=dze, dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe,
+                     G=G, G_exp=Ge, li=li)
+            grads.append(r)
             if li > 1 or self.wl["input_grad"]:
                 e, ee = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
                                            L["st"], L["pad"], L["dil"])
@@ -105,10 +101,19 @@ class IntNet:
         return grads
 
     def update(self, grads):
-        for (L, G, Ge, Gg, Gge, Gb, Gbe) in grads:
-            iseg.weight_update(L["w_m"], G, Ge, self.lr_shift, W_MASTER_EXP, K_U, K_W, L["w_q"])
-            iseg.weight_update(L["g_m"], Gg, Gge, self.lr_shift, GB_MASTER_EXP, K_U, K_W, L["g_q"])
-            iseg.weight_update(L["b_m"], Gb, Gbe, self.lr_shift, GB_MASTER_EXP, K_U, K_W, L["b_q"])
+        for r in grads:
+            L, li = r["L"], r["li"]
+            iseg.weight_update(L["w_m"], r["G"], r["G_exp"], self.lr_shift, W_MASTER_EXP, K_U, K_W,
+                               L["w_q"])
+            C = L["cout"]
+            r["Gg"] = torch.empty(C, dtype=torch.int8, device=self.dev)
+            r["Gb"] = torch.empty(C, dtype=torch.int8, device=self.dev)
+            r["Gg_exp"], r["Gb_exp"] = iseg._out_exp(self.dev), iseg._out_exp(self.dev)
+            iseg.iseg_bn_param_update(r["dgamma"], r["dgamma_exp"], r["dbeta"], r["dbeta_exp"], 8,
+                                      self.seed, 16 * li + 1, 16 * li + 2, self.step_no,
+                                      self.lr_shift, GB_MASTER_EXP, K_U, K_W, L["g_m"], L["b_m"],
+                                      L["g_q"], L["b_q"], r["Gg"], r["Gb"], r["Gg_exp"],
+                                      r["Gb_exp"])
 
     def step(self):
         rec = self.forward()

@@ -83,12 +83,6 @@ def test_requant_small_and_zero(orc, dev):
         assert np.array_equal(H(codes).astype(np.int64), rc) and ev(e) == re
 
 
-def test_philox_host_hook_matches_oracle(orc):
-    from paper_2011_14504_amd import iseg
-    for ctr, key in [([1, 2, 3, 4], [5, 6]), ([0xffffffff, 0, 7, 9], [123, 456])]:
-        assert iseg.iseg_philox4x32_10(ctr, key) == list(orc.philox4x32_10(ctr, key))
-
-
 # ---------------------------------------------------------------------------
 # convolutions
 # ---------------------------------------------------------------------------
@@ -298,3 +292,30 @@ def test_maxpool(orc, dev, k, st, pad):
     dx, dxe = iseg.maxpool_bwd(T(dy, dev), E(-20, dev), T(x, dev), k, st, pad)
     rc, rce = orc.maxpool_bwd(dy, -20, x, k, st, pad)
     assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
+
+
+@pytest.mark.parametrize("C,d_exp", [(64, -30), (128, -12), (2048, -40)])
+def test_bn_param_update(orc, dev, C, d_exp):
+    # Q_G (Eq. 17, stochastic) then Q_U (Eq. 19) of gamma/beta in one launch
+    from paper_2011_14504_amd import iseg
+    import torch
+    rng = synth.rng(C)
+    dg = rng.integers(-(2 ** 40), 2 ** 40, size=C, dtype=np.int64)
+    db = rng.integers(-(2 ** 20), 2 ** 20, size=C, dtype=np.int64)
+    gm = synth.int_codes(C + 1, (C,), -(2 ** 23) + 1, 2 ** 23 - 1, np.int32)
+    bm = synth.int_codes(C + 2, (C,), -(2 ** 23) + 1, 2 ** 23 - 1, np.int32)
+    gm_t, bm_t = T(gm, dev), T(bm, dev)
+    gq = torch.empty(C, dtype=torch.int8, device=dev)
+    bq = torch.empty(C, dtype=torch.int8, device=dev)
+    Gg = torch.empty(C, dtype=torch.int8, device=dev)
+    Gb = torch.empty(C, dtype=torch.int8, device=dev)
+    Gge, Gbe = E(0, dev), E(0, dev)
+    iseg.iseg_bn_param_update(T(dg, dev), E(d_exp, dev), T(db, dev), E(d_exp - 3, dev), 8, 99, 17,
+                              18, 4, 10, -22, 24, 8, gm_t, bm_t, gq, bq, Gg, Gb, Gge, Gbe)
+    for d, e, tid, m, m_t, q_t, G_t, Ge_t in ((dg, d_exp, 17, gm, gm_t, gq, Gg, Gge),
+                                              (db, d_exp - 3, 18, bm, bm_t, bq, Gb, Gbe)):
+        rc, re = orc.requant(d, e, 8, stochastic=True, keep_scale=True, seed=99, tensor_id=tid,
+                             step=4)
+        assert np.array_equal(H(G_t).astype(np.int64), rc) and ev(Ge_t) == re
+        rm, rw = orc.weight_update(m, rc, re, 10, -22, 24, 8)
+        assert np.array_equal(H(m_t), rm) and np.array_equal(H(q_t), rw)
