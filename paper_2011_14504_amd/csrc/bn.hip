@@ -27,8 +27,18 @@
 namespace {
 
 constexpr int kSentinelLo = -(1 << 30);
-constexpr int kUnroll = 4;          // rows in flight per lane
-constexpr int kMaxBlocks = 1024;    // streaming blocks per call (all slices)
+
+// launch geometry of the streaming passes (compile-time tuning knobs)
+#ifndef ISEG_BN_NT
+#define ISEG_BN_NT 1024          // threads per streaming block
+#endif
+#ifndef ISEG_BN_BLOCKS
+#define ISEG_BN_BLOCKS 256       // streaming blocks per call, all channel slices
+#endif
+#ifndef ISEG_BNF_STATS_CPL
+#define ISEG_BNF_STATS_CPL 4     // channels per lane of the forward statistics
+#endif
+constexpr int kMaxBlocks = ISEG_BN_BLOCKS;
 
 // ---------------------------------------------------------------------------
 // saved-state layout (documented in iseg.h)
@@ -86,14 +96,16 @@ int pick_cs(int64_t C, int csmax)
     return 0;
 }
 
-Stream make_stream(int64_t M, int64_t C, int cs)
+constexpr int kNT = ISEG_BN_NT;
+
+Stream make_stream(int64_t M, int64_t C, int cs, int cpl, int unroll, int max_blocks)
 {
     Stream s;
-    s.M = M; s.C = (int32_t)C; s.CS = cs; s.G = cs / 4; s.rpi = 256 / s.G;
+    s.M = M; s.C = (int32_t)C; s.CS = cs; s.G = cs / cpl; s.rpi = kNT / s.G;
     int nsl = (int)(C / cs);
-    int64_t want = kMaxBlocks / nsl;
+    int64_t want = max_blocks / nsl;
     if (want < 1) want = 1;
-    int64_t rows = ceil_div64(M, (int64_t)s.rpi * kUnroll);
+    int64_t rows = ceil_div64(M, (int64_t)s.rpi * unroll);
     s.gx = (int32_t)(rows < want ? rows : want);
     if (s.gx < 1) s.gx = 1;
     return s;
@@ -108,21 +120,46 @@ __device__ __forceinline__ bool stream_lane(const Stream& st, int& g, int& rsub)
     return rsub < st.rpi;
 }
 
-// Iterate the rows of this lane, kUnroll loads in flight: f(row, dword).
-template <typename F>
+// Iterate the rows of this lane with U rows in flight; a lane covers CPL
+// channels (4: one dword, 16: one 16-byte vector).  f(row, words[CPL/4]).
+template <int CPL>
+struct Vec { uint32_t w[CPL / 4]; };
+
+template <int CPL>
+__device__ __forceinline__ Vec<CPL> vload(const int8_t* p)
+{
+    Vec<CPL> v;
+    if (CPL == 16) {
+        uint4 t = *(const uint4*)p;
+        v.w[0] = t.x; v.w[CPL / 4 > 1 ? 1 : 0] = t.y;
+        if (CPL == 16) { v.w[2 % (CPL / 4)] = t.z; v.w[3 % (CPL / 4)] = t.w; }
+    } else {
+        v.w[0] = *(const uint32_t*)p;
+    }
+    return v;
+}
+
+template <int CPL>
+__device__ __forceinline__ void vstore(int8_t* p, const Vec<CPL>& v)
+{
+    if (CPL == 16) *(uint4*)p = make_uint4(v.w[0], v.w[1 % (CPL / 4)], v.w[2 % (CPL / 4)], v.w[3 % (CPL / 4)]);
+    else *(uint32_t*)p = v.w[0];
+}
+
+template <int CPL, int U, typename F>
 __device__ __forceinline__ void stream_rows(const Stream& st, const int8_t* __restrict__ a, int c0,
                                             int rsub, F f)
 {
     const int64_t step = (int64_t)gridDim.x * st.rpi;
-    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += step * kUnroll) {
-        uint32_t v[kUnroll];
+    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += step * U) {
+        Vec<CPL> v[U];
 #pragma unroll
-        for (int u = 0; u < kUnroll; u++) {
+        for (int u = 0; u < U; u++) {
             int64_t rr = r + u * step;
-            v[u] = rr < st.M ? *(const uint32_t*)(a + rr * st.C + c0) : 0u;
+            if (rr < st.M) v[u] = vload<CPL>(a + rr * st.C + c0);
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; u++) {
+        for (int u = 0; u < U; u++) {
             int64_t rr = r + u * step;
             if (rr < st.M) f(rr, v[u]);
         }
@@ -130,21 +167,23 @@ __device__ __forceinline__ void stream_rows(const Stream& st, const int8_t* __re
 }
 
 // two-input variant
-template <typename F>
+template <int CPL, int U, typename F>
 __device__ __forceinline__ void stream_rows2(const Stream& st, const int8_t* __restrict__ a,
                                              const int8_t* __restrict__ b, int c0, int rsub, F f)
 {
     const int64_t step = (int64_t)gridDim.x * st.rpi;
-    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += step * kUnroll) {
-        uint32_t va[kUnroll], vb[kUnroll];
+    for (int64_t r = (int64_t)blockIdx.x * st.rpi + rsub; r < st.M; r += step * U) {
+        Vec<CPL> va[U], vb[U];
 #pragma unroll
-        for (int u = 0; u < kUnroll; u++) {
+        for (int u = 0; u < U; u++) {
             int64_t rr = r + u * step;
-            va[u] = rr < st.M ? *(const uint32_t*)(a + rr * st.C + c0) : 0u;
-            vb[u] = rr < st.M ? *(const uint32_t*)(b + rr * st.C + c0) : 0u;
+            if (rr < st.M) {
+                va[u] = vload<CPL>(a + rr * st.C + c0);
+                vb[u] = vload<CPL>(b + rr * st.C + c0);
+            }
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; u++) {
+        for (int u = 0; u < U; u++) {
             int64_t rr = r + u * step;
             if (rr < st.M) f(rr, va[u], vb[u]);
         }
@@ -194,6 +233,22 @@ struct OpAdd { template <typename T> __device__ T operator()(T a, T b) const { r
 struct OpMin { template <typename T> __device__ T operator()(T a, T b) const { return a < b ? a : b; } };
 struct OpMax { template <typename T> __device__ T operator()(T a, T b) const { return a > b ? a : b; } };
 
+// Lanes of a wave that hold the same channels are G apart.  When G is a power
+// of two dividing 64, fold them with xor-shuffles so that only lanes < G of
+// each wave carry the wave's total into LDS (fewer same-address LDS atomics).
+template <typename T, typename Op>
+__device__ __forceinline__ T group_fold(T v, int G, Op op)
+{
+    if ((G & (G - 1)) != 0 || G > 64) return v;
+    for (int o = G; o < 64; o <<= 1) v = op(v, (T)__shfl_xor(v, o, 64));
+    return v;
+}
+
+__device__ __forceinline__ bool group_leader(int G)
+{
+    return ((G & (G - 1)) != 0 || G > 64) || (int)(threadIdx.x & 63) < G;
+}
+
 // ---------------------------------------------------------------------------
 // forward workspace
 // ---------------------------------------------------------------------------
@@ -230,29 +285,41 @@ FwdWs fwd_ws_map(void* base, const Stream& st)
 // ---------------------------------------------------------------------------
 // forward kernels
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_bnf_stats1(const int8_t* __restrict__ x, Stream st, FwdWs w)
+template <int CPL>
+__global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ x, Stream st, FwdWs w)
 {
     __shared__ int32_t sS[128], sMin[128], sMax[128];
     if ((int)threadIdx.x < st.CS) { sS[threadIdx.x] = 0; sMin[threadIdx.x] = 1000; sMax[threadIdx.x] = -1000; }
     __syncthreads();
     int g, rsub;
-    if (stream_lane(st, g, rsub)) {
-        int s[4] = {0, 0, 0, 0}, mn[4] = {1000, 1000, 1000, 1000}, mx[4] = {-1000, -1000, -1000, -1000};
-        int c0 = blockIdx.y * st.CS + g * 4;
-        stream_rows(st, x, c0, rsub, [&](int64_t, uint32_t v) {
+    const bool active = stream_lane(st, g, rsub);
+    int s[CPL], mn[CPL], mx[CPL];
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                int q = sbyte(v, i);
+    for (int i = 0; i < CPL; i++) { s[i] = 0; mn[i] = 1000; mx[i] = -1000; }
+    if (active) {
+        int c0 = blockIdx.y * st.CS + g * CPL;
+        stream_rows<CPL, 4>(st, x, c0, rsub, [&](int64_t, const Vec<CPL>& v) {
+#pragma unroll
+            for (int i = 0; i < CPL; i++) {
+                int q = sbyte(v.w[i >> 2], i & 3);
                 s[i] += q;
                 mn[i] = q < mn[i] ? q : mn[i];
                 mx[i] = q > mx[i] ? q : mx[i];
             }
         });
+    }
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            atomicAdd(&sS[g * 4 + i], s[i]);
-            atomicMin(&sMin[g * 4 + i], mn[i]);
-            atomicMax(&sMax[g * 4 + i], mx[i]);
+    for (int i = 0; i < CPL; i++) {
+        s[i] = group_fold(s[i], st.G, OpAdd());
+        mn[i] = group_fold(mn[i], st.G, OpMin());
+        mx[i] = group_fold(mx[i], st.G, OpMax());
+    }
+    if (active && group_leader(st.G)) {
+#pragma unroll
+        for (int i = 0; i < CPL; i++) {
+            atomicAdd(&sS[g * CPL + i], s[i]);
+            atomicMin(&sMin[g * CPL + i], mn[i]);
+            atomicMax(&sMax[g * CPL + i], mx[i]);
         }
     }
     __syncthreads();
@@ -295,7 +362,8 @@ __global__ __launch_bounds__(256) void k_bnf_finmu(const int32_t* x_exp, Stream 
     }
 }
 
-__global__ __launch_bounds__(256) void k_bnf_stats2(const int8_t* __restrict__ x, const int32_t* x_exp,
+template <int CPL>
+__global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ x, const int32_t* x_exp,
                                                     Stream st, FwdWs w, Saved sv, BnCfg cf,
                                                     int32_t* dev_status)
 {
@@ -309,23 +377,30 @@ __global__ __launch_bounds__(256) void k_bnf_stats2(const int8_t* __restrict__ x
     __syncthreads();
     const int e_mu = 2 - cf.k_mu;
     int g, rsub;
-    if (stream_lane(st, g, rsub)) {
-        int c0 = blockIdx.y * st.CS + g * 4;
-        int64_t a[4] = {0, 0, 0, 0};
+    const bool active = stream_lane(st, g, rsub);
+    int64_t a[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; i++) a[i] = 0;
+    if (active) {
+        int c0 = blockIdx.y * st.CS + g * CPL;
         const int gg = s_x < e_mu ? s_x : e_mu;
         const int64_t mulq = (int64_t)1 << (s_x - gg);
-        int64_t off[4];
+        int64_t off[CPL];
 #pragma unroll
-        for (int i = 0; i < 4; i++) off[i] = (int64_t)sv.n_mu[c0 + i] * ((int64_t)1 << (e_mu - gg));
-        stream_rows(st, x, c0, rsub, [&](int64_t, uint32_t v) {
+        for (int i = 0; i < CPL; i++) off[i] = (int64_t)sv.n_mu[c0 + i] * ((int64_t)1 << (e_mu - gg));
+        stream_rows<CPL, 4>(st, x, c0, rsub, [&](int64_t, const Vec<CPL>& v) {
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                int64_t D = (int64_t)sbyte(v, i) * mulq - off[i];
+            for (int i = 0; i < CPL; i++) {
+                int64_t D = (int64_t)sbyte(v.w[i >> 2], i & 3) * mulq - off[i];
                 a[i] += D < 0 ? -D : D;
             }
         });
+    }
 #pragma unroll
-        for (int i = 0; i < 4; i++) atomicAdd(&sA[g * 4 + i], (unsigned long long)a[i]);
+    for (int i = 0; i < CPL; i++) a[i] = group_fold(a[i], st.G, OpAdd());
+    if (active && group_leader(st.G)) {
+#pragma unroll
+        for (int i = 0; i < CPL; i++) atomicAdd(&sA[g * CPL + i], (unsigned long long)a[i]);
     }
     __syncthreads();
     if ((int)threadIdx.x < st.CS)
@@ -424,7 +499,8 @@ __global__ __launch_bounds__(256) void k_bnf_fin3(const int32_t* x_exp, FwdWs w,
     }
 }
 
-__global__ __launch_bounds__(256) void k_bnf_apply(const int8_t* __restrict__ x, int8_t* __restrict__ y,
+template <int CPL>
+__global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x, int8_t* __restrict__ y,
                                                    Stream st, Saved sv)
 {
     __shared__ int8_t lut[128 * 256];
@@ -433,13 +509,19 @@ __global__ __launch_bounds__(256) void k_bnf_apply(const int8_t* __restrict__ x,
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
-    const int c0 = blockIdx.y * st.CS + g * 4;
-    const int8_t* l = lut + g * 4 * 256 + 128;
-    stream_rows(st, x, c0, rsub, [&](int64_t r, uint32_t v) {
-        uint32_t o = 0;
+    const int c0 = blockIdx.y * st.CS + g * CPL;
+    const int8_t* l = lut + g * CPL * 256 + 128;
+    stream_rows<CPL, 4>(st, x, c0, rsub, [&](int64_t r, const Vec<CPL>& v) {
+        Vec<CPL> o;
 #pragma unroll
-        for (int i = 0; i < 4; i++) o |= (uint32_t)(uint8_t)l[i * 256 + sbyte(v, i)] << (8 * i);
-        *(uint32_t*)(y + r * st.C + c0) = o;
+        for (int j = 0; j < CPL / 4; j++) {
+            uint32_t ow = 0;
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                ow |= (uint32_t)(uint8_t)l[(j * 4 + i) * 256 + sbyte(v.w[j], i)] << (8 * i);
+            o.w[j] = ow;
+        }
+        vstore<CPL>(y + r * st.C + c0, o);
     });
 }
 
@@ -497,7 +579,7 @@ __device__ __forceinline__ int thr_cls(const Thr& t, int q) { return 1 + (q >= t
 __device__ __forceinline__ bool thr_mask(const Thr& t, int q) { return q >= t.mlo && q <= t.mhi; }
 
 // pass 1: sum delta, sum delta*n_xhat, sum sgn, per-class min/max of delta
-__global__ __launch_bounds__(256) void k_bnb_stats(const int8_t* __restrict__ dy,
+__global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                    Saved sv, int32_t relu)
 {
@@ -519,19 +601,21 @@ __global__ __launch_bounds__(256) void k_bnb_stats(const int8_t* __restrict__ dy
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) { *w.maxF = 0; *w.bdx = kSentinelLo; }
     __syncthreads();
     int g, rsub;
-    if (stream_lane(st, g, rsub)) {
+    const bool active = stream_lane(st, g, rsub);
+    int32_t sd[4] = {0, 0, 0, 0}, z[4] = {0, 0, 0, 0};
+    int64_t sdn[4] = {0, 0, 0, 0};
+    int32_t mm[4][6];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int k = 0; k < 3; k++) { mm[i][2 * k] = 1000; mm[i][2 * k + 1] = -1000; }
+    if (active) {
         const int c0 = (int)cbase + g * 4;
-        int32_t sd[4] = {0, 0, 0, 0}, z[4] = {0, 0, 0, 0};
-        int64_t sdn[4] = {0, 0, 0, 0};
-        int32_t mm[4][6];
         Thr t[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            t[i] = thr[g * 4 + i];
-#pragma unroll
-            for (int k = 0; k < 3; k++) { mm[i][2 * k] = 1000; mm[i][2 * k + 1] = -1000; }
-        }
-        stream_rows2(st, x, dy, c0, rsub, [&](int64_t, uint32_t vx, uint32_t vd) {
+        for (int i = 0; i < 4; i++) t[i] = thr[g * 4 + i];
+        stream_rows2<4, 8>(st, x, dy, c0, rsub, [&](int64_t, const Vec<4>& vxx, const Vec<4>& vdd) {
+            const uint32_t vx = vxx.w[0], vd = vdd.w[0];
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 int q = sbyte(vx, i);
@@ -548,6 +632,19 @@ __global__ __launch_bounds__(256) void k_bnb_stats(const int8_t* __restrict__ dy
                 }
             }
         });
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        sd[i] = group_fold(sd[i], st.G, OpAdd());
+        sdn[i] = group_fold(sdn[i], st.G, OpAdd());
+        z[i] = group_fold(z[i], st.G, OpAdd());
+#pragma unroll
+        for (int k = 0; k < 3; k++) {
+            mm[i][2 * k] = group_fold(mm[i][2 * k], st.G, OpMin());
+            mm[i][2 * k + 1] = group_fold(mm[i][2 * k + 1], st.G, OpMax());
+        }
+    }
+    if (active && group_leader(st.G)) {
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             int cl = g * 4 + i;
@@ -631,7 +728,7 @@ __device__ __forceinline__ int bnb_r2(const BwdWs& w, const BnCfg& cf)
 }
 
 // pass 2 (only when E2's quantizer rounds): sum f and f*n_xhat
-__global__ __launch_bounds__(256) void k_bnb_stats2(const int8_t* __restrict__ dy,
+__global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ dy,
                                                     const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                     Saved sv, BnCfg cf, const int8_t* gamma_q)
 {
@@ -651,14 +748,16 @@ __global__ __launch_bounds__(256) void k_bnb_stats2(const int8_t* __restrict__ d
     __syncthreads();
     const int r2 = bnb_r2(w, cf);
     int g, rsub;
-    if (stream_lane(st, g, rsub)) {
+    const bool active = stream_lane(st, g, rsub);
+    int64_t sf[4] = {0, 0, 0, 0}, sfn[4] = {0, 0, 0, 0};
+    if (active) {
         const int c0 = (int)cbase + g * 4;
         int gq[4];
         Thr t[4];
 #pragma unroll
         for (int i = 0; i < 4; i++) { gq[i] = gamma_q[c0 + i]; t[i] = thr[g * 4 + i]; }
-        int64_t sf[4] = {0, 0, 0, 0}, sfn[4] = {0, 0, 0, 0};
-        stream_rows2(st, x, dy, c0, rsub, [&](int64_t, uint32_t vx, uint32_t vd) {
+        stream_rows2<4, 8>(st, x, dy, c0, rsub, [&](int64_t, const Vec<4>& vxx, const Vec<4>& vdd) {
+            const uint32_t vx = vxx.w[0], vd = vdd.w[0];
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 int q = sbyte(vx, i);
@@ -668,6 +767,13 @@ __global__ __launch_bounds__(256) void k_bnb_stats2(const int8_t* __restrict__ d
                 sfn[i] += f * xc[(g * 4 + i) * 256 + q + 128];
             }
         });
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        sf[i] = group_fold(sf[i], st.G, OpAdd());
+        sfn[i] = group_fold(sfn[i], st.G, OpAdd());
+    }
+    if (active && group_leader(st.G)) {
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             atomicAdd(&sF[g * 4 + i], (unsigned long long)sf[i]);
@@ -780,7 +886,8 @@ __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t 
     }
 }
 
-__global__ __launch_bounds__(256) void k_bnb_apply(const int8_t* __restrict__ dy,
+template <int CPL>
+__global__ __launch_bounds__(1024) void k_bnb_apply(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x,
                                                    int8_t* __restrict__ dx, Stream st, BwdWs w,
                                                    Saved sv, int32_t relu)
@@ -799,20 +906,24 @@ __global__ __launch_bounds__(256) void k_bnb_apply(const int8_t* __restrict__ dy
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
-    const int c0 = (int)cbase + g * 4;
-    Thr t[4];
+    const int c0 = (int)cbase + g * CPL;
+    stream_rows2<CPL, 4>(st, x, dy, c0, rsub, [&](int64_t r, const Vec<CPL>& vx, const Vec<CPL>& vd) {
+        Vec<CPL> o;
 #pragma unroll
-    for (int i = 0; i < 4; i++) t[i] = thr[g * 4 + i];
-    stream_rows2(st, x, dy, c0, rsub, [&](int64_t r, uint32_t vx, uint32_t vd) {
-        uint32_t o = 0;
+        for (int j = 0; j < CPL / 4; j++) {
+            uint32_t ow = 0;
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            int q = sbyte(vx, i);
-            int d = thr_mask(t[i], q) ? sbyte(vd, i) : 0;
-            int cls = thr_cls(t[i], q);
-            o |= (uint32_t)(uint8_t)lut[((g * 4 + i) * 3 + cls) * 256 + d + 128] << (8 * i);
+            for (int i = 0; i < 4; i++) {
+                const int cl = g * CPL + j * 4 + i;
+                const Thr t = thr[cl];
+                int q = sbyte(vx.w[j], i);
+                int d = thr_mask(t, q) ? sbyte(vd.w[j], i) : 0;
+                int cls = thr_cls(t, q);
+                ow |= (uint32_t)(uint8_t)lut[(cl * 3 + cls) * 256 + d + 128] << (8 * i);
+            }
+            o.w[j] = ow;
         }
-        *(uint32_t*)(dx + r * st.C + c0) = o;
+        vstore<CPL>(dx + r * st.C + c0, o);
     });
 }
 
@@ -823,6 +934,13 @@ bool cfg_ok(const iseg_bn_cfg* c)
     return in(c->k_mu, 2, 16) && in(c->k_sigma, 2, 16) && in(c->k_xhat, 2, 16) &&
            in(c->k_gamma, 2, 8) && in(c->k_beta, 2, 8) && in(c->k_A, 2, 8) && in(c->k_E1, 2, 8) &&
            in(c->k_E2, 2, 16) && in(c->eps_code, 0, 1 << 15) && (c->relu == 0 || c->relu == 1);
+}
+
+// forward statistics geometry; the 4-channel-lane variant has the most
+// blocks, so it sizes the workspace for both
+Stream fwd_stats_stream(int64_t M, int64_t C, int cs, bool v16)
+{
+    return make_stream(M, C, cs, v16 && ISEG_BNF_STATS_CPL == 16 ? 16 : 4, 4, kMaxBlocks);
 }
 
 bool shape_ok(int64_t M, int64_t C) { return M >= 1 && C >= 4 && M <= ((int64_t)1 << 22) && C <= (1 << 16); }
@@ -838,14 +956,14 @@ extern "C" size_t iseg_bn_fwd_ws(int64_t M, int64_t C)
 {
     int cs = pick_cs(C, 128);
     if (!shape_ok(M, C) || !cs) return 0;
-    return fwd_ws_bytes(make_stream(M, C, cs));
+    return fwd_ws_bytes(fwd_stats_stream(M, C, cs, false));
 }
 
 extern "C" size_t iseg_bn_bwd_ws(int64_t M, int64_t C)
 {
     int cs = pick_cs(C, 64);
     if (!shape_ok(M, C) || !cs) return 0;
-    return bwd_ws_bytes(make_stream(M, C, cs));
+    return bwd_ws_bytes(make_stream(M, C, cs, 4, 8, kMaxBlocks));
 }
 
 extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
@@ -859,20 +977,38 @@ extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int
         return ISEG_ERR_ARG;
     int cs = pick_cs(C, 128);
     if (!cs || (((uintptr_t)x | (uintptr_t)y_out) & 3)) return ISEG_ERR_UNSUPPORTED;
-    Stream st = make_stream(M, C, cs);
-    if (!ws || ws_bytes < fwd_ws_bytes(st)) return ISEG_ERR_WORKSPACE;
+    const bool v16 = cs % 16 == 0 && (((uintptr_t)x | (uintptr_t)y_out) & 15) == 0;
+    const bool s16 = v16 && ISEG_BNF_STATS_CPL == 16;
+    Stream st = fwd_stats_stream(M, C, cs, v16);
+    if (!ws || ws_bytes < fwd_ws_bytes(fwd_stats_stream(M, C, cs, false))) return ISEG_ERR_WORKSPACE;
     BnCfg cf = to_cfg(cfg);
     Saved sv = saved_map(saved, C);
     FwdWs w = fwd_ws_map(ws, st);
     dim3 sg = stream_grid(st);
     dim3 cb((unsigned)C);
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1, sg, dim3(256), 0, stream, x, st, w);
+    if (s16)
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<16>, sg, dim3(kNT), 0, stream, x, st, w);
+    else
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<4>, sg, dim3(kNT), 0, stream, x, st, w);
     hipLaunchKernelGGL(k_bnf_finmu, cb, dim3(256), 0, stream, x_exp, st, w, sv, cf);
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2, sg, dim3(256), 0, stream, x, x_exp, st, w, sv, cf, dev_status);
+    if (s16)
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2<16>, sg, dim3(kNT), 0, stream, x, x_exp,
+                          st, w, sv, cf, dev_status);
+    else
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2<4>, sg, dim3(kNT), 0, stream, x, x_exp,
+                          st, w, sv, cf, dev_status);
     hipLaunchKernelGGL(k_bnf_finsig, cb, dim3(256), 0, stream, x_exp, st, w, sv, cf);
     hipLaunchKernelGGL(k_bnf_fin2, cb, dim3(256), 0, stream, x_exp, w, sv, cf, gamma_q, beta_q);
     hipLaunchKernelGGL(k_bnf_fin3, cb, dim3(256), 0, stream, x_exp, w, sv, cf, y_exp);
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply, sg, dim3(256), 0, stream, x, y_out, st, sv);
+    if (v16) {
+        Stream a16 = make_stream(M, C, cs, 16, 4, kMaxBlocks);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply<16>, stream_grid(a16), dim3(kNT), 0,
+                          stream, x, y_out, a16, sv);
+    } else {
+        Stream s4 = make_stream(M, C, cs, 4, 4, kMaxBlocks);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply<4>, stream_grid(s4), dim3(kNT), 0, stream,
+                          x, y_out, s4, sv);
+    }
     return launch_ok();
 }
 
@@ -889,7 +1025,7 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
         return ISEG_ERR_ARG;
     int cs = pick_cs(C, 64);
     if (!cs || (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx_out) & 3)) return ISEG_ERR_UNSUPPORTED;
-    Stream st = make_stream(M, C, cs);
+    Stream st = make_stream(M, C, cs, 4, 8, kMaxBlocks);
     if (!ws || ws_bytes < bwd_ws_bytes(st)) return ISEG_ERR_WORKSPACE;
     BnCfg cf = to_cfg(cfg);
     Saved sv = saved_map((void*)saved, C);
@@ -898,15 +1034,22 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     dim3 cb((unsigned)C);
     // E2 = SQ(gamma delta, k_E2) is exact when |gamma delta| <= 127^2 < 2^(k_E2-1)
     const int exact_e2 = cf.k_E2 >= 15;
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats, sg, dim3(256), 0, stream, dy, x, st, w, sv, cf.relu);
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats, sg, dim3(kNT), 0, stream, dy, x, st, w, sv,
+                      cf.relu);
     hipLaunchKernelGGL(k_bnb_fin1, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma,
                        dbeta, dgamma_exp, dbeta_exp, dev_status);
     if (!exact_e2)
-        hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(256), 0, stream, dy, x, st, w, sv, cf, gamma_q);
+        hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(kNT), 0, stream, dy, x, st, w, sv, cf, gamma_q);
     hipLaunchKernelGGL(k_bnb_fin2, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, exact_e2);
     hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2,
                        dx_exp);
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, sg, dim3(256), 0, stream, dy, x, dx_out,
-                      st, w, sv, cf.relu);
+    if (cs % 16 == 0 && (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx_out) & 15) == 0) {
+        Stream s16 = make_stream(M, C, cs, 16, 4, kMaxBlocks);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply<16>, stream_grid(s16), dim3(kNT), 0,
+                          stream, dy, x, dx_out, s16, w, sv, cf.relu);
+    } else {
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply<4>, sg, dim3(kNT), 0, stream, dy, x,
+                          dx_out, st, w, sv, cf.relu);
+    }
     return launch_ok();
 }

@@ -116,6 +116,9 @@ __device__ __forceinline__ int4 load_b_piece(const IgemmArgs& a, int n, int kk0)
     return make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
 }
 
+template <int MODE>
+int launch_igemm_generic(const IgemmArgs& a, hipStream_t s);
+
 template <int MODE, bool VEC, int BM, int BN>
 __global__ __launch_bounds__(256) void k_conv_igemm(IgemmArgs a)
 {
@@ -205,8 +208,139 @@ __global__ __launch_bounds__(256) void k_conv_igemm(IgemmArgs a)
     if (a.maxp) block_atomic_max_u64(mx, a.maxp);
 }
 
+// Implicit GEMM for Ci % 64 == 0: the k-loop runs tap-major in 64-channel
+// chunks, so each step is one tap and one contiguous channel chunk.  Source
+// offsets of a thread's rows are recomputed only when the tap changes; LDS
+// is double-buffered (one barrier per step) and the next step's global
+// loads are in flight while the current step's MFMAs run.
+template <int MODE, int BM, int BN>
+__global__ __launch_bounds__(256) void k_conv_igemm_tap(IgemmArgs a)
+{
+    constexpr int PA = BM * 4 / 256;
+    constexpr int PB = BN * 4 / 256;
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    __shared__ __attribute__((aligned(16))) int8_t As[2][BM * ROW];
+    __shared__ __attribute__((aligned(16))) int8_t Bs[2][BN * ROW];
+
+    const int tid = threadIdx.x;
+    const int part = tid & 3;
+    const int64_t m0 = (int64_t)blockIdx.x * BM;
+    const int n0 = blockIdx.y * BN;
+    const int nchunk = a.Ci / BK;
+    const int nk = a.R * a.S * nchunk;
+
+    RowPix rp[PA];
+#pragma unroll
+    for (int j = 0; j < PA; j++) rp[j] = row_pix(a, m0 + ((tid >> 2) + 64 * j));
+    const int8_t* brow[PB];
+#pragma unroll
+    for (int j = 0; j < PB; j++) {
+        int n = n0 + (tid >> 2) + 64 * j;
+        brow[j] = n < a.Nout ? a.wmat + (int64_t)n * a.Kred + part * 16 : nullptr;
+    }
+
+    int64_t soff[PA];
+    auto set_tap = [&](int tap) {
+        int r = tap / a.S, s = tap - (tap / a.S) * a.S;
+#pragma unroll
+        for (int j = 0; j < PA; j++) {
+            int64_t sp = src_pixel<MODE>(a, rp[j], r, s);
+            soff[j] = sp < 0 ? -1 : sp * a.Ci + part * 16;
+        }
+    };
+    int4 ra[PA], rb[PB];
+    auto load = [&](int kb, int cc) {
+#pragma unroll
+        for (int j = 0; j < PA; j++)
+            ra[j] = soff[j] >= 0 ? *(const int4*)(a.src + soff[j] + cc * BK) : make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < PB; j++)
+            rb[j] = brow[j] ? *(const int4*)(brow[j] + (int64_t)kb * BK) : make_int4(0, 0, 0, 0);
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < PA; j++) *(int4*)&As[buf][((tid >> 2) + 64 * j) * ROW + part * 16] = ra[j];
+#pragma unroll
+        for (int j = 0; j < PB; j++) *(int4*)&Bs[buf][((tid >> 2) + 64 * j) * ROW + part * 16] = rb[j];
+    };
+
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = lane & 15, lk = (lane >> 4) * 16;
+    v4i acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) acc[i][j] = (v4i){0, 0, 0, 0};
+
+    int tap = 0, cc = 0;
+    set_tap(0);
+    load(0, 0);
+    store(0);
+    __syncthreads();
+    for (int kb = 0; kb < nk; kb++) {
+        const bool more = kb + 1 < nk;
+        if (more) {
+            if (++cc == nchunk) { cc = 0; set_tap(++tap); }
+            load(kb + 1, cc);
+        }
+        const int8_t* A = As[kb & 1];
+        const int8_t* B = Bs[kb & 1];
+        v4i fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&A[(wm * WM + i * 16 + lrow) * ROW + lk];
+#pragma unroll
+        for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&B[(wn * WN + j * 16 + lrow) * ROW + lk];
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        if (more) store((kb + 1) & 1);
+        __syncthreads();
+    }
+
+    uint64_t mx = 0;
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) {
+            int n = n0 + wn * WN + j * 16 + lrow;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                int64_t m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + e;
+                if (m < a.Mrows && n < a.Nout) {
+                    int32_t v = acc[i][j][e];
+                    a.out[m * a.Nout + n] = v;
+                    uint64_t av = v < 0 ? (uint64_t)(-(int64_t)v) : (uint64_t)v;
+                    mx = av > mx ? av : mx;
+                }
+            }
+        }
+    if (a.maxp) block_atomic_max_u64(mx, a.maxp);
+}
+
 template <int MODE>
 int launch_igemm(const IgemmArgs& a, hipStream_t s)
+{
+    if (a.Mrows > 0 && a.Nout > 0 && a.Ci % 64 == 0 &&
+        (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0) {
+        const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
+        unsigned gx = (unsigned)ceil_div64(a.Mrows, 128);
+        if (a.Nout > 64) {
+            dim3 grid(gx, (unsigned)ceil_div64(a.Nout, 128));
+            ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_tap<MODE, 128, 128>), grid, dim3(256), 0, s, a);
+        } else {
+            ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_tap<MODE, 128, 64>), dim3(gx, 1), dim3(256), 0, s, a);
+        }
+        return launch_ok();
+    }
+    return launch_igemm_generic<MODE>(a, s);
+}
+
+template <int MODE>
+int launch_igemm_generic(const IgemmArgs& a, hipStream_t s)
 {
     if (a.Mrows <= 0 || a.Nout <= 0) return ISEG_OK;
     bool vec = (a.Ci % 16) == 0 && (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0;
@@ -243,6 +377,41 @@ __global__ void k_w_transpose(const int8_t* __restrict__ w, int8_t* __restrict__
     }
 }
 
+// channel padding for small C: out[pix][c] = c < C ? in[pix][c] : 0
+__global__ void k_pad_channels(const int8_t* __restrict__ in, int8_t* __restrict__ out, int64_t npix,
+                               int32_t C, int32_t Cp)
+{
+    int64_t n = npix * Cp;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t pix = i / Cp;
+        int32_t c = (int32_t)(i - pix * Cp);
+        out[i] = c < C ? in[pix * C + c] : (int8_t)0;
+    }
+}
+
+// drop the padded channels of int64 weight-gradient sums
+__global__ void k_unpad_i64(const long long* __restrict__ in, long long* __restrict__ out, int64_t rows,
+                            int32_t C, int32_t Cp)
+{
+    int64_t n = rows * C;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t r = i / C;
+        out[i] = in[r * Cp + (i - r * C)];
+    }
+}
+
+static int64_t padded_c(int64_t C) { return (C % 16 == 0 || C > 64) ? C : ((C + 15) / 16) * 16; }
+
+static int launch_pad(const int8_t* in, int8_t* out, int64_t npix, int64_t C, int64_t Cp, hipStream_t s)
+{
+    if (npix <= 0) return ISEG_OK;
+    hipLaunchKernelGGL(k_pad_channels, dim3(grid_for(npix * Cp, 256, 8192)), dim3(256), 0, s, in, out,
+                       npix, (int32_t)C, (int32_t)Cp);
+    return launch_ok();
+}
+
 __global__ void k_exp_sum(int32_t* out, const int32_t* a, const int32_t* b)
 {
     *out = (a ? *a : 0) + (b ? *b : 0);
@@ -270,6 +439,8 @@ __device__ __forceinline__ void transpose4x4(const uint32_t in[4], uint32_t out[
         out[c] = byte_of(in[0], c) | (byte_of(in[1], c) << 8) | (byte_of(in[2], c) << 16) |
                  (byte_of(in[3], c) << 24);
 }
+
+int launch_wgrad_generic(WgradArgs a, hipStream_t s);
 
 template <bool VEC, int BM, int BN>
 __global__ __launch_bounds__(256) void k_conv_wgrad(WgradArgs a)
@@ -398,7 +569,554 @@ __global__ __launch_bounds__(256) void k_conv_wgrad(WgradArgs a)
         }
 }
 
+// Backward-weight when C % 64 == 0: a block owns one filter tap (r,s), a
+// 64-channel chunk of C and BM output channels, so every column of its tile
+// shares the tap.  Per 64-pixel step, 64 lanes turn the pixel indices into
+// source offsets once (staged in LDS); the dy and x tiles are then plain
+// dword gathers, transposed 4x4 in registers into pixel-contiguous LDS rows.
+template <int BM>
+__global__ __launch_bounds__(256) void k_conv_wgrad_tap(WgradArgs a)
+{
+    constexpr int BN = 64;
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int QA = BM / 64;
+    __shared__ __attribute__((aligned(16))) int8_t As[BM * ROW];
+    __shared__ __attribute__((aligned(16))) int8_t Bs[BN * ROW];
+    __shared__ int64_t soff[BK];
+
+    const int tid = threadIdx.x;
+    const int nch = a.C / BN;
+    const int tap = blockIdx.x / nch;
+    const int c0 = (blockIdx.x - tap * nch) * BN;
+    const int r = tap / a.S, s = tap - (tap / a.S) * a.S;
+    const int k0 = blockIdx.y * BM;
+    const int64_t pbeg = (int64_t)blockIdx.z * a.pix_per_split;
+    int64_t pend = pbeg + a.pix_per_split;
+    if (pend > a.NPQ) pend = a.NPQ;
+    const int64_t PQ = (int64_t)a.P * a.Q;
+
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = lane & 15, lk = (lane >> 4) * 16;
+    v4i acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) acc[i][j] = (v4i){0, 0, 0, 0};
+
+    for (int64_t pb = pbeg; pb < pend; pb += BK) {
+        if (tid < BK) {
+            int64_t pix = pb + tid;
+            int64_t off = -1;
+            if (pix < pend) {
+                int32_t n = (int32_t)(pix / PQ);
+                int32_t rem = (int32_t)(pix - (int64_t)n * PQ);
+                int32_t p = rem / a.Q, q = rem - (rem / a.Q) * a.Q;
+                int ih = p * a.sh - a.ph + r * a.dh, iw = q * a.sw - a.pw + s * a.dw;
+                if (ih >= 0 && iw >= 0 && ih < a.H && iw < a.W)
+                    off = (((int64_t)n * a.H + ih) * a.W + iw) * a.C + c0;
+            }
+            soff[tid] = off;
+        }
+        __syncthreads();
+        uint32_t ta[QA][4], tb[4];
+#pragma unroll
+        for (int qq = 0; qq < QA; qq++) {
+            int bi = tid + 256 * qq;
+            int cg = bi % (BM / 4), pg = bi / (BM / 4);
+            int kc = k0 + cg * 4;
+            uint32_t in[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                int64_t pix = pb + pg * 4 + i;
+                in[i] = (pix < pend && kc < a.K) ? *(const uint32_t*)(a.dy + pix * a.K + kc) : 0u;
+            }
+            transpose4x4(in, ta[qq]);
+        }
+        {
+            int cg = tid % (BN / 4), pg = tid / (BN / 4);
+            uint32_t in[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                int64_t off = soff[pg * 4 + i];
+                in[i] = off >= 0 ? *(const uint32_t*)(a.x + off + cg * 4) : 0u;
+            }
+            transpose4x4(in, tb);
+        }
+#pragma unroll
+        for (int qq = 0; qq < QA; qq++) {
+            int bi = tid + 256 * qq;
+            int cg = bi % (BM / 4), pg = bi / (BM / 4);
+#pragma unroll
+            for (int c = 0; c < 4; c++) *(uint32_t*)&As[(cg * 4 + c) * ROW + pg * 4] = ta[qq][c];
+        }
+        {
+            int cg = tid % (BN / 4), pg = tid / (BN / 4);
+#pragma unroll
+            for (int c = 0; c < 4; c++) *(uint32_t*)&Bs[(cg * 4 + c) * ROW + pg * 4] = tb[c];
+        }
+        __syncthreads();
+        v4i fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&As[(wm * WM + i * 16 + lrow) * ROW + lk];
+#pragma unroll
+        for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&Bs[(wn * WN + j * 16 + lrow) * ROW + lk];
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+
+    const int colbase = tap * a.C + c0;
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) {
+            int col = colbase + wn * WN + j * 16 + lrow;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                int k = k0 + wm * WM + i * 16 + (lane >> 4) * 4 + e;
+                int32_t v = acc[i][j][e];
+                if (k < a.K && v != 0)
+                    atomicAdd(&a.acc[(int64_t)k * a.RSC + col], (unsigned long long)(int64_t)v);
+            }
+        }
+}
+
+// Backward-weight with transposing LDS reads (C % 64 == 0, K % 16 == 0).
+// Tiles are staged in their natural layout -- [pixel][channel] rows of dy and
+// of the tap-shifted x -- with plain 16-byte copies, and the MFMA operands
+// (16 consecutive pixels of one channel per lane) come out of ds_read_b64_tr_b8:
+// within a 16-lane group, output lane j's byte i is byte (j mod 8) of source
+// lane 2i + j/8, so source lane 2i + h pointing at (pixel i, channels c0 + 8h)
+// hands lane j channel c0 + j of pixels 0..7.  A block owns BM output
+// channels, TAPS filter taps and one 64-channel chunk of C.
+typedef int v2i_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ v4i tr8_frag(const int8_t* lds_rows, int row_bytes, int col0, int lane)
+{
+    // 16-lane group g = lane/16 covers pixels 16g .. 16g+15 of the tile
+    const int g = lane >> 4, sl = lane & 15;
+    const int i = sl >> 1, h = sl & 1;
+    const int8_t* p0 = lds_rows + (16 * g + i) * row_bytes + col0 + 8 * h;
+    const int8_t* p1 = p0 + 8 * row_bytes;
+    v2i_t a = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i_t*)p0);
+    v2i_t b = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i_t*)p1);
+    return (v4i){a.x, a.y, b.x, b.y};
+}
+
+template <int BM, int TAPS>
+__global__ __launch_bounds__(256) void k_conv_wgrad_tr(WgradArgs a)
+{
+    constexpr int BN = 64 * TAPS;
+    constexpr int RA = BM + 16;               // LDS row bytes of the dy tile
+    constexpr int RB = 80;                    // LDS row bytes of an x tile (64 channels)
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int PA = BM / 64;               // 16-byte dy pieces per thread
+    constexpr int D = 4;                      // steps of global loads in flight
+    __shared__ __attribute__((aligned(16))) int8_t As[2][BK * RA];
+    __shared__ __attribute__((aligned(16))) int8_t Bs[2][TAPS][BK * RB];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int nch = a.C / 64;
+    const int tg = blockIdx.x / nch;
+    const int c0 = (blockIdx.x - tg * nch) * 64;
+    const int k0 = blockIdx.y * BM;
+    const int64_t pbeg = (int64_t)blockIdx.z * a.pix_per_split;
+    int64_t pend = pbeg + a.pix_per_split;
+    if (pend > a.NPQ) pend = a.NPQ;
+
+    // this thread stages pixel (step base + tid/4), 16-byte part tid%4
+    const int prow = tid >> 2, part = tid & 3;
+    int tr[TAPS], ts[TAPS];
+    bool tok[TAPS];
+#pragma unroll
+    for (int t = 0; t < TAPS; t++) {
+        int tap = tg * TAPS + t;
+        tok[t] = tap < a.R * a.S;
+        tr[t] = tok[t] ? tap / a.S : 0;
+        ts[t] = tok[t] ? tap - tr[t] * a.S : 0;
+    }
+    // load cursor: coordinates of this thread's pixel, advanced 64 pixels per step
+    int64_t pix = pbeg + prow;
+    const int64_t PQ = (int64_t)a.P * a.Q;
+    int32_t pn = (int32_t)(pix / PQ);
+    int32_t rem = (int32_t)(pix - (int64_t)pn * PQ);
+    int32_t pp = rem / a.Q, pq = rem - (rem / a.Q) * a.Q;
+
+    int4 ra[D][PA], rb[D][TAPS];
+    auto load = [&](int4* pa, int4* pb) {
+        const bool ok = pix < pend;
+#pragma unroll
+        for (int j = 0; j < PA; j++) {
+            int kc = k0 + part * 16 + 64 * j;
+            pa[j] = ok && kc < a.K ? *(const int4*)(a.dy + pix * a.K + kc) : make_int4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int t = 0; t < TAPS; t++) {
+            int ih = pp * a.sh - a.ph + tr[t] * a.dh, iw = pq * a.sw - a.pw + ts[t] * a.dw;
+            bool v = ok && tok[t] && ih >= 0 && iw >= 0 && ih < a.H && iw < a.W;
+            pb[t] = v ? *(const int4*)(a.x + (((int64_t)pn * a.H + ih) * a.W + iw) * a.C + c0 + part * 16)
+                      : make_int4(0, 0, 0, 0);
+        }
+        pix += BK;
+        pq += BK;
+        while (pq >= a.Q) { pq -= a.Q; if (++pp == a.P) { pp = 0; ++pn; } }
+    };
+    auto store = [&](int buf, const int4* pa, const int4* pb) {
+#pragma unroll
+        for (int j = 0; j < PA; j++) *(int4*)&As[buf][prow * RA + part * 16 + 64 * j] = pa[j];
+#pragma unroll
+        for (int t = 0; t < TAPS; t++) *(int4*)&Bs[buf][t][prow * RB + part * 16] = pb[t];
+    };
+
+    v4i acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) acc[i][j] = (v4i){0, 0, 0, 0};
+
+    const int nsteps = (int)((pend - pbeg + BK - 1) / BK);
+#pragma unroll
+    for (int u = 0; u < D; u++)
+        if (u < nsteps) load(ra[u], rb[u]);
+    store(0, ra[0], rb[0]);
+    __syncthreads();
+    for (int st0 = 0; st0 < nsteps; st0 += D) {
+#pragma unroll
+        for (int u = 0; u < D; u++) {
+            const int st = st0 + u;
+            if (st < nsteps) {
+                const int8_t* A = As[st & 1];
+                v4i fa[TM], fb[TN];
+#pragma unroll
+                for (int i = 0; i < TM; i++) fa[i] = tr8_frag(A, RA, wm * WM + i * 16, lane);
+#pragma unroll
+                for (int j = 0; j < TN; j++) {
+                    const int col = wn * WN + j * 16;
+                    fb[j] = tr8_frag(Bs[st & 1][col >> 6], RB, col & 63, lane);
+                }
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+                // stage the next step (its loads were issued D-1 steps ago), then
+                // reuse this slot of the ring for step st + D
+                if (st + 1 < nsteps) store((st + 1) & 1, ra[(u + 1) % D], rb[(u + 1) % D]);
+                if (st + D < nsteps) load(ra[u], rb[u]);
+                __syncthreads();
+            }
+        }
+    }
+
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) {
+            const int colt = wn * WN + j * 16 + (lane & 15);
+            const int t = colt >> 6;
+            const int tap = tg * TAPS + t;
+            if (tap >= a.R * a.S) continue;
+            const int64_t col = (int64_t)tap * a.C + c0 + (colt & 63);
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                int k = k0 + wm * WM + i * 16 + (lane >> 4) * 4 + e;
+                int32_t v = acc[i][j][e];
+                if (k < a.K && v != 0)
+                    atomicAdd(&a.acc[(int64_t)k * a.RSC + col], (unsigned long long)(int64_t)v);
+            }
+        }
+}
+
+// Backward-weight, all taps in one block (C % 64 == 0, K % 64 == 0, R*S <= 16):
+// wave w owns filter tap w, the block owns 64 output channels (k), one
+// 64-channel chunk of C and a run of output pixels.  Per 64-pixel step the dy
+// tile is staged once and shared by every wave; each wave stages its tap's
+// shifted x tile (neighbouring taps overlap, so those loads mostly hit L1).
+// Operands come from ds_read_b64_tr_b8; loads run two steps ahead.  Each
+// block writes its exact int32 partial tile (no atomics); k_wgrad_reduce adds
+// the splits in int64.
+template <int RS>
+__global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_t* __restrict__ part_out)
+{
+    constexpr int RA = 80, RB = 80;           // LDS row bytes (64 bytes + 16 pad)
+    constexpr int D = 2;                      // steps of global loads in flight
+    constexpr int nthr = 64 * RS;
+    constexpr int ndy = (256 + nthr - 1) / nthr;   // 16-byte dy pieces per thread
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+    int8_t* As = smem;                                   // [2][64 * RA]
+    int8_t* Bs = smem + 2 * BK * RA;                     // [2][RS][64 * RB]
+    auto Bbuf = [&](int buf, int t) { return Bs + ((size_t)buf * RS + t) * (BK * RB); };
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;         // wave = tap
+    const int nch = a.C / 64;
+    const int c0 = (blockIdx.x % nch) * 64;
+    const int k0 = (blockIdx.x / nch) * 64;
+    const int64_t pbeg = (int64_t)blockIdx.y * a.pix_per_split;
+    int64_t pend = pbeg + a.pix_per_split;
+    if (pend > a.NPQ) pend = a.NPQ;
+    const int64_t PQ = (int64_t)a.P * a.Q;
+    const int tr = wave / a.S, ts = wave - (wave / a.S) * a.S;
+
+    // x cursors: this lane stages pixels lane/4 + 16 j (j < 4), part lane%4, of its tap
+    const int xpart = lane & 3;
+    int64_t xpix[4];
+    int32_t xn[4], xp[4], xq[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+        xpix[j] = pbeg + (lane >> 2) + 16 * j;
+        int64_t pp = xpix[j] < a.NPQ ? xpix[j] : 0;
+        xn[j] = (int32_t)(pp / PQ);
+        int32_t rem = (int32_t)(pp - (int64_t)xn[j] * PQ);
+        xp[j] = rem / a.Q;
+        xq[j] = rem - xp[j] * a.Q;
+    }
+    int4 rx[D][4], rdy[D][ndy];
+    auto load = [&](int slot, int64_t pstep) {
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            int ih = xp[j] * a.sh - a.ph + tr * a.dh, iw = xq[j] * a.sw - a.pw + ts * a.dw;
+            bool v = xpix[j] < pend && ih >= 0 && iw >= 0 && ih < a.H && iw < a.W;
+            rx[slot][j] = v ? *(const int4*)(a.x + (((int64_t)xn[j] * a.H + ih) * a.W + iw) * a.C + c0 + xpart * 16)
+                            : make_int4(0, 0, 0, 0);
+            xpix[j] += BK;
+            xq[j] += BK;
+            while (xq[j] >= a.Q) { xq[j] -= a.Q; if (++xp[j] == a.P) { xp[j] = 0; ++xn[j]; } }
+        }
+#pragma unroll
+        for (int j = 0; j < ndy; j++) {
+            int pc = tid + j * nthr;
+            if (pc < 256) {
+                int64_t pix = pstep + (pc >> 2);
+                rdy[slot][j] = pix < pend ? *(const int4*)(a.dy + pix * a.K + k0 + (pc & 3) * 16)
+                                          : make_int4(0, 0, 0, 0);
+            }
+        }
+    };
+    auto store = [&](int buf, int slot) {
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+            *(int4*)&Bbuf(buf, wave)[((lane >> 2) + 16 * j) * RB + xpart * 16] = rx[slot][j];
+#pragma unroll
+        for (int j = 0; j < ndy; j++) {
+            int pc = tid + j * nthr;
+            if (pc < 256) *(int4*)&As[(size_t)buf * BK * RA + (pc >> 2) * RA + (pc & 3) * 16] = rdy[slot][j];
+        }
+    };
+
+    v4i acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) acc[i][j] = (v4i){0, 0, 0, 0};
+
+    const int nsteps = (int)((pend - pbeg + BK - 1) / BK);
+#pragma unroll
+    for (int u = 0; u < D; u++)
+        if (u < nsteps) load(u, pbeg + (int64_t)u * BK);
+    store(0, 0);
+    __syncthreads();
+    for (int st0 = 0; st0 < nsteps; st0 += D) {
+#pragma unroll
+        for (int u = 0; u < D; u++) {
+            const int st = st0 + u;
+            if (st < nsteps) {
+                const int8_t* A = As + (size_t)(st & 1) * BK * RA;
+                const int8_t* B = Bbuf(st & 1, wave);
+                v4i fa[4], fb[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++) fa[i] = tr8_frag(A, RA, i * 16, lane);
+#pragma unroll
+                for (int j = 0; j < 4; j++) fb[j] = tr8_frag(B, RB, j * 16, lane);
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+                if (st + 1 < nsteps) store((st + 1) & 1, (u + 1) % D);
+                if (st + D < nsteps) load(u, pbeg + (int64_t)(st + D) * BK);
+                __syncthreads();
+            }
+        }
+    }
+
+    // exact int32 partial tile of this split: part_out[split][k][tap * C + c]
+    int32_t* outp = part_out + (int64_t)blockIdx.y * a.K * a.RSC;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int64_t col = (int64_t)wave * a.C + c0 + j * 16 + (lane & 15);
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const int k = k0 + i * 16 + (lane >> 4) * 4 + e;
+                outp[(int64_t)k * a.RSC + col] = acc[i][j][e];
+            }
+        }
+}
+
+// Sum the per-split int32 partials in int64 (and take their max |.| for the
+// quantizer).  A block owns 256 consecutive elements (one int4 per lane); its
+// 8 waves take every 8th split, four loads in flight each, then fold in LDS.
+constexpr int kRedWaves = 8;
+__global__ __launch_bounds__(64 * kRedWaves) void k_wgrad_reduce(const int32_t* __restrict__ part, int64_t n,
+                                                                 int splits, long long* __restrict__ out,
+                                                                 unsigned long long* maxp)
+{
+    __shared__ long long red[kRedWaves][256];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t e0 = (int64_t)blockIdx.x * 256 + lane * 4;
+    long long s[4] = {0, 0, 0, 0};
+    if (e0 < n) {                         // n % 4 == 0: K is a multiple of 64
+        int k = wave;
+        for (; k + 3 * kRedWaves < splits; k += 4 * kRedWaves) {
+            int4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; u++) v[u] = *(const int4*)(part + (int64_t)(k + u * kRedWaves) * n + e0);
+#pragma unroll
+            for (int u = 0; u < 4; u++) { s[0] += v[u].x; s[1] += v[u].y; s[2] += v[u].z; s[3] += v[u].w; }
+        }
+        for (; k < splits; k += kRedWaves) {
+            int4 v = *(const int4*)(part + (int64_t)k * n + e0);
+            s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; u++) red[wave][lane * 4 + u] = s[u];
+    __syncthreads();
+    uint64_t mx = 0;
+    if (threadIdx.x < 256) {
+        const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+        long long t = 0;
+#pragma unroll
+        for (int w = 0; w < kRedWaves; w++) t += red[w][threadIdx.x];
+        if (e < n) {
+            out[e] = t;
+            mx = t < 0 ? (uint64_t)(-t) : (uint64_t)t;
+        }
+    }
+    if (maxp) block_atomic_max_u64(mx, maxp);
+}
+
+#ifndef ISEG_WGRAD_BLOCKS
+#define ISEG_WGRAD_BLOCKS 384      // target blocks of a split backward-weight launch
+#endif
+
+int64_t wgrad_splits(int64_t NPQ, int64_t tiles, int64_t* pps_out)
+{
+    int64_t splits = ceil_div64(ISEG_WGRAD_BLOCKS, tiles);
+    int64_t min_splits = ceil_div64(NPQ, kWgradSplit);
+    int64_t max_splits = ceil_div64(NPQ, 64 * 4);
+    if (splits > max_splits) splits = max_splits;
+    if (splits < min_splits) splits = min_splits;
+    if (splits > 65535) splits = 65535;
+    int64_t pps = ceil_div64(ceil_div64(NPQ, splits), 64) * 64;
+    if (pps > kWgradSplit) pps = kWgradSplit;
+    *pps_out = pps;
+    return ceil_div64(NPQ, pps);
+}
+
+#ifndef ISEG_WGRAD_TAPS_BLOCKS
+#define ISEG_WGRAD_TAPS_BLOCKS 256 // target blocks of the all-taps backward-weight launch
+#endif
+// shapes the all-taps kernel covers (the operand alignment is checked at launch):
+// filters of 9 taps (3x3); one wave per tap keeps a 576-thread block at three
+// waves per SIMD with no spills
+bool wgrad_taps_shape(int64_t NPQ, int64_t K, int64_t C, int64_t RS)
+{
+    return NPQ > 0 && C % 64 == 0 && K % 64 == 0 && RS == 9;
+}
+
+// split count and pixels per split of the all-taps kernel; the int32 partial
+// of one split stays exact because a split sums at most kWgradSplit products
+int64_t wgrad_taps_splits(int64_t NPQ, int64_t K, int64_t C, int64_t* pps_out)
+{
+    int64_t tiles = (C / 64) * (K / 64);
+    int64_t splits = ceil_div64(ISEG_WGRAD_TAPS_BLOCKS, tiles);
+    int64_t min_splits = ceil_div64(NPQ, kWgradSplit);
+    int64_t max_splits = ceil_div64(NPQ, 64 * 4);
+    if (splits > max_splits) splits = max_splits;
+    if (splits < min_splits) splits = min_splits;
+    if (splits > 65535) splits = 65535;
+    int64_t pps = ceil_div64(ceil_div64(NPQ, splits), 64) * 64;
+    if (pps > kWgradSplit) pps = kWgradSplit;
+    *pps_out = pps;
+    return ceil_div64(NPQ, pps);
+}
+
+size_t wgrad_taps_part_bytes(int64_t NPQ, int64_t K, int64_t C, int64_t RS)
+{
+    if (!wgrad_taps_shape(NPQ, K, C, RS)) return 0;
+    int64_t pps;
+    int64_t splits = wgrad_taps_splits(NPQ, K, C, &pps);
+    return align256((size_t)(splits * K * RS * C) * 4);
+}
+
+// all-taps launch: partials into `part`, then their int64 sum into a.acc (every
+// element written, no fill needed) and its max |.| into maxp when given
+int launch_wgrad_taps(WgradArgs a, int32_t* part, unsigned long long* maxp, hipStream_t s)
+{
+    const int RS = a.R * a.S;
+    int64_t splits = wgrad_taps_splits(a.NPQ, a.K, a.C, &a.pix_per_split);
+    const size_t lds = (size_t)(2 + 2 * RS) * BK * 80;
+    if (RS != 9) return ISEG_ERR_UNSUPPORTED;
+    if (hipFuncSetAttribute((const void*)k_conv_wgrad_taps<9>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds) != hipSuccess)
+        return ISEG_ERR_DEVICE;
+    dim3 grid((unsigned)((a.C / 64) * (a.K / 64)), (unsigned)splits);
+    ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, k_conv_wgrad_taps<9>, grid, dim3(64 * 9), lds, s, a, part);
+    int rc = launch_ok();
+    if (rc) return rc;
+    const int64_t n = (int64_t)a.K * a.RSC;
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)ceil_div64(n, 256)), dim3(64 * kRedWaves), 0, s,
+                       (const int32_t*)part, n, (int)splits, (long long*)a.acc, maxp);
+    return launch_ok();
+}
+
 int launch_wgrad(WgradArgs a, hipStream_t s)
+{
+    if (a.NPQ > 0 && a.C % 64 == 0 && a.K % 64 == 0 &&
+        (((uintptr_t)a.x | (uintptr_t)a.dy) & 15) == 0) {
+        const int BMt = a.K % 128 == 0 ? 128 : 64;
+        const int RS = a.R * a.S;
+        const int TAPS = RS > 1 ? 2 : 1;
+        const int ntg = (RS + TAPS - 1) / TAPS;
+        int64_t tiles = (int64_t)ntg * (a.C / 64) * (a.K / BMt);
+        int64_t splits = wgrad_splits(a.NPQ, tiles, &a.pix_per_split);
+        dim3 grid((unsigned)(ntg * (a.C / 64)), (unsigned)(a.K / BMt), (unsigned)splits);
+        if (BMt == 128 && TAPS == 2)
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, (k_conv_wgrad_tr<128, 2>), grid, dim3(256), 0, s, a);
+        else if (BMt == 128)
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, (k_conv_wgrad_tr<128, 1>), grid, dim3(256), 0, s, a);
+        else if (TAPS == 2)
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, (k_conv_wgrad_tr<64, 2>), grid, dim3(256), 0, s, a);
+        else
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, (k_conv_wgrad_tr<64, 1>), grid, dim3(256), 0, s, a);
+        return launch_ok();
+    }
+    if (a.NPQ > 0 && a.C % 64 == 0 && a.K % 4 == 0 &&
+        (((uintptr_t)a.x | (uintptr_t)a.dy) & 3) == 0) {
+        const int BMt = a.K >= 128 ? 128 : 64;
+        int64_t tiles = (int64_t)a.R * a.S * (a.C / 64) * ceil_div64(a.K, BMt);
+        int64_t splits = wgrad_splits(a.NPQ, tiles, &a.pix_per_split);
+        dim3 grid((unsigned)(a.R * a.S * (a.C / 64)), (unsigned)ceil_div64(a.K, BMt), (unsigned)splits);
+        if (BMt == 128)
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, k_conv_wgrad_tap<128>, grid, dim3(256), 0, s, a);
+        else
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, k_conv_wgrad_tap<64>, grid, dim3(256), 0, s, a);
+        return launch_ok();
+    }
+    return launch_wgrad_generic(a, s);
+}
+
+int launch_wgrad_generic(WgradArgs a, hipStream_t s)
 {
     if (a.NPQ <= 0) return ISEG_OK;
     bool vec = (a.C % 4) == 0 && (a.K % 4) == 0;
@@ -447,6 +1165,9 @@ extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
     if (!geom_ok(g, &P, &Q)) return 0;
     size_t s = 256;
     if (out_mode == ISEG_OUT_Q8) s += align256((size_t)(g->N * P * Q * g->K) * 4);
+    int64_t Cp = padded_c(g->C);
+    if (Cp != g->C)
+        s += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp));
     return s;
 }
 
@@ -462,13 +1183,31 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     if (g->C * g->R * g->S > kMaxKred) return ISEG_ERR_UNSUPPORTED;
     if (!ws || ws_bytes < iseg_conv_fwd_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
     unsigned long long* maxp = (unsigned long long*)ws;
-    int32_t* acc = out_mode == ISEG_OUT_Q8 ? (int32_t*)((char*)ws + 256) : (int32_t*)y;
+    char* wp = (char*)ws + 256;
+    int32_t* acc = (int32_t*)y;
+    if (out_mode == ISEG_OUT_Q8) {
+        acc = (int32_t*)wp;
+        wp += align256((size_t)(g->N * P * Q * g->K) * 4);
+    }
     int rc = launch_fill_u32(maxp, 2, 0, stream);
     if (rc) return rc;
+    // small C: zero-pad channels to a multiple of 16 for the vector path
+    const int64_t Cp = padded_c(g->C);
+    const int8_t* xs = x;
+    const int8_t* wsrc = w;
+    if (Cp != g->C) {
+        int8_t* xp = (int8_t*)wp;
+        wp += align256((size_t)(g->N * g->H * g->W * Cp));
+        int8_t* wpd = (int8_t*)wp;
+        if ((rc = launch_pad(x, xp, g->N * g->H * g->W, g->C, Cp, stream))) return rc;
+        if ((rc = launch_pad(w, wpd, g->K * g->R * g->S, g->C, Cp, stream))) return rc;
+        xs = xp;
+        wsrc = wpd;
+    }
     IgemmArgs a;
-    a.src = x; a.wmat = w; a.out = acc; a.maxp = out_mode == ISEG_OUT_Q8 ? maxp : nullptr;
+    a.src = xs; a.wmat = wsrc; a.out = acc; a.maxp = out_mode == ISEG_OUT_Q8 ? maxp : nullptr;
     a.Mrows = g->N * P * Q;
-    a.Nout = (int32_t)g->K; a.Kred = (int32_t)(g->C * g->R * g->S); a.Ci = (int32_t)g->C;
+    a.Nout = (int32_t)g->K; a.Kred = (int32_t)(Cp * g->R * g->S); a.Ci = (int32_t)Cp;
     a.Hs = (int32_t)g->H; a.Ws = (int32_t)g->W; a.Ho = (int32_t)P; a.Wo = (int32_t)Q;
     a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
@@ -535,7 +1274,12 @@ extern "C" size_t iseg_conv_bwd_weight_ws(const iseg_conv_geom* g, int32_t g_mod
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
     (void)g_mode;
-    return 256 + align256((size_t)(g->K * g->R * g->S * g->C) * 8);
+    size_t s = 256 + align256((size_t)(g->K * g->R * g->S * g->C) * 8);
+    int64_t Cp = padded_c(g->C);
+    if (Cp != g->C)
+        s += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp) * 8);
+    s += wgrad_taps_part_bytes(g->N * P * Q, g->K, Cp, g->R * g->S);
+    return s;
 }
 
 extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
@@ -552,25 +1296,56 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     if (!ws || ws_bytes < iseg_conv_bwd_weight_ws(g, g_mode)) return ISEG_ERR_WORKSPACE;
     unsigned long long* maxp = (unsigned long long*)ws;
     int64_t nw = g->K * g->R * g->S * g->C;
-    unsigned long long* acc = g_mode == ISEG_G_RAW ? (unsigned long long*)dw
-                                                   : (unsigned long long*)((char*)ws + 256);
+    char* wp = (char*)ws + 256;
+    unsigned long long* acc = g_mode == ISEG_G_RAW ? (unsigned long long*)dw : (unsigned long long*)wp;
+    wp += align256((size_t)nw * 8);
+    // small C: sums over zero-padded channels, then the real channels copied out
+    const int64_t Cp = padded_c(g->C);
+    const int8_t* xs = x;
+    unsigned long long* accp = acc;
     int rc = launch_fill_u32(maxp, 2, 0, stream);
-    if (!rc) rc = launch_fill_u32(acc, nw * 2, 0, stream);
     if (rc) return rc;
+    if (Cp != g->C) {
+        int8_t* xp = (int8_t*)wp;
+        wp += align256((size_t)(g->N * g->H * g->W * Cp));
+        accp = (unsigned long long*)wp;
+        if ((rc = launch_pad(x, xp, g->N * g->H * g->W, g->C, Cp, stream))) return rc;
+        xs = xp;
+    }
+    const int64_t nwp = g->K * g->R * g->S * Cp;
+    const int64_t NPQ = g->N * P * Q;
+    const bool taps = wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) &&
+                      (((uintptr_t)xs | (uintptr_t)dy) & 15) == 0;
+    int32_t* part = nullptr;
+    if (wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S)) {
+        part = (int32_t*)wp;
+        wp += wgrad_taps_part_bytes(NPQ, g->K, Cp, g->R * g->S);
+    }
+    if (!taps && (rc = launch_fill_u32(accp, nwp * 2, 0, stream))) return rc;
     WgradArgs a;
-    a.dy = dy; a.x = x; a.acc = acc;
+    a.dy = dy; a.x = xs; a.acc = accp;
     a.NPQ = g->N * P * Q; a.pix_per_split = 0;
-    a.K = (int32_t)g->K; a.C = (int32_t)g->C; a.R = (int32_t)g->R; a.S = (int32_t)g->S;
+    a.K = (int32_t)g->K; a.C = (int32_t)Cp; a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.H = (int32_t)g->H; a.W = (int32_t)g->W; a.P = (int32_t)P; a.Q = (int32_t)Q;
-    a.RSC = (int32_t)(g->R * g->S * g->C);
+    a.RSC = (int32_t)(g->R * g->S * Cp);
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
-    if ((rc = launch_wgrad(a, stream))) return rc;
+    // with no channel padding the reduction also takes the max for the quantizer
+    const bool fused_max = taps && Cp == g->C && g_mode != ISEG_G_RAW;
+    if (taps) rc = launch_wgrad_taps(a, part, fused_max ? maxp : nullptr, stream);
+    else rc = launch_wgrad(a, stream);
+    if (rc) return rc;
+    if (Cp != g->C) {
+        hipLaunchKernelGGL(k_unpad_i64, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream,
+                           (const long long*)accp, (long long*)acc, g->K * g->R * g->S,
+                           (int32_t)g->C, (int32_t)Cp);
+        if ((rc = launch_ok())) return rc;
+    }
     if (g_mode == ISEG_G_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dw_exp, dy_exp, x_exp);
         return launch_ok();
     }
-    if ((rc = launch_absmax(acc, ISEG_I64, nw, maxp, dev_status, stream))) return rc;
+    if (!fused_max && (rc = launch_absmax(acc, ISEG_I64, nw, maxp, dev_status, stream))) return rc;
     int keep = g_mode == ISEG_G_KEEP;
     return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr,
                                 0, bits, 1, keep, seed, tensor_id, step, ISEG_I8, dw, dw_exp,

@@ -98,6 +98,8 @@ CONV_SHAPES = [
     (1, 30, 30, 3, 64, 7, 2, 3, 1),       # 7x7/2 stem
     (1, 9, 11, 128, 130, 3, 1, 1, 1),     # K not a multiple of the tile
     (1, 5, 5, 20, 21, 1, 1, 0, 1),        # C % 16 != 0, K = 21
+    (1, 21, 19, 64, 64, 3, 1, 2, 2),      # dilation 2 on the 64-channel paths
+    (4, 9, 7, 64, 128, 3, 1, 1, 1),       # narrow rows: pixel runs wrap rows and images
 ]
 
 
