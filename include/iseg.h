@@ -195,7 +195,9 @@ int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, const int8_t* 
  *   (least code with x >= mu_q), p0[C] (least code with x > mu_q), mlo[C],
  *   mhi[C] (codes with y > 0 form [mlo, mhi]); int16 xhat_code[C][256] (by
  *   input code + 128); uint8 flags[C][256] (bit0: y > 0, bits1-2: sgn(x -
- *   mu_q) + 1); int8 a_code[C][256]. */
+ *   mu_q) + 1); int8 a_code[C][256]; uint32 bwd_entry[C][256] (by the
+ *   input code's byte, q & 0xff: bit0 y > 0, bits 8-9 sgn(x - mu_q) as a
+ *   two-bit signed field, bit 10 |sgn|, bits 16-31 the xhat code). */
 size_t iseg_bn_saved_bytes(int64_t C);
 size_t iseg_bn_fwd_ws(int64_t M, int64_t C);
 int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,

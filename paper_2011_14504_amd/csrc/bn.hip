@@ -50,12 +50,13 @@ struct Saved {
     int16_t* xcode;                  // [C][256]
     uint8_t* flags;                  // [C][256]
     int8_t* acode;                   // [C][256]
+    uint32_t* btab;                  // [C][256] by q & 0xff: y > 0, sgn, |sgn|, xhat code
 };
 
 size_t saved_bytes(int64_t C)
 {
     return 256 + 9 * align256((size_t)C * 4) + align256((size_t)C * 512) +
-           2 * align256((size_t)C * 256);
+           2 * align256((size_t)C * 256) + align256((size_t)C * 1024);
 }
 
 Saved saved_map(void* base, int64_t C)
@@ -75,7 +76,8 @@ Saved saved_map(void* base, int64_t C)
     s.mhi = (int32_t*)p; p += v;
     s.xcode = (int16_t*)p; p += align256((size_t)C * 512);
     s.flags = (uint8_t*)p; p += align256((size_t)C * 256);
-    s.acode = (int8_t*)p;
+    s.acode = (int8_t*)p; p += align256((size_t)C * 256);
+    s.btab = (uint32_t*)p;
     return s;
 }
 
@@ -247,6 +249,53 @@ __device__ __forceinline__ T group_fold(T v, int G, Op op)
 __device__ __forceinline__ bool group_leader(int G)
 {
     return ((G & (G - 1)) != 0 || G > 64) || (int)(threadIdx.x & 63) < G;
+}
+
+// Copy n 16-byte pieces (n <= V * kNT) from global memory into LDS, every load
+// of a thread issued before its first store.
+template <int V>
+__device__ __forceinline__ void copy_to_lds(uint4* dst, const uint4* __restrict__ src, int n)
+{
+    uint4 v[V];
+#pragma unroll
+    for (int k = 0; k < V; k++) {
+        const int i = threadIdx.x + k * kNT;
+        if (i < n) v[k] = src[i];
+    }
+#pragma unroll
+    for (int k = 0; k < V; k++) {
+        const int i = threadIdx.x + k * kNT;
+        if (i < n) dst[i] = v[k];
+    }
+}
+
+// LDS tables are kept one dword longer per row than in global memory: a
+// table row is 256 entries (a multiple of the bank count), so without the skew
+// every channel's entry for the same input code would sit in the same bank,
+// and real activations concentrate on a few codes.
+constexpr int kRowB = 256 + 4;      // bytes per row of a byte table in LDS
+constexpr int kRowW = 256 + 1;      // dwords per row of a dword table in LDS
+
+// Copy `rows` rows of 256 bytes (global, contiguous) into LDS rows of kRowB
+// bytes; every load of a thread is issued before its first store.
+template <int V>
+__device__ __forceinline__ void copy_rows_to_lds(int8_t* dst, const int8_t* __restrict__ src, int rows)
+{
+    const int n = rows * 16;
+    uint4 v[V];
+#pragma unroll
+    for (int k = 0; k < V; k++) {
+        const int i = threadIdx.x + k * kNT;
+        if (i < n) v[k] = ((const uint4*)src)[i];
+    }
+#pragma unroll
+    for (int k = 0; k < V; k++) {
+        const int i = threadIdx.x + k * kNT;
+        if (i < n) {
+            uint32_t* d = (uint32_t*)(dst + (i >> 4) * kRowB + (i & 15) * 16);
+            d[0] = v[k].x; d[1] = v[k].y; d[2] = v[k].z; d[3] = v[k].w;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -463,6 +512,8 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w,
     sv.xcode[idx] = (int16_t)nx;
     int sg = (D > 0) - (D < 0);
     sv.flags[idx] = (uint8_t)((Y > 0 ? 1 : 0) | ((sg + 1) << 1));
+    sv.btab[c * 256 + (q & 255)] = ((uint32_t)(uint16_t)(int16_t)nx << 16) | ((uint32_t)(sg & 3) << 8) |
+                                   ((uint32_t)(sg != 0) << 10) | (Y > 0 ? 1u : 0u);
     w.Y[idx] = (long long)Y;
     if (D >= 0) atomicMin(&sv.t0[c], q);
     if (D > 0) atomicMin(&sv.p0[c], q);
@@ -503,14 +554,13 @@ template <int CPL>
 __global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x, int8_t* __restrict__ y,
                                                    Stream st, Saved sv)
 {
-    __shared__ int8_t lut[128 * 256];
-    const uint32_t* src = (const uint32_t*)(sv.acode + (int64_t)blockIdx.y * st.CS * 256);
-    for (int i = threadIdx.x; i < st.CS * 64; i += blockDim.x) ((uint32_t*)lut)[i] = src[i];
+    __shared__ __attribute__((aligned(16))) int8_t lut[128 * kRowB];
+    copy_rows_to_lds<128 * 16 / kNT>(lut, sv.acode + (int64_t)blockIdx.y * st.CS * 256, st.CS);
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
     const int c0 = blockIdx.y * st.CS + g * CPL;
-    const int8_t* l = lut + g * CPL * 256 + 128;
+    const int8_t* l = lut + g * CPL * kRowB + 128;
     stream_rows<CPL, 4>(st, x, c0, rsub, [&](int64_t r, const Vec<CPL>& v) {
         Vec<CPL> o;
 #pragma unroll
@@ -518,7 +568,7 @@ __global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x
             uint32_t ow = 0;
 #pragma unroll
             for (int i = 0; i < 4; i++)
-                ow |= (uint32_t)(uint8_t)l[(j * 4 + i) * 256 + sbyte(v.w[j], i)] << (8 * i);
+                ow |= (uint32_t)(uint8_t)l[(j * 4 + i) * kRowB + sbyte(v.w[j], i)] << (8 * i);
             o.w[j] = ow;
         }
         vstore<CPL>(y + r * st.C + c0, o);
@@ -578,23 +628,62 @@ struct Thr {
 __device__ __forceinline__ int thr_cls(const Thr& t, int q) { return 1 + (q >= t.p0) - (q < t.t0); }
 __device__ __forceinline__ bool thr_mask(const Thr& t, int q) { return q >= t.mlo && q <= t.mhi; }
 
-// pass 1: sum delta, sum delta*n_xhat, sum sgn, per-class min/max of delta
+// Copy the channel slice's per-(channel, code) entries (saved by the forward)
+// into LDS rows of kRowW dwords, all loads of a thread issued before the first
+// store.  The ReLU bit becomes a mask byte in bits 0..7 (0xff passes delta).
+// With `lut_off` the upper half is replaced by the offset of the entry's
+// sgn-class row in the slice's dx-code tables (three rows of kRowB bytes per
+// channel, +128 for the signed delta).
+constexpr int kTabV = 64 * 256 / 4 / kNT;    // 16-byte pieces per thread (CS <= 64)
+__device__ __forceinline__ void load_bwd_tab(uint32_t* tab, const uint32_t* src, int CS, int relu,
+                                             bool lut_off)
+{
+    const int nv = CS * 64;
+    uint4 v[kTabV];
+#pragma unroll
+    for (int k = 0; k < kTabV; k++) {
+        const int i = threadIdx.x + k * kNT;
+        if (i < nv) v[k] = ((const uint4*)src)[i];
+    }
+#pragma unroll
+    for (int k = 0; k < kTabV; k++) {
+        const int i = threadIdx.x + k * kNT;
+        if (i < nv) {
+            uint32_t e[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                const uint32_t m = (!relu || (e[j] & 1)) ? 0xffu : 0u;
+                if (lut_off) {
+                    const int cl = (4 * i + j) >> 8;
+                    const int sg = ((int)(e[j] << 22)) >> 30;
+                    e[j] = ((uint32_t)((cl * 3 + sg + 1) * kRowB + 128) << 16) | m;
+                } else {
+                    e[j] = (e[j] & 0xffffff00u) | m;
+                }
+            }
+            uint32_t* d = tab + (i >> 6) * kRowW + (i & 63) * 4;
+            d[0] = e[0]; d[1] = e[1]; d[2] = e[2]; d[3] = e[3];
+        }
+    }
+}
+
+// Pass 1: sum delta, sum delta*xhat, sum sgn and the per-sgn-class extremes of
+// the masked delta d.  The extremes come from four keys per element, d +- 1024 s
+// and d +- 1024 |s| (s = sgn in {-1, 0, 1}, |d| <= 128): the minimum of d + 1024 s
+// lies in class -1 whenever that class is present, its maximum in class +1, and
+// likewise for the others, so six min/max updates replace per-class selects.
+constexpr int kKey = 1024;
+constexpr int kKeyInit = 4 * kKey;
 __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                    Saved sv, int32_t relu)
 {
-    __shared__ int16_t xc[64 * 256];
-    __shared__ Thr thr[64];
+    __shared__ __attribute__((aligned(16))) uint32_t tab[64 * kRowW];
     __shared__ unsigned long long sSdn[64];
     __shared__ int32_t sSd[64], sZ[64], sMM[64 * 6];
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
-    {
-        const uint32_t* src = (const uint32_t*)(sv.xcode + cbase * 256);
-        for (int i = threadIdx.x; i < st.CS * 128; i += blockDim.x) ((uint32_t*)xc)[i] = src[i];
-    }
+    load_bwd_tab(tab, sv.btab + cbase * 256, st.CS, relu, false);
     if ((int)threadIdx.x < st.CS) {
-        int c = (int)cbase + threadIdx.x;
-        thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], relu ? sv.mlo[c] : -1000, relu ? sv.mhi[c] : 1000};
         sSdn[threadIdx.x] = 0; sSd[threadIdx.x] = 0; sZ[threadIdx.x] = 0;
         for (int k = 0; k < 3; k++) { sMM[threadIdx.x * 6 + 2 * k] = 1000; sMM[threadIdx.x * 6 + 2 * k + 1] = -1000; }
     }
@@ -604,34 +693,78 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
     const bool active = stream_lane(st, g, rsub);
     int32_t sd[4] = {0, 0, 0, 0}, z[4] = {0, 0, 0, 0};
     int64_t sdn[4] = {0, 0, 0, 0};
-    int32_t mm[4][6];
+    // key extremes: min(d + 1024 s), max(d + 1024 s), min(d - 1024 s), max(d - 1024 s),
+    // min(d + 1024 |s|), max(d - 1024 |s|)
+    int32_t kmn0[4], kmx0[4], kmn1[4], kmx1[4], kmn2[4], kmx3[4];
 #pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-        for (int k = 0; k < 3; k++) { mm[i][2 * k] = 1000; mm[i][2 * k + 1] = -1000; }
+    for (int i = 0; i < 4; i++) {
+        kmn0[i] = kmn1[i] = kmn2[i] = kKeyInit;
+        kmx0[i] = kmx1[i] = kmx3[i] = -kKeyInit;
+    }
     if (active) {
         const int c0 = (int)cbase + g * 4;
-        Thr t[4];
-#pragma unroll
-        for (int i = 0; i < 4; i++) t[i] = thr[g * 4 + i];
-        stream_rows2<4, 8>(st, x, dy, c0, rsub, [&](int64_t, const Vec<4>& vxx, const Vec<4>& vdd) {
-            const uint32_t vx = vxx.w[0], vd = vdd.w[0];
+        const uint32_t* tb = tab + g * 4 * kRowW;
+        const int64_t step = (int64_t)gridDim.x * st.rpi;
+        auto elem = [&](uint32_t wx, uint32_t wd, int32_t* sdn32) {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                int q = sbyte(vx, i);
-                int d = thr_mask(t[i], q) ? sbyte(vd, i) : 0;
-                int cls = thr_cls(t[i], q);
-                sd[i] += d;
-                sdn[i] += (int64_t)d * xc[(g * 4 + i) * 256 + q + 128];
-                z[i] += cls - 1;
-#pragma unroll
-                for (int k = 0; k < 3; k++) {
-                    bool hit = cls == k;
-                    mm[i][2 * k] = hit && d < mm[i][2 * k] ? d : mm[i][2 * k];
-                    mm[i][2 * k + 1] = hit && d > mm[i][2 * k + 1] ? d : mm[i][2 * k + 1];
-                }
+                const uint32_t e = tb[i * kRowW + ((wx >> (8 * i)) & 0xff)];
+                const int dm = sbyte(wd, i) & (int)(int8_t)(e & 0xff);
+                const int sg = ((int)(e << 22)) >> 30;            // bits 8..9, signed
+                const int ab = (int)((e >> 10) & 1);
+                sd[i] += dm;
+                sdn32[i] += dm * ((int)e >> 16);
+                z[i] += sg;
+                const int k0 = dm + sg * kKey, k1 = dm - sg * kKey;
+                const int k2 = dm + ab * kKey, k3 = dm - ab * kKey;
+                kmn0[i] = min(kmn0[i], k0); kmx0[i] = max(kmx0[i], k0);
+                kmn1[i] = min(kmn1[i], k1); kmx1[i] = max(kmx1[i], k1);
+                kmn2[i] = min(kmn2[i], k2); kmx3[i] = max(kmx3[i], k3);
             }
-        });
+        };
+        // full groups of U rows (all in range), next group's loads issued
+        // before this group's arithmetic; then the remaining rows one by one
+        constexpr int U = 4;
+        int64_t r = (int64_t)blockIdx.x * st.rpi + rsub;
+        const int64_t full_end = st.M - (U - 1) * step;
+        uint32_t vx[U], vd[U], nx[U], nd[U];
+        auto load = [&](int64_t r0, uint32_t* ax, uint32_t* ad) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                ax[u] = *(const uint32_t*)(x + (r0 + u * step) * st.C + c0);
+                ad[u] = *(const uint32_t*)(dy + (r0 + u * step) * st.C + c0);
+            }
+        };
+        if (r < full_end) load(r, vx, vd);
+        while (r < full_end) {
+            const int64_t rn = r + U * step;
+            if (rn < full_end) load(rn, nx, nd);
+            int32_t sdn32[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int u = 0; u < U; u++) elem(vx[u], vd[u], sdn32);
+#pragma unroll
+            for (int i = 0; i < 4; i++) sdn[i] += sdn32[i];
+#pragma unroll
+            for (int u = 0; u < U; u++) { vx[u] = nx[u]; vd[u] = nd[u]; }
+            r = rn;
+        }
+        for (; r < st.M; r += step) {
+            int32_t sdn32[4] = {0, 0, 0, 0};
+            elem(*(const uint32_t*)(x + r * st.C + c0), *(const uint32_t*)(dy + r * st.C + c0), sdn32);
+#pragma unroll
+            for (int i = 0; i < 4; i++) sdn[i] += sdn32[i];
+        }
+    }
+    // decode the keys into (min, max) per class; an empty class gives (1000, -1000)
+    int32_t mm[4][6];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        mm[i][0] = kmn0[i] <= -kKey + 128 ? kmn0[i] + kKey : 1000;     // class -1
+        mm[i][1] = kmx1[i] >= kKey - 128 ? kmx1[i] - kKey : -1000;
+        mm[i][2] = kmn2[i] <= 128 ? kmn2[i] : 1000;                     // class 0
+        mm[i][3] = kmx3[i] >= -128 ? kmx3[i] : -1000;
+        mm[i][4] = kmn1[i] <= -kKey + 128 ? kmn1[i] + kKey : 1000;     // class +1
+        mm[i][5] = kmx0[i] >= kKey - 128 ? kmx0[i] - kKey : -1000;
     }
 #pragma unroll
     for (int i = 0; i < 4; i++) {
@@ -732,13 +865,12 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
                                                     const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                     Saved sv, BnCfg cf, const int8_t* gamma_q)
 {
-    __shared__ int16_t xc[64 * 256];
+    __shared__ __attribute__((aligned(16))) int16_t xc[64 * 256];
     __shared__ Thr thr[64];
     __shared__ unsigned long long sF[64], sFn[64];
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
     {
-        const uint32_t* src = (const uint32_t*)(sv.xcode + cbase * 256);
-        for (int i = threadIdx.x; i < st.CS * 128; i += blockDim.x) ((uint32_t*)xc)[i] = src[i];
+        copy_to_lds<64 * 512 / 16 / kNT>((uint4*)xc, (const uint4*)(sv.xcode + cbase * 256), st.CS * 32);
     }
     if ((int)threadIdx.x < st.CS) {
         int c = (int)cbase + threadIdx.x;
@@ -886,45 +1018,61 @@ __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t 
     }
 }
 
-template <int CPL>
+// Output pass: dx code = lut[c][sgn class][masked delta].  A per-(channel,
+// code) entry gives the offset of the channel's class row in the block's LDS
+// copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
+// element costs two LDS reads and a handful of ALU operations.
 __global__ __launch_bounds__(1024) void k_bnb_apply(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x,
                                                    int8_t* __restrict__ dx, Stream st, BwdWs w,
                                                    Saved sv, int32_t relu)
 {
-    __shared__ int8_t lut[64 * 768];
-    __shared__ Thr thr[64];
+    __shared__ __attribute__((aligned(16))) int8_t lut[64 * 3 * kRowB];
+    __shared__ __attribute__((aligned(16))) uint32_t tab[64 * kRowW];
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
-    {
-        const uint32_t* src = (const uint32_t*)(w.lut + cbase * 768);
-        for (int i = threadIdx.x; i < st.CS * 192; i += blockDim.x) ((uint32_t*)lut)[i] = src[i];
-    }
-    if ((int)threadIdx.x < st.CS) {
-        int c = (int)cbase + threadIdx.x;
-        thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], relu ? sv.mlo[c] : -1000, relu ? sv.mhi[c] : 1000};
-    }
+    copy_rows_to_lds<64 * 3 * 16 / kNT>(lut, w.lut + cbase * 768, st.CS * 3);
+    load_bwd_tab(tab, sv.btab + cbase * 256, st.CS, relu, true);
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
-    const int c0 = (int)cbase + g * CPL;
-    stream_rows2<CPL, 4>(st, x, dy, c0, rsub, [&](int64_t r, const Vec<CPL>& vx, const Vec<CPL>& vd) {
-        Vec<CPL> o;
+    const int c0 = (int)cbase + g * 4;
+    const uint32_t* tb = tab + g * 4 * kRowW;
+    const int64_t step = (int64_t)gridDim.x * st.rpi;
+    auto elem = [&](uint32_t wx, uint32_t wd) {
+        uint32_t ow = 0;
 #pragma unroll
-        for (int j = 0; j < CPL / 4; j++) {
-            uint32_t ow = 0;
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int cl = g * CPL + j * 4 + i;
-                const Thr t = thr[cl];
-                int q = sbyte(vx.w[j], i);
-                int d = thr_mask(t, q) ? sbyte(vd.w[j], i) : 0;
-                int cls = thr_cls(t, q);
-                ow |= (uint32_t)(uint8_t)lut[(cl * 3 + cls) * 256 + d + 128] << (8 * i);
-            }
-            o.w[j] = ow;
+        for (int i = 0; i < 4; i++) {
+            const uint32_t e = tb[i * kRowW + ((wx >> (8 * i)) & 0xff)];
+            const int idx = (int)(e >> 16) + (sbyte(wd, i) & (int)(int8_t)(e & 0xff));
+            ow |= (uint32_t)(uint8_t)lut[idx] << (8 * i);
         }
-        vstore<CPL>(dx + r * st.C + c0, o);
-    });
+        return ow;
+    };
+    // full groups of U rows with the next group's loads in flight, then the rest
+    constexpr int U = 4;
+    int64_t r = (int64_t)blockIdx.x * st.rpi + rsub;
+    const int64_t full_end = st.M - (U - 1) * step;
+    uint32_t vx[U], vd[U], nx[U], nd[U];
+    auto load = [&](int64_t r0, uint32_t* ax, uint32_t* ad) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            ax[u] = *(const uint32_t*)(x + (r0 + u * step) * st.C + c0);
+            ad[u] = *(const uint32_t*)(dy + (r0 + u * step) * st.C + c0);
+        }
+    };
+    if (r < full_end) load(r, vx, vd);
+    while (r < full_end) {
+        const int64_t rn = r + U * step;
+        if (rn < full_end) load(rn, nx, nd);
+#pragma unroll
+        for (int u = 0; u < U; u++) *(uint32_t*)(dx + (r + u * step) * st.C + c0) = elem(vx[u], vd[u]);
+#pragma unroll
+        for (int u = 0; u < U; u++) { vx[u] = nx[u]; vd[u] = nd[u]; }
+        r = rn;
+    }
+    for (; r < st.M; r += step)
+        *(uint32_t*)(dx + r * st.C + c0) =
+            elem(*(const uint32_t*)(x + r * st.C + c0), *(const uint32_t*)(dy + r * st.C + c0));
 }
 
 bool cfg_ok(const iseg_bn_cfg* c)
@@ -1043,13 +1191,7 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     hipLaunchKernelGGL(k_bnb_fin2, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, exact_e2);
     hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2,
                        dx_exp);
-    if (cs % 16 == 0 && (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx_out) & 15) == 0) {
-        Stream s16 = make_stream(M, C, cs, 16, 4, kMaxBlocks);
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply<16>, stream_grid(s16), dim3(kNT), 0,
-                          stream, dy, x, dx_out, s16, w, sv, cf.relu);
-    } else {
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply<4>, sg, dim3(kNT), 0, stream, dy, x,
-                          dx_out, st, w, sv, cf.relu);
-    }
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, sg, dim3(kNT), 0, stream, dy, x, dx_out, st,
+                      w, sv, cf.relu);
     return launch_ok();
 }

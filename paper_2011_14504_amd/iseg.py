@@ -472,6 +472,8 @@ def bn_saved_view(saved, Cc):
     out["flags"] = saved[off:off + 256 * Cc].view(Cc, 256)
     off += al(256 * Cc)
     out["acode"] = saved[off:off + 256 * Cc].view(torch.int8).view(Cc, 256)
+    off += al(256 * Cc)
+    out["bwd_entry"] = saved[off:off + 1024 * Cc].view(torch.int32).view(Cc, 256)
     return out
 
 
