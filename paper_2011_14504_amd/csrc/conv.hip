@@ -32,7 +32,9 @@ struct IgemmArgs {
     const int8_t* src;            // NHWC [N, Hs, Ws, Ci]
     const int8_t* wmat;           // [Nout][Kred]
     int32_t* out;                 // [Mrows][Nout]
-    unsigned long long* maxp;     // max |sum| (may be null)
+    int16_t* out16;               // staged [Mrows][Nout] (int16 path)
+    uint8_t* tshift;              // per (row tile, column tile) staging shift
+    uint64_t* pmax;               // per-block max |sum| partials (may be null)
     int64_t Mrows;
     int32_t Nout, Kred, Ci;
     int32_t Hs, Ws, Ho, Wo;
@@ -117,7 +119,7 @@ __device__ __forceinline__ int4 load_b_piece(const IgemmArgs& a, int n, int kk0)
 }
 
 template <int MODE>
-int launch_igemm_generic(const IgemmArgs& a, hipStream_t s);
+int launch_igemm_generic(const IgemmArgs& a, hipStream_t s, int64_t* nblk);
 
 template <int MODE, bool VEC, int BM, int BN>
 __global__ __launch_bounds__(256) void k_conv_igemm(IgemmArgs a)
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(256) void k_conv_igemm(IgemmArgs a)
                 }
             }
         }
-    if (a.maxp) block_atomic_max_u64(mx, a.maxp);
+    if (a.pmax) block_store_max_u64(mx, a.pmax);
 }
 
 // Implicit GEMM for Ci % 64 == 0: the k-loop runs tap-major in 64-channel
@@ -318,30 +320,638 @@ __global__ __launch_bounds__(256) void k_conv_igemm_tap(IgemmArgs a)
                 }
             }
         }
-    if (a.maxp) block_atomic_max_u64(mx, a.maxp);
+    if (a.pmax) block_store_max_u64(mx, a.pmax);
+}
+
+// ---------------------------------------------------------------------------
+// Implicit GEMM with direct-to-LDS loads (Ci % 64 == 0, Nout % BN == 0).
+//
+// Each step (one tap, one 64-channel chunk) stages a 128 x 64-byte A tile and
+// a BN x 64-byte B tile with global_load_lds_dwordx4: a wave's instruction
+// writes 64 lanes x 16 bytes contiguously, i.e. 16 tile rows.  Pieces are
+// placed with an XOR swizzle (16-byte slot = part ^ ((row >> 2) & 3)) instead
+// of row padding, so the 16 rows read by one ds_read_b128 lane group fall in
+// 16 distinct 4-bank groups.  Taps falling into padding load from a zero page.
+// kStages LDS buffers keep kStages - 1 steps of loads in flight; vmcnt tracks
+// the DMA completions and one barrier per step publishes a stage.
+// ---------------------------------------------------------------------------
+__device__ __attribute__((aligned(64))) int8_t g_conv_zero[64];
+constexpr int kStages = 4;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ void dma16(const void* g, int8_t* lds_wave_base)
+{
+    __builtin_amdgcn_global_load_lds(g, (lds_void_t*)lds_wave_base, 16, 0, 0);
+}
+
+// wait until at most n vector-memory operations of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ int swz(int row, int part) { return row * 64 + ((part ^ ((row >> 2) & 3)) << 4); }
+
+// row -> (image, output row, output column) in 32-bit arithmetic (Mrows < 2^31)
+__device__ __forceinline__ RowPix row_pix32(const IgemmArgs& a, int64_t m)
+{
+    RowPix rp;
+    rp.ok = m < a.Mrows;
+    const uint32_t mm = rp.ok ? (uint32_t)m : 0u;
+    const uint32_t hw = (uint32_t)a.Ho * (uint32_t)a.Wo;
+    rp.n = (int32_t)(mm / hw);
+    const uint32_t rem = mm - (uint32_t)rp.n * hw;
+    rp.oh = (int32_t)(rem / (uint32_t)a.Wo);
+    rp.ow = (int32_t)(rem - (uint32_t)rp.oh * (uint32_t)a.Wo);
+    return rp;
+}
+
+// Staging of the exact int32 sums as int16 with a per-tile right shift
+// t = max(0, bitlen(tile max) - 15): floor(acc / 2^t) fits int16, and since
+// the tensor's requant shift r = bitlen(max) - 7 is >= t + 1 whenever t > 0,
+// rounding floor(acc / 2^t) half-up by the remaining r - t bits gives the same
+// code as rounding acc by r (2^(r-1) is a multiple of 2^t, so the dropped low
+// bits can never carry into the rounding position).
+template <int MODE, int BN, bool OUT16>
+__global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
+{
+    constexpr int BM = 128;
+    constexpr int WM = 64, WN = BN / 2;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int NA = BM / 64;              // A instructions per wave and step (16 rows each)
+    constexpr int NB = BN / 64;              // B instructions per wave and step
+    constexpr int LPW = NA + NB;             // DMA loads per wave and step
+    constexpr int SA = BM * 64, SB = BN * 64;
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];   // [kStages][SA + SB]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // XCD-aware tile order: consecutive pixel tiles go to one XCD (blocks are
+    // dealt to the 8 XCDs round-robin), so halo rows are shared in its L2
+    const int nbx = gridDim.x;
+    int bx = blockIdx.x;
+    if ((nbx & 7) == 0) bx = (bx & 7) * (nbx >> 3) + (bx >> 3);
+    const int64_t m0 = (int64_t)bx * BM;
+    const int n0 = blockIdx.y * BN;
+    const int nchunk = a.Ci / BK;
+    const int nk = a.R * a.S * nchunk;
+
+    // this lane's DMA pieces: row (16 * instr + lane / 4) in slot lane % 4
+    const int rin = lane >> 2;
+    const int part = (lane & 3) ^ ((rin >> 2) & 3);
+    RowPix rp[NA];
+#pragma unroll
+    for (int j = 0; j < NA; j++) rp[j] = row_pix32(a, m0 + 16 * (wave + 4 * j) + rin);
+    const int8_t* brow[NB];
+#pragma unroll
+    for (int j = 0; j < NB; j++) brow[j] = a.wmat + (int64_t)(n0 + 16 * (wave + 4 * j) + rin) * a.Kred + part * 16;
+
+    int64_t soff[NA];
+    auto set_tap = [&](int tap) {
+        const int r = tap / a.S, s = tap - (tap / a.S) * a.S;
+#pragma unroll
+        for (int j = 0; j < NA; j++) {
+            const int64_t sp = src_pixel<MODE>(a, rp[j], r, s);
+            soff[j] = sp < 0 ? -1 : sp * a.Ci + part * 16;
+        }
+    };
+    int ltap = 0, lcc = 0;                    // step being issued
+    auto issue = [&](int kb) {
+        int8_t* st = smem + (kb % kStages) * (SA + SB);
+#pragma unroll
+        for (int j = 0; j < NA; j++) {
+            const void* g = soff[j] >= 0 ? (const void*)(a.src + soff[j] + lcc * BK) : (const void*)g_conv_zero;
+            dma16(g, st + (wave + 4 * j) * 1024);
+        }
+#pragma unroll
+        for (int j = 0; j < NB; j++) dma16(brow[j] + (int64_t)kb * BK, st + SA + (wave + 4 * j) * 1024);
+        if (++lcc == nchunk) { lcc = 0; if (++ltap < a.R * a.S) set_tap(ltap); }
+    };
+
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = lane & 15, lpart = lane >> 4;
+    v4i acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++) acc[i][j] = (v4i){0, 0, 0, 0};
+
+    set_tap(0);
+#pragma unroll
+    for (int p = 0; p < kStages - 1; p++)
+        if (p < nk) issue(p);
+    for (int kb = 0; kb < nk; kb++) {
+        const int ahead = nk - 1 - kb;         // steps issued after kb (at most kStages - 2)
+        if (ahead >= 2) wait_vm<2 * LPW>();
+        else if (ahead == 1) wait_vm<LPW>();
+        else wait_vm<0>();
+        // a plain barrier: __syncthreads() would also drain every DMA in flight
+        __builtin_amdgcn_s_barrier();
+        if (kb + kStages - 1 < nk) issue(kb + kStages - 1);
+        const int8_t* A = smem + (kb % kStages) * (SA + SB);
+        const int8_t* B = A + SA;
+        v4i fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&A[swz(wm * WM + i * 16 + lrow, lpart)];
+#pragma unroll
+        for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&B[swz(wn * WN + j * 16 + lrow, lpart)];
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+
+    // rows of this block that exist (the last row tile may be ragged)
+    const int vrows = a.Mrows - m0 < BM ? (int)(a.Mrows - m0) : BM;
+    if (!OUT16) {
+        uint32_t mx = 0;
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++) {
+                const int n = n0 + wn * WN + j * 16 + lrow;
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int row = wm * WM + i * 16 + lpart * 4 + e;
+                    if (row < vrows) {
+                        const int32_t v = acc[i][j][e];
+                        a.out[(m0 + row) * a.Nout + n] = v;
+                        const uint32_t av = (uint32_t)(v < 0 ? -v : v);
+                        mx = av > mx ? av : mx;
+                    }
+                }
+            }
+        if (a.pmax) block_store_max_u64(mx, a.pmax);
+        return;
+    }
+    // int16 staging: tile max -> shift, shifted tile through LDS, 16-byte stores
+    __shared__ uint32_t wmax[4];
+    uint32_t mx = 0;
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++)
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const int row = wm * WM + i * 16 + lpart * 4 + e;
+                const int32_t v = acc[i][j][e];
+                const uint32_t av = row < vrows ? (uint32_t)(v < 0 ? -v : v) : 0u;
+                mx = av > mx ? av : mx;
+            }
+    mx = wave_max_u32(mx);
+    if (lane == 0) wmax[wave] = mx;
+    __syncthreads();                          // also: every wave is done with the stage buffers
+    uint32_t tmax = wmax[0];
+#pragma unroll
+    for (int w = 1; w < 4; w++) tmax = wmax[w] > tmax ? wmax[w] : tmax;
+    const int t = tmax ? max(0, 32 - __builtin_clz(tmax) - 15) : 0;
+    constexpr int RS16 = BN + 8;              // int16 per LDS row (16-byte pad: bank spread)
+    int16_t* T = (int16_t*)smem;
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++)
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const int row = wm * WM + i * 16 + lpart * 4 + e;
+                T[row * RS16 + wn * WN + j * 16 + lrow] = (int16_t)(acc[i][j][e] >> t);
+            }
+    __syncthreads();
+    constexpr int CPR = BN / 8;               // 16-byte chunks per row
+#pragma unroll
+    for (int k = 0; k < BM * CPR / 256; k++) {
+        const int c = tid + k * 256;
+        const int row = c / CPR, cc = c - (c / CPR) * CPR;
+        if (row < vrows)
+            *(int4*)(a.out16 + (m0 + row) * a.Nout + n0 + cc * 8) = *(const int4*)&T[row * RS16 + cc * 8];
+    }
+    if (tid == 0) {
+        a.tshift[(int64_t)bx * gridDim.y + blockIdx.y] = (uint8_t)t;
+        if (a.pmax) a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = tmax;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 3x3, stride-1 convolution from an LDS halo tile (Ci % 64 == 0, Nout % 64 == 0).
+//
+// A block owns TH = 4 output rows x TW output columns of one image and 64
+// output channels; wave w computes output row w.  Per 64-channel chunk the
+// block stages the (TH + 2 dh) x (TW + 2 dw) input halo and the 9 x 64 x 64
+// weight slice once (direct-to-LDS loads, XOR-swizzled 16-byte slots: slot =
+// part ^ ((index >> 2) & 3), so any 16 consecutive pixels or channels are
+// conflict-free for ds_read_b128), then runs all nine taps from LDS: the A
+// operand of tap (r, s) is the halo shifted by (r dh, s dw).  Backward-data
+// with stride 1 is the same convolution over dy with the flipped, transposed
+// filter and padding dil (R - 1) - pad.
+// ---------------------------------------------------------------------------
+struct HaloArgs {
+    const int8_t* src;            // [N][Hs][Ws][Ci]
+    const int8_t* wmat;           // [Nout][3][3][Ci]
+    int32_t* out;                 // raw sums [N][Ho][Wo][Nout] (when out16 is null)
+    int16_t* out16;               // staged sums
+    uint8_t* tshift;              // per (tile, 64-channel group) staging shift
+    int8_t* out8;                 // final SQ codes (second pass of the two-pass path)
+    const int32_t* exp_a;         // operand exponents and the result exponent (second pass)
+    const int32_t* exp_b;
+    int32_t* out_exp;
+    uint64_t* pmax;               // per-block max |sum| partials
+    int64_t npmax;
+    int32_t N, Hs, Ws, Ci, Ho, Wo, Nout;
+    int32_t ph, pw, dh, dw;       // input row of output row y and tap r: y - ph + r dh
+    int32_t tiles_y, tiles_x;
+};
+
+constexpr int kHaloTH = 4;
+
+size_t halo_lds_bytes(int TW, int dh, int dw)
+{
+    return (size_t)(kHaloTH + 2 * dh) * (TW + 2 * dw) * 64 + 9 * 64 * 64;
+}
+
+// epilogues: raw int32 sums; int16 staging; tile max only (first pass of the
+// two-pass path); final SQ codes from the global max (second pass)
+enum { EPI_RAW = 0, EPI_STAGE16 = 1, EPI_MAX = 2, EPI_Q8 = 3 };
+
+template <int TW, int EPI>
+__global__ __launch_bounds__(256) void k_conv3x3_halo(HaloArgs a)
+{
+    constexpr int TH = kHaloTH, TM = TW / 16, TN = 4;
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+    const int HR = TH + 2 * a.dh, HC = TW + 2 * a.dw;
+    const int nhalo = HR * HC * 4;                        // 16-byte pieces
+    int8_t* halo = smem;
+    int8_t* wts = smem + HR * HC * 64;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nbx = gridDim.x;
+    int bx = blockIdx.x;
+    if ((nbx & 7) == 0) bx = (bx & 7) * (nbx >> 3) + (bx >> 3);
+    const int tx = bx % a.tiles_x, t2 = bx / a.tiles_x;
+    const int ty = t2 % a.tiles_y, n = t2 / a.tiles_y;
+    const int oy0 = ty * TH, ox0 = tx * TW, k0 = blockIdx.y * 64;
+    const int iy0 = oy0 - a.ph, ix0 = ox0 - a.pw;
+    const int lrow = lane & 15, lpart = lane >> 4;
+
+    v4i acc[TM][TN];
+
+    // A-operand LDS addresses of fragment 0 for the nine taps: fragment i adds
+    // 16 pixels = 1024 bytes and leaves the swizzle phase unchanged
+    int aaddr[9];
+#pragma unroll
+    for (int r = 0; r < 3; r++)
+#pragma unroll
+        for (int s2 = 0; s2 < 3; s2++) {
+            const int p = (wave + r * a.dh) * HC + lrow + s2 * a.dw;
+            aaddr[r * 3 + s2] = p * 64 + ((lpart ^ ((p >> 2) & 3)) << 4);
+        }
+    int baddr[TN];
+#pragma unroll
+    for (int j = 0; j < TN; j++) {
+        const int kk = 16 * j + lrow;
+        baddr[j] = kk * 64 + ((lpart ^ ((kk >> 2) & 3)) << 4);
+    }
+    // halo pieces of this lane: instruction k = wave + 4 u covers pixels
+    // 16 k .. 16 k + 15; pixel (hr, hc) advances by 64 per instruction
+    const int p0 = 16 * wave + (lane >> 2);
+    const int hr0 = p0 / HC, hc0 = p0 - (p0 / HC) * HC;
+    // weight pieces: instruction k = wave + 4 j holds tap j (rows of 16
+    // channels kk = 16 (wave) + lane / 4 ... ), same lane slot in every tap
+    const int wkk = ((wave * 64 + lane) >> 2) & 63;
+    const int wpart = (lane & 3) ^ ((wkk >> 2) & 3);
+    const int wtap0 = (wave * 64 + lane) >> 8;
+    const int8_t* wsrc = a.wmat + ((int64_t)(k0 + wkk) * 9 + wtap0) * a.Ci + wpart * 16;
+
+    const int nchunk = a.Ci / 64;
+    uint64_t gmax = 0;
+    for (int cc = 0; cc < nchunk; cc++) {
+        if (cc) __syncthreads();                          // the previous chunk's reads are done
+        {
+            int hr = hr0, hc = hc0;
+            for (int k = wave; k * 64 < nhalo; k += 4) {
+                const int q = k * 64 + lane;
+                if (q < nhalo) {
+                    const int p = q >> 2;
+                    const int part = (q & 3) ^ ((p >> 2) & 3);
+                    const int iy = iy0 + hr, ix = ix0 + hc;
+                    const bool v = (unsigned)iy < (unsigned)a.Hs && (unsigned)ix < (unsigned)a.Ws;
+                    const void* g = v ? (const void*)(a.src + (((int64_t)n * a.Hs + iy) * a.Ws + ix) * a.Ci +
+                                                      cc * 64 + part * 16)
+                                      : (const void*)g_conv_zero;
+                    dma16(g, halo + k * 1024);
+                }
+                hc += 64;
+                while (hc >= HC) { hc -= HC; ++hr; }
+            }
+        }
+        // instruction wave + 4 j covers pieces (wave + 4 j) * 64 + lane: tap =
+        // wtap0 + j (four instructions per tap), same channel row and slot
+#pragma unroll
+        for (int j = 0; j < 9; j++)
+            dma16(wsrc + (int64_t)j * a.Ci + cc * 64, wts + (wave + 4 * j) * 1024);
+        // second pass: the global max, read while the first chunk is in flight
+        if (EPI == EPI_Q8 && cc == 0) gmax = reduce_partials_u64(a.pmax, a.npmax);
+        wait_vm<0>();
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < 9; t++) {
+            v4i fa[TM], fb[TN];
+#pragma unroll
+            for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&halo[aaddr[t] + 1024 * i];
+#pragma unroll
+            for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&wts[t * 4096 + baddr[j]];
+            if (t == 0 && cc == 0) {              // first product: no accumulator to clear
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], (v4i){0, 0, 0, 0}, 0, 0, 0);
+            } else {
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+            }
+        }
+    }
+
+    // acc[i][j][e]: output (row wave, column 16 i + 4 lpart + e), channel k0 + 16 j + lrow
+    const int oy = oy0 + wave;
+    const int64_t rowbase = ((int64_t)n * a.Ho + oy) * a.Wo;
+    if (EPI == EPI_RAW) {
+        if (oy < a.Ho) {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int ox = ox0 + 16 * i + 4 * lpart + e;
+                    if (ox < a.Wo) {
+#pragma unroll
+                        for (int j = 0; j < TN; j++)
+                            a.out[(rowbase + ox) * a.Nout + k0 + 16 * j + lrow] = acc[i][j][e];
+                    }
+                }
+        }
+        return;
+    }
+    const int vcols = a.Wo - ox0 < TW ? a.Wo - ox0 : TW;
+    if (EPI == EPI_Q8) {
+        // codes = SQ(acc) with r = bitlen(global max) - 7; rhu(acc, r) = ((acc >> (r - 1)) + 1) >> 1
+        const uint64_t M = gmax;
+        const int r = M ? (64 - __builtin_clzll(M)) - 7 : 0;
+        if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + r;
+        constexpr int RB8 = 64 + 16;                  // bytes per LDS row of the code tile
+        int8_t* T = smem + (wave * TW + 4 * lpart) * RB8 + lrow;
+        __syncthreads();                              // every wave is done with the halo
+        const int rs = r > 0 ? r - 1 : 0, ls = r > 0 ? 0 : -r;
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+#pragma unroll
+                for (int j = 0; j < TN; j++) {
+                    const int32_t v = acc[i][j][e];
+                    int32_t c = r > 0 ? ((v >> rs) + 1) >> 1 : v << ls;
+                    c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                    T[(16 * i + e) * RB8 + 16 * j] = (int8_t)c;
+                }
+        __syncthreads();
+        if (oy < a.Ho) {
+            // wave w stores tile row w: chunk (pixel lane / 4 + 16 u, channels 16 (lane % 4) ..)
+            const int8_t* T0 = smem + (wave * TW + (lane >> 2)) * RB8 + (lane & 3) * 16;
+            int8_t* g = a.out8 + ((rowbase + ox0 + (lane >> 2)) * a.Nout + k0 + (lane & 3) * 16);
+#pragma unroll
+            for (int u = 0; u < TW / 16; u++)
+                if ((lane >> 2) + 16 * u < vcols)
+                    *(int4*)(g + (int64_t)16 * u * a.Nout) = *(const int4*)&T0[16 * u * RB8];
+        }
+        return;
+    }
+    __shared__ uint32_t wmax[4];
+    // tile max |acc| via running max and min (max3/min3 take two values per op)
+    int32_t vmax = 0, vmin = 0;
+    if (oy < a.Ho) {
+        if (vcols == TW) {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+#pragma unroll
+                    for (int j = 0; j < TN; j += 2) {
+                        vmax = max(vmax, max(acc[i][j][e], acc[i][j + 1][e]));
+                        vmin = min(vmin, min(acc[i][j][e], acc[i][j + 1][e]));
+                    }
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    if (16 * i + 4 * lpart + e < vcols) {
+#pragma unroll
+                        for (int j = 0; j < TN; j += 2) {
+                            vmax = max(vmax, max(acc[i][j][e], acc[i][j + 1][e]));
+                            vmin = min(vmin, min(acc[i][j][e], acc[i][j + 1][e]));
+                        }
+                    }
+        }
+    }
+    uint32_t mx = (uint32_t)max(vmax, -vmin);
+    mx = wave_max_u32(mx);
+    if (EPI == EPI_MAX) {
+        const uint64_t bm = block_max_u64(mx);
+        if (tid == 0) a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = bm;
+        return;
+    }
+    if (lane == 0) wmax[wave] = mx;
+    __syncthreads();                                      // also: all waves are done with the halo
+    uint32_t tmax = wmax[0];
+#pragma unroll
+    for (int w = 1; w < 4; w++) tmax = wmax[w] > tmax ? wmax[w] : tmax;
+    const int tsh = tmax ? max(0, 32 - __builtin_clz(tmax) - 15) : 0;
+    constexpr int RS16 = 64 + 8;
+    int16_t* T = (int16_t*)smem + (wave * TW + 4 * lpart) * RS16 + lrow;
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int e = 0; e < 4; e++)
+#pragma unroll
+            for (int j = 0; j < TN; j++) T[(16 * i + e) * RS16 + 16 * j] = (int16_t)(acc[i][j][e] >> tsh);
+    __syncthreads();
+    // wave w copies tile row w: 16-byte chunk (pixel lane / 8 + 8 u, channels 8 (lane % 8) ..)
+    if (oy < a.Ho) {
+        const int16_t* T0 = (const int16_t*)smem + (wave * TW + (lane >> 3)) * RS16 + (lane & 7) * 8;
+        int16_t* g = a.out16 + ((rowbase + ox0 + (lane >> 3)) * a.Nout + k0 + (lane & 7) * 8);
+#pragma unroll
+        for (int u = 0; u < TW / 8; u++)
+            if ((lane >> 3) + 8 * u < vcols)
+                *(int4*)(g + (int64_t)8 * u * a.Nout) = *(const int4*)&T0[8 * u * RS16];
+    }
+    if (tid == 0) {
+        a.tshift[(int64_t)bx * gridDim.y + blockIdx.y] = (uint8_t)tsh;
+        a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = tmax;
+    }
+}
+
+// weights [K][R][S][C] -> [C][R][S][K] with the taps reversed (backward-data as
+// a forward convolution over dy)
+__global__ void k_w_flip_transpose(const int8_t* __restrict__ w, int8_t* __restrict__ wt, int32_t K,
+                                   int32_t RS, int32_t C)
+{
+    const int64_t n = (int64_t)K * RS * C;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t k = (int32_t)(i % K);
+        const int64_t t = i / K;
+        const int32_t rs = (int32_t)(t % RS);
+        const int32_t c = (int32_t)(t / RS);
+        wt[i] = w[((int64_t)k * RS + (RS - 1 - rs)) * C + c];
+    }
+}
+
+// the halo kernel covers 3x3 filters at stride 1, dilation <= 2, Ci and Nout
+// multiples of 64, 16-byte aligned operands
+struct HaloPlan {
+    bool ok;
+    int TW;
+    int tiles_y, tiles_x;
+    size_t lds;
+};
+
+HaloPlan halo_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Ci, int64_t Nout, int R, int S, int sh, int sw,
+                   int dh, int dw)
+{
+    HaloPlan p{};
+    p.ok = N > 0 && R == 3 && S == 3 && sh == 1 && sw == 1 && dh <= 2 && dw <= 2 && Ci % 64 == 0 &&
+           Nout % 64 == 0 && N * Ho * Wo < ((int64_t)1 << 31);
+    if (!p.ok) return p;
+    // widest tile without a ragged column tile when the width allows it
+    p.TW = (Wo % 112 == 0) ? 112 : 64;
+    p.tiles_y = (int)ceil_div64(Ho, kHaloTH);
+    p.tiles_x = (int)ceil_div64(Wo, p.TW);
+    p.lds = halo_lds_bytes(p.TW, dh, dw);
+    p.ok = N * p.tiles_y * p.tiles_x < ((int64_t)1 << 31);
+    return p;
+}
+
+size_t halo_staged_ws_bytes(const HaloPlan& p, int64_t N, int64_t Ho, int64_t Wo, int64_t Nout)
+{
+    return align256((size_t)(N * Ho * Wo * Nout) * 2) +
+           align256((size_t)(N * p.tiles_y * p.tiles_x * (Nout / 64)));
+}
+
+template <int TW, int EPI>
+int launch_halo_t(const HaloPlan& p, const HaloArgs& a, int kid, hipStream_t s)
+{
+    dim3 grid((unsigned)(a.N * p.tiles_y * p.tiles_x), (unsigned)(a.Nout / 64));
+    if (hipFuncSetAttribute((const void*)k_conv3x3_halo<TW, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)p.lds) != hipSuccess)
+        return ISEG_ERR_DEVICE;
+    ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_halo<TW, EPI>), grid, dim3(256), p.lds, s, a);
+    return launch_ok();
+}
+
+int launch_halo(const HaloPlan& p, HaloArgs a, int epi, int kid, hipStream_t s)
+{
+    a.tiles_y = p.tiles_y;
+    a.tiles_x = p.tiles_x;
+    if (p.TW == 112) {
+        switch (epi) {
+        case EPI_RAW: return launch_halo_t<112, EPI_RAW>(p, a, kid, s);
+        case EPI_STAGE16: return launch_halo_t<112, EPI_STAGE16>(p, a, kid, s);
+        case EPI_MAX: return launch_halo_t<112, EPI_MAX>(p, a, kid, s);
+        default: return launch_halo_t<112, EPI_Q8>(p, a, kid, s);
+        }
+    }
+    switch (epi) {
+    case EPI_RAW: return launch_halo_t<64, EPI_RAW>(p, a, kid, s);
+    case EPI_STAGE16: return launch_halo_t<64, EPI_STAGE16>(p, a, kid, s);
+    case EPI_MAX: return launch_halo_t<64, EPI_MAX>(p, a, kid, s);
+    default: return launch_halo_t<64, EPI_Q8>(p, a, kid, s);
+    }
+}
+
+// Q8 output through the halo kernel: for short reductions (Ci <= kTwoPassMaxCi)
+// a max-only pass and a recomputing pass that writes final codes, else int16
+// staging plus a requant pass.  The recompute costs 9 Ci MACs per output while
+// staging moves 4 more bytes per output through HBM.
+constexpr int kTwoPassMaxCi = 128;
+
+int halo_q8(const HaloPlan& p, HaloArgs h, int kid, const int32_t* exp_a, const int32_t* exp_b, int8_t* out,
+            int32_t* out_exp, unsigned long long* maxp, uint64_t* pmax, int64_t rows, hipStream_t s)
+{
+    int rc;
+    h.pmax = pmax;
+    h.npmax = (int64_t)h.N * p.tiles_y * p.tiles_x * (h.Nout / 64);
+    if (h.Ci <= kTwoPassMaxCi) {
+        if ((rc = launch_halo(p, h, EPI_MAX, kid, s))) return rc;
+        h.out8 = out; h.exp_a = exp_a; h.exp_b = exp_b; h.out_exp = out_exp;
+        return launch_halo(p, h, EPI_Q8, kid, s);
+    }
+    if ((rc = launch_halo(p, h, EPI_STAGE16, kid, s))) return rc;
+    if ((rc = launch_reduce_max(pmax, h.npmax, maxp, s))) return rc;
+    StageMap sm{0, 64, h.Ho, h.Wo, kHaloTH, p.TW, p.tiles_y, p.tiles_x};
+    return launch_requant_staged16(h.out16, h.tshift, rows, h.Nout, sm, exp_a, exp_b, 8, out, out_exp, maxp, s);
+}
+
+// the direct-to-LDS kernel covers Ci % 64 == 0, Nout % 64 == 0, 16-byte
+// aligned operands and fewer than 2^31 rows; its int16-staged output is used
+// whenever the result is requantized
+bool igemm_dma_ok(const IgemmArgs& a)
+{
+    return a.Mrows > 0 && a.Mrows < ((int64_t)1 << 31) && a.Ci % 64 == 0 && a.Nout % 64 == 0 &&
+           (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0;
+}
+int igemm_dma_bn(const IgemmArgs& a) { return a.Nout % 128 == 0 ? 128 : 64; }
+size_t staged_ws_bytes(int64_t rows, int64_t cols)
+{
+    return align256((size_t)(rows * cols) * 2) + align256((size_t)(ceil_div64(rows, 128) * ceil_div64(cols, 64)));
 }
 
 template <int MODE>
-int launch_igemm(const IgemmArgs& a, hipStream_t s)
+int launch_igemm(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
 {
+    *nblk = 0;
     if (a.Mrows > 0 && a.Nout > 0 && a.Ci % 64 == 0 &&
         (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0) {
         const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
         unsigned gx = (unsigned)ceil_div64(a.Mrows, 128);
+        if (igemm_dma_ok(a)) {
+            const bool o16 = a.out16 != nullptr;
+            if (a.Nout % 128 == 0) {
+                dim3 grid(gx, (unsigned)(a.Nout / 128));
+                const size_t lds = kStages * (128 + 128) * 64;
+                if (o16) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 128, true>), grid, dim3(256), lds, s, a);
+                else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 128, false>), grid, dim3(256), lds, s, a);
+                *nblk = (int64_t)grid.x * grid.y;
+            } else {
+                dim3 grid(gx, (unsigned)(a.Nout / 64));
+                const size_t lds = kStages * (128 + 64) * 64;
+                if (o16) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 64, true>), grid, dim3(256), lds, s, a);
+                else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 64, false>), grid, dim3(256), lds, s, a);
+                *nblk = (int64_t)grid.x * grid.y;
+            }
+            return launch_ok();
+        }
         if (a.Nout > 64) {
             dim3 grid(gx, (unsigned)ceil_div64(a.Nout, 128));
             ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_tap<MODE, 128, 128>), grid, dim3(256), 0, s, a);
+            *nblk = (int64_t)grid.x * grid.y;
         } else {
             ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_tap<MODE, 128, 64>), dim3(gx, 1), dim3(256), 0, s, a);
+            *nblk = gx;
         }
         return launch_ok();
     }
-    return launch_igemm_generic<MODE>(a, s);
+    return launch_igemm_generic<MODE>(a, s, nblk);
 }
 
 template <int MODE>
-int launch_igemm_generic(const IgemmArgs& a, hipStream_t s)
+int launch_igemm_generic(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
 {
+    *nblk = 0;
     if (a.Mrows <= 0 || a.Nout <= 0) return ISEG_OK;
     bool vec = (a.Ci % 16) == 0 && (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0;
     dim3 block(256);
@@ -351,10 +961,12 @@ int launch_igemm_generic(const IgemmArgs& a, hipStream_t s)
         dim3 grid(gx, (unsigned)ceil_div64(a.Nout, 128));
         if (vec) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, true, 128, 128>), grid, block, 0, s, a);
         else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, false, 128, 128>), grid, block, 0, s, a);
+        *nblk = (int64_t)grid.x * grid.y;
     } else {
         dim3 grid(gx, 1);
         if (vec) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, true, 128, 64>), grid, block, 0, s, a);
         else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm<MODE, false, 128, 64>), grid, block, 0, s, a);
+        *nblk = gx;
     }
     return launch_ok();
 }
@@ -1159,12 +1771,34 @@ bool geom_ok(const iseg_conv_geom* g, int64_t* P, int64_t* Q)
 // ---------------------------------------------------------------------------
 // C ABI
 // ---------------------------------------------------------------------------
+// room for per-block max partials of any path the output of rows x cols can take
+size_t conv_pmax_bytes(int64_t rows, int64_t cols, const HaloPlan& hp, int64_t N)
+{
+    int64_t nb = ceil_div64(rows, 128) * ceil_div64(cols, 64);
+    if (hp.ok) {
+        const int64_t nh = N * hp.tiles_y * hp.tiles_x * (cols / 64);
+        nb = nb > nh ? nb : nh;
+    }
+    return align256((size_t)nb * 8);
+}
+
 extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
 {
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
     size_t s = 256;
-    if (out_mode == ISEG_OUT_Q8) s += align256((size_t)(g->N * P * Q * g->K) * 4);
+    if (out_mode == ISEG_OUT_Q8) {
+        size_t big = align256((size_t)(g->N * P * Q * g->K) * 4);
+        const size_t s16 = staged_ws_bytes(g->N * P * Q, g->K);
+        big = big > s16 ? big : s16;
+        const HaloPlan hp = halo_plan(g->N, P, Q, g->C, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                      g->dil_h, g->dil_w);
+        if (hp.ok) {
+            const size_t sh = halo_staged_ws_bytes(hp, g->N, P, Q, g->K);
+            big = big > sh ? big : sh;
+        }
+        s += big + conv_pmax_bytes(g->N * P * Q, g->K, hp, g->N);
+    }
     int64_t Cp = padded_c(g->C);
     if (Cp != g->C)
         s += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp));
@@ -1182,17 +1816,29 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     if (!x_exp || !w_exp || !y_exp || (g->N > 0 && (!x || !w || !y))) return ISEG_ERR_ARG;
     if (g->C * g->R * g->S > kMaxKred) return ISEG_ERR_UNSUPPORTED;
     if (!ws || ws_bytes < iseg_conv_fwd_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
+    // ws: [max][per-block max partials][output staging][padded operands]
     unsigned long long* maxp = (unsigned long long*)ws;
+    const int64_t Cp = padded_c(g->C);
+    const HaloPlan hp = halo_plan(g->N, P, Q, Cp, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                  g->dil_h, g->dil_w);
     char* wp = (char*)ws + 256;
+    uint64_t* pmax = nullptr;
     int32_t* acc = (int32_t*)y;
     if (out_mode == ISEG_OUT_Q8) {
+        pmax = (uint64_t*)wp;
+        wp += conv_pmax_bytes(g->N * P * Q, g->K, hp, g->N);
         acc = (int32_t*)wp;
-        wp += align256((size_t)(g->N * P * Q * g->K) * 4);
+        size_t big = align256((size_t)(g->N * P * Q * g->K) * 4);
+        const size_t s16 = staged_ws_bytes(g->N * P * Q, g->K);
+        big = big > s16 ? big : s16;
+        if (hp.ok) {
+            const size_t sh = halo_staged_ws_bytes(hp, g->N, P, Q, g->K);
+            big = big > sh ? big : sh;
+        }
+        wp += big;
     }
-    int rc = launch_fill_u32(maxp, 2, 0, stream);
-    if (rc) return rc;
+    int rc;
     // small C: zero-pad channels to a multiple of 16 for the vector path
-    const int64_t Cp = padded_c(g->C);
     const int8_t* xs = x;
     const int8_t* wsrc = w;
     if (Cp != g->C) {
@@ -1205,17 +1851,45 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         wsrc = wpd;
     }
     IgemmArgs a;
-    a.src = xs; a.wmat = wsrc; a.out = acc; a.maxp = out_mode == ISEG_OUT_Q8 ? maxp : nullptr;
+    a.src = xs; a.wmat = wsrc; a.out = acc; a.pmax = pmax;
+    a.out16 = nullptr; a.tshift = nullptr;
     a.Mrows = g->N * P * Q;
     a.Nout = (int32_t)g->K; a.Kred = (int32_t)(Cp * g->R * g->S); a.Ci = (int32_t)Cp;
     a.Hs = (int32_t)g->H; a.Ws = (int32_t)g->W; a.Ho = (int32_t)P; a.Wo = (int32_t)Q;
     a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
-    if ((rc = launch_igemm<MODE_FWD>(a, stream))) return rc;
+    if (hp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y | (uintptr_t)acc) & 15) == 0) {
+        HaloArgs h{};
+        h.src = xs; h.wmat = wsrc; h.out = acc;
+        h.out16 = out_mode == ISEG_OUT_Q8 ? (int16_t*)acc : nullptr;
+        h.tshift = (uint8_t*)acc + align256((size_t)(a.Mrows * a.Nout) * 2);
+        h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)Cp;
+        h.Ho = (int32_t)P; h.Wo = (int32_t)Q; h.Nout = (int32_t)g->K;
+        h.ph = g->pad_h; h.pw = g->pad_w; h.dh = g->dil_h; h.dw = g->dil_w;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_halo(hp, h, EPI_RAW, ISEG_KID_CONV_FWD, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
+            return launch_ok();
+        }
+        return halo_q8(hp, h, ISEG_KID_CONV_FWD, x_exp, w_exp, (int8_t*)y, y_exp, maxp, pmax, a.Mrows, stream);
+    }
+    const bool staged = out_mode == ISEG_OUT_Q8 && igemm_dma_ok(a) && ((uintptr_t)y & 15) == 0;
+    if (staged) {
+        a.out16 = (int16_t*)acc;
+        a.tshift = (uint8_t*)acc + align256((size_t)(a.Mrows * a.Nout) * 2);
+    }
+    int64_t nblk = 0;
+    if ((rc = launch_igemm<MODE_FWD>(a, stream, &nblk))) return rc;
     if (out_mode == ISEG_OUT_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
         return launch_ok();
+    }
+    if ((rc = launch_reduce_max(pmax, nblk, maxp, stream))) return rc;
+    if (staged) {
+        StageMap sm{128, igemm_dma_bn(a), 0, 0, 0, 0, 0, 0};
+        return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, x_exp, w_exp, 8, (int8_t*)y, y_exp,
+                                       maxp, stream);
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, x_exp, w_exp, 0, 8, 0, 1,
                                 0, 0, 0, ISEG_I8, y, y_exp, maxp, stream);
@@ -1226,7 +1900,18 @@ extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mod
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
     size_t s = 256 + align256((size_t)(g->K * g->R * g->S * g->C));
-    if (out_mode == ISEG_OUT_Q8) s += align256((size_t)(g->N * g->H * g->W * g->C) * 4);
+    if (out_mode == ISEG_OUT_Q8) {
+        size_t big = align256((size_t)(g->N * g->H * g->W * g->C) * 4);
+        const size_t s16 = staged_ws_bytes(g->N * g->H * g->W, g->C);
+        big = big > s16 ? big : s16;
+        const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h,
+                                      g->stride_w, g->dil_h, g->dil_w);
+        if (hp.ok) {
+            const size_t sh = halo_staged_ws_bytes(hp, g->N, g->H, g->W, g->C);
+            big = big > sh ? big : sh;
+        }
+        s += big + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N);
+    }
     return s;
 }
 
@@ -1242,28 +1927,70 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     if (!dy_exp || !w_exp || !dx_exp || (g->N > 0 && (!dy || !w || !dx))) return ISEG_ERR_ARG;
     if (g->K * g->R * g->S > kMaxKred) return ISEG_ERR_UNSUPPORTED;
     if (!ws || ws_bytes < iseg_conv_bwd_data_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
+    // ws: [max][transposed weights][per-block max partials][output staging]
     unsigned long long* maxp = (unsigned long long*)ws;
+    const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                  g->dil_h, g->dil_w);
     int8_t* wt = (int8_t*)ws + 256;
-    size_t wt_bytes = align256((size_t)(g->K * g->R * g->S * g->C));
-    int32_t* acc = out_mode == ISEG_OUT_Q8 ? (int32_t*)((char*)ws + 256 + wt_bytes) : (int32_t*)dx;
-    int rc = launch_fill_u32(maxp, 2, 0, stream);
-    if (rc) return rc;
+    const size_t wt_bytes = align256((size_t)(g->K * g->R * g->S * g->C));
+    uint64_t* pmax = nullptr;
+    int32_t* acc = (int32_t*)dx;
+    if (out_mode == ISEG_OUT_Q8) {
+        pmax = (uint64_t*)((char*)ws + 256 + wt_bytes);
+        acc = (int32_t*)((char*)pmax + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N));
+    }
+    int rc;
     int64_t nw = g->K * g->R * g->S * g->C;
+    if (hp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx | (uintptr_t)acc) & 15) == 0) {
+        // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
+        hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
+                           (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
+        if ((rc = launch_ok())) return rc;
+        HaloArgs h{};
+        h.src = dy; h.wmat = wt; h.out = acc;
+        const int64_t rows = g->N * g->H * g->W;
+        h.out16 = out_mode == ISEG_OUT_Q8 ? (int16_t*)acc : nullptr;
+        h.tshift = (uint8_t*)acc + align256((size_t)(rows * g->C) * 2);
+        h.N = (int32_t)g->N; h.Hs = (int32_t)P; h.Ws = (int32_t)Q; h.Ci = (int32_t)g->K;
+        h.Ho = (int32_t)g->H; h.Wo = (int32_t)g->W; h.Nout = (int32_t)g->C;
+        h.ph = g->dil_h * (int32_t)(g->R - 1) - g->pad_h; h.pw = g->dil_w * (int32_t)(g->S - 1) - g->pad_w;
+        h.dh = g->dil_h; h.dw = g->dil_w;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_halo(hp, h, EPI_RAW, ISEG_KID_CONV_BWD_DATA, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
+            return launch_ok();
+        }
+        return halo_q8(hp, h, ISEG_KID_CONV_BWD_DATA, dy_exp, w_exp, (int8_t*)dx, dx_exp, maxp, pmax, rows,
+                       stream);
+    }
     hipLaunchKernelGGL(k_w_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
                        (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
     if ((rc = launch_ok())) return rc;
     IgemmArgs a;
-    a.src = dy; a.wmat = wt; a.out = acc; a.maxp = out_mode == ISEG_OUT_Q8 ? maxp : nullptr;
+    a.src = dy; a.wmat = wt; a.out = acc; a.pmax = pmax;
+    a.out16 = nullptr; a.tshift = nullptr;
     a.Mrows = g->N * g->H * g->W;
     a.Nout = (int32_t)g->C; a.Kred = (int32_t)(g->K * g->R * g->S); a.Ci = (int32_t)g->K;
     a.Hs = (int32_t)P; a.Ws = (int32_t)Q; a.Ho = (int32_t)g->H; a.Wo = (int32_t)g->W;
     a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
-    if ((rc = launch_igemm<MODE_BWD>(a, stream))) return rc;
+    const bool staged = out_mode == ISEG_OUT_Q8 && igemm_dma_ok(a) && ((uintptr_t)dx & 15) == 0;
+    if (staged) {
+        a.out16 = (int16_t*)acc;
+        a.tshift = (uint8_t*)acc + align256((size_t)(a.Mrows * a.Nout) * 2);
+    }
+    int64_t nblk = 0;
+    if ((rc = launch_igemm<MODE_BWD>(a, stream, &nblk))) return rc;
     if (out_mode == ISEG_OUT_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
         return launch_ok();
+    }
+    if ((rc = launch_reduce_max(pmax, nblk, maxp, stream))) return rc;
+    if (staged) {
+        StageMap sm{128, igemm_dma_bn(a), 0, 0, 0, 0, 0, 0};
+        return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, dy_exp, w_exp, 8, (int8_t*)dx,
+                                       dx_exp, maxp, stream);
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, dy_exp, w_exp, 0, 8, 0, 1,
                                 0, 0, 0, ISEG_I8, dx, dx_exp, maxp, stream);

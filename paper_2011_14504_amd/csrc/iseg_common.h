@@ -166,6 +166,47 @@ __device__ __forceinline__ void block_atomic_max_u64(uint64_t v, unsigned long l
     }
 }
 
+// Device-scope atomics to one address serialize across the chip (several ns
+// each), so grid-wide maxima are formed from per-block partials instead:
+// block b stores its maximum into part[b] and the consumer reduces them.
+__device__ __forceinline__ uint64_t block_max_u64(uint64_t v)
+{
+    __shared__ uint64_t red_bm[16];
+    v = wave_max_u64(v);
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    __syncthreads();                      // red_bm may still be read by a previous call
+    if (lane == 0) red_bm[wid] = v;
+    __syncthreads();
+    uint64_t m = 0;
+    const int nw = (blockDim.x + 63) >> 6;
+    for (int i = 0; i < nw; i++) m = red_bm[i] > m ? red_bm[i] : m;
+    return m;
+}
+
+// block max of v stored (plain store) into part[linear block index]
+__device__ __forceinline__ void block_store_max_u64(uint64_t v, uint64_t* part)
+{
+    const uint64_t m = block_max_u64(v);
+    if (threadIdx.x == 0) part[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = m;
+}
+
+// max over n partials, computed by the whole block (every thread gets it)
+__device__ __forceinline__ uint64_t reduce_partials_u64(const uint64_t* part, int64_t n)
+{
+    uint64_t m = 0;
+    for (int64_t base = 0; base < n; base += 8 * (int64_t)blockDim.x) {
+        uint64_t v[8];                    // eight loads in flight per thread
+#pragma unroll
+        for (int k = 0; k < 8; k++) {
+            const int64_t i = base + k * (int64_t)blockDim.x + threadIdx.x;
+            v[k] = i < n ? part[i] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < 8; k++) m = v[k] > m ? v[k] : m;
+    }
+    return block_max_u64(m);
+}
+
 __device__ __forceinline__ void set_status(int32_t* st, int32_t bits)
 {
     if (st) atomicOr(st, bits);
@@ -195,6 +236,16 @@ __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v);
 
 // device-side requant of an integer buffer whose max |.| is already in *maxp;
 // the input exponent is *exp_a + *exp_b + exp_add (NULL pointers count as 0)
+// tiling of an int16-staged [rows][cols] conv output: row tiles are runs of
+// tile_rows rows (th == 0) or th x tw pixel tiles of Ho x Wo images
+struct StageMap {
+    int32_t tile_rows, tile_cols;
+    int32_t Ho, Wo, th, tw, tiles_y, tiles_x;
+};
+// requant of int16-staged conv sums (per-tile shifts) to int8 SQ codes
+int launch_requant_staged16(const int16_t* in, const uint8_t* tshift, int64_t rows, int32_t cols,
+                            const StageMap& sm, const int32_t* exp_a, const int32_t* exp_b, int bits,
+                            int8_t* out, int32_t* out_exp, const unsigned long long* maxp, hipStream_t s);
 int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t* exp_a,
                          const int32_t* exp_b, int32_t exp_add, int bits, int stochastic,
                          int keep_scale,
@@ -207,6 +258,8 @@ int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* m
                   int32_t* dev_status, hipStream_t s);
 
 int launch_fill_u32(void* p, int64_t n_words, uint32_t v, hipStream_t s);
+// *maxp = max over n block partials (one block)
+int launch_reduce_max(const uint64_t* part, int64_t n, unsigned long long* maxp, hipStream_t s);
 
 // measurement hook (iseg_profile_arm): wrap one kernel launch
 bool prof_begin(int kid, hipStream_t s);

@@ -91,6 +91,19 @@ int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* m
     return launch_ok();
 }
 
+__global__ __launch_bounds__(1024) void k_reduce_max(const uint64_t* __restrict__ part, int64_t n,
+                                                     unsigned long long* maxp)
+{
+    const uint64_t m = reduce_partials_u64(part, n);
+    if (threadIdx.x == 0) *maxp = m;
+}
+
+int launch_reduce_max(const uint64_t* part, int64_t n, unsigned long long* maxp, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_reduce_max, dim3(1), dim3(1024), 0, s, part, n, maxp);
+    return launch_ok();
+}
+
 // ---------------------------------------------------------------------------
 // requant apply: SQ half-up or RQ stochastic with r = bitlen(max) - (bits-1)
 // ---------------------------------------------------------------------------
@@ -198,6 +211,81 @@ int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t*
                            dim3(256), 0, s, (const int64_t*)in, (int16_t*)out, a);
     else
         return ISEG_ERR_ARG;
+    return launch_ok();
+}
+
+// ---------------------------------------------------------------------------
+// requant of int16-staged sums: element (m, n) of a [rows][cols] tensor holds
+// floor(acc / 2^t) with t = tshift of its tile (rows in runs of tile_rows, or
+// 2-D th x tw pixel tiles of an image when th > 0; tile_cols columns)
+// and t <= r - 1 whenever t > 0, so the half-up code of acc by r is the half-up
+// code of the staged value by r - t: ((y >> (r - 1 - t)) + 1) >> 1, clamped.
+// 16 elements per thread step (cols % 16 == 0, all in one tile).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int32_t clamp_k32(int32_t v, int k)
+{
+    const int32_t lim = (1 << (k - 1)) - 1;
+    return v > lim ? lim : (v < -lim ? -lim : v);
+}
+
+__global__ __launch_bounds__(256) void k_requant_s16_i8(const int16_t* __restrict__ in,
+                                                        const uint8_t* __restrict__ tshift, int64_t rows,
+                                                        int32_t cols, StageMap sm, int8_t* __restrict__ out,
+                                                        RqArgs a)
+{
+    const uint64_t M = *a.maxp;
+    const int r = rq_shift(a, M);
+    rq_write_exp(a, M, r);
+    const int32_t cpr = cols >> 4;                        // 16-element chunks per row
+    const int32_t tpr = cols / sm.tile_cols;              // column tiles
+    const int64_t nch = rows * cpr;
+    const int64_t hw = (int64_t)sm.Ho * sm.Wo;
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nch;
+         j += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t m = j / cpr;
+        const int32_t n = (int32_t)(j - m * cpr) << 4;
+        int64_t rt;                                       // row-tile index of row m
+        if (sm.th == 0) {
+            rt = m / sm.tile_rows;
+        } else {                                          // 2-D pixel tiles of th x tw
+            const int64_t img = m / hw;
+            const int32_t rem = (int32_t)(m - img * hw);
+            const int32_t oy = rem / sm.Wo, ox = rem - (rem / sm.Wo) * sm.Wo;
+            rt = (img * sm.tiles_y + oy / sm.th) * sm.tiles_x + ox / sm.tw;
+        }
+        const int t = tshift[rt * tpr + n / sm.tile_cols];
+        const int4 v0 = ((const int4*)in)[2 * j], v1 = ((const int4*)in)[2 * j + 1];
+        const uint32_t h[8] = {(uint32_t)v0.x, (uint32_t)v0.y, (uint32_t)v0.z, (uint32_t)v0.w,
+                               (uint32_t)v1.x, (uint32_t)v1.y, (uint32_t)v1.z, (uint32_t)v1.w};
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            uint32_t o = 0;
+#pragma unroll
+            for (int b = 0; b < 4; b++) {
+                const uint32_t hw = h[(4 * q + b) >> 1];
+                const int32_t y = (int32_t)(int16_t)(((4 * q + b) & 1) ? (hw >> 16) : (hw & 0xffff));
+                const int32_t c = r > 0 ? (((y >> (r - 1 - t)) + 1) >> 1) : (y << -r);
+                o |= (uint32_t)(uint8_t)clamp_k32(c, a.bits) << (8 * b);
+            }
+            w[q] = o;
+        }
+        ((int4*)out)[j] = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
+    }
+}
+
+int launch_requant_staged16(const int16_t* in, const uint8_t* tshift, int64_t rows, int32_t cols,
+                            const StageMap& sm, const int32_t* exp_a, const int32_t* exp_b, int bits,
+                            int8_t* out, int32_t* out_exp, const unsigned long long* maxp, hipStream_t s)
+{
+    RqArgs a;
+    a.n = rows * cols; a.exp_a = exp_a; a.exp_b = exp_b; a.exp_add = 0;
+    a.bits = bits; a.stochastic = 0; a.keep_scale = 1;
+    a.seed = 0; a.tensor_id = 0; a.step = 0;
+    a.out_exp = out_exp; a.maxp = maxp;
+    if (cols % 16 || sm.tile_cols % 16 || (((uintptr_t)in | (uintptr_t)out) & 15)) return ISEG_ERR_ARG;
+    ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_s16_i8, dim3(grid_for(rows * cols, 256 * 16, 8192)), dim3(256),
+                      0, s, in, tshift, rows, cols, sm, out, a);
     return launch_ok();
 }
 
