@@ -795,6 +795,728 @@ __global__ __launch_bounds__(256) void k_conv3x3_halo(HaloArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// 3x3 stride-1 convolution on v_mfma_i32_32x32x32_i8 (Ci % 64 == 0, Nout % 64
+// == 0, dilation 1 or 2).  The 16x16x64 i8 MFMA issues at half the rate of the
+// 32x32x32 form on gfx950, so this is the main path.
+//
+// A block owns a 16 x 32 output tile of one image and 64 output channels.  An
+// A fragment is 32 pixels = 2 rows x 16 columns; wave w computes rows 4w..4w+3
+// (four fragments) for all 64 channels (two B fragments): per tap and
+// 32-channel half, 4 x 2 MFMAs from 6 LDS reads.  The halo (16 + 2 dh rows x
+// 32 + 2 dw columns, one 64-channel chunk) and the 9 x 64 x 64 weight chunk
+// are staged by direct-to-LDS loads.  Halo slots are swizzled by the column
+// (slot = part ^ ((column >> 2) & 3)), which keeps any 16 consecutive pixels
+// of a row conflict-free and leaves the swizzle unchanged by row offsets, so
+// the nine taps need only three per-lane base addresses.
+// ---------------------------------------------------------------------------
+constexpr int kM32TH = 16, kM32TW = 32;
+typedef int v16i_t __attribute__((ext_vector_type(16)));
+
+// The 18 (tap, 32-channel half) steps of one 64-channel chunk.  Fragments of
+// step k + 1 are read from LDS before the MFMAs of step k are issued (two
+// register sets, scheduling barriers between the groups), so a single wave
+// per SIMD keeps the matrix pipe fed instead of waiting on each LDS read.
+template <int DH, int HC, int TM, int TN>
+__device__ __forceinline__ void m32_taps(const int8_t* halo, const int8_t* w, const int (&abase)[3][2],
+                                         const int (&bbase)[TN][2], v16i_t (&acc)[TM][TN], bool first)
+{
+    v4i fa[2][TM], fb[2][TN];
+    auto load = [&](int k, int buf) {
+        const int t = k >> 1, kh = k & 1, r = t / 3, s2 = t - (t / 3) * 3;
+#pragma unroll
+        for (int i = 0; i < TM; i++)          // fragment i: row pair 2 wave + i / 2, column group i % 2
+            fa[buf][i] = *(const v4i*)&halo[abase[s2][kh] + (((i >> 1) * 2 + r * DH) * HC + 16 * (i & 1)) * 64];
+#pragma unroll
+        for (int j = 0; j < TN; j++) fb[buf][j] = *(const v4i*)&w[t * 4096 + bbase[j][kh]];
+    };
+    load(0, 0);
+#pragma unroll
+    for (int k = 0; k < 18; k++) {
+        if (k + 1 < 18) load(k + 1, (k + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        const int b = k & 1;
+        if (k == 0 && first) {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[b][i], fb[b][j], (v16i_t){}, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[b][i], fb[b][j], acc[i][j], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+
+template <int DH, int DW, int EPI>
+__global__ __launch_bounds__(256, 2) void k_conv3x3_m32(HaloArgs a)
+{
+    constexpr int TH = kM32TH, TW = kM32TW, HR = TH + 2 * DH, HC = TW + 2 * DW;
+    constexpr int TM = 4, TN = 2;
+    constexpr int NHALO = HR * HC * 4;                      // 16-byte pieces
+    constexpr int HBYTES = HR * HC * 64;
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+    int8_t* halo = smem;
+    int8_t* wts = smem + HBYTES;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nbx = gridDim.x;
+    int bx = blockIdx.x;
+    if ((nbx & 7) == 0) bx = (bx & 7) * (nbx >> 3) + (bx >> 3);
+    const int tx = bx % a.tiles_x, t2 = bx / a.tiles_x;
+    const int ty = t2 % a.tiles_y, n = t2 / a.tiles_y;
+    const int oy0 = ty * TH, ox0 = tx * TW, k0 = blockIdx.y * 64;
+    const int iy0 = oy0 - a.ph, ix0 = ox0 - a.pw;
+    const int l32 = lane & 31, khalf = lane >> 5;          // fragment row, 16-byte half of a 32-byte k slice
+    const int lr = l32 >> 4, lc = l32 & 15;                // row in the pair, column in the fragment
+
+    // A base address of fragment (row pair 2 wave, column group 0) for column tap s and k half kh:
+    // fragment (rp, cg), tap (r, s) adds ((2 rp + r DH) HC + 16 cg) * 64 (compile-time)
+    int abase[3][2];
+#pragma unroll
+    for (int s2 = 0; s2 < 3; s2++)
+#pragma unroll
+        for (int kh = 0; kh < 2; kh++) {
+            const int hc = lc + s2 * DW, part = 2 * kh + khalf;
+            abase[s2][kh] = ((4 * wave + lr) * HC + hc) * 64 + ((part ^ ((hc >> 2) & 3)) << 4);
+        }
+    int bbase[TN][2];
+#pragma unroll
+    for (int j = 0; j < TN; j++)
+#pragma unroll
+        for (int kh = 0; kh < 2; kh++) {
+            const int kk = 32 * j + l32, part = 2 * kh + khalf;
+            bbase[j][kh] = kk * 64 + ((part ^ ((kk >> 2) & 3)) << 4);
+        }
+    // halo pieces: instruction k = wave + 4 u holds pixels 16 k .. 16 k + 15
+    const int p0 = 16 * wave + (lane >> 2);
+    const int hr0 = p0 / HC, hc0 = p0 - (p0 / HC) * HC;
+    const int wkk = 16 * wave + (lane >> 2);
+    const int wpart = (lane & 3) ^ ((wkk >> 2) & 3);
+    const int8_t* wsrc = a.wmat + (int64_t)(k0 + wkk) * 9 * a.Ci + wpart * 16;
+
+    v16i_t acc[TM][TN];
+    const int nchunk = a.Ci / 64;
+    uint64_t gmax = 0;
+    for (int cc = 0; cc < nchunk; cc++) {
+        if (cc) __syncthreads();                            // the previous chunk's reads are done
+        {
+            int hr = hr0, hc = hc0;
+#pragma unroll
+            for (int k = wave, u = 0; u < (NHALO / 64 + 4) / 4; u++, k += 4) {
+                const int q = k * 64 + lane;
+                if (q < NHALO) {
+                    const int part = (q & 3) ^ ((hc >> 2) & 3);
+                    const int iy = iy0 + hr, ix = ix0 + hc;
+                    const bool v = (unsigned)iy < (unsigned)a.Hs && (unsigned)ix < (unsigned)a.Ws;
+                    const void* g = v ? (const void*)(a.src + (((int64_t)n * a.Hs + iy) * a.Ws + ix) * a.Ci +
+                                                      cc * 64 + part * 16)
+                                      : (const void*)g_conv_zero;
+                    dma16(g, halo + k * 1024);
+                }
+                hc += 64;
+                while (hc >= HC) { hc -= HC; ++hr; }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 9; j++)
+            dma16(wsrc + (int64_t)j * a.Ci + cc * 64, wts + (wave + 4 * j) * 1024);
+        if (EPI == EPI_Q8 && cc == 0) gmax = reduce_partials_u64(a.pmax, a.npmax);
+        wait_vm<0>();
+        __syncthreads();
+        m32_taps<DH, HC, TM, TN>(halo, wts, abase, bbase, acc, cc == 0);
+    }
+
+    // acc[i][j][v]: fragment i (rows 4 wave + 2 (i / 2) + q / 16, columns 16 (i % 2) + q % 16 with
+    // q = 8 (v / 4) + 4 khalf + v % 4), channel k0 + 32 j + l32
+    auto px_row = [&](int i, int v) { return 4 * wave + 2 * (i >> 1) + ((8 * (v >> 2) + 4 * khalf + (v & 3)) >> 4); };
+    auto px_col = [&](int i, int v) { return 16 * (i & 1) + ((8 * (v >> 2) + 4 * khalf + (v & 3)) & 15); };
+    const int vrows = a.Ho - oy0 < TH ? a.Ho - oy0 : TH;
+    const int vcols = a.Wo - ox0 < TW ? a.Wo - ox0 : TW;
+    if (EPI == EPI_RAW) {
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int v = 0; v < 16; v++) {
+                const int ry = px_row(i, v), rx = px_col(i, v);
+                if (ry < vrows && rx < vcols) {
+                    const int64_t pix = ((int64_t)n * a.Ho + oy0 + ry) * a.Wo + ox0 + rx;
+#pragma unroll
+                    for (int j = 0; j < TN; j++) a.out[pix * a.Nout + k0 + 32 * j + l32] = acc[i][j][v];
+                }
+            }
+        return;
+    }
+    if (EPI == EPI_MAX) {
+        int32_t vmax = 0, vmin = 0;
+        const bool full = vrows == TH && vcols == TW;
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int v = 0; v < 16; v++)
+                if (full || (px_row(i, v) < vrows && px_col(i, v) < vcols)) {
+                    vmax = max(vmax, max(acc[i][0][v], acc[i][1][v]));
+                    vmin = min(vmin, min(acc[i][0][v], acc[i][1][v]));
+                }
+        const uint64_t bm = block_max_u64((uint32_t)max(vmax, -vmin));
+        if (tid == 0) a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = bm;
+        return;
+    }
+    // EPI_Q8: final SQ codes with r = bitlen(global max) - 7, staged per pixel row of 64 codes
+    const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+    const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+    constexpr int RB8 = 64 + 16;
+    __syncthreads();                                        // every wave is done with the halo
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int v = 0; v < 16; v++) {
+            const int px = px_row(i, v) * TW + px_col(i, v);
+#pragma unroll
+            for (int j = 0; j < TN; j++) {
+                const int32_t x = acc[i][j][v];
+                int32_t c = rq > 0 ? ((x >> rs) + 1) >> 1 : x << ls;
+                c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                smem[px * RB8 + 32 * j + l32] = (int8_t)c;
+            }
+        }
+    __syncthreads();
+    // 512 pixels x 4 chunks of 16 codes: thread -> chunk (pixel c / 4, part c % 4)
+#pragma unroll
+    for (int u = 0; u < TH * TW * 4 / 256; u++) {
+        const int c = tid + 256 * u;
+        const int px = c >> 2, part = c & 3;
+        const int ry = px / TW, rx = px % TW;
+        if (ry < vrows && rx < vcols)
+            *(int4*)(a.out8 + ((((int64_t)n * a.Ho + oy0 + ry) * a.Wo + ox0 + rx) * a.Nout + k0 + part * 16)) =
+                *(const int4*)&smem[px * RB8 + part * 16];
+    }
+}
+
+// Persistent form of the 32x32 kernel (Ci = 64 or 128): weights of all chunks
+// stay in LDS, the next (tile, chunk) halo streams into the second buffer
+// while the current one runs its taps, and a block walks a contiguous run of
+// tiles (neighbours share halo rows and sit on one XCD).  One block per CU.
+template <int DH, int DW, int EPI>
+__global__ __launch_bounds__(256, 1) void k_conv3x3_m32p(HaloArgs a)
+{
+    constexpr int TH = kM32TH, TW = kM32TW, HR = TH + 2 * DH, HC = TW + 2 * DW;
+    constexpr int TM = 4, TN = 2;
+    constexpr int NHALO = HR * HC * 4;
+    constexpr int RB8 = 64 + 16;
+    constexpr int HBUF = (HR * HC * 64 > TH * TW * RB8 ? HR * HC * 64 : TH * TW * RB8);
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+    const int nchunk = a.Ci / 64;
+    int8_t* wts = smem;                                     // [nchunk][9][64][64]
+    int8_t* hb = smem + nchunk * 36864;                     // two halo / staging buffers of HBUF bytes
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = gridDim.x;
+    int b = blockIdx.x;
+    if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
+    const int ntiles = a.N * a.tiles_y * a.tiles_x;
+    const int t_begin = (int)((int64_t)b * ntiles / G), t_end = (int)((int64_t)(b + 1) * ntiles / G);
+    const int nunits = (t_end - t_begin) * nchunk;
+    const int k0 = blockIdx.y * 64;
+    const int l32 = lane & 31, khalf = lane >> 5;
+    const int lr = l32 >> 4, lc = l32 & 15;
+
+    int abase[3][2];
+#pragma unroll
+    for (int s2 = 0; s2 < 3; s2++)
+#pragma unroll
+        for (int kh = 0; kh < 2; kh++) {
+            const int hc = lc + s2 * DW, part = 2 * kh + khalf;
+            abase[s2][kh] = ((4 * wave + lr) * HC + hc) * 64 + ((part ^ ((hc >> 2) & 3)) << 4);
+        }
+    int bbase[TN][2];
+#pragma unroll
+    for (int j = 0; j < TN; j++)
+#pragma unroll
+        for (int kh = 0; kh < 2; kh++) {
+            const int kk = 32 * j + l32, part = 2 * kh + khalf;
+            bbase[j][kh] = kk * 64 + ((part ^ ((kk >> 2) & 3)) << 4);
+        }
+    const int p0 = 16 * wave + (lane >> 2);
+    const int hr0 = p0 / HC, hc0 = p0 - (p0 / HC) * HC;
+
+    auto tile_origin = [&](int t, int& n, int& oy0, int& ox0) {
+        const int tx = t % a.tiles_x, t2 = t / a.tiles_x;
+        oy0 = (t2 % a.tiles_y) * TH;
+        n = t2 / a.tiles_y;
+        ox0 = tx * TW;
+    };
+    auto issue_halo = [&](int u) {
+        const int t = t_begin + u / nchunk, cc = u - (u / nchunk) * nchunk;
+        int n, oy0, ox0;
+        tile_origin(t, n, oy0, ox0);
+        const int iy0 = oy0 - a.ph, ix0 = ox0 - a.pw;
+        int8_t* dst = hb + (u & 1) * HBUF;
+        int hr = hr0, hc = hc0;
+#pragma unroll
+        for (int k = wave, v = 0; v < (NHALO / 64 + 4) / 4; v++, k += 4) {
+            const int q = k * 64 + lane;
+            if (q < NHALO) {
+                const int part = (q & 3) ^ ((hc >> 2) & 3);
+                const int iy = iy0 + hr, ix = ix0 + hc;
+                const bool ok = (unsigned)iy < (unsigned)a.Hs && (unsigned)ix < (unsigned)a.Ws;
+                const void* g = ok ? (const void*)(a.src + (((int64_t)n * a.Hs + iy) * a.Ws + ix) * a.Ci + cc * 64 +
+                                                   part * 16)
+                                   : (const void*)g_conv_zero;
+                dma16(g, dst + k * 1024);
+            }
+            hc += 64;
+            while (hc >= HC) { hc -= HC; ++hr; }
+        }
+    };
+
+    {
+        const int wkk = 16 * wave + (lane >> 2);
+        const int wpart = (lane & 3) ^ ((wkk >> 2) & 3);
+        const int8_t* wsrc = a.wmat + (int64_t)(k0 + wkk) * 9 * a.Ci + wpart * 16;
+        for (int cc = 0; cc < nchunk; cc++)
+#pragma unroll
+            for (int j = 0; j < 9; j++)
+                dma16(wsrc + (int64_t)j * a.Ci + cc * 64, wts + cc * 36864 + (wave + 4 * j) * 1024);
+    }
+    if (nunits > 0) issue_halo(0);
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);
+    const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+    wait_vm<0>();
+    __syncthreads();
+
+    v16i_t acc[TM][TN];
+    int32_t vmax = 0, vmin = 0;
+    for (int u = 0; u < nunits; u++) {
+        if (u + 1 < nunits) issue_halo(u + 1);
+        const int cc = u - (u / nchunk) * nchunk;
+        const int8_t* halo = hb + (u & 1) * HBUF;
+        const int8_t* w = wts + cc * 36864;
+        m32_taps<DH, HC, TM, TN>(halo, w, abase, bbase, acc, cc == 0);
+        if (cc == nchunk - 1) {
+            int n, oy0, ox0;
+            tile_origin(t_begin + u / nchunk, n, oy0, ox0);
+            const int vrows = a.Ho - oy0 < TH ? a.Ho - oy0 : TH;
+            const int vcols = a.Wo - ox0 < TW ? a.Wo - ox0 : TW;
+            auto px_row = [&](int i, int v) {
+                return 4 * wave + 2 * (i >> 1) + ((8 * (v >> 2) + 4 * khalf + (v & 3)) >> 4);
+            };
+            auto px_col = [&](int i, int v) { return 16 * (i & 1) + ((8 * (v >> 2) + 4 * khalf + (v & 3)) & 15); };
+            if (EPI == EPI_RAW) {
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int v = 0; v < 16; v++) {
+                        const int ry = px_row(i, v), rx = px_col(i, v);
+                        if (ry < vrows && rx < vcols) {
+                            const int64_t pix = ((int64_t)n * a.Ho + oy0 + ry) * a.Wo + ox0 + rx;
+#pragma unroll
+                            for (int j = 0; j < TN; j++) a.out[pix * a.Nout + k0 + 32 * j + l32] = acc[i][j][v];
+                        }
+                    }
+            } else if (EPI == EPI_MAX) {
+                const bool full = vrows == TH && vcols == TW;
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int v = 0; v < 16; v++)
+                        if (full || (px_row(i, v) < vrows && px_col(i, v) < vcols)) {
+                            vmax = max(vmax, max(acc[i][0][v], acc[i][1][v]));
+                            vmin = min(vmin, min(acc[i][0][v], acc[i][1][v]));
+                        }
+            } else {
+                const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+                int8_t* T = hb + (u & 1) * HBUF;            // this unit's halo buffer, now free
+                __syncthreads();                            // every wave is done reading it
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int v = 0; v < 16; v++) {
+                        const int px = px_row(i, v) * TW + px_col(i, v);
+#pragma unroll
+                        for (int j = 0; j < TN; j++) {
+                            const int32_t x = acc[i][j][v];
+                            int32_t c = rq > 0 ? ((x >> rs) + 1) >> 1 : x << ls;
+                            c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                            T[px * RB8 + 32 * j + l32] = (int8_t)c;
+                        }
+                    }
+                __syncthreads();
+#pragma unroll
+                for (int v = 0; v < TH * TW * 4 / 256; v++) {
+                    const int c = tid + 256 * v;
+                    const int px = c >> 2, part = c & 3;
+                    const int ry = px / TW, rx = px % TW;
+                    if (ry < vrows && rx < vcols)
+                        *(int4*)(a.out8 + ((((int64_t)n * a.Ho + oy0 + ry) * a.Wo + ox0 + rx) * a.Nout + k0 +
+                                           part * 16)) = *(const int4*)&T[px * RB8 + part * 16];
+                }
+            }
+        }
+        wait_vm<0>();                                       // the next unit's halo has landed
+        __syncthreads();
+    }
+    if (EPI == EPI_MAX) {
+        const uint64_t bm = block_max_u64((uint32_t)max(vmax, -vmin));
+        if (tid == 0) a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = bm;
+    }
+    if (EPI == EPI_Q8 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+}
+
+struct M32Plan {
+    bool ok;
+    int tiles_y, tiles_x;
+    size_t lds;
+    bool persist;                 // weights resident, double-buffered halos
+    int G;                        // persistent blocks per 64-channel group
+    size_t plds;
+};
+
+M32Plan m32_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Ci, int64_t Nout, int R, int S, int sh, int sw, int dh,
+                 int dw)
+{
+    M32Plan p{};
+    p.ok = N > 0 && R == 3 && S == 3 && sh == 1 && sw == 1 && dh >= 1 && dh <= 2 && dw >= 1 && dw <= 2 &&
+           Ci % 64 == 0 && Ci <= 128 && Nout % 64 == 0 && N * Ho * Wo < ((int64_t)1 << 31);
+    if (!p.ok) return p;
+    p.tiles_y = (int)ceil_div64(Ho, kM32TH);
+    p.tiles_x = (int)ceil_div64(Wo, kM32TW);
+    const size_t halo = (size_t)(kM32TH + 2 * dh) * (kM32TW + 2 * dw) * 64;
+    p.lds = halo + 9 * 64 * 64;
+    const size_t stage = (size_t)kM32TH * kM32TW * 80;
+    if (p.lds < stage) p.lds = stage;
+    p.ok = N * p.tiles_y * p.tiles_x < ((int64_t)1 << 31);
+    const int64_t ntiles = N * p.tiles_y * p.tiles_x, groups = Nout / 64;
+    const size_t hbuf = halo > stage ? halo : stage;
+    p.plds = (size_t)(Ci / 64) * 36864 + 2 * hbuf;
+    int64_t G = 256 / groups;
+    if (G < 8) G = 8;
+    if (G > ntiles) G = ntiles;
+    p.G = (int)G;
+    p.persist = p.plds <= 160 * 1024 && ntiles >= 2 * G;
+    return p;
+}
+
+template <int DH, int DW, int EPI>
+int launch_m32_t(const M32Plan& p, const HaloArgs& a, int kid, hipStream_t s)
+{
+    if (p.persist) {
+        dim3 grid((unsigned)p.G, (unsigned)(a.Nout / 64));
+        if (hipFuncSetAttribute((const void*)k_conv3x3_m32p<DH, DW, EPI>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.plds) != hipSuccess)
+            return ISEG_ERR_DEVICE;
+        ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_m32p<DH, DW, EPI>), grid, dim3(256), p.plds, s, a);
+        return launch_ok();
+    }
+    dim3 grid((unsigned)(a.N * p.tiles_y * p.tiles_x), (unsigned)(a.Nout / 64));
+    if (hipFuncSetAttribute((const void*)k_conv3x3_m32<DH, DW, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)p.lds) != hipSuccess)
+        return ISEG_ERR_DEVICE;
+    ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_m32<DH, DW, EPI>), grid, dim3(256), p.lds, s, a);
+    return launch_ok();
+}
+
+template <int EPI>
+int launch_m32_e(const M32Plan& p, const HaloArgs& a, int kid, hipStream_t s)
+{
+    if (a.dh == 1 && a.dw == 1) return launch_m32_t<1, 1, EPI>(p, a, kid, s);
+    if (a.dh == 2 && a.dw == 2) return launch_m32_t<2, 2, EPI>(p, a, kid, s);
+    if (a.dh == 1) return launch_m32_t<1, 2, EPI>(p, a, kid, s);
+    return launch_m32_t<2, 1, EPI>(p, a, kid, s);
+}
+
+int launch_m32(const M32Plan& p, HaloArgs a, int epi, int kid, hipStream_t s)
+{
+    a.tiles_y = p.tiles_y;
+    a.tiles_x = p.tiles_x;
+    if (epi == EPI_RAW) return launch_m32_e<EPI_RAW>(p, a, kid, s);
+    if (epi == EPI_MAX) return launch_m32_e<EPI_MAX>(p, a, kid, s);
+    return launch_m32_e<EPI_Q8>(p, a, kid, s);
+}
+
+// Q8 through the 32x32 kernel: max pass, then the final-code pass
+int m32_q8(const M32Plan& p, HaloArgs h, int kid, const int32_t* exp_a, const int32_t* exp_b, int8_t* out,
+           int32_t* out_exp, uint64_t* pmax, hipStream_t s)
+{
+    int rc;
+    h.pmax = pmax;
+    h.npmax = p.persist ? (int64_t)p.G * (h.Nout / 64) : (int64_t)h.N * p.tiles_y * p.tiles_x * (h.Nout / 64);
+    if ((rc = launch_m32(p, h, EPI_MAX, kid, s))) return rc;
+    h.out8 = out; h.exp_a = exp_a; h.exp_b = exp_b; h.out_exp = out_exp;
+    return launch_m32(p, h, EPI_Q8, kid, s);
+}
+
+// ---------------------------------------------------------------------------
+// Persistent variant (Ci = 64 or 128): a block keeps its 64 output channels'
+// weights for all chunks resident in LDS and walks a contiguous run of tiles;
+// the input halo of the next (tile, chunk) streams into the second of two
+// buffers while the current one runs its nine taps, so the loads hide behind
+// the MFMAs.  The final-code epilogue stages a tile's codes in the halo buffer
+// it has just finished with.  Blocks are numbered so that neighbouring tiles
+// (which share halo rows) run on one XCD.
+// ---------------------------------------------------------------------------
+template <int TW, int EPI>
+__global__ __launch_bounds__(256) void k_conv3x3_persist(HaloArgs a)
+{
+    constexpr int TH = kHaloTH, TM = TW / 16, TN = 4;
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+    const int HR = TH + 2 * a.dh, HC = TW + 2 * a.dw;
+    const int nhalo = HR * HC * 4;                        // 16-byte pieces per halo
+    const int nchunk = a.Ci / 64;
+    int8_t* wts = smem;                                   // [nchunk][9][64][64]
+    int8_t* hbuf0 = smem + nchunk * 36864;
+    const int hbytes = HR * HC * 64;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = gridDim.x;
+    int b = blockIdx.x;
+    if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
+    const int ntiles = a.N * a.tiles_y * a.tiles_x;
+    const int t_begin = (int)((int64_t)b * ntiles / G), t_end = (int)((int64_t)(b + 1) * ntiles / G);
+    const int nunits = (t_end - t_begin) * nchunk;
+    const int k0 = blockIdx.y * 64;
+    const int lrow = lane & 15, lpart = lane >> 4;
+
+    int aaddr[9];
+#pragma unroll
+    for (int r = 0; r < 3; r++)
+#pragma unroll
+        for (int s2 = 0; s2 < 3; s2++) {
+            const int p = (wave + r * a.dh) * HC + lrow + s2 * a.dw;
+            aaddr[r * 3 + s2] = p * 64 + ((lpart ^ ((p >> 2) & 3)) << 4);
+        }
+    int baddr[TN];
+#pragma unroll
+    for (int j = 0; j < TN; j++) {
+        const int kk = 16 * j + lrow;
+        baddr[j] = kk * 64 + ((lpart ^ ((kk >> 2) & 3)) << 4);
+    }
+    const int p0 = 16 * wave + (lane >> 2);
+    const int hr0 = p0 / HC, hc0 = p0 - (p0 / HC) * HC;
+
+    // tile t -> (image, tile row, tile column)
+    auto tile_origin = [&](int t, int& n, int& oy0, int& ox0) {
+        const int tx = t % a.tiles_x, t2 = t / a.tiles_x;
+        oy0 = (t2 % a.tiles_y) * TH;
+        n = t2 / a.tiles_y;
+        ox0 = tx * TW;
+    };
+    auto issue_halo = [&](int u) {
+        const int t = t_begin + u / nchunk, cc = u - (u / nchunk) * nchunk;
+        int n, oy0, ox0;
+        tile_origin(t, n, oy0, ox0);
+        const int iy0 = oy0 - a.ph, ix0 = ox0 - a.pw;
+        int8_t* dst = hbuf0 + (u & 1) * hbytes;
+        int hr = hr0, hc = hc0;
+        for (int k = wave; k * 64 < nhalo; k += 4) {
+            const int q = k * 64 + lane;
+            if (q < nhalo) {
+                const int p = q >> 2;
+                const int part = (q & 3) ^ ((p >> 2) & 3);
+                const int iy = iy0 + hr, ix = ix0 + hc;
+                const bool v = (unsigned)iy < (unsigned)a.Hs && (unsigned)ix < (unsigned)a.Ws;
+                const void* g = v ? (const void*)(a.src + (((int64_t)n * a.Hs + iy) * a.Ws + ix) * a.Ci + cc * 64 +
+                                                  part * 16)
+                                  : (const void*)g_conv_zero;
+                dma16(g, dst + k * 1024);
+            }
+            hc += 64;
+            while (hc >= HC) { hc -= HC; ++hr; }
+        }
+    };
+
+    // prologue: every chunk's weights, the first halo, the global max (second pass)
+    {
+        const int wkk = 16 * wave + (lane >> 2);
+        const int wpart = (lane & 3) ^ ((wkk >> 2) & 3);
+        const int8_t* wsrc = a.wmat + (int64_t)(k0 + wkk) * 9 * a.Ci + wpart * 16;
+        for (int cc = 0; cc < nchunk; cc++)
+#pragma unroll
+            for (int j = 0; j < 9; j++)
+                dma16(wsrc + (int64_t)j * a.Ci + cc * 64, wts + cc * 36864 + (wave + 4 * j) * 1024);
+    }
+    if (nunits > 0) issue_halo(0);
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);
+    wait_vm<0>();
+    __syncthreads();
+
+    int32_t vmax = 0, vmin = 0;                           // max pass: running extremes
+    v4i acc[TM][TN];
+    for (int u = 0; u < nunits; u++) {
+        if (u + 1 < nunits) issue_halo(u + 1);
+        const int cc = u - (u / nchunk) * nchunk;
+        const int8_t* halo = hbuf0 + (u & 1) * hbytes;
+        const int8_t* w = wts + cc * 36864;
+#pragma unroll
+        for (int t = 0; t < 9; t++) {
+            v4i fa[TM], fb[TN];
+#pragma unroll
+            for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&halo[aaddr[t] + 1024 * i];
+#pragma unroll
+            for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&w[t * 4096 + baddr[j]];
+            if (t == 0 && cc == 0) {
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], (v4i){0, 0, 0, 0}, 0, 0, 0);
+            } else {
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+            }
+        }
+        if (cc == nchunk - 1) {
+            int n, oy0, ox0;
+            tile_origin(t_begin + u / nchunk, n, oy0, ox0);
+            const int oy = oy0 + wave;
+            const int vcols = a.Wo - ox0 < TW ? a.Wo - ox0 : TW;
+            const int64_t rowbase = ((int64_t)n * a.Ho + oy) * a.Wo;
+            if (EPI == EPI_RAW) {
+                if (oy < a.Ho) {
+#pragma unroll
+                    for (int i = 0; i < TM; i++)
+#pragma unroll
+                        for (int e = 0; e < 4; e++)
+                            if (16 * i + 4 * lpart + e < vcols) {
+#pragma unroll
+                                for (int j = 0; j < TN; j++)
+                                    a.out[(rowbase + ox0 + 16 * i + 4 * lpart + e) * a.Nout + k0 + 16 * j + lrow] =
+                                        acc[i][j][e];
+                            }
+                }
+            } else if (EPI == EPI_MAX) {
+                if (oy < a.Ho) {
+#pragma unroll
+                    for (int i = 0; i < TM; i++)
+#pragma unroll
+                        for (int e = 0; e < 4; e++)
+                            if (16 * i + 4 * lpart + e < vcols) {
+#pragma unroll
+                                for (int j = 0; j < TN; j += 2) {
+                                    vmax = max(vmax, max(acc[i][j][e], acc[i][j + 1][e]));
+                                    vmin = min(vmin, min(acc[i][j][e], acc[i][j + 1][e]));
+                                }
+                            }
+                }
+            } else {                                      // EPI_Q8
+                const int r = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+                const int rs = r > 0 ? r - 1 : 0, ls = r > 0 ? 0 : -r;
+                constexpr int RB8 = 64 + 16;
+                int8_t* T = (int8_t*)halo + (wave * TW + 4 * lpart) * RB8 + lrow;
+                __syncthreads();                          // every wave is done reading this halo
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+#pragma unroll
+                        for (int j = 0; j < TN; j++) {
+                            const int32_t v = acc[i][j][e];
+                            int32_t c = r > 0 ? ((v >> rs) + 1) >> 1 : v << ls;
+                            c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                            T[(16 * i + e) * RB8 + 16 * j] = (int8_t)c;
+                        }
+                __syncthreads();
+                if (oy < a.Ho) {
+                    const int8_t* T0 = halo + (wave * TW + (lane >> 2)) * RB8 + (lane & 3) * 16;
+                    int8_t* g = a.out8 + ((rowbase + ox0 + (lane >> 2)) * a.Nout + k0 + (lane & 3) * 16);
+#pragma unroll
+                    for (int u2 = 0; u2 < TW / 16; u2++)
+                        if ((lane >> 2) + 16 * u2 < vcols)
+                            *(int4*)(g + (int64_t)16 * u2 * a.Nout) = *(const int4*)&T0[16 * u2 * RB8];
+                }
+            }
+        }
+        wait_vm<0>();                                     // the next unit's halo has landed
+        __syncthreads();
+    }
+    if (EPI == EPI_MAX) {
+        const uint64_t bm = block_max_u64((uint32_t)max(vmax, -vmin));
+        if (tid == 0) a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = bm;
+    }
+    if (EPI == EPI_Q8 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
+        const int r = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+        *a.out_exp = *a.exp_a + *a.exp_b + r;
+    }
+}
+
+struct PersistPlan {
+    bool ok;
+    int TW, tiles_y, tiles_x, G;
+    size_t lds;
+};
+
+PersistPlan persist_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Ci, int64_t Nout, int R, int S, int sh, int sw,
+                         int dh, int dw)
+{
+    PersistPlan p{};
+    p.ok = N > 0 && R == 3 && S == 3 && sh == 1 && sw == 1 && dh <= 2 && dw <= 2 && (Ci == 64 || Ci == 128) &&
+           Nout % 64 == 0 && N * Ho * Wo < ((int64_t)1 << 31);
+    if (!p.ok) return p;
+    p.TW = (Ci == 64 && Wo % 112 == 0) ? 112 : 64;
+    p.tiles_y = (int)ceil_div64(Ho, kHaloTH);
+    p.tiles_x = (int)ceil_div64(Wo, p.TW);
+    const int64_t ntiles = N * p.tiles_y * p.tiles_x;
+    const int64_t halo = (int64_t)(kHaloTH + 2 * dh) * (p.TW + 2 * dw) * 64;
+    p.lds = (size_t)((Ci / 64) * 36864 + 2 * halo);
+    const int64_t groups = Nout / 64;
+    int64_t G = 256 / groups;
+    if (G < 8) G = 8;
+    if (G > ntiles) G = ntiles;
+    p.G = (int)G;
+    p.ok = ntiles < ((int64_t)1 << 31) && p.lds <= 160 * 1024 &&
+           (int64_t)kHaloTH * p.TW * 80 <= halo;        // code staging fits in a halo buffer
+    return p;
+}
+
+template <int TW, int EPI>
+int launch_persist_t(const PersistPlan& p, const HaloArgs& a, int kid, hipStream_t s)
+{
+    dim3 grid((unsigned)p.G, (unsigned)(a.Nout / 64));
+    if (hipFuncSetAttribute((const void*)k_conv3x3_persist<TW, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)p.lds) != hipSuccess)
+        return ISEG_ERR_DEVICE;
+    ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_persist<TW, EPI>), grid, dim3(256), p.lds, s, a);
+    return launch_ok();
+}
+
+int launch_persist(const PersistPlan& p, HaloArgs a, int epi, int kid, hipStream_t s)
+{
+    a.tiles_y = p.tiles_y;
+    a.tiles_x = p.tiles_x;
+    if (p.TW == 112) {
+        if (epi == EPI_RAW) return launch_persist_t<112, EPI_RAW>(p, a, kid, s);
+        if (epi == EPI_MAX) return launch_persist_t<112, EPI_MAX>(p, a, kid, s);
+        return launch_persist_t<112, EPI_Q8>(p, a, kid, s);
+    }
+    if (epi == EPI_RAW) return launch_persist_t<64, EPI_RAW>(p, a, kid, s);
+    if (epi == EPI_MAX) return launch_persist_t<64, EPI_MAX>(p, a, kid, s);
+    return launch_persist_t<64, EPI_Q8>(p, a, kid, s);
+}
+
+// Q8 through the persistent kernel: max pass, then the final-code pass
+int persist_q8(const PersistPlan& p, HaloArgs h, int kid, const int32_t* exp_a, const int32_t* exp_b, int8_t* out,
+               int32_t* out_exp, uint64_t* pmax, hipStream_t s)
+{
+    int rc;
+    h.pmax = pmax;
+    h.npmax = (int64_t)p.G * (h.Nout / 64);
+    if ((rc = launch_persist(p, h, EPI_MAX, kid, s))) return rc;
+    h.out8 = out; h.exp_a = exp_a; h.exp_b = exp_b; h.out_exp = out_exp;
+    return launch_persist(p, h, EPI_Q8, kid, s);
+}
+
 // weights [K][R][S][C] -> [C][R][S][K] with the taps reversed (backward-data as
 // a forward convolution over dy)
 __global__ void k_w_flip_transpose(const int8_t* __restrict__ w, int8_t* __restrict__ wt, int32_t K,
@@ -1772,13 +2494,15 @@ bool geom_ok(const iseg_conv_geom* g, int64_t* P, int64_t* Q)
 // C ABI
 // ---------------------------------------------------------------------------
 // room for per-block max partials of any path the output of rows x cols can take
-size_t conv_pmax_bytes(int64_t rows, int64_t cols, const HaloPlan& hp, int64_t N)
+size_t conv_pmax_bytes(int64_t rows, int64_t cols, const HaloPlan& hp, int64_t N, int64_t Ho, int64_t Wo)
 {
     int64_t nb = ceil_div64(rows, 128) * ceil_div64(cols, 64);
     if (hp.ok) {
         const int64_t nh = N * hp.tiles_y * hp.tiles_x * (cols / 64);
         nb = nb > nh ? nb : nh;
     }
+    const int64_t nm = N * ceil_div64(Ho, kM32TH) * ceil_div64(Wo, kM32TW) * ceil_div64(cols, 64);
+    nb = nb > nm ? nb : nm;
     return align256((size_t)nb * 8);
 }
 
@@ -1797,7 +2521,7 @@ extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
             const size_t sh = halo_staged_ws_bytes(hp, g->N, P, Q, g->K);
             big = big > sh ? big : sh;
         }
-        s += big + conv_pmax_bytes(g->N * P * Q, g->K, hp, g->N);
+        s += big + conv_pmax_bytes(g->N * P * Q, g->K, hp, g->N, P, Q);
     }
     int64_t Cp = padded_c(g->C);
     if (Cp != g->C)
@@ -1826,7 +2550,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     int32_t* acc = (int32_t*)y;
     if (out_mode == ISEG_OUT_Q8) {
         pmax = (uint64_t*)wp;
-        wp += conv_pmax_bytes(g->N * P * Q, g->K, hp, g->N);
+        wp += conv_pmax_bytes(g->N * P * Q, g->K, hp, g->N, P, Q);
         acc = (int32_t*)wp;
         size_t big = align256((size_t)(g->N * P * Q * g->K) * 4);
         const size_t s16 = staged_ws_bytes(g->N * P * Q, g->K);
@@ -1859,6 +2583,36 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
+    const M32Plan mp = m32_plan(g->N, P, Q, Cp, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h,
+                                g->dil_w);
+    if (mp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y) & 15) == 0) {
+        HaloArgs h{};
+        h.src = xs; h.wmat = wsrc; h.out = (int32_t*)y;
+        h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)Cp;
+        h.Ho = (int32_t)P; h.Wo = (int32_t)Q; h.Nout = (int32_t)g->K;
+        h.ph = g->pad_h; h.pw = g->pad_w; h.dh = g->dil_h; h.dw = g->dil_w;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_m32(mp, h, EPI_RAW, ISEG_KID_CONV_FWD, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
+            return launch_ok();
+        }
+        return m32_q8(mp, h, ISEG_KID_CONV_FWD, x_exp, w_exp, (int8_t*)y, y_exp, pmax, stream);
+    }
+    const PersistPlan pp = persist_plan(g->N, P, Q, Cp, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                        g->dil_h, g->dil_w);
+    if (pp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y) & 15) == 0) {
+        HaloArgs h{};
+        h.src = xs; h.wmat = wsrc; h.out = (int32_t*)y;
+        h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)Cp;
+        h.Ho = (int32_t)P; h.Wo = (int32_t)Q; h.Nout = (int32_t)g->K;
+        h.ph = g->pad_h; h.pw = g->pad_w; h.dh = g->dil_h; h.dw = g->dil_w;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_persist(pp, h, EPI_RAW, ISEG_KID_CONV_FWD, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
+            return launch_ok();
+        }
+        return persist_q8(pp, h, ISEG_KID_CONV_FWD, x_exp, w_exp, (int8_t*)y, y_exp, pmax, stream);
+    }
     if (hp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y | (uintptr_t)acc) & 15) == 0) {
         HaloArgs h{};
         h.src = xs; h.wmat = wsrc; h.out = acc;
@@ -1910,7 +2664,7 @@ extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mod
             const size_t sh = halo_staged_ws_bytes(hp, g->N, g->H, g->W, g->C);
             big = big > sh ? big : sh;
         }
-        s += big + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N);
+        s += big + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N, g->H, g->W);
     }
     return s;
 }
@@ -1937,10 +2691,49 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     int32_t* acc = (int32_t*)dx;
     if (out_mode == ISEG_OUT_Q8) {
         pmax = (uint64_t*)((char*)ws + 256 + wt_bytes);
-        acc = (int32_t*)((char*)pmax + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N));
+        acc = (int32_t*)((char*)pmax + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N, g->H, g->W));
     }
     int rc;
     int64_t nw = g->K * g->R * g->S * g->C;
+    const M32Plan mp = m32_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                g->dil_h, g->dil_w);
+    if (mp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx) & 15) == 0) {
+        hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
+                           (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
+        if ((rc = launch_ok())) return rc;
+        HaloArgs h{};
+        h.src = dy; h.wmat = wt; h.out = (int32_t*)dx;
+        h.N = (int32_t)g->N; h.Hs = (int32_t)P; h.Ws = (int32_t)Q; h.Ci = (int32_t)g->K;
+        h.Ho = (int32_t)g->H; h.Wo = (int32_t)g->W; h.Nout = (int32_t)g->C;
+        h.ph = g->dil_h * (int32_t)(g->R - 1) - g->pad_h; h.pw = g->dil_w * (int32_t)(g->S - 1) - g->pad_w;
+        h.dh = g->dil_h; h.dw = g->dil_w;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_m32(mp, h, EPI_RAW, ISEG_KID_CONV_BWD_DATA, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
+            return launch_ok();
+        }
+        return m32_q8(mp, h, ISEG_KID_CONV_BWD_DATA, dy_exp, w_exp, (int8_t*)dx, dx_exp, pmax, stream);
+    }
+    const PersistPlan pp = persist_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h,
+                                        g->stride_w, g->dil_h, g->dil_w);
+    if (pp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx) & 15) == 0) {
+        // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
+        hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
+                           (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
+        if ((rc = launch_ok())) return rc;
+        HaloArgs h{};
+        h.src = dy; h.wmat = wt; h.out = (int32_t*)dx;
+        h.N = (int32_t)g->N; h.Hs = (int32_t)P; h.Ws = (int32_t)Q; h.Ci = (int32_t)g->K;
+        h.Ho = (int32_t)g->H; h.Wo = (int32_t)g->W; h.Nout = (int32_t)g->C;
+        h.ph = g->dil_h * (int32_t)(g->R - 1) - g->pad_h; h.pw = g->dil_w * (int32_t)(g->S - 1) - g->pad_w;
+        h.dh = g->dil_h; h.dw = g->dil_w;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_persist(pp, h, EPI_RAW, ISEG_KID_CONV_BWD_DATA, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
+            return launch_ok();
+        }
+        return persist_q8(pp, h, ISEG_KID_CONV_BWD_DATA, dy_exp, w_exp, (int8_t*)dx, dx_exp, pmax, stream);
+    }
     if (hp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx | (uintptr_t)acc) & 15) == 0) {
         // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
         hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
