@@ -185,6 +185,104 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd_disjoint(const int8_t* __re
     }
 }
 
+// max |code| of an int8 tensor: one partial per block (no atomics), 16 bytes per load
+__global__ __launch_bounds__(256) void k_absmax_i8_part(const int8_t* __restrict__ p, int64_t n16,
+                                                        uint64_t* __restrict__ part)
+{
+    uint32_t m = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x) {
+        const uint4 v = ((const uint4*)p)[i];
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                const int b = (int)(int8_t)(w[q] >> (8 * j));
+                const uint32_t a = (uint32_t)(b < 0 ? -b : b);
+                m = a > m ? a : m;
+            }
+    }
+    block_store_max_u64(m, part);
+}
+
+// Backward of non-overlapping k x k windows (stride k, no padding), one lane
+// per window and 16 channels: the window's k^2 input vectors are read once,
+// the first maximum of each channel (row-major order) receives the channel's
+// error code and every other input gets 0.  Each input takes at most one
+// error, so max |routed| = max |dy| and the SQ codes are final.  Inputs beyond
+// the last full window are zeroed by k_pool_zero_tail.
+template <int K>
+__global__ __launch_bounds__(256) void k_maxpool_bwd_win(const int8_t* __restrict__ dy,
+                                                         const int8_t* __restrict__ x, int8_t* __restrict__ dx,
+                                                         PoolGeom g, const uint64_t* __restrict__ part, int npart,
+                                                         const int32_t* dy_exp, int32_t* dx_exp, int bits)
+{
+    const uint64_t M = reduce_partials_u64(part, npart);
+    const int r = M ? bitlen_u64(M) - (bits - 1) : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *dx_exp = *dy_exp + r;
+    const int64_t C16 = g.C / 16;
+    const int64_t total = g.N * g.P * g.Q * C16;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t cg = i % C16, wi = i / C16;
+        const int q = (int)(wi % g.Q);
+        const int64_t t = wi / g.Q;
+        const int p = (int)(t % g.P);
+        const int64_t n = t / g.P;
+        uint32_t v[K * K][4];
+#pragma unroll
+        for (int rr = 0; rr < K; rr++)
+#pragma unroll
+            for (int s2 = 0; s2 < K; s2++) {
+                const uint4 u = *(const uint4*)(x + ((n * g.H + p * K + rr) * g.W + q * K + s2) * g.C + cg * 16);
+                v[rr * K + s2][0] = u.x; v[rr * K + s2][1] = u.y; v[rr * K + s2][2] = u.z; v[rr * K + s2][3] = u.w;
+            }
+        const uint4 eu = *(const uint4*)(dy + ((n * g.P + p) * g.Q + q) * g.C + cg * 16);
+        const uint32_t ew[4] = {eu.x, eu.y, eu.z, eu.w};
+        uint32_t o[K * K][4];
+#pragma unroll
+        for (int w = 0; w < K * K; w++)
+#pragma unroll
+            for (int d = 0; d < 4; d++) o[w][d] = 0;
+#pragma unroll
+        for (int d = 0; d < 4; d++)
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                int best = (int)(int8_t)(v[0][d] >> (8 * j)), bpos = 0;
+#pragma unroll
+                for (int w = 1; w < K * K; w++) {
+                    const int b = (int)(int8_t)(v[w][d] >> (8 * j));
+                    if (b > best) { best = b; bpos = w; }
+                }
+                const uint32_t code = (uint32_t)(uint8_t)sq_code((int8_t)(ew[d] >> (8 * j)), r, bits);
+#pragma unroll
+                for (int w = 0; w < K * K; w++) o[w][d] |= (bpos == w ? code : 0u) << (8 * j);
+            }
+#pragma unroll
+        for (int rr = 0; rr < K; rr++)
+#pragma unroll
+            for (int s2 = 0; s2 < K; s2++) {
+                const uint32_t* ow = o[rr * K + s2];
+                *(uint4*)(dx + ((n * g.H + p * K + rr) * g.W + q * K + s2) * g.C + cg * 16) =
+                    make_uint4(ow[0], ow[1], ow[2], ow[3]);
+            }
+    }
+}
+
+// zero the input rows / columns that no full window covers
+__global__ __launch_bounds__(256) void k_pool_zero_tail(int8_t* __restrict__ dx, PoolGeom g)
+{
+    const int64_t C16 = g.C / 16;
+    const int64_t total = g.N * g.H * g.W * C16;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t pix = i / C16;
+        const int w = (int)(pix % g.W);
+        const int h = (int)((pix / g.W) % g.H);
+        if (h >= g.P * g.k || w >= g.Q * g.k) *(uint4*)(dx + i * 16) = make_uint4(0, 0, 0, 0);
+    }
+}
+
 bool pool_geom(int64_t N, int64_t H, int64_t W, int64_t C, int32_t k, int32_t st, int32_t pad,
                PoolGeom* g)
 {
@@ -233,9 +331,27 @@ extern "C" int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const i
     if (!ws || ws_bytes < iseg_maxpool_bwd_ws(N, H, W, C)) return ISEG_ERR_WORKSPACE;
     unsigned long long* maxp = (unsigned long long*)ws;
     int32_t* acc = (int32_t*)((char*)ws + 256);
-    int rc = launch_fill_u32(maxp, 2, 0, stream);
-    if (rc) return rc;
+    int rc;
     int64_t total = N * H * W * C;
+    if (k == stride && pad == 0 && k == 2 && C % 16 == 0 &&
+        (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx) & 15) == 0) {
+        // per-window routing; the max of dy comes from per-block partials
+        uint64_t* part = (uint64_t*)acc;
+        const int64_t ndy = g.N * g.P * g.Q * C;
+        const unsigned nb = (unsigned)grid_for(ndy / 16, 256 * 4, 256);
+        hipLaunchKernelGGL(k_absmax_i8_part, dim3(nb), dim3(256), 0, stream, dy, ndy / 16, part);
+        if ((rc = launch_ok())) return rc;
+        const int64_t nwin = g.N * g.P * g.Q * (C / 16);
+        ISEG_TIMED_LAUNCH(ISEG_KID_MAXPOOL_BWD, stream, k_maxpool_bwd_win<2>, dim3(grid_for(nwin, 256, 8192)),
+                          dim3(256), 0, stream, dy, x, dx, g, part, (int)nb, dy_exp, dx_exp, bits);
+        if ((rc = launch_ok())) return rc;
+        if (g.P * k < H || g.Q * k < W) {
+            hipLaunchKernelGGL(k_pool_zero_tail, dim3(grid_for(total / 16, 256, 4096)), dim3(256), 0, stream, dx, g);
+            if ((rc = launch_ok())) return rc;
+        }
+        return ISEG_OK;
+    }
+    if ((rc = launch_fill_u32(maxp, 2, 0, stream))) return rc;
     if (k == stride && pad == 0 && C % 4 == 0 &&
         (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx) & 3) == 0) {
         int64_t ndy = g.N * g.P * g.Q * C;

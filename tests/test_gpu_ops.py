@@ -296,6 +296,25 @@ def test_maxpool(orc, dev, k, st, pad):
     assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
 
 
+@pytest.mark.parametrize("shape,small", [((2, 29, 31, 32), False), ((1, 8, 8, 64), True),
+                                         ((3, 16, 10, 16), False)])
+def test_maxpool_2x2_window_path(orc, dev, shape, small):
+    """2x2/2 windows with 16-channel vectors (per-window kernel), ragged H/W
+    whose last row/column no window covers, ties, and an error tensor whose
+    max is below 64 (negative requant shift)."""
+    from paper_2011_14504_amd import iseg
+    x = synth.int_codes(73, shape)
+    x[0, :4, :4, :] = -3                      # ties
+    y, ye = iseg.maxpool_fwd(T(x, dev), E(-6, dev), 2, 2, 0)
+    assert np.array_equal(H(y), orc.maxpool_fwd(x, 2, 2, 0))
+    dy = synth.int_codes(74, H(y).shape)
+    if small:
+        dy = (dy // 8).astype(np.int8)
+    dx, dxe = iseg.maxpool_bwd(T(dy, dev), E(-20, dev), T(x, dev), 2, 2, 0)
+    rc, rce = orc.maxpool_bwd(dy, -20, x, 2, 2, 0)
+    assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
+
+
 @pytest.mark.parametrize("C,d_exp", [(64, -30), (128, -12), (2048, -40)])
 def test_bn_param_update(orc, dev, C, d_exp):
     # Q_G (Eq. 17, stochastic) then Q_U (Eq. 19) of gamma/beta in one launch
