@@ -1171,6 +1171,187 @@ __global__ __launch_bounds__(256, 1) void k_conv3x3_m32p(HaloArgs a)
     if (EPI == EPI_Q8 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
 }
 
+// ---------------------------------------------------------------------------
+// Stem convolution for few input channels (C = 3: 3x3 stride 1, 7x7 stride 2),
+// Nout % 64 == 0.  The reduction (tap, channel) of R S C <= 160 entries is
+// padded to k-steps of 32 and fed to v_mfma_i32_32x32x32_i8: a lane's A
+// operand is 16 (tap, channel) bytes of one output pixel gathered from an LDS
+// halo of the input tile, the B operand (the weights, KRSC order = the same
+// reduction order) stays in registers for the whole block.  A block owns 16 x
+// 32 output pixels (wave w: rows 4w..4w+3, one 32-pixel fragment per row) and
+// 64 output channels.  Epilogues as for the 3x3 kernels (raw sums, max pass,
+// final codes).
+// ---------------------------------------------------------------------------
+template <int C, int R, int S, int ST, int EPI>
+__global__ __launch_bounds__(256) void k_conv_stem(HaloArgs a)
+{
+    constexpr int TH = 16, TW = 32, KRED = R * S * C, NKS = (KRED + 31) / 32;
+    constexpr int HROWS = (TH - 1) * ST + R, HCOLS = (TW - 1) * ST + S;
+    constexpr int HBYTES = (HROWS * HCOLS * C + 15) & ~15;
+    constexpr int RB8 = 64 + 16;
+    __shared__ __attribute__((aligned(16))) int8_t smem[HBYTES > TH * TW * RB8 ? HBYTES : TH * TW * RB8];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int tx = blockIdx.x % a.tiles_x, t2 = blockIdx.x / a.tiles_x;
+    const int ty = t2 % a.tiles_y, n = t2 / a.tiles_y;
+    const int oy0 = ty * TH, ox0 = tx * TW, k0 = blockIdx.y * 64;
+    const int iy0 = oy0 * ST - a.ph, ix0 = ox0 * ST - a.pw;
+
+    // halo: rows iy0 .. iy0 + HROWS - 1, columns ix0 .., all C channels (zero outside the
+    // image); every load of a thread is issued before its first LDS store
+    {
+        constexpr int NH = HROWS * HCOLS * C, PER = (NH + 255) / 256;
+        int8_t hv[PER];
+#pragma unroll
+        for (int u = 0; u < PER; u++) {
+            const int i = tid + 256 * u;
+            const int hr = i / (HCOLS * C), rem = i - hr * (HCOLS * C);
+            const int hc = rem / C, c = rem - hc * C;
+            const int iy = iy0 + hr, ix = ix0 + hc;
+            const bool v = i < NH && (unsigned)iy < (unsigned)a.Hs && (unsigned)ix < (unsigned)a.Ws;
+            hv[u] = v ? a.src[(((int64_t)n * a.Hs + iy) * a.Ws + ix) * C + c] : (int8_t)0;
+        }
+#pragma unroll
+        for (int u = 0; u < PER; u++)
+            if (tid + 256 * u < NH) smem[tid + 256 * u] = hv[u];
+    }
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);
+    // B: weights of channels k0 + 32 j + l32, reduction bytes 32 ks + 16 h + b (zero past KRED)
+    v4i fb[NKS][2];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks++)
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            uint32_t wv[4] = {0, 0, 0, 0};
+            const int8_t* wr = a.wmat + (int64_t)(k0 + 32 * j + l32) * KRED;
+#pragma unroll
+            for (int b = 0; b < 16; b++) {
+                const int k = 32 * ks + 16 * h + b;
+                if (k < KRED) wv[b >> 2] |= (uint32_t)(uint8_t)wr[k] << (8 * (b & 3));
+            }
+            fb[ks][j] = (v4i){(int)wv[0], (int)wv[1], (int)wv[2], (int)wv[3]};
+        }
+    // A gather offsets (relative to the pixel's halo origin) of this lane's 16 reduction bytes
+    int aoff[NKS][16];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks++)
+#pragma unroll
+        for (int b = 0; b < 16; b++) {
+            const int k = 32 * ks + 16 * h + b;
+            const int tap = k / C, c = k - (k / C) * C, r = tap / S, s2 = tap - (tap / S) * S;
+            aoff[ks][b] = k < KRED ? (r * HCOLS + s2) * C + c : -1;
+        }
+    __syncthreads();
+
+    typedef int v16i __attribute__((ext_vector_type(16)));
+    v16i acc[4][2];
+#pragma unroll
+    for (int f = 0; f < 4; f++) {
+        const int pbase = ((4 * wave + f) * ST * HCOLS + l32 * ST) * C;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ks++) {
+            uint32_t av[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int b = 0; b < 16; b++)
+                if (aoff[ks][b] >= 0) av[b >> 2] |= (uint32_t)(uint8_t)smem[pbase + aoff[ks][b]] << (8 * (b & 3));
+            const v4i fa = (v4i){(int)av[0], (int)av[1], (int)av[2], (int)av[3]};
+#pragma unroll
+            for (int j = 0; j < 2; j++)
+                acc[f][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa, fb[ks][j], ks ? acc[f][j] : (v16i){}, 0, 0, 0);
+        }
+    }
+
+    // acc[f][j][v]: output row 4 wave + f, column 8 (v / 4) + 4 h + v % 4, channel k0 + 32 j + l32
+    const int vrows = a.Ho - oy0 < TH ? a.Ho - oy0 : TH;
+    const int vcols = a.Wo - ox0 < TW ? a.Wo - ox0 : TW;
+    auto colof = [&](int v) { return 8 * (v >> 2) + 4 * h + (v & 3); };
+    if (EPI == EPI_RAW) {
+#pragma unroll
+        for (int f = 0; f < 4; f++)
+#pragma unroll
+            for (int v = 0; v < 16; v++)
+                if (4 * wave + f < vrows && colof(v) < vcols) {
+                    const int64_t pix = ((int64_t)n * a.Ho + oy0 + 4 * wave + f) * a.Wo + ox0 + colof(v);
+#pragma unroll
+                    for (int j = 0; j < 2; j++) a.out[pix * a.Nout + k0 + 32 * j + l32] = acc[f][j][v];
+                }
+        return;
+    }
+    if (EPI == EPI_MAX) {
+        int32_t vmax = 0, vmin = 0;
+#pragma unroll
+        for (int f = 0; f < 4; f++)
+#pragma unroll
+            for (int v = 0; v < 16; v++)
+                if (4 * wave + f < vrows && colof(v) < vcols) {
+                    vmax = max(vmax, max(acc[f][0][v], acc[f][1][v]));
+                    vmin = min(vmin, min(acc[f][0][v], acc[f][1][v]));
+                }
+        const uint64_t bm = block_max_u64((uint32_t)max(vmax, -vmin));
+        if (tid == 0) a.pmax[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = bm;
+        return;
+    }
+    const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+    const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+    __syncthreads();                                         // the halo is no longer read
+#pragma unroll
+    for (int f = 0; f < 4; f++)
+#pragma unroll
+        for (int v = 0; v < 16; v++) {
+            const int px = (4 * wave + f) * TW + colof(v);
+#pragma unroll
+            for (int j = 0; j < 2; j++) {
+                const int32_t x = acc[f][j][v];
+                int32_t c = rq > 0 ? ((x >> rs) + 1) >> 1 : x << ls;
+                c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                smem[px * RB8 + 32 * j + l32] = (int8_t)c;
+            }
+        }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < TH * TW * 4 / 256; u++) {
+        const int c = tid + 256 * u;
+        const int px = c >> 2, part = c & 3;
+        const int ry = px / TW, rx = px % TW;
+        if (ry < vrows && rx < vcols)
+            *(int4*)(a.out8 + ((((int64_t)n * a.Ho + oy0 + ry) * a.Wo + ox0 + rx) * a.Nout + k0 + part * 16)) =
+                *(const int4*)&smem[px * RB8 + part * 16];
+    }
+}
+
+// shapes of the stem kernel: C = 3 with 3x3 / stride 1 or 7x7 / stride 2, no dilation
+int stem_kind(int64_t C, int R, int S, int sh, int sw, int dh, int dw, int64_t Nout)
+{
+    if (C != 3 || dh != 1 || dw != 1 || Nout % 64 != 0) return 0;
+    if (R == 3 && S == 3 && sh == 1 && sw == 1) return 1;
+    if (R == 7 && S == 7 && sh == 2 && sw == 2) return 2;
+    return 0;
+}
+
+template <int R, int ST, int EPI>
+int launch_stem_t(const HaloArgs& a, int kid, hipStream_t s)
+{
+    dim3 grid((unsigned)(a.N * a.tiles_y * a.tiles_x), (unsigned)(a.Nout / 64));
+    ISEG_TIMED_LAUNCH(kid, s, (k_conv_stem<3, R, R, ST, EPI>), grid, dim3(256), 0, s, a);
+    return launch_ok();
+}
+
+int launch_stem(int kind, HaloArgs a, int epi, int kid, hipStream_t s)
+{
+    a.tiles_y = (int)ceil_div64(a.Ho, 16);
+    a.tiles_x = (int)ceil_div64(a.Wo, 32);
+    if (kind == 1) {
+        if (epi == EPI_RAW) return launch_stem_t<3, 1, EPI_RAW>(a, kid, s);
+        if (epi == EPI_MAX) return launch_stem_t<3, 1, EPI_MAX>(a, kid, s);
+        return launch_stem_t<3, 1, EPI_Q8>(a, kid, s);
+    }
+    if (epi == EPI_RAW) return launch_stem_t<7, 2, EPI_RAW>(a, kid, s);
+    if (epi == EPI_MAX) return launch_stem_t<7, 2, EPI_MAX>(a, kid, s);
+    return launch_stem_t<7, 2, EPI_Q8>(a, kid, s);
+}
+
 struct M32Plan {
     bool ok;
     int tiles_y, tiles_x;
@@ -2339,6 +2520,130 @@ __global__ __launch_bounds__(64 * kRedWaves) void k_wgrad_reduce(const int32_t* 
     if (maxp) block_atomic_max_u64(mx, maxp);
 }
 
+// ---------------------------------------------------------------------------
+// Backward-weight of the few-channel stem (C = 3, 3x3 / stride 1 or 7x7 /
+// stride 2) on v_mfma_i32_32x32x32_i8 with pixels as the reduction: per output
+// row of a 16 x 32 tile, A = dy^T (64 output channels x 32 pixels, read with
+// ds_read_b64_tr_b8 from the block's dy tile) and B = the 32 pixels' input
+// patches ((tap, channel) x pixel, gathered from the LDS halo).  Wave w takes
+// rows 4w..4w+3; the four waves' sums are added in LDS and the block writes
+// its exact int32 partial [K][R S C] (k_wgrad_reduce adds the blocks in int64).
+// ---------------------------------------------------------------------------
+template <int C, int R, int S, int ST>
+__global__ __launch_bounds__(256) void k_wgrad_stem(const int8_t* __restrict__ dy, const int8_t* __restrict__ x,
+                                                   int32_t* __restrict__ part, HaloArgs a)
+{
+    constexpr int TH = 16, TW = 32, KRED = R * S * C, NKS = (KRED + 31) / 32;
+    constexpr int HROWS = (TH - 1) * ST + R, HCOLS = (TW - 1) * ST + S;
+    constexpr int NH = HROWS * HCOLS * C;
+    constexpr int RD = 80;                                   // LDS bytes per dy pixel row (64 + pad)
+    constexpr int DYB = TH * TW * RD;
+    __shared__ __attribute__((aligned(16))) int8_t sdy[DYB];
+    __shared__ __attribute__((aligned(16))) int8_t shalo[(NH + 15) & ~15];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int tx = blockIdx.x % a.tiles_x, t2 = blockIdx.x / a.tiles_x;
+    const int ty = t2 % a.tiles_y, n = t2 / a.tiles_y;
+    const int oy0 = ty * TH, ox0 = tx * TW, k0 = blockIdx.y * 64;
+    const int iy0 = oy0 * ST - a.ph, ix0 = ox0 * ST - a.pw;
+
+    {   // dy tile: 512 pixels x 64 channels, 16-byte pieces, zero outside the output
+        int4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+            const int c = tid + 256 * u, px = c >> 2, part4 = c & 3;
+            const int ry = px / TW, rx = px % TW;
+            const bool ok = oy0 + ry < a.Ho && ox0 + rx < a.Wo;
+            v[u] = ok ? *(const int4*)(dy + (((int64_t)n * a.Ho + oy0 + ry) * a.Wo + ox0 + rx) * a.Nout + k0 +
+                                       part4 * 16)
+                      : make_int4(0, 0, 0, 0);
+        }
+        constexpr int PER = (NH + 255) / 256;
+        int8_t hv[PER];
+#pragma unroll
+        for (int u = 0; u < PER; u++) {
+            const int i = tid + 256 * u;
+            const int hr = i / (HCOLS * C), rem = i - hr * (HCOLS * C);
+            const int hc = rem / C, c = rem - hc * C;
+            const int iy = iy0 + hr, ix = ix0 + hc;
+            const bool ok = i < NH && (unsigned)iy < (unsigned)a.Hs && (unsigned)ix < (unsigned)a.Ws;
+            hv[u] = ok ? x[(((int64_t)n * a.Hs + iy) * a.Ws + ix) * C + c] : (int8_t)0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+            const int c = tid + 256 * u;
+            *(int4*)&sdy[(c >> 2) * RD + (c & 3) * 16] = v[u];
+        }
+#pragma unroll
+        for (int u = 0; u < PER; u++)
+            if (tid + 256 * u < NH) shalo[tid + 256 * u] = hv[u];
+    }
+    // B gather offsets: this lane's column j = 32 ks + l32 = (tap, channel), -1 past KRED
+    int boff[NKS];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks++) {
+        const int j = 32 * ks + l32;
+        const int tap = j / C, c = j - (j / C) * C, r = tap / S, s2 = tap - (tap / S) * S;
+        boff[ks] = j < KRED ? (r * HCOLS + s2) * C + c : -1;
+    }
+    __syncthreads();
+
+    typedef int v16i __attribute__((ext_vector_type(16)));
+    v16i acc[2][NKS];
+    const int g16 = lane >> 4, sl = lane & 15;
+#pragma unroll
+    for (int yy = 0; yy < 4; yy++) {
+        const int y = 4 * wave + yy;
+        // A: channels 32 m + 16 (g16 & 1) + (lane % 16), pixels 16 (g16 >> 1) + 0..15 of row y
+        v4i fa[2];
+#pragma unroll
+        for (int m = 0; m < 2; m++) {
+            const int c0 = 32 * m + 16 * (g16 & 1);
+            const int px0 = y * TW + 16 * (g16 >> 1);
+            const int8_t* p0 = sdy + (px0 + (sl >> 1)) * RD + c0 + 8 * (sl & 1);
+            const v2i_t lo = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i_t*)p0);
+            const v2i_t hi =
+                __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i_t*)(p0 + 8 * RD));
+            fa[m] = (v4i){lo.x, lo.y, hi.x, hi.y};
+        }
+#pragma unroll
+        for (int ks = 0; ks < NKS; ks++) {
+            uint32_t bv[4] = {0, 0, 0, 0};
+            if (boff[ks] >= 0) {
+                const int8_t* hp = shalo + (y * ST * HCOLS + 16 * h * ST) * C + boff[ks];
+#pragma unroll
+                for (int b = 0; b < 16; b++) bv[b >> 2] |= (uint32_t)(uint8_t)hp[b * ST * C] << (8 * (b & 3));
+            }
+            const v4i fb = (v4i){(int)bv[0], (int)bv[1], (int)bv[2], (int)bv[3]};
+#pragma unroll
+            for (int m = 0; m < 2; m++)
+                acc[m][ks] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[m], fb, yy ? acc[m][ks] : (v16i){}, 0, 0, 0);
+        }
+    }
+    // sum the four waves in LDS (reusing the dy tile), one 32-column group at a
+    // time, and store the block partial
+    int32_t* red = (int32_t*)sdy;                           // [4 waves][2][16 values][64 lanes] = 32 KB
+    int32_t* outp = part + (int64_t)blockIdx.x * a.Nout * KRED;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks++) {
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < 2; m++)
+#pragma unroll
+            for (int v = 0; v < 16; v++) red[((wave * 2 + m) * 16 + v) * 64 + lane] = acc[m][ks][v];
+        __syncthreads();
+        for (int e = tid; e < 2 * 16 * 64; e += 256) {
+            const int m = e >> 10, v = (e >> 6) & 15, ln = e & 63;
+            int32_t t = 0;
+#pragma unroll
+            for (int w = 0; w < 4; w++) t += red[((w * 2 + m) * 16 + v) * 64 + ln];
+            const int ch = 32 * m + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3);
+            const int col = 32 * ks + (ln & 31);
+            if (col < KRED) outp[(int64_t)(k0 + ch) * KRED + col] = t;
+        }
+    }
+}
+
 #ifndef ISEG_WGRAD_BLOCKS
 #define ISEG_WGRAD_BLOCKS 384      // target blocks of a split backward-weight launch
 #endif
@@ -2562,6 +2867,24 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         wp += big;
     }
     int rc;
+    const int stem = stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K);
+    if (stem && g->N > 0) {
+        HaloArgs h{};
+        h.src = x; h.wmat = w; h.out = (int32_t*)y;
+        h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)g->C;
+        h.Ho = (int32_t)P; h.Wo = (int32_t)Q; h.Nout = (int32_t)g->K;
+        h.ph = g->pad_h; h.pw = g->pad_w; h.dh = 1; h.dw = 1;
+        if (out_mode == ISEG_OUT_RAW) {
+            if ((rc = launch_stem(stem, h, EPI_RAW, ISEG_KID_CONV_FWD, stream))) return rc;
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
+            return launch_ok();
+        }
+        h.pmax = pmax;
+        h.npmax = (int64_t)g->N * ceil_div64(P, 16) * ceil_div64(Q, 32) * (g->K / 64);
+        if ((rc = launch_stem(stem, h, EPI_MAX, ISEG_KID_CONV_FWD, stream))) return rc;
+        h.out8 = (int8_t*)y; h.exp_a = x_exp; h.exp_b = w_exp; h.out_exp = y_exp;
+        return launch_stem(stem, h, EPI_Q8, ISEG_KID_CONV_FWD, stream);
+    }
     // small C: zero-pad channels to a multiple of 16 for the vector path
     const int8_t* xs = x;
     const int8_t* wsrc = w;
@@ -2799,6 +3122,8 @@ extern "C" size_t iseg_conv_bwd_weight_ws(const iseg_conv_geom* g, int32_t g_mod
     if (Cp != g->C)
         s += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp) * 8);
     s += wgrad_taps_part_bytes(g->N * P * Q, g->K, Cp, g->R * g->S);
+    if (stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K))
+        s += align256((size_t)(g->N * ceil_div64(P, 16) * ceil_div64(Q, 32)) * g->K * g->R * g->S * g->C * 4);
     return s;
 }
 
@@ -2825,6 +3150,39 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     unsigned long long* accp = acc;
     int rc = launch_fill_u32(maxp, 2, 0, stream);
     if (rc) return rc;
+    const int stem = stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K);
+    if (stem && g->N > 0 && ((uintptr_t)dy & 15) == 0) {
+        // few-channel stem: MFMA over pixels, block partials, int64 sum + max
+        if (Cp != g->C) {                                   // skip the padded-operand regions
+            wp += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp) * 8);
+        }
+        wp += wgrad_taps_part_bytes(g->N * P * Q, g->K, Cp, g->R * g->S);
+        int32_t* spart = (int32_t*)wp;
+        HaloArgs h{};
+        h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)g->C;
+        h.Ho = (int32_t)P; h.Wo = (int32_t)Q; h.Nout = (int32_t)g->K; h.ph = g->pad_h; h.pw = g->pad_w;
+        h.tiles_y = (int)ceil_div64(P, 16); h.tiles_x = (int)ceil_div64(Q, 32);
+        const unsigned nbx = (unsigned)(g->N * h.tiles_y * h.tiles_x);
+        dim3 grid(nbx, (unsigned)(g->K / 64));
+        if (stem == 1)
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, stream, (k_wgrad_stem<3, 3, 3, 1>), grid, dim3(256), 0, stream, dy,
+                              x, spart, h);
+        else
+            ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, stream, (k_wgrad_stem<3, 7, 7, 2>), grid, dim3(256), 0, stream, dy,
+                              x, spart, h);
+        if ((rc = launch_ok())) return rc;
+        const bool want_max = g_mode != ISEG_G_RAW;
+        hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)ceil_div64(nw, 256)), dim3(64 * kRedWaves), 0, stream,
+                           (const int32_t*)spart, nw, (int)nbx, (long long*)acc, want_max ? maxp : nullptr);
+        if ((rc = launch_ok())) return rc;
+        if (!want_max) {
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dw_exp, dy_exp, x_exp);
+            return launch_ok();
+        }
+        const int keep = g_mode == ISEG_G_KEEP;
+        return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr, 0, bits, 1,
+                                    keep, seed, tensor_id, step, ISEG_I8, dw, dw_exp, maxp, stream);
+    }
     if (Cp != g->C) {
         int8_t* xp = (int8_t*)wp;
         wp += align256((size_t)(g->N * g->H * g->W * Cp));
