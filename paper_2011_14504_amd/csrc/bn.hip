@@ -302,17 +302,19 @@ __device__ __forceinline__ void copy_rows_to_lds(int8_t* dst, const int8_t* __re
 // forward workspace
 // ---------------------------------------------------------------------------
 struct FwdWs {
-    int32_t* b_glob;                 // exponent of Q_xhat's scale (atomicMax)
-    unsigned long long* maxY;
+    int32_t* b_glob;                 // exponent of Q_xhat's scale (atomicMax over channels)
+    unsigned long long* maxY;        // unused (kept for the layout)
     int32_t *p_s1, *p_min, *p_max;   // [gx][C] partials
     long long* p_abs;                // [gx][C]
     long long* Y;                    // [C][256] y on the grid 2^e_y (before ReLU)
+    unsigned long long* maxYc;       // [C] max |ReLU(y)| of channel c over its occupied codes
 };
 
 size_t fwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C;
-    return 256 + 3 * align256(pc * 4) + align256(pc * 8) + align256((size_t)st.C * 256 * 8);
+    return 256 + 3 * align256(pc * 4) + align256(pc * 8) + align256((size_t)st.C * 256 * 8) +
+           align256((size_t)st.C * 8);
 }
 
 FwdWs fwd_ws_map(void* base, const Stream& st)
@@ -327,7 +329,8 @@ FwdWs fwd_ws_map(void* base, const Stream& st)
     w.p_min = (int32_t*)p; p += align256(pc * 4);
     w.p_max = (int32_t*)p; p += align256(pc * 4);
     w.p_abs = (long long*)p; p += align256(pc * 8);
-    w.Y = (long long*)p;
+    w.Y = (long long*)p; p += align256((size_t)st.C * 256 * 8);
+    w.maxYc = (unsigned long long*)p;
     return w;
 }
 
@@ -515,12 +518,30 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w,
     sv.btab[c * 256 + (q & 255)] = ((uint32_t)(uint16_t)(int16_t)nx << 16) | ((uint32_t)(sg & 3) << 8) |
                                    ((uint32_t)(sg != 0) << 10) | (Y > 0 ? 1u : 0u);
     w.Y[idx] = (long long)Y;
-    if (D >= 0) atomicMin(&sv.t0[c], q);
-    if (D > 0) atomicMin(&sv.p0[c], q);
-    if (Y > 0) { atomicMin(&sv.mlo[c], q); atomicMax(&sv.mhi[c], q); }
-    if (q == sv.qmin[c] || q == sv.qmax[c]) {
-        i128 Yr = cf.relu && Y < 0 ? 0 : Y;
-        atomicMax(w.maxY, (unsigned long long)abs128(Yr));
+    // thresholds (least code with D >= 0, least with D > 0, code range with y > 0)
+    // and the channel's max |ReLU(y)| over its occupied code extremes, by block
+    // reductions: same-address atomics would serialize 256 updates per channel
+    int v0 = D >= 0 ? q : 128, v1 = D > 0 ? q : 128, v2 = Y > 0 ? q : 128, v3 = Y > 0 ? q : -129;
+    const i128 Yr = cf.relu && Y < 0 ? 0 : Y;
+    uint64_t ay = (q == sv.qmin[c] || q == sv.qmax[c]) ? (uint64_t)abs128(Yr) : 0;
+    for (int o = 32; o > 0; o >>= 1) {
+        v0 = min(v0, __shfl_xor(v0, o)); v1 = min(v1, __shfl_xor(v1, o));
+        v2 = min(v2, __shfl_xor(v2, o)); v3 = max(v3, __shfl_xor(v3, o));
+        const uint64_t t = __shfl_xor(ay, o);
+        ay = t > ay ? t : ay;
+    }
+    __shared__ int32_t red[4][4];
+    __shared__ uint64_t ry[4];
+    const int wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) { red[wv][0] = v0; red[wv][1] = v1; red[wv][2] = v2; red[wv][3] = v3; ry[wv] = ay; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int k = 1; k < 4; k++) {
+            v0 = min(v0, red[k][0]); v1 = min(v1, red[k][1]); v2 = min(v2, red[k][2]); v3 = max(v3, red[k][3]);
+            ay = ry[k] > ay ? ry[k] : ay;
+        }
+        sv.t0[c] = v0; sv.p0[c] = v1; sv.mlo[c] = v2; sv.mhi[c] = v3;
+        w.maxYc[c] = ay;
     }
 }
 
@@ -535,7 +556,9 @@ __global__ __launch_bounds__(256) void k_bnf_fin3(const int32_t* x_exp, FwdWs w,
     const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
     const int e_xh = b - (cf.k_xhat - 1);
     const int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
-    uint64_t M = *w.maxY;
+    uint64_t M = 0;                                  // max over the channels' candidates
+    for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) M = w.maxYc[k] > M ? w.maxYc[k] : M;
+    M = block_max_u64(M);
     int r = M ? bitlen_u64(M) - (cf.k_A - 1) : 0;
     int idx = c * 256 + threadIdx.x;
     long long Y = w.Y[idx];

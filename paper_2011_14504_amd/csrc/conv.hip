@@ -1382,7 +1382,8 @@ M32Plan m32_plan(int64_t N, int64_t Ho, int64_t Wo, int64_t Ci, int64_t Nout, in
     if (G < 8) G = 8;
     if (G > ntiles) G = ntiles;
     p.G = (int)G;
-    p.persist = p.plds <= 160 * 1024 && ntiles >= 2 * G;
+    p.persist = false;   // measured slower than two resident blocks per CU at these sizes
+    (void)ntiles;
     return p;
 }
 
