@@ -216,17 +216,16 @@ BnCfg to_cfg(const iseg_bn_cfg* c)
     return b;
 }
 
-// block-wide reductions of one value per thread (256 threads)
+// block-wide reduction of one value per thread (256 threads): xor-shuffles
+// within each wave, then the four wave results through LDS (two barriers)
 template <typename T, typename Op>
 __device__ __forceinline__ T block_reduce(T v, Op op, T* sh)
 {
-    sh[threadIdx.x] = v;
+    for (int o = 32; o > 0; o >>= 1) v = op(v, (T)__shfl_xor(v, o, 64));
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
     __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-        if ((int)threadIdx.x < o) sh[threadIdx.x] = op(sh[threadIdx.x], sh[threadIdx.x + o]);
-        __syncthreads();
-    }
     T r = sh[0];
+    for (int k = 1; k < (int)(blockDim.x >> 6); k++) r = op(r, sh[k]);
     __syncthreads();
     return r;
 }

@@ -30,9 +30,16 @@ ISEG_HD i128 abs128(i128 v) { return v < 0 ? -v : v; }
 ISEG_HD int bitlen_i128(i128 v) { return bitlen_u128((u128)abs128(v)); }
 ISEG_HD i128 pow2_128(int e) { return (i128)1 << e; }
 
-// floor(a / b) for b > 0
+// floor(a / b) for b > 0; operands that fit 64 bits take the 64-bit divide
+// (a 128-bit divide is a long software loop on the GPU)
 ISEG_HD i128 floordiv128(i128 a, i128 b)
 {
+    if (a == (i128)(int64_t)a && b == (i128)(int64_t)b) {
+        const int64_t x = (int64_t)a, y = (int64_t)b;
+        int64_t q = x / y;
+        if (x % y != 0 && x < 0) q -= 1;
+        return q;
+    }
     i128 q = a / b;
     if ((a % b) != 0 && a < 0) q -= 1;
     return q;
