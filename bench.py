@@ -63,11 +63,11 @@ def timed_kernel_info(name, N, detail):
     ops = 2 * detail[1]["macs"]
     table = {
         "conv_fwd": (iseg.ISEG_KID_CONV_FWD, conv_key, "mfma", ops,
-                     "k_conv_igemm fwd (conv1_2, 64->64 3x3, 224x224)"),
+                     "k_conv3x3_m32 fwd, max pass (conv1_2, 64->64 3x3, 224x224)"),
         "conv_bwd_data": (iseg.ISEG_KID_CONV_BWD_DATA, conv_key, "mfma", ops,
-                          "k_conv_igemm bwd-data (conv1_2)"),
+                          "k_conv3x3_m32 bwd-data, max pass (conv1_2)"),
         "conv_wgrad": (iseg.ISEG_KID_CONV_WGRAD, conv_key, "mfma", ops,
-                       "k_conv_wgrad (conv1_2)"),
+                       "k_conv_wgrad_taps (conv1_2)"),
         # bytes per element: stats reads x and dy; apply reads x, dy and writes dx
         "bn_bwd_stats": (iseg.ISEG_KID_BN_BWD_STATS, (M, C), "hbm", 2 * M * C,
                          "k_bnb_stats (L1BN backward statistics, conv1_2 output)"),
@@ -79,7 +79,7 @@ def timed_kernel_info(name, N, detail):
                          "k_bnf_apply (L1BN forward output pass, conv1_2 output)"),
         # reads x (M C) and dy (M C / 4), writes dx (M C)
         "maxpool_bwd": (iseg.ISEG_KID_MAXPOOL_BWD, (N, 224, 224, 64), "hbm", M * C * 9 // 4,
-                        "k_maxpool_bwd_disjoint (2x2/2 after conv1_2)"),
+                        "k_maxpool_bwd_win (2x2/2 after conv1_2)"),
     }
     kid, key, bound, work, label = table[name]
     return dict(kid=kid, key=key, bound=bound, work=work, name=label)
@@ -110,7 +110,7 @@ def main():
     ap.add_argument("--batch", type=int, default=8)
     ap.add_argument("--cpu-images", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--timed-kernel", default="bn_bwd_stats",
+    ap.add_argument("--timed-kernel", default="conv_fwd",
                     choices=["conv_fwd", "conv_bwd_data", "conv_wgrad", "bn_bwd_stats",
                              "bn_bwd_apply", "bn_fwd_stats1", "bn_fwd_apply", "maxpool_bwd"])
     args = ap.parse_args()
