@@ -178,6 +178,35 @@ int orc_quantize_f32(const float* x, int64_t n, int k, int mode,
     return ORC_OK;
 }
 
+/* The same quantizer on float64 input (the loss gradient of the float
+ * softmax region is held in double precision): identical rules, the decision
+ * floor(v + 1/2) taken exactly on the double value. */
+int orc_quantize_f64(const double* x, int64_t n, int k, int mode,
+                     int64_t* codes, int32_t* exp_out)
+{
+    if (k < 2 || k > 31 || n < 0) return ORC_ERR_ARG;
+    double M = 0.0;
+    for (int64_t i = 0; i < n; i++) {
+        if (!isfinite(x[i])) return ORC_ERR_RANGE;
+        double a = fabs(x[i]);
+        if (a > M) M = a;
+    }
+    int b = 0;
+    if (mode == 1) {
+        if (M > 0.0) {
+            int e;
+            frexp(M, &e);
+            b = e;
+        }
+    } else if (mode != 0) {
+        return ORC_ERR_ARG;
+    }
+    for (int64_t i = 0; i < n; i++)
+        codes[i] = orc_uq_code_f64(ldexp(x[i], -b), k);
+    *exp_out = b + 1 - k;
+    return ORC_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Eq. 4 (SQ) and Eq. 5-6 (RQ) on an integer tensor with exponent in_exp.    */
 /* Scale(x) (Eq. 3) read as the smallest power of two strictly greater than  */

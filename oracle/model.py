@@ -1,15 +1,22 @@
-"""Oracle of one integer training step of a conv / L1BN / ReLU / max-pool
-stack (TEST INFRASTRUCTURE ONLY), composed from the oracle's functions in the
-order of the paper's dataflow (Sec. 3):
+"""Oracle of one integer training step of a workload graph (TEST
+INFRASTRUCTURE ONLY), composed from the oracle's functions in the order of the
+paper's dataflow (Sec. 3):
 
-  forward   W_q = Q_W(W_m) (Eq. 8); Z = SQ8(conv(A, W_q)) (Eq. 15);
-            A' = Q_A(ReLU(L1BN(Z))) (Eq. 12-15); max pooling keeps codes
-  backward  L1BN backward -> G = Q_G(sum dy x) (Eq. 17, stochastic),
-            E1 = Q_E(sum dy w) (Eq. 16), Q_G of the raw dgamma / dbeta sums
+  forward   W_q = Q_W(W_m) (Eq. 8); Z = SQ8(conv(A, W_q)) (Eq. 15); with BN
+            A' = Q_A(ReLU?(L1BN(Z))) (Eq. 12-15); max pooling keeps codes;
+            residual add, concatenation and global pooling are SQ8 of the
+            exact result
+  loss      given int8 error at the output, or the float64 softmax
+            cross-entropy of the bilinearly upsampled logits whose gradient
+            is quantized by SQ8 (the error E1 at the logits)
+  backward  nodes in reverse order; the error of a tensor read by several
+            nodes is SQ8 of the exact sum of what they send back (Eq. 16);
+            L1BN backward -> G = Q_G(sum dy x) (Eq. 17, stochastic), E1 =
+            Q_E(sum dy w) (Eq. 16), Q_G of the raw dgamma / dbeta sums
   update    Eq. 19 on the 24-bit masters (lr = 2^-lr_shift), then Eq. 8
 
 Stochastic rounding keys: workload seed, step, tensor id 16*l + {0,1,2} for
-W, gamma, beta of conv layer l = 1, 2, ...
+W, gamma, beta of the l-th conv (l = 1, 2, ... in node order).
 """
 import numpy as np
 
@@ -26,86 +33,175 @@ class OracleNet:
         self.cfg = dict(O.BN_DEFAULT, **(bn_cfg or {}))
         self.step_no = 0
         self.x, self.x_exp = inputs["x"], inputs["x_exp"]
-        self.dy, self.dy_exp = inputs["dy"], inputs["dy_exp"]
+        self.dy, self.dy_exp = inputs.get("dy"), inputs.get("dy_exp")
+        self.labels = inputs.get("labels")
         self.w_exp = 1 - K_U + K_U - K_W          # -7
-        self.convs = []
-        wi = 0
-        for layer in wl["layers"]:
-            if layer[0] != "conv":
+        self.convs = {}
+        ci = 0
+        for nd in wl["nodes"]:
+            if nd["kind"] != "conv":
                 continue
-            _, cin, cout, R, st, pad, dil = layer
-            w_m, e = O.master_init(inputs["weights"][wi], K_U)   # Eq. 7
-            wi += 1
+            w_m, e = O.master_init(inputs["weights"][ci], K_U)   # Eq. 7
+            ci += 1
+            cout = nd["cout"]
             g_m = np.full(cout, 1 << (K_U - 2), np.int32)           # gamma = 1 at 2^-22
             b_m = np.zeros(cout, np.int32)
-            self.convs.append(dict(cin=cin, cout=cout, R=R, st=st, pad=pad, dil=dil,
-                                   w_m=w_m, g_m=g_m, b_m=b_m,
-                                   w_q=O.weight_quant(w_m, K_U, K_W),
-                                   g_q=O.weight_quant(g_m, K_U, K_W),
-                                   b_q=O.weight_quant(b_m, K_U, K_W)))
+            self.convs[nd["name"]] = dict(l=ci, w_m=w_m, g_m=g_m, b_m=b_m,
+                                          w_q=O.weight_quant(w_m, K_U, K_W),
+                                          g_q=O.weight_quant(g_m, K_U, K_W),
+                                          b_q=O.weight_quant(b_m, K_U, K_W))
+        self.loss = None
+
+    def _bn_cfg(self, nd):
+        return dict(self.cfg, relu=int(nd["relu"]))
 
     @staticmethod
-    def _geom(a_shape, L):
+    def _geom(a_shape, nd):
         N, H, W, C = a_shape
-        return (N, H, W, C, L["cout"], L["R"], L["R"], L["st"], L["st"], L["pad"], L["pad"],
-                L["dil"], L["dil"])
+        return (N, H, W, C, nd["cout"], nd["R"], nd["R"], nd["stride"], nd["stride"], nd["pad"],
+                nd["pad"], nd["dil"], nd["dil"])
 
+    # ------------------------------------------------------------------
     def forward(self):
-        a, ae = self.x, self.x_exp
-        rec = []
-        ci = 0
-        for layer in self.wl["layers"]:
-            if layer[0] == "conv":
-                L = self.convs[ci]
-                ci += 1
-                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, L))
+        act = {"input": (self.x, self.x_exp)}
+        rec = {}
+        for nd in self.wl["nodes"]:
+            k, name = nd["kind"], nd["name"]
+            a, ae = act[nd["src"][0]]
+            r = dict(kind=k, a_in=a, a_in_exp=ae)
+            if k == "conv":
+                L = self.convs[name]
+                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd))
                 z = z.astype(np.int8)
-                r = O.bn_fwd(z, ze, L["g_q"], L["b_q"], self.cfg)
-                rec.append(dict(kind="conv", L=L, a_in=a, a_in_exp=ae, z=z, z_exp=ze,
-                                a_out=r["y"], a_out_exp=r["y_exp"], bn=r))
-                a, ae = r["y"], r["y_exp"]
+                r.update(z=z, z_exp=ze)
+                if nd["bn"]:
+                    b = O.bn_fwd(z, ze, L["g_q"], L["b_q"], self._bn_cfg(nd))
+                    y, ye = b["y"], b["y_exp"]
+                else:
+                    y, ye = z, ze
+            elif k == "maxpool":
+                y, ye = O.maxpool_fwd(a, nd["k"], nd["stride"], nd["pad"]), ae
+            elif k == "add":
+                b_, be = act[nd["src"][1]]
+                y, ye = O.sum_requant([a, b_], [ae, be], 8, relu=nd["relu"])
+                y = y.astype(np.int8)
+                r.update(b_in=b_, b_in_exp=be)
+            elif k == "gap":
+                y, ye = O.gap_fwd(a, ae)
+                y = y.astype(np.int8)
+            elif k == "concat":
+                parts = [act[s] for s in nd["src"]]
+                H = max(p[0].shape[1] for p in parts)
+                W = max(p[0].shape[2] for p in parts)
+                y, ye = O.concat_requant([p[0] for p in parts], [p[1] for p in parts], (H, W))
+                y = y.astype(np.int8)
+                r.update(widths=[p[0].shape[3] for p in parts],
+                         bcast=[p[0].shape[1:3] != (H, W) for p in parts])
             else:
-                _, k, st, pad = layer
-                y = O.maxpool_fwd(a, k, st, pad)
-                rec.append(dict(kind="pool", k=k, st=st, pad=pad, a_in=a, a_out=y, a_out_exp=ae))
-                a = y
+                raise ValueError(k)
+            r.update(a_out=y, a_out_exp=ye)
+            rec[name] = r
+            act[name] = (y, ye)
         return rec
 
+    # ------------------------------------------------------------------
+    def loss_error(self, rec):
+        """The error arriving at the output node, and the loss if any."""
+        out = rec[self.wl["nodes"][-1]["name"]]
+        if self.wl["loss"] == "given":
+            return self.dy, self.dy_exp
+        loss, grad = O.softmax_ce(out["a_out"], out["a_out_exp"], self.labels)
+        e, ee = O.quantize_f64(grad, 8)
+        self.loss, self.loss_grad = loss, grad
+        return e.astype(np.int8), ee
+
     def backward(self, rec):
-        e, ee = self.dy, self.dy_exp
+        contrib = {}
+
+        def send(name, codes, exp):
+            contrib.setdefault(name, []).append((codes, exp))
+
+        def merged(name):
+            parts = contrib.pop(name)
+            if len(parts) == 1:
+                return parts[0]
+            e, ee = O.sum_requant([p[0] for p in parts], [p[1] for p in parts], 8)
+            return e.astype(np.int8), ee
+
+        e, ee = self.loss_error(rec)
+        send(self.wl["nodes"][-1]["name"], e, ee)
+        want_input = self.wl["input_grad"]
         grads = []
-        li = len(self.convs)
-        for r in reversed(rec):
-            if r["kind"] == "pool":
-                e, ee = O.maxpool_bwd(e, ee, r["a_in"], r["k"], r["st"], r["pad"])
-                e = e.astype(np.int8)
-                r["e_in"], r["e_in_exp"] = e, ee
-                continue
-            L = r["L"]
-            b = O.bn_bwd(e, ee, r["z"], r["z_exp"], L["g_q"], L["b_q"], self.cfg)
-            dz, dze = b["dx"], b["dx_exp"]
-            geom = self._geom(r["a_in"].shape, L)
-            G, Ge = O.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], geom, 8, True, self.seed,
-                                      16 * li, self.step_no)
-            Gg, Gge = O.requant(b["dgamma"], b["dgamma_exp"], 8, True, True, self.seed, 16 * li + 1,
-                                self.step_no)
-            Gb, Gbe = O.requant(b["dbeta"], b["dbeta_exp"], 8, True, True, self.seed, 16 * li + 2,
-                                self.step_no)
-            r.update(dz=dz, dz_exp=dze, dgamma=b["dgamma"], dbeta=b["dbeta"], G=G, G_exp=Ge,
-                     Gg=Gg, Gg_exp=Gge, Gb=Gb, Gb_exp=Gbe)
-            grads.append((L, G, Ge, Gg, Gge, Gb, Gbe))
-            if li > 1 or self.wl["input_grad"]:
-                e, ee = O.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, geom)
-                e = e.astype(np.int8)
-                r["e_in"], r["e_in_exp"] = e, ee
-            li -= 1
+        for nd in reversed(self.wl["nodes"]):
+            k, name = nd["kind"], nd["name"]
+            r = rec[name]
+            e, ee = merged(name)
+            r.update(e_out=e, e_out_exp=ee)
+            src = nd["src"][0]
+            need_in = src != "input" or want_input
+            if k == "conv":
+                L = self.convs[name]
+                if nd["bn"]:
+                    b = O.bn_bwd(e, ee, r["z"], r["z_exp"], L["g_q"], L["b_q"], self._bn_cfg(nd))
+                    dz, dze = b["dx"], b["dx_exp"]
+                    l = L["l"]
+                    Gg, Gge = O.requant(b["dgamma"], b["dgamma_exp"], 8, True, True, self.seed,
+                                        16 * l + 1, self.step_no)
+                    Gb, Gbe = O.requant(b["dbeta"], b["dbeta_exp"], 8, True, True, self.seed,
+                                        16 * l + 2, self.step_no)
+                    r.update(dgamma=b["dgamma"], dbeta=b["dbeta"], Gg=Gg, Gg_exp=Gge, Gb=Gb,
+                             Gb_exp=Gbe)
+                else:
+                    dz, dze = e, ee
+                geom = self._geom(r["a_in"].shape, nd)
+                G, Ge = O.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], geom, 8, True,
+                                          self.seed, 16 * L["l"], self.step_no)
+                r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
+                grads.append((nd, r))
+                if need_in:
+                    ei, eie = O.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, geom)
+                    ei = ei.astype(np.int8)
+                    r.update(e_in=ei, e_in_exp=eie)
+                    send(src, ei, eie)
+            elif k == "maxpool":
+                if need_in:
+                    ei, eie = O.maxpool_bwd(e, ee, r["a_in"], nd["k"], nd["stride"], nd["pad"])
+                    ei = ei.astype(np.int8)
+                    r.update(e_in=ei, e_in_exp=eie)
+                    send(src, ei, eie)
+            elif k == "add":
+                d = O.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]])
+                r.update(e_in=d, e_in_exp=ee)
+                for s in nd["src"]:
+                    if s != "input" or want_input:
+                        send(s, d, ee)
+            elif k == "gap":
+                if need_in:
+                    H, W = r["a_in"].shape[1:3]
+                    send(src, e, O.gap_bwd_exp(ee, H, W))
+            elif k == "concat":
+                parts = O.concat_split(e, r["widths"])
+                for s, p, bc in zip(nd["src"], parts, r["bcast"]):
+                    if bc:
+                        pe, pee = O.bcast_bwd(p, ee)
+                        send(s, pe.astype(np.int8), pee)
+                    else:
+                        send(s, p, ee)
+        if want_input:
+            e, ee = merged("input")
+            rec["input"] = dict(kind="input", e_out=e, e_out_exp=ee)
         return grads
 
     def update(self, grads):
-        for (L, G, Ge, Gg, Gge, Gb, Gbe) in grads:
-            L["w_m"], L["w_q"] = O.weight_update(L["w_m"], G, Ge, self.lr_shift, 1 - K_U, K_U, K_W)
-            L["g_m"], L["g_q"] = O.weight_update(L["g_m"], Gg, Gge, self.lr_shift, 2 - K_U, K_U, K_W)
-            L["b_m"], L["b_q"] = O.weight_update(L["b_m"], Gb, Gbe, self.lr_shift, 2 - K_U, K_U, K_W)
+        for nd, r in grads:
+            L = self.convs[nd["name"]]
+            L["w_m"], L["w_q"] = O.weight_update(L["w_m"], r["G"], r["G_exp"], self.lr_shift,
+                                                 1 - K_U, K_U, K_W)
+            if nd["bn"]:
+                L["g_m"], L["g_q"] = O.weight_update(L["g_m"], r["Gg"], r["Gg_exp"], self.lr_shift,
+                                                     2 - K_U, K_U, K_W)
+                L["b_m"], L["b_q"] = O.weight_update(L["b_m"], r["Gb"], r["Gb_exp"], self.lr_shift,
+                                                     2 - K_U, K_U, K_W)
 
     def step(self):
         rec = self.forward()

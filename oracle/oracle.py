@@ -44,6 +44,7 @@ def lib():
         L.orc_uq_code_f64.argtypes = [C.c_double, C.c_int]
         L.orc_uq_code_f64.restype = i64
         L.orc_quantize_f32.argtypes = [P, i64, C.c_int, C.c_int, P, P]
+        L.orc_quantize_f64.argtypes = [P, i64, C.c_int, C.c_int, P, P]
         L.orc_requant.argtypes = [P, i64, i32, C.c_int, C.c_int, C.c_int, u64, u32, u32, P, P]
         for f in ("orc_conv_fwd_raw", "orc_conv_bwd_data_raw", "orc_conv_bwd_weight_raw"):
             getattr(L, f).argtypes = [P, P, P, P]
@@ -104,6 +105,16 @@ def quantize_f32(x, k, mode="sq"):
     e = np.zeros(1, dtype=np.int32)
     rc = lib().orc_quantize_f32(_p(x), x.size, int(k), {"uq": 0, "sq": 1}[mode], _p(codes), _p(e))
     _check(rc, "quantize_f32")
+    return codes, int(e[0])
+
+
+def quantize_f64(x, k, mode="sq"):
+    """float64 tensor -> (int64 codes, exponent), the same rules as quantize_f32."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    codes = np.zeros(x.shape, dtype=np.int64)
+    e = np.zeros(1, dtype=np.int32)
+    rc = lib().orc_quantize_f64(_p(x), x.size, int(k), {"uq": 0, "sq": 1}[mode], _p(codes), _p(e))
+    _check(rc, "quantize_f64")
     return codes, int(e[0])
 
 
@@ -297,3 +308,139 @@ def maxpool_bwd_raw(dy, x, k, stride, pad):
 def maxpool_bwd(dy, dy_exp, x, k, stride, pad, k_E1=8):
     """Routed errors, then Q_E (Eq. 16)."""
     return requant(maxpool_bwd_raw(dy, x, k, stride, pad), dy_exp, k_E1)
+
+
+# --------------------------------------------------------------------------
+# merges of quantized tensors (residual add, ASPP concat, pooling branch)
+# --------------------------------------------------------------------------
+# A merge takes int8 tensors a_i with exponents e_i, forms the exact real
+# result on the grid 2^min(e_i) and applies one quantizer to it: every tensor
+# the dataflow carries is an 8-bit object with one scale (Sec. 3.1), so a sum
+# or a concatenation of such objects is requantized as a new object (Eq. 4,
+# or Eq. 16 for errors).  Exponent gaps above MAX_GAP are rejected so that the
+# aligned terms stay far inside int64.
+MAX_GAP = 48
+
+
+def _align(tensors, exps):
+    e0 = min(int(e) for e in exps)
+    if max(int(e) for e in exps) - e0 > MAX_GAP:
+        raise OracleError("merge: exponent gap above %d" % MAX_GAP)
+    return [np.asarray(t, dtype=np.int64) * (np.int64(1) << np.int64(int(e) - e0))
+            for t, e in zip(tensors, exps)], e0
+
+
+def exact_sum(tensors, exps):
+    """Exact sum of code tensors (value = code 2^e) on the grid 2^min(e);
+    a [N,1,1,C] term is broadcast over the spatial axes."""
+    terms, e0 = _align(tensors, exps)
+    shape = np.broadcast_shapes(*[t.shape for t in terms])
+    s = np.zeros(shape, dtype=np.int64)
+    for t in terms:
+        s = s + t
+    return s, e0
+
+
+def sum_requant(tensors, exps, k=8, relu=False):
+    """SQ_k(ReLU?(sum_i a_i 2^e_i)): residual add (with the ReLU that follows
+    it) and the sum of the errors a tensor receives from several consumers."""
+    s, e0 = exact_sum(tensors, exps)
+    if relu:
+        s = np.maximum(s, 0)
+    return requant(s, e0, k)
+
+
+def relu_mask_bwd(dy, tensors, exps):
+    """Backward of ReLU(sum_i a_i 2^e_i): dy where the exact sum is > 0, else 0
+    (the values stay on dy's grid, so dy's exponent is kept)."""
+    s, _ = exact_sum(tensors, exps)
+    return np.where(s > 0, np.asarray(dy, dtype=np.int64), 0).astype(np.int8)
+
+
+def concat_requant(tensors, exps, spatial=None, k=8):
+    """SQ_k of the channel concatenation of a_i 2^e_i (one object, one scale).
+    A [N,1,1,C] part is broadcast to `spatial` = (H, W) first."""
+    terms, e0 = _align(tensors, exps)
+    if spatial is not None:
+        terms = [np.broadcast_to(t, t.shape[:1] + tuple(spatial) + t.shape[3:]) for t in terms]
+    return requant(np.concatenate(terms, axis=-1), e0, k)
+
+
+def concat_split(dy, widths):
+    """Backward of a concatenation: the channel slices of dy, dy's exponent."""
+    out, c0 = [], 0
+    for w in widths:
+        out.append(np.ascontiguousarray(dy[..., c0:c0 + w]))
+        c0 += w
+    return out
+
+
+def gap_fwd(x, x_exp, k=8):
+    """Global average pooling over H x W (a power of two, so the mean is the
+    exact sum with exponent x_exp - log2(HW)), then SQ_k."""
+    N, H, W, Cc = x.shape
+    t = (H * W).bit_length() - 1
+    if (1 << t) != H * W:
+        raise OracleError("gap: H*W must be a power of two")
+    s = np.asarray(x, dtype=np.int64).sum(axis=(1, 2), keepdims=True)
+    return requant(s, x_exp - t, k)
+
+
+def gap_bwd_exp(dy_exp, H, W):
+    """Backward of the mean: every input position receives dy / (H W); the
+    codes are dy's, broadcast, and the exponent drops by log2(H W)."""
+    t = (H * W).bit_length() - 1
+    return dy_exp - t
+
+
+def bcast_bwd(dy, dy_exp, k=8):
+    """Backward of broadcasting a [N,1,1,C] tensor over H x W: the exact
+    spatial sum of the error, then Q_E = SQ_k (Eq. 16)."""
+    s = np.asarray(dy, dtype=np.int64).sum(axis=(1, 2), keepdims=True)
+    return requant(s, dy_exp, k)
+
+
+# --------------------------------------------------------------------------
+# float region of the segmentation loss (float64)
+# --------------------------------------------------------------------------
+def bilinear_matrix(n_in, n_out):
+    """[n_out, n_in] matrix of 1-D linear interpolation with half-pixel
+    centres (source coordinate (o + 1/2) n_in / n_out - 1/2, clamped at 0;
+    the upper neighbour clamped at n_in - 1)."""
+    A = np.zeros((n_out, n_in), dtype=np.float64)
+    for o in range(n_out):
+        src = (o + 0.5) * n_in / n_out - 0.5
+        if src < 0:
+            src = 0.0
+        i0 = int(np.floor(src))
+        i1 = min(i0 + 1, n_in - 1)
+        lam = src - i0
+        A[o, i0] += 1.0 - lam
+        A[o, i1] += lam
+    return A
+
+
+def softmax_ce(logits, logit_exp, labels):
+    """Pixel-wise softmax cross-entropy of the bilinearly upsampled logits.
+    logits: int codes [N,h,w,K] with exponent logit_exp; labels [N,H,W] in
+    [0, K).  Returns (mean loss, d loss / d logits as float64 [N,h,w,K])."""
+    N, h, w, K = logits.shape
+    _, H, W = labels.shape
+    Ay, Ax = bilinear_matrix(h, H), bilinear_matrix(w, W)
+    x = np.asarray(logits, dtype=np.float64) * 2.0 ** logit_exp
+    loss = 0.0
+    grad = np.zeros((N, h, w, K), dtype=np.float64)
+    P = N * H * W
+    for n in range(N):
+        up = np.einsum("yi,ijk,xj->yxk", Ay, x[n], Ax, optimize=True)   # [H, W, K]
+        m = up.max(axis=-1, keepdims=True)
+        z = np.exp(up - m)
+        s = z.sum(axis=-1, keepdims=True)
+        lab = labels[n].astype(np.int64)
+        logp = (up - m - np.log(s))
+        loss -= np.take_along_axis(logp, lab[..., None], axis=-1).sum()
+        g = z / s
+        np.put_along_axis(g, lab[..., None], np.take_along_axis(g, lab[..., None], -1) - 1.0, -1)
+        g /= P
+        grad[n] = np.einsum("yi,yxk,xj->ijk", Ay, g, Ax, optimize=True)
+    return loss / P, grad

@@ -58,48 +58,195 @@ def uniform_f32(seed, shape, lo=-1.0, hi=1.0):
 # ---------------------------------------------------------------------------
 # workload shapes (shapes and seeds only)
 # ---------------------------------------------------------------------------
-# A layer is ("conv", C_in, C_out, R, stride, pad, dilation) -- each conv is
-# followed by L1BN + ReLU -- or ("maxpool", k, stride, pad).
+# A workload is a list of nodes in topological order; each node names its
+# input node(s) ("input" is the workload's input tensor):
+#   conv     src, cin, cout, R, stride, pad, dil, bn, relu
+#            conv -> SQ8; then, if bn, L1BN (+ ReLU if relu) -> Q_A
+#   maxpool  src, k, stride, pad
+#   add      srcs = [a, b], relu: residual merge SQ8(ReLU(a + b))
+#   gap      src: global average pooling over H x W -> [N,1,1,C]
+#   concat   srcs: channel concatenation, SQ8; a [N,1,1,C] source (the
+#            image-pooling branch) is broadcast over the spatial size first
+# The last node is the output.  loss = "given": an int8 error (uniform codes,
+# exponent -20) arrives at the output; "softmax_ce": the output logits are
+# upsampled bilinearly to the image size and scored against per-pixel labels.
+
+
+def conv(name, src, cin, cout, R, stride=1, pad=0, dil=1, bn=True, relu=True):
+    return dict(kind="conv", name=name, src=[src], cin=cin, cout=cout, R=R, stride=stride,
+                pad=pad, dil=dil, bn=bn, relu=relu)
+
+
+def maxpool(name, src, k, stride, pad=0):
+    return dict(kind="maxpool", name=name, src=[src], k=k, stride=stride, pad=pad)
+
+
+def add_relu(name, a, b):
+    return dict(kind="add", name=name, src=[a, b], relu=True)
+
+
+def gap(name, src):
+    return dict(kind="gap", name=name, src=[src])
+
+
+def concat(name, srcs):
+    return dict(kind="concat", name=name, src=list(srcs))
+
+
+def bottleneck(prefix, src, cin, mid, cout, stride=1, dil=1, proj=False):
+    """ResNet-50 v1.5 bottleneck: 1x1 -> 3x3 (stride, dilation) -> 1x1 (L1BN,
+    no ReLU), projection shortcut (1x1 with the stride, L1BN, no ReLU) when
+    the shape changes, ReLU after the residual add."""
+    nodes = []
+    sc = src
+    if proj:
+        nodes.append(conv(prefix + ".proj", src, cin, cout, 1, stride, 0, 1, relu=False))
+        sc = prefix + ".proj"
+    nodes.append(conv(prefix + ".conv1", src, cin, mid, 1))
+    nodes.append(conv(prefix + ".conv2", prefix + ".conv1", mid, mid, 3, stride, dil, dil))
+    nodes.append(conv(prefix + ".conv3", prefix + ".conv2", mid, cout, 1, relu=False))
+    nodes.append(add_relu(prefix + ".out", prefix + ".conv3", sc))
+    return nodes, prefix + ".out"
+
+
+def res_stage(prefix, src, cin, mid, cout, blocks, stride=1, dil_first=1, dil_rest=1):
+    nodes = []
+    for b in range(blocks):
+        nb, src = bottleneck(f"{prefix}.{b}", src, cin if b == 0 else cout, mid, cout,
+                             stride if b == 0 else 1, dil_first if b == 0 else dil_rest,
+                             proj=(b == 0))
+        nodes += nb
+    return nodes, src
+
+
+def aspp(prefix, src, cin, classes, rates=(6, 12, 18), mid=256):
+    """DeepLabv3 ASPP head: 1x1 branch, three 3x3 atrous branches (pad =
+    dilation), image pooling (GAP -> 1x1 -> L1BN + ReLU, broadcast back),
+    concatenation, 1x1 fuse, 1x1 classifier (no BN, no ReLU)."""
+    nodes = [conv(prefix + ".b0", src, cin, mid, 1)]
+    for i, d in enumerate(rates):
+        nodes.append(conv(f"{prefix}.b{i + 1}", src, cin, mid, 3, 1, d, d))
+    nodes.append(gap(prefix + ".pool", src))
+    nodes.append(conv(prefix + ".b4", prefix + ".pool", cin, mid, 1))
+    nodes.append(concat(prefix + ".cat", [f"{prefix}.b{i}" for i in range(5)]))
+    nodes.append(conv(prefix + ".fuse", prefix + ".cat", 5 * mid, mid, 1))
+    nodes.append(conv(prefix + ".cls", prefix + ".fuse", mid, classes, 1, bn=False, relu=False))
+    return nodes, prefix + ".cls"
+
+
+def resnet50_os16(src="input"):
+    """ResNet-50 v1.5 backbone at output stride 16: layer4 keeps stride 1 and
+    uses dilation 2 in its blocks 1-2 (block 0 keeps dilation 1)."""
+    nodes = [conv("stem", src, 3, 64, 7, 2, 3),
+             maxpool("pool", "stem", 3, 2, 1)]
+    out = "pool"
+    for name, mid, cout, blocks, stride, d0, d1 in (("layer1", 64, 256, 3, 1, 1, 1),
+                                                    ("layer2", 128, 512, 4, 2, 1, 1),
+                                                    ("layer3", 256, 1024, 6, 2, 1, 1),
+                                                    ("layer4", 512, 2048, 3, 1, 1, 2)):
+        cin = 64 if name == "layer1" else mid * 2
+        nb, out = res_stage(name, out, cin, mid, cout, blocks, stride, d0, d1)
+        nodes += nb
+    return nodes, out
+
 
 # Single 3x3 conv 16 -> 16, stride 1, pad 1, on a 1x32x32 map, then L1BN over
 # 16 channels; the input gradient is computed too.
 SINGLE_CONV = dict(id=1, name="single-conv3x3-16ch-32x32-n1", N=1, H=32, W=32, C=16,
-                   input_grad=True,
-                   layers=[("conv", 16, 16, 3, 1, 1, 1)])
+                   input_grad=True, loss="given",
+                   nodes=[conv("conv", "input", 16, 16, 3, 1, 1)])
 
 # FCN-VGG16 encoder slice: conv1_1, conv1_2, maxpool 2x2/2, conv2_1, conv2_2,
 # batch 8 of 3x224x224 images; no gradient is taken w.r.t. the image.
 VGG16_BLOCKS12 = dict(id=2, name="fcn-vgg16-blocks1-2-n8-224", N=8, H=224, W=224, C=3,
-                      input_grad=False,
-                      layers=[("conv", 3, 64, 3, 1, 1, 1),
-                              ("conv", 64, 64, 3, 1, 1, 1),
-                              ("maxpool", 2, 2, 0),
-                              ("conv", 64, 128, 3, 1, 1, 1),
-                              ("conv", 128, 128, 3, 1, 1, 1)])
+                      input_grad=False, loss="given",
+                      nodes=[conv("conv1_1", "input", 3, 64, 3, 1, 1),
+                             conv("conv1_2", "conv1_1", 64, 64, 3, 1, 1),
+                             maxpool("pool1", "conv1_2", 2, 2, 0),
+                             conv("conv2_1", "pool1", 64, 128, 3, 1, 1),
+                             conv("conv2_2", "conv2_1", 128, 128, 3, 1, 1)])
 
-WORKLOADS = {1: SINGLE_CONV, 2: VGG16_BLOCKS12}
+# ResNet-50 stage conv2_x: three bottlenecks 64 -> (64, 64, 256), the first
+# with a projection shortcut, on batch 16 of 64x56x56 features.
+RESNET50_CONV2X = dict(id=3, name="resnet50-conv2x-n16-56", N=16, H=56, W=56, C=64,
+                       input_grad=True, loss="given",
+                       nodes=res_stage("conv2_x", "input", 64, 64, 256, 3)[0])
+
+# DeepLabv3 ASPP head on batch 8 of 2048x32x32 features, 21 classes.
+ASPP_HEAD = dict(id=4, name="deeplabv3-aspp-2048ch-32x32-n8", N=8, H=32, W=32, C=2048,
+                 input_grad=True, loss="given",
+                 nodes=aspp("aspp", "input", 2048, 21)[0])
+
+# Full DeepLabv3-ResNet50 training step at output stride 16: batch 8 of
+# 3x512x512 images, 150 classes (ADE20K's count), per-pixel labels.
+_R50 = resnet50_os16()
+DEEPLABV3_R50 = dict(id=5, name="deeplabv3-r50-os16-n8-512", N=8, H=512, W=512, C=3,
+                     input_grad=False, loss="softmax_ce", classes=150,
+                     nodes=_R50[0] + aspp("aspp", _R50[1], 2048, 150)[0])
+
+WORKLOADS = {1: SINGLE_CONV, 2: VGG16_BLOCKS12, 3: RESNET50_CONV2X, 4: ASPP_HEAD,
+             5: DEEPLABV3_R50}
+
+
+def scaled(wl, N=None, H=None, W=None):
+    """The same workload at another batch or input size (parity tests)."""
+    d = dict(wl)
+    if N is not None:
+        d["N"] = N
+    if H is not None:
+        d["H"] = H
+    if W is not None:
+        d["W"] = W
+    return d
+
+
+def node_shapes(wl):
+    """Output shape [N, H, W, C] of every node (pure shape arithmetic)."""
+    shapes = {"input": (wl["N"], wl["H"], wl["W"], wl["C"])}
+    for nd in wl["nodes"]:
+        N, H, W, Cc = shapes[nd["src"][0]]
+        k = nd["kind"]
+        if k == "conv":
+            P = (H + 2 * nd["pad"] - nd["dil"] * (nd["R"] - 1) - 1) // nd["stride"] + 1
+            Q = (W + 2 * nd["pad"] - nd["dil"] * (nd["R"] - 1) - 1) // nd["stride"] + 1
+            shapes[nd["name"]] = (N, P, Q, nd["cout"])
+        elif k == "maxpool":
+            shapes[nd["name"]] = (N, (H + 2 * nd["pad"] - nd["k"]) // nd["stride"] + 1,
+                                  (W + 2 * nd["pad"] - nd["k"]) // nd["stride"] + 1, Cc)
+        elif k == "add":
+            shapes[nd["name"]] = (N, H, W, Cc)
+        elif k == "gap":
+            shapes[nd["name"]] = (N, 1, 1, Cc)
+        elif k == "concat":
+            sp = [shapes[s] for s in nd["src"]]
+            Hs = max(t[1] for t in sp)
+            Ws = max(t[2] for t in sp)
+            shapes[nd["name"]] = (N, Hs, Ws, sum(t[3] for t in sp))
+        else:
+            raise ValueError(k)
+    return shapes
+
+
+def conv_nodes(wl):
+    return [nd for nd in wl["nodes"] if nd["kind"] == "conv"]
 
 
 def workload_inputs(wl, N=None):
     """Seeded inputs of a workload: image/activation codes, float weights per
-    conv (He-normal), and the error arriving at the last activation."""
-    N = wl["N"] if N is None else N
+    conv (He-normal), and either the error arriving at the output or the
+    per-pixel labels."""
+    wl = scaled(wl, N)
+    N = wl["N"]
     x = int_codes(seed_for(wl["id"], 0), (N, wl["H"], wl["W"], wl["C"]))
     weights = []
-    Hh, W = wl["H"], wl["W"]
-    ordinal = 1
-    for layer in wl["layers"]:
-        if layer[0] == "conv":
-            _, cin, cout, R, st, pad, dil = layer
-            weights.append(he_normal(seed_for(wl["id"], ordinal), (cout, R, R, cin), cin * R * R))
-            ordinal += 1
-            Hh = (Hh + 2 * pad - dil * (R - 1) - 1) // st + 1
-            W = (W + 2 * pad - dil * (R - 1) - 1) // st + 1
-            cl = cout
-        else:
-            _, k, st, pad = layer
-            Hh = (Hh + 2 * pad - k) // st + 1
-            W = (W + 2 * pad - k) // st + 1
-    dy = int_codes(seed_for(wl["id"], 50), (N, Hh, W, cl))
-    return dict(x=x, x_exp=ACT_EXP, weights=weights, dy=dy, dy_exp=ERR_EXP,
-                seed=seed_for(wl["id"], 0))
+    for i, nd in enumerate(conv_nodes(wl)):
+        R, cin, cout = nd["R"], nd["cin"], nd["cout"]
+        weights.append(he_normal(seed_for(wl["id"], i + 1), (cout, R, R, cin), cin * R * R))
+    out = dict(x=x, x_exp=ACT_EXP, weights=weights, seed=seed_for(wl["id"], 0))
+    shp = node_shapes(wl)[wl["nodes"][-1]["name"]]
+    if wl["loss"] == "given":
+        out["dy"] = int_codes(seed_for(wl["id"], 50), shp)
+        out["dy_exp"] = ERR_EXP
+    else:
+        out["labels"] = labels(seed_for(wl["id"], 51), (N, wl["H"], wl["W"]), wl["classes"])
+    return out
