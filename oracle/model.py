@@ -178,7 +178,9 @@ class OracleNet:
             elif k == "gap":
                 if need_in:
                     H, W = r["a_in"].shape[1:3]
-                    send(src, e, O.gap_bwd_exp(ee, H, W))
+                    eg, ege = O.gap_bwd(e, ee, H, W)
+                    r.update(e_in=eg.astype(np.int8), e_in_exp=ege)
+                    send(src, eg.astype(np.int8), ege)
             elif k == "concat":
                 parts = O.concat_split(e, r["widths"])
                 for s, p, bc in zip(nd["src"], parts, r["bcast"]):

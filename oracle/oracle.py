@@ -375,22 +375,45 @@ def concat_split(dy, widths):
     return out
 
 
+def mean_requant(sums, exp, divisor, k=8):
+    """SQ_k of the rationals sums * 2^exp / divisor (Eq. 4 with the
+    power-of-two Scale): b = the smallest integer with max|value| < 2^b,
+    code = floor(value 2^(k-1-b) + 1/2) decided exactly, exponent b + 1 - k.
+    All-zero sums keep exponent exp - ceil(log2 divisor).  For a power-of-two
+    divisor this is SQ of the integer tensor `sums` on the grid 2^(exp - t)."""
+    s = [int(v) for v in np.ravel(sums)]
+    D = int(divisor)
+    M = max((abs(v) for v in s), default=0)
+    if M == 0:
+        return np.zeros(np.shape(sums), np.int64), exp - (D - 1).bit_length()
+    u = 0                     # smallest u with M < D 2^u
+    while not (M < D * 2 ** u if u >= 0 else M * 2 ** -u < D):
+        u += 1
+    while (M < D * 2 ** (u - 1) if u - 1 >= 0 else M * 2 ** (1 - u) < D):
+        u -= 1
+    sh = k - 1 - u
+    lim = 2 ** (k - 1) - 1
+    codes = []
+    for v in s:
+        num, den = (v * 2 ** sh, D) if sh >= 0 else (v, D * 2 ** -sh)
+        c = (2 * num + den) // (2 * den)          # floor(num/den + 1/2)
+        codes.append(max(-lim, min(lim, c)))
+    return np.array(codes, np.int64).reshape(np.shape(sums)), exp + u + 1 - k
+
+
 def gap_fwd(x, x_exp, k=8):
-    """Global average pooling over H x W (a power of two, so the mean is the
-    exact sum with exponent x_exp - log2(HW)), then SQ_k."""
+    """Global average pooling over H x W: the exact mean sum / (H W) of the
+    codes at exponent x_exp, then SQ_k -> [N,1,1,C]."""
     N, H, W, Cc = x.shape
-    t = (H * W).bit_length() - 1
-    if (1 << t) != H * W:
-        raise OracleError("gap: H*W must be a power of two")
     s = np.asarray(x, dtype=np.int64).sum(axis=(1, 2), keepdims=True)
-    return requant(s, x_exp - t, k)
+    return mean_requant(s, x_exp, H * W, k)
 
 
-def gap_bwd_exp(dy_exp, H, W):
-    """Backward of the mean: every input position receives dy / (H W); the
-    codes are dy's, broadcast, and the exponent drops by log2(H W)."""
-    t = (H * W).bit_length() - 1
-    return dy_exp - t
+def gap_bwd(dy, dy_exp, H, W, k=8):
+    """Backward of the mean: every input position receives dy / (H W); Q_E =
+    SQ_k of that [N,1,1,C] value, broadcast over H x W by the consumer (for a
+    power-of-two H W the values are kept exactly)."""
+    return mean_requant(np.asarray(dy, dtype=np.int64), dy_exp, H * W, k)
 
 
 def bcast_bwd(dy, dy_exp, k=8):

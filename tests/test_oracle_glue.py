@@ -132,28 +132,43 @@ def test_gap_hand_examples(orc, case):
     assert int(codes.ravel()[0]) == case["code"] and e == case["exp"]
 
 
-def test_gap_vs_torch_mean_and_brute_force(orc):
+@pytest.mark.parametrize("shape", [(3, 8, 4, 6), (2, 6, 5, 3), (1, 3, 3, 4)], ids=str)
+def test_gap_vs_torch_mean_and_brute_force(orc, shape):
     import torch
-    x = synth.int_codes(40, (3, 8, 4, 6))
+    x = synth.int_codes(40, shape)
     codes, e = orc.gap_fwd(x, -7)
-    mean = torch.from_numpy(x.astype(np.float64)).mean(dim=(1, 2), keepdim=True) * 2.0 ** -7
-    exact = [Fr(float(v)) for v in mean.numpy().ravel()]     # exact: 32 divides into binary
-    assert codes.shape == (3, 1, 1, 6)
+    HW = shape[1] * shape[2]
+    mean = torch.from_numpy(x.astype(np.float64)).mean(dim=(1, 2), keepdim=True)
+    # the exact rational mean; torch's float64 mean agrees with it to rounding
+    exact = [Fr(int(v), HW) * Fr(2) ** -7 for v in x.astype(np.int64).sum(axis=(1, 2)).ravel()]
+    assert np.allclose([float(v) for v in exact], mean.numpy().ravel() * 2.0 ** -7, rtol=1e-15)
+    assert codes.shape == (shape[0], 1, 1, shape[3])
     assert _vals(codes, e) == _brute_sq(exact)
-    with pytest.raises(orc.OracleError):
-        orc.gap_fwd(synth.int_codes(41, (1, 3, 5, 2)), -7)
 
 
-def test_gap_backward_is_adjoint_of_mean():
-    # <mean(x), d> = <x, bcast(d) / HW>: the backward's codes are d's with the
-    # exponent lowered by log2(HW)
-    from oracle import oracle as O
-    x = synth.int_codes(42, (2, 4, 8, 3))
+def test_gap_all_zero(orc):
+    codes, e = orc.gap_fwd(np.zeros((1, 6, 5, 2), np.int8), -7)
+    assert not codes.any() and e == -7 - 5          # ceil(log2 30) = 5
+    codes, e = orc.gap_fwd(np.zeros((1, 4, 8, 2), np.int8), -7)
+    assert not codes.any() and e == -12
+
+
+@pytest.mark.parametrize("hw", [(4, 8), (6, 5)], ids=str)
+def test_gap_backward(orc, hw):
+    # <mean(x), d> = <x, bcast(d / HW)>: the backward's value at every position
+    # is d / HW, quantized by SQ8; for a power-of-two HW exactly (values kept)
+    H, W = hw
     d = synth.int_codes(43, (2, 1, 1, 3))
-    lhs = sum(Fr(int(v)) for v in x.astype(np.int64).sum(axis=(1, 2)).ravel() * d.ravel()) / 32
-    e = O.gap_bwd_exp(0, 4, 8)
-    rhs = sum(Fr(int(a)) * Fr(int(b)) * Fr(2) ** e
-              for a, b in zip(x.ravel(), np.broadcast_to(d, x.shape).ravel()))
+    codes, e = orc.gap_bwd(d, -9, H, W)
+    exact = [Fr(int(v), H * W) * Fr(2) ** -9 for v in d.ravel()]
+    assert _vals(codes, e) == _brute_sq(exact)
+    if (H * W) & (H * W - 1) == 0:
+        assert _vals(codes, e) == exact
+    x = synth.int_codes(42, (2, H, W, 3))
+    lhs = sum(Fr(int(s), H * W) * Fr(int(v)) for s, v in
+              zip(x.astype(np.int64).sum(axis=(1, 2)).ravel(), d.ravel()))
+    rhs = sum(Fr(int(a)) * Fr(int(b), H * W) for a, b in
+              zip(x.ravel(), np.broadcast_to(d, x.shape).ravel()))
     assert lhs == rhs
 
 
