@@ -1,12 +1,14 @@
-"""Benchmark: one integer training step (forward, backward, update) of the
-FCN-VGG16 encoder slice (conv1_1, conv1_2, maxpool, conv2_1, conv2_2, L1BN +
-ReLU after each conv) at batch 8 and 224x224, on one MI355X.
+"""Benchmark: one integer training step (forward, softmax loss, backward,
+update) of DeepLabv3-ResNet50 at output stride 16 on a batch of 8 synthetic
+512x512 images with 150 classes, on one MI355X.  Other workload graphs
+(--workload) are kept for comparison.
 
-Prints ONE JSON line.  `value` is int8 conv throughput (valid-tap MACs x 2 of
-forward, backward-data and backward-weight, per step) divided by the whole
-step's wall time, with inputs already in HBM.  `roofline` reports the
-dominant kernel, timed by HIP events bracketing each of its launches inside
-the timed steps; `cpu_baseline` is the CPU oracle timed on a bounded sample.
+Prints ONE JSON line.  `value` is int8 conv throughput: valid-tap MACs x 2 of
+the forward, backward-data and backward-weight convolutions per step, divided
+by the whole step's wall time (inputs already in HBM); images/s is in
+`config`.  `roofline` reports one kernel timed in place by HIP events that the
+library records around each of its launches inside the timed steps;
+`cpu_baseline` is the CPU oracle timed on a bounded sample.
 """
 import argparse
 import json
@@ -21,6 +23,8 @@ METRIC = "int8 conv TOPS fwd+bwd (% MFMA peak); train images/s DeepLabv3-R50 512
 INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA
 HBM_PEAK_GBS = 8000.0
 
+WORKLOAD_IDS = {"deeplabv3": 5, "aspp": 4, "resnet-stage": 3, "vgg16": 2, "single-conv": 1}
+
 
 def conv_valid_macs(N, H, W, C, K, R, st, pad, dil):
     """Multiply-adds of a conv that touch real (non-padding) input."""
@@ -31,88 +35,82 @@ def conv_valid_macs(N, H, W, C, K, R, st, pad, dil):
     return N * rows * cols * C * K
 
 
-def workload_ops(wl, N):
-    """Valid-tap int8 ops (2 per MAC) per training step, and per-conv detail."""
-    H, W = wl["H"], wl["W"]
+def workload_ops(wl, N=None):
+    """Valid-tap int8 ops (2 per MAC) per training step, and per-conv detail:
+    forward, backward-weight, and backward-data unless the conv reads the
+    input image and no input gradient is wanted."""
+    from paper_2011_14504_amd import synth
+    wl = synth.scaled(wl, N)
+    shapes = synth.node_shapes(wl)
     total, detail = 0, []
-    first = True
-    for layer in wl["layers"]:
-        if layer[0] == "conv":
-            _, cin, cout, R, st, pad, dil = layer
-            macs = conv_valid_macs(N, H, W, cin, cout, R, st, pad, dil)
-            passes = 3 if (not first or wl["input_grad"]) else 2
-            total += 2 * macs * passes
-            detail.append(dict(shape=(N, H, W, cin, cout, R, st, pad, dil), macs=macs))
-            H = (H + 2 * pad - dil * (R - 1) - 1) // st + 1
-            W = (W + 2 * pad - dil * (R - 1) - 1) // st + 1
-            first = False
-        else:
-            _, k, st, pad = layer
-            H = (H + 2 * pad - k) // st + 1
-            W = (W + 2 * pad - k) // st + 1
+    for nd in synth.conv_nodes(wl):
+        n, H, W, cin = shapes[nd["src"][0]]
+        macs = conv_valid_macs(n, H, W, cin, nd["cout"], nd["R"], nd["stride"], nd["pad"], nd["dil"])
+        passes = 3 if (nd["src"][0] != "input" or wl["input_grad"]) else 2
+        total += 2 * macs * passes
+        detail.append(dict(name=nd["name"], key=(n, H, W, cin, nd["cout"], nd["R"], nd["stride"],
+                                                 nd["pad"], nd["dil"]), macs=macs))
     return total, detail
 
 
-def timed_kernel_info(name, N, detail):
-    """Kernel family, layer key and algorithmic work per launch of the kernels
-    the benchmark can time in place; all on the conv1_2 layer (64 -> 64 3x3 at
-    224x224) or the L1BN that follows it (M = N*224*224 rows, 64 channels)."""
-    from paper_2011_14504_amd import iseg
-    M, C = N * 224 * 224, 64
-    conv_key = (N, 224, 224, 64, 64)
-    ops = 2 * detail[1]["macs"]
-    table = {
-        "conv_fwd": (iseg.ISEG_KID_CONV_FWD, conv_key, "mfma", ops,
-                     "k_conv3x3_m32 fwd, max pass (conv1_2, 64->64 3x3, 224x224)"),
-        "conv_bwd_data": (iseg.ISEG_KID_CONV_BWD_DATA, conv_key, "mfma", ops,
-                          "k_conv3x3_m32 bwd-data, max pass (conv1_2)"),
-        "conv_wgrad": (iseg.ISEG_KID_CONV_WGRAD, conv_key, "mfma", ops,
-                       "k_conv_wgrad_taps (conv1_2)"),
-        # bytes per element: stats reads x and dy; apply reads x, dy and writes dx
-        "bn_bwd_stats": (iseg.ISEG_KID_BN_BWD_STATS, (M, C), "hbm", 2 * M * C,
-                         "k_bnb_stats (L1BN backward statistics, conv1_2 output)"),
-        "bn_bwd_apply": (iseg.ISEG_KID_BN_BWD_APPLY, (M, C), "hbm", 3 * M * C,
-                         "k_bnb_apply (L1BN backward output pass, conv1_2 output)"),
-        "bn_fwd_stats1": (iseg.ISEG_KID_BN_FWD_STATS1, (M, C), "hbm", M * C,
-                          "k_bnf_stats1 (L1BN forward mean pass, conv1_2 output)"),
-        "bn_fwd_apply": (iseg.ISEG_KID_BN_FWD_APPLY, (M, C), "hbm", 2 * M * C,
-                         "k_bnf_apply (L1BN forward output pass, conv1_2 output)"),
-        # reads x (M C) and dy (M C / 4), writes dx (M C)
-        "maxpool_bwd": (iseg.ISEG_KID_MAXPOOL_BWD, (N, 224, 224, 64), "hbm", M * C * 9 // 4,
-                        "k_maxpool_bwd_win (2x2/2 after conv1_2)"),
-    }
-    kid, key, bound, work, label = table[name]
-    return dict(kid=kid, key=key, bound=bound, work=work, name=label)
+def timed_kernel_info(name, wl, detail):
+    """Kernel family, layer key and algorithmic work per launch of the kernel
+    timed in place.  Conv kernels: ops of one launch of the named layer.
+    L1BN kernels: bytes of the layer's output tensor moved by the pass."""
+    from paper_2011_14504_amd import iseg, synth
+    kind, _, layer = name.partition(":")
+    d = next(x for x in detail if x["name"] == layer)
+    shapes = synth.node_shapes(wl)
+    conv_kids = {"conv_fwd": iseg.ISEG_KID_CONV_FWD, "conv_bwd_data": iseg.ISEG_KID_CONV_BWD_DATA,
+                 "conv_wgrad": iseg.ISEG_KID_CONV_WGRAD}
+    if kind in conv_kids:
+        return dict(kid=conv_kids[kind], key=d["key"], bound="mfma", work=2 * d["macs"],
+                    name=f"{kind} of {layer} (N,H,W,C,K,R,stride,pad,dil = {d['key']})")
+    N, P, Q, K = shapes[layer]
+    M = N * P * Q
+    # bytes per element: stats1/stats2 read x; apply reads x, writes y; the
+    # backward statistics read x and dy; the backward apply reads x, dy, writes dx
+    bn = {"bn_fwd_stats1": (iseg.ISEG_KID_BN_FWD_STATS1, 1), "bn_fwd_stats2": (iseg.ISEG_KID_BN_FWD_STATS2, 1),
+          "bn_fwd_apply": (iseg.ISEG_KID_BN_FWD_APPLY, 2), "bn_bwd_stats": (iseg.ISEG_KID_BN_BWD_STATS, 2),
+          "bn_bwd_apply": (iseg.ISEG_KID_BN_BWD_APPLY, 3)}
+    kid, bpe = bn[kind]
+    return dict(kid=kid, key=(M, K), bound="hbm", work=bpe * M * K,
+                name=f"{kind} of the L1BN after {layer} (M = {M}, C = {K})")
 
 
-def cpu_baseline(wl, n_img):
-    """The oracle's training step on n_img images, timed on the host cores."""
+def cpu_baseline(wl, sample_hw):
+    """The oracle's whole training step on one image at sample_hw x sample_hw,
+    timed on the host cores; scaled to the benchmark's unit by the ratio of
+    valid-tap conv ops."""
     from oracle import oracle as O
     from oracle.model import OracleNet
     from paper_2011_14504_amd import synth
-    inp = synth.workload_inputs(wl, n_img)
-    net = OracleNet(wl, inp)
+    small = synth.scaled(wl, 1, sample_hw, sample_hw)
+    inp = synth.workload_inputs(small)
+    net = OracleNet(small, inp)
     t0 = time.perf_counter()
     net.step()
     dt = time.perf_counter() - t0
-    ops, _ = workload_ops(wl, n_img)
+    ops, _ = workload_ops(small)
+    full_ops, _ = workload_ops(wl)
     return dict(value=ops / dt / 1e12, unit="TOPS", cores=O.num_threads(), kind="oracle",
-                sample=f"one full training step (fwd+bwd+update) of the same workload at batch "
-                       f"{n_img}: {dt:.2f} s",
-                images_per_s=n_img / dt)
+                sample=f"one full training step (fwd, loss, bwd, update) of the same network on one "
+                       f"{sample_hw}x{sample_hw} image: {dt:.2f} s for {ops / 1e9:.1f} G conv ops",
+                images_per_s_est=(ops / full_ops) * wl["N"] / dt)
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--batch", type=int, default=8)
-    ap.add_argument("--cpu-images", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="deeplabv3", choices=sorted(WORKLOAD_IDS))
+    ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--cpu-sample-hw", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--timed-kernel", default="conv_fwd",
-                    choices=["conv_fwd", "conv_bwd_data", "conv_wgrad", "bn_bwd_stats",
-                             "bn_bwd_apply", "bn_fwd_stats1", "bn_fwd_apply", "maxpool_bwd"])
+    ap.add_argument("--timed-kernel", default="conv_fwd:aspp.b1",
+                    help="<family>:<layer>, family one of conv_fwd, conv_bwd_data, conv_wgrad, "
+                         "bn_fwd_stats1, bn_fwd_stats2, bn_fwd_apply, bn_bwd_stats, bn_bwd_apply")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
@@ -123,13 +121,15 @@ def main():
     from paper_2011_14504_amd import iseg, synth
     from paper_2011_14504_amd.model import IntNet
 
-    wl = synth.VGG16_BLOCKS12
-    N = args.batch
-    inp = synth.workload_inputs(wl, N)
+    wl = synth.scaled(synth.WORKLOADS[WORKLOAD_IDS[args.workload]], args.batch)
+    N = wl["N"]
+    inp = synth.workload_inputs(wl)
     net = IntNet(wl, inp, "cuda:0")
-    ops, detail = workload_ops(wl, N)
-
-    kinfo = timed_kernel_info(args.timed_kernel, N, detail)
+    ops, detail = workload_ops(wl)
+    tk = args.timed_kernel
+    if args.workload != "deeplabv3" and tk == "conv_fwd:aspp.b1":
+        tk = "conv_fwd:" + detail[min(1, len(detail) - 1)]["name"]
+    kinfo = timed_kernel_info(tk, wl, detail)
     prof = iseg.KernelTimer(kinfo["kid"], layer_match=kinfo["key"])
 
     for _ in range(args.warmup):
@@ -147,28 +147,29 @@ def main():
 
     k_ms = prof.mean_ms()
     per_launch = kinfo["work"]
+    launches = prof.count()
     if kinfo["bound"] == "mfma":
         ach = per_launch / (k_ms * 1e-3) / 1e12 if k_ms else None
         roof = dict(kernel=kinfo["name"], bound="mfma", achieved=ach, peak=INT8_PEAK_TOPS,
                     unit="TFLOP/s", frac=(ach / INT8_PEAK_TOPS) if ach else None, traffic=None,
-                    algorithmic_ops_per_launch=per_launch, avg_launch_ms=k_ms,
-                    launches=prof.count())
+                    algorithmic_ops_per_launch=per_launch, avg_launch_ms=k_ms, launches=launches)
     else:
         ach = per_launch / (k_ms * 1e-3) / 1e9 if k_ms else None
         roof = dict(kernel=kinfo["name"], bound="hbm", achieved=ach, peak=HBM_PEAK_GBS,
                     unit="GB/s", frac=(ach / HBM_PEAK_GBS) if ach else None, traffic=None,
-                    algorithmic_bytes_per_launch=per_launch, avg_launch_ms=k_ms,
-                    launches=prof.count())
-
+                    algorithmic_bytes_per_launch=per_launch, avg_launch_ms=k_ms, launches=launches)
+    prof.close()
+    cfg = dict(workload=wl["name"], batch=N, image=f"{wl['H']}x{wl['W']}",
+               convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
+               pct_int8_peak=100.0 * value / INT8_PEAK_TOPS)
+    if net.loss is not None:
+        cfg["loss"] = float(net.loss.item())
     out = dict(metric=METRIC, value=value, unit="TOPS", n_gpus=1, steps=args.steps,
                warmup=args.warmup, ms_per_step=ms, higher_is_better=True, scaling="weak",
-               vs_baseline=None, dtype="int8", data="synthetic",
-               config=dict(workload=wl["name"], batch=N, image=224, convs=4, bn="L1BN x4",
-                           conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
-                           pct_int8_peak=100.0 * value / INT8_PEAK_TOPS),
-               roofline=roof)
+               vs_baseline=None, dtype="int8", data="synthetic", config=cfg, roofline=roof)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_images)
+        sample = args.cpu_sample_hw if wl["H"] > args.cpu_sample_hw else wl["H"]
+        out["cpu_baseline"] = cpu_baseline(wl, sample)
     print(json.dumps(out))
 
 

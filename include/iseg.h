@@ -280,6 +280,94 @@ int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
                      void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Merges of quantized tensors (residual add, error sums, ASPP concat, global */
+/* pooling).  Every tensor of the dataflow is an 8-bit object with one scale */
+/* (Sec. 3.1), so a merge forms the exact result on the grid 2^min(e_i) and   */
+/* applies one SQ (Eq. 4; Eq. 16 for errors).  Exponents more than 48 apart   */
+/* set ISEG_DEV_RANGE (outputs then unspecified).  Input arrays of pointers,  */
+/* exponent pointers and per-input integers are HOST arrays of n_in entries   */
+/* (n_in in [1, 8]) holding device pointers.                                  */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_sum_requant -- out = SQ(ReLU?(sum_i in_i 2^(*in_exp[i] + exp_add[i])),
+ * bits): the residual add of a bottleneck (relu = 1, the ReLU that follows
+ * it) and the sum of the errors a tensor receives from several consumers
+ * (relu = 0).  Input i is [N, HW, C] int8, or [N, 1, C] broadcast over the HW
+ * positions when bcast[i] != 0 (the backward of global average pooling:
+ * its error codes with exp_add = -log2(HW)).  exp_add and bcast may be NULL
+ * (all zero).  out [N, HW, C] int8 with exponent *out_exp = min_i(e_i) + r,
+ * r = bitlen(max|sum|) - (bits-1) (the minimum exponent itself for an
+ * all-zero result).  bits in [2, 8]. */
+size_t iseg_sum_requant_ws(int64_t N, int64_t HW, int64_t C);
+int iseg_sum_requant(int32_t n_in, const int8_t* const* in, const int32_t* const* in_exp,
+                     const int32_t* exp_add, const int32_t* bcast, int64_t N, int64_t HW, int64_t C,
+                     int32_t relu, int32_t bits, int8_t* out, int32_t* out_exp,
+                     void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_relu_mask_bwd -- backward of ReLU(sum_i in_i 2^(e_i + exp_add[i])):
+ * dx = dy where the exact sum is > 0, else 0.  The values stay on dy's grid,
+ * so dx takes dy's exponent (not written).  All tensors [n] int8, n a
+ * multiple of the channel count C (C steers the vector path only). */
+int iseg_relu_mask_bwd(const int8_t* dy, int32_t n_in, const int8_t* const* in,
+                       const int32_t* const* in_exp, const int32_t* exp_add, int64_t n, int64_t C,
+                       int8_t* dx, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_concat_requant -- out = SQ(concat_c(in_i 2^(*in_exp[i])), bits), one
+ * object with one scale: the ASPP concatenation.  Input i is [N, HW, C_in[i]]
+ * int8, or [N, 1, C_in[i]] broadcast over HW when bcast[i] != 0 (the image
+ * pooling branch, whose 1x1 map is upsampled to the others' size); out
+ * [N, HW, sum C_in] int8, *out_exp = min_i(e_i) + r. */
+size_t iseg_concat_requant_ws(int32_t n_in);
+int iseg_concat_requant(int32_t n_in, const int8_t* const* in, const int32_t* const* in_exp,
+                        const int64_t* C_in, const int32_t* bcast, int64_t N, int64_t HW, int32_t bits,
+                        int8_t* out, int32_t* out_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                        hipStream_t stream);
+
+/* iseg_concat_split -- backward of the concatenation: out[i] [rows, C_in[i]]
+ * = dy[:, off_i : off_i + C_in[i]] (off_i = sum of the earlier widths); the
+ * slices keep dy's exponent.  A NULL out[i] is skipped (a broadcast part's
+ * error is reduced by iseg_spatial_sum straight from dy instead). */
+int iseg_concat_split(const int8_t* dy, int64_t rows, int32_t n_in, const int64_t* C_in,
+                      int8_t* const* out, hipStream_t stream);
+
+/* iseg_spatial_sum -- out[n, c] = SQ(sum_{hw} x[n, hw, c0 + c] / divisor, bits)
+ * for x [N, HW, ldc] int8 with exponent *x_exp, c in [0, C): the scale is
+ * 2^(x_exp + u), u the smallest integer with max|sum| < divisor 2^u, and
+ * code = floor(sum 2^(bits-1-u) / divisor + 1/2) decided exactly.  Global
+ * average pooling is divisor = HW (the exact mean); the backward of the mean
+ * is HW = 1, divisor = the pooled H W (Q_E of dy / (H W), Eq. 16); the
+ * backward of broadcasting a [N,1,C] tensor over HW positions is divisor = 1
+ * (the exact spatial sum of the error, then Q_E).  out [N, C] int8; an
+ * all-zero result has exponent *x_exp - ceil(log2 divisor).  Requires
+ * N C <= 2^20, HW <= 2^23, divisor in [1, 2^30]. */
+size_t iseg_spatial_sum_ws(int64_t N, int64_t HW, int64_t C);
+int iseg_spatial_sum(const int8_t* x, const int32_t* x_exp, int64_t N, int64_t HW, int64_t ldc,
+                     int64_t c0, int64_t C, int64_t divisor, int32_t bits, int8_t* out,
+                     int32_t* out_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                     hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Segmentation loss (float region)                                          */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_softmax_ce -- pixel-wise softmax cross-entropy of the logits
+ * upsampled bilinearly to the label size (half-pixel centres: source
+ * coordinate (o + 1/2) n_in / n_out - 1/2 clamped at 0, the upper neighbour
+ * clamped at the edge), averaged over the N H W pixels; its gradient w.r.t.
+ * the int8 logits (the adjoint of the upsampling applied to (softmax -
+ * onehot) / (N H W)); and E1 = SQ(gradient, bits), the int8 error at the
+ * logits (Eq. 4 / 16), exponent *err_exp.  Computed in float64.
+ *   logits [N, h, w, K] int8 with exponent *logit_exp; labels [N, H, W]
+ *   uint8 in [0, K) (otherwise ISEG_DEV_RANGE); loss: one device double
+ *   (may be NULL); grad [N, h, w, K] device doubles (may be NULL); err
+ *   [N, h, w, K] int8.  K <= 256, H >= h, W >= w. */
+size_t iseg_softmax_ce_ws(int64_t N, int64_t h, int64_t w, int64_t K, int64_t H, int64_t W);
+int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, const uint8_t* labels,
+                    int64_t N, int64_t h, int64_t w, int64_t K, int64_t H, int64_t W, int32_t bits,
+                    double* loss, double* grad, int8_t* err, int32_t* err_exp,
+                    void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Host-side utilities                                                       */
 /* ------------------------------------------------------------------------ */
 
@@ -290,9 +378,9 @@ void iseg_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t o
 /* Measurement hook.  Kernel families that can be timed in place: */
 enum iseg_kernel_id {
     ISEG_KID_NONE = 0,
-    ISEG_KID_CONV_FWD = 1,       /* implicit GEMM of iseg_conv_fwd */
-    ISEG_KID_CONV_BWD_DATA = 2,  /* implicit GEMM of iseg_conv_bwd_data */
-    ISEG_KID_CONV_WGRAD = 3,     /* implicit GEMM of iseg_conv_bwd_weight */
+    ISEG_KID_CONV_FWD = 1,       /* every kernel of one iseg_conv_fwd call */
+    ISEG_KID_CONV_BWD_DATA = 2,  /* every kernel of one iseg_conv_bwd_data call */
+    ISEG_KID_CONV_WGRAD = 3,     /* every kernel of one iseg_conv_bwd_weight call */
     ISEG_KID_REQUANT = 4,        /* SQ/RQ code pass of any requantization */
     ISEG_KID_BN_FWD_APPLY = 5,   /* output pass of iseg_bn_fwd */
     ISEG_KID_BN_BWD_APPLY = 6,   /* output pass of iseg_bn_bwd */
@@ -303,7 +391,8 @@ enum iseg_kernel_id {
 };
 
 /* iseg_profile_arm -- the next launch of kernel family `kernel_id` (by any
- * entry point, on any stream) records `start` immediately before and `stop`
+ * entry point, on any stream; for the conv ids: the next call of that entry
+ * point, all its kernels) records `start` immediately before and `stop`
  * immediately after itself on its own stream, then the hook disarms.  The
  * events are the caller's (hipEventCreate).  Process-global and not
  * thread-safe: meant for benchmarks.  kernel_id ISEG_KID_NONE disarms. */

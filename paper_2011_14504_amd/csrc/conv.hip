@@ -17,6 +17,10 @@
 // Sums are exact: |sum| <= 131071 * 128^2 < 2^31 for every supported shape.
 #include "iseg_common.h"
 
+// a convolution is timed as a whole entry-point call (ProfScope), not per kernel
+#undef ISEG_TIMED_LAUNCH
+#define ISEG_TIMED_LAUNCH(kid, stream, ...) hipLaunchKernelGGL(__VA_ARGS__)
+
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 namespace {
@@ -2839,6 +2843,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
                              const iseg_conv_geom* g, int32_t out_mode, void* y, int32_t* y_exp,
                              void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
 {
+    ProfScope prof_scope(ISEG_KID_CONV_FWD, stream);
     (void)dev_status;
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
@@ -2998,6 +3003,7 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
                                   void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes,
                                   int32_t* dev_status, hipStream_t stream)
 {
+    ProfScope prof_scope(ISEG_KID_CONV_BWD_DATA, stream);
     (void)dev_status;
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
@@ -3134,6 +3140,7 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
                                     void* dw, int32_t* dw_exp, void* ws, size_t ws_bytes,
                                     int32_t* dev_status, hipStream_t stream)
 {
+    ProfScope prof_scope(ISEG_KID_CONV_WGRAD, stream);
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
     if (g_mode != ISEG_G_KEEP && g_mode != ISEG_G_DROP && g_mode != ISEG_G_RAW) return ISEG_ERR_ARG;

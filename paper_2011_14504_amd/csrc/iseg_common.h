@@ -278,3 +278,15 @@ void prof_end(int kid, hipStream_t s);
         hipLaunchKernelGGL(__VA_ARGS__);               \
         if (iseg_timed_) prof_end((kid), (stream));    \
     } while (0)
+
+// measurement hook around a whole entry-point call (every kernel it enqueues)
+struct ProfScope {
+    int kid;
+    hipStream_t s;
+    bool on;
+    ProfScope(int k, hipStream_t st) : kid(k), s(st), on(prof_begin(k, st)) {}
+    ~ProfScope()
+    {
+        if (on) prof_end(kid, s);
+    }
+};

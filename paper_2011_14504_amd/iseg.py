@@ -78,6 +78,19 @@ _SIGS = {
                           _SZ, _P, _P], C.c_int),
     "iseg_bn_param_update": ([_P, _P, _P, _P, _I64, _I32, _U64, _U32, _U32, _U32, _I32, _I32, _I32,
                               _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
+    "iseg_sum_requant_ws": ([_I64, _I64, _I64], _SZ),
+    "iseg_sum_requant": ([_I32, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _I32, _P, _P, _P, _SZ, _P, _P],
+                         C.c_int),
+    "iseg_relu_mask_bwd": ([_P, _I32, _P, _P, _P, _I64, _I64, _P, _P, _P], C.c_int),
+    "iseg_concat_requant_ws": ([_I32], _SZ),
+    "iseg_concat_requant": ([_I32, _P, _P, _P, _P, _I64, _I64, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_concat_split": ([_P, _I64, _I32, _P, _P, _P], C.c_int),
+    "iseg_spatial_sum_ws": ([_I64, _I64, _I64], _SZ),
+    "iseg_spatial_sum": ([_P, _P, _I64, _I64, _I64, _I64, _I64, _I64, _I32, _P, _P, _P, _SZ, _P, _P],
+                         C.c_int),
+    "iseg_softmax_ce_ws": ([_I64, _I64, _I64, _I64, _I64, _I64], _SZ),
+    "iseg_softmax_ce": ([_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _SZ,
+                         _P, _P], C.c_int),
     "iseg_philox4x32_10": ([_P, _P, _P], None),
     "iseg_profile_arm": ([_I32, _P, _P], C.c_int),
     "iseg_version": ([], C.c_char_p),
@@ -204,6 +217,64 @@ def iseg_maxpool_bwd(dy, dy_exp, x, k, stride, pad, bits, dx, dx_exp, ws, status
     rc = lib().iseg_maxpool_bwd(_ptr(dy), _ptr(dy_exp), _ptr(x), N, H, W, Cc, k, stride, pad, bits,
                                 _ptr(dx), _ptr(dx_exp), *_ws_tuple(ws), _ptr(status), _stream())
     _check(rc, "iseg_maxpool_bwd")
+
+
+def _ptr_array(ts):
+    return (C.c_void_p * len(ts))(*[None if t is None else t.data_ptr() for t in ts])
+
+
+def _i32_array(v):
+    return (C.c_int32 * len(v))(*[int(x) for x in v])
+
+
+def _i64_array(v):
+    return (C.c_int64 * len(v))(*[int(x) for x in v])
+
+
+def iseg_sum_requant(ins, in_exps, exp_add, bcast, N, HW, Cc, relu, bits, out, out_exp, ws,
+                     status=None):
+    n = len(ins)
+    rc = lib().iseg_sum_requant(n, _ptr_array(ins), _ptr_array(in_exps),
+                                _i32_array(exp_add or [0] * n), _i32_array(bcast or [0] * n),
+                                N, HW, Cc, relu, bits, _ptr(out), _ptr(out_exp), *_ws_tuple(ws),
+                                _ptr(status), _stream())
+    _check(rc, "iseg_sum_requant")
+
+
+def iseg_relu_mask_bwd(dy, ins, in_exps, exp_add, Cc, dx, status=None):
+    n = len(ins)
+    rc = lib().iseg_relu_mask_bwd(_ptr(dy), n, _ptr_array(ins), _ptr_array(in_exps),
+                                  _i32_array(exp_add or [0] * n), dy.numel(), Cc, _ptr(dx),
+                                  _ptr(status), _stream())
+    _check(rc, "iseg_relu_mask_bwd")
+
+
+def iseg_concat_requant(ins, in_exps, widths, bcast, N, HW, bits, out, out_exp, ws, status=None):
+    n = len(ins)
+    rc = lib().iseg_concat_requant(n, _ptr_array(ins), _ptr_array(in_exps), _i64_array(widths),
+                                   _i32_array(bcast or [0] * n), N, HW, bits, _ptr(out),
+                                   _ptr(out_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_concat_requant")
+
+
+def iseg_concat_split(dy, rows, widths, outs):
+    rc = lib().iseg_concat_split(_ptr(dy), rows, len(widths), _i64_array(widths), _ptr_array(outs),
+                                 _stream())
+    _check(rc, "iseg_concat_split")
+
+
+def iseg_spatial_sum(x, x_exp, N, HW, ldc, c0, Cc, divisor, bits, out, out_exp, ws, status=None):
+    rc = lib().iseg_spatial_sum(_ptr(x), _ptr(x_exp), N, HW, ldc, c0, Cc, divisor, bits, _ptr(out),
+                                _ptr(out_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_spatial_sum")
+
+
+def iseg_softmax_ce(logits, logit_exp, labels, N, h, w, K, H, W, bits, loss, grad, err, err_exp,
+                    ws, status=None):
+    rc = lib().iseg_softmax_ce(_ptr(logits), _ptr(logit_exp), _ptr(labels), N, h, w, K, H, W, bits,
+                               _ptr(loss), _ptr(grad), _ptr(err), _ptr(err_exp), *_ws_tuple(ws),
+                               _ptr(status), _stream())
+    _check(rc, "iseg_softmax_ce")
 
 
 def iseg_philox4x32_10(ctr, key):
@@ -393,7 +464,7 @@ def conv_fwd(x, x_exp, w, w_exp, stride=1, pad=0, dil=1, out_mode=ISEG_OUT_Q8, s
                     device=x.device)
     e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_conv_fwd_ws(C.byref(g), out_mode))
-    _maybe_arm(ISEG_KID_CONV_FWD, (N, H, W, Cc, K))
+    _maybe_arm(ISEG_KID_CONV_FWD, (N, H, W, Cc, K, R, g.stride_h, g.pad_h, g.dil_h))
     iseg_conv_fwd(x, x_exp, w, w_exp, g, out_mode, y, e, ws, status)
     return y, e
 
@@ -407,7 +478,7 @@ def conv_bwd_data(dy, dy_exp, w, w_exp, x_shape, stride=1, pad=0, dil=1, out_mod
                      device=dy.device)
     e = _out_exp(dy.device)
     ws = workspace(dy.device).get(lib().iseg_conv_bwd_data_ws(C.byref(g), out_mode))
-    _maybe_arm(ISEG_KID_CONV_BWD_DATA, (N, H, W, Cc, K))
+    _maybe_arm(ISEG_KID_CONV_BWD_DATA, (N, H, W, Cc, K, R, g.stride_h, g.pad_h, g.dil_h))
     iseg_conv_bwd_data(dy, dy_exp, w, w_exp, g, out_mode, dx, e, ws, status)
     return dx, e
 
@@ -421,7 +492,7 @@ def conv_bwd_weight(dy, dy_exp, x, x_exp, w_shape, stride=1, pad=0, dil=1, g_mod
                      device=x.device)
     e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_conv_bwd_weight_ws(C.byref(g), g_mode))
-    _maybe_arm(ISEG_KID_CONV_WGRAD, (N, H, W, Cc, K))
+    _maybe_arm(ISEG_KID_CONV_WGRAD, (N, H, W, Cc, K, R, g.stride_h, g.pad_h, g.dil_h))
     iseg_conv_bwd_weight(dy, dy_exp, x, x_exp, g, g_mode, bits, seed, tensor_id, step, dw, e, ws,
                          status)
     return dw, e
@@ -508,3 +579,82 @@ def maxpool_bwd(dy, dy_exp, x, k, stride, pad=0, bits=8, status=None):
     _maybe_arm(ISEG_KID_MAXPOOL_BWD, (N, H, W, Cc))
     iseg_maxpool_bwd(dy, dy_exp, x, k, stride, pad, bits, dx, e, ws, status)
     return dx, e
+
+
+def sum_requant(ins, in_exps, relu=False, exp_add=None, bcast=None, bits=8, status=None):
+    """SQ(ReLU?(sum of the inputs)); the first input fixes the shape [N,H,W,C]
+    (a broadcast input is [N,1,1,C])."""
+    ref = next(t for t, b in zip(ins, bcast or [0] * len(ins)) if not b)
+    N, H, W, Cc = ref.shape
+    out = torch.empty_like(ref)
+    e = _out_exp(ref.device)
+    ws = workspace(ref.device).get(lib().iseg_sum_requant_ws(N, H * W, Cc))
+    iseg_sum_requant(ins, in_exps, exp_add, bcast, N, H * W, Cc, int(relu), bits, out, e, ws, status)
+    return out, e
+
+
+def relu_mask_bwd(dy, ins, in_exps, status=None):
+    dx = torch.empty_like(dy)
+    iseg_relu_mask_bwd(dy, ins, in_exps, None, dy.shape[-1], dx, status)
+    return dx
+
+
+def concat_requant(ins, in_exps, bits=8, status=None):
+    """Channel concatenation of [N,H,W,C_i] tensors (a [N,1,1,C_i] part is
+    broadcast to H x W), SQ to `bits`."""
+    N = ins[0].shape[0]
+    H = max(t.shape[1] for t in ins)
+    W = max(t.shape[2] for t in ins)
+    widths = [t.shape[3] for t in ins]
+    bc = [int(tuple(t.shape[1:3]) != (H, W)) for t in ins]
+    out = torch.empty((N, H, W, sum(widths)), dtype=torch.int8, device=ins[0].device)
+    e = _out_exp(ins[0].device)
+    ws = workspace(ins[0].device).get(lib().iseg_concat_requant_ws(len(ins)))
+    iseg_concat_requant(ins, in_exps, widths, bc, N, H * W, bits, out, e, ws, status)
+    return out, e
+
+
+def concat_split(dy, widths, skip=None):
+    """Channel slices of dy (None where skip[i])."""
+    N, H, W, _ = dy.shape
+    outs = [None if (skip and skip[i]) else
+            torch.empty((N, H, W, c), dtype=torch.int8, device=dy.device)
+            for i, c in enumerate(widths)]
+    iseg_concat_split(dy, N * H * W, widths, outs)
+    return outs
+
+
+def spatial_sum(x, x_exp, divisor=1, c0=0, Cc=None, bits=8, status=None):
+    """SQ(sum over H x W of channels [c0, c0 + Cc) / divisor) -> [N,1,1,Cc]."""
+    N, H, W, ldc = x.shape
+    Cc = ldc - c0 if Cc is None else Cc
+    out = torch.empty((N, 1, 1, Cc), dtype=torch.int8, device=x.device)
+    e = _out_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_spatial_sum_ws(N, H * W, Cc))
+    iseg_spatial_sum(x, x_exp, N, H * W, ldc, c0, Cc, divisor, bits, out, e, ws, status)
+    return out, e
+
+
+def gap_fwd(x, x_exp, bits=8, status=None):
+    """Global average pooling over H x W -> [N,1,1,C] (SQ of the exact mean)."""
+    return spatial_sum(x, x_exp, x.shape[1] * x.shape[2], bits=bits, status=status)
+
+
+def gap_bwd(dy, dy_exp, H, W, bits=8, status=None):
+    """Backward of the mean over H x W: SQ(dy / (H W)), [N,1,1,C], to be
+    broadcast over H x W by the consumer."""
+    return spatial_sum(dy, dy_exp, H * W, bits=bits, status=status)
+
+
+def softmax_ce(logits, logit_exp, labels, bits=8, want_grad=False, status=None):
+    """Loss (device double), optional float64 gradient, and E1 = SQ(gradient)."""
+    N, h, w, K = logits.shape
+    _, H, W = labels.shape
+    dev = logits.device
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    grad = torch.empty((N, h, w, K), dtype=torch.float64, device=dev) if want_grad else None
+    err = torch.empty((N, h, w, K), dtype=torch.int8, device=dev)
+    e = _out_exp(dev)
+    ws = workspace(dev).get(lib().iseg_softmax_ce_ws(N, h, w, K, H, W))
+    iseg_softmax_ce(logits, logit_exp, labels, N, h, w, K, H, W, bits, loss, grad, err, e, ws, status)
+    return loss, grad, err, e

@@ -1,16 +1,22 @@
-"""One integer training step of a conv / L1BN / ReLU / max-pool stack on the
-GPU, built from the libiseg entry points (Sec. 3 dataflow of arXiv
-2011.14504).
+"""One integer training step of a workload graph on the GPU, built from the
+libiseg entry points (Sec. 3 dataflow of arXiv 2011.14504).
 
-Forward, per conv layer l:  W_q = Q_W(W_m) (Eq. 8);  Z = SQ8(conv(A, W_q))
-(Eq. 15 on the MAC output);  A' = L1BN + ReLU + Q_A (Eq. 12-15).
-Backward, in reverse:  L1BN backward (E2, Eq. 16) -> G = Q_G(conv_bwd_weight)
-(Eq. 17, stochastic) and E1 = Q_E(conv_bwd_data) (Eq. 16); the raw dgamma /
-dbeta sums go through Q_G too.  Update, after the backward:  Eq. 19 on the
-24-bit masters of W, gamma and beta (learning rate 2^-lr_shift), then Q_W.
+Forward, in node order:  conv: W_q = Q_W(W_m) (Eq. 8), Z = SQ8(conv(A, W_q))
+(Eq. 15 on the MAC output), then with BN A' = Q_A(ReLU?(L1BN(Z))) (Eq. 12-15);
+max pooling keeps codes; residual add (+ReLU), concatenation and global
+average pooling are SQ8 of their exact result.
+Loss:  a given int8 error at the output, or the float64 softmax cross-entropy
+of the bilinearly upsampled logits, whose gradient is quantized to E1.
+Backward, in reverse node order:  the error of a tensor read by several nodes
+is SQ8 of the exact sum of their contributions (Eq. 16); L1BN backward (E2) ->
+G = Q_G(conv_bwd_weight) (Eq. 17, stochastic) and E1 = Q_E(conv_bwd_data);
+the raw dgamma / dbeta sums go through Q_G too.
+Update, after the backward:  Eq. 19 on the 24-bit masters of W, gamma and
+beta (learning rate 2^-lr_shift), then Q_W.
 
 Stochastic rounding keys: seed of the workload, step counter, tensor id
-16*l + {0: W, 1: gamma, 2: beta} for conv layer l = 1, 2, ...
+16*l + {0: W, 1: gamma, 2: beta} for the l-th conv (l = 1, 2, ... in node
+order).
 """
 import torch
 
@@ -27,93 +33,173 @@ class IntNet:
         self.dev = torch.device(device)
         self.lr_shift = lr_shift
         self.seed = inputs["seed"]
-        self.cfg = bn_cfg or iseg.bn_cfg()
+        self.cfg = dict(iseg.BN_DEFAULT, **(bn_cfg or {}))
+        self._cfgs = {r: iseg.bn_cfg(**dict(self.cfg, relu=r)) for r in (0, 1)}
         self.step_no = 0
         self.x = torch.from_numpy(inputs["x"]).to(self.dev)
         self.x_exp = iseg.new_exp(self.dev, inputs["x_exp"])
-        self.dy = torch.from_numpy(inputs["dy"]).to(self.dev)
-        self.dy_exp = iseg.new_exp(self.dev, inputs["dy_exp"])
+        self.dy = self.labels = None
+        if wl["loss"] == "given":
+            self.dy = torch.from_numpy(inputs["dy"]).to(self.dev)
+            self.dy_exp = iseg.new_exp(self.dev, inputs["dy_exp"])
+        else:
+            self.labels = torch.from_numpy(inputs["labels"]).to(self.dev)
         self.w_exp = iseg.new_exp(self.dev, W_MASTER_EXP + K_U - K_W)
-        self.convs = []
-        wi = 0
-        for layer in wl["layers"]:
-            if layer[0] != "conv":
+        self.convs = {}
+        ci = 0
+        for nd in wl["nodes"]:
+            if nd["kind"] != "conv":
                 continue
-            _, cin, cout, R, st, pad, dil = layer
-            wf = torch.from_numpy(inputs["weights"][wi]).to(self.dev)
-            wi += 1
+            wf = torch.from_numpy(inputs["weights"][ci]).to(self.dev)
+            ci += 1
             master, mexp = iseg.quantize(wf, K_U, iseg.ISEG_Q_UQ)          # Eq. 7
             assert int(mexp.item()) == W_MASTER_EXP
+            cout = nd["cout"]
             g_m = torch.full((cout,), 1 << (-GB_MASTER_EXP), dtype=torch.int32, device=self.dev)
             b_m = torch.zeros(cout, dtype=torch.int32, device=self.dev)
-            self.convs.append(dict(
-                cin=cin, cout=cout, R=R, st=st, pad=pad, dil=dil,
-                w_m=master, g_m=g_m, b_m=b_m,
-                w_q=iseg.weight_quant(master, K_U, K_W),
-                g_q=iseg.weight_quant(g_m, K_U, K_W),
-                b_q=iseg.weight_quant(b_m, K_U, K_W)))
+            L = dict(l=ci, w_m=master, g_m=g_m, b_m=b_m,
+                     w_q=iseg.weight_quant(master, K_U, K_W),
+                     g_q=iseg.weight_quant(g_m, K_U, K_W),
+                     b_q=iseg.weight_quant(b_m, K_U, K_W))
+            self.convs[nd["name"]] = L
+        self.loss = None
 
     # -------------------------------------------------------------------
     def forward(self):
-        a, ae = self.x, self.x_exp
-        rec = []
-        ci = 0
-        for layer in self.wl["layers"]:
-            if layer[0] == "conv":
-                L = self.convs[ci]
-                ci += 1
-                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, L["st"], L["pad"], L["dil"])
-                y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self.cfg)
-                rec.append(dict(kind="conv", L=L, a_in=a, a_in_exp=ae, z=z, z_exp=ze,
-                                saved=saved, a_out=y, a_out_exp=ye))
-                a, ae = y, ye
+        act = {"input": (self.x, self.x_exp)}
+        rec = {}
+        for nd in self.wl["nodes"]:
+            k, name = nd["kind"], nd["name"]
+            a, ae = act[nd["src"][0]]
+            r = dict(kind=k, a_in=a, a_in_exp=ae)
+            if k == "conv":
+                L = self.convs[name]
+                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"])
+                r.update(z=z, z_exp=ze)
+                if nd["bn"]:
+                    y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])])
+                    r["saved"] = saved
+                else:
+                    y, ye = z, ze
+            elif k == "maxpool":
+                y, ye = iseg.maxpool_fwd(a, ae, nd["k"], nd["stride"], nd["pad"])
+            elif k == "add":
+                b, be = act[nd["src"][1]]
+                y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"])
+                r.update(b_in=b, b_in_exp=be)
+            elif k == "gap":
+                y, ye = iseg.gap_fwd(a, ae)
+            elif k == "concat":
+                parts = [act[s] for s in nd["src"]]
+                y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts])
+                H, W = y.shape[1], y.shape[2]
+                r.update(widths=[p[0].shape[3] for p in parts],
+                         bcast=[tuple(p[0].shape[1:3]) != (H, W) for p in parts])
             else:
-                _, k, st, pad = layer
-                y, ye = iseg.maxpool_fwd(a, ae, k, st, pad)
-                rec.append(dict(kind="pool", k=k, st=st, pad=pad, a_in=a, a_out=y, a_out_exp=ye))
-                a, ae = y, ye
+                raise ValueError(k)
+            r.update(a_out=y, a_out_exp=ye)
+            rec[name] = r
+            act[name] = (y, ye)
         return rec
 
+    def loss_error(self, rec):
+        out = rec[self.wl["nodes"][-1]["name"]]
+        if self.wl["loss"] == "given":
+            return self.dy, self.dy_exp
+        loss, grad, e, ee = iseg.softmax_ce(out["a_out"], out["a_out_exp"], self.labels)
+        self.loss = loss
+        return e, ee
+
     def backward(self, rec):
-        e, ee = self.dy, self.dy_exp
+        contrib = {}
+
+        def send(name, codes, exp, exp_add=0, bcast=0):
+            contrib.setdefault(name, []).append((codes, exp, exp_add, bcast))
+
+        def merged(name):
+            parts = contrib.pop(name)
+            if len(parts) == 1 and not parts[0][2] and not parts[0][3]:
+                return parts[0][0], parts[0][1]
+            return iseg.sum_requant([p[0] for p in parts], [p[1] for p in parts],
+                                    exp_add=[p[2] for p in parts], bcast=[p[3] for p in parts])
+
+        e, ee = self.loss_error(rec)
+        send(self.wl["nodes"][-1]["name"], e, ee)
+        want_input = self.wl["input_grad"]
         grads = []
-        nconv = len(self.convs)
-        li = nconv
-        for i in range(len(rec) - 1, -1, -1):
-            r = rec[i]
-            if r["kind"] == "pool":
-                e, ee = iseg.maxpool_bwd(e, ee, r["a_in"], r["k"], r["st"], r["pad"])
-                r["e_in"], r["e_in_exp"] = e, ee
-                continue
-            L = r["L"]
-            dz, dze, dg, db, dge, dbe = iseg.bn_bwd(e, ee, r["z"], L["g_q"], r["saved"], self.cfg)
-            G, Ge = iseg.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape,
-                                         L["st"], L["pad"], L["dil"], iseg.ISEG_G_KEEP, 8,
-                                         self.seed, 16 * li, self.step_no)
-            r.update(dz=dz, dz_exp=dze, dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe,
-                     G=G, G_exp=Ge, li=li)
-            grads.append(r)
-            if li > 1 or self.wl["input_grad"]:
-                e, ee = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
-                                           L["st"], L["pad"], L["dil"])
-                r["e_in"], r["e_in_exp"] = e, ee
-            li -= 1
+        for nd in reversed(self.wl["nodes"]):
+            k, name = nd["kind"], nd["name"]
+            r = rec[name]
+            e, ee = merged(name)
+            r.update(e_out=e, e_out_exp=ee)
+            src = nd["src"][0]
+            need_in = src != "input" or want_input
+            if k == "conv":
+                L = self.convs[name]
+                if nd["bn"]:
+                    dz, dze, dg, db, dge, dbe = iseg.bn_bwd(e, ee, r["z"], L["g_q"], r["saved"],
+                                                            self._cfgs[int(nd["relu"])])
+                    r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
+                else:
+                    dz, dze = e, ee
+                G, Ge = iseg.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape,
+                                             nd["stride"], nd["pad"], nd["dil"], iseg.ISEG_G_KEEP, 8,
+                                             self.seed, 16 * L["l"], self.step_no)
+                r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
+                grads.append((nd, r))
+                if need_in:
+                    ei, eie = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
+                                                 nd["stride"], nd["pad"], nd["dil"])
+                    r.update(e_in=ei, e_in_exp=eie)
+                    send(src, ei, eie)
+            elif k == "maxpool":
+                if need_in:
+                    ei, eie = iseg.maxpool_bwd(e, ee, r["a_in"], nd["k"], nd["stride"], nd["pad"])
+                    r.update(e_in=ei, e_in_exp=eie)
+                    send(src, ei, eie)
+            elif k == "add":
+                d = iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]])
+                r.update(e_in=d, e_in_exp=ee)
+                for s in nd["src"]:
+                    if s != "input" or want_input:
+                        send(s, d, ee)
+            elif k == "gap":
+                if need_in:
+                    H, W = r["a_in"].shape[1:3]
+                    eg, ege = iseg.gap_bwd(e, ee, H, W)
+                    r.update(e_in=eg, e_in_exp=ege)
+                    send(src, eg, ege, bcast=1)
+            elif k == "concat":
+                parts = iseg.concat_split(e, r["widths"], skip=r["bcast"])
+                c0 = 0
+                for s, p, wdt, bc in zip(nd["src"], parts, r["widths"], r["bcast"]):
+                    if bc:
+                        pe, pee = iseg.spatial_sum(e, ee, 1, c0, wdt)
+                        send(s, pe, pee)
+                    else:
+                        send(s, p, ee)
+                    c0 += wdt
+        if want_input:
+            e, ee = merged("input")
+            rec["input"] = dict(kind="input", e_out=e, e_out_exp=ee)
         return grads
 
     def update(self, grads):
-        for r in grads:
-            L, li = r["L"], r["li"]
+        for nd, r in grads:
+            L = self.convs[nd["name"]]
+            l = L["l"]
             iseg.weight_update(L["w_m"], r["G"], r["G_exp"], self.lr_shift, W_MASTER_EXP, K_U, K_W,
                                L["w_q"])
-            C = L["cout"]
-            r["Gg"] = torch.empty(C, dtype=torch.int8, device=self.dev)
-            r["Gb"] = torch.empty(C, dtype=torch.int8, device=self.dev)
-            r["Gg_exp"], r["Gb_exp"] = iseg._out_exp(self.dev), iseg._out_exp(self.dev)
-            iseg.iseg_bn_param_update(r["dgamma"], r["dgamma_exp"], r["dbeta"], r["dbeta_exp"], 8,
-                                      self.seed, 16 * li + 1, 16 * li + 2, self.step_no,
-                                      self.lr_shift, GB_MASTER_EXP, K_U, K_W, L["g_m"], L["b_m"],
-                                      L["g_q"], L["b_q"], r["Gg"], r["Gb"], r["Gg_exp"],
-                                      r["Gb_exp"])
+            if nd["bn"]:
+                C = nd["cout"]
+                r["Gg"] = torch.empty(C, dtype=torch.int8, device=self.dev)
+                r["Gb"] = torch.empty(C, dtype=torch.int8, device=self.dev)
+                r["Gg_exp"], r["Gb_exp"] = iseg._out_exp(self.dev), iseg._out_exp(self.dev)
+                iseg.iseg_bn_param_update(r["dgamma"], r["dgamma_exp"], r["dbeta"], r["dbeta_exp"], 8,
+                                          self.seed, 16 * l + 1, 16 * l + 2, self.step_no,
+                                          self.lr_shift, GB_MASTER_EXP, K_U, K_W, L["g_m"], L["b_m"],
+                                          L["g_q"], L["b_q"], r["Gg"], r["Gb"], r["Gg_exp"],
+                                          r["Gb_exp"])
 
     def step(self):
         rec = self.forward()

@@ -1,6 +1,7 @@
-"""GPU parity of whole training steps (forward, backward, update) against the
-oracle's composition of the same steps: every activation, error, gradient
-code, exponent and the updated masters, bit-exact."""
+"""GPU parity of whole training steps (forward, loss, backward, update) of the
+workload graphs against the oracle's composition of the same steps: every
+activation, merged error, gradient code, exponent and the updated masters,
+bit-exact; the float loss within 1e-12 relative."""
 import numpy as np
 import pytest
 
@@ -18,43 +19,76 @@ def _ev(t):
     return int(t.item())
 
 
-def _run_both(wl, N, steps=1):
+CONV_KEYS = ("z", "dz", "G", "Gg", "Gb", "dgamma", "dbeta")
+EXP_KEYS = ("z_exp", "dz_exp", "G_exp", "Gg_exp", "Gb_exp")
+
+
+def _run_both(wl, steps=1):
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from oracle.model import OracleNet
     from paper_2011_14504_amd.model import IntNet
-    inp = synth.workload_inputs(wl, N)
+    inp = synth.workload_inputs(wl)
     gnet = IntNet(wl, inp, "cuda:0")
     onet = OracleNet(wl, inp)
     for s in range(steps):
+        print(f"[pipeline] {wl['name']} N={wl['N']} {wl['H']}x{wl['W']} step {s}", flush=True)
         grec = gnet.step()
         orec = onet.step()
         torch.cuda.synchronize()
-        for i, (g, o) in enumerate(zip(grec, orec)):
-            tag = f"step {s} layer {i} ({g['kind']})"
+        for nd in wl["nodes"]:
+            name = nd["name"]
+            g, o = grec[name], orec[name]
+            tag = f"step {s} {name} ({nd['kind']})"
             _cmp(g["a_out"], o["a_out"], tag + " activation")
             assert _ev(g["a_out_exp"]) == o["a_out_exp"], tag
-            if g["kind"] == "conv":
-                _cmp(g["z"], o["z"], tag + " conv output")
-                assert _ev(g["z_exp"]) == o["z_exp"], tag
-                for k in ("dz", "G", "Gg", "Gb", "dgamma", "dbeta"):
+            _cmp(g["e_out"], o["e_out"], tag + " error")
+            assert _ev(g["e_out_exp"]) == o["e_out_exp"], tag
+            for k in CONV_KEYS + ("e_in",):
+                if k in o:
                     _cmp(g[k], o[k], tag + " " + k)
-                for k in ("dz_exp", "G_exp", "Gg_exp", "Gb_exp"):
+            for k in EXP_KEYS + ("e_in_exp",):
+                if k in o:
                     assert _ev(g[k]) == o[k], tag + " " + k
-            if "e_in" in o:
-                _cmp(g["e_in"], o["e_in"], tag + " input error")
-                assert _ev(g["e_in_exp"]) == o["e_in_exp"], tag
-        for gl, ol in zip(gnet.convs, onet.convs):
+        if "input" in orec:
+            _cmp(grec["input"]["e_out"], orec["input"]["e_out"], f"step {s} input error")
+            assert _ev(grec["input"]["e_out_exp"]) == orec["input"]["e_out_exp"]
+        if wl["loss"] == "softmax_ce":
+            gl = float(gnet.loss.item())
+            assert abs(gl - onet.loss) <= 1e-12 * abs(onet.loss), (gl, onet.loss)
+        for name in gnet.convs:
             for k in ("w_m", "g_m", "b_m", "w_q", "g_q", "b_q"):
-                _cmp(gl[k], ol[k], f"step {s} {k}")
+                _cmp(gnet.convs[name][k], onet.convs[name][k], f"step {s} {name} {k}")
 
 
 def test_single_conv_two_steps():
-    _run_both(synth.SINGLE_CONV, None, steps=2)
+    _run_both(synth.SINGLE_CONV, steps=2)
 
 
 def test_vgg16_blocks12_one_image():
     # full 224x224 resolution, one image: every tile and ragged tail of the
     # real layer shapes, compared element by element
-    _run_both(synth.VGG16_BLOCKS12, 1)
+    _run_both(synth.scaled(synth.VGG16_BLOCKS12, 1))
+
+
+def test_resnet50_conv2x_two_images_two_steps():
+    # full 56x56 resolution, batch 2: projection and identity shortcuts
+    _run_both(synth.scaled(synth.RESNET50_CONV2X, 2), steps=2)
+
+
+def test_aspp_head_one_image():
+    # full 2048x32x32 input, batch 1: atrous rates 6/12/18, image pooling
+    # branch (L1BN over one sample per channel), concat, fuse, classifier
+    _run_both(synth.scaled(synth.ASPP_HEAD, 1))
+
+
+def test_deeplabv3_r50_128px():
+    # the whole DeepLabv3-ResNet50 step at 128x128 (ASPP on a 8x8 map, where
+    # rates 12 and 18 leave only the centre tap), softmax loss over 150 classes
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 128, 128))
+
+
+def test_deeplabv3_r50_ragged_96x80_two_steps():
+    # an input size that leaves ragged tiles at every stage (6x5 ASPP map)
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 96, 80), steps=2)
