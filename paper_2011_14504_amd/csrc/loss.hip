@@ -11,196 +11,372 @@
 // Float64 throughout, so that the integer codes decided at the end agree with
 // a float64 reference except where a value sits within ~1e-14 relative of a
 // rounding boundary.  Deterministic: every sum runs in a fixed order.
-//   k_ce_rows   one block per hi-res row: softmax per pixel (one wave per
-//               pixel, lanes over classes), gradient staged in LDS for 16
-//               pixels, folded into the row's column adjoint held in LDS;
-//               writes the row adjoint [N,H,w,K] and the row's loss
-//   k_ce_cols   one lane per low-res element: the row adjoint folded over
-//               the hi-res rows that read it -> gradient, |.| max partials
-//   k_ce_quant  SQ codes and exponent; block 0 also forms the mean loss
+//   k_ce_cells    one wave per bilinear cell (a run of output rows that read
+//                 the same two source rows x a run of columns): softmax of each
+//                 pixel with lanes over classes, the gradient folded into the
+//                 cell's four source corners, the cell's loss
+//   k_ce_combine  one block per low-res row: the corner sums of every cell
+//                 touching each low-res element, in cell order -> gradient
+//   k_ce_quant    SQ codes and exponent; block 0 also forms the mean loss
 #include <math.h>
 
 #include "iseg_common.h"
 
 namespace {
 
-struct CeArgs {
+// 64-bit value moved across lanes by a DPP control (both 32-bit halves)
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_mov_dpp((int)b, CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int l)
+{
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)b, l);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Wave-wide sum / max, the same value in every lane: within each row of 16
+// lanes by DPP steps whose pairs are symmetric (quad swaps, half-row and row
+// mirrors), then the four row results added in a fixed order.
+__device__ __forceinline__ double wave_sum_f64(double v)
+{
+    v += dpp_f64<0xB1>(v);      // quad_perm [1,0,3,2]
+    v += dpp_f64<0x4E>(v);      // quad_perm [2,3,0,1]
+    v += dpp_f64<0x141>(v);     // row_half_mirror
+    v += dpp_f64<0x140>(v);     // row_mirror
+    return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+}
+
+__device__ __forceinline__ double wave_max_f64(double v)
+{
+    v = fmax(v, dpp_f64<0xB1>(v));
+    v = fmax(v, dpp_f64<0x4E>(v));
+    v = fmax(v, dpp_f64<0x141>(v));
+    v = fmax(v, dpp_f64<0x140>(v));
+    return fmax(fmax(readlane_f64(v, 0), readlane_f64(v, 16)), fmax(readlane_f64(v, 32), readlane_f64(v, 48)));
+}
+
+// ---------------------------------------------------------------------------
+// Runs: maximal ranges of output coordinates that read the same two source
+// positions (i0, i1) with the same clamping, so that the interpolation weight
+// is affine in the coordinate inside a run.  A cell is (row run) x (column
+// run): its logits are bilinear in (x, y), so exp(l - m) follows a 2-D
+// multiplicative recurrence: exp at one corner, the x-step ratio, the y-step
+// ratio and the change of the x-step per row (4 exps per class and cell).
+// ---------------------------------------------------------------------------
+constexpr int kMaxRuns = 136;
+
+struct Run {
+    int16_t start, len, i0, i1;
+};
+
+struct CeCellArgs {
     const int8_t* logits;
     const int32_t* logit_exp;
     const uint8_t* labels;
     int32_t N, h, w, K, H, W;
-    double* gx;          // [N, H, w, K]
-    double* row_loss;    // [N * H]
-    double* grad;        // [N, h, w, K]
-    uint64_t* part;      // |grad| max partials
+    int32_t nry, nrx;
+    Run ry[kMaxRuns];
+    Run rx[kMaxRuns];
+    double* cell;        // [N][nry][nrx][4][K]: corner sums (i0,j0),(i0,j1),(i1,j0),(i1,j1)
+    double* cell_loss;   // [N][nry][nrx]
+    double* grad;        // [N][h][w][K]
+    uint64_t* part;      // |grad| max partials, one per combine block
     int32_t* status;
 };
 
-__device__ __forceinline__ void src_coord(int o, int n_in, int n_out, int& i0, int& i1, double& lam)
+__host__ __device__ __forceinline__ void src_coord_hd(int o, int n_in, int n_out, int& i0, int& i1, double& lam,
+                                                       bool& clamped)
 {
     double src = ((double)o + 0.5) * (double)n_in / (double)n_out - 0.5;
-    if (src < 0.0) src = 0.0;
+    clamped = src < 0.0;
+    if (clamped) src = 0.0;
     i0 = (int)floor(src);
     i1 = i0 + 1 < n_in ? i0 + 1 : n_in - 1;
     lam = src - (double)i0;
 }
 
-__device__ __forceinline__ double wave_max_f64(double v)
+// host: run table of one axis; returns the count, or -1 above kMaxRuns
+static int make_runs(int n_in, int n_out, Run* runs)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
-    return v;
+    int n = 0, pi0 = -1, pi1 = -1;
+    bool pcl = false;
+    for (int o = 0; o < n_out; o++) {
+        int i0, i1;
+        double lam;
+        bool cl;
+        src_coord_hd(o, n_in, n_out, i0, i1, lam, cl);
+        if (o == 0 || i0 != pi0 || i1 != pi1 || cl != pcl) {
+            if (n == kMaxRuns) return -1;
+            runs[n].start = (int16_t)o;
+            runs[n].len = 0;
+            runs[n].i0 = (int16_t)i0;
+            runs[n].i1 = (int16_t)i1;
+            n++;
+        }
+        runs[n - 1].len++;
+        pi0 = i0;
+        pi1 = i1;
+        pcl = cl;
+    }
+    return n;
 }
 
-__device__ __forceinline__ double wave_sum_f64(double v)
+__device__ __forceinline__ double interp(double a00, double a01, double a10, double a11, double wx0, double wx1,
+                                         double wy0, double wy1, double scale)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+    const double top = wx0 * a00 + wx1 * a01;
+    const double bot = wx0 * a10 + wx1 * a11;
+    return (wy0 * top + wy1 * bot) * scale;
 }
 
-constexpr int kChunk = 16;     // pixels whose gradient is staged in LDS at a time
+// one block per cell, its rows split over the 4 waves: softmax of every pixel
+// (lanes over classes), the gradient folded into the cell's four low-res
+// corners (x first within a row, then the row weights), the cell's loss; the
+// waves' corner sums are added in wave order
+constexpr int kCellWaves = 4;
+constexpr int kMaxRunLen = 256;
+constexpr int kLabBuf = 1024;
 
 template <int KT>
-__global__ __launch_bounds__(256) void k_ce_rows(CeArgs a)
+__global__ __launch_bounds__(256) void k_ce_cells(const CeCellArgs a)
 {
     extern __shared__ __align__(16) char smem[];
-    __shared__ int cj0[kChunk], cj1[kChunk];
-    __shared__ double cw0[kChunk], cw1[kChunk];
-    __shared__ double wloss[4];
-    const int y = blockIdx.x, n = blockIdx.y;
-    const int K = a.K, w = a.w, wk = a.w * a.K;
-    int8_t* L0 = (int8_t*)smem;                                   // [w][K] top source row
-    int8_t* L1 = L0 + wk;                                         // [w][K] bottom source row
-    double* gbuf = (double*)(smem + ((2 * wk + 15) & ~15));       // [kChunk][K]
-    double* gx = gbuf + kChunk * K;                               // [w][K]
-
-    int i0, i1;
-    double ly;
-    src_coord(y, a.h, a.H, i0, i1, ly);
-    const double wy0 = 1.0 - ly, wy1 = ly;
-    const int8_t* r0 = a.logits + ((int64_t)n * a.h + i0) * wk;
-    const int8_t* r1 = a.logits + ((int64_t)n * a.h + i1) * wk;
-    for (int t = threadIdx.x; t < wk; t += blockDim.x) {
-        L0[t] = r0[t];
-        L1[t] = r1[t];
-        gx[t] = 0.0;
-    }
-    const double scale = ldexp(1.0, *a.logit_exp);
-    const double P = (double)a.N * (double)a.H * (double)a.W;
+    __shared__ double wxs[kMaxRunLen];                     // column weight lambda_x per pixel of the run
+    __shared__ double wl[kCellWaves];
+    __shared__ uint8_t labs[kCellWaves][kLabBuf];          // each wave's labels, a chunk of rows at a time
+    const int n = blockIdx.z, sy = blockIdx.y, sx = blockIdx.x;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const uint8_t* lab_row = a.labels + ((int64_t)n * a.H + y) * a.W;
-    double lsum = 0.0;
-    bool bad_label = false;
+    const int K = a.K, wk = a.w * a.K;
+    const Run ry = a.ry[sy], rx = a.rx[sx];
+    const int j0 = rx.i0, j1 = rx.i1;
+    // the four corner columns of both source rows, and the reduction buffer
+    int8_t* C0 = (int8_t*)smem;                            // [4][K]: (i0,j0) (i0,j1) (i1,j0) (i1,j1)
+    double* red = (double*)(smem + ((4 * K + 15) & ~15));  // [waves][4][K]
+    const int8_t* r0 = a.logits + ((int64_t)n * a.h + ry.i0) * wk;
+    const int8_t* r1 = a.logits + ((int64_t)n * a.h + ry.i1) * wk;
+    for (int t = threadIdx.x; t < K; t += blockDim.x) {
+        C0[t] = r0[j0 * K + t];
+        C0[K + t] = r0[j1 * K + t];
+        C0[2 * K + t] = r1[j0 * K + t];
+        C0[3 * K + t] = r1[j1 * K + t];
+    }
+    for (int c = threadIdx.x; c < rx.len; c += blockDim.x) {
+        int e0, e1;
+        bool ecl;
+        double lx;
+        src_coord_hd(rx.start + c, a.w, a.W, e0, e1, lx, ecl);
+        wxs[c] = lx;
+    }
     __syncthreads();
-    for (int x0 = 0; x0 < a.W; x0 += kChunk) {
-        const int npx = a.W - x0 < kChunk ? a.W - x0 : kChunk;
-        if (threadIdx.x < npx) {
-            int j0, j1;
-            double lx;
-            src_coord(x0 + threadIdx.x, w, a.W, j0, j1, lx);
-            cj0[threadIdx.x] = j0;
-            cj1[threadIdx.x] = j1;
-            cw0[threadIdx.x] = 1.0 - lx;
-            cw1[threadIdx.x] = lx;
-        }
-        __syncthreads();
-        // softmax of each pixel: one wave per pixel, lane k + 64 t holds class k + 64 t
-        for (int pi = wv; pi < npx; pi += 4) {
-            const int j0 = cj0[pi], j1 = cj1[pi];
-            const double wx0 = cw0[pi], wx1 = cw1[pi];
-            const int lab = lab_row[x0 + pi];
-            bad_label |= lab >= K;
-            double l[KT];
-            double m = -INFINITY;
+    const double scale = ldexp(1.0, *a.logit_exp);
+    const double invP = 1.0 / ((double)a.N * (double)a.H * (double)a.W);
+
+    double c00[KT], c01[KT], c10[KT], c11[KT];
+    double m = -INFINITY;
 #pragma unroll
-            for (int t = 0; t < KT; t++) {
-                const int k = lane + 64 * t;
-                if (k < K) {
-                    const double top = wx0 * (double)L0[j0 * K + k] + wx1 * (double)L0[j1 * K + k];
-                    const double bot = wx0 * (double)L1[j0 * K + k] + wx1 * (double)L1[j1 * K + k];
-                    l[t] = (wy0 * top + wy1 * bot) * scale;
-                    m = fmax(m, l[t]);
-                } else {
-                    l[t] = 0.0;
+    for (int t = 0; t < KT; t++) {
+        const int k = lane + 64 * t;
+        if (k < K) {
+            c00[t] = C0[k];
+            c01[t] = C0[K + k];
+            c10[t] = C0[2 * K + k];
+            c11[t] = C0[3 * K + k];
+            m = fmax(m, fmax(fmax(c00[t], c01[t]), fmax(c10[t], c11[t])) * scale);
+        } else {
+            c00[t] = c01[t] = c10[t] = c11[t] = 0.0;
+        }
+    }
+    m = wave_max_f64(m);
+
+    // this wave's rows, and the weights at its first two rows / the run's first two columns
+    const int rc = (ry.len + kCellWaves - 1) / kCellWaves;
+    const int rbeg = wv * rc;
+    const int rend = rbeg + rc < ry.len ? rbeg + rc : ry.len;
+    double G00[KT], G01[KT], G10[KT], G11[KT];
+#pragma unroll
+    for (int t = 0; t < KT; t++) G00[t] = G01[t] = G10[t] = G11[t] = 0.0;
+    double lsum = 0.0, luni = 0.0, llab = 0.0, sv = 1.0;
+    int pc = 0;
+    bool bad = false;
+    if (rbeg < rend) {
+        int d0, d1;
+        bool dcl;
+        double ly0, ly1;
+        const double lx0 = wxs[0], lx1 = wxs[rx.len > 1 ? 1 : 0];
+        src_coord_hd(ry.start + rbeg, a.h, a.H, d0, d1, ly0, dcl);
+        src_coord_hd(ry.start + rbeg + (rend - rbeg > 1 ? 1 : 0), a.h, a.H, d0, d1, ly1, dcl);
+        double Er[KT], Rr[KT], Qy[KT], Tx[KT];
+#pragma unroll
+        for (int t = 0; t < KT; t++) {
+            const double l00 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx0, lx0, 1.0 - ly0, ly0, scale);
+            const double l10 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx1, lx1, 1.0 - ly0, ly0, scale);
+            const double l01 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx0, lx0, 1.0 - ly1, ly1, scale);
+            const double l11 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx1, lx1, 1.0 - ly1, ly1, scale);
+            const bool on = lane + 64 * t < K;
+            Er[t] = on ? exp(l00 - m) : 0.0;
+            Rr[t] = exp(l10 - l00);
+            Qy[t] = exp(l01 - l00);
+            Tx[t] = exp((l11 - l01) - (l10 - l00));
+        }
+        const int chunk_rows = kLabBuf / rx.len;
+        for (int r = rbeg; r < rend; r++) {
+            const int y = ry.start + r;
+            if ((r - rbeg) % chunk_rows == 0) {
+                // the labels of the next rows of this wave, loaded in one go
+                const int nr = rend - r < chunk_rows ? rend - r : chunk_rows;
+                for (int t = lane; t < nr * rx.len; t += 64)
+                    labs[wv][t] = a.labels[((int64_t)n * a.H + y + t / rx.len) * a.W + rx.start + t % rx.len];
+                __builtin_amdgcn_wave_barrier();
+            }
+            const uint8_t* lab_row = &labs[wv][((r - rbeg) % chunk_rows) * rx.len];
+            int e0, e1;
+            bool ecl;
+            double ly;
+            src_coord_hd(y, a.h, a.H, e0, e1, ly, ecl);
+            const double wy0 = 1.0 - ly, wy1 = ly;
+            if (r > rbeg) {
+#pragma unroll
+                for (int t = 0; t < KT; t++) {
+                    Er[t] *= Qy[t];
+                    Rr[t] *= Tx[t];
                 }
             }
-            m = wave_max_f64(m);
-            double e[KT];
-            double s = 0.0, ll = 0.0;
+            double E[KT], alo[KT], ahi[KT], olo[KT], ohi[KT];
 #pragma unroll
             for (int t = 0; t < KT; t++) {
-                const int k = lane + 64 * t;
-                e[t] = k < K ? exp(l[t] - m) : 0.0;
-                s += e[t];
-                if (k == lab) ll = l[t];
+                E[t] = Er[t];
+                alo[t] = ahi[t] = olo[t] = ohi[t] = 0.0;
             }
-            s = wave_sum_f64(s);
-            ll = wave_sum_f64(ll);                 // one lane holds the label's logit
+            for (int c = 0; c < rx.len; c++) {
+                const double lx = wxs[c];
+                const double wx0 = 1.0 - lx, wx1 = lx;
+                if (c > 0) {
+#pragma unroll
+                    for (int t = 0; t < KT; t++) E[t] *= Rr[t];
+                }
+                double s = 0.0;
+#pragma unroll
+                for (int t = 0; t < KT; t++) s += E[t];
+                s = wave_sum_f64(s);
+                const double cp = invP / s;
+                // softmax part of the gradient: E / s / P
+#pragma unroll
+                for (int t = 0; t < KT; t++) {
+                    const double g = E[t] * cp;
+                    alo[t] += wx0 * g;
+                    ahi[t] += wx1 * g;
+                }
+                // one-hot part: the label's lane collects the pixel's column weights
+                const int lab = lab_row[c];
+                bad |= lab >= K;
+                const bool mine = lane == (lab & 63);
+#pragma unroll
+                for (int t = 0; t < KT; t++)
+                    if ((lab >> 6) == t && mine) {
+                        olo[t] += wx0;
+                        ohi[t] += wx1;
+                    }
+                // loss: log(s) + m - l(label); the logs are taken 64 pixels at a time,
+                // the label logits at the end of the row from the one-hot weights
+                luni += m;
+                if ((pc & 63) == lane) sv = s;
+                pc++;
+                if ((pc & 63) == 0) lsum += log(sv);
+            }
 #pragma unroll
             for (int t = 0; t < KT; t++) {
-                const int k = lane + 64 * t;
-                if (k < K) gbuf[pi * K + k] = (e[t] / s - (k == lab ? 1.0 : 0.0)) / P;
+                const double glo = alo[t] - olo[t] * invP, ghi = ahi[t] - ohi[t] * invP;
+                G00[t] += wy0 * glo;
+                G01[t] += wy0 * ghi;
+                G10[t] += wy1 * glo;
+                G11[t] += wy1 * ghi;
+                // sum over the row's pixels labelled k of l_k = the corners' bilinear mix
+                llab += (wy0 * (c00[t] * olo[t] + c01[t] * ohi[t]) + wy1 * (c10[t] * olo[t] + c11[t] * ohi[t])) *
+                        scale;
             }
-            if (lane == 0) lsum += log(s) + m - ll;
         }
-        __syncthreads();
-        // fold the chunk into the columns it touches, pixels in ascending order
-        const int jlo = cj0[0], jhi = cj1[npx - 1];
-        const int ncol = jhi - jlo + 1;
-        for (int t = threadIdx.x; t < ncol * K; t += blockDim.x) {
-            const int j = jlo + t / K, k = t % K;
-            double acc = gx[j * K + k];
-            for (int pi = 0; pi < npx; pi++) {
-                double wgt = 0.0;
-                if (cj0[pi] == j) wgt += cw0[pi];
-                if (cj1[pi] == j) wgt += cw1[pi];
-                if (wgt != 0.0) acc += wgt * gbuf[pi * K + k];
-            }
-            gx[j * K + k] = acc;
-        }
-        __syncthreads();
     }
-    double* out = a.gx + ((int64_t)n * a.H + y) * wk;
-    for (int t = threadIdx.x; t < wk; t += blockDim.x) out[t] = gx[t];
-    if (lane == 0) wloss[wv] = lsum;
-    if (bad_label && lane == 0) set_status(a.status, ISEG_DEV_RANGE);
+    if (lane < (pc & 63)) lsum += log(sv);
+    lsum = wave_sum_f64(lsum - llab);
+#pragma unroll
+    for (int t = 0; t < KT; t++) {
+        const int k = lane + 64 * t;
+        if (k < K) {
+            double* o = red + (int64_t)wv * 4 * K;
+            o[k] = G00[t];
+            o[K + k] = G01[t];
+            o[2 * K + k] = G10[t];
+            o[3 * K + k] = G11[t];
+        }
+    }
+    if (lane == 0) {
+        wl[wv] = lsum + luni;
+        if (bad) set_status(a.status, ISEG_DEV_RANGE);
+    }
     __syncthreads();
-    if (threadIdx.x == 0) a.row_loss[(int64_t)n * a.H + y] = ((wloss[0] + wloss[1]) + wloss[2]) + wloss[3];
+    const int64_t cid = ((int64_t)n * a.nry + sy) * a.nrx + sx;
+    double* out = a.cell + cid * 4 * K;
+    for (int t = threadIdx.x; t < 4 * K; t += blockDim.x)
+        out[t] = ((red[t] + red[4 * K + t]) + red[8 * K + t]) + red[12 * K + t];
+    if (threadIdx.x == 0) a.cell_loss[cid] = ((wl[0] + wl[1]) + wl[2]) + wl[3];
 }
 
-// grad[n,i,j,k] = sum over hi-res rows y of Ay[y,i] gx[n,y,j,k], y ascending
-__global__ __launch_bounds__(256) void k_ce_cols(CeArgs a)
+// grad[n,i,j,k]: sum over the cells with a corner at (i, j), in cell order
+// (row runs, then column runs, then corners); one block per (n, i)
+__global__ __launch_bounds__(256) void k_ce_combine(const CeCellArgs a)
 {
-    const int64_t total = (int64_t)a.N * a.h * a.w * a.K;
-    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    uint64_t m = 0;
-    if (e < total) {
-        const int64_t wk = (int64_t)a.w * a.K;
-        const int64_t jk = e % wk;
-        const int64_t ni = e / wk;
-        const int i = (int)(ni % a.h);
-        const int n = (int)(ni / a.h);
-        const double sc = (double)a.H / (double)a.h;
-        int ylo = (int)floor(((double)i - 0.5) * sc - 0.5) - 1;
-        int yhi = (int)ceil(((double)i + 1.5) * sc - 0.5) + 1;
-        ylo = ylo < 0 ? 0 : ylo;
-        yhi = yhi > a.H - 1 ? a.H - 1 : yhi;
-        double acc = 0.0;
-        const double* col = a.gx + (int64_t)n * a.H * wk + jk;
-        for (int y = ylo; y <= yhi; y++) {
-            int i0, i1;
-            double ly;
-            src_coord(y, a.h, a.H, i0, i1, ly);
-            double wgt = 0.0;
-            if (i0 == i) wgt += 1.0 - ly;
-            if (i1 == i) wgt += ly;
-            if (wgt != 0.0) acc += wgt * col[(int64_t)y * wk];
-        }
-        a.grad[e] = acc;
-        m = (uint64_t)__double_as_longlong(acc) & 0x7fffffffffffffffull;
+    const int n = blockIdx.y, i = blockIdx.x;
+    __shared__ int ys_lo, ys_hi;
+    __shared__ int2 xs[256];             // column run range per low-res column
+    if (threadIdx.x == 0) {
+        int lo = a.nry, hi = -1;
+        for (int s = 0; s < a.nry; s++)
+            if (a.ry[s].i0 == i || a.ry[s].i1 == i) {
+                lo = s < lo ? s : lo;
+                hi = s;
+            }
+        ys_lo = lo;
+        ys_hi = hi;
     }
-    block_store_max_u64(m, a.part);
+    for (int j = threadIdx.x; j < a.w; j += blockDim.x) {
+        int lo = a.nrx, hi = -1;
+        for (int s = 0; s < a.nrx; s++)
+            if (a.rx[s].i0 == j || a.rx[s].i1 == j) {
+                lo = s < lo ? s : lo;
+                hi = s;
+            }
+        xs[j] = make_int2(lo, hi);
+    }
+    __syncthreads();
+    const int wk = a.w * a.K;
+    uint64_t mx = 0;
+    for (int e = threadIdx.x; e < wk; e += blockDim.x) {
+        const int j = e / a.K, k = e % a.K;
+        double acc = 0.0;
+        for (int s = ys_lo; s <= ys_hi; s++) {
+            const Run ry = a.ry[s];
+            for (int g = xs[j].x; g <= xs[j].y; g++) {
+                const Run rx = a.rx[g];
+                const double* c = a.cell + (((int64_t)n * a.nry + s) * a.nrx + g) * 4 * a.K + k;
+                if (ry.i0 == i && rx.i0 == j) acc += c[0];
+                if (ry.i0 == i && rx.i1 == j) acc += c[a.K];
+                if (ry.i1 == i && rx.i0 == j) acc += c[2 * a.K];
+                if (ry.i1 == i && rx.i1 == j) acc += c[3 * a.K];
+            }
+        }
+        a.grad[((int64_t)n * a.h + i) * wk + e] = acc;
+        const uint64_t b = (uint64_t)__double_as_longlong(acc) & 0x7fffffffffffffffull;
+        mx = b > mx ? b : mx;
+    }
+    block_store_max_u64(mx, a.part);
 }
 
 // smallest e with |v| < 2^e for the positive double with bits mb (frexp's exponent)
@@ -212,7 +388,7 @@ __device__ __forceinline__ int frexp_exp_bits64(uint64_t mb)
     return E - 1022;
 }
 
-__global__ __launch_bounds__(256) void k_ce_quant(CeArgs a, const unsigned long long* maxp, int bits,
+__global__ __launch_bounds__(256) void k_ce_quant(const CeCellArgs a, const unsigned long long* maxp, int bits,
                                                   int8_t* __restrict__ err, int32_t* err_exp, double* loss)
 {
     const uint64_t mb = *maxp;
@@ -220,11 +396,11 @@ __global__ __launch_bounds__(256) void k_ce_quant(CeArgs a, const unsigned long 
     const int64_t total = (int64_t)a.N * a.h * a.w * a.K;
     if (blockIdx.x == 0) {
         if (threadIdx.x == 0) *err_exp = b + 1 - bits;
-        // mean loss: row losses summed in a fixed tree order
+        // mean loss: cell losses summed in a fixed tree order
         __shared__ double red[256];
         double s = 0.0;
-        const int64_t rows = (int64_t)a.N * a.H;
-        for (int64_t r = threadIdx.x; r < rows; r += blockDim.x) s += a.row_loss[r];
+        const int64_t cells = (int64_t)a.N * a.nry * a.nrx;
+        for (int64_t r = threadIdx.x; r < cells; r += blockDim.x) s += a.cell_loss[r];
         red[threadIdx.x] = s;
         __syncthreads();
         for (int o = 128; o > 0; o >>= 1) {
@@ -244,28 +420,33 @@ __global__ __launch_bounds__(256) void k_ce_quant(CeArgs a, const unsigned long 
 }
 
 template <int KT>
-int launch_rows(const CeArgs& a, size_t lds, hipStream_t s)
+int launch_cells(const CeCellArgs& a, size_t lds, hipStream_t s)
 {
-    if (hipFuncSetAttribute((const void*)k_ce_rows<KT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+    if (hipFuncSetAttribute((const void*)k_ce_cells<KT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
         return ISEG_ERR_DEVICE;
-    hipLaunchKernelGGL(k_ce_rows<KT>, dim3((unsigned)a.H, (unsigned)a.N), dim3(256), lds, s, a);
+    hipLaunchKernelGGL(k_ce_cells<KT>, dim3((unsigned)a.nrx, (unsigned)a.nry, (unsigned)a.N), dim3(256), lds, s, a);
     return launch_ok();
-}
-
-size_t rows_lds(int64_t w, int64_t K)
-{
-    return (size_t)((2 * w * K + 15) & ~(int64_t)15) + (size_t)(kChunk * K + w * K) * 8;
 }
 
 }  // namespace
 
+// workspace: [max][cells][cell losses][grad (if not given)][max partials]
+static size_t ce_cell_bytes(int64_t N, int64_t nry, int64_t nrx, int64_t K)
+{
+    return align256((size_t)(N * nry * nrx * 4 * K) * 8);
+}
+
 extern "C" size_t iseg_softmax_ce_ws(int64_t N, int64_t h, int64_t w, int64_t K, int64_t H, int64_t W)
 {
-    (void)W;
-    const int64_t nlow = N * h * w * K;
-    return 256 + align256((size_t)(N * H * w * K) * 8) + align256((size_t)(N * H) * 8) +
-           align256((size_t)nlow * 8) + align256((size_t)ceil_div64(nlow, 256) * 8);
+    if (N < 1 || h < 1 || w < 1 || K < 1 || H < h || W < w || h > 64 || w > 64 || H > 32767 || W > 32767)
+        return 0;
+    Run tmp[kMaxRuns];
+    const int nry = make_runs((int)h, (int)H, tmp), nrx = make_runs((int)w, (int)W, tmp);
+    if (nry < 0 || nrx < 0) return 0;
+    return 256 + ce_cell_bytes(N, nry, nrx, K) +
+           align256((size_t)(N * nry * nrx) * 8) + align256((size_t)(N * h * w * K) * 8) +
+           align256((size_t)(N * h) * 8);
 }
 
 extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, const uint8_t* labels, int64_t N,
@@ -275,35 +456,41 @@ extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, c
 {
     if (N < 1 || h < 1 || w < 1 || K < 1 || H < h || W < w || bits < 2 || bits > 8) return ISEG_ERR_ARG;
     if (!logits || !logit_exp || !labels || !err || !err_exp) return ISEG_ERR_ARG;
-    if (K > 256 || H > 65535 || N > 65535 || rows_lds(w, K) > 150 * 1024) return ISEG_ERR_UNSUPPORTED;
-    if (!ws || ws_bytes < iseg_softmax_ce_ws(N, h, w, K, H, W)) return ISEG_ERR_WORKSPACE;
-    CeArgs a{};
+    if (K > 256 || h > 64 || w > 64 || H > 32767 || W > 32767 || N > 65535) return ISEG_ERR_UNSUPPORTED;
+    const size_t need = iseg_softmax_ce_ws(N, h, w, K, H, W);
+    if (need == 0) return ISEG_ERR_UNSUPPORTED;
+    if (!ws || ws_bytes < need) return ISEG_ERR_WORKSPACE;
+    CeCellArgs a{};
     a.logits = logits; a.logit_exp = logit_exp; a.labels = labels;
     a.N = (int32_t)N; a.h = (int32_t)h; a.w = (int32_t)w; a.K = (int32_t)K; a.H = (int32_t)H; a.W = (int32_t)W;
+    a.nry = make_runs((int)h, (int)H, a.ry);
+    a.nrx = make_runs((int)w, (int)W, a.rx);
+    for (int i = 0; i < a.nrx; i++)
+        if (a.rx[i].len > kMaxRunLen) return ISEG_ERR_UNSUPPORTED;
     a.status = dev_status;
     char* p = (char*)ws;
     unsigned long long* maxp = (unsigned long long*)p;
     p += 256;
-    a.gx = (double*)p;
-    p += align256((size_t)(N * H * w * K) * 8);
-    a.row_loss = (double*)p;
-    p += align256((size_t)(N * H) * 8);
+    a.cell = (double*)p;
+    p += ce_cell_bytes(N, a.nry, a.nrx, K);
+    a.cell_loss = (double*)p;
+    p += align256((size_t)(N * a.nry * a.nrx) * 8);
     double* gws = (double*)p;
     p += align256((size_t)(N * h * w * K) * 8);
     a.part = (uint64_t*)p;
     a.grad = grad ? grad : gws;
-    const int64_t nlow = N * h * w * K;
-    const size_t lds = rows_lds(w, K);
+    int rc;
+    const size_t lds = (size_t)((4 * K + 15) & ~(int64_t)15) + (size_t)(kCellWaves * 4 * K) * 8;
     const int kt = (int)((K + 63) / 64);
-    int rc = kt == 1 ? launch_rows<1>(a, lds, stream)
-           : kt == 2 ? launch_rows<2>(a, lds, stream)
-           : kt == 3 ? launch_rows<3>(a, lds, stream)
-                     : launch_rows<4>(a, lds, stream);
+    rc = kt == 1 ? launch_cells<1>(a, lds, stream)
+       : kt == 2 ? launch_cells<2>(a, lds, stream)
+       : kt == 3 ? launch_cells<3>(a, lds, stream)
+                 : launch_cells<4>(a, lds, stream);
     if (rc) return rc;
-    const unsigned nb = (unsigned)ceil_div64(nlow, 256);
-    hipLaunchKernelGGL(k_ce_cols, dim3(nb), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)h, (unsigned)N), dim3(256), 0, stream, a);
     if ((rc = launch_ok())) return rc;
-    if ((rc = launch_reduce_max(a.part, nb, maxp, stream))) return rc;
+    if ((rc = launch_reduce_max(a.part, N * h, maxp, stream))) return rc;
+    const int64_t nlow = N * h * w * K;
     hipLaunchKernelGGL(k_ce_quant, dim3(grid_for(nlow, 256, 2048)), dim3(256), 0, stream, a,
                        (const unsigned long long*)maxp, (int)bits, err, err_exp, loss);
     return launch_ok();
