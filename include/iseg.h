@@ -255,6 +255,37 @@ int iseg_bn_param_update(const int64_t* dgamma, const int32_t* dgamma_exp,
                          int8_t* g_gamma, int8_t* g_beta, int32_t* g_gamma_exp, int32_t* g_beta_exp,
                          int32_t* dev_status, hipStream_t stream);
 
+/* One parameter tensor of iseg_update_multi (a DEVICE array of these). */
+enum iseg_update_kind {
+    ISEG_UPD_CODES = 0,    /* g: int8 codes of a quantized gradient (conv weights after Q_G) */
+    ISEG_UPD_RAW = 1       /* g: int64 raw sums (L1BN dgamma / dbeta); Q_G applied first */
+};
+typedef struct iseg_update_desc {
+    int32_t* master;       /* k_U-bit master codes, updated in place */
+    int8_t* w_q;           /* out: UQ(master, k_W) */
+    const void* g;         /* gradient: int8 codes or int64 sums, see kind */
+    const int32_t* g_exp;  /* device exponent of g */
+    int8_t* g_q;           /* ISEG_UPD_RAW: out, the Q_G codes (may be NULL) */
+    int32_t* g_q_exp;      /* ISEG_UPD_RAW: out, their exponent (may be NULL) */
+    int64_t n;             /* elements; ISEG_UPD_RAW requires n <= 65536 */
+    int32_t kind;          /* enum iseg_update_kind */
+    int32_t master_exp;    /* 1-k_U for conv weights, 2-k_U for gamma / beta (x2 fold) */
+    uint32_t tensor_id;    /* ISEG_UPD_RAW: Philox tensor id of Q_G */
+    int32_t reserved;
+} iseg_update_desc;
+
+/* iseg_update_multi -- the update step of a whole network in one launch: for
+ * every descriptor, Q_G (ISEG_UPD_RAW: stochastic RQ to `bits` keeping the
+ * scale, Eq. 5-6 and 17, Philox index = the element, key (seed, tensor_id),
+ * counter step), then Delta = UQ(G 2^-lr_shift, k_U) (Eq. 19), master <-
+ * clamp(master - Delta), w_q = UQ(master, k_W) (Eq. 8, or Eq. 14's fold for
+ * gamma / beta).  Equal to iseg_weight_update / iseg_bn_param_update per
+ * tensor.  descs: device array of n_desc descriptors (caller-owned; the
+ * tensors they point to must not overlap). */
+int iseg_update_multi(const iseg_update_desc* descs, int32_t n_desc, int32_t bits, uint64_t seed,
+                      uint32_t step, int32_t lr_shift, int32_t k_U, int32_t k_W, int32_t* dev_status,
+                      hipStream_t stream);
+
 /* iseg_weight_quant -- Eq. 8 alone: w_q = UQ(master, k_W) from k_U-bit masters. */
 int iseg_weight_quant(const int32_t* master, int64_t n, int32_t k_U, int32_t k_W,
                       int8_t* w_q, hipStream_t stream);

@@ -294,6 +294,117 @@ bool pool_geom(int64_t N, int64_t H, int64_t W, int64_t C, int32_t k, int32_t st
     return true;
 }
 
+// ---------------------------------------------------------------------------
+// Backward for any window / stride / padding, 16 channels per lane:
+//   k_pool_argtap16   per output window: the tap (r k + s, row-major) of each
+//                     channel's first maximum, one byte per element
+//   k_pool_gather16   per input position: the sum of dy over the covering
+//                     windows whose tap is this position (at most
+//                     ceil(k/st)^2 windows); pass 0 writes per-block max |sum|
+//                     partials, pass 1 reduces them and writes the SQ codes
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_pool_argtap16(const int8_t* __restrict__ x, uint8_t* __restrict__ tap,
+                                                       PoolGeom g)
+{
+    const int64_t C16 = g.C / 16;
+    const int64_t total = g.N * g.P * g.Q * C16;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t c16 = i % C16;
+        int64_t t = i / C16;
+        const int q = (int)(t % g.Q);
+        t /= g.Q;
+        const int p = (int)(t % g.P);
+        const int64_t n = t / g.P;
+        int best[16], bt[16];
+#pragma unroll
+        for (int j = 0; j < 16; j++) { best[j] = -1000; bt[j] = 0; }
+        for (int r = 0; r < g.k; r++) {
+            const int h = p * g.st - g.pad + r;
+            if (h < 0 || h >= g.H) continue;
+            for (int s2 = 0; s2 < g.k; s2++) {
+                const int w = q * g.st - g.pad + s2;
+                if (w < 0 || w >= g.W) continue;
+                const uint4 v = *(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + c16 * 16);
+                const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+                const int tp = r * g.k + s2;
+#pragma unroll
+                for (int j = 0; j < 16; j++) {
+                    const int b = (int)(int8_t)(vw[j >> 2] >> (8 * (j & 3)));
+                    if (b > best[j]) { best[j] = b; bt[j] = tp; }
+                }
+            }
+        }
+        uint32_t o[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int j = 0; j < 16; j++) o[j >> 2] |= (uint32_t)(uint8_t)bt[j] << (8 * (j & 3));
+        *(uint4*)(tap + i * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+}
+
+template <int PASS>
+__global__ __launch_bounds__(256) void k_pool_gather16(const int8_t* __restrict__ dy, const uint8_t* __restrict__ tap,
+                                                       PoolGeom g, uint64_t* part, int64_t nparts,
+                                                       const int32_t* dy_exp, int32_t* dx_exp, int bits,
+                                                       int8_t* __restrict__ dx)
+{
+    int r = 0;
+    if (PASS == 1) {
+        const uint64_t M = reduce_partials_u64(part, nparts);
+        r = M ? bitlen_u64(M) - (bits - 1) : 0;
+        if (blockIdx.x == 0 && threadIdx.x == 0) *dx_exp = *dy_exp + r;
+    }
+    const int64_t C16 = g.C / 16;
+    const int64_t total = g.N * g.H * g.W * C16;
+    uint64_t mx = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t c16 = i % C16;
+        int64_t t = i / C16;
+        const int w = (int)(t % g.W);
+        t /= g.W;
+        const int h = (int)(t % g.H);
+        const int64_t n = t / g.H;
+        // windows p with p st - pad <= h <= p st - pad + k - 1
+        int plo = h + g.pad - g.k + 1;
+        plo = plo <= 0 ? 0 : (plo + g.st - 1) / g.st;
+        int phi = (h + g.pad) / g.st;
+        phi = phi < g.P - 1 ? phi : (int)g.P - 1;
+        int qlo = w + g.pad - g.k + 1;
+        qlo = qlo <= 0 ? 0 : (qlo + g.st - 1) / g.st;
+        int qhi = (w + g.pad) / g.st;
+        qhi = qhi < g.Q - 1 ? qhi : (int)g.Q - 1;
+        int sum[16];
+#pragma unroll
+        for (int j = 0; j < 16; j++) sum[j] = 0;
+        for (int p = plo; p <= phi; p++)
+            for (int q = qlo; q <= qhi; q++) {
+                const int me = (h - (p * g.st - g.pad)) * g.k + (w - (q * g.st - g.pad));
+                const int64_t o = ((n * g.P + p) * g.Q + q) * g.C + c16 * 16;
+                const uint4 tv = *(const uint4*)(tap + o);
+                const uint4 dv = *(const uint4*)(dy + o);
+                const uint32_t tw[4] = {tv.x, tv.y, tv.z, tv.w}, dw[4] = {dv.x, dv.y, dv.z, dv.w};
+#pragma unroll
+                for (int j = 0; j < 16; j++)
+                    if ((int)((tw[j >> 2] >> (8 * (j & 3))) & 0xff) == me)
+                        sum[j] += (int)(int8_t)(dw[j >> 2] >> (8 * (j & 3)));
+            }
+        if (PASS == 0) {
+#pragma unroll
+            for (int j = 0; j < 16; j++) {
+                const uint64_t a = (uint64_t)(sum[j] < 0 ? -sum[j] : sum[j]);
+                mx = a > mx ? a : mx;
+            }
+        } else {
+            uint32_t o[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int j = 0; j < 16; j++) o[j >> 2] |= (uint32_t)(uint8_t)sq_code(sum[j], r, bits) << (8 * (j & 3));
+            *(uint4*)(dx + i * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+    }
+    if (PASS == 0) block_store_max_u64(mx, part);
+}
+
 }  // namespace
 
 extern "C" int iseg_maxpool_fwd(const int8_t* x, const int32_t* x_exp, int64_t N, int64_t H, int64_t W,
@@ -350,6 +461,23 @@ extern "C" int iseg_maxpool_bwd(const int8_t* dy, const int32_t* dy_exp, const i
             if ((rc = launch_ok())) return rc;
         }
         return ISEG_OK;
+    }
+    const size_t tap_need = align256((size_t)(g.N * g.P * g.Q * C)) + 1024 * 8;
+    if (C % 16 == 0 && k <= 15 && (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx) & 15) == 0 && total > 0 &&
+        tap_need <= align256((size_t)total * 4)) {
+        // any window: per-window argmax taps, then two gathers (max, codes)
+        uint8_t* tap = (uint8_t*)acc;
+        uint64_t* part = (uint64_t*)((char*)acc + align256((size_t)(g.N * g.P * g.Q * C)));
+        const int64_t nwin = g.N * g.P * g.Q * (C / 16);
+        hipLaunchKernelGGL(k_pool_argtap16, dim3(grid_for(nwin, 256, 8192)), dim3(256), 0, stream, x, tap, g);
+        if ((rc = launch_ok())) return rc;
+        const unsigned nb = grid_for(total / 16, 256, 1024);
+        ISEG_TIMED_LAUNCH(ISEG_KID_MAXPOOL_BWD, stream, k_pool_gather16<0>, dim3(nb), dim3(256), 0, stream, dy, tap,
+                          g, part, (int64_t)nb, dy_exp, dx_exp, bits, dx);
+        if ((rc = launch_ok())) return rc;
+        hipLaunchKernelGGL(k_pool_gather16<1>, dim3(grid_for(total / 16, 256, 4096)), dim3(256), 0, stream, dy, tap,
+                           g, part, (int64_t)nb, dy_exp, dx_exp, bits, dx);
+        return launch_ok();
     }
     if ((rc = launch_fill_u32(maxp, 2, 0, stream))) return rc;
     if (k == stride && pad == 0 && C % 4 == 0 &&

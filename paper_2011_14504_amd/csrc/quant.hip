@@ -524,6 +524,79 @@ extern "C" int iseg_bn_param_update(const int64_t* dgamma, const int32_t* dgamma
     return launch_ok();
 }
 
+// ---------------------------------------------------------------------------
+// every parameter of a network in one launch: block (x, t) takes part of
+// descriptor t.  ISEG_UPD_CODES tensors (conv weights, G already quantized by
+// Q_G) are split over the x blocks; ISEG_UPD_RAW tensors (L1BN gamma / beta:
+// raw int64 sums, Q_G = stochastic RQ with the tensor's max first) are small
+// and handled by block x = 0 alone.
+// ---------------------------------------------------------------------------
+struct UpdCfg {
+    uint64_t seed;
+    uint32_t step;
+    int32_t bits, lr_shift, k_U, k_W;
+};
+
+__device__ __forceinline__ int64_t upd_delta(int64_t g, int sh, int k_U, int64_t lim)
+{
+    if (g == 0 || sh < -40) return 0;
+    if (sh > 40) return g > 0 ? lim : -lim;
+    if (sh >= 0) return clamp_k(g * ((int64_t)1 << sh), k_U);
+    return clamp_k(shr_rhu(g, -sh), k_U);
+}
+
+__global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __restrict__ descs, UpdCfg u)
+{
+    const iseg_update_desc d = descs[blockIdx.y];
+    const int dq = u.k_U - u.k_W;
+    const int64_t lim = ((int64_t)1 << (u.k_U - 1)) - 1;
+    if (d.kind == ISEG_UPD_CODES) {
+        const int8_t* g = (const int8_t*)d.g;
+        const int sh = *d.g_exp - u.lr_shift - d.master_exp;     // Delta W code = g 2^sh, rounded
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d.n;
+             i += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t m = clamp_k((int64_t)d.master[i] - upd_delta(g[i], sh, u.k_U, lim), u.k_U);
+            d.master[i] = (int32_t)m;
+            d.w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), u.k_W);
+        }
+        return;
+    }
+    if (blockIdx.x != 0) return;
+    const int64_t* g = (const int64_t*)d.g;
+    uint64_t m = 0;
+    for (int64_t c = threadIdx.x; c < d.n; c += blockDim.x) {
+        const uint64_t v = uabs64(g[c]);
+        m = v > m ? v : m;
+    }
+    m = block_max_u64(m);
+    const int r = m ? bitlen_u64(m) - (u.bits - 1) : 0;
+    const int32_t gexp = *d.g_exp + r;                            // Eq. 17 keeps the scale
+    if (threadIdx.x == 0 && d.g_q_exp) *d.g_q_exp = gexp;
+    const int sh = gexp - u.lr_shift - d.master_exp;
+    for (int64_t c = threadIdx.x; c < d.n; c += blockDim.x) {
+        const int64_t q = r > 0 ? rq_code(g[c], r, u.bits, philox_draw(u.seed, d.tensor_id, u.step, (uint64_t)c))
+                                : sq_code(g[c], r, u.bits);
+        if (d.g_q) d.g_q[c] = (int8_t)q;
+        const int64_t mm = clamp_k((int64_t)d.master[c] - upd_delta(q, sh, u.k_U, lim), u.k_U);
+        d.master[c] = (int32_t)mm;
+        d.w_q[c] = (int8_t)clamp_k(shr_rhu(mm, dq), u.k_W);
+    }
+}
+
+extern "C" int iseg_update_multi(const iseg_update_desc* descs, int32_t n_desc, int32_t bits, uint64_t seed,
+                                 uint32_t step, int32_t lr_shift, int32_t k_U, int32_t k_W, int32_t* dev_status,
+                                 hipStream_t stream)
+{
+    (void)dev_status;
+    if (n_desc < 0 || n_desc > 65535 || (n_desc > 0 && !descs)) return ISEG_ERR_ARG;
+    if (bits < 2 || bits > 8 || k_U < 9 || k_U > 31 || k_W < 2 || k_W > 8) return ISEG_ERR_ARG;
+    if (n_desc == 0) return ISEG_OK;
+    UpdCfg u;
+    u.seed = seed; u.step = step; u.bits = bits; u.lr_shift = lr_shift; u.k_U = k_U; u.k_W = k_W;
+    hipLaunchKernelGGL(k_update_multi, dim3(64, (unsigned)n_desc), dim3(256), 0, stream, descs, u);
+    return launch_ok();
+}
+
 __global__ __launch_bounds__(256) void k_weight_quant(const int32_t* __restrict__ master, int64_t n,
                                                       int32_t dq, int32_t k_W, int8_t* __restrict__ w_q)
 {

@@ -40,6 +40,15 @@ class ConvGeom(C.Structure):
                [(n, C.c_int32) for n in ("stride_h", "stride_w", "pad_h", "pad_w", "dil_h", "dil_w")]
 
 
+class UpdateDesc(C.Structure):
+    _fields_ = [("master", C.c_void_p), ("w_q", C.c_void_p), ("g", C.c_void_p), ("g_exp", C.c_void_p),
+                ("g_q", C.c_void_p), ("g_q_exp", C.c_void_p), ("n", C.c_int64), ("kind", C.c_int32),
+                ("master_exp", C.c_int32), ("tensor_id", C.c_uint32), ("reserved", C.c_int32)]
+
+
+ISEG_UPD_CODES, ISEG_UPD_RAW = 0, 1
+
+
 class BnCfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("k_mu", "k_sigma", "k_xhat", "k_gamma", "k_beta",
                                          "k_A", "k_E1", "k_E2", "eps_code", "relu")]
@@ -91,6 +100,7 @@ _SIGS = {
     "iseg_softmax_ce_ws": ([_I64, _I64, _I64, _I64, _I64, _I64], _SZ),
     "iseg_softmax_ce": ([_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _SZ,
                          _P, _P], C.c_int),
+    "iseg_update_multi": ([_P, _I32, _I32, _U64, _U32, _I32, _I32, _I32, _P, _P], C.c_int),
     "iseg_philox4x32_10": ([_P, _P, _P], None),
     "iseg_profile_arm": ([_I32, _P, _P], C.c_int),
     "iseg_version": ([], C.c_char_p),
@@ -198,6 +208,12 @@ def iseg_bn_param_update(dgamma, dgamma_exp, dbeta, dbeta_exp, bits, seed, tid_g
                                     _ptr(beta_q), _ptr(g_gamma), _ptr(g_beta), _ptr(g_gamma_exp),
                                     _ptr(g_beta_exp), _ptr(status), _stream())
     _check(rc, "iseg_bn_param_update")
+
+
+def iseg_update_multi(descs, n_desc, bits, seed, step, lr_shift, k_U, k_W, status=None):
+    rc = lib().iseg_update_multi(_ptr(descs), n_desc, bits, seed, step, lr_shift, k_U, k_W, _ptr(status),
+                                 _stream())
+    _check(rc, "iseg_update_multi")
 
 
 def iseg_weight_quant(master, k_U, k_W, w_q):
@@ -484,13 +500,16 @@ def conv_bwd_data(dy, dy_exp, w, w_exp, x_shape, stride=1, pad=0, dil=1, out_mod
 
 
 def conv_bwd_weight(dy, dy_exp, x, x_exp, w_shape, stride=1, pad=0, dil=1, g_mode=ISEG_G_KEEP,
-                    bits=8, seed=0, tensor_id=0, step=0, status=None):
+                    bits=8, seed=0, tensor_id=0, step=0, status=None, out=None):
     N, H, W, Cc = x.shape
     K, R, S, _ = w_shape
     g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
-    dw = torch.empty((K, R, S, Cc), dtype=torch.int64 if g_mode == ISEG_G_RAW else torch.int8,
-                     device=x.device)
-    e = _out_exp(x.device)
+    if out is None:
+        dw = torch.empty((K, R, S, Cc), dtype=torch.int64 if g_mode == ISEG_G_RAW else torch.int8,
+                         device=x.device)
+        e = _out_exp(x.device)
+    else:
+        dw, e = out
     ws = workspace(x.device).get(lib().iseg_conv_bwd_weight_ws(C.byref(g), g_mode))
     _maybe_arm(ISEG_KID_CONV_WGRAD, (N, H, W, Cc, K, R, g.stride_h, g.pad_h, g.dil_h))
     iseg_conv_bwd_weight(dy, dy_exp, x, x_exp, g, g_mode, bits, seed, tensor_id, step, dw, e, ws,
@@ -513,15 +532,18 @@ def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None, saved=None, status=None):
     return y, e, saved
 
 
-def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None):
+def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None, dgb_out=None):
     Cc = x.shape[-1]
     M = x.numel() // Cc
     cfg = cfg or bn_cfg()
     dx = torch.empty_like(x)
     e = _out_exp(x.device)
-    dg = torch.empty(Cc, dtype=torch.int64, device=x.device)
-    db = torch.empty(Cc, dtype=torch.int64, device=x.device)
-    dge, dbe = _out_exp(x.device), _out_exp(x.device)
+    if dgb_out is None:
+        dg = torch.empty(Cc, dtype=torch.int64, device=x.device)
+        db = torch.empty(Cc, dtype=torch.int64, device=x.device)
+        dge, dbe = _out_exp(x.device), _out_exp(x.device)
+    else:
+        dg, db, dge, dbe = dgb_out
     ws = workspace(x.device).get(lib().iseg_bn_bwd_ws(M, Cc))
     for kid in (ISEG_KID_BN_BWD_APPLY, ISEG_KID_BN_BWD_STATS):
         _maybe_arm(kid, (M, Cc))
@@ -658,3 +680,25 @@ def softmax_ce(logits, logit_exp, labels, bits=8, want_grad=False, status=None):
     ws = workspace(dev).get(lib().iseg_softmax_ce_ws(N, h, w, K, H, W))
     iseg_softmax_ce(logits, logit_exp, labels, N, h, w, K, H, W, bits, loss, grad, err, e, ws, status)
     return loss, grad, err, e
+
+
+def update_table(entries, device):
+    """Device array of iseg_update_desc for iseg_update_multi.  entries: dicts
+    with master, w_q, g, g_exp, kind, master_exp and, for ISEG_UPD_RAW,
+    tensor_id, g_q, g_q_exp (torch tensors; their storage must stay alive)."""
+    n = len(entries)
+    host = (UpdateDesc * max(n, 1))()
+    for i, e in enumerate(entries):
+        d = host[i]
+        d.master = e["master"].data_ptr()
+        d.w_q = e["w_q"].data_ptr()
+        d.g = e["g"].data_ptr()
+        d.g_exp = e["g_exp"].data_ptr()
+        d.g_q = e["g_q"].data_ptr() if e.get("g_q") is not None else None
+        d.g_q_exp = e["g_q_exp"].data_ptr() if e.get("g_q_exp") is not None else None
+        d.n = e["master"].numel()
+        d.kind = e["kind"]
+        d.master_exp = e["master_exp"]
+        d.tensor_id = e.get("tensor_id", 0)
+    raw = torch.frombuffer(bytearray(bytes(host)), dtype=torch.uint8)
+    return raw.to(device), n

@@ -60,9 +60,37 @@ class IntNet:
             L = dict(l=ci, w_m=master, g_m=g_m, b_m=b_m,
                      w_q=iseg.weight_quant(master, K_U, K_W),
                      g_q=iseg.weight_quant(g_m, K_U, K_W),
-                     b_q=iseg.weight_quant(b_m, K_U, K_W))
+                     b_q=iseg.weight_quant(b_m, K_U, K_W),
+                     # gradient buffers, written every step (fixed addresses for the update table)
+                     G=torch.empty(master.shape, dtype=torch.int8, device=self.dev),
+                     G_exp=iseg._out_exp(self.dev))
+            if nd["bn"]:
+                L.update(dg=torch.empty(cout, dtype=torch.int64, device=self.dev),
+                         db=torch.empty(cout, dtype=torch.int64, device=self.dev),
+                         dg_exp=iseg._out_exp(self.dev), db_exp=iseg._out_exp(self.dev),
+                         Gg=torch.empty(cout, dtype=torch.int8, device=self.dev),
+                         Gb=torch.empty(cout, dtype=torch.int8, device=self.dev),
+                         Gg_exp=iseg._out_exp(self.dev), Gb_exp=iseg._out_exp(self.dev))
             self.convs[nd["name"]] = L
+        self._build_update_table()
         self.loss = None
+
+    def _build_update_table(self):
+        """Every parameter tensor of the network for one iseg_update_multi launch."""
+        ents = []
+        for nd in self.wl["nodes"]:
+            if nd["kind"] != "conv":
+                continue
+            L = self.convs[nd["name"]]
+            ents.append(dict(master=L["w_m"], w_q=L["w_q"], g=L["G"], g_exp=L["G_exp"],
+                             kind=iseg.ISEG_UPD_CODES, master_exp=W_MASTER_EXP))
+            if nd["bn"]:
+                for m, q, g, ge, gq, gqe, t in (("g_m", "g_q", "dg", "dg_exp", "Gg", "Gg_exp", 1),
+                                                ("b_m", "b_q", "db", "db_exp", "Gb", "Gb_exp", 2)):
+                    ents.append(dict(master=L[m], w_q=L[q], g=L[g], g_exp=L[ge], g_q=L[gq],
+                                     g_q_exp=L[gqe], kind=iseg.ISEG_UPD_RAW,
+                                     master_exp=GB_MASTER_EXP, tensor_id=16 * L["l"] + t))
+        self.upd_table, self.upd_n = iseg.update_table(ents, self.dev)
 
     # -------------------------------------------------------------------
     def forward(self):
@@ -138,13 +166,16 @@ class IntNet:
                 L = self.convs[name]
                 if nd["bn"]:
                     dz, dze, dg, db, dge, dbe = iseg.bn_bwd(e, ee, r["z"], L["g_q"], r["saved"],
-                                                            self._cfgs[int(nd["relu"])])
+                                                            self._cfgs[int(nd["relu"])],
+                                                            dgb_out=(L["dg"], L["db"], L["dg_exp"],
+                                                                     L["db_exp"]))
                     r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
                 else:
                     dz, dze = e, ee
                 G, Ge = iseg.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape,
                                              nd["stride"], nd["pad"], nd["dil"], iseg.ISEG_G_KEEP, 8,
-                                             self.seed, 16 * L["l"], self.step_no)
+                                             self.seed, 16 * L["l"], self.step_no,
+                                             out=(L["G"], L["G_exp"]))
                 r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
                 grads.append((nd, r))
                 if need_in:
@@ -185,21 +216,13 @@ class IntNet:
         return grads
 
     def update(self, grads):
+        """Q_G of gamma / beta, Eq. 19 and Q_W for every parameter: one launch."""
+        iseg.iseg_update_multi(self.upd_table, self.upd_n, 8, self.seed, self.step_no, self.lr_shift,
+                               K_U, K_W)
         for nd, r in grads:
-            L = self.convs[nd["name"]]
-            l = L["l"]
-            iseg.weight_update(L["w_m"], r["G"], r["G_exp"], self.lr_shift, W_MASTER_EXP, K_U, K_W,
-                               L["w_q"])
             if nd["bn"]:
-                C = nd["cout"]
-                r["Gg"] = torch.empty(C, dtype=torch.int8, device=self.dev)
-                r["Gb"] = torch.empty(C, dtype=torch.int8, device=self.dev)
-                r["Gg_exp"], r["Gb_exp"] = iseg._out_exp(self.dev), iseg._out_exp(self.dev)
-                iseg.iseg_bn_param_update(r["dgamma"], r["dgamma_exp"], r["dbeta"], r["dbeta_exp"], 8,
-                                          self.seed, 16 * l + 1, 16 * l + 2, self.step_no,
-                                          self.lr_shift, GB_MASTER_EXP, K_U, K_W, L["g_m"], L["b_m"],
-                                          L["g_q"], L["b_q"], r["Gg"], r["Gb"], r["Gg_exp"],
-                                          r["Gb_exp"])
+                L = self.convs[nd["name"]]
+                r.update(Gg=L["Gg"], Gb=L["Gb"], Gg_exp=L["Gg_exp"], Gb_exp=L["Gb_exp"])
 
     def step(self):
         rec = self.forward()

@@ -315,6 +315,54 @@ def test_maxpool_2x2_window_path(orc, dev, shape, small):
     assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
 
 
+@pytest.mark.parametrize("shape,k,st,pad", [((2, 64, 64, 64), 3, 2, 1), ((1, 29, 31, 16), 3, 2, 1),
+                                            ((2, 17, 12, 32), 3, 1, 1), ((1, 23, 19, 48), 5, 3, 2),
+                                            ((1, 9, 9, 16), 2, 1, 0)], ids=str)
+def test_maxpool_overlapping_vector_path(orc, dev, shape, k, st, pad):
+    """Overlapping windows with 16-channel vectors (per-window argmax taps and
+    two gathers): the ResNet stem's 3x3/2 pad 1, stride 1, a 5x5/3 pad 2 and a
+    2x2/1 case, with ties inside windows."""
+    from paper_2011_14504_amd import iseg
+    x = synth.int_codes(75, shape)
+    x[0, :5, :5, :] = 7                       # ties across overlapping windows
+    y, ye = iseg.maxpool_fwd(T(x, dev), E(-6, dev), k, st, pad)
+    assert np.array_equal(H(y), orc.maxpool_fwd(x, k, st, pad))
+    dy = synth.int_codes(76, H(y).shape)
+    dx, dxe = iseg.maxpool_bwd(T(dy, dev), E(-19, dev), T(x, dev), k, st, pad)
+    rc, rce = orc.maxpool_bwd(dy, -19, x, k, st, pad)
+    assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
+
+
+def test_update_multi_matches_oracle(orc, dev):
+    """One launch updating conv weights (quantized G) and L1BN gamma / beta (raw
+    sums, Q_G first) equals the oracle's per-tensor Eq. 19 / Eq. 8."""
+    import torch
+    from paper_2011_14504_amd import iseg
+    r = synth.rng(90)
+    ents, ref = [], []
+    for i, n in enumerate((64 * 9 * 64, 1000, 3)):
+        m = r.integers(-(2 ** 23) + 1, 2 ** 23, size=n).astype(np.int32)
+        g = r.integers(-127, 128, size=n).astype(np.int8)
+        mt, gt = T(m, dev), T(g, dev)
+        ents.append(dict(master=mt, w_q=torch.empty(n, dtype=torch.int8, device=dev), g=gt,
+                         g_exp=E(-25 - i, dev), kind=iseg.ISEG_UPD_CODES, master_exp=-23))
+        ref.append(orc.weight_update(m, g, -25 - i, 10, -23, 24, 8))
+    for i, C in enumerate((64, 2048)):
+        m = r.integers(-(2 ** 23) + 1, 2 ** 23, size=C).astype(np.int32)
+        d = r.integers(-(2 ** 40), 2 ** 40, size=C).astype(np.int64)
+        ents.append(dict(master=T(m, dev), w_q=torch.empty(C, dtype=torch.int8, device=dev), g=T(d, dev),
+                         g_exp=E(-30, dev), kind=iseg.ISEG_UPD_RAW, master_exp=-22, tensor_id=17 + i,
+                         g_q=torch.empty(C, dtype=torch.int8, device=dev), g_q_exp=E(0, dev)))
+        gq, gqe = orc.requant(d, -30, 8, True, True, 55, 17 + i, 4)
+        ref.append(orc.weight_update(m, gq, gqe, 10, -22, 24, 8) + (gq, gqe))
+    table, n = iseg.update_table(ents, dev)
+    iseg.iseg_update_multi(table, n, 8, 55, 4, 10, 24, 8)
+    for e, rr in zip(ents, ref):
+        assert np.array_equal(H(e["master"]), rr[0]) and np.array_equal(H(e["w_q"]), rr[1])
+        if e["kind"] == iseg.ISEG_UPD_RAW:
+            assert np.array_equal(H(e["g_q"]).astype(np.int64), rr[2]) and ev(e["g_q_exp"]) == rr[3]
+
+
 @pytest.mark.parametrize("C,d_exp", [(64, -30), (128, -12), (2048, -40)])
 def test_bn_param_update(orc, dev, C, d_exp):
     # Q_G (Eq. 17, stochastic) then Q_U (Eq. 19) of gamma/beta in one launch
