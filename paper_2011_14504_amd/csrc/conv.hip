@@ -19,7 +19,11 @@
 
 // a convolution is timed as a whole entry-point call (ProfScope), not per kernel
 #undef ISEG_TIMED_LAUNCH
-#define ISEG_TIMED_LAUNCH(kid, stream, ...) hipLaunchKernelGGL(__VA_ARGS__)
+#define ISEG_TIMED_LAUNCH(kid, stream, ...) \
+    do {                                    \
+        (void)(kid);                        \
+        hipLaunchKernelGGL(__VA_ARGS__);    \
+    } while (0)
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
@@ -1799,9 +1803,10 @@ int halo_q8(const HaloPlan& p, HaloArgs h, int kid, const int32_t* exp_a, const 
         return launch_halo(p, h, EPI_Q8, kid, s);
     }
     if ((rc = launch_halo(p, h, EPI_STAGE16, kid, s))) return rc;
-    if ((rc = launch_reduce_max(pmax, h.npmax, maxp, s))) return rc;
+    (void)maxp;
     StageMap sm{0, 64, h.Ho, h.Wo, kHaloTH, p.TW, p.tiles_y, p.tiles_x};
-    return launch_requant_staged16(h.out16, h.tshift, rows, h.Nout, sm, exp_a, exp_b, 8, out, out_exp, maxp, s);
+    return launch_requant_staged16(h.out16, h.tshift, rows, h.Nout, sm, exp_a, exp_b, 8, out, out_exp, nullptr, s,
+                                   pmax, h.npmax);
 }
 
 // the direct-to-LDS kernel covers Ci % 64 == 0, Nout % 64 == 0, 16-byte
@@ -1944,6 +1949,7 @@ struct WgradArgs {
     const int8_t* dy;        // [NPQ][K]
     const int8_t* x;         // [N,H,W,C]
     unsigned long long* acc; // int64 [K][RSC], accumulated atomically
+    int32_t* part;           // or, when set: int32 [split][K][RSC], stored (k_conv_wgrad_tr)
     int64_t NPQ, pix_per_split;
     int32_t K, C, R, S, H, W, P, Q, RSC;
     int32_t sh, sw, ph, pw, dh, dw;
@@ -2199,7 +2205,10 @@ __global__ __launch_bounds__(256) void k_conv_wgrad_tap(WgradArgs a)
             for (int e = 0; e < 4; e++) {
                 int k = k0 + wm * WM + i * 16 + (lane >> 4) * 4 + e;
                 int32_t v = acc[i][j][e];
-                if (k < a.K && v != 0)
+                if (k >= a.K) continue;
+                if (a.part)
+                    a.part[((int64_t)blockIdx.z * a.K + k) * a.RSC + col] = v;
+                else if (v != 0)
                     atomicAdd(&a.acc[(int64_t)k * a.RSC + col], (unsigned long long)(int64_t)v);
             }
         }
@@ -2348,7 +2357,10 @@ __global__ __launch_bounds__(256) void k_conv_wgrad_tr(WgradArgs a)
             for (int e = 0; e < 4; e++) {
                 int k = k0 + wm * WM + i * 16 + (lane >> 4) * 4 + e;
                 int32_t v = acc[i][j][e];
-                if (k < a.K && v != 0)
+                if (k >= a.K) continue;
+                if (a.part)
+                    a.part[((int64_t)blockIdx.z * a.K + k) * a.RSC + col] = v;
+                else if (v != 0)
                     atomicAdd(&a.acc[(int64_t)k * a.RSC + col], (unsigned long long)(int64_t)v);
             }
         }
@@ -2488,7 +2500,7 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
 constexpr int kRedWaves = 8;
 __global__ __launch_bounds__(64 * kRedWaves) void k_wgrad_reduce(const int32_t* __restrict__ part, int64_t n,
                                                                  int splits, long long* __restrict__ out,
-                                                                 unsigned long long* maxp)
+                                                                 uint64_t* pmax)
 {
     __shared__ long long red[kRedWaves][256];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -2522,7 +2534,72 @@ __global__ __launch_bounds__(64 * kRedWaves) void k_wgrad_reduce(const int32_t* 
             mx = t < 0 ? (uint64_t)(-t) : (uint64_t)t;
         }
     }
-    if (maxp) block_atomic_max_u64(mx, maxp);
+    if (pmax) block_store_max_u64(mx, pmax);
+}
+
+// Two-level variant for weight tensors too small to fill the chip with one
+// block per 256 weights: blockIdx.y takes a chunk of the splits and writes an
+// int64 partial; k_wgrad_reduce_fin adds the chunks in order.
+__global__ __launch_bounds__(256) void k_wgrad_reduce_part(const int32_t* __restrict__ part, int64_t n,
+                                                           int splits, int chunk, long long* __restrict__ out2)
+{
+    const int64_t e0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (e0 >= n) return;                  // n % 4 == 0
+    const int k0 = blockIdx.y * chunk;
+    const int k1 = k0 + chunk < splits ? k0 + chunk : splits;
+    long long s[4] = {0, 0, 0, 0};
+    int k = k0;
+    for (; k + 3 < k1; k += 4) {
+        int4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; u++) v[u] = *(const int4*)(part + (int64_t)(k + u) * n + e0);
+#pragma unroll
+        for (int u = 0; u < 4; u++) { s[0] += v[u].x; s[1] += v[u].y; s[2] += v[u].z; s[3] += v[u].w; }
+    }
+    for (; k < k1; k++) {
+        const int4 v = *(const int4*)(part + (int64_t)k * n + e0);
+        s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+    }
+    long long* o = out2 + (int64_t)blockIdx.y * n + e0;
+#pragma unroll
+    for (int u = 0; u < 4; u++) o[u] = s[u];
+}
+
+// few splits: one lane per 4 weights over all splits, sum and max in one pass
+__global__ __launch_bounds__(256) void k_wgrad_reduce_flat(const int32_t* __restrict__ part, int64_t n, int splits,
+                                                           long long* __restrict__ out, uint64_t* pmax)
+{
+    const int64_t e0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    uint64_t mx = 0;
+    if (e0 < n) {
+        long long s[4] = {0, 0, 0, 0};
+        for (int k = 0; k < splits; k++) {
+            const int4 v = *(const int4*)(part + (int64_t)k * n + e0);
+            s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+        }
+        *(longlong2*)(out + e0) = make_longlong2(s[0], s[1]);
+        *(longlong2*)(out + e0 + 2) = make_longlong2(s[2], s[3]);
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const uint64_t a = s[u] < 0 ? (uint64_t)(-s[u]) : (uint64_t)s[u];
+            mx = a > mx ? a : mx;
+        }
+    }
+    if (pmax) block_store_max_u64(mx, pmax);
+}
+
+__global__ __launch_bounds__(256) void k_wgrad_reduce_fin(const long long* __restrict__ out2, int64_t n, int nchunks,
+                                                          long long* __restrict__ out, uint64_t* pmax)
+{
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    uint64_t mx = 0;
+    if (e < n) {
+        long long t = 0;
+        for (int c = 0; c < nchunks; c++) t += out2[(int64_t)c * n + e];
+        out[e] = t;
+        mx = t < 0 ? (uint64_t)(-t) : (uint64_t)t;
+    }
+    if (pmax) block_store_max_u64(mx, pmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -2695,17 +2772,67 @@ int64_t wgrad_taps_splits(int64_t NPQ, int64_t K, int64_t C, int64_t* pps_out)
     return ceil_div64(NPQ, pps);
 }
 
+// chunks of the splits reduced by separate blocks: enough blocks for the chip
+// when the weight tensor alone gives too few, each chunk still >= 8 splits
+int wgrad_reduce_chunks(int64_t n, int64_t splits)
+{
+    const int64_t bx = ceil_div64(n, 1024);
+    if (bx >= 512 || splits < 16) return 1;
+    int64_t c = ceil_div64(1024, bx);
+    const int64_t cmax = splits / 8;
+    c = c < cmax ? c : cmax;
+    return (int)(c < 1 ? 1 : c);
+}
+
 size_t wgrad_taps_part_bytes(int64_t NPQ, int64_t K, int64_t C, int64_t RS)
 {
     if (!wgrad_taps_shape(NPQ, K, C, RS)) return 0;
     int64_t pps;
     int64_t splits = wgrad_taps_splits(NPQ, K, C, &pps);
-    return align256((size_t)(splits * K * RS * C) * 4);
+    const int64_t n = K * RS * C;
+    const int nch = wgrad_reduce_chunks(n, splits);
+    return align256((size_t)(splits * n) * 4) + (nch > 1 ? align256((size_t)(nch * n) * 8) : 0);
 }
 
 // all-taps launch: partials into `part`, then their int64 sum into a.acc (every
 // element written, no fill needed) and its max |.| into maxp when given
-int launch_wgrad_taps(WgradArgs a, int32_t* part, unsigned long long* maxp, hipStream_t s)
+// int64 sums of `splits` int32 partials [splits][n] (n % 4 == 0) into out and,
+// when pmax is set, per-block max |sum| partials (their count into *npmax);
+// the two-level variant keeps its chunk sums right after the partials
+int launch_wgrad_reduce(const int32_t* part, int64_t n, int64_t splits, long long* out, uint64_t* pmax,
+                        int64_t* npmax, hipStream_t s)
+{
+    const int nch = wgrad_reduce_chunks(n, splits);
+    if (nch > 1) {
+        long long* out2 = (long long*)((char*)part + align256((size_t)(splits * n) * 4));
+        const int chunk = (int)ceil_div64(splits, nch);
+        hipLaunchKernelGGL(k_wgrad_reduce_part, dim3((unsigned)ceil_div64(n, 1024), (unsigned)nch), dim3(256), 0, s,
+                           part, n, (int)splits, chunk, out2);
+        int rc = launch_ok();
+        if (rc) return rc;
+        if (npmax) *npmax = ceil_div64(n, 256);
+        hipLaunchKernelGGL(k_wgrad_reduce_fin, dim3((unsigned)ceil_div64(n, 256)), dim3(256), 0, s,
+                           (const long long*)out2, n, nch, out, pmax);
+        return launch_ok();
+    }
+    if (splits <= 8 && (((uintptr_t)out) & 15) == 0) {
+        if (npmax) *npmax = ceil_div64(n, 1024);
+        hipLaunchKernelGGL(k_wgrad_reduce_flat, dim3((unsigned)ceil_div64(n, 1024)), dim3(256), 0, s, part, n,
+                           (int)splits, out, pmax);
+        return launch_ok();
+    }
+    if (npmax) *npmax = ceil_div64(n, 256);
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)ceil_div64(n, 256)), dim3(64 * kRedWaves), 0, s, part, n,
+                       (int)splits, out, pmax);
+    return launch_ok();
+}
+
+// max-partial count of launch_wgrad_reduce for a shape (workspace sizing)
+int64_t wgrad_reduce_npmax(int64_t n) { return ceil_div64(n, 256); }
+
+// all-taps launch: partials into `part`, then their int64 sum into a.acc (every
+// element written, no fill needed) and its max |.| partials into pmax when given
+int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax, hipStream_t s)
 {
     const int RS = a.R * a.S;
     int64_t splits = wgrad_taps_splits(a.NPQ, a.K, a.C, &a.pix_per_split);
@@ -2718,10 +2845,59 @@ int launch_wgrad_taps(WgradArgs a, int32_t* part, unsigned long long* maxp, hipS
     ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, k_conv_wgrad_taps<9>, grid, dim3(64 * 9), lds, s, a, part);
     int rc = launch_ok();
     if (rc) return rc;
-    const int64_t n = (int64_t)a.K * a.RSC;
-    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)ceil_div64(n, 256)), dim3(64 * kRedWaves), 0, s,
-                       (const int32_t*)part, n, (int)splits, (long long*)a.acc, maxp);
-    return launch_ok();
+    return launch_wgrad_reduce(part, (int64_t)a.K * a.RSC, splits, (long long*)a.acc, pmax, npmax, s);
+}
+
+// the transposed-operand kernel over split pixel ranges: int32 partials per
+// split stored into `part`, summed like the all-taps kernel's (C % 64 == 0,
+// K % 64 == 0, 16-byte aligned operands)
+bool wgrad_tr_ok(const WgradArgs& a)
+{
+    return a.NPQ > 0 && a.C % 64 == 0 && a.K % 64 == 0 && (((uintptr_t)a.x | (uintptr_t)a.dy) & 15) == 0;
+}
+
+int64_t wgrad_tr_splits(const WgradArgs& a, int64_t* pps)
+{
+    const int BMt = a.K % 128 == 0 ? 128 : 64;
+    const int RS = a.R * a.S;
+    const int TAPS = RS > 1 ? 2 : 1;
+    const int ntg = (RS + TAPS - 1) / TAPS;
+    const int64_t tiles = (int64_t)ntg * (a.C / 64) * (a.K / BMt);
+    return wgrad_splits(a.NPQ, tiles, pps);
+}
+
+size_t wgrad_tr_part_bytes(int64_t NPQ, int64_t K, int64_t C, int64_t RS)
+{
+    if (NPQ <= 0 || C % 64 || K % 64) return 0;
+    WgradArgs a{};
+    a.NPQ = NPQ; a.K = (int32_t)K; a.C = (int32_t)C; a.R = (int32_t)RS; a.S = 1;
+    int64_t pps;
+    const int64_t splits = wgrad_tr_splits(a, &pps);
+    const int64_t n = K * RS * C;
+    const int nch = wgrad_reduce_chunks(n, splits);
+    return align256((size_t)(splits * n) * 4) + (nch > 1 ? align256((size_t)(nch * n) * 8) : 0);
+}
+
+int launch_wgrad_tr_split(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax, hipStream_t s)
+{
+    const int BMt = a.K % 128 == 0 ? 128 : 64;
+    const int RS = a.R * a.S;
+    const int TAPS = RS > 1 ? 2 : 1;
+    const int ntg = (RS + TAPS - 1) / TAPS;
+    const int64_t splits = wgrad_tr_splits(a, &a.pix_per_split);
+    a.part = part;
+    dim3 grid((unsigned)(ntg * (a.C / 64)), (unsigned)(a.K / BMt), (unsigned)splits);
+    if (BMt == 128 && TAPS == 2)
+        hipLaunchKernelGGL((k_conv_wgrad_tr<128, 2>), grid, dim3(256), 0, s, a);
+    else if (BMt == 128)
+        hipLaunchKernelGGL((k_conv_wgrad_tr<128, 1>), grid, dim3(256), 0, s, a);
+    else if (TAPS == 2)
+        hipLaunchKernelGGL((k_conv_wgrad_tr<64, 2>), grid, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_conv_wgrad_tr<64, 1>), grid, dim3(256), 0, s, a);
+    int rc = launch_ok();
+    if (rc) return rc;
+    return launch_wgrad_reduce(part, (int64_t)a.K * a.RSC, splits, (long long*)a.acc, pmax, npmax, s);
 }
 
 int launch_wgrad(WgradArgs a, hipStream_t s)
@@ -2968,14 +3144,13 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
         return launch_ok();
     }
-    if ((rc = launch_reduce_max(pmax, nblk, maxp, stream))) return rc;
     if (staged) {
         StageMap sm{128, igemm_dma_bn(a), 0, 0, 0, 0, 0, 0};
         return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, x_exp, w_exp, 8, (int8_t*)y, y_exp,
-                                       maxp, stream);
+                                       nullptr, stream, pmax, nblk);
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, x_exp, w_exp, 0, 8, 0, 1,
-                                0, 0, 0, ISEG_I8, y, y_exp, maxp, stream);
+                                0, 0, 0, ISEG_I8, y, y_exp, nullptr, stream, pmax, nblk);
 }
 
 extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mode)
@@ -3109,14 +3284,21 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
         return launch_ok();
     }
-    if ((rc = launch_reduce_max(pmax, nblk, maxp, stream))) return rc;
     if (staged) {
         StageMap sm{128, igemm_dma_bn(a), 0, 0, 0, 0, 0, 0};
         return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, dy_exp, w_exp, 8, (int8_t*)dx,
-                                       dx_exp, maxp, stream);
+                                       dx_exp, nullptr, stream, pmax, nblk);
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, dy_exp, w_exp, 0, 8, 0, 1,
-                                0, 0, 0, ISEG_I8, dx, dx_exp, maxp, stream);
+                                0, 0, 0, ISEG_I8, dx, dx_exp, nullptr, stream, pmax, nblk);
+}
+
+// workspace: [max word][int64 sums][max partials][padded operands][int32
+// split partials of the taps / split kernels][stem partials]
+static size_t wgrad_part_region(int64_t NPQ, int64_t K, int64_t Cp, int64_t RS)
+{
+    const size_t t = wgrad_taps_part_bytes(NPQ, K, Cp, RS), r = wgrad_tr_part_bytes(NPQ, K, Cp, RS);
+    return t > r ? t : r;
 }
 
 extern "C" size_t iseg_conv_bwd_weight_ws(const iseg_conv_geom* g, int32_t g_mode)
@@ -3124,13 +3306,18 @@ extern "C" size_t iseg_conv_bwd_weight_ws(const iseg_conv_geom* g, int32_t g_mod
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
     (void)g_mode;
-    size_t s = 256 + align256((size_t)(g->K * g->R * g->S * g->C) * 8);
-    int64_t Cp = padded_c(g->C);
+    const int64_t Cp = padded_c(g->C);
+    const int64_t nwp = g->K * g->R * g->S * Cp;
+    size_t s = 256 + align256((size_t)(g->K * g->R * g->S * g->C) * 8) + align256((size_t)wgrad_reduce_npmax(nwp) * 8);
     if (Cp != g->C)
-        s += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp) * 8);
-    s += wgrad_taps_part_bytes(g->N * P * Q, g->K, Cp, g->R * g->S);
-    if (stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K))
-        s += align256((size_t)(g->N * ceil_div64(P, 16) * ceil_div64(Q, 32)) * g->K * g->R * g->S * g->C * 4);
+        s += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)nwp * 8);
+    s += wgrad_part_region(g->N * P * Q, g->K, Cp, g->R * g->S);
+    if (stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K)) {
+        const int64_t nbx = g->N * ceil_div64(P, 16) * ceil_div64(Q, 32), nw = g->K * g->R * g->S * g->C;
+        s += align256((size_t)(nbx * nw) * 4);
+        const int nch = wgrad_reduce_chunks(nw, nbx);
+        if (nch > 1) s += align256((size_t)(nch * nw) * 8);
+    }
     return s;
 }
 
@@ -3148,23 +3335,35 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     if (!dy_exp || !x_exp || !dw_exp || !dw || (g->N > 0 && (!dy || !x))) return ISEG_ERR_ARG;
     if (!ws || ws_bytes < iseg_conv_bwd_weight_ws(g, g_mode)) return ISEG_ERR_WORKSPACE;
     unsigned long long* maxp = (unsigned long long*)ws;
-    int64_t nw = g->K * g->R * g->S * g->C;
-    char* wp = (char*)ws + 256;
-    unsigned long long* acc = g_mode == ISEG_G_RAW ? (unsigned long long*)dw : (unsigned long long*)wp;
-    wp += align256((size_t)nw * 8);
-    // small C: sums over zero-padded channels, then the real channels copied out
+    const int64_t nw = g->K * g->R * g->S * g->C;
     const int64_t Cp = padded_c(g->C);
-    const int8_t* xs = x;
-    unsigned long long* accp = acc;
-    int rc = launch_fill_u32(maxp, 2, 0, stream);
-    if (rc) return rc;
+    const int64_t nwp = g->K * g->R * g->S * Cp;
+    const int64_t NPQ = g->N * P * Q;
+    const bool raw = g_mode == ISEG_G_RAW;
+    const int keep = g_mode == ISEG_G_KEEP;
+    char* wp = (char*)ws + 256;
+    unsigned long long* acc = raw ? (unsigned long long*)dw : (unsigned long long*)wp;
+    wp += align256((size_t)nw * 8);
+    uint64_t* pmax = (uint64_t*)wp;
+    wp += align256((size_t)wgrad_reduce_npmax(nwp) * 8);
+    char* pad_region = wp;
+    if (Cp != g->C) wp += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)nwp * 8);
+    int32_t* part = (int32_t*)wp;
+    wp += wgrad_part_region(NPQ, g->K, Cp, g->R * g->S);
+    int rc;
+    int64_t npmax = 0;
+    // the int64 sums are done: their exponent (raw) or Q_G from the max partials
+    auto finish = [&]() -> int {
+        if (raw) {
+            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dw_exp, dy_exp, x_exp);
+            return launch_ok();
+        }
+        return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr, 0, bits, 1,
+                                    keep, seed, tensor_id, step, ISEG_I8, dw, dw_exp, nullptr, stream, pmax, npmax);
+    };
     const int stem = stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K);
     if (stem && g->N > 0 && ((uintptr_t)dy & 15) == 0) {
-        // few-channel stem: MFMA over pixels, block partials, int64 sum + max
-        if (Cp != g->C) {                                   // skip the padded-operand regions
-            wp += align256((size_t)(g->N * g->H * g->W * Cp)) + align256((size_t)(g->K * g->R * g->S * Cp) * 8);
-        }
-        wp += wgrad_taps_part_bytes(g->N * P * Q, g->K, Cp, g->R * g->S);
+        // few-channel stem: MFMA over pixels, block partials, int64 sum + max partials
         int32_t* spart = (int32_t*)wp;
         HaloArgs h{};
         h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)g->C;
@@ -3179,61 +3378,46 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
             ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, stream, (k_wgrad_stem<3, 7, 7, 2>), grid, dim3(256), 0, stream, dy,
                               x, spart, h);
         if ((rc = launch_ok())) return rc;
-        const bool want_max = g_mode != ISEG_G_RAW;
-        hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)ceil_div64(nw, 256)), dim3(64 * kRedWaves), 0, stream,
-                           (const int32_t*)spart, nw, (int)nbx, (long long*)acc, want_max ? maxp : nullptr);
-        if ((rc = launch_ok())) return rc;
-        if (!want_max) {
-            hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dw_exp, dy_exp, x_exp);
-            return launch_ok();
-        }
-        const int keep = g_mode == ISEG_G_KEEP;
-        return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr, 0, bits, 1,
-                                    keep, seed, tensor_id, step, ISEG_I8, dw, dw_exp, maxp, stream);
+        if ((rc = launch_wgrad_reduce(spart, nw, nbx, (long long*)acc, raw ? nullptr : pmax, &npmax, stream)))
+            return rc;
+        return finish();
     }
-    if (Cp != g->C) {
-        int8_t* xp = (int8_t*)wp;
-        wp += align256((size_t)(g->N * g->H * g->W * Cp));
-        accp = (unsigned long long*)wp;
-        if ((rc = launch_pad(x, xp, g->N * g->H * g->W, g->C, Cp, stream))) return rc;
-        xs = xp;
-    }
-    const int64_t nwp = g->K * g->R * g->S * Cp;
-    const int64_t NPQ = g->N * P * Q;
-    const bool taps = wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) &&
-                      (((uintptr_t)xs | (uintptr_t)dy) & 15) == 0;
-    int32_t* part = nullptr;
-    if (wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S)) {
-        part = (int32_t*)wp;
-        wp += wgrad_taps_part_bytes(NPQ, g->K, Cp, g->R * g->S);
-    }
-    if (!taps && (rc = launch_fill_u32(accp, nwp * 2, 0, stream))) return rc;
-    WgradArgs a;
-    a.dy = dy; a.x = xs; a.acc = accp;
-    a.NPQ = g->N * P * Q; a.pix_per_split = 0;
+    WgradArgs a{};
+    a.dy = dy; a.x = x; a.acc = acc; a.part = nullptr;
+    a.NPQ = NPQ; a.pix_per_split = 0;
     a.K = (int32_t)g->K; a.C = (int32_t)Cp; a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.H = (int32_t)g->H; a.W = (int32_t)g->W; a.P = (int32_t)P; a.Q = (int32_t)Q;
     a.RSC = (int32_t)(g->R * g->S * Cp);
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
-    // with no channel padding the reduction also takes the max for the quantizer
-    const bool fused_max = taps && Cp == g->C && g_mode != ISEG_G_RAW;
-    if (taps) rc = launch_wgrad_taps(a, part, fused_max ? maxp : nullptr, stream);
-    else rc = launch_wgrad(a, stream);
-    if (rc) return rc;
+    if (Cp == g->C && wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) && (((uintptr_t)x | (uintptr_t)dy) & 15) == 0) {
+        if ((rc = launch_wgrad_taps(a, part, raw ? nullptr : pmax, &npmax, stream))) return rc;
+        return finish();
+    }
+    if (Cp == g->C && wgrad_tr_ok(a)) {
+        if ((rc = launch_wgrad_tr_split(a, part, raw ? nullptr : pmax, &npmax, stream))) return rc;
+        return finish();
+    }
+    // other shapes: atomic int64 accumulation (zero-filled), then the max pass
+    unsigned long long* accp = acc;
+    if (Cp != g->C) {
+        int8_t* xp = (int8_t*)pad_region;
+        accp = (unsigned long long*)(pad_region + align256((size_t)(g->N * g->H * g->W * Cp)));
+        if ((rc = launch_pad(x, xp, g->N * g->H * g->W, g->C, Cp, stream))) return rc;
+        a.x = xp;
+        a.acc = accp;
+    }
+    if ((rc = launch_fill_u32(accp, nwp * 2, 0, stream))) return rc;
+    if ((rc = launch_wgrad(a, stream))) return rc;
     if (Cp != g->C) {
         hipLaunchKernelGGL(k_unpad_i64, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream,
                            (const long long*)accp, (long long*)acc, g->K * g->R * g->S,
                            (int32_t)g->C, (int32_t)Cp);
         if ((rc = launch_ok())) return rc;
     }
-    if (g_mode == ISEG_G_RAW) {
-        hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dw_exp, dy_exp, x_exp);
-        return launch_ok();
-    }
-    if (!fused_max && (rc = launch_absmax(acc, ISEG_I64, nw, maxp, dev_status, stream))) return rc;
-    int keep = g_mode == ISEG_G_KEEP;
-    return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr,
-                                0, bits, 1, keep, seed, tensor_id, step, ISEG_I8, dw, dw_exp,
-                                maxp, stream);
+    if (raw) return finish();
+    if ((rc = launch_fill_u32(maxp, 2, 0, stream))) return rc;
+    if ((rc = launch_absmax(acc, ISEG_I64, nw, maxp, dev_status, stream))) return rc;
+    return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr, 0, bits, 1, keep,
+                                seed, tensor_id, step, ISEG_I8, dw, dw_exp, maxp, stream);
 }

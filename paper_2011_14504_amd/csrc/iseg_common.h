@@ -250,15 +250,19 @@ struct StageMap {
     int32_t Ho, Wo, th, tw, tiles_y, tiles_x;
 };
 // requant of int16-staged conv sums (per-tile shifts) to int8 SQ codes
+// the tensor max comes from *maxp, or (maxp == NULL) from nparts per-block
+// partials that every block of the requant kernel reduces itself
 int launch_requant_staged16(const int16_t* in, const uint8_t* tshift, int64_t rows, int32_t cols,
                             const StageMap& sm, const int32_t* exp_a, const int32_t* exp_b, int bits,
-                            int8_t* out, int32_t* out_exp, const unsigned long long* maxp, hipStream_t s);
+                            int8_t* out, int32_t* out_exp, const unsigned long long* maxp, hipStream_t s,
+                            const uint64_t* part = nullptr, int64_t nparts = 0);
 int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t* exp_a,
                          const int32_t* exp_b, int32_t exp_add, int bits, int stochastic,
                          int keep_scale,
                          uint64_t seed, uint32_t tensor_id, uint32_t step,
                          int out_dtype, void* out, int32_t* out_exp,
-                         const unsigned long long* maxp, hipStream_t s);
+                         const unsigned long long* maxp, hipStream_t s,
+                         const uint64_t* part = nullptr, int64_t nparts = 0);
 
 // max |.| of an int32/int64 buffer into *maxp (which must be zeroed first)
 int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* maxp,

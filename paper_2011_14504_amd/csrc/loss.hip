@@ -388,10 +388,10 @@ __device__ __forceinline__ int frexp_exp_bits64(uint64_t mb)
     return E - 1022;
 }
 
-__global__ __launch_bounds__(256) void k_ce_quant(const CeCellArgs a, const unsigned long long* maxp, int bits,
+__global__ __launch_bounds__(256) void k_ce_quant(const CeCellArgs a, int64_t nparts, int bits,
                                                   int8_t* __restrict__ err, int32_t* err_exp, double* loss)
 {
-    const uint64_t mb = *maxp;
+    const uint64_t mb = reduce_partials_u64(a.part, nparts);
     const int b = mb ? frexp_exp_bits64(mb) : 0;
     const int64_t total = (int64_t)a.N * a.h * a.w * a.K;
     if (blockIdx.x == 0) {
@@ -469,7 +469,6 @@ extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, c
         if (a.rx[i].len > kMaxRunLen) return ISEG_ERR_UNSUPPORTED;
     a.status = dev_status;
     char* p = (char*)ws;
-    unsigned long long* maxp = (unsigned long long*)p;
     p += 256;
     a.cell = (double*)p;
     p += ce_cell_bytes(N, a.nry, a.nrx, K);
@@ -489,9 +488,8 @@ extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, c
     if (rc) return rc;
     hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)h, (unsigned)N), dim3(256), 0, stream, a);
     if ((rc = launch_ok())) return rc;
-    if ((rc = launch_reduce_max(a.part, N * h, maxp, stream))) return rc;
     const int64_t nlow = N * h * w * K;
-    hipLaunchKernelGGL(k_ce_quant, dim3(grid_for(nlow, 256, 2048)), dim3(256), 0, stream, a,
-                       (const unsigned long long*)maxp, (int)bits, err, err_exp, loss);
+    hipLaunchKernelGGL(k_ce_quant, dim3(grid_for(nlow, 256, 2048)), dim3(256), 0, stream, a, N * h, (int)bits, err,
+                       err_exp, loss);
     return launch_ok();
 }

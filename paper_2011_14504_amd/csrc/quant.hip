@@ -117,7 +117,15 @@ struct RqArgs {
     uint32_t tensor_id, step;
     int32_t* out_exp;
     const unsigned long long* maxp;
+    const uint64_t* part;
+    int64_t nparts;
 };
+
+// the tensor max: from *maxp, or reduced by this block from the partials
+__device__ __forceinline__ uint64_t rq_max(const RqArgs& a)
+{
+    return a.maxp ? (uint64_t)*a.maxp : reduce_partials_u64(a.part, a.nparts);
+}
 
 __device__ __forceinline__ int rq_shift(const RqArgs& a, uint64_t M)
 {
@@ -144,7 +152,7 @@ __device__ __forceinline__ int64_t rq_one(const RqArgs& a, int64_t q, int r, int
 __global__ __launch_bounds__(256) void k_requant_i32_i8(const int32_t* __restrict__ in,
                                                         int8_t* __restrict__ out, RqArgs a)
 {
-    uint64_t M = *a.maxp;
+    uint64_t M = rq_max(a);
     int r = rq_shift(a, M);
     rq_write_exp(a, M, r);
     int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -174,7 +182,7 @@ template <typename TIn, typename TOut>
 __global__ __launch_bounds__(256) void k_requant_generic(const TIn* __restrict__ in,
                                                          TOut* __restrict__ out, RqArgs a)
 {
-    uint64_t M = *a.maxp;
+    uint64_t M = rq_max(a);
     int r = rq_shift(a, M);
     rq_write_exp(a, M, r);
     for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < a.n;
@@ -186,28 +194,30 @@ int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t*
                          const int32_t* exp_b, int32_t exp_add, int bits, int stochastic,
                          int keep_scale, uint64_t seed, uint32_t tensor_id, uint32_t step,
                          int out_dtype, void* out, int32_t* out_exp,
-                         const unsigned long long* maxp, hipStream_t s)
+                         const unsigned long long* maxp, hipStream_t s, const uint64_t* part, int64_t nparts)
 {
     RqArgs a;
+    a.part = part; a.nparts = nparts;
     a.n = n; a.exp_a = exp_a; a.exp_b = exp_b; a.exp_add = exp_add;
     a.bits = bits; a.stochastic = stochastic; a.keep_scale = keep_scale;
     a.seed = seed; a.tensor_id = tensor_id; a.step = step;
     a.out_exp = out_exp; a.maxp = maxp;
+    const unsigned cap = part ? 1024 : 4096;        // partials are read by every block
     bool aligned = (((uintptr_t)in | (uintptr_t)out) & 15) == 0;
     if (in_dtype == ISEG_I32 && out_dtype == ISEG_I8 && aligned)
-        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_i32_i8, dim3(grid_for(n, 256 * 16, 4096)), dim3(256), 0, s,
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_i32_i8, dim3(grid_for(n, 256 * 16, cap)), dim3(256), 0, s,
                            (const int32_t*)in, (int8_t*)out, a);
     else if (in_dtype == ISEG_I32 && out_dtype == ISEG_I8)
-        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int32_t, int8_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int32_t, int8_t>), dim3(grid_for(n, 256, cap)),
                            dim3(256), 0, s, (const int32_t*)in, (int8_t*)out, a);
     else if (in_dtype == ISEG_I32 && out_dtype == ISEG_I16)
-        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int32_t, int16_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int32_t, int16_t>), dim3(grid_for(n, 256, cap)),
                            dim3(256), 0, s, (const int32_t*)in, (int16_t*)out, a);
     else if (in_dtype == ISEG_I64 && out_dtype == ISEG_I8)
-        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int64_t, int8_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int64_t, int8_t>), dim3(grid_for(n, 256, cap)),
                            dim3(256), 0, s, (const int64_t*)in, (int8_t*)out, a);
     else if (in_dtype == ISEG_I64 && out_dtype == ISEG_I16)
-        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int64_t, int16_t>), dim3(grid_for(n, 256, 4096)),
+        ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, (k_requant_generic<int64_t, int16_t>), dim3(grid_for(n, 256, cap)),
                            dim3(256), 0, s, (const int64_t*)in, (int16_t*)out, a);
     else
         return ISEG_ERR_ARG;
@@ -233,7 +243,7 @@ __global__ __launch_bounds__(256) void k_requant_s16_i8(const int16_t* __restric
                                                         int32_t cols, StageMap sm, int8_t* __restrict__ out,
                                                         RqArgs a)
 {
-    const uint64_t M = *a.maxp;
+    const uint64_t M = rq_max(a);
     const int r = rq_shift(a, M);
     rq_write_exp(a, M, r);
     const int32_t cpr = cols >> 4;                        // 16-element chunks per row
@@ -276,15 +286,18 @@ __global__ __launch_bounds__(256) void k_requant_s16_i8(const int16_t* __restric
 
 int launch_requant_staged16(const int16_t* in, const uint8_t* tshift, int64_t rows, int32_t cols,
                             const StageMap& sm, const int32_t* exp_a, const int32_t* exp_b, int bits,
-                            int8_t* out, int32_t* out_exp, const unsigned long long* maxp, hipStream_t s)
+                            int8_t* out, int32_t* out_exp, const unsigned long long* maxp, hipStream_t s,
+                            const uint64_t* part, int64_t nparts)
 {
     RqArgs a;
+    a.part = part; a.nparts = nparts;
     a.n = rows * cols; a.exp_a = exp_a; a.exp_b = exp_b; a.exp_add = 0;
     a.bits = bits; a.stochastic = 0; a.keep_scale = 1;
     a.seed = 0; a.tensor_id = 0; a.step = 0;
     a.out_exp = out_exp; a.maxp = maxp;
     if (cols % 16 || sm.tile_cols % 16 || (((uintptr_t)in | (uintptr_t)out) & 15)) return ISEG_ERR_ARG;
-    ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_s16_i8, dim3(grid_for(rows * cols, 256 * 16, 8192)), dim3(256),
+    ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_s16_i8, dim3(grid_for(rows * cols, 256 * 16, part ? 1024 : 8192)),
+                      dim3(256),
                       0, s, in, tshift, rows, cols, sm, out, a);
     return launch_ok();
 }
