@@ -280,8 +280,8 @@ typedef struct iseg_update_desc {
  * counter step), then Delta = UQ(G 2^-lr_shift, k_U) (Eq. 19), master <-
  * clamp(master - Delta), w_q = UQ(master, k_W) (Eq. 8, or Eq. 14's fold for
  * gamma / beta).  Equal to iseg_weight_update / iseg_bn_param_update per
- * tensor.  descs: device array of n_desc descriptors (caller-owned; the
- * tensors they point to must not overlap). */
+ * tensor.  descs: device array of n_desc <= 4096 descriptors (caller-owned;
+ * the tensors they point to must not overlap). */
 int iseg_update_multi(const iseg_update_desc* descs, int32_t n_desc, int32_t bits, uint64_t seed,
                       uint32_t step, int32_t lr_shift, int32_t k_U, int32_t k_W, int32_t* dev_status,
                       hipStream_t stream);

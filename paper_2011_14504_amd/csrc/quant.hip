@@ -558,41 +558,97 @@ __device__ __forceinline__ int64_t upd_delta(int64_t g, int sh, int k_U, int64_t
     return clamp_k(shr_rhu(g, -sh), k_U);
 }
 
-__global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __restrict__ descs, UpdCfg u)
+// Work split into chunks of kUpdChunk elements over all ISEG_UPD_CODES
+// tensors (one chunk per ISEG_UPD_RAW tensor, which one block handles whole);
+// a fixed grid strides over the chunks, each block first forming the chunk
+// offsets of the descriptors in LDS.
+constexpr int kUpdChunk = 4096;
+constexpr int kUpdMaxDesc = 4096;
+
+__global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __restrict__ descs, int n_desc,
+                                                      UpdCfg u)
 {
-    const iseg_update_desc d = descs[blockIdx.y];
+    __shared__ int32_t first[kUpdMaxDesc + 1];
+    __shared__ int32_t tot[256];
+    __shared__ uint64_t red[4];
+    {
+        // chunk counts of a run of descriptors per thread (loads in parallel),
+        // then an exclusive scan of the per-thread totals
+        const int per = (n_desc + 255) / 256;
+        const int d0 = threadIdx.x * per;
+        int32_t t = 0;
+        for (int d = d0; d < d0 + per && d < n_desc; d++) {
+            const int32_t c = descs[d].kind == ISEG_UPD_CODES ? (int32_t)((descs[d].n + kUpdChunk - 1) / kUpdChunk) : 1;
+            first[d] = c;
+            t += c;
+        }
+        tot[threadIdx.x] = t;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int32_t acc = 0;
+            for (int i = 0; i < 256; i++) {
+                const int32_t v = tot[i];
+                tot[i] = acc;
+                acc += v;
+            }
+            first[n_desc] = acc;
+        }
+        __syncthreads();
+        int32_t acc = tot[threadIdx.x];
+        for (int d = d0; d < d0 + per && d < n_desc; d++) {
+            const int32_t c = first[d];
+            first[d] = acc;
+            acc += c;
+        }
+        __syncthreads();
+    }
+    const int nchunks = first[n_desc];
     const int dq = u.k_U - u.k_W;
     const int64_t lim = ((int64_t)1 << (u.k_U - 1)) - 1;
-    if (d.kind == ISEG_UPD_CODES) {
-        const int8_t* g = (const int8_t*)d.g;
-        const int sh = *d.g_exp - u.lr_shift - d.master_exp;     // Delta W code = g 2^sh, rounded
-        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d.n;
-             i += (int64_t)gridDim.x * blockDim.x) {
-            const int64_t m = clamp_k((int64_t)d.master[i] - upd_delta(g[i], sh, u.k_U, lim), u.k_U);
-            d.master[i] = (int32_t)m;
-            d.w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), u.k_W);
+    for (int ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
+        int lo = 0, hi = n_desc - 1;                 // last descriptor with first <= ch
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (first[mid] <= ch) lo = mid;
+            else hi = mid - 1;
         }
-        return;
-    }
-    if (blockIdx.x != 0) return;
-    const int64_t* g = (const int64_t*)d.g;
-    uint64_t m = 0;
-    for (int64_t c = threadIdx.x; c < d.n; c += blockDim.x) {
-        const uint64_t v = uabs64(g[c]);
-        m = v > m ? v : m;
-    }
-    m = block_max_u64(m);
-    const int r = m ? bitlen_u64(m) - (u.bits - 1) : 0;
-    const int32_t gexp = *d.g_exp + r;                            // Eq. 17 keeps the scale
-    if (threadIdx.x == 0 && d.g_q_exp) *d.g_q_exp = gexp;
-    const int sh = gexp - u.lr_shift - d.master_exp;
-    for (int64_t c = threadIdx.x; c < d.n; c += blockDim.x) {
-        const int64_t q = r > 0 ? rq_code(g[c], r, u.bits, philox_draw(u.seed, d.tensor_id, u.step, (uint64_t)c))
-                                : sq_code(g[c], r, u.bits);
-        if (d.g_q) d.g_q[c] = (int8_t)q;
-        const int64_t mm = clamp_k((int64_t)d.master[c] - upd_delta(q, sh, u.k_U, lim), u.k_U);
-        d.master[c] = (int32_t)mm;
-        d.w_q[c] = (int8_t)clamp_k(shr_rhu(mm, dq), u.k_W);
+        const iseg_update_desc d = descs[lo];
+        if (d.kind == ISEG_UPD_CODES) {
+            const int8_t* g = (const int8_t*)d.g;
+            const int sh = *d.g_exp - u.lr_shift - d.master_exp;      // Delta W code = g 2^sh, rounded
+            const int64_t i0 = (int64_t)(ch - first[lo]) * kUpdChunk;
+            const int64_t i1 = i0 + kUpdChunk < d.n ? i0 + kUpdChunk : d.n;
+            for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+                const int64_t m = clamp_k((int64_t)d.master[i] - upd_delta(g[i], sh, u.k_U, lim), u.k_U);
+                d.master[i] = (int32_t)m;
+                d.w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), u.k_W);
+            }
+            continue;
+        }
+        const int64_t* g = (const int64_t*)d.g;
+        uint64_t m = 0;
+        for (int64_t c = threadIdx.x; c < d.n; c += blockDim.x) {
+            const uint64_t v = uabs64(g[c]);
+            m = v > m ? v : m;
+        }
+        m = wave_max_u64(m);
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+        __syncthreads();
+        m = red[0];
+        for (int i = 1; i < (int)(blockDim.x >> 6); i++) m = red[i] > m ? red[i] : m;
+        __syncthreads();
+        const int r = m ? bitlen_u64(m) - (u.bits - 1) : 0;
+        const int32_t gexp = *d.g_exp + r;                             // Eq. 17 keeps the scale
+        if (threadIdx.x == 0 && d.g_q_exp) *d.g_q_exp = gexp;
+        const int sh = gexp - u.lr_shift - d.master_exp;
+        for (int64_t c = threadIdx.x; c < d.n; c += blockDim.x) {
+            const int64_t q = r > 0 ? rq_code(g[c], r, u.bits, philox_draw(u.seed, d.tensor_id, u.step, (uint64_t)c))
+                                    : sq_code(g[c], r, u.bits);
+            if (d.g_q) d.g_q[c] = (int8_t)q;
+            const int64_t mm = clamp_k((int64_t)d.master[c] - upd_delta(q, sh, u.k_U, lim), u.k_U);
+            d.master[c] = (int32_t)mm;
+            d.w_q[c] = (int8_t)clamp_k(shr_rhu(mm, dq), u.k_W);
+        }
     }
 }
 
@@ -601,12 +657,12 @@ extern "C" int iseg_update_multi(const iseg_update_desc* descs, int32_t n_desc, 
                                  hipStream_t stream)
 {
     (void)dev_status;
-    if (n_desc < 0 || n_desc > 65535 || (n_desc > 0 && !descs)) return ISEG_ERR_ARG;
+    if (n_desc < 0 || n_desc > kUpdMaxDesc || (n_desc > 0 && !descs)) return ISEG_ERR_ARG;
     if (bits < 2 || bits > 8 || k_U < 9 || k_U > 31 || k_W < 2 || k_W > 8) return ISEG_ERR_ARG;
     if (n_desc == 0) return ISEG_OK;
     UpdCfg u;
     u.seed = seed; u.step = step; u.bits = bits; u.lr_shift = lr_shift; u.k_U = k_U; u.k_W = k_W;
-    hipLaunchKernelGGL(k_update_multi, dim3(64, (unsigned)n_desc), dim3(256), 0, stream, descs, u);
+    hipLaunchKernelGGL(k_update_multi, dim3(2048), dim3(256), 0, stream, descs, (int)n_desc, u);
     return launch_ok();
 }
 
