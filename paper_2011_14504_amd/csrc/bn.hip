@@ -301,19 +301,20 @@ __device__ __forceinline__ void copy_rows_to_lds(int8_t* dst, const int8_t* __re
 // forward workspace
 // ---------------------------------------------------------------------------
 struct FwdWs {
-    int32_t* b_glob;                 // exponent of Q_xhat's scale (atomicMax over channels)
+    int32_t* b_glob;                 // exponent of Q_xhat's scale (written by fin2)
     unsigned long long* maxY;        // unused (kept for the layout)
     int32_t *p_s1, *p_min, *p_max;   // [gx][C] partials
     long long* p_abs;                // [gx][C]
     long long* Y;                    // [C][256] y on the grid 2^e_y (before ReLU)
     unsigned long long* maxYc;       // [C] max |ReLU(y)| of channel c over its occupied codes
+    int32_t* bcand;                  // [C] channel candidates for b
 };
 
 size_t fwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C;
     return 256 + 3 * align256(pc * 4) + align256(pc * 8) + align256((size_t)st.C * 256 * 8) +
-           align256((size_t)st.C * 8);
+           align256((size_t)st.C * 8) + align256((size_t)st.C * 4);
 }
 
 FwdWs fwd_ws_map(void* base, const Stream& st)
@@ -329,7 +330,8 @@ FwdWs fwd_ws_map(void* base, const Stream& st)
     w.p_max = (int32_t*)p; p += align256(pc * 4);
     w.p_abs = (long long*)p; p += align256(pc * 8);
     w.Y = (long long*)p; p += align256((size_t)st.C * 256 * 8);
-    w.maxYc = (unsigned long long*)p;
+    w.maxYc = (unsigned long long*)p; p += align256((size_t)st.C * 8);
+    w.bcand = (int32_t*)p;
     return w;
 }
 
@@ -409,7 +411,7 @@ __global__ __launch_bounds__(256) void k_bnf_finmu(const int32_t* x_exp, Stream 
         sv.qmin[c] = mn;
         sv.qmax[c] = mx;
         sv.t0[c] = 128; sv.p0[c] = 128; sv.mlo[c] = 128; sv.mhi[c] = -129;
-        if (c == 0) { *w.b_glob = kSentinelLo; *w.maxY = 0; }
+
     }
 }
 
@@ -468,6 +470,7 @@ __global__ __launch_bounds__(256) void k_bnf_finsig(const int32_t* x_exp, Stream
     for (int b = threadIdx.x; b < st.gx; b += 256) a += w.p_abs[(int64_t)b * st.C + c];
     a = block_reduce(a, OpAdd(), sh64);
     if (threadIdx.x != 0) return;
+    w.bcand[c] = kSentinelLo;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
     const int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
@@ -487,7 +490,7 @@ __global__ __launch_bounds__(256) void k_bnf_finsig(const int32_t* x_exp, Stream
         int e = ceil_pow2_exp128(abs128((i128)D), (i128)den) + gg - e_sig;
         best = e > best ? e : best;
     }
-    if (best > kSentinelLo) atomicMax(w.b_glob, best);
+    w.bcand[c] = best;
 }
 
 // per (channel, code): xhat code, y, flags, thresholds; max |ReLU(y)| over the
@@ -499,8 +502,18 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w,
     const int q = (int)threadIdx.x - 128;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
-    int b = *w.b_glob;
+    // b: the largest channel candidate (one block max over C values)
+    int b = kSentinelLo;
+    for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) b = w.bcand[k] > b ? w.bcand[k] : b;
+    {
+        __shared__ int32_t rb[4];
+        for (int o = 32; o > 0; o >>= 1) b = max(b, __shfl_xor(b, o));
+        if ((threadIdx.x & 63) == 0) rb[threadIdx.x >> 6] = b;
+        __syncthreads();
+        b = max(max(rb[0], rb[1]), max(rb[2], rb[3]));
+    }
     if (b == kSentinelLo) b = 0;
+    if (c == 0 && threadIdx.x == 0) *w.b_glob = b;
     const int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
     const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
     const int e_xh = b - (cf.k_xhat - 1);
@@ -550,8 +563,7 @@ __global__ __launch_bounds__(256) void k_bnf_fin3(const int32_t* x_exp, FwdWs w,
     const int c = blockIdx.x;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
-    int b = *w.b_glob;
-    if (b == kSentinelLo) b = 0;
+    const int b = *w.b_glob;
     const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
     const int e_xh = b - (cf.k_xhat - 1);
     const int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
@@ -609,13 +621,14 @@ struct BwdWs {
     long long *sd, *sdn, *sf, *sfn;  // [C] reduced
     int32_t *Z, *mm;                 // [C], [C][6]
     int8_t* lut;                     // [C][3][256] dx codes
+    int32_t* cand;                   // [C] exponent candidates of max|dx|
 };
 
 size_t bwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
     return 256 + 2 * align256(pc * 4) + 3 * align256(pc * 8) + align256(pc * 24) +
-           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768);
+           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768) + align256(C * 4);
 }
 
 BwdWs bwd_ws_map(void* base, const Stream& st)
@@ -638,7 +651,8 @@ BwdWs bwd_ws_map(void* base, const Stream& st)
     w.sfn = (long long*)p; p += align256(C * 8);
     w.Z = (int32_t*)p; p += align256(C * 4);
     w.mm = (int32_t*)p; p += align256(C * 24);
-    w.lut = (int8_t*)p;
+    w.lut = (int8_t*)p; p += align256(C * 768);
+    w.cand = (int32_t*)p;
     return w;
 }
 
@@ -1040,6 +1054,129 @@ __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t 
     }
 }
 
+// ---------------------------------------------------------------------------
+// Exact E2 (k_E2 >= 15, |gamma delta| <= 127^2 < 2^(k_E2-1)): E2's requant
+// shift r2 is <= 0 and scales every term of the bracket and the exponent base
+// by inverse powers of two, so dx, its exponent bound and its codes are those
+// of r2 = 0, with f = gamma_q delta; one finalize kernel replaces fin1 + fin2.
+// ---------------------------------------------------------------------------
+// per channel: pass-1 partials -> sums, dgamma, dbeta; the candidate exponent
+// of max|dx| over the channel's per-class extreme deltas
+__global__ __launch_bounds__(256) void k_bnb_fin_exact(const int32_t* dy_exp, Stream st, BwdWs w, Saved sv,
+                                                       BnCfg cf, const int8_t* gamma_q, int64_t* dgamma,
+                                                       int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
+                                                       int32_t* dev_status)
+{
+    __shared__ long long r64[4][2];
+    __shared__ int32_t r32[4][7];
+    const int c = blockIdx.x;
+    const size_t pc = (size_t)st.gx * st.C;
+    long long sd = 0, sdn = 0;
+    int z = 0;
+    int mm[6] = {1000, -1000, 1000, -1000, 1000, -1000};
+    for (int b = threadIdx.x; b < st.gx; b += 256) {
+        const int64_t o = (int64_t)b * st.C + c;
+        sd += w.p_sd[o];
+        sdn += w.p_sdn[o];
+        z += w.p_z[o];
+#pragma unroll
+        for (int k = 0; k < 6; k++) {
+            const int v = w.p_mm[k * pc + o];
+            mm[k] = (k & 1) ? (v > mm[k] ? v : mm[k]) : (v < mm[k] ? v : mm[k]);
+        }
+    }
+    // all nine reductions in one round: wave shuffles, then the four waves via LDS
+    for (int o = 32; o > 0; o >>= 1) {
+        sd += __shfl_xor(sd, o);
+        sdn += __shfl_xor(sdn, o);
+        z += __shfl_xor(z, o);
+#pragma unroll
+        for (int k = 0; k < 6; k++) {
+            const int v = __shfl_xor(mm[k], o);
+            mm[k] = (k & 1) ? max(mm[k], v) : min(mm[k], v);
+        }
+    }
+    const int wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        r64[wv][0] = sd; r64[wv][1] = sdn; r32[wv][0] = z;
+#pragma unroll
+        for (int k = 0; k < 6; k++) r32[wv][k + 1] = mm[k];
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int k2 = 1; k2 < 4; k2++) {
+        sd += r64[k2][0]; sdn += r64[k2][1]; z += r32[k2][0];
+#pragma unroll
+        for (int k = 0; k < 6; k++) mm[k] = (k & 1) ? max(mm[k], r32[k2][k + 1]) : min(mm[k], r32[k2][k + 1]);
+    }
+    const int32_t s_d = *dy_exp;
+    if (c == 0) {
+        if (s_d < -60 || s_d > 16) set_status(dev_status, ISEG_DEV_RANGE);
+        *dbeta_exp = s_d;
+        *dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
+    }
+    w.sd[c] = sd; w.sdn[c] = sdn; w.Z[c] = z;
+#pragma unroll
+    for (int k = 0; k < 6; k++) w.mm[c * 6 + k] = mm[k];
+    dbeta[c] = sd;
+    dgamma[c] = sdn;
+    const int gq = gamma_q[c];
+    const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
+    const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
+    const int Ebase = s_d + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
+    const i128 M = st.M;
+    const i128 Dd = (i128)sv.den[c] * M * M;
+    const i128 Sf = (i128)gq * sd, T = (i128)gq * sdn, Z = z;
+    int best = kSentinelLo;
+    for (int k = 0; k < 3; k++) {
+        const int lo = mm[2 * k], hi = mm[2 * k + 1];
+        if (lo > hi) continue;
+        const int ds[2] = {lo, hi};
+        for (int t = 0; t < 2; t++) {      // |dx| is extreme at the class's extreme deltas
+            const int64_t f = clamp_k((int64_t)gq * ds[t], cf.k_E2);
+            const i128 B = bnb_bracket(f, k - 1, M, Sf, T, Z, e_xh);
+            if (B == 0) continue;
+            const int e = ceil_pow2_exp128(abs128(B), Dd) + Ebase;
+            best = e > best ? e : best;
+        }
+    }
+    w.cand[c] = best;
+}
+
+// dx code table of a channel (one thread per masked error code, three sgn
+// classes); E1's exponent from the largest candidate over the C channels
+__global__ __launch_bounds__(256) void k_bnb_lut_exact(const int32_t* dy_exp, int64_t Mrows, BwdWs w, Saved sv,
+                                                       BnCfg cf, const int8_t* gamma_q, int32_t* dx_exp)
+{
+    __shared__ int32_t rb[4];
+    const int c = blockIdx.x;
+    int bdx = kSentinelLo;
+    for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) bdx = w.cand[k] > bdx ? w.cand[k] : bdx;
+    for (int o = 32; o > 0; o >>= 1) bdx = max(bdx, __shfl_xor(bdx, o));
+    if ((threadIdx.x & 63) == 0) rb[threadIdx.x >> 6] = bdx;
+    __syncthreads();
+    bdx = max(max(rb[0], rb[1]), max(rb[2], rb[3]));
+    if (bdx == kSentinelLo) bdx = 0;
+    if (c == 0 && threadIdx.x == 0) *dx_exp = bdx - (cf.k_E1 - 1);
+    const int d = (int)threadIdx.x - 128;
+    const int gq = gamma_q[c];
+    const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
+    const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
+    const int Ebase = *dy_exp + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
+    const i128 M = Mrows;
+    const i128 Dd = (i128)sv.den[c] * M * M;
+    const i128 Sf = (i128)gq * w.sd[c], T = (i128)gq * w.sdn[c], Z = w.Z[c];
+    const int64_t f = d < -127 ? 0 : clamp_k((int64_t)gq * d, cf.k_E2);
+    for (int k = 0; k < 3; k++) {
+        int8_t code = 0;
+        if (d >= -127) {
+            const i128 B = bnb_bracket(f, k - 1, M, Sf, T, Z, e_xh);
+            code = (int8_t)clamp_k128(rhu128(B, Ebase + (cf.k_E1 - 1) - bdx, Dd), cf.k_E1);
+        }
+        w.lut[((int64_t)c * 3 + k) * 256 + threadIdx.x] = code;
+    }
+}
+
 // Output pass: dx code = lut[c][sgn class][masked delta].  A per-(channel,
 // code) entry gives the offset of the channel's class row in the block's LDS
 // copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
@@ -1206,13 +1343,18 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     const int exact_e2 = cf.k_E2 >= 15;
     ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats, sg, dim3(kNT), 0, stream, dy, x, st, w, sv,
                       cf.relu);
-    hipLaunchKernelGGL(k_bnb_fin1, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma,
-                       dbeta, dgamma_exp, dbeta_exp, dev_status);
-    if (!exact_e2)
+    if (exact_e2) {
+        hipLaunchKernelGGL(k_bnb_fin_exact, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma, dbeta,
+                           dgamma_exp, dbeta_exp, dev_status);
+        hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, dx_exp);
+    } else {
+        hipLaunchKernelGGL(k_bnb_fin1, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma,
+                           dbeta, dgamma_exp, dbeta_exp, dev_status);
         hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(kNT), 0, stream, dy, x, st, w, sv, cf, gamma_q);
-    hipLaunchKernelGGL(k_bnb_fin2, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, exact_e2);
-    hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2,
-                       dx_exp);
+        hipLaunchKernelGGL(k_bnb_fin2, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, exact_e2);
+        hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2,
+                           dx_exp);
+    }
     ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, sg, dim3(kNT), 0, stream, dy, x, dx_out, st,
                       w, sv, cf.relu);
     return launch_ok();
