@@ -16,7 +16,8 @@ namespace {
 
 constexpr int kMaxIn = 8;
 constexpr int kMaxGap = 48;        // aligned int8 terms stay below 2^55
-constexpr int kMaxPartials = 512;  // pass-1 grid cap (partials reduced by each pass-2 block)
+constexpr int kMaxPartials = 1024; // pass-1 grid cap (partials reduced by each pass-2 block)
+constexpr int kU = 4;              // 16-byte vectors in flight per lane
 
 struct MergeArgs {
     const int8_t* p[kMaxIn];
@@ -74,6 +75,35 @@ __device__ __forceinline__ void merge_sum16(const MergeArgs& a, const int* sh, i
     }
 }
 
+// the 16-byte vectors of every input for output vector v (v < nv)
+template <int NIN>
+__device__ __forceinline__ void merge_load16(const MergeArgs& a, int64_t v, int64_t nv, int4* raw)
+{
+    if (v >= nv) return;
+    const int64_t j = v * 16;
+    const int64_t img = j / (a.HW * a.C);
+    const int64_t c = j % a.C;
+#pragma unroll
+    for (int i = 0; i < NIN; i++) raw[i] = *(const int4*)(a.p[i] + (a.bc[i] ? img * a.C + c : j));
+}
+
+template <int NIN>
+__device__ __forceinline__ void merge_sum16_raw(const MergeArgs& a, const int* sh, const int4* raw, int64_t* s)
+{
+#pragma unroll
+    for (int t = 0; t < 16; t++) s[t] = 0;
+#pragma unroll
+    for (int i = 0; i < NIN; i++) {
+        const int32_t w[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+        for (int t = 0; t < 16; t++) s[t] += (int64_t)(int8_t)(w[t >> 2] >> (8 * (t & 3))) << sh[i];
+    }
+    if (a.relu) {
+#pragma unroll
+        for (int t = 0; t < 16; t++) s[t] = s[t] > 0 ? s[t] : 0;
+    }
+}
+
 __device__ __forceinline__ int64_t merge_sum1(const MergeArgs& a, const int* sh, int64_t j)
 {
     const int64_t img = j / (a.HW * a.C);
@@ -87,7 +117,7 @@ __device__ __forceinline__ int64_t merge_sum1(const MergeArgs& a, const int* sh,
     return s;
 }
 
-template <bool VEC>
+template <bool VEC, int NIN>
 __global__ __launch_bounds__(256) void k_merge_max(MergeArgs a)
 {
     int sh[kMaxIn], e0;
@@ -95,14 +125,32 @@ __global__ __launch_bounds__(256) void k_merge_max(MergeArgs a)
     uint64_t m = 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (VEC) {
+    if (VEC && NIN > 0) {
+        const int64_t nv = a.n / 16;
+        for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
+            int4 raw[kU][NIN > 0 ? NIN : 1];
+#pragma unroll
+            for (int u = 0; u < kU; u++) merge_load16<NIN>(a, v0 + u * stride, nv, raw[u]);
+#pragma unroll
+            for (int u = 0; u < kU; u++) {
+                if (v0 + u * stride >= nv) break;
+                int64_t s[16];
+                merge_sum16_raw<NIN>(a, sh, raw[u], s);
+#pragma unroll
+                for (int t = 0; t < 16; t++) {
+                    const uint64_t w = (uint64_t)(s[t] < 0 ? -s[t] : s[t]);
+                    m = w > m ? w : m;
+                }
+            }
+        }
+    } else if (VEC) {
         for (int64_t v = t0; v < a.n / 16; v += stride) {
             int64_t s[16];
             merge_sum16(a, sh, v * 16, s);
 #pragma unroll
             for (int t = 0; t < 16; t++) {
-                const uint64_t u = (uint64_t)(s[t] < 0 ? -s[t] : s[t]);
-                m = u > m ? u : m;
+                const uint64_t w = (uint64_t)(s[t] < 0 ? -s[t] : s[t]);
+                m = w > m ? w : m;
             }
         }
     } else {
@@ -115,7 +163,7 @@ __global__ __launch_bounds__(256) void k_merge_max(MergeArgs a)
     block_store_max_u64(m, a.part);
 }
 
-template <bool VEC>
+template <bool VEC, int NIN>
 __global__ __launch_bounds__(256) void k_merge_apply(MergeArgs a, int64_t nparts)
 {
     int sh[kMaxIn], e0;
@@ -125,7 +173,26 @@ __global__ __launch_bounds__(256) void k_merge_apply(MergeArgs a, int64_t nparts
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.out_exp = e0 + r;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (VEC) {
+    if (VEC && NIN > 0) {
+        const int64_t nv = a.n / 16;
+        for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
+            int4 raw[kU][NIN > 0 ? NIN : 1];
+#pragma unroll
+            for (int u = 0; u < kU; u++) merge_load16<NIN>(a, v0 + u * stride, nv, raw[u]);
+#pragma unroll
+            for (int u = 0; u < kU; u++) {
+                const int64_t v = v0 + u * stride;
+                if (v >= nv) break;
+                int64_t s[16];
+                merge_sum16_raw<NIN>(a, sh, raw[u], s);
+                uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+                for (int t = 0; t < 16; t++)
+                    w[t >> 2] |= (uint32_t)(uint8_t)sq_code(s[t], r, a.bits) << (8 * (t & 3));
+                *(int4*)(a.out + v * 16) = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
+            }
+        }
+    } else if (VEC) {
         for (int64_t v = t0; v < a.n / 16; v += stride) {
             int64_t s[16];
             merge_sum16(a, sh, v * 16, s);
@@ -141,14 +208,38 @@ __global__ __launch_bounds__(256) void k_merge_apply(MergeArgs a, int64_t nparts
 }
 
 // ReLU mask of a merged sum: dx = dy where sum_i a_i 2^e_i > 0, else 0
-template <bool VEC>
+template <bool VEC, int NIN>
 __global__ __launch_bounds__(256) void k_relu_mask(MergeArgs a, const int8_t* __restrict__ dy)
 {
     int sh[kMaxIn], e0;
     if (!merge_shifts(a, sh, &e0) && blockIdx.x == 0 && threadIdx.x == 0) set_status(a.status, ISEG_DEV_RANGE);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (VEC) {
+    if (VEC && NIN > 0) {
+        const int64_t nv = a.n / 16;
+        for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
+          int4 raw[kU][NIN > 0 ? NIN : 1], dr[kU];
+#pragma unroll
+          for (int u = 0; u < kU; u++) {
+              merge_load16<NIN>(a, v0 + u * stride, nv, raw[u]);
+              if (v0 + u * stride < nv) dr[u] = *(const int4*)(dy + (v0 + u * stride) * 16);
+          }
+#pragma unroll
+          for (int u = 0; u < kU; u++) {
+            const int64_t v = v0 + u * stride;
+            if (v >= nv) break;
+            int64_t s[16];
+            merge_sum16_raw<NIN>(a, sh, raw[u], s);
+            const int4 d = dr[u];
+            const uint32_t dw[4] = {(uint32_t)d.x, (uint32_t)d.y, (uint32_t)d.z, (uint32_t)d.w};
+            uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int t = 0; t < 16; t++)
+                if (s[t] > 0) w[t >> 2] |= dw[t >> 2] & (0xffu << (8 * (t & 3)));
+            *(int4*)(a.out + v * 16) = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
+          }
+        }
+    } else if (VEC) {
         for (int64_t v = t0; v < a.n / 16; v += stride) {
             int64_t s[16];
             merge_sum16(a, sh, v * 16, s);
@@ -450,14 +541,17 @@ extern "C" int iseg_sum_requant(int32_t n_in, const int8_t* const* in, const int
     bool vec = (C % 16) == 0 && ((uintptr_t)out & 15) == 0;
     for (int i = 0; i < n_in; i++) vec = vec && (((uintptr_t)in[i]) & 15) == 0;
     const int64_t units = vec ? n / 16 : n;
-    const unsigned g1 = grid_for(units, 256, kMaxPartials);
-    if (vec) hipLaunchKernelGGL(k_merge_max<true>, dim3(g1), dim3(256), 0, stream, a);
-    else hipLaunchKernelGGL(k_merge_max<false>, dim3(g1), dim3(256), 0, stream, a);
+    const unsigned g1 = grid_for(units, 256 * kU, kMaxPartials);
+    const bool two = n_in == 2;
+    if (vec && two) hipLaunchKernelGGL((k_merge_max<true, 2>), dim3(g1), dim3(256), 0, stream, a);
+    else if (vec) hipLaunchKernelGGL((k_merge_max<true, 0>), dim3(g1), dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((k_merge_max<false, 0>), dim3(g1), dim3(256), 0, stream, a);
     int rc = launch_ok();
     if (rc) return rc;
-    const unsigned g2 = grid_for(units, 256, 2048);
-    if (vec) hipLaunchKernelGGL(k_merge_apply<true>, dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
-    else hipLaunchKernelGGL(k_merge_apply<false>, dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
+    const unsigned g2 = grid_for(units, 256 * kU, 1024);
+    if (vec && two) hipLaunchKernelGGL((k_merge_apply<true, 2>), dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
+    else if (vec) hipLaunchKernelGGL((k_merge_apply<true, 0>), dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
+    else hipLaunchKernelGGL((k_merge_apply<false, 0>), dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
     return launch_ok();
 }
 
@@ -476,9 +570,10 @@ extern "C" int iseg_relu_mask_bwd(const int8_t* dy, int32_t n_in, const int8_t* 
     for (int i = 0; i < n_in; i++) vec = vec && (((uintptr_t)in[i]) & 15) == 0;
     a.n = n; a.HW = n / C; a.C = C;
     a.out = dx; a.status = dev_status;
-    const dim3 grid(grid_for(vec ? n / 16 : n, 256, 4096));
-    if (vec) hipLaunchKernelGGL(k_relu_mask<true>, grid, dim3(256), 0, stream, a, dy);
-    else hipLaunchKernelGGL(k_relu_mask<false>, grid, dim3(256), 0, stream, a, dy);
+    const dim3 grid(grid_for(vec ? n / 16 : n, vec ? 256 * kU : 256, 2048));
+    if (vec && n_in == 2) hipLaunchKernelGGL((k_relu_mask<true, 2>), grid, dim3(256), 0, stream, a, dy);
+    else if (vec) hipLaunchKernelGGL((k_relu_mask<true, 0>), grid, dim3(256), 0, stream, a, dy);
+    else hipLaunchKernelGGL((k_relu_mask<false, 0>), grid, dim3(256), 0, stream, a, dy);
     return launch_ok();
 }
 
