@@ -11,6 +11,7 @@ library records around each of its launches inside the timed steps;
 `cpu_baseline` is the CPU oracle timed on a bounded sample.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -22,6 +23,19 @@ sys.path.insert(0, ROOT)
 METRIC = "int8 conv TOPS fwd+bwd (% MFMA peak); train images/s DeepLabv3-R50 512²"
 INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA
 HBM_PEAK_GBS = 8000.0
+
+# HBM bytes per launch of a timed region, from two rocprofv3 --pmc runs of
+# this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, summed over the
+# kernels of the region) scaled by what the same counters read for the plain
+# copy kernel of --copy-kernel-mib (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0 on
+# MI355X).  Keyed by the timed region; `src` is the SHA-256 of the sources the
+# region's kernels are built from when the counters were taken: a figure whose
+# sources have changed since is reported as null.
+TRAFFIC = {
+    "conv_fwd:aspp.b1": dict(bytes=65280819, src="73e6400e7196b94e0f76ee775b4fa8b109826fbb8f2a3395b027b85091782c9d",
+                             profile="profiles/deeplabv3_r50_512_n8_step_kernel_stats.md"),
+}
+TRAFFIC_SRC = {"conv_fwd": ("conv.hip", "quant.hip", "iseg_common.h")}
 
 WORKLOAD_IDS = {"deeplabv3": 5, "aspp": 4, "resnet-stage": 3, "vgg16": 2, "single-conv": 1}
 
@@ -78,6 +92,38 @@ def timed_kernel_info(name, wl, detail):
                 name=f"{kind} of the L1BN after {layer} (M = {M}, C = {K})")
 
 
+def src_digest(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2011_14504_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(tk):
+    """HBM bytes per launch of the timed region from the committed counter
+    runs, or None when none were taken or its kernels have changed since."""
+    t = TRAFFIC.get(tk)
+    kind = tk.partition(":")[0]
+    if not t or kind not in TRAFFIC_SRC or src_digest(TRAFFIC_SRC[kind]) != t["src"]:
+        return None
+    return t["bytes"]
+
+
+def copy_kernel(mib):
+    """The counter calibration: one plain elementwise kernel that reads and
+    writes `mib` MiB each (float32 negation), run three times."""
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.neg(x, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_kernel_bytes_read": n * 4, "copy_kernel_bytes_written": n * 4}))
+
+
 def cpu_baseline(wl, sample_hw):
     """The oracle's whole training step on one image at sample_hw x sample_hw,
     timed on the host cores; scaled to the benchmark's unit by the ratio of
@@ -108,6 +154,8 @@ def main():
     ap.add_argument("--batch", type=int, default=None)
     ap.add_argument("--cpu-sample-hw", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-kernel-mib", type=int, default=0,
+                    help="only run the plain copy kernel used to calibrate the HBM byte counters")
     ap.add_argument("--timed-kernel", default="conv_fwd:aspp.b1",
                     help="<family>:<layer>, family one of conv_fwd, conv_bwd_data, conv_wgrad, "
                          "bn_fwd_stats1, bn_fwd_stats2, bn_fwd_apply, bn_bwd_stats, bn_bwd_apply")
@@ -116,6 +164,10 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               f"sharding of this path is described in DESIGN.md and not built.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_kernel_mib:
+        copy_kernel(args.copy_kernel_mib)
+        return
 
     import torch
     from paper_2011_14504_amd import iseg, synth
@@ -158,6 +210,11 @@ def main():
         roof = dict(kernel=kinfo["name"], bound="hbm", achieved=ach, peak=HBM_PEAK_GBS,
                     unit="GB/s", frac=(ach / HBM_PEAK_GBS) if ach else None, traffic=None,
                     algorithmic_bytes_per_launch=per_launch, avg_launch_ms=k_ms, launches=launches)
+    traffic = measured_traffic(tk)
+    roof["traffic"] = traffic
+    roof["traffic_unit"] = "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)"
+    if tk in TRAFFIC:
+        roof["profile"] = TRAFFIC[tk]["profile"]
     prof.close()
     cfg = dict(workload=wl["name"], batch=N, image=f"{wl['H']}x{wl['W']}",
                convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
