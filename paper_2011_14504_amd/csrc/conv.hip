@@ -43,6 +43,11 @@ struct IgemmArgs {
     int16_t* out16;               // staged [Mrows][Nout] (int16 path)
     uint8_t* tshift;              // per (row tile, column tile) staging shift
     uint64_t* pmax;               // per-block max |sum| partials (may be null)
+    int8_t* out8;                 // final SQ codes (second pass of the two-pass path)
+    const int32_t* exp_a;         // operand exponents and the result exponent (second pass)
+    const int32_t* exp_b;
+    int32_t* out_exp;
+    int64_t npmax;                // partials written by the first pass
     int64_t Mrows;
     int32_t Nout, Kred, Ci;
     int32_t Hs, Ws, Ho, Wo;
@@ -337,14 +342,20 @@ __global__ __launch_bounds__(256) void k_conv_igemm_tap(IgemmArgs a)
 // Each step (one tap, one 64-channel chunk) stages a 128 x 64-byte A tile and
 // a BN x 64-byte B tile with global_load_lds_dwordx4: a wave's instruction
 // writes 64 lanes x 16 bytes contiguously, i.e. 16 tile rows.  Pieces are
-// placed with an XOR swizzle (16-byte slot = part ^ ((row >> 2) & 3)) instead
-// of row padding, so the 16 rows read by one ds_read_b128 lane group fall in
-// 16 distinct 4-bank groups.  Taps falling into padding load from a zero page.
+// placed with an XOR swizzle (16-byte slot = part ^ ((row >> 1) & 3)) instead
+// of row padding: for the fragment reads of v_mfma_i32_16x16x64_i8 (lane l
+// reads row l % 16, slot l / 16) this is the placement that gfx950's LDS
+// serves without bank conflicts (measured with SQ_LDS_BANK_CONFLICT; the
+// (row >> 2) and padded-row placements both conflict).  Taps falling into
+// padding load from a zero page.
 // kStages LDS buffers keep kStages - 1 steps of loads in flight; vmcnt tracks
 // the DMA completions and one barrier per step publishes a stage.
 // ---------------------------------------------------------------------------
 __device__ __attribute__((aligned(64))) int8_t g_conv_zero[64];
-constexpr int kStages = 4;
+#ifndef ISEG_IGEMM_STAGES
+#define ISEG_IGEMM_STAGES 3      // LDS stages of the direct-to-LDS implicit GEMM
+#endif
+constexpr int kStages = ISEG_IGEMM_STAGES;
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -361,7 +372,7 @@ __device__ __forceinline__ void wait_vm()
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-__device__ __forceinline__ int swz(int row, int part) { return row * 64 + ((part ^ ((row >> 2) & 3)) << 4); }
+__device__ __forceinline__ int swz(int row, int part) { return row * 64 + ((part ^ ((row >> 1) & 3)) << 4); }
 
 // row -> (image, output row, output column) in 32-bit arithmetic (Mrows < 2^31)
 __device__ __forceinline__ RowPix row_pix32(const IgemmArgs& a, int64_t m)
@@ -377,17 +388,35 @@ __device__ __forceinline__ RowPix row_pix32(const IgemmArgs& a, int64_t m)
     return rp;
 }
 
+// epilogues: raw int32 sums; int16 staging; tile max only (first pass of the
+// two-pass path); final SQ codes from the global max (second pass); int32
+// partial sums of one split of the reduction
+enum { EPI_RAW = 0, EPI_STAGE16 = 1, EPI_MAX = 2, EPI_Q8 = 3, EPI_PART = 4 };
+
+// wait until this wave's LDS reads have returned and at most n vector-memory
+// operations are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+}
+
 // Staging of the exact int32 sums as int16 with a per-tile right shift
 // t = max(0, bitlen(tile max) - 15): floor(acc / 2^t) fits int16, and since
 // the tensor's requant shift r = bitlen(max) - 7 is >= t + 1 whenever t > 0,
 // rounding floor(acc / 2^t) half-up by the remaining r - t bits gives the same
 // code as rounding acc by r (2^(r-1) is a multiple of 2^t, so the dropped low
 // bits can never carry into the rounding position).
-template <int MODE, int BN, bool OUT16>
+//
+// Pipeline: step kb's A/B fragments are read from LDS into registers one step
+// ahead, so the ds_reads of step kb + 1 run under the MFMAs of step kb; once a
+// step's fragments are in registers its LDS stage is free and receives the
+// DMA of step kb + kStages, which keeps kStages - 1 steps of loads in flight.
+template <int MODE, int BM, int BN, int EPI, bool PIPE>
 __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
 {
-    constexpr int BM = 128;
-    constexpr int WM = 64, WN = BN / 2;
+    constexpr int WM = BM / 2, WN = BN / 2;  // 2 x 2 waves
     constexpr int TM = WM / 16, TN = WN / 16;
     constexpr int NA = BM / 64;              // A instructions per wave and step (16 rows each)
     constexpr int NB = BN / 64;              // B instructions per wave and step
@@ -404,17 +433,21 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
     const int64_t m0 = (int64_t)bx * BM;
     const int n0 = blockIdx.y * BN;
     const int nchunk = a.Ci / BK;
-    const int nk = a.R * a.S * nchunk;
+    const int nk_all = a.R * a.S * nchunk;
+    // split of the reduction (blockIdx.z of gridDim.z): steps [kb0, kb0 + nk)
+    const int kb0 = (int)((int64_t)nk_all * blockIdx.z / gridDim.z);
+    const int nk = (int)((int64_t)nk_all * (blockIdx.z + 1) / gridDim.z) - kb0;
 
     // this lane's DMA pieces: row (16 * instr + lane / 4) in slot lane % 4
     const int rin = lane >> 2;
-    const int part = (lane & 3) ^ ((rin >> 2) & 3);
+    const int part = (lane & 3) ^ ((rin >> 1) & 3);
     RowPix rp[NA];
 #pragma unroll
     for (int j = 0; j < NA; j++) rp[j] = row_pix32(a, m0 + 16 * (wave + 4 * j) + rin);
     const int8_t* brow[NB];
 #pragma unroll
-    for (int j = 0; j < NB; j++) brow[j] = a.wmat + (int64_t)(n0 + 16 * (wave + 4 * j) + rin) * a.Kred + part * 16;
+    for (int j = 0; j < NB; j++)
+        brow[j] = a.wmat + (int64_t)(n0 + 16 * (wave + 4 * j) + rin) * a.Kred + (int64_t)kb0 * BK + part * 16;
 
     int64_t soff[NA];
     auto set_tap = [&](int tap) {
@@ -425,8 +458,8 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
             soff[j] = sp < 0 ? -1 : sp * a.Ci + part * 16;
         }
     };
-    int ltap = 0, lcc = 0;                    // step being issued
-    auto issue = [&](int kb) {
+    int ltap = kb0 / nchunk, lcc = kb0 - (kb0 / nchunk) * nchunk;   // step being issued
+    auto issue = [&](int kb) {               // kb: step within this split
         int8_t* st = smem + (kb % kStages) * (SA + SB);
 #pragma unroll
         for (int j = 0; j < NA; j++) {
@@ -446,35 +479,101 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
 #pragma unroll
         for (int j = 0; j < TN; j++) acc[i][j] = (v4i){0, 0, 0, 0};
 
-    set_tap(0);
-#pragma unroll
-    for (int p = 0; p < kStages - 1; p++)
-        if (p < nk) issue(p);
-    for (int kb = 0; kb < nk; kb++) {
-        const int ahead = nk - 1 - kb;         // steps issued after kb (at most kStages - 2)
-        if (ahead >= 2) wait_vm<2 * LPW>();
-        else if (ahead == 1) wait_vm<LPW>();
-        else wait_vm<0>();
-        // a plain barrier: __syncthreads() would also drain every DMA in flight
-        __builtin_amdgcn_s_barrier();
-        if (kb + kStages - 1 < nk) issue(kb + kStages - 1);
+    auto frags = [&](int kb, v4i* fa, v4i* fb) {
         const int8_t* A = smem + (kb % kStages) * (SA + SB);
         const int8_t* B = A + SA;
-        v4i fa[TM], fb[TN];
 #pragma unroll
         for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&A[swz(wm * WM + i * 16 + lrow, lpart)];
 #pragma unroll
         for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&B[swz(wn * WN + j * 16 + lrow, lpart)];
+        // keep the reads ahead of the MFMAs that follow (they run under them)
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto mma = [&](const v4i* fa, const v4i* fb) {
 #pragma unroll
         for (int i = 0; i < TM; i++)
 #pragma unroll
             for (int j = 0; j < TN; j++)
                 acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    };
+    // Every step slot issues LPW loads per wave (past the last step: loads of
+    // the zero page into the stage just freed), so the number of loads in
+    // flight behind any step is the same in every trip and one wait count fits.
+    auto issue_any = [&](int kb) {
+        if (kb < nk) {
+            issue(kb);
+        } else {
+            int8_t* st = smem + (kb % kStages) * (SA + SB);
+#pragma unroll
+            for (int j = 0; j < LPW; j++) dma16(g_conv_zero, st + (wave + 4 * j) * 1024);
+        }
+    };
+    // make step kb + 1 visible to every wave and free step kb's stage for the
+    // DMA of step kb + kStages (steps kb + 2 .. kb + kStages - 1 stay in flight)
+    static_assert(kStages >= 2 && (kStages - 1) * LPW < 64, "vmcnt range");
+    auto advance = [&](int kb) {
+        wait_vm_lgkm0<(kStages - 2) * LPW>();
+        // a plain barrier: __syncthreads() would also drain every DMA in flight
+        __builtin_amdgcn_s_barrier();
+        issue_any(kb + kStages);
+    };
+
+    if (nk > 0) set_tap(ltap);
+#pragma unroll
+    for (int p = 0; p < kStages; p++) issue_any(p);
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);
+    wait_vm<(kStages - 1) * LPW>();           // step 0 has landed
+    __builtin_amdgcn_s_barrier();
+    if (PIPE) {
+        // fragments one step ahead in registers: the ds_reads of step kb + 1
+        // are issued before the MFMAs of step kb
+        v4i fa[TM], fb[TN], na[TM], nb[TN];
+        if (nk > 0) frags(0, fa, fb);
+        for (int kb = 0; kb < nk; kb++) {
+            const bool more = kb + 1 < nk;
+            if (more) {
+                advance(kb);
+                frags(kb + 1, na, nb);
+            }
+            mma(fa, fb);
+            if (more) {
+#pragma unroll
+                for (int i = 0; i < TM; i++) fa[i] = na[i];
+#pragma unroll
+                for (int j = 0; j < TN; j++) fb[j] = nb[j];
+            }
+        }
+    } else {
+        // one fragment set: the other resident wave of the SIMD covers the
+        // LDS latency
+        v4i fa[TM], fb[TN];
+        for (int kb = 0; kb < nk; kb++) {
+            frags(kb, fa, fb);
+            mma(fa, fb);
+            if (kb + 1 < nk) advance(kb);
+        }
     }
+    wait_vm<0>();                             // the zero-page loads still in flight
 
     // rows of this block that exist (the last row tile may be ragged)
     const int vrows = a.Mrows - m0 < BM ? (int)(a.Mrows - m0) : BM;
-    if (!OUT16) {
+    if (EPI == EPI_PART) {
+        int32_t* out = a.out + (int64_t)blockIdx.z * a.Mrows * a.Nout;
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++) {
+                const int n = n0 + wn * WN + j * 16 + lrow;
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int row = wm * WM + i * 16 + lpart * 4 + e;
+                    if (row < vrows) out[(m0 + row) * a.Nout + n] = acc[i][j][e];
+                }
+            }
+        return;
+    }
+    if (EPI == EPI_RAW) {
         uint32_t mx = 0;
 #pragma unroll
         for (int i = 0; i < TM; i++)
@@ -495,8 +594,6 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
         if (a.pmax) block_store_max_u64(mx, a.pmax);
         return;
     }
-    // int16 staging: tile max -> shift, shifted tile through LDS, 16-byte stores
-    __shared__ uint32_t wmax[4];
     uint32_t mx = 0;
 #pragma unroll
     for (int i = 0; i < TM; i++)
@@ -509,6 +606,42 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
                 const uint32_t av = row < vrows ? (uint32_t)(v < 0 ? -v : v) : 0u;
                 mx = av > mx ? av : mx;
             }
+    if (EPI == EPI_MAX) {
+        block_store_max_u64(mx, a.pmax);
+        return;
+    }
+    if (EPI == EPI_Q8) {
+        // final SQ codes with r = bitlen(global max) - 7, staged through LDS
+        const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+        if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+        const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+        constexpr int RB8 = BN + 16;          // codes per LDS row (16-byte pad: bank spread)
+        __syncthreads();                      // every wave is done with the stage buffers
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++)
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int row = wm * WM + i * 16 + lpart * 4 + e;
+                    const int32_t x = acc[i][j][e];
+                    int32_t c = rq > 0 ? ((x >> rs) + 1) >> 1 : x << ls;
+                    c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                    smem[row * RB8 + wn * WN + j * 16 + lrow] = (int8_t)c;
+                }
+        __syncthreads();
+        constexpr int CPR = BN / 16;          // 16-byte chunks per row
+#pragma unroll
+        for (int k = 0; k < BM * CPR / 256; k++) {
+            const int c = tid + k * 256;
+            const int row = c / CPR, cc = c - (c / CPR) * CPR;
+            if (row < vrows)
+                *(int4*)(a.out8 + (m0 + row) * a.Nout + n0 + cc * 16) = *(const int4*)&smem[row * RB8 + cc * 16];
+        }
+        return;
+    }
+    // int16 staging: tile max -> shift, shifted tile through LDS, 16-byte stores
+    __shared__ uint32_t wmax[4];
     mx = wave_max_u32(mx);
     if (lane == 0) wmax[wave] = mx;
     __syncthreads();                          // also: every wave is done with the stage buffers
@@ -578,10 +711,6 @@ size_t halo_lds_bytes(int TW, int dh, int dw)
 {
     return (size_t)(kHaloTH + 2 * dh) * (TW + 2 * dw) * 64 + 9 * 64 * 64;
 }
-
-// epilogues: raw int32 sums; int16 staging; tile max only (first pass of the
-// two-pass path); final SQ codes from the global max (second pass)
-enum { EPI_RAW = 0, EPI_STAGE16 = 1, EPI_MAX = 2, EPI_Q8 = 3 };
 
 template <int TW, int EPI>
 __global__ __launch_bounds__(256) void k_conv3x3_halo(HaloArgs a)
@@ -1817,12 +1946,117 @@ bool igemm_dma_ok(const IgemmArgs& a)
     return a.Mrows > 0 && a.Mrows < ((int64_t)1 << 31) && a.Ci % 64 == 0 && a.Nout % 64 == 0 &&
            (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0;
 }
-int igemm_dma_bn(const IgemmArgs& a) { return a.Nout % 128 == 0 ? 128 : 64; }
 size_t staged_ws_bytes(int64_t rows, int64_t cols)
 {
     return align256((size_t)(rows * cols) * 2) + align256((size_t)(ceil_div64(rows, 128) * ceil_div64(cols, 64)));
 }
 
+// Direct-to-LDS GEMM plan.  Short reductions (Kred <= 256) with final codes
+// take two passes over 128-row tiles (max partials, then recomputed codes):
+// cheaper than staging when each output costs few MACs.  Otherwise ISEG_IGEMM_BM-row
+// tiles, with the reduction split over gridDim.z when the output tiles alone
+// would leave CUs idle and the reduction is long (at least 32 steps of 64 per
+// split: a split costs a reduce and an int32 requant pass).  256-row tiles
+// (ISEG_IGEMM_BM) cut LDS and L2 traffic per MAC by a quarter but need more
+// registers than two waves per SIMD allow; 128-row tiles measure faster.
+#ifndef ISEG_IGEMM_BM
+#define ISEG_IGEMM_BM 128
+#endif
+#ifndef ISEG_IGEMM_PIPE
+#define ISEG_IGEMM_PIPE 1
+#endif
+#ifndef ISEG_IGEMM_SPLIT_BLOCKS
+#define ISEG_IGEMM_SPLIT_BLOCKS 512       // split until this many blocks (0: never split)
+#endif
+constexpr int kTwoPassMaxKred = 256;
+constexpr int kMaxSplits = 8;
+struct DmaPlan {
+    bool two_pass;
+    int bm, bn, splits;
+};
+DmaPlan dma_plan(int64_t Mrows, int32_t Nout, int32_t Kred, bool q8)
+{
+    DmaPlan p;
+    p.bn = Nout % 128 == 0 ? 128 : 64;
+    p.two_pass = q8 && Kred <= kTwoPassMaxKred;
+    p.bm = (p.two_pass || Mrows < 256) ? 128 : ISEG_IGEMM_BM;
+    p.splits = 1;
+    if (q8 && !p.two_pass) {
+        const int64_t blocks = ceil_div64(Mrows, p.bm) * (Nout / p.bn);
+        const int nk = Kred / BK;
+        while (p.splits < kMaxSplits && blocks * p.splits < ISEG_IGEMM_SPLIT_BLOCKS && nk / (2 * p.splits) >= 32)
+            p.splits *= 2;
+    }
+    return p;
+}
+// int32 workspace of a plan beyond the int16 staging: split partials
+size_t dma_split_bytes(const DmaPlan& p, int64_t Mrows, int32_t Nout)
+{
+    return p.splits > 1 ? align256((size_t)p.splits * (size_t)Mrows * (size_t)Nout * 4) : 0;
+}
+
+template <int MODE, int BM, int BN, int EPI>
+int launch_dma_t(const IgemmArgs& a, int splits, hipStream_t s, int64_t* nblk)
+{
+    const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
+    dim3 grid((unsigned)ceil_div64(a.Mrows, BM), (unsigned)(a.Nout / BN), (unsigned)splits);
+    size_t lds = (size_t)kStages * (BM + BN) * 64;
+    const size_t epi_lds = EPI == EPI_STAGE16 ? (size_t)BM * (BN + 8) * 2 : EPI == EPI_Q8 ? (size_t)BM * (BN + 16) : 0;
+    lds = lds > epi_lds ? lds : epi_lds;
+    constexpr bool pipe = ISEG_IGEMM_PIPE != 0;
+    if (lds > 65536 && hipFuncSetAttribute((const void*)k_conv_igemm_dma<MODE, BM, BN, EPI, pipe>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return ISEG_ERR_DEVICE;
+    ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, BM, BN, EPI, pipe>), grid, dim3(256), lds, s, a);
+    *nblk = (int64_t)grid.x * grid.y;
+    return launch_ok();
+}
+
+template <int MODE, int BM, int BN>
+int launch_dma_e(const IgemmArgs& a, int epi, int splits, hipStream_t s, int64_t* nblk)
+{
+    switch (epi) {
+    case EPI_STAGE16: return launch_dma_t<MODE, BM, BN, EPI_STAGE16>(a, splits, s, nblk);
+    case EPI_MAX: return launch_dma_t<MODE, BM, BN, EPI_MAX>(a, splits, s, nblk);
+    case EPI_Q8: return launch_dma_t<MODE, BM, BN, EPI_Q8>(a, splits, s, nblk);
+    case EPI_PART: return launch_dma_t<MODE, BM, BN, EPI_PART>(a, splits, s, nblk);
+    default: return launch_dma_t<MODE, BM, BN, EPI_RAW>(a, splits, s, nblk);
+    }
+}
+
+template <int MODE>
+int launch_igemm_dma(const IgemmArgs& a, const DmaPlan& p, int epi, hipStream_t s, int64_t* nblk)
+{
+    if (p.bm == 256)
+        return p.bn == 128 ? launch_dma_e<MODE, 256, 128>(a, epi, p.splits, s, nblk)
+                           : launch_dma_e<MODE, 256, 64>(a, epi, p.splits, s, nblk);
+    return p.bn == 128 ? launch_dma_e<MODE, 128, 128>(a, epi, p.splits, s, nblk)
+                       : launch_dma_e<MODE, 128, 64>(a, epi, p.splits, s, nblk);
+}
+
+// sum of the split partials [splits][n] into out (in place allowed), with
+// per-block max |sum| partials
+__global__ __launch_bounds__(256) void k_splitk_reduce(const int32_t* part, int32_t splits, int64_t n,
+                                                       int32_t* out, uint64_t* pmax)
+{
+    uint32_t mx = 0;
+    const int64_t n4 = n >> 2;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+        int4 v = ((const int4*)part)[i];
+        for (int z = 1; z < splits; z++) {
+            const int4 w = ((const int4*)(part + (int64_t)z * n))[i];
+            v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+        }
+        ((int4*)out)[i] = v;
+        const uint32_t m01 = max((uint32_t)abs(v.x), (uint32_t)abs(v.y));
+        const uint32_t m23 = max((uint32_t)abs(v.z), (uint32_t)abs(v.w));
+        mx = max(mx, max(m01, m23));
+    }
+    if (pmax) block_store_max_u64(mx, pmax);
+}
+
+// int32 sums (+ per-block max partials) of any shape through the generic or
+// tap kernels (the direct-to-LDS kernel is driven by igemm_dma_run)
 template <int MODE>
 int launch_igemm(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
 {
@@ -1831,23 +2065,6 @@ int launch_igemm(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
         (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0) {
         const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
         unsigned gx = (unsigned)ceil_div64(a.Mrows, 128);
-        if (igemm_dma_ok(a)) {
-            const bool o16 = a.out16 != nullptr;
-            if (a.Nout % 128 == 0) {
-                dim3 grid(gx, (unsigned)(a.Nout / 128));
-                const size_t lds = kStages * (128 + 128) * 64;
-                if (o16) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 128, true>), grid, dim3(256), lds, s, a);
-                else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 128, false>), grid, dim3(256), lds, s, a);
-                *nblk = (int64_t)grid.x * grid.y;
-            } else {
-                dim3 grid(gx, (unsigned)(a.Nout / 64));
-                const size_t lds = kStages * (128 + 64) * 64;
-                if (o16) ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 64, true>), grid, dim3(256), lds, s, a);
-                else ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, 64, false>), grid, dim3(256), lds, s, a);
-                *nblk = (int64_t)grid.x * grid.y;
-            }
-            return launch_ok();
-        }
         if (a.Nout > 64) {
             dim3 grid(gx, (unsigned)ceil_div64(a.Nout, 128));
             ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_tap<MODE, 128, 128>), grid, dim3(256), 0, s, a);
@@ -1859,6 +2076,60 @@ int launch_igemm(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
         return launch_ok();
     }
     return launch_igemm_generic<MODE>(a, s, nblk);
+}
+
+__global__ void k_exp_sum(int32_t* out, const int32_t* a, const int32_t* b);
+
+// The whole direct-to-LDS path of a forward / backward-data conv (igemm_dma_ok
+// and a 16-byte aligned output): raw sums, or final codes by two passes,
+// split partials + reduce + requant, or int16 staging + requant.  `work` is
+// the int32 / staging region of the workspace, `pmax` its max partials.
+template <int MODE>
+int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t* exp_b, void* y,
+                  int32_t* y_exp, uint64_t* pmax, int32_t* work, hipStream_t s)
+{
+    const DmaPlan p = dma_plan(a.Mrows, a.Nout, a.Kred, out_mode == ISEG_OUT_Q8);
+    int rc;
+    int64_t nblk = 0;
+    a.out16 = nullptr;
+    a.tshift = nullptr;
+    if (out_mode == ISEG_OUT_RAW) {
+        a.out = (int32_t*)y;
+        a.pmax = nullptr;
+        if ((rc = launch_igemm_dma<MODE>(a, p, EPI_RAW, s, &nblk))) return rc;
+        hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, s, y_exp, exp_a, exp_b);
+        return launch_ok();
+    }
+    if (p.two_pass) {
+        a.pmax = pmax;
+        if ((rc = launch_igemm_dma<MODE>(a, p, EPI_MAX, s, &nblk))) return rc;
+        a.npmax = nblk;
+        a.out8 = (int8_t*)y; a.exp_a = exp_a; a.exp_b = exp_b; a.out_exp = y_exp;
+        return launch_igemm_dma<MODE>(a, p, EPI_Q8, s, &nblk);
+    }
+    const int64_t n = a.Mrows * a.Nout;
+    if (p.splits > 1) {
+        a.out = work;
+        a.pmax = nullptr;
+        if ((rc = launch_igemm_dma<MODE>(a, p, EPI_PART, s, &nblk))) return rc;
+        // as many reduce blocks as the max-partial region holds for 128 x 64 tiles
+        const int64_t cap = ceil_div64(a.Mrows, 128) * ceil_div64(a.Nout, 64);
+        int64_t nb = ceil_div64(n / 4, 256 * 4);
+        nb = nb < cap ? nb : cap;
+        nb = nb < 1 ? 1 : nb;
+        hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)nb), dim3(256), 0, s, work, (int32_t)p.splits, n, work,
+                           pmax);
+        if ((rc = launch_ok())) return rc;
+        return launch_requant_apply(work, ISEG_I32, n, exp_a, exp_b, 0, 8, 0, 1, 0, 0, 0, ISEG_I8, y, y_exp,
+                                    nullptr, s, pmax, nb);
+    }
+    a.out16 = (int16_t*)work;
+    a.tshift = (uint8_t*)work + align256((size_t)n * 2);
+    a.pmax = pmax;
+    if ((rc = launch_igemm_dma<MODE>(a, p, EPI_STAGE16, s, &nblk))) return rc;
+    StageMap sm{p.bm, p.bn, 0, 0, 0, 0, 0, 0};
+    return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, exp_a, exp_b, 8, (int8_t*)y, y_exp,
+                                   nullptr, s, pmax, nblk);
 }
 
 template <int MODE>
@@ -3001,6 +3272,9 @@ extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
         size_t big = align256((size_t)(g->N * P * Q * g->K) * 4);
         const size_t s16 = staged_ws_bytes(g->N * P * Q, g->K);
         big = big > s16 ? big : s16;
+        const DmaPlan dp = dma_plan(g->N * P * Q, (int32_t)g->K, (int32_t)(padded_c(g->C) * g->R * g->S), true);
+        const size_t sk = dma_split_bytes(dp, g->N * P * Q, (int32_t)g->K);
+        big = big > sk ? big : sk;
         const HaloPlan hp = halo_plan(g->N, P, Q, g->C, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
                                       g->dil_h, g->dil_w);
         if (hp.ok) {
@@ -3042,6 +3316,9 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         size_t big = align256((size_t)(g->N * P * Q * g->K) * 4);
         const size_t s16 = staged_ws_bytes(g->N * P * Q, g->K);
         big = big > s16 ? big : s16;
+        const DmaPlan dp = dma_plan(g->N * P * Q, (int32_t)g->K, (int32_t)(Cp * g->R * g->S), true);
+        const size_t sk = dma_split_bytes(dp, g->N * P * Q, (int32_t)g->K);
+        big = big > sk ? big : sk;
         if (hp.ok) {
             const size_t sh = halo_staged_ws_bytes(hp, g->N, P, Q, g->K);
             big = big > sh ? big : sh;
@@ -3079,7 +3356,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         xs = xp;
         wsrc = wpd;
     }
-    IgemmArgs a;
+    IgemmArgs a{};
     a.src = xs; a.wmat = wsrc; a.out = acc; a.pmax = pmax;
     a.out16 = nullptr; a.tshift = nullptr;
     a.Mrows = g->N * P * Q;
@@ -3133,21 +3410,13 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         }
         return halo_q8(hp, h, ISEG_KID_CONV_FWD, x_exp, w_exp, (int8_t*)y, y_exp, maxp, pmax, a.Mrows, stream);
     }
-    const bool staged = out_mode == ISEG_OUT_Q8 && igemm_dma_ok(a) && ((uintptr_t)y & 15) == 0;
-    if (staged) {
-        a.out16 = (int16_t*)acc;
-        a.tshift = (uint8_t*)acc + align256((size_t)(a.Mrows * a.Nout) * 2);
-    }
+    if (igemm_dma_ok(a) && ((uintptr_t)y & 15) == 0)
+        return igemm_dma_run<MODE_FWD>(a, out_mode, x_exp, w_exp, y, y_exp, pmax, acc, stream);
     int64_t nblk = 0;
     if ((rc = launch_igemm<MODE_FWD>(a, stream, &nblk))) return rc;
     if (out_mode == ISEG_OUT_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
         return launch_ok();
-    }
-    if (staged) {
-        StageMap sm{128, igemm_dma_bn(a), 0, 0, 0, 0, 0, 0};
-        return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, x_exp, w_exp, 8, (int8_t*)y, y_exp,
-                                       nullptr, stream, pmax, nblk);
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, x_exp, w_exp, 0, 8, 0, 1,
                                 0, 0, 0, ISEG_I8, y, y_exp, nullptr, stream, pmax, nblk);
@@ -3162,6 +3431,9 @@ extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mod
         size_t big = align256((size_t)(g->N * g->H * g->W * g->C) * 4);
         const size_t s16 = staged_ws_bytes(g->N * g->H * g->W, g->C);
         big = big > s16 ? big : s16;
+        const DmaPlan dp = dma_plan(g->N * g->H * g->W, (int32_t)g->C, (int32_t)(g->K * g->R * g->S), true);
+        const size_t sk = dma_split_bytes(dp, g->N * g->H * g->W, (int32_t)g->C);
+        big = big > sk ? big : sk;
         const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h,
                                       g->stride_w, g->dil_h, g->dil_w);
         if (hp.ok) {
@@ -3264,7 +3536,7 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     hipLaunchKernelGGL(k_w_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
                        (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
     if ((rc = launch_ok())) return rc;
-    IgemmArgs a;
+    IgemmArgs a{};
     a.src = dy; a.wmat = wt; a.out = acc; a.pmax = pmax;
     a.out16 = nullptr; a.tshift = nullptr;
     a.Mrows = g->N * g->H * g->W;
@@ -3273,21 +3545,13 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     a.R = (int32_t)g->R; a.S = (int32_t)g->S;
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
-    const bool staged = out_mode == ISEG_OUT_Q8 && igemm_dma_ok(a) && ((uintptr_t)dx & 15) == 0;
-    if (staged) {
-        a.out16 = (int16_t*)acc;
-        a.tshift = (uint8_t*)acc + align256((size_t)(a.Mrows * a.Nout) * 2);
-    }
+    if (igemm_dma_ok(a) && ((uintptr_t)dx & 15) == 0)
+        return igemm_dma_run<MODE_BWD>(a, out_mode, dy_exp, w_exp, dx, dx_exp, pmax, acc, stream);
     int64_t nblk = 0;
     if ((rc = launch_igemm<MODE_BWD>(a, stream, &nblk))) return rc;
     if (out_mode == ISEG_OUT_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
         return launch_ok();
-    }
-    if (staged) {
-        StageMap sm{128, igemm_dma_bn(a), 0, 0, 0, 0, 0, 0};
-        return launch_requant_staged16(a.out16, a.tshift, a.Mrows, a.Nout, sm, dy_exp, w_exp, 8, (int8_t*)dx,
-                                       dx_exp, nullptr, stream, pmax, nblk);
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, dy_exp, w_exp, 0, 8, 0, 1,
                                 0, 0, 0, ISEG_I8, dx, dx_exp, nullptr, stream, pmax, nblk);

@@ -100,6 +100,13 @@ CONV_SHAPES = [
     (1, 5, 5, 20, 21, 1, 1, 0, 1),        # C % 16 != 0, K = 21
     (1, 21, 19, 64, 64, 3, 1, 2, 2),      # dilation 2 on the 64-channel paths
     (4, 9, 7, 64, 128, 3, 1, 1, 1),       # narrow rows: pixel runs wrap rows and images
+    # direct-to-LDS implicit GEMM: two-pass codes for reductions <= 256
+    # (1, 2, 3 steps of 64), int16 staging above (odd and even step counts)
+    (1, 13, 11, 128, 64, 1, 1, 0, 1),
+    (1, 12, 10, 192, 128, 1, 1, 0, 1),
+    (2, 9, 10, 320, 64, 1, 1, 0, 1),
+    (1, 18, 17, 128, 128, 3, 1, 6, 6),    # atrous 6: 18 steps, padding-only taps
+    (1, 11, 13, 64, 128, 3, 1, 3, 3),     # dilation 3: 9 steps
 ]
 
 
@@ -169,6 +176,52 @@ def test_conv_bwd_weight_long_reduction(orc, dev):
                                   1, 0, 1, g_mode=iseg.ISEG_G_RAW)
     ref = orc.conv_bwd_weight_raw(dy, x, (3, 220, 220, 4, 4, 1, 1, 1, 1, 0, 0, 1, 1))
     assert np.array_equal(H(raw), ref)
+
+
+# Full-size shapes of the DeepLabv3 step whose reduction is split across
+# blocks (ASPP 3x3 branches) or tiled without a split: raw int32 sums at
+# sampled output pixels against exact integer dot products, and the final
+# codes against the requant of those sums under the exponent the kernel chose.
+FULL_SHAPES = [
+    (8, 32, 32, 2048, 256, 3, 1, 6, 6),
+    (8, 32, 32, 2048, 256, 3, 1, 18, 18),
+    (8, 32, 32, 1024, 2048, 1, 1, 0, 1),
+]
+
+
+def _sampled_conv_ref(x, w, s, pix):
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    out = []
+    for (n, p, q) in pix:
+        acc = np.zeros(K, np.int64)
+        for r in range(R):
+            for t in range(R):
+                ih, iw = p * st - pad + r * d, q * st - pad + t * d
+                if 0 <= ih < Hh and 0 <= iw < W:
+                    acc += w[:, r, t, :].astype(np.int64) @ x[n, ih, iw, :].astype(np.int64)
+        out.append(acc)
+    return np.stack(out)
+
+
+@pytest.mark.parametrize("s", FULL_SHAPES, ids=str)
+def test_conv_fwd_full_size_sampled(orc, dev, s):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    x = synth.int_codes(91, (N, Hh, W, Cc))
+    w = synth.int_codes(92, (K, R, R, Cc))
+    raw, _ = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d,
+                           out_mode=iseg.ISEG_OUT_RAW)
+    y, ye = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d)
+    rng = synth.rng(93)
+    pix = [(int(rng.integers(N)), int(rng.integers(Hh)), int(rng.integers(W))) for _ in range(24)]
+    pix += [(0, 0, 0), (N - 1, Hh - 1, W - 1), (3, 0, W - 1)]
+    ref = _sampled_conv_ref(x, w, s, pix)
+    R_ = H(raw)
+    got = np.stack([R_[n, p, q] for (n, p, q) in pix]).astype(np.int64)
+    assert np.array_equal(got, ref)
+    # codes: the requant of the full raw tensor (checked above at the samples)
+    rc, rce = orc.requant(R_.astype(np.int64), -14, 8)
+    assert ev(ye) == rce and np.array_equal(H(y).astype(np.int64), rc)
 
 
 def test_conv_zero_input(orc, dev):
