@@ -2,7 +2,9 @@
 //
 // Exact integer arithmetic (bit lengths, floor division, half-up rounding of
 // rationals scaled by powers of two), the Philox4x32-10 block, 64-wide wave
-// reductions and the small launch helpers.  Nothing here is float.
+// reductions and the small launch helpers.  The one use of floating point is a
+// quotient estimate inside floordiv128 that an integer remainder check makes
+// exact.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -30,14 +32,27 @@ ISEG_HD i128 abs128(i128 v) { return v < 0 ? -v : v; }
 ISEG_HD int bitlen_i128(i128 v) { return bitlen_u128((u128)abs128(v)); }
 ISEG_HD i128 pow2_128(int e) { return (i128)1 << e; }
 
-// floor(a / b) for b > 0; operands that fit 64 bits take the 64-bit divide
-// (a 128-bit divide is a long software loop on the GPU)
+// double of an i128 up to two roundings of its magnitude (relative error
+// < 2^-51; the halves of |v| are both non-negative, so nothing cancels)
+ISEG_HD double i128_to_double(i128 v)
+{
+    const u128 m = (u128)(v < 0 ? -v : v);
+    const double d = (double)(uint64_t)(m >> 64) * 18446744073709551616.0 + (double)(uint64_t)m;
+    return v < 0 ? -d : d;
+}
+
+// floor(a / b) for b > 0, exact.  When |a| / b < 2^48 (bit lengths differ by
+// less than 48) the double quotient is off the true one by less than 0.2, so
+// its floor is within one of floor(a / b) and the integer remainder check
+// settles it; only larger quotients take the software 128-bit divide (a long
+// loop on the GPU, which has no integer divide instruction).
 ISEG_HD i128 floordiv128(i128 a, i128 b)
 {
-    if (a == (i128)(int64_t)a && b == (i128)(int64_t)b) {
-        const int64_t x = (int64_t)a, y = (int64_t)b;
-        int64_t q = x / y;
-        if (x % y != 0 && x < 0) q -= 1;
+    if (bitlen_i128(a) - bitlen_i128(b) < 48) {
+        i128 q = (i128)(int64_t)floor(i128_to_double(a) / i128_to_double(b));
+        i128 r = a - q * b;
+        for (int i = 0; i < 2 && r < 0; i++) { q -= 1; r += b; }
+        for (int i = 0; i < 2 && r >= b; i++) { q += 1; r -= b; }
         return q;
     }
     i128 q = a / b;

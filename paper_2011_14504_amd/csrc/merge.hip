@@ -24,6 +24,7 @@ struct MergeArgs {
     const int32_t* e[kMaxIn];
     int32_t add[kMaxIn];
     int32_t bc[kMaxIn];            // 1: [N,1,1,C] input broadcast over HW
+    int32_t any_bc;                // some input is broadcast (its element index needs (n, c))
     int32_t n_in;
     int64_t n, HW, C;
     int32_t relu, bits;
@@ -75,20 +76,29 @@ __device__ __forceinline__ void merge_sum16(const MergeArgs& a, const int* sh, i
     }
 }
 
-// the 16-byte vectors of every input for output vector v (v < nv)
+// the 16-byte vectors of every input for output vector v (v < nv); the
+// (image, channel) split of the element index only when an input is broadcast
 template <int NIN>
 __device__ __forceinline__ void merge_load16(const MergeArgs& a, int64_t v, int64_t nv, int4* raw)
 {
     if (v >= nv) return;
     const int64_t j = v * 16;
+    if (!a.any_bc) {
+#pragma unroll
+        for (int i = 0; i < NIN; i++) raw[i] = *(const int4*)(a.p[i] + j);
+        return;
+    }
     const int64_t img = j / (a.HW * a.C);
     const int64_t c = j % a.C;
 #pragma unroll
     for (int i = 0; i < NIN; i++) raw[i] = *(const int4*)(a.p[i] + (a.bc[i] ? img * a.C + c : j));
 }
 
-template <int NIN>
-__device__ __forceinline__ void merge_sum16_raw(const MergeArgs& a, const int* sh, const int4* raw, int64_t* s)
+// exact sums of 16 elements on the grid 2^e0 in T: int32 when every shift is
+// at most kW32Shift (eight int8 terms stay below 2^31), else int64
+constexpr int kW32Shift = 20;
+template <int NIN, typename T>
+__device__ __forceinline__ void merge_sum16_raw(const MergeArgs& a, const int* sh, const int4* raw, T* s)
 {
 #pragma unroll
     for (int t = 0; t < 16; t++) s[t] = 0;
@@ -96,12 +106,27 @@ __device__ __forceinline__ void merge_sum16_raw(const MergeArgs& a, const int* s
     for (int i = 0; i < NIN; i++) {
         const int32_t w[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
 #pragma unroll
-        for (int t = 0; t < 16; t++) s[t] += (int64_t)(int8_t)(w[t >> 2] >> (8 * (t & 3))) << sh[i];
+        for (int t = 0; t < 16; t++) s[t] += (T)(int8_t)(w[t >> 2] >> (8 * (t & 3))) << sh[i];
     }
     if (a.relu) {
 #pragma unroll
         for (int t = 0; t < 16; t++) s[t] = s[t] > 0 ? s[t] : 0;
     }
+}
+
+// SQ code of an int32 on a given shift (r <= 0 only when max |q| < 2^(k-1))
+__device__ __forceinline__ int32_t sq_code32(int32_t q, int r, int k)
+{
+    const int32_t lim = (1 << (k - 1)) - 1;
+    const int32_t v = r > 0 ? (q + (1 << (r - 1))) >> r : q << -r;
+    return v > lim ? lim : (v < -lim ? -lim : v);
+}
+
+__device__ __forceinline__ int max_shift(const MergeArgs& a, const int* sh)
+{
+    int m = 0;
+    for (int i = 0; i < a.n_in; i++) m = sh[i] > m ? sh[i] : m;
+    return m;
 }
 
 __device__ __forceinline__ int64_t merge_sum1(const MergeArgs& a, const int* sh, int64_t j)
@@ -127,6 +152,8 @@ __global__ __launch_bounds__(256) void k_merge_max(MergeArgs a)
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (VEC && NIN > 0) {
         const int64_t nv = a.n / 16;
+        const bool w32 = max_shift(a, sh) <= kW32Shift;
+        uint32_t m32 = 0;
         for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
             int4 raw[kU][NIN > 0 ? NIN : 1];
 #pragma unroll
@@ -134,15 +161,23 @@ __global__ __launch_bounds__(256) void k_merge_max(MergeArgs a)
 #pragma unroll
             for (int u = 0; u < kU; u++) {
                 if (v0 + u * stride >= nv) break;
-                int64_t s[16];
-                merge_sum16_raw<NIN>(a, sh, raw[u], s);
+                if (w32) {
+                    int32_t s[16];
+                    merge_sum16_raw<NIN>(a, sh, raw[u], s);
 #pragma unroll
-                for (int t = 0; t < 16; t++) {
-                    const uint64_t w = (uint64_t)(s[t] < 0 ? -s[t] : s[t]);
-                    m = w > m ? w : m;
+                    for (int t = 0; t < 16; t++) m32 = max(m32, (uint32_t)abs(s[t]));
+                } else {
+                    int64_t s[16];
+                    merge_sum16_raw<NIN>(a, sh, raw[u], s);
+#pragma unroll
+                    for (int t = 0; t < 16; t++) {
+                        const uint64_t w = (uint64_t)(s[t] < 0 ? -s[t] : s[t]);
+                        m = w > m ? w : m;
+                    }
                 }
             }
         }
+        m = m > m32 ? m : m32;
     } else if (VEC) {
         for (int64_t v = t0; v < a.n / 16; v += stride) {
             int64_t s[16];
@@ -175,6 +210,7 @@ __global__ __launch_bounds__(256) void k_merge_apply(MergeArgs a, int64_t nparts
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (VEC && NIN > 0) {
         const int64_t nv = a.n / 16;
+        const bool w32 = max_shift(a, sh) <= kW32Shift;
         for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
             int4 raw[kU][NIN > 0 ? NIN : 1];
 #pragma unroll
@@ -183,12 +219,20 @@ __global__ __launch_bounds__(256) void k_merge_apply(MergeArgs a, int64_t nparts
             for (int u = 0; u < kU; u++) {
                 const int64_t v = v0 + u * stride;
                 if (v >= nv) break;
-                int64_t s[16];
-                merge_sum16_raw<NIN>(a, sh, raw[u], s);
                 uint32_t w[4] = {0, 0, 0, 0};
+                if (w32) {
+                    int32_t s[16];
+                    merge_sum16_raw<NIN>(a, sh, raw[u], s);
 #pragma unroll
-                for (int t = 0; t < 16; t++)
-                    w[t >> 2] |= (uint32_t)(uint8_t)sq_code(s[t], r, a.bits) << (8 * (t & 3));
+                    for (int t = 0; t < 16; t++)
+                        w[t >> 2] |= (uint32_t)(uint8_t)sq_code32(s[t], r, a.bits) << (8 * (t & 3));
+                } else {
+                    int64_t s[16];
+                    merge_sum16_raw<NIN>(a, sh, raw[u], s);
+#pragma unroll
+                    for (int t = 0; t < 16; t++)
+                        w[t >> 2] |= (uint32_t)(uint8_t)sq_code(s[t], r, a.bits) << (8 * (t & 3));
+                }
                 *(int4*)(a.out + v * 16) = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
             }
         }
@@ -217,6 +261,7 @@ __global__ __launch_bounds__(256) void k_relu_mask(MergeArgs a, const int8_t* __
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (VEC && NIN > 0) {
         const int64_t nv = a.n / 16;
+        const bool w32 = max_shift(a, sh) <= kW32Shift;
         for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
           int4 raw[kU][NIN > 0 ? NIN : 1], dr[kU];
 #pragma unroll
@@ -228,14 +273,22 @@ __global__ __launch_bounds__(256) void k_relu_mask(MergeArgs a, const int8_t* __
           for (int u = 0; u < kU; u++) {
             const int64_t v = v0 + u * stride;
             if (v >= nv) break;
-            int64_t s[16];
-            merge_sum16_raw<NIN>(a, sh, raw[u], s);
             const int4 d = dr[u];
             const uint32_t dw[4] = {(uint32_t)d.x, (uint32_t)d.y, (uint32_t)d.z, (uint32_t)d.w};
             uint32_t w[4] = {0, 0, 0, 0};
+            if (w32) {
+                int32_t s[16];
+                merge_sum16_raw<NIN>(a, sh, raw[u], s);
 #pragma unroll
-            for (int t = 0; t < 16; t++)
-                if (s[t] > 0) w[t >> 2] |= dw[t >> 2] & (0xffu << (8 * (t & 3)));
+                for (int t = 0; t < 16; t++)
+                    if (s[t] > 0) w[t >> 2] |= dw[t >> 2] & (0xffu << (8 * (t & 3)));
+            } else {
+                int64_t s[16];
+                merge_sum16_raw<NIN>(a, sh, raw[u], s);
+#pragma unroll
+                for (int t = 0; t < 16; t++)
+                    if (s[t] > 0) w[t >> 2] |= dw[t >> 2] & (0xffu << (8 * (t & 3)));
+            }
             *(int4*)(a.out + v * 16) = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
           }
         }
@@ -513,6 +566,8 @@ bool fill_merge_inputs(MergeArgs& m, int32_t n_in, const int8_t* const* in, cons
         m.bc[i] = bcast ? (bcast[i] != 0) : 0;
         if (m.add[i] < -256 || m.add[i] > 256) return false;
     }
+    m.any_bc = 0;
+    for (int i = 0; i < n_in; i++) m.any_bc |= m.bc[i];
     return true;
 }
 

@@ -50,6 +50,9 @@ SUM_CASES = [
     ((1, 1, 1, 3), (-3, -12), True, False),        # tiny
     ((2, 8, 8, 32), (-20, -30), False, True),      # error sum with a pooled term
     ((4, 13, 3, 48), (-11, -11), False, False),
+    ((2, 5, 6, 32), (-3, -40), True, False),       # gap 37: 64-bit sums
+    ((1, 4, 4, 16), (-10, -31), False, False),     # gap 21: just past the int32 path
+    ((1, 4, 4, 16), (-10, -30), True, False),      # gap 20: the widest int32 case
 ]
 
 
@@ -90,16 +93,17 @@ def test_sum_requant_all_zero_and_gap_flag(orc, dev):
     assert ev(st) & iseg.ISEG_DEV_RANGE
 
 
-@pytest.mark.parametrize("shape", [(2, 9, 7, 64), (1, 5, 3, 24)], ids=str)
-def test_relu_mask_bwd(orc, dev, shape):
+@pytest.mark.parametrize("shape,exps", [((2, 9, 7, 64), (-8, -7)), ((1, 5, 3, 24), (-8, -7)),
+                                        ((2, 6, 6, 32), (-2, -36))], ids=str)
+def test_relu_mask_bwd(orc, dev, shape, exps):
     from paper_2011_14504_amd import iseg
     a = _codes(30, shape)
     b = _codes(31, shape)
     a[0, 0, :2, :] = 0
     b[0, 0, :2, :] = 0
     dy = _codes(32, shape)
-    d = iseg.relu_mask_bwd(T(dy, dev), [T(a, dev), T(b, dev)], [E(-8, dev), E(-7, dev)])
-    assert np.array_equal(H(d), orc.relu_mask_bwd(dy, [a, b], [-8, -7]))
+    d = iseg.relu_mask_bwd(T(dy, dev), [T(a, dev), T(b, dev)], [E(exps[0], dev), E(exps[1], dev)])
+    assert np.array_equal(H(d), orc.relu_mask_bwd(dy, [a, b], list(exps)))
 
 
 CAT_CASES = [
