@@ -1529,15 +1529,13 @@ int launch_m32_t(const M32Plan& p, const HaloArgs& a, int kid, hipStream_t s)
 {
     if (p.persist) {
         dim3 grid((unsigned)p.G, (unsigned)(a.Nout / 64));
-        if (hipFuncSetAttribute((const void*)k_conv3x3_m32p<DH, DW, EPI>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.plds) != hipSuccess)
+        if (!lds_limit((const void*)k_conv3x3_m32p<DH, DW, EPI>, (size_t)p.plds))
             return ISEG_ERR_DEVICE;
         ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_m32p<DH, DW, EPI>), grid, dim3(256), p.plds, s, a);
         return launch_ok();
     }
     dim3 grid((unsigned)(a.N * p.tiles_y * p.tiles_x), (unsigned)(a.Nout / 64));
-    if (hipFuncSetAttribute((const void*)k_conv3x3_m32<DH, DW, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)p.lds) != hipSuccess)
+    if (!lds_limit((const void*)k_conv3x3_m32<DH, DW, EPI>, (size_t)p.lds))
         return ISEG_ERR_DEVICE;
     ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_m32<DH, DW, EPI>), grid, dim3(256), p.lds, s, a);
     return launch_ok();
@@ -1803,8 +1801,7 @@ template <int TW, int EPI>
 int launch_persist_t(const PersistPlan& p, const HaloArgs& a, int kid, hipStream_t s)
 {
     dim3 grid((unsigned)p.G, (unsigned)(a.Nout / 64));
-    if (hipFuncSetAttribute((const void*)k_conv3x3_persist<TW, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)p.lds) != hipSuccess)
+    if (!lds_limit((const void*)k_conv3x3_persist<TW, EPI>, (size_t)p.lds))
         return ISEG_ERR_DEVICE;
     ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_persist<TW, EPI>), grid, dim3(256), p.lds, s, a);
     return launch_ok();
@@ -1887,8 +1884,7 @@ template <int TW, int EPI>
 int launch_halo_t(const HaloPlan& p, const HaloArgs& a, int kid, hipStream_t s)
 {
     dim3 grid((unsigned)(a.N * p.tiles_y * p.tiles_x), (unsigned)(a.Nout / 64));
-    if (hipFuncSetAttribute((const void*)k_conv3x3_halo<TW, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)p.lds) != hipSuccess)
+    if (!lds_limit((const void*)k_conv3x3_halo<TW, EPI>, (size_t)p.lds))
         return ISEG_ERR_DEVICE;
     ISEG_TIMED_LAUNCH(kid, s, (k_conv3x3_halo<TW, EPI>), grid, dim3(256), p.lds, s, a);
     return launch_ok();
@@ -2004,8 +2000,7 @@ int launch_dma_t(const IgemmArgs& a, int splits, hipStream_t s, int64_t* nblk)
     const size_t epi_lds = EPI == EPI_STAGE16 ? (size_t)BM * (BN + 8) * 2 : EPI == EPI_Q8 ? (size_t)BM * (BN + 16) : 0;
     lds = lds > epi_lds ? lds : epi_lds;
     constexpr bool pipe = ISEG_IGEMM_PIPE != 0;
-    if (lds > 65536 && hipFuncSetAttribute((const void*)k_conv_igemm_dma<MODE, BM, BN, EPI, pipe>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    if (lds > 65536 && !lds_limit((const void*)k_conv_igemm_dma<MODE, BM, BN, EPI, pipe>, lds))
         return ISEG_ERR_DEVICE;
     ISEG_TIMED_LAUNCH(kid, s, (k_conv_igemm_dma<MODE, BM, BN, EPI, pipe>), grid, dim3(256), lds, s, a);
     *nblk = (int64_t)grid.x * grid.y;
@@ -3109,8 +3104,7 @@ int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax
     int64_t splits = wgrad_taps_splits(a.NPQ, a.K, a.C, &a.pix_per_split);
     const size_t lds = (size_t)(2 + 2 * RS) * BK * 80;
     if (RS != 9) return ISEG_ERR_UNSUPPORTED;
-    if (hipFuncSetAttribute((const void*)k_conv_wgrad_taps<9>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
+    if (!lds_limit((const void*)k_conv_wgrad_taps<9>, lds))
         return ISEG_ERR_DEVICE;
     dim3 grid((unsigned)((a.C / 64) * (a.K / 64)), (unsigned)splits);
     ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, k_conv_wgrad_taps<9>, grid, dim3(64 * 9), lds, s, a, part);

@@ -284,6 +284,8 @@ int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* m
                   int32_t* dev_status, hipStream_t s);
 
 int launch_fill_u32(void* p, int64_t n_words, uint32_t v, hipStream_t s);
+// raise a kernel's dynamic LDS limit (cached per device and kernel)
+bool lds_limit(const void* f, size_t bytes);
 // *maxp = max over n block partials (one block)
 int launch_reduce_max(const uint64_t* part, int64_t n, unsigned long long* maxp, hipStream_t s);
 

@@ -422,8 +422,7 @@ __global__ __launch_bounds__(256) void k_ce_quant(const CeCellArgs a, int64_t np
 template <int KT>
 int launch_cells(const CeCellArgs& a, size_t lds, hipStream_t s)
 {
-    if (hipFuncSetAttribute((const void*)k_ce_cells<KT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-        hipSuccess)
+    if (!lds_limit((const void*)k_ce_cells<KT>, lds))
         return ISEG_ERR_DEVICE;
     hipLaunchKernelGGL(k_ce_cells<KT>, dim3((unsigned)a.nrx, (unsigned)a.nry, (unsigned)a.N), dim3(256), lds, s, a);
     return launch_ok();

@@ -126,8 +126,23 @@ def _ptr(t):
     return None if t is None else C.c_void_p(t.data_ptr())
 
 
+_raw_stream = torch._C._cuda_getCurrentRawStream if hasattr(torch._C, "_cuda_getCurrentRawStream") else None
+_raw_device = torch._C._cuda_getDevice if hasattr(torch._C, "_cuda_getDevice") else torch.cuda.current_device
+
+
+def _stream_handle(dev_index=None):
+    """Raw handle of the current stream of a device (the current device by
+    default): the launch path asks for it on every call, so it bypasses the
+    Stream object construction of torch.cuda.current_stream()."""
+    if dev_index is None:
+        dev_index = _raw_device()
+    if _raw_stream is not None:
+        return _raw_stream(dev_index)
+    return torch.cuda.current_stream(dev_index).cuda_stream
+
+
 def _stream():
-    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    return C.c_void_p(_stream_handle())
 
 
 def _check(rc, name):
@@ -394,7 +409,7 @@ def _maybe_arm(kid, key):
 # --------------------------------------------------------------------------
 class Workspace:
     """A growable device scratch buffer shared by consecutive calls on one
-    stream (stream order keeps the uses apart)."""
+    stream (stream order keeps the uses apart); each stream has its own."""
 
     def __init__(self, device="cuda"):
         self.device = device
@@ -411,13 +426,16 @@ _WS = {}
 
 
 def workspace(device):
-    d = torch.device(device)
-    if d.type == "cuda" and d.index is None:
-        d = torch.device("cuda", torch.cuda.current_device())
-    key = str(d)
-    if key not in _WS:
-        _WS[key] = Workspace(d)
-    return _WS[key]
+    d = device if isinstance(device, torch.device) else torch.device(device)
+    if d.type == "cuda":
+        idx = d.index if d.index is not None else _raw_device()
+        key = (idx, _stream_handle(idx))
+    else:
+        idx, key = None, (str(d), 0)
+    ws = _WS.get(key)
+    if ws is None:
+        ws = _WS[key] = Workspace(torch.device("cuda", idx) if d.type == "cuda" else d)
+    return ws
 
 
 def _out_exp(device):

@@ -36,6 +36,10 @@ class IntNet:
         self.cfg = dict(iseg.BN_DEFAULT, **(bn_cfg or {}))
         self._cfgs = {r: iseg.bn_cfg(**dict(self.cfg, relu=r)) for r in (0, 1)}
         self.step_no = 0
+        # backward-weight runs on a second stream (default priority): each
+        # conv's weight gradient only needs its dz and input, so it overlaps
+        # the backward-data / L1BN / merge chain of the layers below
+        self.side = torch.cuda.Stream(device=self.dev) if self.dev.type == "cuda" else None
         self.x = torch.from_numpy(inputs["x"]).to(self.dev)
         self.x_exp = iseg.new_exp(self.dev, inputs["x_exp"])
         self.dy = self.labels = None
@@ -172,10 +176,7 @@ class IntNet:
                     r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
                 else:
                     dz, dze = e, ee
-                G, Ge = iseg.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape,
-                                             nd["stride"], nd["pad"], nd["dil"], iseg.ISEG_G_KEEP, 8,
-                                             self.seed, 16 * L["l"], self.step_no,
-                                             out=(L["G"], L["G_exp"]))
+                G, Ge = self._wgrad(nd, L, r, dz, dze)
                 r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
                 grads.append((nd, r))
                 if need_in:
@@ -213,7 +214,24 @@ class IntNet:
         if want_input:
             e, ee = merged("input")
             rec["input"] = dict(kind="input", e_out=e, e_out_exp=ee)
+        if self.side is not None:
+            torch.cuda.current_stream(self.dev).wait_stream(self.side)
         return grads
+
+    def _wgrad(self, nd, L, r, dz, dze):
+        """Q_G(backward-weight) of one conv (Eq. 17), on the side stream once
+        dz is ready; its inputs are marked as in use there."""
+        args = (dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"],
+                iseg.ISEG_G_KEEP, 8, self.seed, 16 * L["l"], self.step_no)
+        if self.side is None:
+            return iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]))
+        ready = torch.cuda.current_stream(self.dev).record_event()
+        with torch.cuda.stream(self.side):
+            self.side.wait_event(ready)
+            G, Ge = iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]))
+        for t in (dz, dze, r["a_in"], r["a_in_exp"]):
+            t.record_stream(self.side)
+        return G, Ge
 
     def update(self, grads):
         """Q_G of gamma / beta, Eq. 19 and Q_W for every parameter: one launch."""
