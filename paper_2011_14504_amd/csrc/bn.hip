@@ -38,6 +38,9 @@ constexpr int kSentinelLo = -(1 << 30);
 #ifndef ISEG_BNF_STATS_CPL
 #define ISEG_BNF_STATS_CPL 4     // channels per lane of the forward statistics
 #endif
+#ifndef ISEG_BNB_ROWS
+#define ISEG_BNB_ROWS 8          // row groups per lane that size the backward grid
+#endif
 constexpr int kMaxBlocks = ISEG_BN_BLOCKS;
 
 // ---------------------------------------------------------------------------
@@ -1270,7 +1273,7 @@ extern "C" size_t iseg_bn_bwd_ws(int64_t M, int64_t C)
 {
     int cs = pick_cs(C, 64);
     if (!shape_ok(M, C) || !cs) return 0;
-    return bwd_ws_bytes(make_stream(M, C, cs, 4, 8, kMaxBlocks));
+    return bwd_ws_bytes(make_stream(M, C, cs, 4, ISEG_BNB_ROWS, kMaxBlocks));
 }
 
 extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
@@ -1332,7 +1335,7 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
         return ISEG_ERR_ARG;
     int cs = pick_cs(C, 64);
     if (!cs || (((uintptr_t)x | (uintptr_t)dy | (uintptr_t)dx_out) & 3)) return ISEG_ERR_UNSUPPORTED;
-    Stream st = make_stream(M, C, cs, 4, 8, kMaxBlocks);
+    Stream st = make_stream(M, C, cs, 4, ISEG_BNB_ROWS, kMaxBlocks);
     if (!ws || ws_bytes < bwd_ws_bytes(st)) return ISEG_ERR_WORKSPACE;
     BnCfg cf = to_cfg(cfg);
     Saved sv = saved_map((void*)saved, C);

@@ -2030,22 +2030,41 @@ int launch_igemm_dma(const IgemmArgs& a, const DmaPlan& p, int epi, hipStream_t 
 }
 
 // sum of the split partials [splits][n] into out (in place allowed), with
-// per-block max |sum| partials
+// per-block max |sum| partials; four 16-byte groups per thread in flight
 __global__ __launch_bounds__(256) void k_splitk_reduce(const int32_t* part, int32_t splits, int64_t n,
                                                        int32_t* out, uint64_t* pmax)
 {
+    constexpr int U = 4;
     uint32_t mx = 0;
     const int64_t n4 = n >> 2;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
-        int4 v = ((const int4*)part)[i];
-        for (int z = 1; z < splits; z++) {
-            const int4 w = ((const int4*)(part + (int64_t)z * n))[i];
-            v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x; i0 < n4; i0 += stride * U) {
+        int4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t i = i0 + u * stride;
+            v[u] = i < n4 ? ((const int4*)part)[i] : make_int4(0, 0, 0, 0);
         }
-        ((int4*)out)[i] = v;
-        const uint32_t m01 = max((uint32_t)abs(v.x), (uint32_t)abs(v.y));
-        const uint32_t m23 = max((uint32_t)abs(v.z), (uint32_t)abs(v.w));
-        mx = max(mx, max(m01, m23));
+        for (int z = 1; z < splits; z++) {
+            int4 w[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int64_t i = i0 + u * stride;
+                w[u] = i < n4 ? ((const int4*)(part + (int64_t)z * n))[i] : make_int4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) { v[u].x += w[u].x; v[u].y += w[u].y; v[u].z += w[u].z; v[u].w += w[u].w; }
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t i = i0 + u * stride;
+            if (i < n4) {
+                ((int4*)out)[i] = v[u];
+                const uint32_t m01 = max((uint32_t)abs(v[u].x), (uint32_t)abs(v[u].y));
+                const uint32_t m23 = max((uint32_t)abs(v[u].z), (uint32_t)abs(v[u].w));
+                mx = max(mx, max(m01, m23));
+            }
+        }
     }
     if (pmax) block_store_max_u64(mx, pmax);
 }
@@ -2109,7 +2128,7 @@ int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t
         if ((rc = launch_igemm_dma<MODE>(a, p, EPI_PART, s, &nblk))) return rc;
         // as many reduce blocks as the max-partial region holds for 128 x 64 tiles
         const int64_t cap = ceil_div64(a.Mrows, 128) * ceil_div64(a.Nout, 64);
-        int64_t nb = ceil_div64(n / 4, 256 * 4);
+        int64_t nb = ceil_div64(n / 4, 256 * 4);    // four 16-byte groups per thread
         nb = nb < cap ? nb : cap;
         nb = nb < 1 ? 1 : nb;
         hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)nb), dim3(256), 0, s, work, (int32_t)p.splits, n, work,
