@@ -157,6 +157,46 @@ int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w,
                        const iseg_conv_geom* g, int32_t out_mode, void* dx, int32_t* dx_exp,
                        void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
+/* Transposed weight layouts that backward-data convolves dy with (Eq. 16's
+ * adjoint): ISEG_WT_CRSK is wt[c][r][s][k] = w[k][r][s][c]; ISEG_WT_CRSK_FLIP
+ * also reverses the taps, wt[c][R-1-r][S-1-s][k] (stride-1 paths). */
+enum iseg_wt_kind { ISEG_WT_NONE = 0, ISEG_WT_CRSK = 1, ISEG_WT_CRSK_FLIP = 2 };
+
+/* iseg_conv_bwd_data_wt_kind -- the layout iseg_conv_bwd_data builds in its
+ * workspace for this geometry (ISEG_WT_NONE for an invalid geometry). */
+int32_t iseg_conv_bwd_data_wt_kind(const iseg_conv_geom* g);
+
+/* iseg_conv_bwd_data_t -- iseg_conv_bwd_data with the transposed weights
+ * supplied by the caller: wt (device, 16-byte aligned, K*R*S*C bytes) holds
+ * w in layout wt_kind, e.g. from iseg_weight_transpose_multi after the last
+ * weight update.  When the path chosen for the call needs another layout
+ * (or wt is NULL / unaligned) it builds its own from w as iseg_conv_bwd_data
+ * does, so the result is the same either way; w must always be valid.
+ * ISEG_ERR_ARG for an unknown wt_kind. */
+int iseg_conv_bwd_data_t(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
+                         const int8_t* wt, int32_t wt_kind, const iseg_conv_geom* g, int32_t out_mode,
+                         void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                         hipStream_t stream);
+
+/* One weight tensor of iseg_weight_transpose_multi: w [K][RS][C] int8 -> wt
+ * in layout kind (ISEG_WT_CRSK or ISEG_WT_CRSK_FLIP, RS = R*S taps).  The
+ * tensor is cut into ceil(C/64) * ceil(K/64) * RS tiles; tile_begin is the
+ * number of tiles of the descriptors before it (descriptors in order). */
+typedef struct iseg_wt_desc {
+    const int8_t* w;
+    int8_t* wt;
+    int32_t K, RS, C, kind;
+    int64_t tile_begin;
+} iseg_wt_desc;
+
+/* iseg_weight_transpose_multi -- every descriptor's transposed copy in one
+ * launch (one 64 x 64 LDS tile per block).  descs: device array of n_desc
+ * descriptors (caller-owned, outputs must not overlap); total_tiles = the
+ * last tile_begin plus that descriptor's tile count.  Not part of the
+ * paper's arithmetic: a data layout for the backward-data convolutions. */
+int iseg_weight_transpose_multi(const iseg_wt_desc* descs, int32_t n_desc, int64_t total_tiles,
+                                hipStream_t stream);
+
 /* iseg_conv_bwd_weight -- G[k,r,s,c] = sum_{n,p,q} dy[n,p,q,k] * x[n, p st_h -
  * pad_h + r dil_h, q st_w - pad_w + s dil_w, c] exactly (int32 partial sums of
  * at most 131008 pixels, added in int64); then Q_G: stochastic RQ to `bits`

@@ -1833,21 +1833,6 @@ int persist_q8(const PersistPlan& p, HaloArgs h, int kid, const int32_t* exp_a, 
     return launch_persist(p, h, EPI_Q8, kid, s);
 }
 
-// weights [K][R][S][C] -> [C][R][S][K] with the taps reversed (backward-data as
-// a forward convolution over dy)
-__global__ void k_w_flip_transpose(const int8_t* __restrict__ w, int8_t* __restrict__ wt, int32_t K,
-                                   int32_t RS, int32_t C)
-{
-    const int64_t n = (int64_t)K * RS * C;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t k = (int32_t)(i % K);
-        const int64_t t = i / K;
-        const int32_t rs = (int32_t)(t % RS);
-        const int32_t c = (int32_t)(t / RS);
-        wt[i] = w[((int64_t)k * RS + (RS - 1 - rs)) * C + c];
-    }
-}
 
 // the halo kernel covers 3x3 filters at stride 1, dilation <= 2, Ci and Nout
 // multiples of 64, 16-byte aligned operands
@@ -2172,19 +2157,63 @@ int launch_igemm_generic(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
 // ---------------------------------------------------------------------------
 // weights KRSC -> CRSK for the backward-data GEMM
 // ---------------------------------------------------------------------------
-__global__ void k_w_transpose(const int8_t* __restrict__ w, int8_t* __restrict__ wt,
-                              int32_t K, int32_t RS, int32_t C)
+// One 64 x 64 tile of a weight transpose: w[K][RS][C] -> wt[C][RS][K] (tap
+// rs of the source goes to tap RS-1-rs when `flip`, the backward-data filter
+// of a stride-1 conv).  The tile (k0.., c0.., tap rs) is read as 64 rows of
+// 64 contiguous channel bytes and written as 64 rows of 64 contiguous output
+// channels through an LDS tile (one padding byte per row against bank
+// conflicts); 256 threads, every index in 32-bit arithmetic.
+__device__ __forceinline__ void wt_tile(const int8_t* __restrict__ w, int8_t* __restrict__ wt, int32_t K,
+                                        int32_t RS, int32_t C, bool flip, int32_t k0, int32_t c0, int32_t rs)
 {
-    int64_t n = (int64_t)K * RS * C;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        // i indexes wt [c][rs][k]
-        int32_t k = (int32_t)(i % K);
-        int64_t t = i / K;
-        int32_t rs = (int32_t)(t % RS);
-        int32_t c = (int32_t)(t / RS);
-        wt[i] = w[((int64_t)k * RS + rs) * C + c];
+    __shared__ int8_t t[64][65];
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+#pragma unroll
+    for (int j = 0; j < 16; j++) {
+        const int k = k0 + ty + 4 * j, c = c0 + tx;
+        t[ty + 4 * j][tx] = (k < K && c < C) ? w[((uint32_t)k * RS + rs) * (uint32_t)C + c] : (int8_t)0;
     }
+    __syncthreads();
+    const int rso = flip ? RS - 1 - rs : rs;
+#pragma unroll
+    for (int j = 0; j < 16; j++) {
+        const int c = c0 + ty + 4 * j, k = k0 + tx;
+        if (c < C && k < K) wt[((uint32_t)c * RS + rso) * (uint32_t)K + k] = t[tx][ty + 4 * j];
+    }
+}
+
+// grid (ceil(C/64), ceil(K/64), RS)
+__global__ __launch_bounds__(256) void k_w_transpose_t(const int8_t* __restrict__ w, int8_t* __restrict__ wt,
+                                                       int32_t K, int32_t RS, int32_t C, int32_t flip)
+{
+    wt_tile(w, wt, K, RS, C, flip != 0, blockIdx.y * 64, blockIdx.x * 64, blockIdx.z);
+}
+
+int launch_w_transpose(const int8_t* w, int8_t* wt, int64_t K, int64_t RS, int64_t C, bool flip, hipStream_t s)
+{
+    dim3 grid((unsigned)ceil_div64(C, 64), (unsigned)ceil_div64(K, 64), (unsigned)RS);
+    hipLaunchKernelGGL(k_w_transpose_t, grid, dim3(256), 0, s, w, wt, (int32_t)K, (int32_t)RS, (int32_t)C,
+                       (int32_t)flip);
+    return launch_ok();
+}
+
+// every tensor of a descriptor table in one launch: block b takes the tile
+// b - tile_begin of the last descriptor whose tile_begin <= b
+__global__ __launch_bounds__(256) void k_w_transpose_multi(const iseg_wt_desc* __restrict__ d, int32_t n)
+{
+    const int64_t b = blockIdx.x;
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {                       // last descriptor with tile_begin <= b
+        const int mid = (lo + hi + 1) >> 1;
+        if (d[mid].tile_begin <= b) lo = mid; else hi = mid - 1;
+    }
+    const iseg_wt_desc e = d[lo];
+    const int32_t tc = (e.C + 63) / 64, tk = (e.K + 63) / 64;
+    const int64_t t = b - e.tile_begin;
+    const int32_t rs = (int32_t)(t / ((int64_t)tc * tk));
+    if (rs >= e.RS) return;                 // total_tiles larger than the table's sum
+    const int32_t r2 = (int32_t)(t - (int64_t)rs * tc * tk);
+    wt_tile(e.w, e.wt, e.K, e.RS, e.C, e.kind == ISEG_WT_CRSK_FLIP, (r2 / tc) * 64, (r2 % tc) * 64, rs);
 }
 
 // channel padding for small C: out[pix][c] = c < C ? in[pix][c] : 0
@@ -3458,10 +3487,13 @@ extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mod
     return s;
 }
 
-extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w,
-                                  const int32_t* w_exp, const iseg_conv_geom* g, int32_t out_mode,
-                                  void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes,
-                                  int32_t* dev_status, hipStream_t stream)
+// backward-data with the transposed weights either built here from w (KRSC) or
+// given by the caller (wt_in in layout wt_kind); a given layout that the
+// chosen path does not use is ignored and the path builds its own
+static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
+                              const int8_t* wt_in, int32_t wt_kind, const iseg_conv_geom* g, int32_t out_mode,
+                              void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                              hipStream_t stream)
 {
     ProfScope prof_scope(ISEG_KID_CONV_BWD_DATA, stream);
     (void)dev_status;
@@ -3475,7 +3507,7 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     unsigned long long* maxp = (unsigned long long*)ws;
     const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
                                   g->dil_h, g->dil_w);
-    int8_t* wt = (int8_t*)ws + 256;
+    int8_t* wt_ws = (int8_t*)ws + 256;
     const size_t wt_bytes = align256((size_t)(g->K * g->R * g->S * g->C));
     uint64_t* pmax = nullptr;
     int32_t* acc = (int32_t*)dx;
@@ -3484,13 +3516,16 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
         acc = (int32_t*)((char*)pmax + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N, g->H, g->W));
     }
     int rc;
-    int64_t nw = g->K * g->R * g->S * g->C;
+    // the caller's transposed weights when they are in the layout a path needs
+    auto pick_wt = [&](int32_t kind) -> const int8_t* {
+        return (wt_in && wt_kind == kind && ((uintptr_t)wt_in & 15) == 0) ? wt_in : wt_ws;
+    };
+    const int8_t* wt = wt_ws;
     const M32Plan mp = m32_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
                                 g->dil_h, g->dil_w);
+    wt = pick_wt(ISEG_WT_CRSK_FLIP);
     if (mp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx) & 15) == 0) {
-        hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
-                           (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
-        if ((rc = launch_ok())) return rc;
+        if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, true, stream))) return rc;
         HaloArgs h{};
         h.src = dy; h.wmat = wt; h.out = (int32_t*)dx;
         h.N = (int32_t)g->N; h.Hs = (int32_t)P; h.Ws = (int32_t)Q; h.Ci = (int32_t)g->K;
@@ -3506,11 +3541,10 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     }
     const PersistPlan pp = persist_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h,
                                         g->stride_w, g->dil_h, g->dil_w);
+    wt = pick_wt(ISEG_WT_CRSK_FLIP);
     if (pp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx) & 15) == 0) {
         // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
-        hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
-                           (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
-        if ((rc = launch_ok())) return rc;
+        if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, true, stream))) return rc;
         HaloArgs h{};
         h.src = dy; h.wmat = wt; h.out = (int32_t*)dx;
         h.N = (int32_t)g->N; h.Hs = (int32_t)P; h.Ws = (int32_t)Q; h.Ci = (int32_t)g->K;
@@ -3524,11 +3558,10 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
         }
         return persist_q8(pp, h, ISEG_KID_CONV_BWD_DATA, dy_exp, w_exp, (int8_t*)dx, dx_exp, pmax, stream);
     }
+    wt = pick_wt(ISEG_WT_CRSK_FLIP);
     if (hp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx | (uintptr_t)acc) & 15) == 0) {
         // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
-        hipLaunchKernelGGL(k_w_flip_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
-                           (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
-        if ((rc = launch_ok())) return rc;
+        if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, true, stream))) return rc;
         HaloArgs h{};
         h.src = dy; h.wmat = wt; h.out = acc;
         const int64_t rows = g->N * g->H * g->W;
@@ -3546,9 +3579,8 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
         return halo_q8(hp, h, ISEG_KID_CONV_BWD_DATA, dy_exp, w_exp, (int8_t*)dx, dx_exp, maxp, pmax, rows,
                        stream);
     }
-    hipLaunchKernelGGL(k_w_transpose, dim3(grid_for(nw, 256, 4096)), dim3(256), 0, stream, w, wt,
-                       (int32_t)g->K, (int32_t)(g->R * g->S), (int32_t)g->C);
-    if ((rc = launch_ok())) return rc;
+    wt = pick_wt(ISEG_WT_CRSK);
+    if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, false, stream))) return rc;
     IgemmArgs a{};
     a.src = dy; a.wmat = wt; a.out = acc; a.pmax = pmax;
     a.out16 = nullptr; a.tshift = nullptr;
@@ -3568,6 +3600,48 @@ extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const
     }
     return launch_requant_apply(acc, ISEG_I32, a.Mrows * a.Nout, dy_exp, w_exp, 0, 8, 0, 1,
                                 0, 0, 0, ISEG_I8, dx, dx_exp, nullptr, stream, pmax, nblk);
+}
+
+extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w,
+                                  const int32_t* w_exp, const iseg_conv_geom* g, int32_t out_mode,
+                                  void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes,
+                                  int32_t* dev_status, hipStream_t stream)
+{
+    return conv_bwd_data_impl(dy, dy_exp, w, w_exp, nullptr, ISEG_WT_NONE, g, out_mode, dx, dx_exp, ws, ws_bytes,
+                              dev_status, stream);
+}
+
+extern "C" int iseg_conv_bwd_data_t(const int8_t* dy, const int32_t* dy_exp, const int8_t* w,
+                                    const int32_t* w_exp, const int8_t* wt, int32_t wt_kind,
+                                    const iseg_conv_geom* g, int32_t out_mode, void* dx, int32_t* dx_exp,
+                                    void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    if (wt_kind != ISEG_WT_NONE && wt_kind != ISEG_WT_CRSK && wt_kind != ISEG_WT_CRSK_FLIP) return ISEG_ERR_ARG;
+    return conv_bwd_data_impl(dy, dy_exp, w, w_exp, wt, wt_kind, g, out_mode, dx, dx_exp, ws, ws_bytes,
+                              dev_status, stream);
+}
+
+extern "C" int32_t iseg_conv_bwd_data_wt_kind(const iseg_conv_geom* g)
+{
+    int64_t P, Q;
+    if (!geom_ok(g, &P, &Q)) return ISEG_WT_NONE;
+    const M32Plan mp = m32_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                g->dil_h, g->dil_w);
+    const PersistPlan pp = persist_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h,
+                                        g->stride_w, g->dil_h, g->dil_w);
+    const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
+                                  g->dil_h, g->dil_w);
+    return (mp.ok || pp.ok || hp.ok) ? ISEG_WT_CRSK_FLIP : ISEG_WT_CRSK;
+}
+
+extern "C" int iseg_weight_transpose_multi(const iseg_wt_desc* descs, int32_t n_desc, int64_t total_tiles,
+                                           hipStream_t stream)
+{
+    if (n_desc == 0) return ISEG_OK;
+    if (n_desc < 0 || total_tiles < 1 || !descs) return ISEG_ERR_ARG;
+    if (total_tiles > ((int64_t)1 << 31) - 1) return ISEG_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(k_w_transpose_multi, dim3((unsigned)total_tiles), dim3(256), 0, stream, descs, n_desc);
+    return launch_ok();
 }
 
 // workspace: [max word][int64 sums][max partials][padded operands][int32

@@ -49,6 +49,14 @@ class UpdateDesc(C.Structure):
 ISEG_UPD_CODES, ISEG_UPD_RAW = 0, 1
 
 
+class WtDesc(C.Structure):
+    _fields_ = [("w", C.c_void_p), ("wt", C.c_void_p), ("K", C.c_int32), ("RS", C.c_int32), ("C", C.c_int32),
+                ("kind", C.c_int32), ("tile_begin", C.c_int64)]
+
+
+ISEG_WT_NONE, ISEG_WT_CRSK, ISEG_WT_CRSK_FLIP = 0, 1, 2
+
+
 class BnCfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("k_mu", "k_sigma", "k_xhat", "k_gamma", "k_beta",
                                          "k_A", "k_E1", "k_E2", "eps_code", "relu")]
@@ -70,6 +78,9 @@ _SIGS = {
     "iseg_conv_fwd": ([_P, _P, _P, _P, _P, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
     "iseg_conv_bwd_data_ws": ([_P, _I32], _SZ),
     "iseg_conv_bwd_data": ([_P, _P, _P, _P, _P, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_conv_bwd_data_t": ([_P, _P, _P, _P, _P, _I32, _P, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_conv_bwd_data_wt_kind": ([_P], C.c_int32),
+    "iseg_weight_transpose_multi": ([_P, _I32, _I64, _P], C.c_int),
     "iseg_conv_bwd_weight_ws": ([_P, _I32], _SZ),
     "iseg_conv_bwd_weight": ([_P, _P, _P, _P, _P, _I32, _I32, _U64, _U32, _U32, _P, _P, _P, _SZ,
                               _P, _P], C.c_int),
@@ -182,6 +193,22 @@ def iseg_conv_bwd_data(dy, dy_exp, w, w_exp, geom, out_mode, dx, dx_exp, ws, sta
                                   out_mode, _ptr(dx), _ptr(dx_exp), *_ws_tuple(ws), _ptr(status),
                                   _stream())
     _check(rc, "iseg_conv_bwd_data")
+
+
+def iseg_conv_bwd_data_t(dy, dy_exp, w, w_exp, wt, wt_kind, geom, out_mode, dx, dx_exp, ws, status=None):
+    rc = lib().iseg_conv_bwd_data_t(_ptr(dy), _ptr(dy_exp), _ptr(w), _ptr(w_exp), _ptr(wt), wt_kind,
+                                    C.byref(geom), out_mode, _ptr(dx), _ptr(dx_exp), *_ws_tuple(ws),
+                                    _ptr(status), _stream())
+    _check(rc, "iseg_conv_bwd_data_t")
+
+
+def iseg_conv_bwd_data_wt_kind(geom):
+    return int(lib().iseg_conv_bwd_data_wt_kind(C.byref(geom)))
+
+
+def iseg_weight_transpose_multi(table, n, total_tiles):
+    rc = lib().iseg_weight_transpose_multi(_ptr(table), n, total_tiles, _stream())
+    _check(rc, "iseg_weight_transpose_multi")
 
 
 def iseg_conv_bwd_weight(dy, dy_exp, x, x_exp, geom, g_mode, bits, seed, tensor_id, step, dw,
@@ -504,7 +531,7 @@ def conv_fwd(x, x_exp, w, w_exp, stride=1, pad=0, dil=1, out_mode=ISEG_OUT_Q8, s
 
 
 def conv_bwd_data(dy, dy_exp, w, w_exp, x_shape, stride=1, pad=0, dil=1, out_mode=ISEG_OUT_Q8,
-                  status=None):
+                  status=None, wt=None, wt_kind=ISEG_WT_NONE):
     N, H, W, Cc = x_shape
     K, R, S, _ = w.shape
     g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
@@ -513,7 +540,10 @@ def conv_bwd_data(dy, dy_exp, w, w_exp, x_shape, stride=1, pad=0, dil=1, out_mod
     e = _out_exp(dy.device)
     ws = workspace(dy.device).get(lib().iseg_conv_bwd_data_ws(C.byref(g), out_mode))
     _maybe_arm(ISEG_KID_CONV_BWD_DATA, (N, H, W, Cc, K, R, g.stride_h, g.pad_h, g.dil_h))
-    iseg_conv_bwd_data(dy, dy_exp, w, w_exp, g, out_mode, dx, e, ws, status)
+    if wt is None:
+        iseg_conv_bwd_data(dy, dy_exp, w, w_exp, g, out_mode, dx, e, ws, status)
+    else:
+        iseg_conv_bwd_data_t(dy, dy_exp, w, w_exp, wt, wt_kind, g, out_mode, dx, e, ws, status)
     return dx, e
 
 
@@ -698,6 +728,30 @@ def softmax_ce(logits, logit_exp, labels, bits=8, want_grad=False, status=None):
     ws = workspace(dev).get(lib().iseg_softmax_ce_ws(N, h, w, K, H, W))
     iseg_softmax_ce(logits, logit_exp, labels, N, h, w, K, H, W, bits, loss, grad, err, e, ws, status)
     return loss, grad, err, e
+
+
+def wt_kind(x_shape, w_shape, stride=1, pad=0, dil=1):
+    """Transposed-weight layout the backward-data of this conv uses."""
+    N, H, W, Cc = x_shape
+    K, R, S, _ = w_shape
+    return iseg_conv_bwd_data_wt_kind(geom(N, H, W, Cc, K, R, S, stride, pad, dil))
+
+
+def wt_table(entries, device):
+    """Device array of iseg_wt_desc for iseg_weight_transpose_multi.  entries:
+    (w [K,R,S,C] int8, wt same size, kind); returns (table, n, total_tiles)."""
+    n = len(entries)
+    host = (WtDesc * max(n, 1))()
+    tiles = 0
+    for i, (w, wt, kind) in enumerate(entries):
+        K, R, S, Cc = w.shape
+        d = host[i]
+        d.w, d.wt = w.data_ptr(), wt.data_ptr()
+        d.K, d.RS, d.C, d.kind = K, R * S, Cc, kind
+        d.tile_begin = tiles
+        tiles += ((Cc + 63) // 64) * ((K + 63) // 64) * R * S
+    raw = torch.frombuffer(bytearray(bytes(host)), dtype=torch.uint8)
+    return raw.to(device), n, tiles
 
 
 def update_table(entries, device):

@@ -77,6 +77,7 @@ class IntNet:
                          Gg_exp=iseg._out_exp(self.dev), Gb_exp=iseg._out_exp(self.dev))
             self.convs[nd["name"]] = L
         self._build_update_table()
+        self.wt_tab = None
         self.loss = None
 
     def _build_update_table(self):
@@ -95,6 +96,24 @@ class IntNet:
                                      g_q_exp=L[gqe], kind=iseg.ISEG_UPD_RAW,
                                      master_exp=GB_MASTER_EXP, tensor_id=16 * L["l"] + t))
         self.upd_table, self.upd_n = iseg.update_table(ents, self.dev)
+
+    def _build_wt_table(self, rec):
+        """Transposed copy of every weight whose backward-data runs, in the
+        layout that conv's backward-data plan reads ([C, RS, K], taps reversed
+        for the stride-1 plans); written by one launch after each update."""
+        ents = []
+        for nd in self.wl["nodes"]:
+            if nd["kind"] != "conv" or (nd["src"][0] == "input" and not self.wl["input_grad"]):
+                continue
+            L = self.convs[nd["name"]]
+            L["wt_kind"] = iseg.wt_kind(rec[nd["name"]]["a_in"].shape, L["w_q"].shape, nd["stride"],
+                                        nd["pad"], nd["dil"])
+            L["w_t"] = torch.empty_like(L["w_q"])
+            ents.append((L["w_q"], L["w_t"], L["wt_kind"]))
+        self.wt_tab, self.wt_n, self.wt_tiles = iseg.wt_table(ents, self.dev)
+
+    def _transpose_weights(self):
+        iseg.iseg_weight_transpose_multi(self.wt_tab, self.wt_n, self.wt_tiles)
 
     # -------------------------------------------------------------------
     def forward(self):
@@ -155,6 +174,9 @@ class IntNet:
             return iseg.sum_requant([p[0] for p in parts], [p[1] for p in parts],
                                     exp_add=[p[2] for p in parts], bcast=[p[3] for p in parts])
 
+        if self.wt_tab is None:
+            self._build_wt_table(rec)
+            self._transpose_weights()
         e, ee = self.loss_error(rec)
         send(self.wl["nodes"][-1]["name"], e, ee)
         want_input = self.wl["input_grad"]
@@ -181,7 +203,8 @@ class IntNet:
                 grads.append((nd, r))
                 if need_in:
                     ei, eie = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
-                                                 nd["stride"], nd["pad"], nd["dil"])
+                                                 nd["stride"], nd["pad"], nd["dil"], wt=L["w_t"],
+                                                 wt_kind=L["wt_kind"])
                     r.update(e_in=ei, e_in_exp=eie)
                     send(src, ei, eie)
             elif k == "maxpool":
@@ -237,6 +260,8 @@ class IntNet:
         """Q_G of gamma / beta, Eq. 19 and Q_W for every parameter: one launch."""
         iseg.iseg_update_multi(self.upd_table, self.upd_n, 8, self.seed, self.step_no, self.lr_shift,
                                K_U, K_W)
+        if self.wt_tab is not None:
+            self._transpose_weights()
         for nd, r in grads:
             if nd["bn"]:
                 L = self.convs[nd["name"]]

@@ -147,6 +147,77 @@ def test_conv_bwd_data(orc, dev, s):
     assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
 
 
+def _wt_layout(w, kind):
+    """[K, R, S, C] -> [C, R*S, K] (taps reversed for the flipped kind): a plain
+    permutation of the weight codes, the layout backward-data reads."""
+    K, R, S, Cc = w.shape
+    t = np.transpose(w.reshape(K, R * S, Cc), (2, 1, 0))
+    return np.ascontiguousarray(t[:, ::-1, :] if kind == 2 else t)
+
+
+@pytest.mark.parametrize("s", CONV_SHAPES, ids=str)
+def test_conv_bwd_data_pretransposed(orc, dev, s):
+    """Backward-data with a caller-transposed weight: the layout the plan asks
+    for, the other layout (ignored, the library transposes itself) and none."""
+    import torch
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    P, Q = orc.conv_out_hw(_geom(s))
+    dy = synth.int_codes(23, (N, P, Q, K))
+    w = synth.int_codes(24, (K, R, R, Cc))
+    ref = orc.conv_bwd_data_raw(dy, w, _geom(s))
+    rc, rce = orc.requant(ref, -27, 8)
+    kind = iseg.wt_kind((N, Hh, W, Cc), w.shape, st, pad, d)
+    assert kind in (iseg.ISEG_WT_CRSK, iseg.ISEG_WT_CRSK_FLIP)
+    other = iseg.ISEG_WT_CRSK + iseg.ISEG_WT_CRSK_FLIP - kind
+    for k in (kind, other):
+        wt = T(_wt_layout(w, k), dev)
+        for mode in (iseg.ISEG_OUT_RAW, iseg.ISEG_OUT_Q8):
+            o, oe = iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc),
+                                       st, pad, d, out_mode=mode, wt=wt, wt_kind=k)
+            if mode == iseg.ISEG_OUT_RAW:
+                assert np.array_equal(H(o).astype(np.int64), ref) and ev(oe) == -27
+            else:
+                assert np.array_equal(H(o).astype(np.int64), rc) and ev(oe) == rce
+    # a weight whose layout does not match its stated kind must not be read
+    # when the kind is the other one: garbage in the unused layout is harmless
+    junk = torch.full((Cc * R * R * K,), 77, dtype=torch.int8, device=dev)
+    o, oe = iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc),
+                               st, pad, d, out_mode=iseg.ISEG_OUT_RAW, wt=junk, wt_kind=other)
+    assert np.array_equal(H(o).astype(np.int64), ref)
+
+
+def test_weight_transpose_multi(dev):
+    """One launch transposes a table of weights of ragged sizes, both layouts,
+    and leaves the bytes beyond each destination alone."""
+    import torch
+    from paper_2011_14504_amd import iseg
+    shapes = [(16, 3, 3, 16), (130, 3, 3, 128), (21, 1, 1, 20), (64, 7, 7, 3), (256, 1, 1, 2048),
+              (1, 1, 1, 1), (65, 3, 3, 67)]
+    ents, ws, outs, kinds = [], [], [], []
+    for i, (K, R, S, Cc) in enumerate(shapes):
+        w = synth.int_codes(40 + i, (K, R, S, Cc))
+        kind = iseg.ISEG_WT_CRSK_FLIP if i % 2 else iseg.ISEG_WT_CRSK
+        wd = T(w, dev)
+        buf = torch.full((w.size + 64,), 99, dtype=torch.int8, device=dev)
+        ents.append((wd, buf[:w.size].view(w.shape), kind))
+        ws.append(w)
+        outs.append(buf)
+        kinds.append(kind)
+    tab, n, tiles = iseg.wt_table(ents, dev)
+    iseg.iseg_weight_transpose_multi(tab, n, tiles)
+    for w, buf, kind in zip(ws, outs, kinds):
+        got = H(buf)
+        assert np.array_equal(got[:w.size], _wt_layout(w, kind).reshape(-1))
+        assert (got[w.size:] == 99).all()
+    # a tile count beyond the table's sum launches idle blocks only
+    iseg.iseg_weight_transpose_multi(tab, n, tiles + 37)
+    for w, buf, kind in zip(ws, outs, kinds):
+        got = H(buf)
+        assert np.array_equal(got[:w.size], _wt_layout(w, kind).reshape(-1))
+        assert (got[w.size:] == 99).all()
+
+
 @pytest.mark.parametrize("s", CONV_SHAPES, ids=str)
 def test_conv_bwd_weight(orc, dev, s):
     from paper_2011_14504_amd import iseg

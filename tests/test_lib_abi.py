@@ -79,3 +79,18 @@ def test_workspace_queries(lib):
     assert lib.iseg_bn_saved_bytes(64) > 64 * 1024
     assert lib.iseg_bn_fwd_ws(401408, 64) > 0 and lib.iseg_bn_bwd_ws(401408, 64) > 0
     assert lib.iseg_bn_fwd_ws(10, 3) == 0
+
+
+def test_transposed_weight_host_checks(lib):
+    from paper_2011_14504_amd import iseg
+    g = iseg.geom(1, 8, 8, 16, 16, 3, 3, 1, 1, 1)
+    assert lib.iseg_conv_bwd_data_t(None, None, None, None, None, 7, C.byref(g), 0, None, None, None,
+                                    0, None, None) == iseg.ISEG_ERR_ARG
+    bad = iseg.geom(1, 2, 2, 3, 4, 5, 5, 1, 0, 1)
+    assert lib.iseg_conv_bwd_data_wt_kind(C.byref(bad)) == iseg.ISEG_WT_NONE
+    assert lib.iseg_conv_bwd_data_wt_kind(C.byref(g)) in (iseg.ISEG_WT_CRSK, iseg.ISEG_WT_CRSK_FLIP)
+    s2 = iseg.geom(1, 16, 16, 64, 128, 3, 3, 2, 1, 1)     # stride 2: only the implicit GEMM reads it
+    assert lib.iseg_conv_bwd_data_wt_kind(C.byref(s2)) == iseg.ISEG_WT_CRSK
+    assert lib.iseg_weight_transpose_multi(None, 0, 0, None) == iseg.ISEG_OK
+    assert lib.iseg_weight_transpose_multi(None, -1, 1, None) == iseg.ISEG_ERR_ARG
+    assert lib.iseg_weight_transpose_multi(None, 1, 0, None) == iseg.ISEG_ERR_ARG
