@@ -21,6 +21,13 @@
  * owns all memory.  The library never allocates: scratch space comes from a
  * caller workspace `ws` of at least the size returned by the matching
  * iseg_*_ws() query (256-byte aligned).  Inputs and outputs must not alias.
+ * The workspace of iseg_bn_bwd begins with arrival counters
+ * (ISEG_BN_WS_ZERO(C) bytes) that must be zero before the first call with
+ * that buffer: zero it once when it is allocated.  Every iseg_bn_bwd call
+ * leaves them zero again, so a buffer kept for those calls on one stream
+ * stays ready; a buffer that other entry points also use must be zeroed again
+ * before the next iseg_bn_bwd call, and calls that may run at the same time
+ * need buffers of their own.
  *
  * Streams.  Every compute call only enqueues work on `stream` (0 = the null
  * stream) and returns; results are ready when the stream reaches that point.
@@ -80,6 +87,10 @@ enum iseg_out_mode { ISEG_OUT_Q8 = 0, ISEG_OUT_RAW = 1 };
 /* weight-gradient quantizer: Eq. 17 keeps Scale(G), Eq. 18 drops it; RAW
  * returns the exact int64 sums */
 enum iseg_g_mode { ISEG_G_KEEP = 0, ISEG_G_DROP = 1, ISEG_G_RAW = 2 };
+
+/* bytes of arrival counters at the head of a BN backward workspace for C
+ * channels */
+#define ISEG_BN_WS_ZERO(C) ((((size_t)(C) + 511) / 256) * 256)
 
 /* Convolution geometry.  Input NHWC [N,H,W,C]; weights KRSC [K,R,S,C];
  * output [N,P,Q,K] with P = floor((H + 2 pad_h - dil_h (R-1) - 1)/stride_h)+1
@@ -256,6 +267,8 @@ int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
  *            s = sgn(x - mu_q), means over the channel's M values
  *   E1     = SQ(dx, k_E1) -> dx_out int8, dx_exp                (Eq. 16)
  * dy [M, C] int8 with exponent in [-60, 16]. */
+/* workspace of iseg_bn_bwd; its first ISEG_BN_WS_ZERO(C) bytes are the
+ * arrival counters described under Pointers */
 size_t iseg_bn_bwd_ws(int64_t M, int64_t C);
 int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
                 int64_t M, int64_t C, const int8_t* gamma_q, const iseg_bn_cfg* cfg,

@@ -9,9 +9,12 @@
 //     lane), four rows in flight per lane, per-channel sums reduced in LDS and
 //     written as one partial per block and channel (no global atomics, so no
 //     same-address serialization across blocks);
-//   * per-channel finalize kernels (one block per channel) that reduce the
-//     partials and do the exact rational arithmetic in __int128, once per
-//     channel or per table entry.
+//   * finalize steps that reduce the partials and do the exact rational
+//     arithmetic in __int128 once per channel or per table entry: per-channel
+//     kernels (one block per channel) in the forward; in the backward the
+//     per-channel step runs in the tail of the streaming pass, in the last
+//     block of each channel slice to finish (an arrival counter picks it, no
+//     block waits), and the grid-wide maximum in the last slice to finish.
 // sgn(x - mu_q) and the ReLU mask are monotone in the input code, so the
 // streaming passes get them from two thresholds per channel instead of a
 // table.
@@ -20,8 +23,9 @@
 //           -> finsig (n_sigma, den, max|xhat| exponent) -> fin2 (xhat codes,
 //           y, thresholds, max|y|) -> fin3 (A codes) -> apply (table gather).
 // Backward: stats (sum delta, sum delta*xhat, sum sgn, per-class extremes of
-//           delta) -> fin1 (dgamma, dbeta, max|gamma delta|) -> [stats2 for
-//           k_E2 < 15] -> fin2 (max|dx| exponent) -> table -> apply (gather).
+//           delta | tails for k_E2 >= 15: dgamma, dbeta, then E1's exponent)
+//           -> table -> apply (gather).  k_E2 < 15 keeps separate kernels:
+//           fin1 (dgamma, dbeta, max|gamma delta|) -> stats2 -> fin2 -> table.
 #include "iseg_common.h"
 
 namespace {
@@ -298,6 +302,54 @@ __device__ __forceinline__ void copy_rows_to_lds(int8_t* dst, const int8_t* __re
             d[0] = v[k].x; d[1] = v[k].y; d[2] = v[k].z; d[3] = v[k].w;
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// arrival counters.  The backward workspace starts with ctr_bytes(C) bytes of
+// uint32 counters: ctr[0] counts the channel slices whose partials are final,
+// ctr[1 + y] the blocks of slice y that have published theirs.  atomicInc
+// with limit n - 1 hands n - 1 to the n-th arrival and wraps the counter to
+// zero there, so each kernel leaves the counters as it found them (zero); no
+// block ever waits for another.
+// ---------------------------------------------------------------------------
+size_t ctr_bytes(int64_t C) { return ISEG_BN_WS_ZERO(C); }   // >= 4 (1 + C / 4)
+
+// Values that cross blocks inside one kernel (partials, per-channel results
+// a later tail reads) are stored and loaded as relaxed agent-scope atomics:
+// write-through stores and loads that are coherent across the XCDs' L2
+// caches.  Device-scope fences would give the same ordering by writing back
+// and invalidating each whole L2, far too costly once per block.
+template <typename T>
+__device__ __forceinline__ void st_x(T* p, T v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+template <typename T>
+__device__ __forceinline__ T ld_x(const T* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+
+// Called by every thread of a block after its st_x stores: true in all
+// threads of the block that arrives last of n.  Each thread waits for its
+// stores to complete (vmcnt 0) before the barrier, and the counter update
+// follows the barrier, so every earlier arrival's stores precede the last
+// block's ld_x loads.
+__device__ __forceinline__ bool arrive_last(uint32_t* ctr, unsigned n)
+{
+    __shared__ int s_last;
+    __builtin_amdgcn_s_waitcnt(0x0F70);     // vmcnt(0)
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = atomicInc(ctr, n - 1) == n - 1;
+    __syncthreads();
+    return s_last != 0;
+}
+
+// max over the kNT threads of a block (every thread gets it)
+template <typename T>
+__device__ __forceinline__ T block_max_nt(T v, T* sh)
+{
+    for (int o = 32; o > 0; o >>= 1) { const T u = __shfl_xor(v, o, 64); v = u > v ? u : v; }
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    T m = sh[0];
+    for (int k = 1; k < kNT / 64; k++) m = sh[k] > m ? sh[k] : m;
+    __syncthreads();
+    return m;
 }
 
 // ---------------------------------------------------------------------------
@@ -616,6 +668,7 @@ __global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x
 // backward workspace
 // ---------------------------------------------------------------------------
 struct BwdWs {
+    uint32_t* ctr;                   // arrival counters
     int32_t* bdx;                    // exponent of E1's scale (atomicMax)
     unsigned long long* maxF;        // max |gamma delta|
     int32_t *p_sd, *p_z;             // [gx][C] partials
@@ -630,7 +683,7 @@ struct BwdWs {
 size_t bwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
-    return 256 + 2 * align256(pc * 4) + 3 * align256(pc * 8) + align256(pc * 24) +
+    return ctr_bytes(st.C) + 256 + 2 * align256(pc * 4) + 3 * align256(pc * 8) + align256(pc * 24) +
            4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768) + align256(C * 4);
 }
 
@@ -639,6 +692,7 @@ BwdWs bwd_ws_map(void* base, const Stream& st)
     char* p = (char*)base;
     size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
     BwdWs w;
+    w.ctr = (uint32_t*)p; p += ctr_bytes(st.C);
     w.bdx = (int32_t*)p;
     w.maxF = (unsigned long long*)(p + 64);
     p += 256;
@@ -713,10 +767,22 @@ __device__ __forceinline__ void load_bwd_tab(uint32_t* tab, const uint32_t* src,
 // likewise for the others, so six min/max updates replace per-class selects.
 constexpr int kKey = 1024;
 constexpr int kKeyInit = 4 * kKey;
+struct BnbOut {
+    const int32_t* dy_exp;
+    const int8_t* gamma_q;
+    int64_t *dgamma, *dbeta;
+    int32_t *dgamma_exp, *dbeta_exp, *dx_exp, *dev_status;
+};
+
+__device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
+                                               const BnCfg& cf, const BnbOut& o);
+
+template <bool TAIL>
 __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x, Stream st, BwdWs w,
-                                                   Saved sv, int32_t relu)
+                                                   Saved sv, BnCfg cf, BnbOut out)
 {
+    const int relu = cf.relu;
     __shared__ __attribute__((aligned(16))) uint32_t tab[64 * kRowW];
     __shared__ unsigned long long sSdn[64];
     __shared__ int32_t sSd[64], sZ[64], sMM[64 * 6];
@@ -726,7 +792,7 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
         sSdn[threadIdx.x] = 0; sSd[threadIdx.x] = 0; sZ[threadIdx.x] = 0;
         for (int k = 0; k < 3; k++) { sMM[threadIdx.x * 6 + 2 * k] = 1000; sMM[threadIdx.x * 6 + 2 * k + 1] = -1000; }
     }
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) { *w.maxF = 0; *w.bdx = kSentinelLo; }
+    if (!TAIL && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) { *w.maxF = 0; *w.bdx = kSentinelLo; }
     __syncthreads();
     int g, rsub;
     const bool active = stream_lane(st, g, rsub);
@@ -834,11 +900,19 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
     if ((int)threadIdx.x < st.CS) {
         const size_t pc = (size_t)st.gx * st.C;
         int64_t o = (int64_t)blockIdx.x * st.C + cbase + threadIdx.x;
-        w.p_sd[o] = sSd[threadIdx.x];
-        w.p_sdn[o] = (long long)sSdn[threadIdx.x];
-        w.p_z[o] = sZ[threadIdx.x];
-        for (int k = 0; k < 6; k++) w.p_mm[k * pc + o] = sMM[threadIdx.x * 6 + k];
+        if (TAIL) {
+            st_x(&w.p_sd[o], sSd[threadIdx.x]);
+            st_x(&w.p_sdn[o], (long long)sSdn[threadIdx.x]);
+            st_x(&w.p_z[o], sZ[threadIdx.x]);
+            for (int k = 0; k < 6; k++) st_x(&w.p_mm[k * pc + o], sMM[threadIdx.x * 6 + k]);
+        } else {
+            w.p_sd[o] = sSd[threadIdx.x];
+            w.p_sdn[o] = (long long)sSdn[threadIdx.x];
+            w.p_z[o] = sZ[threadIdx.x];
+            for (int k = 0; k < 6; k++) w.p_mm[k * pc + o] = sMM[threadIdx.x * 6 + k];
+        }
     }
+    if (TAIL && arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) bnb_exact_tail(tab, st, w, sv, cf, out);
 }
 
 // per channel: reduce pass-1 partials; dgamma, dbeta; max |gamma delta|
@@ -1061,106 +1135,123 @@ __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t 
 // Exact E2 (k_E2 >= 15, |gamma delta| <= 127^2 < 2^(k_E2-1)): E2's requant
 // shift r2 is <= 0 and scales every term of the bracket and the exponent base
 // by inverse powers of two, so dx, its exponent bound and its codes are those
-// of r2 = 0, with f = gamma_q delta; one finalize kernel replaces fin1 + fin2.
+// of r2 = 0, with f = gamma_q delta; the stats kernel's tails replace fin1 + fin2.
 // ---------------------------------------------------------------------------
-// per channel: pass-1 partials -> sums, dgamma, dbeta; the candidate exponent
-// of max|dx| over the channel's per-class extreme deltas
-__global__ __launch_bounds__(256) void k_bnb_fin_exact(const int32_t* dy_exp, Stream st, BwdWs w, Saved sv,
-                                                       BnCfg cf, const int8_t* gamma_q, int64_t* dgamma,
-                                                       int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
-                                                       int32_t* dev_status)
+// stats tail (exact E2).  Slice: the pass-1 sums, dgamma and dbeta of its
+// channels and each channel's bound on max|dx| (|dx| is extreme at a class's
+// extreme deltas: six candidates per channel, one thread each).  Last slice:
+// E1's exponent from the largest bound over all channels.  `lds` is the
+// stats table, no longer read once the block has arrived.
+__device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
+                                               const BnCfg& cf, const BnbOut& o)
 {
-    __shared__ long long r64[4][2];
-    __shared__ int32_t r32[4][7];
-    const int c = blockIdx.x;
+    const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
+    int32_t* tSd = (int32_t*)lds;                       // [kNT]
+    int32_t* tZ = tSd + kNT;                            // [kNT]
+    int32_t* tMM = tZ + kNT;                            // [6][kNT]
+    long long* tSdn = (long long*)(tMM + 6 * kNT);      // [kNT]
+    int32_t* tCand = (int32_t*)(tSdn + kNT);            // [6 * CS]
     const size_t pc = (size_t)st.gx * st.C;
-    long long sd = 0, sdn = 0;
-    int z = 0;
+    const int64_t cb = (int64_t)blockIdx.y * CS;
+    int sd = 0, z = 0;
+    long long sdn = 0;
     int mm[6] = {1000, -1000, 1000, -1000, 1000, -1000};
-    for (int b = threadIdx.x; b < st.gx; b += 256) {
-        const int64_t o = (int64_t)b * st.C + c;
-        sd += w.p_sd[o];
-        sdn += w.p_sdn[o];
-        z += w.p_z[o];
+    constexpr int U = 4;                    // partial rows whose loads are in flight together
+    if (grp < ng)
+        for (int b0 = grp; b0 < st.gx; b0 += U * ng) {
+            int32_t vsd[U], vz[U], vmm[U][6];
+            long long vsdn[U];
 #pragma unroll
-        for (int k = 0; k < 6; k++) {
-            const int v = w.p_mm[k * pc + o];
-            mm[k] = (k & 1) ? (v > mm[k] ? v : mm[k]) : (v < mm[k] ? v : mm[k]);
+            for (int u = 0; u < U; u++) {
+                const int b = b0 + u * ng;
+                const int64_t q = (int64_t)(b < st.gx ? b : b0) * st.C + cb + ch;
+                vsd[u] = ld_x(&w.p_sd[q]);
+                vsdn[u] = ld_x(&w.p_sdn[q]);
+                vz[u] = ld_x(&w.p_z[q]);
+#pragma unroll
+                for (int k = 0; k < 6; k++) vmm[u][k] = ld_x(&w.p_mm[k * pc + q]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                if (b0 + u * ng >= st.gx) continue;
+                sd += vsd[u]; sdn += vsdn[u]; z += vz[u];
+#pragma unroll
+                for (int k = 0; k < 6; k++) mm[k] = (k & 1) ? max(mm[k], vmm[u][k]) : min(mm[k], vmm[u][k]);
+            }
         }
-    }
-    // all nine reductions in one round: wave shuffles, then the four waves via LDS
-    for (int o = 32; o > 0; o >>= 1) {
-        sd += __shfl_xor(sd, o);
-        sdn += __shfl_xor(sdn, o);
-        z += __shfl_xor(z, o);
+    tSd[t] = sd; tZ[t] = z; tSdn[t] = sdn;
 #pragma unroll
-        for (int k = 0; k < 6; k++) {
-            const int v = __shfl_xor(mm[k], o);
-            mm[k] = (k & 1) ? max(mm[k], v) : min(mm[k], v);
+    for (int k = 0; k < 6; k++) tMM[k * kNT + t] = mm[k];
+    __syncthreads();
+    if (t < CS) {
+        for (int g2 = 1; g2 < ng; g2++) {
+            const int i = g2 * CS + t;
+            sd += tSd[i]; z += tZ[i]; sdn += tSdn[i];
+#pragma unroll
+            for (int k = 0; k < 6; k++) {
+                const int v = tMM[k * kNT + i];
+                mm[k] = (k & 1) ? max(mm[k], v) : min(mm[k], v);
+            }
         }
-    }
-    const int wv = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-        r64[wv][0] = sd; r64[wv][1] = sdn; r32[wv][0] = z;
+        const int64_t c = cb + t;
+        w.sd[c] = sd; w.sdn[c] = sdn; w.Z[c] = z;
 #pragma unroll
-        for (int k = 0; k < 6; k++) r32[wv][k + 1] = mm[k];
+        for (int k = 0; k < 6; k++) w.mm[c * 6 + k] = mm[k];
+        o.dbeta[c] = sd;
+        o.dgamma[c] = sdn;
+        // the channel totals, in the slots of group 0, for the candidate threads
+        tSd[t] = sd; tZ[t] = z; tSdn[t] = sdn;
+#pragma unroll
+        for (int k = 0; k < 6; k++) tMM[k * kNT + t] = mm[k];
     }
     __syncthreads();
-    if (threadIdx.x != 0) return;
-    for (int k2 = 1; k2 < 4; k2++) {
-        sd += r64[k2][0]; sdn += r64[k2][1]; z += r32[k2][0];
-#pragma unroll
-        for (int k = 0; k < 6; k++) mm[k] = (k & 1) ? max(mm[k], r32[k2][k + 1]) : min(mm[k], r32[k2][k + 1]);
-    }
-    const int32_t s_d = *dy_exp;
-    if (c == 0) {
-        if (s_d < -60 || s_d > 16) set_status(dev_status, ISEG_DEV_RANGE);
-        *dbeta_exp = s_d;
-        *dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
-    }
-    w.sd[c] = sd; w.sdn[c] = sdn; w.Z[c] = z;
-#pragma unroll
-    for (int k = 0; k < 6; k++) w.mm[c * 6 + k] = mm[k];
-    dbeta[c] = sd;
-    dgamma[c] = sdn;
-    const int gq = gamma_q[c];
+    const int32_t s_d = *o.dy_exp;
     const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
     const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
     const int Ebase = s_d + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
-    const i128 M = st.M;
-    const i128 Dd = (i128)sv.den[c] * M * M;
-    const i128 Sf = (i128)gq * sd, T = (i128)gq * sdn, Z = z;
-    int best = kSentinelLo;
-    for (int k = 0; k < 3; k++) {
-        const int lo = mm[2 * k], hi = mm[2 * k + 1];
-        if (lo > hi) continue;
-        const int ds[2] = {lo, hi};
-        for (int t = 0; t < 2; t++) {      // |dx| is extreme at the class's extreme deltas
-            const int64_t f = clamp_k((int64_t)gq * ds[t], cf.k_E2);
-            const i128 B = bnb_bracket(f, k - 1, M, Sf, T, Z, e_xh);
-            if (B == 0) continue;
-            const int e = ceil_pow2_exp128(abs128(B), Dd) + Ebase;
-            best = e > best ? e : best;
+    if (t < 6 * CS) {
+        const int cl = t / 6, k = t % 6;                // channel of the slice; class k / 2, low / high
+        const int64_t c = cb + cl;
+        const int lo = tMM[(k & ~1) * kNT + cl], hi = tMM[(k | 1) * kNT + cl];
+        int best = kSentinelLo;
+        if (lo <= hi) {
+            const int gq = o.gamma_q[c];
+            const i128 M = st.M;
+            const int64_t f = clamp_k((int64_t)gq * ((k & 1) ? hi : lo), cf.k_E2);
+            const i128 B = bnb_bracket(f, (k >> 1) - 1, M, (i128)gq * tSd[cl], (i128)gq * tSdn[cl],
+                                       (i128)tZ[cl], e_xh);
+            if (B != 0) best = ceil_pow2_exp128(abs128(B), (i128)sv.den[c] * M * M) + Ebase;
         }
+        tCand[t] = best;
     }
-    w.cand[c] = best;
+    __syncthreads();
+    if (t < CS) {
+        int best = tCand[6 * t];
+        for (int j = 1; j < 6; j++) best = max(best, tCand[6 * t + j]);
+        st_x(&w.cand[cb + t], best);
+    }
+    if (!arrive_last(w.ctr, gridDim.y)) return;
+    __shared__ int32_t rb[kNT / 64];
+    int bdx = kSentinelLo;
+    for (int c = t; c < st.C; c += kNT) bdx = max(bdx, ld_x(&w.cand[c]));
+    bdx = block_max_nt(bdx, rb);
+    if (bdx == kSentinelLo) bdx = 0;
+    if (t == 0) {
+        *w.bdx = bdx;
+        *o.dx_exp = bdx - (cf.k_E1 - 1);
+        if (s_d < -60 || s_d > 16) set_status(o.dev_status, ISEG_DEV_RANGE);
+        *o.dbeta_exp = s_d;
+        *o.dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
+    }
 }
 
 // dx code table of a channel (one thread per masked error code, three sgn
-// classes); E1's exponent from the largest candidate over the C channels
+// classes), with E1's exponent from the stats kernel's last tail
 __global__ __launch_bounds__(256) void k_bnb_lut_exact(const int32_t* dy_exp, int64_t Mrows, BwdWs w, Saved sv,
-                                                       BnCfg cf, const int8_t* gamma_q, int32_t* dx_exp)
+                                                       BnCfg cf, const int8_t* gamma_q)
 {
-    __shared__ int32_t rb[4];
     const int c = blockIdx.x;
-    int bdx = kSentinelLo;
-    for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) bdx = w.cand[k] > bdx ? w.cand[k] : bdx;
-    for (int o = 32; o > 0; o >>= 1) bdx = max(bdx, __shfl_xor(bdx, o));
-    if ((threadIdx.x & 63) == 0) rb[threadIdx.x >> 6] = bdx;
-    __syncthreads();
-    bdx = max(max(rb[0], rb[1]), max(rb[2], rb[3]));
-    if (bdx == kSentinelLo) bdx = 0;
-    if (c == 0 && threadIdx.x == 0) *dx_exp = bdx - (cf.k_E1 - 1);
+    const int bdx = *w.bdx;                 // the stats kernel's last tail
     const int d = (int)threadIdx.x - 128;
     const int gq = gamma_q[c];
     const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
@@ -1344,13 +1435,14 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     dim3 cb((unsigned)C);
     // E2 = SQ(gamma delta, k_E2) is exact when |gamma delta| <= 127^2 < 2^(k_E2-1)
     const int exact_e2 = cf.k_E2 >= 15;
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats, sg, dim3(kNT), 0, stream, dy, x, st, w, sv,
-                      cf.relu);
+    const BnbOut out{dy_exp, gamma_q, dgamma, dbeta, dgamma_exp, dbeta_exp, dx_exp, dev_status};
     if (exact_e2) {
-        hipLaunchKernelGGL(k_bnb_fin_exact, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma, dbeta,
-                           dgamma_exp, dbeta_exp, dev_status);
-        hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, dx_exp);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<true>, sg, dim3(kNT), 0, stream, dy, x, st, w,
+                          sv, cf, out);
+        hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q);
     } else {
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<false>, sg, dim3(kNT), 0, stream, dy, x, st,
+                          w, sv, cf, out);
         hipLaunchKernelGGL(k_bnb_fin1, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma,
                            dbeta, dgamma_exp, dbeta_exp, dev_status);
         hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(kNT), 0, stream, dy, x, st, w, sv, cf, gamma_q);

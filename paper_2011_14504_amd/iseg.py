@@ -436,32 +436,37 @@ def _maybe_arm(kid, key):
 # --------------------------------------------------------------------------
 class Workspace:
     """A growable device scratch buffer shared by consecutive calls on one
-    stream (stream order keeps the uses apart); each stream has its own."""
+    stream (stream order keeps the uses apart); each stream has its own.
+    `zeroed` buffers start at zero (the BN backward workspace, whose arrival
+    counters every call leaves at zero)."""
 
-    def __init__(self, device="cuda"):
+    def __init__(self, device="cuda", zeroed=False):
         self.device = device
+        self.zeroed = zeroed
         self.buf = None
 
     def get(self, nbytes):
         nbytes = max(int(nbytes), 256)
         if self.buf is None or self.buf.numel() < nbytes:
-            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+            alloc = torch.zeros if self.zeroed else torch.empty
+            self.buf = alloc(nbytes, dtype=torch.uint8, device=self.device)
         return self.buf[:nbytes]
 
 
 _WS = {}
 
 
-def workspace(device):
+def workspace(device, bn=False):
+    """The workspace of the current stream; the BN backward has one of its own."""
     d = device if isinstance(device, torch.device) else torch.device(device)
     if d.type == "cuda":
         idx = d.index if d.index is not None else _raw_device()
-        key = (idx, _stream_handle(idx))
+        key = (idx, _stream_handle(idx), bn)
     else:
-        idx, key = None, (str(d), 0)
+        idx, key = None, (str(d), 0, bn)
     ws = _WS.get(key)
     if ws is None:
-        ws = _WS[key] = Workspace(torch.device("cuda", idx) if d.type == "cuda" else d)
+        ws = _WS[key] = Workspace(torch.device("cuda", idx) if d.type == "cuda" else d, zeroed=bn)
     return ws
 
 
@@ -592,7 +597,7 @@ def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None, dgb_out=None):
         dge, dbe = _out_exp(x.device), _out_exp(x.device)
     else:
         dg, db, dge, dbe = dgb_out
-    ws = workspace(x.device).get(lib().iseg_bn_bwd_ws(M, Cc))
+    ws = workspace(x.device, bn=True).get(lib().iseg_bn_bwd_ws(M, Cc))
     for kid in (ISEG_KID_BN_BWD_APPLY, ISEG_KID_BN_BWD_STATS):
         _maybe_arm(kid, (M, Cc))
     iseg_bn_bwd(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, e, dg, db, dge, dbe, ws, status)

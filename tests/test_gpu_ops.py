@@ -325,6 +325,13 @@ BN_CASES = [
     dict(M=5, C=4, x_exp=-30, cfg={}),
     dict(M=2000, C=48, x_exp=-11, cfg=dict(k_E2=8, relu=0), const=True),
     dict(M=1500, C=20, x_exp=-7, cfg=dict(k_xhat=8, k_mu=8, k_sigma=8)),
+    # the per-slice tails at scale: one slice of 256 blocks; 16 forward / 32
+    # backward slices; C = 4 * 67, 67 four-channel slices (256 row groups in
+    # each tail), both E2 paths
+    dict(M=65536 + 37, C=64, x_exp=-8, cfg={}),
+    dict(M=4096 + 3, C=2048, x_exp=-6, cfg=dict(relu=0)),
+    dict(M=3001, C=268, x_exp=-10, cfg=dict(k_E2=8)),
+    dict(M=3001, C=268, x_exp=-10, cfg={}),
 ]
 
 
@@ -371,6 +378,28 @@ def test_bn_bwd(orc, dev, i):
     assert np.array_equal(H(db), r["dbeta"]) and ev(dbe) == r["dbeta_exp"]
     assert np.array_equal(H(dg), r["dgamma"]) and ev(dge) == r["dgamma_exp"]
     assert np.array_equal(H(dx), r["dx"]) and ev(dxe) == r["dx_exp"]
+
+
+def test_bn_repeated_calls_same_workspace(orc, dev):
+    """Back-to-back calls of different shapes on one workspace: each call
+    must leave the arrival counters at zero for the next."""
+    from paper_2011_14504_amd import iseg
+    refs = {}
+    for rep in range(2):
+        for i in (0, 3, 7, 9):
+            case = BN_CASES[i]
+            x, gq, bq, dA = _bn_inputs(i, case)
+            cfg = dict(orc.BN_DEFAULT, **case["cfg"])
+            c = iseg.bn_cfg(**cfg)
+            y, ye, saved = iseg.bn_fwd(T(x, dev), E(case["x_exp"], dev), T(gq, dev), T(bq, dev), c)
+            dx, dxe, dg, db, dge, dbe = iseg.bn_bwd(T(dA, dev), E(-20, dev), T(x, dev), T(gq, dev), saved, c)
+            if i not in refs:
+                refs[i] = (orc.bn_fwd(x, case["x_exp"], gq, bq, cfg),
+                           orc.bn_bwd(dA, -20, x, case["x_exp"], gq, bq, cfg))
+            r, rb = refs[i]
+            assert np.array_equal(H(y), r["y"]) and ev(ye) == r["y_exp"], (rep, i)
+            assert np.array_equal(H(dx), rb["dx"]) and ev(dxe) == rb["dx_exp"], (rep, i)
+            assert np.array_equal(H(dg), rb["dgamma"]), (rep, i)
 
 
 def test_bn_exponent_out_of_range_flags_status(dev):
