@@ -676,6 +676,288 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Short reductions with final codes (Kred <= 256: at most four 64-byte steps),
+// persistent over row tiles.  A block owns one BN-column slice of W, staged in
+// LDS once for all its tiles, and `tpb` consecutive 128-row tiles.  A tiles
+// are double-buffered whole: the loads of tile t + 1 are issued as tile t
+// starts, so they run under tile t's MFMAs and epilogue.  The only vector-
+// memory operations issued after them are tile t's epilogue stores (SX per
+// thread), so "tile t + 1 has landed" is the constant wait vmcnt <= SX; plain
+// barriers (no __syncthreads, which would drain the loads in flight) order
+// the LDS buffers.  EPI_MAX folds every tile into one running max and leaves
+// one partial per block; EPI_Q8 writes the codes from the global max.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void wait_lgkm0()
+{
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));   // lgkmcnt(0), vmcnt untouched
+}
+
+template <int BN, int EPI>
+constexpr size_t short_lds_bytes(int nk)
+{
+    return (size_t)nk * BN * 64 + 2 * (size_t)nk * 128 * 64 + (EPI == EPI_Q8 ? (size_t)128 * (BN + 16) : 0);
+}
+
+template <int MODE, int BN, int EPI>
+__global__ __launch_bounds__(256) void k_conv_short(IgemmArgs a, int tpb)
+{
+    constexpr int BM = 128, WM = BM / 2, WN = BN / 2;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int NA = BM / 64, NB = BN / 64;
+    constexpr int SA = BM * 64, SB = BN * 64;
+    constexpr int RB8 = BN + 16;                          // codes per staging row (16-byte pad)
+    constexpr int SX = EPI == EPI_Q8 ? BM * (BN / 16) / 256 : 0;
+    static_assert(SX < 64, "vmcnt range");
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+    const int nk = a.Kred / BK;
+    // the staging rows first, at a fixed offset: provably apart from every
+    // DMA target, so reading them waits for no load in flight
+    constexpr int SE = EPI == EPI_Q8 ? BM * RB8 : 0;
+    int8_t* El = smem;                                    // [BM][RB8]
+    int8_t* Bl = smem + SE;                               // [nk][SB]
+    int8_t* Al = Bl + nk * SB;                            // [2][nk][SA]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n0 = blockIdx.y * BN;
+    const int64_t nt = (a.Mrows + BM - 1) / BM;
+    const int64_t tbeg = (int64_t)blockIdx.x * tpb;
+    const int ntile = (int)(nt - tbeg < tpb ? nt - tbeg : tpb);
+    const int nchunk = a.Ci / BK;
+    const int rin = lane >> 2;
+    const int part = (lane & 3) ^ ((rin >> 1) & 3);
+
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);   // before any load is in flight
+    const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+    if (EPI == EPI_Q8 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+
+    // the block's slice of W for every step
+    for (int kb = 0; kb < nk; kb++)
+#pragma unroll
+        for (int j = 0; j < NB; j++)
+            dma16(a.wmat + (int64_t)(n0 + 16 * (wave + 4 * j) + rin) * a.Kred + kb * BK + part * 16,
+                  Bl + kb * SB + (wave + 4 * j) * 1024);
+    auto issue_tile = [&](int64_t tile, int buf) {
+        RowPix rp[NA];
+#pragma unroll
+        for (int j = 0; j < NA; j++) rp[j] = row_pix32(a, tile * BM + 16 * (wave + 4 * j) + rin);
+        int64_t soff[NA];
+        int tap = 0, cc = 0;
+        for (int kb = 0; kb < nk; kb++) {
+            if (cc == 0) {
+                const int r = tap / a.S, s = tap - (tap / a.S) * a.S;
+#pragma unroll
+                for (int j = 0; j < NA; j++) {
+                    const int64_t sp = src_pixel<MODE>(a, rp[j], r, s);
+                    soff[j] = sp < 0 ? -1 : sp * a.Ci + part * 16;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NA; j++) {
+                const void* g = soff[j] >= 0 ? (const void*)(a.src + soff[j] + cc * BK) : (const void*)g_conv_zero;
+                dma16(g, Al + (buf * nk + kb) * SA + (wave + 4 * j) * 1024);
+            }
+            if (++cc == nchunk) { cc = 0; ++tap; }
+        }
+    };
+    if (ntile > 0) issue_tile(tbeg, 0);
+
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = lane & 15, lpart = lane >> 4;
+    const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+    uint32_t run_max = 0;
+    for (int t = 0; t < ntile; t++) {
+        const int buf = t & 1;
+        if (t == 0) wait_vm<0>();                         // W slice and tile 0
+        else wait_vm<SX>();                               // tile t (tile t - 1's stores may still run)
+        // every wave's part of tile t is in LDS; every wave is done with the
+        // other buffer (tile t - 1) and with the staging rows
+        __builtin_amdgcn_s_barrier();
+        if (t + 1 < ntile) issue_tile(tbeg + t + 1, buf ^ 1);
+        v4i acc[TM][TN];
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++) acc[i][j] = (v4i){0, 0, 0, 0};
+        for (int kb = 0; kb < nk; kb++) {
+            const int8_t* A = Al + (buf * nk + kb) * SA;
+            const int8_t* B = Bl + kb * SB;
+            v4i fa[TM], fb[TN];
+#pragma unroll
+            for (int i = 0; i < TM; i++) fa[i] = *(const v4i*)&A[swz(wm * WM + i * 16 + lrow, lpart)];
+#pragma unroll
+            for (int j = 0; j < TN; j++) fb[j] = *(const v4i*)&B[swz(wn * WN + j * 16 + lrow, lpart)];
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+        const int64_t m0 = (tbeg + t) * BM;
+        const int vrows = a.Mrows - m0 < BM ? (int)(a.Mrows - m0) : BM;
+        if (EPI == EPI_MAX) {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        const int row = wm * WM + i * 16 + lpart * 4 + e;
+                        const int32_t v = acc[i][j][e];
+                        const uint32_t av = row < vrows ? (uint32_t)(v < 0 ? -v : v) : 0u;
+                        run_max = av > run_max ? av : run_max;
+                    }
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        const int row = wm * WM + i * 16 + lpart * 4 + e;
+                        const int32_t x = acc[i][j][e];
+                        int32_t c = rq > 0 ? ((x >> rs) + 1) >> 1 : x << ls;
+                        c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                        El[row * RB8 + wn * WN + j * 16 + lrow] = (int8_t)c;
+                    }
+            wait_lgkm0();
+            __builtin_amdgcn_s_barrier();                 // the tile's codes are in LDS
+            constexpr int CPR = BN / 16;                  // 16-byte chunks per row
+            int4 v[SX > 0 ? SX : 1];
+#pragma unroll
+            for (int k = 0; k < SX; k++) {
+                const int c = tid + k * 256;
+                v[k] = *(const int4*)&El[(c / CPR) * RB8 + (c % CPR) * 16];
+            }
+            // every chunk in registers before the guarded stores (kept from
+            // being sunk into them, where each would reuse one register set)
+#pragma unroll
+            for (int k = 0; k < SX; k++) asm volatile("" : "+v"(v[k].x), "+v"(v[k].y), "+v"(v[k].z), "+v"(v[k].w));
+#pragma unroll
+            for (int k = 0; k < SX; k++) {
+                const int c = tid + k * 256;
+                const int row = c / CPR, cc = c % CPR;
+                if (row < vrows) *(int4*)(a.out8 + (m0 + row) * a.Nout + n0 + cc * 16) = v[k];
+            }
+        }
+    }
+    wait_vm<0>();
+    if (EPI == EPI_MAX) block_store_max_u64(run_max, a.pmax);
+}
+
+// ---------------------------------------------------------------------------
+// Short 1x1 stride-1 convolutions with final codes: a plain GEMM
+// out[m][n] = sum_k A[m][k] B[n][k] over contiguous pixels, Kred = 64 NK <=
+// 256, entirely in registers.  A wave owns 64 output channels, whose B
+// fragments stay in VGPRs, and walks blocks of 16 MT pixels, loading the next
+// block's A fragments (16 bytes per lane, 1 KB contiguous per 16 pixels)
+// while the current block's MFMAs run.  The product is formed as W x A^T, so
+// a lane's four results are four consecutive channels of one pixel: one
+// packed dword per 16 x 16 tile.  No LDS and no barriers in the loop:
+// occupancy is set by registers alone and many loads stay in flight.
+// Waves of a block share their pixel blocks when there are >= 4 channel
+// groups (their A loads meet in the CU's L1).  EPI_MAX leaves one max
+// partial per block; EPI_Q8 writes the codes from the global max.
+// ---------------------------------------------------------------------------
+template <int NK, int EPI>
+__global__ __launch_bounds__(256) void k_gemm_short(IgemmArgs a)
+{
+    constexpr int MT = NK <= 2 ? 2 : 1;                   // 16-pixel tiles per block of pixels
+    constexpr int PB = 16 * MT;
+    const int lane = threadIdx.x & 63;
+    const int lr = lane & 15, lk = lane >> 4;
+    const int ncg = a.Nout / 64;
+    const int64_t gw = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int cg = (int)(gw % ncg);
+    const int64_t wstride = (int64_t)gridDim.x * 4 / ncg;    // the grid's waves are a multiple of ncg
+    const int64_t npb = (a.Mrows + PB - 1) / PB;
+
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);
+    const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+    const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+    if (EPI == EPI_Q8 && blockIdx.x == 0 && threadIdx.x == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+
+    v4i fb[4][NK];
+#pragma unroll
+    for (int j = 0; j < 4; j++)
+#pragma unroll
+        for (int s = 0; s < NK; s++)
+            fb[j][s] = *(const v4i*)(a.wmat + (int64_t)(cg * 64 + j * 16 + lr) * a.Kred + s * 64 + lk * 16);
+    auto load_a = [&](int64_t pb, v4i (&fa)[MT][NK]) {
+#pragma unroll
+        for (int i = 0; i < MT; i++) {
+            int64_t m = pb * PB + i * 16 + lr;
+            m = m < a.Mrows ? m : a.Mrows - 1;             // rows past the end: loaded, never used
+            const int8_t* p = a.src + m * a.Kred + lk * 16;
+#pragma unroll
+            for (int s = 0; s < NK; s++) fa[i][s] = *(const v4i*)(p + s * 64);
+        }
+    };
+    uint32_t mx = 0;
+    // one block of PB pixels from fa: acc[j][i][e] is pixel pb PB + 16 i + lr,
+    // channel 64 cg + 16 j + 4 lk + e.  Full blocks store unconditionally, so
+    // the compiler can count the stores behind the next block's loads.
+    auto block = [&](int64_t pb, const v4i (&fa)[MT][NK], bool ragged) {
+        v4i acc[4][MT];
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+#pragma unroll
+            for (int i = 0; i < MT; i++) acc[j][i] = (v4i){0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < NK; s++)
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+#pragma unroll
+                for (int i = 0; i < MT; i++)
+                    acc[j][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fb[j][s], fa[i][s], acc[j][i], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < MT; i++) {
+            const int64_t m = pb * PB + i * 16 + lr;
+            if (ragged && m >= a.Mrows) continue;
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                if (EPI == EPI_MAX) {
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        const int32_t v = acc[j][i][e];
+                        const uint32_t av = (uint32_t)(v < 0 ? -v : v);
+                        mx = av > mx ? av : mx;
+                    }
+                } else {
+                    uint32_t packed = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        const int32_t x = acc[j][i][e];
+                        int32_t c = rq > 0 ? ((x >> rs) + 1) >> 1 : x << ls;
+                        c = c > 127 ? 127 : (c < -127 ? -127 : c);
+                        packed |= (uint32_t)(uint8_t)(int8_t)c << (8 * e);
+                    }
+                    *(uint32_t*)(a.out8 + m * a.Nout + cg * 64 + j * 16 + lk * 4) = packed;
+                }
+            }
+        }
+    };
+    const int64_t nfull = a.Mrows / PB;
+    int64_t pb = gw / ncg;
+    v4i fa[MT][NK], na[MT][NK];
+    if (pb < npb) load_a(pb, fa);
+    for (; pb < nfull; pb += wstride) {
+        const bool more = pb + wstride < npb;
+        if (more) load_a(pb + wstride, na);
+        block(pb, fa, false);
+        if (more) {
+#pragma unroll
+            for (int i = 0; i < MT; i++)
+#pragma unroll
+                for (int s = 0; s < NK; s++) fa[i][s] = na[i][s];
+        }
+    }
+    if (pb < npb) block(pb, fa, true);         // the ragged last block, already in fa
+    if (EPI == EPI_MAX) block_store_max_u64(mx, a.pmax);
+}
+
+// ---------------------------------------------------------------------------
 // 3x3, stride-1 convolution from an LDS halo tile (Ci % 64 == 0, Nout % 64 == 0).
 //
 // A block owns TH = 4 output rows x TW output columns of one image and 64
@@ -1976,6 +2258,94 @@ size_t dma_split_bytes(const DmaPlan& p, int64_t Mrows, int32_t Nout)
     return p.splits > 1 ? align256((size_t)p.splits * (size_t)Mrows * (size_t)Nout * 4) : 0;
 }
 
+// persistent short-reduction launch: as many tiles per block as leave about
+// one round of blocks at the occupancy the LDS allows
+#ifndef ISEG_CONV_SHORT
+#define ISEG_CONV_SHORT 1
+#endif
+#ifndef ISEG_SHORT_TPB
+#define ISEG_SHORT_TPB 0         // row tiles per block of the short kernel (0: sized from occupancy)
+#endif
+template <int MODE, int BN, int EPI>
+int launch_short_t(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
+{
+    const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
+    const int nk = a.Kred / BK;
+    const size_t lds = short_lds_bytes<BN, EPI>(nk);
+    const int64_t nt = ceil_div64(a.Mrows, 128), ncol = a.Nout / BN;
+    int64_t occ = (int64_t)((160 * 1024) / lds);
+    occ = occ < 1 ? 1 : (occ > 4 ? 4 : occ);
+    int64_t tpb = ISEG_SHORT_TPB > 0 ? ISEG_SHORT_TPB : ceil_div64(nt * ncol, 256 * occ);
+    tpb = tpb < 1 ? 1 : tpb;
+    dim3 grid((unsigned)ceil_div64(nt, tpb), (unsigned)ncol);
+    if (lds > 65536 && !lds_limit((const void*)k_conv_short<MODE, BN, EPI>, lds)) return ISEG_ERR_DEVICE;
+    ISEG_TIMED_LAUNCH(kid, s, (k_conv_short<MODE, BN, EPI>), grid, dim3(256), lds, s, a, (int)tpb);
+    *nblk = (int64_t)grid.x * grid.y;
+    return launch_ok();
+}
+
+// the register GEMM for 1x1 stride-1 convs (rows are contiguous pixels): each
+// wave loads its own W fragments, so it pays off for few channel groups, at
+// most two reduction steps and many pixels (measured on the DeepLabv3 shapes)
+bool gemm_short_ok(const IgemmArgs& a)
+{
+    return ISEG_CONV_SHORT && a.R == 1 && a.S == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0 &&
+           a.Ho == a.Hs && a.Wo == a.Ws && a.Kred % 64 == 0 && a.Kred <= 128 && a.Nout % 64 == 0 &&
+           a.Nout <= 256 && a.Mrows >= 32768 &&
+           (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0 && ((uintptr_t)a.out8 & 3) == 0;
+}
+
+// the persistent LDS kernel: its double-buffered A tiles cost occupancy at
+// three or four reduction steps, and it needs enough row tiles to fill the chip
+bool lds_short_ok(const IgemmArgs& a) { return ISEG_CONV_SHORT && a.Kred <= 2 * BK && a.Mrows >= 16384; }
+
+template <int MODE, int NK, int EPI>
+int launch_gemm_short_t(const IgemmArgs& a, hipStream_t s, int64_t* nblk)
+{
+    const int kid = MODE == MODE_FWD ? ISEG_KID_CONV_FWD : ISEG_KID_CONV_BWD_DATA;
+    constexpr int PB = NK <= 2 ? 32 : 16;
+    const int64_t ncg = a.Nout / 64;
+    const int64_t units = ceil_div64(a.Mrows, PB) * ncg;
+    // waves: at most the units, at most 4 per SIMD over the chip, a multiple of
+    // max(4, ncg) so that every wave keeps one channel group
+    const int64_t q = ncg > 4 ? ncg : 4;
+    int64_t waves = units < 4096 ? units : 4096;
+    waves = ceil_div64(waves, q) * q;
+    dim3 grid((unsigned)(waves / 4));
+    ISEG_TIMED_LAUNCH(kid, s, (k_gemm_short<NK, EPI>), grid, dim3(256), 0, s, a);
+    *nblk = grid.x;
+    return launch_ok();
+}
+
+template <int MODE, int NK>
+int launch_gemm_short_k(const IgemmArgs& a, int epi, hipStream_t s, int64_t* nblk)
+{
+    return epi == EPI_MAX ? launch_gemm_short_t<MODE, NK, EPI_MAX>(a, s, nblk)
+                          : launch_gemm_short_t<MODE, NK, EPI_Q8>(a, s, nblk);
+}
+
+template <int MODE>
+int launch_gemm_short(const IgemmArgs& a, int epi, hipStream_t s, int64_t* nblk)
+{
+    switch (a.Kred / 64) {
+    case 1: return launch_gemm_short_k<MODE, 1>(a, epi, s, nblk);
+    case 2: return launch_gemm_short_k<MODE, 2>(a, epi, s, nblk);
+    case 3: return launch_gemm_short_k<MODE, 3>(a, epi, s, nblk);
+    default: return launch_gemm_short_k<MODE, 4>(a, epi, s, nblk);
+    }
+}
+
+template <int MODE>
+int launch_short(const IgemmArgs& a, int epi, hipStream_t s, int64_t* nblk)
+{
+    if (gemm_short_ok(a)) return launch_gemm_short<MODE>(a, epi, s, nblk);
+    if (a.Nout % 128 == 0)
+        return epi == EPI_MAX ? launch_short_t<MODE, 128, EPI_MAX>(a, s, nblk)
+                              : launch_short_t<MODE, 128, EPI_Q8>(a, s, nblk);
+    return epi == EPI_MAX ? launch_short_t<MODE, 64, EPI_MAX>(a, s, nblk)
+                          : launch_short_t<MODE, 64, EPI_Q8>(a, s, nblk);
+}
+
 template <int MODE, int BM, int BN, int EPI>
 int launch_dma_t(const IgemmArgs& a, int splits, hipStream_t s, int64_t* nblk)
 {
@@ -2101,10 +2471,12 @@ int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t
     }
     if (p.two_pass) {
         a.pmax = pmax;
-        if ((rc = launch_igemm_dma<MODE>(a, p, EPI_MAX, s, &nblk))) return rc;
+        a.out8 = (int8_t*)y; a.exp_a = exp_a; a.exp_b = exp_b; a.out_exp = y_exp;   // both passes pick one kernel
+        const bool sh = gemm_short_ok(a) || lds_short_ok(a);
+        if ((rc = sh ? launch_short<MODE>(a, EPI_MAX, s, &nblk) : launch_igemm_dma<MODE>(a, p, EPI_MAX, s, &nblk)))
+            return rc;
         a.npmax = nblk;
-        a.out8 = (int8_t*)y; a.exp_a = exp_a; a.exp_b = exp_b; a.out_exp = y_exp;
-        return launch_igemm_dma<MODE>(a, p, EPI_Q8, s, &nblk);
+        return sh ? launch_short<MODE>(a, EPI_Q8, s, &nblk) : launch_igemm_dma<MODE>(a, p, EPI_Q8, s, &nblk);
     }
     const int64_t n = a.Mrows * a.Nout;
     if (p.splits > 1) {

@@ -212,16 +212,19 @@ __device__ __forceinline__ void block_store_max_u64(uint64_t v, uint64_t* part)
     if (threadIdx.x == 0) part[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = m;
 }
 
-// max over n partials, computed by the whole block (every thread gets it)
+// max over n partials, computed by the whole block (every thread gets it).
+// The loads are unconditional (an index past the end re-reads partial 0, a
+// value already in the max) so the eight of a thread are in flight together;
+// a guarded load would be compiled as a branch with a wait after each.
 __device__ __forceinline__ uint64_t reduce_partials_u64(const uint64_t* part, int64_t n)
 {
     uint64_t m = 0;
     for (int64_t base = 0; base < n; base += 8 * (int64_t)blockDim.x) {
-        uint64_t v[8];                    // eight loads in flight per thread
+        uint64_t v[8];
 #pragma unroll
         for (int k = 0; k < 8; k++) {
             const int64_t i = base + k * (int64_t)blockDim.x + threadIdx.x;
-            v[k] = i < n ? part[i] : 0;
+            v[k] = part[i < n ? i : 0];
         }
 #pragma unroll
         for (int k = 0; k < 8; k++) m = v[k] > m ? v[k] : m;

@@ -250,13 +250,17 @@ def test_conv_bwd_weight_long_reduction(orc, dev):
 
 
 # Full-size shapes of the DeepLabv3 step whose reduction is split across
-# blocks (ASPP 3x3 branches) or tiled without a split: raw int32 sums at
+# blocks (ASPP 3x3 branches), tiled without a split, or short enough for
+# the two-pass persistent kernel: raw int32 sums at
 # sampled output pixels against exact integer dot products, and the final
 # codes against the requant of those sums under the exponent the kernel chose.
 FULL_SHAPES = [
     (8, 32, 32, 2048, 256, 3, 1, 6, 6),
     (8, 32, 32, 2048, 256, 3, 1, 18, 18),
     (8, 32, 32, 1024, 2048, 1, 1, 0, 1),
+    # short reductions, persistent blocks of several row tiles each
+    (8, 128, 128, 64, 256, 1, 1, 0, 1),
+    (8, 32, 32, 256, 1024, 1, 1, 0, 1),
 ]
 
 
