@@ -3252,23 +3252,40 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce_part(const int32_t* __rest
 }
 
 // few splits: one lane per 4 weights over all splits, sum and max in one pass
-__global__ __launch_bounds__(256) void k_wgrad_reduce_flat(const int32_t* __restrict__ part, int64_t n, int splits,
+// S <= 8 splits, four elements per thread step with every split's 16-byte
+// load in flight together; the int64 sums into `out` unless it is null (the
+// max partials alone, for a requant that re-sums the splits itself)
+template <int S>
+__global__ __launch_bounds__(256) void k_wgrad_reduce_flat(const int32_t* __restrict__ part, int64_t n,
                                                            long long* __restrict__ out, uint64_t* pmax)
 {
-    const int64_t e0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    constexpr int U = S >= 8 ? 1 : 8 / S;      // grid steps per trip: about eight loads in flight
+    const int64_t n4 = n >> 2, stride = (int64_t)gridDim.x * 256;
     uint64_t mx = 0;
-    if (e0 < n) {
-        long long s[4] = {0, 0, 0, 0};
-        for (int k = 0; k < splits; k++) {
-            const int4 v = *(const int4*)(part + (int64_t)k * n + e0);
-            s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
-        }
-        *(longlong2*)(out + e0) = make_longlong2(s[0], s[1]);
-        *(longlong2*)(out + e0 + 2) = make_longlong2(s[2], s[3]);
+    for (int64_t j0 = (int64_t)blockIdx.x * 256 + threadIdx.x; j0 < n4; j0 += U * stride) {
+        int4 v[U][S];
 #pragma unroll
-        for (int u = 0; u < 4; u++) {
-            const uint64_t a = s[u] < 0 ? (uint64_t)(-s[u]) : (uint64_t)s[u];
-            mx = a > mx ? a : mx;
+        for (int u = 0; u < U; u++) {
+            const int64_t j = j0 + u * stride < n4 ? j0 + u * stride : j0;   // past the end: a repeat
+#pragma unroll
+            for (int k = 0; k < S; k++) v[u][k] = *(const int4*)(part + (int64_t)k * n + j * 4);
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t j = j0 + u * stride;
+            if (j >= n4) break;
+            long long s[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int k = 0; k < S; k++) { s[0] += v[u][k].x; s[1] += v[u][k].y; s[2] += v[u][k].z; s[3] += v[u][k].w; }
+            if (out) {
+                *(longlong2*)(out + j * 4) = make_longlong2(s[0], s[1]);
+                *(longlong2*)(out + j * 4 + 2) = make_longlong2(s[2], s[3]);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const uint64_t a = s[e] < 0 ? (uint64_t)(-s[e]) : (uint64_t)s[e];
+                mx = a > mx ? a : mx;
+            }
         }
     }
     if (pmax) block_store_max_u64(mx, pmax);
@@ -3485,6 +3502,8 @@ size_t wgrad_taps_part_bytes(int64_t NPQ, int64_t K, int64_t C, int64_t RS)
 // int64 sums of `splits` int32 partials [splits][n] (n % 4 == 0) into out and,
 // when pmax is set, per-block max |sum| partials (their count into *npmax);
 // the two-level variant keeps its chunk sums right after the partials
+bool wgrad_flat_ok(int64_t n, int64_t splits) { return splits >= 1 && splits <= 8 && n % 4 == 0; }
+
 int launch_wgrad_reduce(const int32_t* part, int64_t n, int64_t splits, long long* out, uint64_t* pmax,
                         int64_t* npmax, hipStream_t s)
 {
@@ -3501,16 +3520,34 @@ int launch_wgrad_reduce(const int32_t* part, int64_t n, int64_t splits, long lon
                            (const long long*)out2, n, nch, out, pmax);
         return launch_ok();
     }
-    if (splits <= 8 && (((uintptr_t)out) & 15) == 0) {
-        if (npmax) *npmax = ceil_div64(n, 1024);
-        hipLaunchKernelGGL(k_wgrad_reduce_flat, dim3((unsigned)ceil_div64(n, 1024)), dim3(256), 0, s, part, n,
-                           (int)splits, out, pmax);
+    if (wgrad_flat_ok(n, splits) && (((uintptr_t)out) & 15) == 0) {
+        // a capped grid: the requant that follows reduces every max partial in each block
+        const unsigned nb = (unsigned)std::min<int64_t>(ceil_div64(n / 4, 256), 512);
+        if (npmax) *npmax = nb;
+        switch (splits) {
+#define ISEG_RF(S) case S: hipLaunchKernelGGL(k_wgrad_reduce_flat<S>, dim3(nb), dim3(256), 0, s, part, n, out, pmax); break;
+        ISEG_RF(1) ISEG_RF(2) ISEG_RF(3) ISEG_RF(4) ISEG_RF(5) ISEG_RF(6) ISEG_RF(7) ISEG_RF(8)
+#undef ISEG_RF
+        }
         return launch_ok();
     }
+    if (!out) return ISEG_ERR_ARG;
     if (npmax) *npmax = ceil_div64(n, 256);
     hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)ceil_div64(n, 256)), dim3(64 * kRedWaves), 0, s, part, n,
                        (int)splits, out, pmax);
     return launch_ok();
+}
+
+// The split reduction ahead of Q_G.  When `qg` is given and the splits allow
+// the flat reduce, only the max partials are formed and *qg = splits: the
+// requant re-sums the int32 splits itself (launch_requant_splits), so the
+// int64 sums are never written; otherwise the int64 sums go to `out`, *qg = 0.
+int launch_wgrad_reduce_qg(const int32_t* part, int64_t n, int64_t splits, long long* out, uint64_t* pmax,
+                           int64_t* npmax, hipStream_t s, int* qg)
+{
+    const bool fuse = qg && pmax && wgrad_flat_ok(n, splits);
+    if (qg) *qg = fuse ? (int)splits : 0;
+    return launch_wgrad_reduce(part, n, splits, fuse ? nullptr : out, pmax, npmax, s);
 }
 
 // max-partial count of launch_wgrad_reduce for a shape (workspace sizing)
@@ -3518,7 +3555,7 @@ int64_t wgrad_reduce_npmax(int64_t n) { return ceil_div64(n, 256); }
 
 // all-taps launch: partials into `part`, then their int64 sum into a.acc (every
 // element written, no fill needed) and its max |.| partials into pmax when given
-int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax, hipStream_t s)
+int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax, hipStream_t s, int* qg)
 {
     const int RS = a.R * a.S;
     int64_t splits = wgrad_taps_splits(a.NPQ, a.K, a.C, &a.pix_per_split);
@@ -3530,7 +3567,7 @@ int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax
     ISEG_TIMED_LAUNCH(ISEG_KID_CONV_WGRAD, s, k_conv_wgrad_taps<9>, grid, dim3(64 * 9), lds, s, a, part);
     int rc = launch_ok();
     if (rc) return rc;
-    return launch_wgrad_reduce(part, (int64_t)a.K * a.RSC, splits, (long long*)a.acc, pmax, npmax, s);
+    return launch_wgrad_reduce_qg(part, (int64_t)a.K * a.RSC, splits, (long long*)a.acc, pmax, npmax, s, qg);
 }
 
 // the transposed-operand kernel over split pixel ranges: int32 partials per
@@ -3563,7 +3600,7 @@ size_t wgrad_tr_part_bytes(int64_t NPQ, int64_t K, int64_t C, int64_t RS)
     return align256((size_t)(splits * n) * 4) + (nch > 1 ? align256((size_t)(nch * n) * 8) : 0);
 }
 
-int launch_wgrad_tr_split(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax, hipStream_t s)
+int launch_wgrad_tr_split(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax, hipStream_t s, int* qg)
 {
     const int BMt = a.K % 128 == 0 ? 128 : 64;
     const int RS = a.R * a.S;
@@ -3582,7 +3619,7 @@ int launch_wgrad_tr_split(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* n
         hipLaunchKernelGGL((k_conv_wgrad_tr<64, 1>), grid, dim3(256), 0, s, a);
     int rc = launch_ok();
     if (rc) return rc;
-    return launch_wgrad_reduce(part, (int64_t)a.K * a.RSC, splits, (long long*)a.acc, pmax, npmax, s);
+    return launch_wgrad_reduce_qg(part, (int64_t)a.K * a.RSC, splits, (long long*)a.acc, pmax, npmax, s, qg);
 }
 
 int launch_wgrad(WgradArgs a, hipStream_t s)
@@ -4075,12 +4112,16 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     wp += wgrad_part_region(NPQ, g->K, Cp, g->R * g->S);
     int rc;
     int64_t npmax = 0;
+    int qg = 0;                   // > 0: Q_G re-sums that many int32 splits (no int64 sums)
     // the int64 sums are done: their exponent (raw) or Q_G from the max partials
     auto finish = [&]() -> int {
         if (raw) {
             hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dw_exp, dy_exp, x_exp);
             return launch_ok();
         }
+        if (qg)
+            return launch_requant_splits(part, qg, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr, bits, 1, keep,
+                                         seed, tensor_id, step, (int8_t*)dw, dw_exp, stream, pmax, npmax);
         return launch_requant_apply(acc, ISEG_I64, nw, keep ? dy_exp : nullptr, keep ? x_exp : nullptr, 0, bits, 1,
                                     keep, seed, tensor_id, step, ISEG_I8, dw, dw_exp, nullptr, stream, pmax, npmax);
     };
@@ -4114,11 +4155,11 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
     if (Cp == g->C && wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) && (((uintptr_t)x | (uintptr_t)dy) & 15) == 0) {
-        if ((rc = launch_wgrad_taps(a, part, raw ? nullptr : pmax, &npmax, stream))) return rc;
+        if ((rc = launch_wgrad_taps(a, part, raw ? nullptr : pmax, &npmax, stream, raw ? nullptr : &qg))) return rc;
         return finish();
     }
     if (Cp == g->C && wgrad_tr_ok(a)) {
-        if ((rc = launch_wgrad_tr_split(a, part, raw ? nullptr : pmax, &npmax, stream))) return rc;
+        if ((rc = launch_wgrad_tr_split(a, part, raw ? nullptr : pmax, &npmax, stream, raw ? nullptr : &qg))) return rc;
         return finish();
     }
     // other shapes: atomic int64 accumulation (zero-filled), then the max pass

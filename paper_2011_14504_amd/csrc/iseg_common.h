@@ -281,6 +281,12 @@ int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t*
                          int out_dtype, void* out, int32_t* out_exp,
                          const unsigned long long* maxp, hipStream_t s,
                          const uint64_t* part = nullptr, int64_t nparts = 0);
+// SQ / RQ of the sum of `splits` (<= 8) int32 partial tensors [splits][n]
+// (n % 4 == 0, 16-byte aligned partials) into int8 codes; the max from the
+// npmax max partials in pmax
+int launch_requant_splits(const int32_t* part, int splits, int64_t n, const int32_t* exp_a, const int32_t* exp_b,
+                          int bits, int stochastic, int keep_scale, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                          int8_t* out, int32_t* out_exp, hipStream_t s, const uint64_t* pmax, int64_t npmax);
 
 // max |.| of an int32/int64 buffer into *maxp (which must be zeroed first)
 int launch_absmax(const void* in, int in_dtype, int64_t n, unsigned long long* maxp,

@@ -224,6 +224,52 @@ int launch_requant_apply(const void* in, int in_dtype, int64_t n, const int32_t*
     return launch_ok();
 }
 
+// SQ / RQ (Eq. 3-6) of the exact sum of S int32 partial tensors [S][n]
+// (n % 4 == 0): four elements per thread step, every split's 16-byte load in
+// flight together, the int64 sum formed in registers (never stored).
+template <int S>
+__global__ __launch_bounds__(256) void k_requant_splits_i8(const int32_t* __restrict__ part,
+                                                           int8_t* __restrict__ out, RqArgs a)
+{
+    const uint64_t M = rq_max(a);
+    const int r = rq_shift(a, M);
+    rq_write_exp(a, M, r);
+    const int64_t n4 = a.n >> 2;
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < n4; j += (int64_t)gridDim.x * blockDim.x) {
+        int4 v[S];
+#pragma unroll
+        for (int k = 0; k < S; k++) v[k] = *(const int4*)(part + (int64_t)k * a.n + j * 4);
+        int64_t s[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int k = 0; k < S; k++) { s[0] += v[k].x; s[1] += v[k].y; s[2] += v[k].z; s[3] += v[k].w; }
+        uint32_t w = 0;
+#pragma unroll
+        for (int e = 0; e < 4; e++) w |= (uint32_t)(uint8_t)rq_one(a, s[e], r, j * 4 + e) << (8 * e);
+        *(uint32_t*)(out + j * 4) = w;
+    }
+}
+
+int launch_requant_splits(const int32_t* part, int splits, int64_t n, const int32_t* exp_a, const int32_t* exp_b,
+                          int bits, int stochastic, int keep_scale, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                          int8_t* out, int32_t* out_exp, hipStream_t s, const uint64_t* pmax, int64_t npmax)
+{
+    if (splits < 1 || splits > 8 || n % 4 != 0 || (((uintptr_t)part) & 15) || (((uintptr_t)out) & 3))
+        return ISEG_ERR_ARG;
+    RqArgs a;
+    a.part = pmax; a.nparts = npmax;
+    a.n = n; a.exp_a = exp_a; a.exp_b = exp_b; a.exp_add = 0;
+    a.bits = bits; a.stochastic = stochastic; a.keep_scale = keep_scale;
+    a.seed = seed; a.tensor_id = tensor_id; a.step = step;
+    a.out_exp = out_exp; a.maxp = nullptr;
+    const dim3 grid(grid_for(n / 4, 256, 2048));
+    switch (splits) {
+#define ISEG_RQS(S) case S: ISEG_TIMED_LAUNCH(ISEG_KID_REQUANT, s, k_requant_splits_i8<S>, grid, dim3(256), 0, s, part, out, a); break;
+    ISEG_RQS(1) ISEG_RQS(2) ISEG_RQS(3) ISEG_RQS(4) ISEG_RQS(5) ISEG_RQS(6) ISEG_RQS(7) ISEG_RQS(8)
+#undef ISEG_RQS
+    }
+    return launch_ok();
+}
+
 // ---------------------------------------------------------------------------
 // requant of int16-staged sums: element (m, n) of a [rows][cols] tensor holds
 // floor(acc / 2^t) with t = tshift of its tile (rows in runs of tile_rows, or

@@ -299,6 +299,36 @@ def test_conv_fwd_full_size_sampled(orc, dev, s):
     assert ev(ye) == rce and np.array_equal(H(y).astype(np.int64), rc)
 
 
+@pytest.mark.parametrize("s", [(8, 32, 32, 2048, 256, 3, 1, 6, 6), (8, 64, 64, 128, 512, 1, 1, 0, 1)], ids=str)
+def test_conv_bwd_weight_full_size_sampled(orc, dev, s):
+    """Full-size weight gradients whose reduction is split over blocks: raw
+    sums at sampled weights against exact dot products over every output
+    pixel, and Q_G (kept and dropped scale) of the whole tensor against the
+    oracle's requant of the raw sums."""
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    P, Q = orc.conv_out_hw(_geom(s))
+    dy = synth.int_codes(94, (N, P, Q, K))
+    x = synth.int_codes(95, (N, Hh, W, Cc))
+    raw, re = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (K, R, R, Cc),
+                                   st, pad, d, g_mode=iseg.ISEG_G_RAW)
+    R_ = H(raw)
+    rng = synth.rng(96)
+    xp = np.zeros((N, Hh + 2 * pad, W + 2 * pad, Cc), np.int64)
+    xp[:, pad:pad + Hh, pad:pad + W, :] = x
+    dyl = dy.astype(np.int64)
+    for _ in range(12):
+        k, r, t, c = (int(rng.integers(K)), int(rng.integers(R)), int(rng.integers(R)), int(rng.integers(Cc)))
+        win = xp[:, r * d:r * d + (P - 1) * st + 1:st, t * d:t * d + (Q - 1) * st + 1:st, c]
+        assert int(R_[k, r, t, c]) == int((dyl[..., k] * win).sum()), (k, r, t, c)
+    for mode, keep in ((iseg.ISEG_G_KEEP, True), (iseg.ISEG_G_DROP, False)):
+        g, ge = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (K, R, R, Cc),
+                                     st, pad, d, g_mode=mode, seed=77, tensor_id=48, step=5)
+        rc, rce = orc.requant(R_.astype(np.int64), ev(re), 8, stochastic=True, keep_scale=keep, seed=77,
+                              tensor_id=48, step=5)
+        assert np.array_equal(H(g).astype(np.int64), rc) and ev(ge) == rce
+
+
 def test_conv_zero_input(orc, dev):
     from paper_2011_14504_amd import iseg
     x = np.zeros((1, 8, 8, 16), np.int8)
