@@ -356,6 +356,42 @@ __device__ __attribute__((aligned(64))) int8_t g_conv_zero[64];
 #define ISEG_IGEMM_STAGES 3      // LDS stages of the direct-to-LDS implicit GEMM
 #endif
 constexpr int kStages = ISEG_IGEMM_STAGES;
+#ifndef ISEG_IGEMM_TAPSKIP
+#define ISEG_IGEMM_TAPSKIP 1     // skip the taps that read only padding for a whole tile (stride 1)
+#endif
+
+// Taps of a stride-1 conv that read only padding for every row of the tile
+// [m0, m0 + rows): the source pixel is the output pixel shifted by a per-tap
+// constant (r dh - ph forward; ph - r dh for backward-data), so a tap is
+// empty when the tile's output-row or output-column range, shifted, misses
+// the source extent.  A tile crossing an image (row) keeps the full row
+// (column) range.  Returns the mask of taps to run.
+template <int MODE>
+__device__ __forceinline__ uint64_t live_taps(const IgemmArgs& a, int64_t m0, int rows)
+{
+    const int RS = a.R * a.S;                 // <= 64 (igemm_dma_ok)
+    const uint64_t all = RS == 64 ? ~0ull : (1ull << RS) - 1;
+    if (!ISEG_IGEMM_TAPSKIP || RS == 1 || a.sh != 1 || a.sw != 1) return all;
+    const int64_t m1 = m0 + rows - 1;
+    const int64_t hw = (int64_t)a.Ho * a.Wo;
+    const int64_t n0 = m0 / hw, n1 = m1 / hw;
+    const int32_t p0 = (int32_t)(m0 - n0 * hw), p1 = (int32_t)(m1 - n1 * hw);
+    int oh_lo = p0 / a.Wo, oh_hi = p1 / a.Wo;
+    int ow_lo = p0 - oh_lo * a.Wo, ow_hi = p1 - oh_hi * a.Wo;
+    if (n0 != n1) { oh_lo = 0; oh_hi = a.Ho - 1; }
+    if (n0 != n1 || oh_lo != oh_hi) { ow_lo = 0; ow_hi = a.Wo - 1; }
+    uint64_t mask = 0;
+    for (int r = 0; r < a.R; r++) {
+        const int cr = MODE == MODE_FWD ? r * a.dh - a.ph : a.ph - r * a.dh;
+        if (oh_hi + cr < 0 || oh_lo + cr >= a.Hs) continue;
+        for (int t = 0; t < a.S; t++) {
+            const int cs = MODE == MODE_FWD ? t * a.dw - a.pw : a.pw - t * a.dw;
+            if (ow_hi + cs < 0 || ow_lo + cs >= a.Ws) continue;
+            mask |= 1ull << (r * a.S + t);
+        }
+    }
+    return mask;
+}
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -433,7 +469,12 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
     const int64_t m0 = (int64_t)bx * BM;
     const int n0 = blockIdx.y * BN;
     const int nchunk = a.Ci / BK;
-    const int nk_all = a.R * a.S * nchunk;
+    // the taps this tile runs (all but those reading only padding), in order;
+    // the steps are (live tap, chunk) pairs, tap-major
+    const int RS = a.R * a.S;
+    const int64_t vr = a.Mrows - m0;
+    const uint64_t tmask = live_taps<MODE>(a, m0, vr < BM ? (int)vr : BM);
+    const int nk_all = __builtin_popcountll(tmask) * nchunk;
     // split of the reduction (blockIdx.z of gridDim.z): steps [kb0, kb0 + nk)
     const int kb0 = (int)((int64_t)nk_all * blockIdx.z / gridDim.z);
     const int nk = (int)((int64_t)nk_all * (blockIdx.z + 1) / gridDim.z) - kb0;
@@ -446,8 +487,7 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
     for (int j = 0; j < NA; j++) rp[j] = row_pix32(a, m0 + 16 * (wave + 4 * j) + rin);
     const int8_t* brow[NB];
 #pragma unroll
-    for (int j = 0; j < NB; j++)
-        brow[j] = a.wmat + (int64_t)(n0 + 16 * (wave + 4 * j) + rin) * a.Kred + (int64_t)kb0 * BK + part * 16;
+    for (int j = 0; j < NB; j++) brow[j] = a.wmat + (int64_t)(n0 + 16 * (wave + 4 * j) + rin) * a.Kred + part * 16;
 
     int64_t soff[NA];
     auto set_tap = [&](int tap) {
@@ -458,7 +498,13 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
             soff[j] = sp < 0 ? -1 : sp * a.Ci + part * 16;
         }
     };
-    int ltap = kb0 / nchunk, lcc = kb0 - (kb0 / nchunk) * nchunk;   // step being issued
+    // (tap, chunk) of the step being issued: the (kb0 / nchunk)-th live tap
+    int ltap = 0, lcc = kb0 - (kb0 / nchunk) * nchunk;
+    {
+        uint64_t mm = tmask;
+        for (int i = kb0 / nchunk; i > 0 && mm; i--) mm &= mm - 1;
+        ltap = mm ? __builtin_ctzll(mm) : RS;
+    }
     auto issue = [&](int kb) {               // kb: step within this split
         int8_t* st = smem + (kb % kStages) * (SA + SB);
 #pragma unroll
@@ -466,9 +512,15 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
             const void* g = soff[j] >= 0 ? (const void*)(a.src + soff[j] + lcc * BK) : (const void*)g_conv_zero;
             dma16(g, st + (wave + 4 * j) * 1024);
         }
+        const int64_t boff = (int64_t)ltap * a.Ci + lcc * BK;
 #pragma unroll
-        for (int j = 0; j < NB; j++) dma16(brow[j] + (int64_t)kb * BK, st + SA + (wave + 4 * j) * 1024);
-        if (++lcc == nchunk) { lcc = 0; if (++ltap < a.R * a.S) set_tap(ltap); }
+        for (int j = 0; j < NB; j++) dma16(brow[j] + boff, st + SA + (wave + 4 * j) * 1024);
+        if (++lcc == nchunk) {
+            lcc = 0;
+            const uint64_t rest = ltap + 1 < 64 ? tmask >> (ltap + 1) : 0ull;
+            ltap = rest ? ltap + 1 + __builtin_ctzll(rest) : RS;
+            if (ltap < RS) set_tap(ltap);
+        }
     };
 
     const int wm = wave >> 1, wn = wave & 1;
@@ -2206,7 +2258,7 @@ int halo_q8(const HaloPlan& p, HaloArgs h, int kid, const int32_t* exp_a, const 
 // whenever the result is requantized
 bool igemm_dma_ok(const IgemmArgs& a)
 {
-    return a.Mrows > 0 && a.Mrows < ((int64_t)1 << 31) && a.Ci % 64 == 0 && a.Nout % 64 == 0 &&
+    return a.Mrows > 0 && a.Mrows < ((int64_t)1 << 31) && a.Ci % 64 == 0 && a.Nout % 64 == 0 && a.R * a.S <= 64 &&
            (((uintptr_t)a.src | (uintptr_t)a.wmat) & 15) == 0;
 }
 size_t staged_ws_bytes(int64_t rows, int64_t cols)
