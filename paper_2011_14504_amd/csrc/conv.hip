@@ -53,6 +53,7 @@ struct IgemmArgs {
     int32_t Hs, Ws, Ho, Wo;
     int32_t R, S;
     int32_t sh, sw, ph, pw, dh, dw;
+    int32_t tap_balance;          // every tile skips a tap: split its live steps evenly
 };
 
 struct RowPix {
@@ -367,7 +368,7 @@ constexpr int kStages = ISEG_IGEMM_STAGES;
 // the source extent.  A tile crossing an image (row) keeps the full row
 // (column) range.  Returns the mask of taps to run.
 template <int MODE>
-__device__ __forceinline__ uint64_t live_taps(const IgemmArgs& a, int64_t m0, int rows)
+__host__ __device__ __forceinline__ uint64_t live_taps(const IgemmArgs& a, int64_t m0, int rows)
 {
     const int RS = a.R * a.S;                 // <= 64 (igemm_dma_ok)
     const uint64_t all = RS == 64 ? ~0ull : (1ull << RS) - 1;
@@ -469,15 +470,30 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
     const int64_t m0 = (int64_t)bx * BM;
     const int n0 = blockIdx.y * BN;
     const int nchunk = a.Ci / BK;
-    // the taps this tile runs (all but those reading only padding), in order;
-    // the steps are (live tap, chunk) pairs, tap-major
+    // the taps this tile runs (all but those reading only padding).  Steps
+    // are (tap, chunk) pairs, tap-major; a split (blockIdx.z of gridDim.z)
+    // owns the same step range [kb0, kb1) in every tile, so the blocks of one
+    // split read one slice of W (shared in L2), and runs the live steps in it.
     const int RS = a.R * a.S;
     const int64_t vr = a.Mrows - m0;
     const uint64_t tmask = live_taps<MODE>(a, m0, vr < BM ? (int)vr : BM);
-    const int nk_all = __builtin_popcountll(tmask) * nchunk;
-    // split of the reduction (blockIdx.z of gridDim.z): steps [kb0, kb0 + nk)
-    const int kb0 = (int)((int64_t)nk_all * blockIdx.z / gridDim.z);
-    const int nk = (int)((int64_t)nk_all * (blockIdx.z + 1) / gridDim.z) - kb0;
+    // When every tile skips a tap (tap_balance, decided on the host) the live
+    // steps themselves are split evenly: the splits of one tile then stay
+    // balanced, at the cost of W slices that differ between tiles.
+    const int nk_full = a.tap_balance ? __builtin_popcountll(tmask) * nchunk : RS * nchunk;
+    const int kb0 = (int)((int64_t)nk_full * blockIdx.z / gridDim.z);
+    const int kb1 = (int)((int64_t)nk_full * (blockIdx.z + 1) / gridDim.z);
+    int nk = 0;
+    if (a.tap_balance) {
+        nk = kb1 - kb0;
+    } else {
+        for (int t = 0; t < RS; t++) {
+            if (!((tmask >> t) & 1)) continue;
+            const int lo = kb0 > t * nchunk ? kb0 : t * nchunk;
+            const int hi = kb1 < (t + 1) * nchunk ? kb1 : (t + 1) * nchunk;
+            nk += hi > lo ? hi - lo : 0;
+        }
+    }
 
     // this lane's DMA pieces: row (16 * instr + lane / 4) in slot lane % 4
     const int rin = lane >> 2;
@@ -498,12 +514,17 @@ __global__ __launch_bounds__(256) void k_conv_igemm_dma(IgemmArgs a)
             soff[j] = sp < 0 ? -1 : sp * a.Ci + part * 16;
         }
     };
-    // (tap, chunk) of the step being issued: the (kb0 / nchunk)-th live tap
-    int ltap = 0, lcc = kb0 - (kb0 / nchunk) * nchunk;
-    {
+    // (tap, chunk) of the step being issued: balanced, the (kb0 / nchunk)-th
+    // live tap; aligned, the first live step at or after kb0
+    int ltap = kb0 / nchunk, lcc = kb0 - (kb0 / nchunk) * nchunk;
+    if (a.tap_balance) {
         uint64_t mm = tmask;
         for (int i = kb0 / nchunk; i > 0 && mm; i--) mm &= mm - 1;
         ltap = mm ? __builtin_ctzll(mm) : RS;
+    } else if (ltap < RS && !((tmask >> ltap) & 1)) {
+        const uint64_t rest = ltap + 1 < 64 ? tmask >> (ltap + 1) : 0ull;
+        ltap = rest ? ltap + 1 + __builtin_ctzll(rest) : RS;
+        lcc = 0;
     }
     auto issue = [&](int kb) {               // kb: step within this split
         int8_t* st = smem + (kb % kStages) * (SA + SB);
@@ -2505,11 +2526,29 @@ __global__ void k_exp_sum(int32_t* out, const int32_t* a, const int32_t* b);
 // and a 16-byte aligned output): raw sums, or final codes by two passes,
 // split partials + reduce + requant, or int16 staging + requant.  `work` is
 // the int32 / staging region of the workspace, `pmax` its max partials.
+// true when every row tile of the plan skips at least one tap (the same test
+// as the kernel's, over all tiles on the host)
+template <int MODE>
+bool every_tile_skips(const IgemmArgs& a, int bm)
+{
+    const int RS = a.R * a.S;
+    if (!ISEG_IGEMM_TAPSKIP || RS == 1 || RS > 64 || a.sh != 1 || a.sw != 1) return false;
+    const uint64_t all = RS == 64 ? ~0ull : (1ull << RS) - 1;
+    const int64_t nt = ceil_div64(a.Mrows, bm);
+    if (nt > 65536) return false;
+    for (int64_t t = 0; t < nt; t++) {
+        const int64_t m0 = t * bm, vr = a.Mrows - m0;
+        if (live_taps<MODE>(a, m0, vr < bm ? (int)vr : bm) == all) return false;
+    }
+    return true;
+}
+
 template <int MODE>
 int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t* exp_b, void* y,
                   int32_t* y_exp, uint64_t* pmax, int32_t* work, hipStream_t s)
 {
     const DmaPlan p = dma_plan(a.Mrows, a.Nout, a.Kred, out_mode == ISEG_OUT_Q8);
+    a.tap_balance = every_tile_skips<MODE>(a, p.bm) ? 1 : 0;
     int rc;
     int64_t nblk = 0;
     a.out16 = nullptr;
