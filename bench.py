@@ -124,7 +124,7 @@ def copy_kernel(mib):
     print(json.dumps({"copy_kernel_bytes_read": n * 4, "copy_kernel_bytes_written": n * 4}))
 
 
-def cpu_baseline(wl, sample_hw):
+def cpu_baseline(wl, sample_hw, widths=None):
     """The oracle's whole training step on one image at sample_hw x sample_hw,
     timed on the host cores; scaled to the benchmark's unit by the ratio of
     valid-tap conv ops."""
@@ -133,7 +133,7 @@ def cpu_baseline(wl, sample_hw):
     from paper_2011_14504_amd import synth
     small = synth.scaled(wl, 1, sample_hw, sample_hw)
     inp = synth.workload_inputs(small)
-    net = OracleNet(small, inp)
+    net = OracleNet(small, inp, **(widths or {}))
     t0 = time.perf_counter()
     net.step()
     dt = time.perf_counter() - t0
@@ -154,6 +154,10 @@ def main():
     ap.add_argument("--batch", type=int, default=None)
     ap.add_argument("--cpu-sample-hw", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--k-w", type=int, default=8, help="weight code width k_W (Table 1 rows: 8, 4)")
+    ap.add_argument("--k-a", type=int, default=8, help="activation code width k_A")
+    ap.add_argument("--k-e2", type=int, default=16, help="BN error width k_E2 (8 or 16)")
+    ap.add_argument("--k-u", type=int, default=24, help="master / update width k_U")
     ap.add_argument("--copy-kernel-mib", type=int, default=0,
                     help="only run the plain copy kernel used to calibrate the HBM byte counters")
     ap.add_argument("--timed-kernel", default="conv_fwd:aspp.b1",
@@ -176,7 +180,8 @@ def main():
     wl = synth.scaled(synth.WORKLOADS[WORKLOAD_IDS[args.workload]], args.batch)
     N = wl["N"]
     inp = synth.workload_inputs(wl)
-    net = IntNet(wl, inp, "cuda:0")
+    widths = dict(k_W=args.k_w, k_U=args.k_u, bn_cfg={"k_A": args.k_a, "k_E2": args.k_e2})
+    net = IntNet(wl, inp, "cuda:0", **widths)
     ops, detail = workload_ops(wl)
     tk = args.timed_kernel
     if args.workload != "deeplabv3" and tk == "conv_fwd:aspp.b1":
@@ -218,7 +223,8 @@ def main():
     prof.close()
     cfg = dict(workload=wl["name"], batch=N, image=f"{wl['H']}x{wl['W']}",
                convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
-               pct_int8_peak=100.0 * value / INT8_PEAK_TOPS)
+               pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
+               bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u))
     if net.loss is not None:
         cfg["loss"] = float(net.loss.item())
     out = dict(metric=METRIC, value=value, unit="TOPS", n_gpus=1, steps=args.steps,
@@ -226,7 +232,7 @@ def main():
                vs_baseline=None, dtype="int8", data="synthetic", config=cfg, roofline=roof)
     if not args.no_cpu_baseline:
         sample = args.cpu_sample_hw if wl["H"] > args.cpu_sample_hw else wl["H"]
-        out["cpu_baseline"] = cpu_baseline(wl, sample)
+        out["cpu_baseline"] = cpu_baseline(wl, sample, widths)
     print(json.dumps(out))
 
 

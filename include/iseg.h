@@ -74,7 +74,8 @@ enum iseg_status {
 /* bits OR-ed into *dev_status by kernels */
 enum iseg_dev_status {
     ISEG_DEV_RANGE = 1,        /* an exponent outside its documented range */
-    ISEG_DEV_NONFINITE = 4     /* a NaN or infinity in a float input */
+    ISEG_DEV_NONFINITE = 4,    /* a NaN or infinity in a float input */
+    ISEG_DEV_DESC = 8          /* a device descriptor field out of range (entry skipped) */
 };
 
 enum iseg_dtype { ISEG_I8 = 0, ISEG_I16 = 1, ISEG_I32 = 2, ISEG_I64 = 3 };
@@ -324,7 +325,10 @@ typedef struct iseg_update_desc {
     int32_t kind;          /* enum iseg_update_kind */
     int32_t master_exp;    /* 1-k_U for conv weights, 2-k_U for gamma / beta (x2 fold) */
     uint32_t tensor_id;    /* ISEG_UPD_RAW: Philox tensor id of Q_G */
-    int32_t reserved;
+    int32_t k_w;           /* code width of w_q for this tensor, 2..8 (k_W of conv
+                              weights, k_gamma / k_beta of Sec. 3.2's BN); 0 = the
+                              call's k_W.  Out of range: the entry is left as it
+                              was and ISEG_DEV_DESC is set in *dev_status */
 } iseg_update_desc;
 
 /* iseg_update_multi -- the update step of a whole network in one launch: for
@@ -332,8 +336,8 @@ typedef struct iseg_update_desc {
  * scale, Eq. 5-6 and 17, Philox index = the element, key (seed, tensor_id),
  * counter step), then Delta = UQ(G 2^-lr_shift, k_U) (Eq. 19), master <-
  * clamp(master - Delta), w_q = UQ(master, k_W) (Eq. 8, or Eq. 14's fold for
- * gamma / beta).  Equal to iseg_weight_update / iseg_bn_param_update per
- * tensor.  descs: device array of n_desc <= 4096 descriptors (caller-owned;
+ * gamma / beta; k_W per descriptor, see k_w).  Equal to iseg_weight_update
+ * / iseg_bn_param_update per tensor.  descs: device array of n_desc <= 4096 descriptors (caller-owned;
  * the tensors they point to must not overlap). */
 int iseg_update_multi(const iseg_update_desc* descs, int32_t n_desc, int32_t bits, uint64_t seed,
                       uint32_t step, int32_t lr_shift, int32_t k_U, int32_t k_W, int32_t* dev_status,

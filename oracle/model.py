@@ -13,7 +13,15 @@ paper's dataflow (Sec. 3):
             nodes is SQ8 of the exact sum of what they send back (Eq. 16);
             L1BN backward -> G = Q_G(sum dy x) (Eq. 17, stochastic), E1 =
             Q_E(sum dy w) (Eq. 16), Q_G of the raw dgamma / dbeta sums
-  update    Eq. 19 on the 24-bit masters (lr = 2^-lr_shift), then Eq. 8
+  update    Eq. 19 on the k_U-bit masters (lr = 2^-lr_shift), then Eq. 8
+
+Bit widths (Table 1's rows): k_W for conv weights (W = code 2^(1-k_W)), k_U
+for the masters (Eq. 7, 19), k_gamma / k_beta of the BN configuration for the
+BN parameters, and k_A for every activation a conv reads: Q_A of the BN
+output, the output of a conv without BN, and the forward merges (residual
+add, concatenation, global pooling).  A conv feeding BN keeps its output at 8
+bits (BN's input), max pooling keeps codes, and errors and gradients stay at
+8 bits (k_E1 = k_G = 8 in every row of Table 1).
 
 Stochastic rounding keys: workload seed, step, tensor id 16*l + {0,1,2} for
 W, gamma, beta of the l-th conv (l = 1, 2, ... in node order).
@@ -22,34 +30,33 @@ import numpy as np
 
 from . import oracle as O
 
-K_U, K_W = 24, 8
-
-
 class OracleNet:
-    def __init__(self, wl, inputs, lr_shift=10, bn_cfg=None):
+    def __init__(self, wl, inputs, lr_shift=10, bn_cfg=None, k_W=8, k_U=24):
         self.wl = wl
         self.lr_shift = lr_shift
+        self.k_W, self.k_U = k_W, k_U
         self.seed = inputs["seed"]
         self.cfg = dict(O.BN_DEFAULT, **(bn_cfg or {}))
         self.step_no = 0
         self.x, self.x_exp = inputs["x"], inputs["x_exp"]
         self.dy, self.dy_exp = inputs.get("dy"), inputs.get("dy_exp")
         self.labels = inputs.get("labels")
-        self.w_exp = 1 - K_U + K_U - K_W          # -7
+        self.k_A = self.cfg["k_A"]
+        self.w_exp = 1 - k_W                      # Eq. 8: UQ to k_W bits
         self.convs = {}
         ci = 0
         for nd in wl["nodes"]:
             if nd["kind"] != "conv":
                 continue
-            w_m, e = O.master_init(inputs["weights"][ci], K_U)   # Eq. 7
+            w_m, e = O.master_init(inputs["weights"][ci], k_U)   # Eq. 7
             ci += 1
             cout = nd["cout"]
-            g_m = np.full(cout, 1 << (K_U - 2), np.int32)           # gamma = 1 at 2^-22
+            g_m = np.full(cout, 1 << (k_U - 2), np.int32)           # gamma = 1 at 2^(2-k_U)
             b_m = np.zeros(cout, np.int32)
             self.convs[nd["name"]] = dict(l=ci, w_m=w_m, g_m=g_m, b_m=b_m,
-                                          w_q=O.weight_quant(w_m, K_U, K_W),
-                                          g_q=O.weight_quant(g_m, K_U, K_W),
-                                          b_q=O.weight_quant(b_m, K_U, K_W))
+                                          w_q=O.weight_quant(w_m, k_U, k_W),
+                                          g_q=O.weight_quant(g_m, k_U, self.cfg["k_gamma"]),
+                                          b_q=O.weight_quant(b_m, k_U, self.cfg["k_beta"]))
         self.loss = None
 
     def _bn_cfg(self, nd):
@@ -71,7 +78,9 @@ class OracleNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd))
+                # Z feeds BN at 8 bits; without BN it is the activation (Q_A)
+                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd),
+                                   8 if nd["bn"] else self.k_A)
                 z = z.astype(np.int8)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
@@ -83,17 +92,18 @@ class OracleNet:
                 y, ye = O.maxpool_fwd(a, nd["k"], nd["stride"], nd["pad"]), ae
             elif k == "add":
                 b_, be = act[nd["src"][1]]
-                y, ye = O.sum_requant([a, b_], [ae, be], 8, relu=nd["relu"])
+                y, ye = O.sum_requant([a, b_], [ae, be], self.k_A, relu=nd["relu"])
                 y = y.astype(np.int8)
                 r.update(b_in=b_, b_in_exp=be)
             elif k == "gap":
-                y, ye = O.gap_fwd(a, ae)
+                y, ye = O.gap_fwd(a, ae, self.k_A)
                 y = y.astype(np.int8)
             elif k == "concat":
                 parts = [act[s] for s in nd["src"]]
                 H = max(p[0].shape[1] for p in parts)
                 W = max(p[0].shape[2] for p in parts)
-                y, ye = O.concat_requant([p[0] for p in parts], [p[1] for p in parts], (H, W))
+                y, ye = O.concat_requant([p[0] for p in parts], [p[1] for p in parts], (H, W),
+                                         self.k_A)
                 y = y.astype(np.int8)
                 r.update(widths=[p[0].shape[3] for p in parts],
                          bcast=[p[0].shape[1:3] != (H, W) for p in parts])
@@ -195,15 +205,16 @@ class OracleNet:
         return grads
 
     def update(self, grads):
+        k_U, k_W, cf = self.k_U, self.k_W, self.cfg
         for nd, r in grads:
             L = self.convs[nd["name"]]
             L["w_m"], L["w_q"] = O.weight_update(L["w_m"], r["G"], r["G_exp"], self.lr_shift,
-                                                 1 - K_U, K_U, K_W)
+                                                 1 - k_U, k_U, k_W)
             if nd["bn"]:
                 L["g_m"], L["g_q"] = O.weight_update(L["g_m"], r["Gg"], r["Gg_exp"], self.lr_shift,
-                                                     2 - K_U, K_U, K_W)
+                                                     2 - k_U, k_U, cf["k_gamma"])
                 L["b_m"], L["b_q"] = O.weight_update(L["b_m"], r["Gb"], r["Gb_exp"], self.lr_shift,
-                                                     2 - K_U, K_U, K_W)
+                                                     2 - k_U, k_U, cf["k_beta"])
 
     def step(self):
         rec = self.forward()

@@ -612,7 +612,7 @@ constexpr int kUpdChunk = 4096;
 constexpr int kUpdMaxDesc = 4096;
 
 __global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __restrict__ descs, int n_desc,
-                                                      UpdCfg u)
+                                                      UpdCfg u, int32_t* __restrict__ dev_status)
 {
     __shared__ int32_t first[kUpdMaxDesc + 1];
     __shared__ int32_t tot[256];
@@ -649,7 +649,6 @@ __global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __
         __syncthreads();
     }
     const int nchunks = first[n_desc];
-    const int dq = u.k_U - u.k_W;
     const int64_t lim = ((int64_t)1 << (u.k_U - 1)) - 1;
     for (int ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
         int lo = 0, hi = n_desc - 1;                 // last descriptor with first <= ch
@@ -659,6 +658,12 @@ __global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __
             else hi = mid - 1;
         }
         const iseg_update_desc d = descs[lo];
+        const int kw = d.k_w ? d.k_w : u.k_W;                        // Q_W width of this tensor
+        if (kw < 2 || kw > 8) {
+            if (threadIdx.x == 0) set_status(dev_status, ISEG_DEV_DESC);
+            continue;
+        }
+        const int dq = u.k_U - kw;
         if (d.kind == ISEG_UPD_CODES) {
             const int8_t* g = (const int8_t*)d.g;
             const int sh = *d.g_exp - u.lr_shift - d.master_exp;      // Delta W code = g 2^sh, rounded
@@ -667,7 +672,7 @@ __global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __
             for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
                 const int64_t m = clamp_k((int64_t)d.master[i] - upd_delta(g[i], sh, u.k_U, lim), u.k_U);
                 d.master[i] = (int32_t)m;
-                d.w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), u.k_W);
+                d.w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), kw);
             }
             continue;
         }
@@ -693,7 +698,7 @@ __global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __
             if (d.g_q) d.g_q[c] = (int8_t)q;
             const int64_t mm = clamp_k((int64_t)d.master[c] - upd_delta(q, sh, u.k_U, lim), u.k_U);
             d.master[c] = (int32_t)mm;
-            d.w_q[c] = (int8_t)clamp_k(shr_rhu(mm, dq), u.k_W);
+            d.w_q[c] = (int8_t)clamp_k(shr_rhu(mm, dq), kw);
         }
     }
 }
@@ -702,13 +707,13 @@ extern "C" int iseg_update_multi(const iseg_update_desc* descs, int32_t n_desc, 
                                  uint32_t step, int32_t lr_shift, int32_t k_U, int32_t k_W, int32_t* dev_status,
                                  hipStream_t stream)
 {
-    (void)dev_status;
     if (n_desc < 0 || n_desc > kUpdMaxDesc || (n_desc > 0 && !descs)) return ISEG_ERR_ARG;
     if (bits < 2 || bits > 8 || k_U < 9 || k_U > 31 || k_W < 2 || k_W > 8) return ISEG_ERR_ARG;
     if (n_desc == 0) return ISEG_OK;
     UpdCfg u;
     u.seed = seed; u.step = step; u.bits = bits; u.lr_shift = lr_shift; u.k_U = k_U; u.k_W = k_W;
-    hipLaunchKernelGGL(k_update_multi, dim3(2048), dim3(256), 0, stream, descs, (int)n_desc, u);
+    hipLaunchKernelGGL(k_update_multi, dim3(2048), dim3(256), 0, stream, descs, (int)n_desc, u,
+                       dev_status);
     return launch_ok();
 }
 

@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "lib", "libiseg.so")
 
 ISEG_OK, ISEG_ERR_ARG, ISEG_ERR_SHAPE, ISEG_ERR_UNSUPPORTED, ISEG_ERR_WORKSPACE, ISEG_ERR_DEVICE = range(6)
-ISEG_DEV_RANGE, ISEG_DEV_NONFINITE = 1, 4
+ISEG_DEV_RANGE, ISEG_DEV_NONFINITE, ISEG_DEV_DESC = 1, 4, 8
 ISEG_I8, ISEG_I16, ISEG_I32, ISEG_I64 = range(4)
 ISEG_Q_UQ, ISEG_Q_SQ = 0, 1
 ISEG_OUT_Q8, ISEG_OUT_RAW = 0, 1
@@ -43,7 +43,7 @@ class ConvGeom(C.Structure):
 class UpdateDesc(C.Structure):
     _fields_ = [("master", C.c_void_p), ("w_q", C.c_void_p), ("g", C.c_void_p), ("g_exp", C.c_void_p),
                 ("g_q", C.c_void_p), ("g_q_exp", C.c_void_p), ("n", C.c_int64), ("kind", C.c_int32),
-                ("master_exp", C.c_int32), ("tensor_id", C.c_uint32), ("reserved", C.c_int32)]
+                ("master_exp", C.c_int32), ("tensor_id", C.c_uint32), ("k_w", C.c_int32)]
 
 
 ISEG_UPD_CODES, ISEG_UPD_RAW = 0, 1
@@ -499,9 +499,15 @@ def bn_cfg(**kw):
                                   "k_E2", "eps_code", "relu")])
 
 
-def quantize(x, bits, mode=ISEG_Q_SQ, status=None):
-    dt = {8: (torch.int8, ISEG_I8), 16: (torch.int16, ISEG_I16)}.get(
-        8 if bits <= 8 else 16 if bits <= 16 else 32, (torch.int32, ISEG_I32))
+def quantize(x, bits, mode=ISEG_Q_SQ, status=None, out_dtype=None):
+    """Codes in the narrowest of int8 / int16 / int32 that holds `bits`, or in
+    out_dtype (a torch integer dtype at least that wide)."""
+    w = 8 if bits <= 8 else 16 if bits <= 16 else 32
+    if out_dtype is not None:
+        w = {torch.int8: 8, torch.int16: 16, torch.int32: 32}[out_dtype]
+        if (w == 8 and bits > 8) or (w == 16 and bits > 16):
+            raise ValueError("out_dtype too narrow for bits")
+    dt = {8: (torch.int8, ISEG_I8), 16: (torch.int16, ISEG_I16), 32: (torch.int32, ISEG_I32)}[w]
     out = torch.empty(x.shape, dtype=dt[0], device=x.device)
     e = _out_exp(x.device)
     ws = workspace(x.device).get(lib().iseg_quantize_ws(x.numel()))
@@ -762,7 +768,8 @@ def wt_table(entries, device):
 def update_table(entries, device):
     """Device array of iseg_update_desc for iseg_update_multi.  entries: dicts
     with master, w_q, g, g_exp, kind, master_exp and, for ISEG_UPD_RAW,
-    tensor_id, g_q, g_q_exp (torch tensors; their storage must stay alive)."""
+    tensor_id, g_q, g_q_exp (torch tensors; their storage must stay alive);
+    optional k_w, the tensor's own Q_W width (0 = the call's k_W)."""
     n = len(entries)
     host = (UpdateDesc * max(n, 1))()
     for i, e in enumerate(entries):
@@ -777,5 +784,6 @@ def update_table(entries, device):
         d.kind = e["kind"]
         d.master_exp = e["master_exp"]
         d.tensor_id = e.get("tensor_id", 0)
+        d.k_w = e.get("k_w", 0)
     raw = torch.frombuffer(bytearray(bytes(host)), dtype=torch.uint8)
     return raw.to(device), n

@@ -11,8 +11,15 @@ Backward, in reverse node order:  the error of a tensor read by several nodes
 is SQ8 of the exact sum of their contributions (Eq. 16); L1BN backward (E2) ->
 G = Q_G(conv_bwd_weight) (Eq. 17, stochastic) and E1 = Q_E(conv_bwd_data);
 the raw dgamma / dbeta sums go through Q_G too.
-Update, after the backward:  Eq. 19 on the 24-bit masters of W, gamma and
+Update, after the backward:  Eq. 19 on the k_U-bit masters of W, gamma and
 beta (learning rate 2^-lr_shift), then Q_W.
+
+Bit widths (Table 1's rows): k_W for conv weights, k_U for the masters,
+k_gamma / k_beta of the BN configuration for the BN parameters (their own
+width in the update table), k_A for every activation a conv reads (Q_A of the
+BN output, a conv output without BN, the forward merges).  A conv feeding BN
+keeps its output at 8 bits; errors and gradients stay at 8 bits.  Codes of
+fewer than 8 bits run through the same int8 kernels.
 
 Stochastic rounding keys: seed of the workload, step counter, tensor id
 16*l + {0: W, 1: gamma, 2: beta} for the l-th conv (l = 1, 2, ... in node
@@ -22,19 +29,20 @@ import torch
 
 from . import iseg
 
-K_U, K_W = 24, 8
-W_MASTER_EXP = 1 - K_U          # -23
-GB_MASTER_EXP = 2 - K_U         # -22: gamma/beta quantizers carry the x2 fold
-
-
 class IntNet:
-    def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None):
+    def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24):
+        if not (2 <= k_W <= 8 and 9 <= k_U <= 31):
+            raise ValueError("k_W must be in [2, 8] and k_U in [9, 31]")
         self.wl = wl
+        self.k_W, self.k_U = k_W, k_U
+        self.w_master_exp = 1 - k_U             # Eq. 7
+        self.gb_master_exp = 2 - k_U            # gamma/beta quantizers carry the x2 fold
         self.dev = torch.device(device)
         self.lr_shift = lr_shift
         self.seed = inputs["seed"]
         self.cfg = dict(iseg.BN_DEFAULT, **(bn_cfg or {}))
         self._cfgs = {r: iseg.bn_cfg(**dict(self.cfg, relu=r)) for r in (0, 1)}
+        self.k_A = self.cfg["k_A"]
         self.step_no = 0
         # backward-weight runs on a second stream (default priority): each
         # conv's weight gradient only needs its dz and input, so it overlaps
@@ -48,7 +56,7 @@ class IntNet:
             self.dy_exp = iseg.new_exp(self.dev, inputs["dy_exp"])
         else:
             self.labels = torch.from_numpy(inputs["labels"]).to(self.dev)
-        self.w_exp = iseg.new_exp(self.dev, W_MASTER_EXP + K_U - K_W)
+        self.w_exp = iseg.new_exp(self.dev, 1 - k_W)                         # Eq. 8
         self.convs = {}
         ci = 0
         for nd in wl["nodes"]:
@@ -56,15 +64,15 @@ class IntNet:
                 continue
             wf = torch.from_numpy(inputs["weights"][ci]).to(self.dev)
             ci += 1
-            master, mexp = iseg.quantize(wf, K_U, iseg.ISEG_Q_UQ)          # Eq. 7
-            assert int(mexp.item()) == W_MASTER_EXP
+            master, mexp = iseg.quantize(wf, k_U, iseg.ISEG_Q_UQ, out_dtype=torch.int32)   # Eq. 7
+            assert int(mexp.item()) == self.w_master_exp
             cout = nd["cout"]
-            g_m = torch.full((cout,), 1 << (-GB_MASTER_EXP), dtype=torch.int32, device=self.dev)
+            g_m = torch.full((cout,), 1 << (-self.gb_master_exp), dtype=torch.int32, device=self.dev)
             b_m = torch.zeros(cout, dtype=torch.int32, device=self.dev)
             L = dict(l=ci, w_m=master, g_m=g_m, b_m=b_m,
-                     w_q=iseg.weight_quant(master, K_U, K_W),
-                     g_q=iseg.weight_quant(g_m, K_U, K_W),
-                     b_q=iseg.weight_quant(b_m, K_U, K_W),
+                     w_q=iseg.weight_quant(master, k_U, k_W),
+                     g_q=iseg.weight_quant(g_m, k_U, self.cfg["k_gamma"]),
+                     b_q=iseg.weight_quant(b_m, k_U, self.cfg["k_beta"]),
                      # gradient buffers, written every step (fixed addresses for the update table)
                      G=torch.empty(master.shape, dtype=torch.int8, device=self.dev),
                      G_exp=iseg._out_exp(self.dev))
@@ -88,13 +96,15 @@ class IntNet:
                 continue
             L = self.convs[nd["name"]]
             ents.append(dict(master=L["w_m"], w_q=L["w_q"], g=L["G"], g_exp=L["G_exp"],
-                             kind=iseg.ISEG_UPD_CODES, master_exp=W_MASTER_EXP))
+                             kind=iseg.ISEG_UPD_CODES, master_exp=self.w_master_exp))
             if nd["bn"]:
-                for m, q, g, ge, gq, gqe, t in (("g_m", "g_q", "dg", "dg_exp", "Gg", "Gg_exp", 1),
-                                                ("b_m", "b_q", "db", "db_exp", "Gb", "Gb_exp", 2)):
+                for m, q, g, ge, gq, gqe, t, kw in (
+                        ("g_m", "g_q", "dg", "dg_exp", "Gg", "Gg_exp", 1, self.cfg["k_gamma"]),
+                        ("b_m", "b_q", "db", "db_exp", "Gb", "Gb_exp", 2, self.cfg["k_beta"])):
                     ents.append(dict(master=L[m], w_q=L[q], g=L[g], g_exp=L[ge], g_q=L[gq],
                                      g_q_exp=L[gqe], kind=iseg.ISEG_UPD_RAW,
-                                     master_exp=GB_MASTER_EXP, tensor_id=16 * L["l"] + t))
+                                     master_exp=self.gb_master_exp, tensor_id=16 * L["l"] + t,
+                                     k_w=kw))
         self.upd_table, self.upd_n = iseg.update_table(ents, self.dev)
 
     def _build_wt_table(self, rec):
@@ -125,7 +135,12 @@ class IntNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"])
+                if nd["bn"] or self.k_A == 8:
+                    z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"])
+                else:                       # the activation itself: Q_A to k_A bits of the sums
+                    acc, acc_e = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"],
+                                               nd["dil"], out_mode=iseg.ISEG_OUT_RAW)
+                    z, ze = iseg.requant(acc, acc_e, self.k_A)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
                     y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])])
@@ -136,13 +151,13 @@ class IntNet:
                 y, ye = iseg.maxpool_fwd(a, ae, nd["k"], nd["stride"], nd["pad"])
             elif k == "add":
                 b, be = act[nd["src"][1]]
-                y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"])
+                y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"], bits=self.k_A)
                 r.update(b_in=b, b_in_exp=be)
             elif k == "gap":
-                y, ye = iseg.gap_fwd(a, ae)
+                y, ye = iseg.gap_fwd(a, ae, bits=self.k_A)
             elif k == "concat":
                 parts = [act[s] for s in nd["src"]]
-                y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts])
+                y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts], bits=self.k_A)
                 H, W = y.shape[1], y.shape[2]
                 r.update(widths=[p[0].shape[3] for p in parts],
                          bcast=[tuple(p[0].shape[1:3]) != (H, W) for p in parts])
@@ -259,7 +274,7 @@ class IntNet:
     def update(self, grads):
         """Q_G of gamma / beta, Eq. 19 and Q_W for every parameter: one launch."""
         iseg.iseg_update_multi(self.upd_table, self.upd_n, 8, self.seed, self.step_no, self.lr_shift,
-                               K_U, K_W)
+                               self.k_U, self.k_W)
         if self.wt_tab is not None:
             self._transpose_weights()
         for nd, r in grads:

@@ -550,6 +550,40 @@ def test_update_multi_matches_oracle(orc, dev):
             assert np.array_equal(H(e["g_q"]).astype(np.int64), rr[2]) and ev(e["g_q_exp"]) == rr[3]
 
 
+def test_update_multi_per_tensor_width(orc, dev):
+    """k_U = 16 with 4-bit conv weights and 8-bit gamma / beta in one launch
+    (each descriptor's own k_w; 0 takes the call's k_W); an entry whose width
+    is out of range is left untouched and flags ISEG_DEV_DESC."""
+    import torch
+    from paper_2011_14504_amd import iseg
+    r = synth.rng(91)
+    k_U = 16
+    ents, ref = [], []
+    for i, (n, kw) in enumerate(((3 * 3 * 64 * 32, 0), (777, 4), (33, 9))):
+        m = r.integers(-(2 ** 15) + 1, 2 ** 15, size=n).astype(np.int32)
+        g = r.integers(-127, 128, size=n).astype(np.int8)
+        ents.append(dict(master=T(m, dev), w_q=torch.full((n,), 99, dtype=torch.int8, device=dev),
+                         g=T(g, dev), g_exp=E(-18 - i, dev), kind=iseg.ISEG_UPD_CODES,
+                         master_exp=1 - k_U, k_w=kw))
+        ref.append(orc.weight_update(m, g, -18 - i, 6, 1 - k_U, k_U, 4) if kw != 9 else
+                   (m, np.full(n, 99, np.int8)))
+    C = 256
+    m = r.integers(-(2 ** 15) + 1, 2 ** 15, size=C).astype(np.int32)
+    d = r.integers(-(2 ** 30), 2 ** 30, size=C).astype(np.int64)
+    ents.append(dict(master=T(m, dev), w_q=torch.empty(C, dtype=torch.int8, device=dev), g=T(d, dev),
+                     g_exp=E(-28, dev), kind=iseg.ISEG_UPD_RAW, master_exp=2 - k_U, tensor_id=33,
+                     g_q=torch.empty(C, dtype=torch.int8, device=dev), g_q_exp=E(0, dev), k_w=8))
+    gq, gqe = orc.requant(d, -28, 8, True, True, 56, 33, 2)
+    ref.append(orc.weight_update(m, gq, gqe, 6, 2 - k_U, k_U, 8))
+    table, n = iseg.update_table(ents, dev)
+    st = E(0, dev)
+    iseg.iseg_update_multi(table, n, 8, 56, 2, 6, k_U, 4, st)
+    for e, rr in zip(ents, ref):
+        assert np.array_equal(H(e["master"]), rr[0]) and np.array_equal(H(e["w_q"]), rr[1])
+    assert np.abs(H(ents[0]["w_q"]).astype(np.int64)).max() <= 7
+    assert ev(st) == iseg.ISEG_DEV_DESC
+
+
 @pytest.mark.parametrize("C,d_exp", [(64, -30), (128, -12), (2048, -40)])
 def test_bn_param_update(orc, dev, C, d_exp):
     # Q_G (Eq. 17, stochastic) then Q_U (Eq. 19) of gamma/beta in one launch

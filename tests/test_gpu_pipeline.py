@@ -23,17 +23,17 @@ CONV_KEYS = ("z", "dz", "G", "Gg", "Gb", "dgamma", "dbeta")
 EXP_KEYS = ("z_exp", "dz_exp", "G_exp", "Gg_exp", "Gb_exp")
 
 
-def _run_both(wl, steps=1):
+def _run_both(wl, steps=1, **widths):
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from oracle.model import OracleNet
     from paper_2011_14504_amd.model import IntNet
     inp = synth.workload_inputs(wl)
-    gnet = IntNet(wl, inp, "cuda:0")
-    onet = OracleNet(wl, inp)
+    gnet = IntNet(wl, inp, "cuda:0", **widths)
+    onet = OracleNet(wl, inp, **widths)
     for s in range(steps):
-        print(f"[pipeline] {wl['name']} N={wl['N']} {wl['H']}x{wl['W']} step {s}", flush=True)
+        print(f"[pipeline] {wl['name']} N={wl['N']} {wl['H']}x{wl['W']} {widths} step {s}", flush=True)
         grec = gnet.step()
         orec = onet.step()
         torch.cuda.synchronize()
@@ -92,3 +92,33 @@ def test_deeplabv3_r50_128px():
 def test_deeplabv3_r50_ragged_96x80_two_steps():
     # an input size that leaves ragged tiles at every stage (6x5 ASPP map)
     _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 96, 80), steps=2)
+
+
+# Table 1's bit-width rows and Fig. 10's k_U axis: codes of fewer than 8 bits
+# run through the same int8 kernels
+W4A4 = dict(k_W=4, bn_cfg={"k_A": 4, "k_E2": 8})
+
+
+def test_resnet50_conv2x_w4a4_two_steps():
+    _run_both(synth.scaled(synth.RESNET50_CONV2X, 1), steps=2, **W4A4)
+
+
+def test_aspp_head_w4a4():
+    # concat, image pooling and the classifier (a conv without BN: Q_A of its
+    # sums to 4 bits) at k_A = 4
+    _run_both(synth.scaled(synth.ASPP_HEAD, 1), **W4A4)
+
+
+def test_deeplabv3_r50_w4a4_k_e2_8_96x80_two_steps():
+    # the last DeepLab row of Table 1 (W 4, A 4, G 8, E1 8, E2 8, U 24)
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 96, 80), steps=2, **W4A4)
+
+
+def test_deeplabv3_r50_k_e2_8_128px():
+    # the 8-bit row with k_E2 = 8
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 128, 128), bn_cfg={"k_E2": 8})
+
+
+@pytest.mark.parametrize("k_U", [12, 16, 20])
+def test_resnet50_conv2x_k_u_two_steps(k_U):
+    _run_both(synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28), steps=2, k_U=k_U)
