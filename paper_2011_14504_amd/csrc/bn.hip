@@ -23,9 +23,10 @@
 //           -> finsig (n_sigma, den, max|xhat| exponent) -> fin2 (xhat codes,
 //           y, thresholds, max|y|) -> fin3 (A codes) -> apply (table gather).
 // Backward: stats (sum delta, sum delta*xhat, sum sgn, per-class extremes of
-//           delta | tails for k_E2 >= 15: dgamma, dbeta, then E1's exponent)
-//           -> table -> apply (gather).  k_E2 < 15 keeps separate kernels:
-//           fin1 (dgamma, dbeta, max|gamma delta|) -> stats2 -> fin2 -> table.
+//           delta | tails: dgamma, dbeta, then for k_E2 >= 15 E1's exponent)
+//           -> table -> apply (gather).  k_E2 < 15 adds a second streaming
+//           pass: stats tails give max|gamma delta| (E2's scale), stats2 sums
+//           the rounded E2 terms and its tails give E1's exponent.
 #include "iseg_common.h"
 
 namespace {
@@ -776,8 +777,10 @@ struct BnbOut {
 
 __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
                                                const BnCfg& cf, const BnbOut& o);
+__device__ __forceinline__ void bnb_round_tail1(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
+                                                const BnCfg& cf, const BnbOut& o);
 
-template <bool TAIL>
+template <int TAIL>                      // 0: none, 1: exact E2, 2: rounding E2
 __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                    Saved sv, BnCfg cf, BnbOut out)
@@ -912,59 +915,10 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
             for (int k = 0; k < 6; k++) w.p_mm[k * pc + o] = sMM[threadIdx.x * 6 + k];
         }
     }
-    if (TAIL && arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) bnb_exact_tail(tab, st, w, sv, cf, out);
-}
-
-// per channel: reduce pass-1 partials; dgamma, dbeta; max |gamma delta|
-__global__ __launch_bounds__(256) void k_bnb_fin1(const int32_t* dy_exp, Stream st, BwdWs w, Saved sv,
-                                                  BnCfg cf, const int8_t* gamma_q, int64_t* dgamma,
-                                                  int64_t* dbeta, int32_t* dgamma_exp,
-                                                  int32_t* dbeta_exp, int32_t* dev_status)
-{
-    __shared__ long long sh64[256];
-    __shared__ int32_t sh32[256];
-    const int c = blockIdx.x;
-    const size_t pc = (size_t)st.gx * st.C;
-    long long sd = 0, sdn = 0;
-    int z = 0;
-    int mm[6] = {1000, -1000, 1000, -1000, 1000, -1000};
-    for (int b = threadIdx.x; b < st.gx; b += 256) {
-        int64_t o = (int64_t)b * st.C + c;
-        sd += w.p_sd[o];
-        sdn += w.p_sdn[o];
-        z += w.p_z[o];
-        for (int k = 0; k < 6; k++) {
-            int v = w.p_mm[k * pc + o];
-            mm[k] = (k & 1) ? (v > mm[k] ? v : mm[k]) : (v < mm[k] ? v : mm[k]);
-        }
+    if (TAIL && arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) {
+        if constexpr (TAIL == 1) bnb_exact_tail(tab, st, w, sv, cf, out);
+        else bnb_round_tail1(tab, st, w, sv, cf, out);
     }
-    sd = block_reduce(sd, OpAdd(), sh64);
-    sdn = block_reduce(sdn, OpAdd(), sh64);
-    z = block_reduce(z, OpAdd(), sh32);
-    for (int k = 0; k < 6; k++)
-        mm[k] = (k & 1) ? block_reduce(mm[k], OpMax(), sh32) : block_reduce(mm[k], OpMin(), sh32);
-    if (threadIdx.x != 0) return;
-    int32_t s_d = *dy_exp;
-    if (c == 0) {
-        if (s_d < -60 || s_d > 16) set_status(dev_status, ISEG_DEV_RANGE);
-        *dbeta_exp = s_d;
-        *dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
-    }
-    w.sd[c] = sd; w.sdn[c] = sdn; w.Z[c] = z;
-    for (int k = 0; k < 6; k++) w.mm[c * 6 + k] = mm[k];
-    dbeta[c] = sd;
-    dgamma[c] = sdn;
-    int amax = 0;
-    for (int k = 0; k < 3; k++) {
-        int lo = mm[2 * k], hi = mm[2 * k + 1];
-        if (lo > hi) continue;
-        int a = lo < 0 ? -lo : lo, bb = hi < 0 ? -hi : hi;
-        amax = a > amax ? a : amax;
-        amax = bb > amax ? bb : amax;
-    }
-    int gq = gamma_q[c];
-    uint64_t F = (uint64_t)(gq < 0 ? -gq : gq) * (uint64_t)amax;
-    if (F) atomicMax(w.maxF, (unsigned long long)F);
 }
 
 __device__ __forceinline__ int bnb_r2(const BwdWs& w, const BnCfg& cf)
@@ -973,12 +927,18 @@ __device__ __forceinline__ int bnb_r2(const BwdWs& w, const BnCfg& cf)
     return MF ? bitlen_u64(MF) - (cf.k_E2 - 1) : 0;
 }
 
-// pass 2 (only when E2's quantizer rounds): sum f and f*n_xhat
+__device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st, const BwdWs& w,
+                                                const Saved& sv, const BnCfg& cf, const BnbOut& o);
+
+// pass 2 (only when E2's quantizer rounds): sum f and f*n_xhat; the tails
+// reduce them and give E1's exponent
 __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ dy,
                                                     const int8_t* __restrict__ x, Stream st, BwdWs w,
-                                                    Saved sv, BnCfg cf, const int8_t* gamma_q)
+                                                    Saved sv, BnCfg cf, BnbOut out)
 {
+    const int8_t* gamma_q = out.gamma_q;
     __shared__ __attribute__((aligned(16))) int16_t xc[64 * 256];
+    __shared__ int16_t ft[64 * 256];                  // f = SQ(gamma_q d, k_E2) per (channel, d)
     __shared__ Thr thr[64];
     __shared__ unsigned long long sF[64], sFn[64];
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
@@ -990,26 +950,30 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
         thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], cf.relu ? sv.mlo[c] : -1000, cf.relu ? sv.mhi[c] : 1000};
         sF[threadIdx.x] = 0; sFn[threadIdx.x] = 0;
     }
+    {
+        // |f| < 2^(k_E2-1) <= 2^13 on this path
+        const int r2 = bnb_r2(w, cf);
+        for (int e = threadIdx.x; e < st.CS * 256; e += blockDim.x)
+            ft[e] = (int16_t)sq_code((int64_t)gamma_q[cbase + (e >> 8)] * ((e & 255) - 128), r2, cf.k_E2);
+    }
     __syncthreads();
-    const int r2 = bnb_r2(w, cf);
     int g, rsub;
     const bool active = stream_lane(st, g, rsub);
     int64_t sf[4] = {0, 0, 0, 0}, sfn[4] = {0, 0, 0, 0};
     if (active) {
         const int c0 = (int)cbase + g * 4;
-        int gq[4];
         Thr t[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++) { gq[i] = gamma_q[c0 + i]; t[i] = thr[g * 4 + i]; }
+        for (int i = 0; i < 4; i++) t[i] = thr[g * 4 + i];
         stream_rows2<4, 8>(st, x, dy, c0, rsub, [&](int64_t, const Vec<4>& vxx, const Vec<4>& vdd) {
             const uint32_t vx = vxx.w[0], vd = vdd.w[0];
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 int q = sbyte(vx, i);
                 int d = thr_mask(t[i], q) ? sbyte(vd, i) : 0;
-                int64_t f = sq_code((int64_t)gq[i] * d, r2, cf.k_E2);
+                const int f = ft[(g * 4 + i) * 256 + d + 128];
                 sf[i] += f;
-                sfn[i] += f * xc[(g * 4 + i) * 256 + q + 128];
+                sfn[i] += f * (int)xc[(g * 4 + i) * 256 + q + 128];     // |f x| < 2^28
             }
         });
     }
@@ -1028,9 +992,10 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
     __syncthreads();
     if ((int)threadIdx.x < st.CS) {
         int64_t o = (int64_t)blockIdx.x * st.C + cbase + threadIdx.x;
-        w.p_sf[o] = (long long)sF[threadIdx.x];
-        w.p_sfn[o] = (long long)sFn[threadIdx.x];
+        st_x(&w.p_sf[o], (long long)sF[threadIdx.x]);
+        st_x(&w.p_sfn[o], (long long)sFn[threadIdx.x]);
     }
+    if (arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) bnb_round_tail2((uint32_t*)xc, st, w, sv, cf, out);
 }
 
 // bracket of the exact dx (times den M^2 / 2^Ebase) for a (f, sgn) pair
@@ -1046,16 +1011,22 @@ struct BnbChan {
     int e_xh, Ebase, r2;
 };
 
+// exponents of a channel's bracket for E2's shift r2
+__device__ __forceinline__ BnbChan bnb_chan_exps(int r2, int32_t dy_exp, const Saved& sv, const BnCfg& cf)
+{
+    BnbChan ch;
+    ch.r2 = r2;
+    ch.e_xh = sv.hdr[0] - (cf.k_xhat - 1);
+    const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
+    const int s2 = dy_exp + e_g + r2;
+    ch.Ebase = s2 - e_sig + (ch.e_xh < 0 ? ch.e_xh : 0);
+    return ch;
+}
+
 __device__ __forceinline__ BnbChan bnb_chan(int c, const int32_t* dy_exp, const BwdWs& w,
                                             const Saved& sv, const BnCfg& cf, int gq, bool exact_e2)
 {
-    BnbChan ch;
-    ch.r2 = bnb_r2(w, cf);
-    const int b = sv.hdr[0];
-    ch.e_xh = b - (cf.k_xhat - 1);
-    const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
-    const int s2 = *dy_exp + e_g + ch.r2;
-    ch.Ebase = s2 - e_sig + (ch.e_xh < 0 ? ch.e_xh : 0);
+    BnbChan ch = bnb_chan_exps(bnb_r2(w, cf), *dy_exp, sv, cf);
     if (exact_e2) {
         // E2 exact: f = gamma_q delta 2^-r2 with r2 <= 0
         ch.Sf = (i128)gq * (i128)w.sd[c] * pow2_128(-ch.r2);
@@ -1068,56 +1039,15 @@ __device__ __forceinline__ BnbChan bnb_chan(int c, const int32_t* dy_exp, const 
     return ch;
 }
 
-// per channel: (reduce pass-2 partials,) exponent bound of max|dx|
-__global__ __launch_bounds__(256) void k_bnb_fin2(const int32_t* dy_exp, Stream st, BwdWs w, Saved sv,
-                                                  BnCfg cf, const int8_t* gamma_q, int exact_e2)
-{
-    __shared__ long long sh64[256];
-    const int c = blockIdx.x;
-    if (!exact_e2) {
-        long long sf = 0, sfn = 0;
-        for (int b = threadIdx.x; b < st.gx; b += 256) {
-            int64_t o = (int64_t)b * st.C + c;
-            sf += w.p_sf[o];
-            sfn += w.p_sfn[o];
-        }
-        sf = block_reduce(sf, OpAdd(), sh64);
-        sfn = block_reduce(sfn, OpAdd(), sh64);
-        if (threadIdx.x == 0) { w.sf[c] = sf; w.sfn[c] = sfn; }
-    }
-    if (threadIdx.x != 0) return;
-    const int gq = gamma_q[c];
-    BnbChan ch = bnb_chan(c, dy_exp, w, sv, cf, gq, exact_e2);
-    const i128 M = st.M;
-    const i128 Dd = (i128)sv.den[c] * M * M;
-    int best = kSentinelLo;
-    for (int k = 0; k < 3; k++) {
-        int lo = w.mm[c * 6 + 2 * k], hi = w.mm[c * 6 + 2 * k + 1];
-        if (lo > hi) continue;
-        int ds[2] = {lo, hi};
-        for (int t = 0; t < 2; t++) {      // |dx| is extreme at the class's extreme deltas
-            int64_t f = sq_code((int64_t)gq * ds[t], ch.r2, cf.k_E2);
-            i128 B = bnb_bracket(f, k - 1, M, ch.Sf, ch.T, ch.Z, ch.e_xh);
-            if (B == 0) continue;
-            int e = ceil_pow2_exp128(abs128(B), Dd) + ch.Ebase;
-            best = e > best ? e : best;
-        }
-    }
-    if (best > kSentinelLo) atomicMax(w.bdx, best);
-}
-
 // dx code table for every (sgn class, masked error code) of a channel
 __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t Mrows, BwdWs w, Saved sv,
-                                                 BnCfg cf, const int8_t* gamma_q, int exact_e2,
-                                                 int32_t* dx_exp)
+                                                 BnCfg cf, const int8_t* gamma_q, int exact_e2)
 {
     const int c = blockIdx.x;
     const int d = (int)threadIdx.x - 128;
     const int gq = gamma_q[c];
     BnbChan ch = bnb_chan(c, dy_exp, w, sv, cf, gq, exact_e2);
-    int bdx = *w.bdx;
-    if (bdx == kSentinelLo) bdx = 0;
-    if (c == 0 && threadIdx.x == 0) *dx_exp = bdx - (cf.k_E1 - 1);
+    const int bdx = *w.bdx;                 // stats2's last tail
     const i128 M = Mrows;
     const i128 Dd = (i128)sv.den[c] * M * M;
     const int64_t f = d < -127 ? 0 : sq_code((int64_t)gq * d, ch.r2, cf.k_E2);
@@ -1142,15 +1072,27 @@ __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t 
 // extreme deltas: six candidates per channel, one thread each).  Last slice:
 // E1's exponent from the largest bound over all channels.  `lds` is the
 // stats table, no longer read once the block has arrived.
-__device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
-                                               const BnCfg& cf, const BnbOut& o)
+struct Tail1Lds {
+    int32_t *sd, *z, *mm, *cand;        // [kNT], [kNT], [6][kNT], [6 * CS]
+    long long* sdn;                     // [kNT]
+    __device__ explicit Tail1Lds(uint32_t* lds)
+    {
+        sd = (int32_t*)lds; z = sd + kNT; mm = z + kNT;
+        sdn = (long long*)(mm + 6 * kNT); cand = (int32_t*)(sdn + kNT);
+    }
+};
+
+// the slice's pass-1 sums from all blocks' partials: w.sd / sdn / Z / mm,
+// dgamma, dbeta, and the channel totals in the group-0 slots of the LDS table
+__device__ __forceinline__ void bnb_tail_reduce1(uint32_t* lds, const Stream& st, const BwdWs& w,
+                                                 const BnbOut& o)
 {
     const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
-    int32_t* tSd = (int32_t*)lds;                       // [kNT]
-    int32_t* tZ = tSd + kNT;                            // [kNT]
-    int32_t* tMM = tZ + kNT;                            // [6][kNT]
-    long long* tSdn = (long long*)(tMM + 6 * kNT);      // [kNT]
-    int32_t* tCand = (int32_t*)(tSdn + kNT);            // [6 * CS]
+    const Tail1Lds L(lds);
+    int32_t* tSd = L.sd;
+    int32_t* tZ = L.z;
+    int32_t* tMM = L.mm;
+    long long* tSdn = L.sdn;
     const size_t pc = (size_t)st.gx * st.C;
     const int64_t cb = (int64_t)blockIdx.y * CS;
     int sd = 0, z = 0;
@@ -1205,6 +1147,28 @@ __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, 
         for (int k = 0; k < 6; k++) tMM[k * kNT + t] = mm[k];
     }
     __syncthreads();
+}
+
+__device__ __forceinline__ void bnb_exps_out(const Saved& sv, const BnCfg& cf, const BnbOut& o)
+{
+    const int32_t s_d = *o.dy_exp;
+    if (s_d < -60 || s_d > 16) set_status(o.dev_status, ISEG_DEV_RANGE);
+    *o.dbeta_exp = s_d;
+    *o.dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
+}
+
+__device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
+                                               const BnCfg& cf, const BnbOut& o)
+{
+    bnb_tail_reduce1(lds, st, w, o);
+    const int CS = st.CS, t = threadIdx.x;
+    const Tail1Lds L(lds);
+    int32_t* tSd = L.sd;
+    int32_t* tZ = L.z;
+    int32_t* tMM = L.mm;
+    long long* tSdn = L.sdn;
+    int32_t* tCand = L.cand;
+    const int64_t cb = (int64_t)blockIdx.y * CS;
     const int32_t s_d = *o.dy_exp;
     const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
     const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
@@ -1239,9 +1203,106 @@ __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, 
     if (t == 0) {
         *w.bdx = bdx;
         *o.dx_exp = bdx - (cf.k_E1 - 1);
-        if (s_d < -60 || s_d > 16) set_status(o.dev_status, ISEG_DEV_RANGE);
-        *o.dbeta_exp = s_d;
-        *o.dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
+        bnb_exps_out(sv, cf, o);
+    }
+}
+
+// stats tail (rounding E2).  Slice: the pass-1 sums, dgamma, dbeta and each
+// channel's max |gamma_q delta| over its sgn classes.  Last slice: the largest
+// over all channels, the Scale of E2 = SQ(gamma delta, k_E2) read by stats2.
+__device__ __forceinline__ void bnb_round_tail1(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
+                                                const BnCfg& cf, const BnbOut& o)
+{
+    bnb_tail_reduce1(lds, st, w, o);
+    const int CS = st.CS, t = threadIdx.x;
+    const Tail1Lds L(lds);
+    const int64_t cb = (int64_t)blockIdx.y * CS;
+    if (t < CS) {
+        int amax = 0;
+        for (int k = 0; k < 3; k++) {
+            const int lo = L.mm[2 * k * kNT + t], hi = L.mm[(2 * k + 1) * kNT + t];
+            if (lo > hi) continue;                     // empty class
+            amax = max(amax, max(lo < 0 ? -lo : lo, hi < 0 ? -hi : hi));
+        }
+        const int gq = o.gamma_q[cb + t];
+        st_x(&w.cand[cb + t], (gq < 0 ? -gq : gq) * amax);      // <= 128 * 128
+    }
+    if (!arrive_last(w.ctr, gridDim.y)) return;
+    __shared__ int32_t rb[kNT / 64];
+    int F = 0;
+    for (int c = t; c < st.C; c += kNT) F = max(F, ld_x(&w.cand[c]));
+    F = block_max_nt(F, rb);
+    if (t == 0) {
+        *w.maxF = (unsigned long long)F;
+        bnb_exps_out(sv, cf, o);
+    }
+}
+
+// stats2 tail.  Slice: the pass-2 sums (sum f, sum f n_xhat) and each
+// channel's bound on max|dx| (six candidates, as the exact tail); last slice:
+// E1's exponent.  `lds` is stats2's x-hat table, no longer read.
+__device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st, const BwdWs& w,
+                                                const Saved& sv, const BnCfg& cf, const BnbOut& o)
+{
+    const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
+    long long* tSf = (long long*)lds;                   // [kNT]
+    long long* tSfn = tSf + kNT;                        // [kNT]
+    int32_t* tCand = (int32_t*)(tSfn + kNT);            // [6 * CS]
+    const int64_t cb = (int64_t)blockIdx.y * CS;
+    long long sf = 0, sfn = 0;
+    constexpr int U = 4;                    // partial rows whose loads are in flight together
+    if (grp < ng)
+        for (int b0 = grp; b0 < st.gx; b0 += U * ng) {
+            long long vf[U], vn[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int b = b0 + u * ng;
+                const int64_t q = (int64_t)(b < st.gx ? b : b0) * st.C + cb + ch;
+                vf[u] = ld_x(&w.p_sf[q]);
+                vn[u] = ld_x(&w.p_sfn[q]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++)
+                if (b0 + u * ng < st.gx) { sf += vf[u]; sfn += vn[u]; }
+        }
+    tSf[t] = sf; tSfn[t] = sfn;
+    __syncthreads();
+    if (t < CS) {
+        for (int g2 = 1; g2 < ng; g2++) { sf += tSf[g2 * CS + t]; sfn += tSfn[g2 * CS + t]; }
+        w.sf[cb + t] = sf; w.sfn[cb + t] = sfn;
+        tSf[t] = sf; tSfn[t] = sfn;                     // only thread t reads slot t above
+    }
+    __syncthreads();
+    if (t < 6 * CS) {
+        const int cl = t / 6, k = t % 6;                // channel of the slice; class k / 2, low / high
+        const int64_t c = cb + cl;
+        const int lo = w.mm[c * 6 + (k & ~1)], hi = w.mm[c * 6 + (k | 1)];
+        int best = kSentinelLo;
+        if (lo <= hi) {
+            const int gq = o.gamma_q[c];
+            const BnbChan e = bnb_chan_exps(bnb_r2(w, cf), *o.dy_exp, sv, cf);
+            const i128 M = st.M;
+            const int64_t f = sq_code((int64_t)gq * ((k & 1) ? hi : lo), e.r2, cf.k_E2);
+            const i128 B = bnb_bracket(f, (k >> 1) - 1, M, (i128)tSf[cl], (i128)tSfn[cl], (i128)w.Z[c], e.e_xh);
+            if (B != 0) best = ceil_pow2_exp128(abs128(B), (i128)sv.den[c] * M * M) + e.Ebase;
+        }
+        tCand[t] = best;
+    }
+    __syncthreads();
+    if (t < CS) {
+        int best = tCand[6 * t];
+        for (int j = 1; j < 6; j++) best = max(best, tCand[6 * t + j]);
+        st_x(&w.cand[cb + t], best);
+    }
+    if (!arrive_last(w.ctr, gridDim.y)) return;
+    __shared__ int32_t rb[kNT / 64];
+    int bdx = kSentinelLo;
+    for (int c = t; c < st.C; c += kNT) bdx = max(bdx, ld_x(&w.cand[c]));
+    bdx = block_max_nt(bdx, rb);
+    if (bdx == kSentinelLo) bdx = 0;
+    if (t == 0) {
+        *w.bdx = bdx;
+        *o.dx_exp = bdx - (cf.k_E1 - 1);
     }
 }
 
@@ -1437,18 +1498,14 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     const int exact_e2 = cf.k_E2 >= 15;
     const BnbOut out{dy_exp, gamma_q, dgamma, dbeta, dgamma_exp, dbeta_exp, dx_exp, dev_status};
     if (exact_e2) {
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<true>, sg, dim3(kNT), 0, stream, dy, x, st, w,
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<1>, sg, dim3(kNT), 0, stream, dy, x, st, w,
                           sv, cf, out);
         hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q);
     } else {
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<false>, sg, dim3(kNT), 0, stream, dy, x, st,
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<2>, sg, dim3(kNT), 0, stream, dy, x, st,
                           w, sv, cf, out);
-        hipLaunchKernelGGL(k_bnb_fin1, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, dgamma,
-                           dbeta, dgamma_exp, dbeta_exp, dev_status);
-        hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(kNT), 0, stream, dy, x, st, w, sv, cf, gamma_q);
-        hipLaunchKernelGGL(k_bnb_fin2, cb, dim3(256), 0, stream, dy_exp, st, w, sv, cf, gamma_q, exact_e2);
-        hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2,
-                           dx_exp);
+        hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(kNT), 0, stream, dy, x, st, w, sv, cf, out);
+        hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2);
     }
     ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, sg, dim3(kNT), 0, stream, dy, x, dx_out, st,
                       w, sv, cf.relu);

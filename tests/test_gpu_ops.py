@@ -366,6 +366,11 @@ BN_CASES = [
     dict(M=4096 + 3, C=2048, x_exp=-6, cfg=dict(relu=0)),
     dict(M=3001, C=268, x_exp=-10, cfg=dict(k_E2=8)),
     dict(M=3001, C=268, x_exp=-10, cfg={}),
+    # rounding E2 (k_E2 < 15) at scale: its two streaming passes each end in
+    # per-slice tails, one slice of 256 blocks / 32 slices / narrow E2
+    dict(M=65536 + 37, C=64, x_exp=-8, cfg=dict(k_E2=8)),
+    dict(M=4096 + 3, C=2048, x_exp=-6, cfg=dict(k_E2=12, relu=0)),
+    dict(M=999, C=96, x_exp=-9, cfg=dict(k_E2=4)),
 ]
 
 
@@ -420,7 +425,7 @@ def test_bn_repeated_calls_same_workspace(orc, dev):
     from paper_2011_14504_amd import iseg
     refs = {}
     for rep in range(2):
-        for i in (0, 3, 7, 9):
+        for i in (0, 3, 7, 9, 10, 11, 12, 13):
             case = BN_CASES[i]
             x, gq, bq, dA = _bn_inputs(i, case)
             cfg = dict(orc.BN_DEFAULT, **case["cfg"])
