@@ -31,8 +31,9 @@ import numpy as np
 from . import oracle as O
 
 class OracleNet:
-    def __init__(self, wl, inputs, lr_shift=10, bn_cfg=None, k_W=8, k_U=24):
+    def __init__(self, wl, inputs, lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1):
         self.wl = wl
+        self.gq = gq                              # 1: Eq. 17 keeps Scale(G); 2: Eq. 18 drops it
         self.lr_shift = lr_shift
         self.k_W, self.k_U = k_W, k_U
         self.seed = inputs["seed"]
@@ -78,14 +79,16 @@ class OracleNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                # Z feeds BN at 8 bits; without BN it is the activation (Q_A)
-                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd),
-                                   8 if nd["bn"] else self.k_A)
+                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd))
                 z = z.astype(np.int8)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
                     b = O.bn_fwd(z, ze, L["g_q"], L["b_q"], self._bn_cfg(nd))
                     y, ye = b["y"], b["y_exp"]
+                elif nd["relu"] or self.k_A < 8:
+                    # without BN: A = Q_A(ReLU?(Z)) on the 8-bit conv output
+                    y, ye = O.sum_requant([z], [ze], self.k_A, relu=nd["relu"])
+                    y = y.astype(np.int8)
                 else:
                     y, ye = z, ze
             elif k == "maxpool":
@@ -161,10 +164,12 @@ class OracleNet:
                                         16 * l + 2, self.step_no)
                     r.update(dgamma=b["dgamma"], dbeta=b["dbeta"], Gg=Gg, Gg_exp=Gge, Gb=Gb,
                              Gb_exp=Gbe)
+                elif nd["relu"]:
+                    dz, dze = O.relu_mask_bwd(e, [r["z"]], [r["z_exp"]]), ee
                 else:
                     dz, dze = e, ee
                 geom = self._geom(r["a_in"].shape, nd)
-                G, Ge = O.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], geom, 8, True,
+                G, Ge = O.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], geom, 8, self.gq == 1,
                                           self.seed, 16 * L["l"], self.step_no)
                 r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
                 grads.append((nd, r))

@@ -17,8 +17,9 @@ beta (learning rate 2^-lr_shift), then Q_W.
 Bit widths (Table 1's rows): k_W for conv weights, k_U for the masters,
 k_gamma / k_beta of the BN configuration for the BN parameters (their own
 width in the update table), k_A for every activation a conv reads (Q_A of the
-BN output, a conv output without BN, the forward merges).  A conv feeding BN
-keeps its output at 8 bits; errors and gradients stay at 8 bits.  Codes of
+BN output, Q_A(ReLU?(Z)) after a conv without BN, the forward merges).  Every
+conv output Z is 8 bits; errors and gradients stay at 8 bits.  gq selects
+Q_G: Eq. 17 keeps Scale(G) (GQ1), Eq. 18 drops it (GQ2).  Codes of
 fewer than 8 bits run through the same int8 kernels.
 
 Stochastic rounding keys: seed of the workload, step counter, tensor id
@@ -30,10 +31,13 @@ import torch
 from . import iseg
 
 class IntNet:
-    def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24):
-        if not (2 <= k_W <= 8 and 9 <= k_U <= 31):
-            raise ValueError("k_W must be in [2, 8] and k_U in [9, 31]")
+    def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1):
+        if not (2 <= k_W <= 8 and 9 <= k_U <= 31 and gq in (1, 2)):
+            raise ValueError("k_W must be in [2, 8], k_U in [9, 31], gq 1 or 2")
         self.wl = wl
+        # weight-gradient quantizer: GQ1 (Eq. 17, the DeepLab setting) keeps
+        # Scale(G); GQ2 (Eq. 18, the FCN setting) drops it
+        self.g_mode = iseg.ISEG_G_KEEP if gq == 1 else iseg.ISEG_G_DROP
         self.k_W, self.k_U = k_W, k_U
         self.w_master_exp = 1 - k_U             # Eq. 7
         self.gb_master_exp = 2 - k_U            # gamma/beta quantizers carry the x2 fold
@@ -135,16 +139,14 @@ class IntNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                if nd["bn"] or self.k_A == 8:
-                    z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"])
-                else:                       # the activation itself: Q_A to k_A bits of the sums
-                    acc, acc_e = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"],
-                                               nd["dil"], out_mode=iseg.ISEG_OUT_RAW)
-                    z, ze = iseg.requant(acc, acc_e, self.k_A)
+                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"])
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
                     y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])])
                     r["saved"] = saved
+                elif nd["relu"] or self.k_A < 8:
+                    # without BN: A = Q_A(ReLU?(Z)) on the 8-bit conv output
+                    y, ye = iseg.sum_requant([z], [ze], relu=nd["relu"], bits=self.k_A)
                 else:
                     y, ye = z, ze
             elif k == "maxpool":
@@ -211,6 +213,8 @@ class IntNet:
                                                             dgb_out=(L["dg"], L["db"], L["dg_exp"],
                                                                      L["db_exp"]))
                     r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
+                elif nd["relu"]:
+                    dz, dze = iseg.relu_mask_bwd(e, [r["z"]], [r["z_exp"]]), ee
                 else:
                     dz, dze = e, ee
                 G, Ge = self._wgrad(nd, L, r, dz, dze)
@@ -260,7 +264,7 @@ class IntNet:
         """Q_G(backward-weight) of one conv (Eq. 17), on the side stream once
         dz is ready; its inputs are marked as in use there."""
         args = (dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"],
-                iseg.ISEG_G_KEEP, 8, self.seed, 16 * L["l"], self.step_no)
+                self.g_mode, 8, self.seed, 16 * L["l"], self.step_no)
         if self.side is None:
             return iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]))
         ready = torch.cuda.current_stream(self.dev).record_event()

@@ -188,6 +188,15 @@ WORKLOADS = {1: SINGLE_CONV, 2: VGG16_BLOCKS12, 3: RESNET50_CONV2X, 4: ASPP_HEAD
              5: DEEPLABV3_R50}
 
 
+def without_bn(wl):
+    """The same graph with every conv's L1BN removed (the paper's FCN has no
+    BN); a conv's ReLU then follows its output quantizer's input."""
+    d = dict(wl)
+    d["name"] = wl["name"] + "-nobn"
+    d["nodes"] = [dict(n, bn=False) if n["kind"] == "conv" else n for n in wl["nodes"]]
+    return d
+
+
 def scaled(wl, N=None, H=None, W=None):
     """The same workload at another batch or input size (parity tests)."""
     d = dict(wl)

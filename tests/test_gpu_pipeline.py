@@ -122,3 +122,13 @@ def test_deeplabv3_r50_k_e2_8_128px():
 @pytest.mark.parametrize("k_U", [12, 16, 20])
 def test_resnet50_conv2x_k_u_two_steps(k_U):
     _run_both(synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28), steps=2, k_U=k_U)
+
+
+def test_vgg16_blocks12_no_bn_gq2_two_steps():
+    # the paper's FCN setting on its encoder: no BN (ReLU + Q_A on each 8-bit
+    # conv output), gradients by Eq. 18
+    _run_both(synth.without_bn(synth.scaled(synth.VGG16_BLOCKS12, 1, 96, 80)), steps=2, gq=2)
+
+
+def test_resnet50_conv2x_no_bn_gq2_w4a4():
+    _run_both(synth.without_bn(synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28)), steps=2, gq=2, **W4A4)

@@ -130,3 +130,30 @@ def test_low_bit_widths(wl):
         assert np.abs(d).max() <= 2.0 ** -k_W
         for q in ("g_q", "b_q"):
             assert np.abs(L[q].astype(np.int64)).max() <= 127
+
+
+def test_no_bn_gq2_step():
+    """The no-BN network with GQ2 (Eq. 18): one step's gradient codes equal
+    GQ1's (the same stochastic RQ; only the exponent differs, 1 - k_G), ReLU
+    convs output non-negative k_A-bit codes, and their backward passes the
+    error exactly where the 8-bit conv output is positive."""
+    from oracle.model import OracleNet
+    wl = synth.without_bn(synth.scaled(synth.RESNET50_CONV2X, 1, 6, 7))
+    inp = synth.workload_inputs(wl)
+    r1 = OracleNet(wl, inp, gq=1).step()
+    r2 = OracleNet(wl, inp, gq=2).step()
+    for nd in wl["nodes"]:
+        a, b = r1[nd["name"]], r2[nd["name"]]
+        if nd["kind"] != "conv":
+            continue
+        # the forward is the same; G codes agree, exponents follow Eq. 17 / 18
+        assert np.array_equal(a["a_out"], b["a_out"])
+        if np.array_equal(a["dz"], b["dz"]) and a["dz_exp"] == b["dz_exp"]:
+            assert np.array_equal(a["G"], b["G"]), nd["name"]
+        assert b["G_exp"] == 1 - 8
+        if nd["relu"]:
+            assert a["a_out"].min() >= 0 and a["a_out"].max() <= 127
+            z = a["z"].astype(np.int64)
+            e = a["e_out"].astype(np.int64)
+            assert np.array_equal(a["dz"].astype(np.int64), np.where(z > 0, e, 0)), nd["name"]
+            assert a["dz_exp"] == a["e_out_exp"]
