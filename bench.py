@@ -158,6 +158,9 @@ def main():
     ap.add_argument("--k-a", type=int, default=8, help="activation code width k_A")
     ap.add_argument("--k-e2", type=int, default=16, help="BN error width k_E2 (8 or 16)")
     ap.add_argument("--k-u", type=int, default=24, help="master / update width k_U")
+    ap.add_argument("--gq", type=int, default=1, choices=(1, 2),
+                    help="weight-gradient quantizer: 1 keeps Scale(G) (Eq. 17), 2 drops it (Eq. 18)")
+    ap.add_argument("--no-bn", action="store_true", help="the same network without L1BN")
     ap.add_argument("--copy-kernel-mib", type=int, default=0,
                     help="only run the plain copy kernel used to calibrate the HBM byte counters")
     ap.add_argument("--timed-kernel", default="conv_fwd:aspp.b1",
@@ -178,9 +181,11 @@ def main():
     from paper_2011_14504_amd.model import IntNet
 
     wl = synth.scaled(synth.WORKLOADS[WORKLOAD_IDS[args.workload]], args.batch)
+    if args.no_bn:
+        wl = synth.without_bn(wl)
     N = wl["N"]
     inp = synth.workload_inputs(wl)
-    widths = dict(k_W=args.k_w, k_U=args.k_u, bn_cfg={"k_A": args.k_a, "k_E2": args.k_e2})
+    widths = dict(k_W=args.k_w, k_U=args.k_u, bn_cfg={"k_A": args.k_a, "k_E2": args.k_e2}, gq=args.gq)
     net = IntNet(wl, inp, "cuda:0", **widths)
     ops, detail = workload_ops(wl)
     tk = args.timed_kernel
@@ -224,7 +229,8 @@ def main():
     cfg = dict(workload=wl["name"], batch=N, image=f"{wl['H']}x{wl['W']}",
                convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
                pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
-               bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u))
+               bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u), gq=args.gq,
+               l1bn=not args.no_bn)
     if net.loss is not None:
         cfg["loss"] = float(net.loss.item())
     out = dict(metric=METRIC, value=value, unit="TOPS", n_gpus=1, steps=args.steps,
