@@ -374,6 +374,15 @@ void orc_conv_bwd_weight_raw(const int8_t* dy, const int8_t* x, const int64_t* g
 /* sits between the affine step and Q_A; SQ uses the power-of-two scale; an   */
 /* all-zero xhat takes b = 0 (exponent 1-k_xhat).                             */
 /* Preconditions (else ORC_ERR_RANGE): s_x in [-40, 16], 1 <= m <= 2^22.      */
+/* Why 16: with g = min(s_x, e_mu) = -14 for s_x >= -14, a centred value     */
+/* D = q 2^(s_x+14) - n_mu has |D| <= 127 2^30 + 32767 < 2^37 at s_x = 16,    */
+/* so the per-channel sum of |D| over m <= 2^22 rows stays below 2^59: a     */
+/* signed 64-bit accumulator (the GPU keeps these partial sums in int64)     */
+/* with four bits to spare.  At s_x = 20 the same sum could reach           */
+/* 127 2^34 2^22 ~ 2^63 and overflow.  Every other intermediate is smaller:  */
+/* |xhat| < 2^37 (b <= 37), y on its grid < 2^44, and the backward bracket   */
+/* m^2 f - m sum f - (sum f n_xhat) 2^(b-15) (m s - Z) < 2^96 in __int128.   */
+/* s_x = -40 keeps 2^(e_mu - g) = 2^26 and the sum of |D| likewise in range. */
 /* ------------------------------------------------------------------------ */
 typedef struct {
     int k_mu, k_sigma, k_xhat, k_gamma, k_beta, k_A, k_E1, k_E2, eps_code, relu;

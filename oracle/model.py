@@ -162,8 +162,8 @@ class OracleNet:
                                         16 * l + 1, self.step_no)
                     Gb, Gbe = O.requant(b["dbeta"], b["dbeta_exp"], 8, True, True, self.seed,
                                         16 * l + 2, self.step_no)
-                    r.update(dgamma=b["dgamma"], dbeta=b["dbeta"], Gg=Gg, Gg_exp=Gge, Gb=Gb,
-                             Gb_exp=Gbe)
+                    r.update(dgamma=b["dgamma"], dbeta=b["dbeta"], dgamma_exp=b["dgamma_exp"],
+                             dbeta_exp=b["dbeta_exp"], Gg=Gg, Gg_exp=Gge, Gb=Gb, Gb_exp=Gbe)
                 elif nd["relu"]:
                     dz, dze = O.relu_mask_bwd(e, [r["z"]], [r["z_exp"]]), ee
                 else:

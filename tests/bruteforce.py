@@ -46,6 +46,16 @@ def SQ(values, k):
     return [S * UQ(v / S, k) for v in values]
 
 
+def SQ_max(values, k):
+    """Eq. 3-4 as printed: Scale(x) = max|x| exactly (not a power of two), so
+    the largest element maps to x/Scale = 1 and is clipped to 1 - Delta.
+    Used only to measure how far the power-of-two reading departs from it."""
+    M = max(abs(v) for v in values)
+    if M == 0:
+        return [Fr(0)] * len(values)
+    return [M * UQ(v / M, k) for v in values]
+
+
 def RQ_probs(v, S, k):
     """Eq. 5-6 for one value scaled by S: returns {quantized value: prob}."""
     d = delta(k)

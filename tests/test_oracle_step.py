@@ -1,0 +1,166 @@
+"""The oracle's composition of whole training steps, pinned by an independent
+exact-rational brute force (tests/bruteforce_step.py): forward order, the
+routing of errors to both branches of a residual block and their merge, the
+inputs of every weight gradient, the Philox keys of Q_G, and the update of
+every master.  The brute force shares no code with the oracle; it is written
+from Eq. 2-8 and 12-19 with Fractions.  Every activation, error, gradient
+code, exponent and updated master of OracleNet.step() must equal it."""
+import numpy as np
+import pytest
+
+from paper_2011_14504_amd import synth
+import bruteforce_step as B
+
+
+def _same(codes, exp, vals, vexp, what, check_exp=True):
+    got = B.values(np.asarray(codes).astype(np.int64), exp)
+    assert got.shape == vals.shape, what
+    assert all(g == v for g, v in zip(got.ravel(), vals.ravel())), what
+    if check_exp and vexp is not None:
+        assert exp == vexp, (what, exp, vexp)
+
+
+def _compare_node(o, b, name):
+    for key in ("z", "a_out", "e_out", "dz", "G", "e_in", "Gg", "Gb"):
+        if key in b:
+            assert key in o, (name, key)
+            _same(o[key], o[key + "_exp"], b[key], b[key + "_exp"], f"{name} {key}")
+    for key in ("dgamma", "dbeta"):
+        if key in b:
+            _same(o[key], o[key + "_exp"], np.array(b[key], dtype=object), None, f"{name} {key}")
+
+
+def _compare_params(onet, bnet, k_U, k_W, cfg):
+    for name, L in bnet.L.items():
+        O = onet.convs[name]
+        _same(O["w_m"], 1 - k_U, L["w_m"], None, f"{name} w_m")
+        _same(O["w_q"], 1 - k_W, bnet.w_q(name), None, f"{name} w_q")
+        if L["nd"]["bn"]:
+            g, b = bnet.gamma_beta(name)
+            _same(O["g_m"], 2 - k_U, np.array(L["g_m"], dtype=object), None, f"{name} g_m")
+            _same(O["b_m"], 2 - k_U, np.array(L["b_m"], dtype=object), None, f"{name} b_m")
+            _same(O["g_q"], 2 - cfg["k_gamma"], np.array(g, dtype=object), None, f"{name} g_q")
+            _same(O["b_q"], 2 - cfg["k_beta"], np.array(b, dtype=object), None, f"{name} b_q")
+
+
+def test_python_philox_known_answers():
+    # Random123 known-answer vectors for Philox4x32-10
+    assert B.philox4x32_10([0, 0, 0, 0], [0, 0]) == [0x6627e8d5, 0xe169c58d, 0xbc57ac4c, 0x9b00dbd8]
+    assert B.philox4x32_10([0xffffffff] * 4, [0xffffffff] * 2) == \
+        [0x408f276d, 0x41c83b0e, 0xa20bc7c6, 0x6d5451fd]
+    assert B.philox4x32_10([0x243f6a88, 0x85a308d3, 0x13198a2e, 0x03707344],
+                           [0xa4093822, 0x299f31d0]) == [0xd16cfe09, 0x94fdcceb, 0x5001e420, 0x24126ea1]
+
+
+def test_bruteforce_conv_adjoints():
+    """The brute force's own conv, data gradient and weight gradient satisfy
+    <conv(x, w), dy> = <x, dgrad(dy, w)> = <w, wgrad(dy, x)> exactly."""
+    from fractions import Fraction as Fr
+    rng = synth.rng(4242)
+    for (N, H, W, C, K, R, st, pad, dil) in [(1, 7, 6, 3, 4, 3, 2, 1, 1), (2, 5, 5, 2, 3, 3, 1, 2, 2),
+                                            (1, 6, 4, 3, 2, 1, 2, 0, 1)]:
+        x = B.values(rng.integers(-127, 128, (N, H, W, C)), -3)
+        w = B.values(rng.integers(-127, 128, (K, R, R, C)), -7)
+        y = B.conv(x, w, st, pad, dil)
+        dy = B.values(rng.integers(-127, 128, y.shape), -5)
+        lhs = sum((a * b for a, b in zip(y.ravel(), dy.ravel())), Fr(0))
+        dx = B.conv_data_grad(dy, w, H, W, st, pad, dil)
+        assert lhs == sum((a * b for a, b in zip(x.ravel(), dx.ravel())), Fr(0))
+        dw = B.conv_weight_grad(dy, x, R, st, pad, dil)
+        assert lhs == sum((a * b for a, b in zip(w.ravel(), dw.ravel())), Fr(0))
+
+
+def test_single_conv_two_steps_match_bruteforce():
+    """Workload 1 at its full size (1x32x32, 16 -> 16 channels, 3x3): two
+    steps, so the second one runs with updated W, gamma, beta and step 1 of
+    the Philox counter."""
+    from oracle.model import OracleNet
+    wl = synth.SINGLE_CONV
+    inp = synth.workload_inputs(wl)
+    onet = OracleNet(wl, inp)
+    bnet = B.Net(wl, inp, dict(onet.cfg))
+    for s in range(2):
+        orec = onet.step()
+        brec = B.single_conv_step(bnet, inp["x"], inp["x_exp"], inp["dy"], inp["dy_exp"])
+        _compare_node(orec["conv"], brec["conv"], f"step {s} conv")
+        _compare_params(onet, bnet, 24, 8, onet.cfg)
+
+
+TINY_STAGE = dict(id=3, name="tiny-stage-8ch-7x6", N=1, H=7, W=6, C=8, input_grad=True, loss="given",
+                  nodes=synth.res_stage("s", "input", 8, 4, 16, 2, stride=2)[0])
+
+
+@pytest.mark.parametrize("variant", ["bn", "bn-w4a4-e2-8", "no-bn-gq2"])
+def test_residual_stage_two_steps_match_bruteforce(variant):
+    """Two bottlenecks (the first strided, with a projection shortcut; the
+    second with the identity) on a 1x7x6x8 input with the input gradient:
+    every tensor of two training steps against the brute force.  Variants:
+    the 8-bit DeepLab setting; W4A4 with E2 at 8 bits (Table 1); the network
+    without BN and Eq. 18's gradient quantizer."""
+    from oracle.model import OracleNet
+    wl = TINY_STAGE
+    kw = {}
+    if variant == "bn-w4a4-e2-8":
+        kw = dict(k_W=4, k_U=16, bn_cfg={"k_A": 4, "k_E2": 8})
+    if variant == "no-bn-gq2":
+        wl = synth.without_bn(wl)
+        kw = dict(gq=2)
+    inp = synth.workload_inputs(wl)
+    # random gamma / beta would need another draw; the update moves them off 1 / 0
+    onet = OracleNet(wl, inp, **kw)
+    bnet = B.Net(wl, inp, dict(onet.cfg), k_W=kw.get("k_W", 8), k_U=kw.get("k_U", 24),
+                 gq=kw.get("gq", 1))
+    for s in range(2):
+        orec = onet.step()
+        brec = B.stage_step(bnet, inp["x"], inp["x_exp"], inp["dy"], inp["dy_exp"], "s", 2)
+        for nd in wl["nodes"]:
+            _compare_node(orec[nd["name"]], brec[nd["name"]], f"step {s} {nd['name']}")
+        _same(orec["input"]["e_out"], orec["input"]["e_out_exp"], brec["input"]["e_out"],
+              brec["input"]["e_out_exp"], f"step {s} input error")
+        _compare_params(onet, bnet, kw.get("k_U", 24), kw.get("k_W", 8), onet.cfg)
+
+
+def test_max_exact_scale_deviation_single_conv():
+    """How far the power-of-two Scale departs from Eq. 3's literal max|x|, at
+    every SQ of one step of workload 1 (the same pre-quantizer values fed to
+    both readings).  Both stay within a step of the exact value; the counts
+    of elements whose quantized value differs are printed (recorded with the
+    readings of the paper)."""
+    from fractions import Fraction as Fr
+    import bruteforce as bf
+    wl = synth.SINGLE_CONV
+    inp = synth.workload_inputs(wl)
+    from oracle import oracle as O
+    seen = []
+    orig = B.SQ
+
+    def spy(arr, k):
+        seen.append((arr, k))
+        return orig(arr, k)
+
+    B.SQ = spy
+    try:
+        bnet = B.Net(wl, inp, dict(O.BN_DEFAULT))
+        B.single_conv_step(bnet, inp["x"], inp["x_exp"], inp["dy"], inp["dy_exp"])
+    finally:
+        B.SQ = orig
+    report = []
+    for arr, k in seen:
+        flat = list(arr.ravel())
+        M = max(abs(v) for v in flat)
+        if M == 0:
+            continue
+        p2 = bf.SQ(flat, k)
+        mx = bf.SQ_max(flat, k)
+        S2 = bf.pow2_scale(flat)
+        step2, stepm = S2 * bf.delta(k), M * bf.delta(k)
+        differ = sum(1 for a, b in zip(p2, mx) if a != b)
+        for v, a, b in zip(flat, p2, mx):
+            assert abs(a - v) <= step2 / 2 and abs(b - v) <= stepm
+        mean_dev = sum((abs(a - b) for a, b in zip(p2, mx)), Fr(0)) / len(flat) / stepm
+        report.append((k, len(flat), differ, float(S2 / M), float(mean_dev)))
+    print("\n[max-exact vs power-of-two] (k, elements, differing, S_pow2/max, mean |diff| in "
+          "max-scale steps):")
+    for r in report:
+        print("  ", r)
+    assert len(report) >= 4
