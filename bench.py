@@ -13,6 +13,7 @@ library records around each of its launches inside the timed steps;
 import argparse
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -231,8 +232,13 @@ def main():
                pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
                bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u), gq=args.gq,
                l1bn=not args.no_bn)
+    status = net.read_status()
     if net.loss is not None:
         cfg["loss"] = float(net.loss.item())
+    if status != 0 or (net.loss is not None and not math.isfinite(cfg["loss"])):
+        print(f"bench.py: the training step flagged device status {status} (loss "
+              f"{cfg.get('loss')}); the measurement is not valid", file=sys.stderr)
+        sys.exit(3)
     out = dict(metric=METRIC, value=value, unit="TOPS", n_gpus=1, steps=args.steps,
                warmup=args.warmup, ms_per_step=ms, higher_is_better=True, scaling="weak",
                vs_baseline=None, dtype="int8", data="synthetic", config=cfg, roofline=roof)

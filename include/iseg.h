@@ -7,8 +7,12 @@
  * ---------------------------------------
  * Quantized tensor.  A tensor of integer codes n plus ONE int32 exponent e per
  * tensor; the value of an element is n * 2^e.  Codes of a k-bit object lie in
- * [-(2^(k-1)-1), 2^(k-1)-1] (the clip range of Eq. 2); -128 never appears in
- * an int8 code tensor.  Exponents live in DEVICE memory (one int32 each) so
+ * [-(2^(k-1)-1), 2^(k-1)-1] (the clip range of Eq. 2): no entry point ever
+ * writes -128.  The compute entry points do not re-check their inputs (a pass
+ * over every input per call would cost about as much as the call itself): an
+ * input code of -128 is computed exactly as the value -128 * 2^e, and every
+ * bound below allows for it.  Tensors from outside the library can be checked
+ * once with iseg_check_codes.  Exponents live in DEVICE memory (one int32 each) so
  * that a producer's data-dependent scale reaches its consumer without a host
  * round trip.
  *
@@ -445,7 +449,10 @@ int iseg_spatial_sum(const int8_t* x, const int32_t* x_exp, int64_t N, int64_t H
  * the int8 logits (the adjoint of the upsampling applied to (softmax -
  * onehot) / (N H W)); and E1 = SQ(gradient, bits), the int8 error at the
  * logits (Eq. 4 / 16), exponent *err_exp.  Computed in float64.
- *   logits [N, h, w, K] int8 with exponent *logit_exp; labels [N, H, W]
+ *   logits [N, h, w, K] int8 with exponent *logit_exp in [-1000, 0]
+ *   (|logit| < 128: every exponential the region takes, of differences of
+ *   at most 4 * 127 in magnitude, stays a normal finite double; outside it ISEG_DEV_RANGE, E1 codes 0, *loss NaN); a non-finite
+ *   gradient sets ISEG_DEV_NONFINITE with the same outputs; labels [N, H, W]
  *   uint8 in [0, K) (otherwise ISEG_DEV_RANGE); loss: one device double
  *   (may be NULL); grad [N, h, w, K] device doubles (may be NULL); err
  *   [N, h, w, K] int8.  K <= 256, H >= h, W >= w. */
@@ -482,9 +489,38 @@ enum iseg_kernel_id {
  * entry point, on any stream; for the conv ids: the next call of that entry
  * point, all its kernels) records `start` immediately before and `stop`
  * immediately after itself on its own stream, then the hook disarms.  The
- * events are the caller's (hipEventCreate).  Process-global and not
- * thread-safe: meant for benchmarks.  kernel_id ISEG_KID_NONE disarms. */
+ * events are the caller's (hipEventCreate).  One arming per process: arming
+ * again replaces it.  Thread-safe: exactly one launch claims an arming, even
+ * when several threads launch at once.  kernel_id ISEG_KID_NONE disarms. */
 int iseg_profile_arm(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
+
+/* iseg_conv_last_plan -- the kernel path the calling thread's last
+ * iseg_conv_fwd / iseg_conv_bwd_data(_t) / iseg_conv_bwd_weight call took:
+ * "stem", "m32", "persist", "halo", "gemm_short", "conv_short",
+ * "dma_two_pass", "dma_split", "dma_stage16", "dma" (raw sums), "igemm",
+ * "wgrad_stem", "wgrad_taps", "wgrad_tr", "wgrad_atomic", or "none" when it
+ * returned before choosing one.  Static storage, per thread.  For tests that
+ * must reach a given kernel. */
+const char* iseg_conv_last_plan(void);
+
+/* ------------------------------------------------------------------------ */
+/* Device status word                                                        */
+/* ------------------------------------------------------------------------ */
+
+/* iseg_status_read -- copy the sticky status word (device int32) to *value
+ * (host) after the work already enqueued on `stream`; waits for the stream.
+ * ISEG_ERR_DEVICE if the copy fails. */
+int iseg_status_read(const int32_t* dev_status, int32_t* value, hipStream_t stream);
+
+/* iseg_status_clear -- zero the status word on `stream` (a one-thread kernel,
+ * so the call can sit in a captured graph). */
+int iseg_status_clear(int32_t* dev_status, hipStream_t stream);
+
+/* iseg_check_codes -- ISEG_DEV_RANGE in *dev_status if any of the n int8
+ * codes of x (device, 16-byte aligned) lies outside [-(2^(bits-1)-1),
+ * 2^(bits-1)-1] (Eq. 2's clip range), e.g. -128 in an 8-bit tensor from
+ * outside the library. */
+int iseg_check_codes(const int8_t* x, int64_t n, int32_t bits, int32_t* dev_status, hipStream_t stream);
 
 /* Library version string (static storage). */
 const char* iseg_version(void);

@@ -145,10 +145,50 @@ def _geom(geom):
     return np.asarray(geom, dtype=np.int64)
 
 
+# Large convolutions take their exact sums from a library routine instead of
+# the plain loops of the C file: torch's float64 CPU convolution (unfold and a
+# dgemm, or its transpose) adds integer products, and every partial sum here
+# stays below 2^53 (at most 2^22 pixels times 127^2), so each addition is
+# exact whatever the order.  The C loops are pinned to the same routine on
+# small shapes; this only saves time at the workloads' full sizes.
+LIBRARY_CONV_MACS = 1 << 26
+
+
+def _conv_macs(geom):
+    N, H, W, Cc, K, R, S = geom[:7]
+    P, Q = conv_out_hw(geom)
+    return N * P * Q * K * R * S * Cc
+
+
+def _nchw(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64)).permute(0, 3, 1, 2).contiguous()
+
+
+def _nhwc_int(t):
+    return t.permute(0, 2, 3, 1).contiguous().numpy().astype(np.int64)
+
+
+def _library_conv(which, a, b, geom):
+    import torch
+    import torch.nn.functional as F
+    N, H, W, Cc, K, R, S, sh, sw, ph, pw, dh, dw = [int(v) for v in geom]
+    kw = dict(stride=(sh, sw), padding=(ph, pw), dilation=(dh, dw))
+    with torch.no_grad():
+        if which == "fwd":
+            return _nhwc_int(F.conv2d(_nchw(a), _nchw(b), **kw))
+        if which == "data":
+            return _nhwc_int(torch.nn.grad.conv2d_input((N, Cc, H, W), _nchw(b), _nchw(a), **kw))
+        dwt = torch.nn.grad.conv2d_weight(_nchw(b), (K, Cc, R, S), _nchw(a), **kw)
+        return dwt.permute(0, 2, 3, 1).contiguous().numpy().astype(np.int64)
+
+
 def conv_fwd_raw(x, w, geom):
     """Exact integer forward sums (NHWC x, KRSC w) -> int64 NPQK."""
     N, H, W, Cc, K, R, S = geom[:7]
     P, Q = conv_out_hw(geom)
+    if _conv_macs(geom) >= LIBRARY_CONV_MACS:
+        return _library_conv("fwd", x, w, geom)
     x = np.ascontiguousarray(x, dtype=np.int8)
     w = np.ascontiguousarray(w, dtype=np.int8)
     out = np.zeros((N, P, Q, K), dtype=np.int64)
@@ -158,6 +198,8 @@ def conv_fwd_raw(x, w, geom):
 
 def conv_bwd_data_raw(dy, w, geom):
     N, H, W, Cc = geom[:4]
+    if _conv_macs(geom) >= LIBRARY_CONV_MACS:
+        return _library_conv("data", dy, w, geom)
     dy = np.ascontiguousarray(dy, dtype=np.int8)
     w = np.ascontiguousarray(w, dtype=np.int8)
     out = np.zeros((N, H, W, Cc), dtype=np.int64)
@@ -167,6 +209,8 @@ def conv_bwd_data_raw(dy, w, geom):
 
 def conv_bwd_weight_raw(dy, x, geom):
     K, R, S, Cc = geom[4], geom[5], geom[6], geom[3]
+    if _conv_macs(geom) >= LIBRARY_CONV_MACS:
+        return _library_conv("weight", dy, x, geom)
     dy = np.ascontiguousarray(dy, dtype=np.int8)
     x = np.ascontiguousarray(x, dtype=np.int8)
     out = np.zeros((K, R, S, Cc), dtype=np.int64)
@@ -443,10 +487,18 @@ def bilinear_matrix(n_in, n_out):
     return A
 
 
+LOGIT_EXP_MIN, LOGIT_EXP_MAX = -1000, 0
+
+
 def softmax_ce(logits, logit_exp, labels):
     """Pixel-wise softmax cross-entropy of the bilinearly upsampled logits.
     logits: int codes [N,h,w,K] with exponent logit_exp; labels [N,H,W] in
-    [0, K).  Returns (mean loss, d loss / d logits as float64 [N,h,w,K])."""
+    [0, K).  Returns (mean loss, d loss / d logits as float64 [N,h,w,K]).
+    The region's domain is logit_exp in [-1000, 0] (|logit| < 128); outside
+    it the call is rejected, as the GPU flags it."""
+    if not (LOGIT_EXP_MIN <= int(logit_exp) <= LOGIT_EXP_MAX):
+        raise OracleError("softmax_ce: logit exponent %d outside [%d, %d]"
+                          % (int(logit_exp), LOGIT_EXP_MIN, LOGIT_EXP_MAX))
     N, h, w, K = logits.shape
     _, H, W = labels.shape
     Ay, Ax = bilinear_matrix(h, H), bilinear_matrix(w, W)

@@ -2554,6 +2554,7 @@ int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t
     a.out16 = nullptr;
     a.tshift = nullptr;
     if (out_mode == ISEG_OUT_RAW) {
+        conv_plan_set("dma");
         a.out = (int32_t*)y;
         a.pmax = nullptr;
         if ((rc = launch_igemm_dma<MODE>(a, p, EPI_RAW, s, &nblk))) return rc;
@@ -2564,6 +2565,7 @@ int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t
         a.pmax = pmax;
         a.out8 = (int8_t*)y; a.exp_a = exp_a; a.exp_b = exp_b; a.out_exp = y_exp;   // both passes pick one kernel
         const bool sh = gemm_short_ok(a) || lds_short_ok(a);
+        conv_plan_set(gemm_short_ok(a) ? "gemm_short" : sh ? "conv_short" : "dma_two_pass");
         if ((rc = sh ? launch_short<MODE>(a, EPI_MAX, s, &nblk) : launch_igemm_dma<MODE>(a, p, EPI_MAX, s, &nblk)))
             return rc;
         a.npmax = nblk;
@@ -2571,6 +2573,7 @@ int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t
     }
     const int64_t n = a.Mrows * a.Nout;
     if (p.splits > 1) {
+        conv_plan_set("dma_split");
         a.out = work;
         a.pmax = nullptr;
         if ((rc = launch_igemm_dma<MODE>(a, p, EPI_PART, s, &nblk))) return rc;
@@ -2585,6 +2588,7 @@ int igemm_dma_run(IgemmArgs a, int out_mode, const int32_t* exp_a, const int32_t
         return launch_requant_apply(work, ISEG_I32, n, exp_a, exp_b, 0, 8, 0, 1, 0, 0, 0, ISEG_I8, y, y_exp,
                                     nullptr, s, pmax, nb);
     }
+    conv_plan_set("dma_stage16");
     a.out16 = (int16_t*)work;
     a.tshift = (uint8_t*)work + align256((size_t)n * 2);
     a.pmax = pmax;
@@ -3836,6 +3840,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
                              void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
 {
     ProfScope prof_scope(ISEG_KID_CONV_FWD, stream);
+    conv_plan_set("none");
     (void)dev_status;
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
@@ -3870,6 +3875,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     int rc;
     const int stem = stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K);
     if (stem && g->N > 0) {
+        conv_plan_set("stem");
         HaloArgs h{};
         h.src = x; h.wmat = w; h.out = (int32_t*)y;
         h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)g->C;
@@ -3910,6 +3916,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     const M32Plan mp = m32_plan(g->N, P, Q, Cp, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h,
                                 g->dil_w);
     if (mp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y) & 15) == 0) {
+        conv_plan_set("m32");
         HaloArgs h{};
         h.src = xs; h.wmat = wsrc; h.out = (int32_t*)y;
         h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)Cp;
@@ -3925,6 +3932,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     const PersistPlan pp = persist_plan(g->N, P, Q, Cp, g->K, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
                                         g->dil_h, g->dil_w);
     if (pp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y) & 15) == 0) {
+        conv_plan_set("persist");
         HaloArgs h{};
         h.src = xs; h.wmat = wsrc; h.out = (int32_t*)y;
         h.N = (int32_t)g->N; h.Hs = (int32_t)g->H; h.Ws = (int32_t)g->W; h.Ci = (int32_t)Cp;
@@ -3938,6 +3946,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
         return persist_q8(pp, h, ISEG_KID_CONV_FWD, x_exp, w_exp, (int8_t*)y, y_exp, pmax, stream);
     }
     if (hp.ok && (((uintptr_t)xs | (uintptr_t)wsrc | (uintptr_t)y | (uintptr_t)acc) & 15) == 0) {
+        conv_plan_set("halo");
         HaloArgs h{};
         h.src = xs; h.wmat = wsrc; h.out = acc;
         h.out16 = out_mode == ISEG_OUT_Q8 ? (int16_t*)acc : nullptr;
@@ -3955,6 +3964,7 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
     if (igemm_dma_ok(a) && ((uintptr_t)y & 15) == 0)
         return igemm_dma_run<MODE_FWD>(a, out_mode, x_exp, w_exp, y, y_exp, pmax, acc, stream);
     int64_t nblk = 0;
+    conv_plan_set("igemm");
     if ((rc = launch_igemm<MODE_FWD>(a, stream, &nblk))) return rc;
     if (out_mode == ISEG_OUT_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, y_exp, x_exp, w_exp);
@@ -3996,6 +4006,7 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
                               hipStream_t stream)
 {
     ProfScope prof_scope(ISEG_KID_CONV_BWD_DATA, stream);
+    conv_plan_set("none");
     (void)dev_status;
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
@@ -4025,6 +4036,7 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
                                 g->dil_h, g->dil_w);
     wt = pick_wt(ISEG_WT_CRSK_FLIP);
     if (mp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx) & 15) == 0) {
+        conv_plan_set("m32");
         if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, true, stream))) return rc;
         HaloArgs h{};
         h.src = dy; h.wmat = wt; h.out = (int32_t*)dx;
@@ -4043,6 +4055,7 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
                                         g->stride_w, g->dil_h, g->dil_w);
     wt = pick_wt(ISEG_WT_CRSK_FLIP);
     if (pp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx) & 15) == 0) {
+        conv_plan_set("persist");
         // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
         if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, true, stream))) return rc;
         HaloArgs h{};
@@ -4060,6 +4073,7 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
     }
     wt = pick_wt(ISEG_WT_CRSK_FLIP);
     if (hp.ok && (((uintptr_t)dy | (uintptr_t)wt | (uintptr_t)dx | (uintptr_t)acc) & 15) == 0) {
+        conv_plan_set("halo");
         // stride 1: dx = conv(dy, flipped W^T) with padding dil (R - 1) - pad
         if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, true, stream))) return rc;
         HaloArgs h{};
@@ -4093,6 +4107,7 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
     if (igemm_dma_ok(a) && ((uintptr_t)dx & 15) == 0)
         return igemm_dma_run<MODE_BWD>(a, out_mode, dy_exp, w_exp, dx, dx_exp, pmax, acc, stream);
     int64_t nblk = 0;
+    conv_plan_set("igemm");
     if ((rc = launch_igemm<MODE_BWD>(a, stream, &nblk))) return rc;
     if (out_mode == ISEG_OUT_RAW) {
         hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
@@ -4179,6 +4194,7 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
                                     int32_t* dev_status, hipStream_t stream)
 {
     ProfScope prof_scope(ISEG_KID_CONV_WGRAD, stream);
+    conv_plan_set("none");
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
     if (g_mode != ISEG_G_KEEP && g_mode != ISEG_G_DROP && g_mode != ISEG_G_RAW) return ISEG_ERR_ARG;
@@ -4218,6 +4234,7 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     };
     const int stem = stem_kind(g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w, g->dil_h, g->dil_w, g->K);
     if (stem && g->N > 0 && ((uintptr_t)dy & 15) == 0) {
+        conv_plan_set("wgrad_stem");
         // few-channel stem: MFMA over pixels, block partials, int64 sum + max partials
         int32_t* spart = (int32_t*)wp;
         HaloArgs h{};
@@ -4246,14 +4263,17 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
     if (Cp == g->C && wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) && (((uintptr_t)x | (uintptr_t)dy) & 15) == 0) {
+        conv_plan_set("wgrad_taps");
         if ((rc = launch_wgrad_taps(a, part, raw ? nullptr : pmax, &npmax, stream, raw ? nullptr : &qg))) return rc;
         return finish();
     }
     if (Cp == g->C && wgrad_tr_ok(a)) {
+        conv_plan_set("wgrad_tr");
         if ((rc = launch_wgrad_tr_split(a, part, raw ? nullptr : pmax, &npmax, stream, raw ? nullptr : &qg))) return rc;
         return finish();
     }
     // other shapes: atomic int64 accumulation (zero-filled), then the max pass
+    conv_plan_set("wgrad_atomic");
     unsigned long long* accp = acc;
     if (Cp != g->C) {
         int8_t* xp = (int8_t*)pad_region;

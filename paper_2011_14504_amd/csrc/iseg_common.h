@@ -298,25 +298,30 @@ bool lds_limit(const void* f, size_t bytes);
 // *maxp = max over n block partials (one block)
 int launch_reduce_max(const uint64_t* part, int64_t n, unsigned long long* maxp, hipStream_t s);
 
-// measurement hook (iseg_profile_arm): wrap one kernel launch
-bool prof_begin(int kid, hipStream_t s);
-void prof_end(int kid, hipStream_t s);
+// measurement hook (iseg_profile_arm): wrap one kernel launch.  prof_begin
+// claims the armed hook for this launch (at most one launch ever claims one
+// arming) and returns the event to record after it, or nullptr.
+hipEvent_t prof_begin(int kid, hipStream_t s);
+void prof_end(hipEvent_t stop, hipStream_t s);
 
-#define ISEG_TIMED_LAUNCH(kid, stream, ...)            \
-    do {                                               \
-        bool iseg_timed_ = prof_begin((kid), (stream)); \
-        hipLaunchKernelGGL(__VA_ARGS__);               \
-        if (iseg_timed_) prof_end((kid), (stream));    \
+#define ISEG_TIMED_LAUNCH(kid, stream, ...)                   \
+    do {                                                      \
+        hipEvent_t iseg_timed_ = prof_begin((kid), (stream)); \
+        hipLaunchKernelGGL(__VA_ARGS__);                      \
+        if (iseg_timed_) prof_end(iseg_timed_, (stream));     \
     } while (0)
 
 // measurement hook around a whole entry-point call (every kernel it enqueues)
 struct ProfScope {
-    int kid;
     hipStream_t s;
-    bool on;
-    ProfScope(int k, hipStream_t st) : kid(k), s(st), on(prof_begin(k, st)) {}
+    hipEvent_t stop;
+    ProfScope(int k, hipStream_t st) : s(st), stop(prof_begin(k, st)) {}
     ~ProfScope()
     {
-        if (on) prof_end(kid, s);
+        if (stop) prof_end(stop, s);
     }
 };
+
+// name of the kernel path the calling thread's last convolution entry point
+// took (iseg_conv_last_plan); set by the dispatch, per thread
+void conv_plan_set(const char* name);

@@ -24,6 +24,12 @@
 
 namespace {
 
+// the logit exponents the region accepts: |logit| < 128, so every exp() of a
+// difference of (bilinear mixes of) logits stays a normal finite double
+constexpr int kLogitExpMin = -1000, kLogitExpMax = 0;
+__device__ __forceinline__ bool logit_exp_ok(int32_t e) { return e >= kLogitExpMin && e <= kLogitExpMax; }
+
+
 // 64-bit value moved across lanes by a DPP control (both 32-bit halves)
 template <int CTRL>
 __device__ __forceinline__ double dpp_f64(double v)
@@ -176,7 +182,8 @@ __global__ __launch_bounds__(256) void k_ce_cells(const CeCellArgs a)
         wxs[c] = lx;
     }
     __syncthreads();
-    const double scale = ldexp(1.0, *a.logit_exp);
+    // outside the documented range the outputs are discarded (k_ce_quant)
+    const double scale = logit_exp_ok(*a.logit_exp) ? ldexp(1.0, *a.logit_exp) : 0.0;
     const double invP = 1.0 / ((double)a.N * (double)a.H * (double)a.W);
 
     double c00[KT], c01[KT], c10[KT], c11[KT];
@@ -392,8 +399,22 @@ __global__ __launch_bounds__(256) void k_ce_quant(const CeCellArgs a, int64_t np
                                                   int8_t* __restrict__ err, int32_t* err_exp, double* loss)
 {
     const uint64_t mb = reduce_partials_u64(a.part, nparts);
-    const int b = mb ? frexp_exp_bits64(mb) : 0;
     const int64_t total = (int64_t)a.N * a.h * a.w * a.K;
+    const bool range_ok = logit_exp_ok(*a.logit_exp);
+    if (!range_ok || mb >= 0x7ff0000000000000ull) {
+        // logits outside the region's domain, or a NaN / infinite gradient:
+        // flag it, zero codes, NaN loss
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+            set_status(a.status, range_ok ? ISEG_DEV_NONFINITE : ISEG_DEV_RANGE);
+            *err_exp = 1 - bits;
+            if (loss) *loss = __longlong_as_double(0x7ff8000000000000ll);
+        }
+        for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+             e += (int64_t)gridDim.x * blockDim.x)
+            err[e] = 0;
+        return;
+    }
+    const int b = mb ? frexp_exp_bits64(mb) : 0;
     if (blockIdx.x == 0) {
         if (threadIdx.x == 0) *err_exp = b + 1 - bits;
         // mean loss: cell losses summed in a fixed tree order

@@ -114,6 +114,10 @@ _SIGS = {
     "iseg_update_multi": ([_P, _I32, _I32, _U64, _U32, _I32, _I32, _I32, _P, _P], C.c_int),
     "iseg_philox4x32_10": ([_P, _P, _P], None),
     "iseg_profile_arm": ([_I32, _P, _P], C.c_int),
+    "iseg_conv_last_plan": ([], C.c_char_p),
+    "iseg_status_read": ([_P, _P, _P], C.c_int),
+    "iseg_status_clear": ([_P, _P], C.c_int),
+    "iseg_check_codes": ([_P, _I64, _I32, _P, _P], C.c_int),
     "iseg_version": ([], C.c_char_p),
 }
 
@@ -341,6 +345,24 @@ def iseg_philox4x32_10(ctr, key):
     o = (C.c_uint32 * 4)()
     lib().iseg_philox4x32_10(c, k, o)
     return list(o)
+
+
+def iseg_conv_last_plan():
+    return lib().iseg_conv_last_plan().decode()
+
+
+def iseg_status_read(status):
+    v = C.c_int32(0)
+    _check(lib().iseg_status_read(_ptr(status), C.byref(v), _stream()), "iseg_status_read")
+    return v.value
+
+
+def iseg_status_clear(status):
+    _check(lib().iseg_status_clear(_ptr(status), _stream()), "iseg_status_clear")
+
+
+def iseg_check_codes(x, bits, status):
+    _check(lib().iseg_check_codes(_ptr(x), x.numel(), bits, _ptr(status), _stream()), "iseg_check_codes")
 
 
 def iseg_version():

@@ -52,8 +52,14 @@ class IntNet:
         # conv's weight gradient only needs its dz and input, so it overlaps
         # the backward-data / L1BN / merge chain of the layers below
         self.side = torch.cuda.Stream(device=self.dev) if self.dev.type == "cuda" else None
+        # one sticky device status word for every call of the step (range
+        # violations the kernels detect: merge exponent gaps, BN exponents out
+        # of range, bad labels, logits outside the loss region's domain)
+        self.status = torch.zeros(1, dtype=torch.int32, device=self.dev)
         self.x = torch.from_numpy(inputs["x"]).to(self.dev)
         self.x_exp = iseg.new_exp(self.dev, inputs["x_exp"])
+        # the input codes come from outside the library: check their range once
+        iseg.iseg_check_codes(self.x, 8, self.status)
         self.dy = self.labels = None
         if wl["loss"] == "given":
             self.dy = torch.from_numpy(inputs["dy"]).to(self.dev)
@@ -139,27 +145,31 @@ class IntNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"])
+                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
+                                      status=self.status)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
-                    y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])])
+                    y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])],
+                                               status=self.status)
                     r["saved"] = saved
                 elif nd["relu"] or self.k_A < 8:
                     # without BN: A = Q_A(ReLU?(Z)) on the 8-bit conv output
-                    y, ye = iseg.sum_requant([z], [ze], relu=nd["relu"], bits=self.k_A)
+                    y, ye = iseg.sum_requant([z], [ze], relu=nd["relu"], bits=self.k_A, status=self.status)
                 else:
                     y, ye = z, ze
             elif k == "maxpool":
                 y, ye = iseg.maxpool_fwd(a, ae, nd["k"], nd["stride"], nd["pad"])
             elif k == "add":
                 b, be = act[nd["src"][1]]
-                y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"], bits=self.k_A)
+                y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"], bits=self.k_A,
+                                          status=self.status)
                 r.update(b_in=b, b_in_exp=be)
             elif k == "gap":
-                y, ye = iseg.gap_fwd(a, ae, bits=self.k_A)
+                y, ye = iseg.gap_fwd(a, ae, bits=self.k_A, status=self.status)
             elif k == "concat":
                 parts = [act[s] for s in nd["src"]]
-                y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts], bits=self.k_A)
+                y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts], bits=self.k_A,
+                                             status=self.status)
                 H, W = y.shape[1], y.shape[2]
                 r.update(widths=[p[0].shape[3] for p in parts],
                          bcast=[tuple(p[0].shape[1:3]) != (H, W) for p in parts])
@@ -174,7 +184,7 @@ class IntNet:
         out = rec[self.wl["nodes"][-1]["name"]]
         if self.wl["loss"] == "given":
             return self.dy, self.dy_exp
-        loss, grad, e, ee = iseg.softmax_ce(out["a_out"], out["a_out_exp"], self.labels)
+        loss, grad, e, ee = iseg.softmax_ce(out["a_out"], out["a_out_exp"], self.labels, status=self.status)
         self.loss = loss
         return e, ee
 
@@ -189,7 +199,8 @@ class IntNet:
             if len(parts) == 1 and not parts[0][2] and not parts[0][3]:
                 return parts[0][0], parts[0][1]
             return iseg.sum_requant([p[0] for p in parts], [p[1] for p in parts],
-                                    exp_add=[p[2] for p in parts], bcast=[p[3] for p in parts])
+                                    exp_add=[p[2] for p in parts], bcast=[p[3] for p in parts],
+                                    status=self.status)
 
         if self.wt_tab is None:
             self._build_wt_table(rec)
@@ -210,11 +221,11 @@ class IntNet:
                 if nd["bn"]:
                     dz, dze, dg, db, dge, dbe = iseg.bn_bwd(e, ee, r["z"], L["g_q"], r["saved"],
                                                             self._cfgs[int(nd["relu"])],
-                                                            dgb_out=(L["dg"], L["db"], L["dg_exp"],
+                                                            status=self.status, dgb_out=(L["dg"], L["db"], L["dg_exp"],
                                                                      L["db_exp"]))
                     r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
                 elif nd["relu"]:
-                    dz, dze = iseg.relu_mask_bwd(e, [r["z"]], [r["z_exp"]]), ee
+                    dz, dze = iseg.relu_mask_bwd(e, [r["z"]], [r["z_exp"]], status=self.status), ee
                 else:
                     dz, dze = e, ee
                 G, Ge = self._wgrad(nd, L, r, dz, dze)
@@ -223,16 +234,18 @@ class IntNet:
                 if need_in:
                     ei, eie = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
                                                  nd["stride"], nd["pad"], nd["dil"], wt=L["w_t"],
-                                                 wt_kind=L["wt_kind"])
+                                                 wt_kind=L["wt_kind"], status=self.status)
                     r.update(e_in=ei, e_in_exp=eie)
                     send(src, ei, eie)
             elif k == "maxpool":
                 if need_in:
-                    ei, eie = iseg.maxpool_bwd(e, ee, r["a_in"], nd["k"], nd["stride"], nd["pad"])
+                    ei, eie = iseg.maxpool_bwd(e, ee, r["a_in"], nd["k"], nd["stride"], nd["pad"],
+                                               status=self.status)
                     r.update(e_in=ei, e_in_exp=eie)
                     send(src, ei, eie)
             elif k == "add":
-                d = iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]])
+                d = iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]],
+                                       status=self.status)
                 r.update(e_in=d, e_in_exp=ee)
                 for s in nd["src"]:
                     if s != "input" or want_input:
@@ -240,7 +253,7 @@ class IntNet:
             elif k == "gap":
                 if need_in:
                     H, W = r["a_in"].shape[1:3]
-                    eg, ege = iseg.gap_bwd(e, ee, H, W)
+                    eg, ege = iseg.gap_bwd(e, ee, H, W, status=self.status)
                     r.update(e_in=eg, e_in_exp=ege)
                     send(src, eg, ege, bcast=1)
             elif k == "concat":
@@ -248,7 +261,7 @@ class IntNet:
                 c0 = 0
                 for s, p, wdt, bc in zip(nd["src"], parts, r["widths"], r["bcast"]):
                     if bc:
-                        pe, pee = iseg.spatial_sum(e, ee, 1, c0, wdt)
+                        pe, pee = iseg.spatial_sum(e, ee, 1, c0, wdt, status=self.status)
                         send(s, pe, pee)
                     else:
                         send(s, p, ee)
@@ -266,11 +279,11 @@ class IntNet:
         args = (dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"],
                 self.g_mode, 8, self.seed, 16 * L["l"], self.step_no)
         if self.side is None:
-            return iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]))
+            return iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]), status=self.status)
         ready = torch.cuda.current_stream(self.dev).record_event()
         with torch.cuda.stream(self.side):
             self.side.wait_event(ready)
-            G, Ge = iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]))
+            G, Ge = iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]), status=self.status)
         for t in (dz, dze, r["a_in"], r["a_in_exp"]):
             t.record_stream(self.side)
         return G, Ge
@@ -278,13 +291,18 @@ class IntNet:
     def update(self, grads):
         """Q_G of gamma / beta, Eq. 19 and Q_W for every parameter: one launch."""
         iseg.iseg_update_multi(self.upd_table, self.upd_n, 8, self.seed, self.step_no, self.lr_shift,
-                               self.k_U, self.k_W)
+                               self.k_U, self.k_W, status=self.status)
         if self.wt_tab is not None:
             self._transpose_weights()
         for nd, r in grads:
             if nd["bn"]:
                 L = self.convs[nd["name"]]
                 r.update(Gg=L["Gg"], Gb=L["Gb"], Gg_exp=L["Gg_exp"], Gb_exp=L["Gb_exp"])
+
+    def read_status(self):
+        """The sticky status word after the work enqueued so far (waits for
+        the current stream): 0, or ISEG_DEV_* bits."""
+        return iseg.iseg_status_read(self.status)
 
     def step(self):
         rec = self.forward()

@@ -249,62 +249,66 @@ def test_conv_bwd_weight_long_reduction(orc, dev):
     assert np.array_equal(H(raw), ref)
 
 
-# Full-size shapes of the DeepLabv3 step whose reduction is split across
-# blocks (ASPP 3x3 branches), tiled without a split, or short enough for
-# the two-pass persistent kernel: raw int32 sums at
-# sampled output pixels against exact integer dot products, and the final
-# codes against the requant of those sums under the exponent the kernel chose.
-FULL_SHAPES = [
-    (8, 32, 32, 2048, 256, 3, 1, 6, 6),
-    (8, 32, 32, 2048, 256, 3, 1, 18, 18),
-    (8, 32, 32, 1024, 2048, 1, 1, 0, 1),
-    # short reductions, persistent blocks of several row tiles each
-    (8, 128, 128, 64, 256, 1, 1, 0, 1),
-    (8, 32, 32, 256, 1024, 1, 1, 0, 1),
+# Full-size layer shapes of the DeepLabv3-ResNet50 step (batch 8, 512x512),
+# one per kernel path the step takes: (pass, N, H, W, C, K, R, stride, pad,
+# dil, the path iseg_conv_last_plan must report for the final codes).  Whole
+# tensors are compared: the raw int32 sums with the oracle's exact sums (its
+# library path: float64 convolutions, exact on these integers), the codes
+# with the oracle's requant of those sums -- never of the GPU's own sums.
+FULL_CASES = [
+    ("fwd", 8, 32, 32, 2048, 256, 3, 1, 6, 6, "dma_split"),        # ASPP branches
+    ("fwd", 8, 32, 32, 2048, 256, 3, 1, 18, 18, "dma_split"),
+    ("fwd", 8, 32, 32, 1024, 2048, 1, 1, 0, 1, "dma_stage16"),     # layer4.0 projection
+    ("fwd", 8, 128, 128, 64, 256, 1, 1, 0, 1, "gemm_short"),      # layer1 conv3
+    ("fwd", 8, 64, 64, 128, 512, 1, 1, 0, 1, "conv_short"),       # layer2 conv3
+    ("fwd", 8, 32, 32, 256, 1024, 1, 1, 0, 1, "dma_two_pass"),    # layer3 conv3
+    ("data", 8, 64, 64, 512, 128, 1, 1, 0, 1, "conv_short"),      # layer2.{1-3}.conv1
+    ("data", 8, 128, 128, 256, 64, 1, 1, 0, 1, "gemm_short"),     # layer1.{1,2}.conv1
+    ("data", 8, 32, 32, 2048, 256, 3, 1, 6, 6, None),             # ASPP branches
+    ("data", 8, 32, 32, 2048, 256, 3, 1, 12, 12, None),
+    ("data", 8, 32, 32, 2048, 256, 3, 1, 18, 18, None),
+    ("data", 8, 64, 64, 512, 1024, 1, 2, 0, 1, None),              # layer3.0 projection (strided)
 ]
 
 
-def _sampled_conv_ref(x, w, s, pix):
-    N, Hh, W, Cc, K, R, st, pad, d = s
-    out = []
-    for (n, p, q) in pix:
-        acc = np.zeros(K, np.int64)
-        for r in range(R):
-            for t in range(R):
-                ih, iw = p * st - pad + r * d, q * st - pad + t * d
-                if 0 <= ih < Hh and 0 <= iw < W:
-                    acc += w[:, r, t, :].astype(np.int64) @ x[n, ih, iw, :].astype(np.int64)
-        out.append(acc)
-    return np.stack(out)
-
-
-@pytest.mark.parametrize("s", FULL_SHAPES, ids=str)
-def test_conv_fwd_full_size_sampled(orc, dev, s):
+@pytest.mark.parametrize("case", FULL_CASES, ids=lambda c: "-".join(str(v) for v in c))
+def test_conv_full_size(orc, dev, case):
     from paper_2011_14504_amd import iseg
+    which, plan, s = case[0], case[-1], case[1:-1]
     N, Hh, W, Cc, K, R, st, pad, d = s
-    x = synth.int_codes(91, (N, Hh, W, Cc))
+    g = _geom(s)
+    P, Q = orc.conv_out_hw(g)
     w = synth.int_codes(92, (K, R, R, Cc))
-    raw, _ = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d,
-                           out_mode=iseg.ISEG_OUT_RAW)
-    y, ye = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d)
-    rng = synth.rng(93)
-    pix = [(int(rng.integers(N)), int(rng.integers(Hh)), int(rng.integers(W))) for _ in range(24)]
-    pix += [(0, 0, 0), (N - 1, Hh - 1, W - 1), (3, 0, W - 1)]
-    ref = _sampled_conv_ref(x, w, s, pix)
-    R_ = H(raw)
-    got = np.stack([R_[n, p, q] for (n, p, q) in pix]).astype(np.int64)
-    assert np.array_equal(got, ref)
-    # codes: the requant of the full raw tensor (checked above at the samples)
-    rc, rce = orc.requant(R_.astype(np.int64), -14, 8)
+    print(f"[full-size conv] {which} {s}", flush=True)
+    if which == "fwd":
+        x = synth.int_codes(91, (N, Hh, W, Cc))
+        ref = orc._library_conv("fwd", x, w, g)
+        raw, _ = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d,
+                               out_mode=iseg.ISEG_OUT_RAW)
+        y, ye = iseg.conv_fwd(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d)
+    else:
+        dy = synth.int_codes(93, (N, P, Q, K))
+        ref = orc._library_conv("data", dy, w, g)
+        raw, _ = iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc),
+                                    st, pad, d, out_mode=iseg.ISEG_OUT_RAW)
+        y, ye = iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc),
+                                   st, pad, d)
+    took = iseg.iseg_conv_last_plan()
+    print(f"  path {took}", flush=True)
+    if plan is not None:
+        assert took == plan, (took, plan)
+    assert np.array_equal(H(raw).astype(np.int64), ref)
+    rc, rce = orc.requant(ref, -14 if which == "fwd" else -27, 8)
     assert ev(ye) == rce and np.array_equal(H(y).astype(np.int64), rc)
 
 
-@pytest.mark.parametrize("s", [(8, 32, 32, 2048, 256, 3, 1, 6, 6), (8, 64, 64, 128, 512, 1, 1, 0, 1)], ids=str)
-def test_conv_bwd_weight_full_size_sampled(orc, dev, s):
-    """Full-size weight gradients whose reduction is split over blocks: raw
-    sums at sampled weights against exact dot products over every output
-    pixel, and Q_G (kept and dropped scale) of the whole tensor against the
-    oracle's requant of the raw sums."""
+@pytest.mark.parametrize("s", [(8, 32, 32, 2048, 256, 3, 1, 6, 6), (8, 64, 64, 128, 512, 1, 1, 0, 1),
+                               (8, 128, 128, 64, 64, 3, 1, 1, 1), (8, 32, 32, 512, 512, 3, 1, 2, 2)],
+                         ids=str)
+def test_conv_bwd_weight_full_size(orc, dev, s):
+    """Full-size weight gradients whose reduction is split over blocks: the
+    whole raw int64 tensor against the oracle's exact sums, and Q_G (kept
+    and dropped scale) against the oracle's requant of those sums."""
     from paper_2011_14504_amd import iseg
     N, Hh, W, Cc, K, R, st, pad, d = s
     P, Q = orc.conv_out_hw(_geom(s))
@@ -312,19 +316,13 @@ def test_conv_bwd_weight_full_size_sampled(orc, dev, s):
     x = synth.int_codes(95, (N, Hh, W, Cc))
     raw, re = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (K, R, R, Cc),
                                    st, pad, d, g_mode=iseg.ISEG_G_RAW)
-    R_ = H(raw)
-    rng = synth.rng(96)
-    xp = np.zeros((N, Hh + 2 * pad, W + 2 * pad, Cc), np.int64)
-    xp[:, pad:pad + Hh, pad:pad + W, :] = x
-    dyl = dy.astype(np.int64)
-    for _ in range(12):
-        k, r, t, c = (int(rng.integers(K)), int(rng.integers(R)), int(rng.integers(R)), int(rng.integers(Cc)))
-        win = xp[:, r * d:r * d + (P - 1) * st + 1:st, t * d:t * d + (Q - 1) * st + 1:st, c]
-        assert int(R_[k, r, t, c]) == int((dyl[..., k] * win).sum()), (k, r, t, c)
+    ref = orc._library_conv("weight", dy, x, _geom(s))
+    assert np.array_equal(H(raw), ref) and ev(re) == -27
     for mode, keep in ((iseg.ISEG_G_KEEP, True), (iseg.ISEG_G_DROP, False)):
         g, ge = iseg.conv_bwd_weight(T(dy, dev), E(-20, dev), T(x, dev), E(-7, dev), (K, R, R, Cc),
                                      st, pad, d, g_mode=mode, seed=77, tensor_id=48, step=5)
-        rc, rce = orc.requant(R_.astype(np.int64), ev(re), 8, stochastic=True, keep_scale=keep, seed=77,
+        print(f"  wgrad path {iseg.iseg_conv_last_plan()}", flush=True)
+        rc, rce = orc.requant(ref, -27, 8, stochastic=True, keep_scale=keep, seed=77,
                               tensor_id=48, step=5)
         assert np.array_equal(H(g).astype(np.int64), rc) and ev(ge) == rce
 

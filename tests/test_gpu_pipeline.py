@@ -35,8 +35,10 @@ def _run_both(wl, steps=1, **widths):
     for s in range(steps):
         print(f"[pipeline] {wl['name']} N={wl['N']} {wl['H']}x{wl['W']} {widths} step {s}", flush=True)
         grec = gnet.step()
-        orec = onet.step()
         torch.cuda.synchronize()
+        print(f"[pipeline]   GPU step done; oracle step", flush=True)
+        orec = onet.step()
+        assert gnet.read_status() == 0, f"step {s}: device status {gnet.read_status()}"
         for nd in wl["nodes"]:
             name = nd["name"]
             g, o = grec[name], orec[name]
@@ -132,3 +134,23 @@ def test_vgg16_blocks12_no_bn_gq2_two_steps():
 
 def test_resnet50_conv2x_no_bn_gq2_w4a4():
     _run_both(synth.without_bn(synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28)), steps=2, gq=2, **W4A4)
+
+
+# The workloads at their stated batch sizes (workloads 2-4) and the benchmarked
+# DeepLabv3-ResNet50 step at its full 512x512 resolution (batch 2 of the
+# benchmark's 8: the oracle takes about a minute per image), every tensor
+# compared element by element.
+def test_vgg16_blocks12_full_batch_8():
+    _run_both(synth.VGG16_BLOCKS12)
+
+
+def test_resnet50_conv2x_full_batch_16():
+    _run_both(synth.RESNET50_CONV2X)
+
+
+def test_aspp_head_full_batch_8():
+    _run_both(synth.ASPP_HEAD)
+
+
+def test_deeplabv3_r50_512px_batch_2():
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 2))

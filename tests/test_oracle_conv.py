@@ -105,3 +105,29 @@ def test_conv_requant_composition(orc):
     acc = orc.conv_fwd_raw(x, w, _geom(s))
     ref = bf.SQ([Fr(int(v)) * Fr(2) ** -14 for v in acc.ravel()], 8)
     assert [Fr(int(c)) * Fr(2) ** e for c in codes.ravel()] == ref
+
+
+@pytest.mark.parametrize("geom", [(2, 19, 17, 32, 48, 3, 3, 2, 2, 2, 2, 2, 2),
+                                  (1, 23, 21, 24, 40, 3, 3, 1, 1, 6, 6, 6, 6),
+                                  (3, 16, 16, 64, 32, 1, 1, 2, 2, 0, 0, 1, 1)])
+def test_library_conv_path_equals_loops(orc, geom):
+    """The library path the oracle takes for large convolutions gives the
+    same exact sums as its plain loops (forced on medium shapes here)."""
+    rng = synth.rng(977)
+    N, H, W, Cc, K, R, S = geom[:7]
+    P, Q = orc.conv_out_hw(geom)
+    x = rng.integers(-127, 128, (N, H, W, Cc)).astype(np.int8)
+    w = rng.integers(-127, 128, (K, R, S, Cc)).astype(np.int8)
+    dy = rng.integers(-127, 128, (N, P, Q, K)).astype(np.int8)
+    saved = orc.LIBRARY_CONV_MACS
+    try:
+        orc.LIBRARY_CONV_MACS = 1 << 62
+        loops = (orc.conv_fwd_raw(x, w, geom), orc.conv_bwd_data_raw(dy, w, geom),
+                 orc.conv_bwd_weight_raw(dy, x, geom))
+        orc.LIBRARY_CONV_MACS = 0
+        lib_ = (orc.conv_fwd_raw(x, w, geom), orc.conv_bwd_data_raw(dy, w, geom),
+                orc.conv_bwd_weight_raw(dy, x, geom))
+    finally:
+        orc.LIBRARY_CONV_MACS = saved
+    for a, b in zip(loops, lib_):
+        assert a.dtype == b.dtype == np.int64 and np.array_equal(a, b)
