@@ -261,6 +261,25 @@ int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
                 int8_t* y_out, int32_t* y_exp, void* saved,
                 void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
+/* iseg_bn_fwd_noalloc -- iseg_bn_fwd for callers that cannot allocate
+ * device memory (code under graph capture, serving loops, harnesses that
+ * forbid hipMalloc): the same computation and outputs, with the workspace in
+ * a static device array of iseg_bn_fwd_noalloc_max_bytes() bytes (8 MiB,
+ * one per GPU, held until the process ends) instead of a caller buffer.
+ * Enough for every C <= 2048 at any M; a shape whose iseg_bn_fwd_ws()
+ * exceeds it returns ISEG_ERR_WORKSPACE before anything is enqueued.  Every
+ * call on a GPU uses that GPU's one array: calls that overlap on one GPU
+ * (other streams, other threads) race and must be serialized by the caller.
+ * Nothing has to be cleared between calls.  Allocates nothing (no hipMalloc,
+ * no library routine that allocates); the array's device address is looked
+ * up once per device on the first call there (ISEG_ERR_DEVICE if that
+ * fails). */
+size_t iseg_bn_fwd_noalloc_max_bytes(void);
+int iseg_bn_fwd_noalloc(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
+                        const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
+                        int8_t* y_out, int32_t* y_exp, void* saved, int32_t* dev_status,
+                        hipStream_t stream);
+
 /* iseg_bn_bwd -- exact derivative of Eq. 12-13 with straight-through
  * quantizers (the paper prints no backward formula), for the forward that
  * filled `saved` from the same x:

@@ -27,6 +27,8 @@
 //           -> table -> apply (gather).  k_E2 < 15 adds a second streaming
 //           pass: stats tails give max|gamma delta| (E2's scale), stats2 sums
 //           the rounded E2 terms and its tails give E1's exponent.
+#include <mutex>
+
 #include "iseg_common.h"
 
 namespace {
@@ -1428,10 +1430,10 @@ extern "C" size_t iseg_bn_bwd_ws(int64_t M, int64_t C)
     return bwd_ws_bytes(make_stream(M, C, cs, 4, ISEG_BNB_ROWS, kMaxBlocks));
 }
 
-extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
-                           const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
-                           int8_t* y_out, int32_t* y_exp, void* saved,
-                           void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+static int bn_fwd_impl(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
+                       const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
+                       int8_t* y_out, int32_t* y_exp, void* saved,
+                       void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
 {
     if (M < 1 || C < 4) return ISEG_ERR_SHAPE;
     if (!shape_ok(M, C)) return ISEG_ERR_UNSUPPORTED;
@@ -1472,6 +1474,62 @@ extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int
                           x, y_out, s4, sv);
     }
     return launch_ok();
+}
+
+extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
+                           const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
+                           int8_t* y_out, int32_t* y_exp, void* saved,
+                           void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    return bn_fwd_impl(x, x_exp, M, C, gamma_q, beta_q, cfg, y_out, y_exp, saved, ws, ws_bytes, dev_status,
+                       stream);
+}
+
+// ---------------------------------------------------------------------------
+// iseg_bn_fwd_noalloc: the same forward with its workspace in a static device
+// array (one copy per GPU, held until the process ends) instead of a caller
+// buffer.  In host code `scratch` names a host-side stand-in, not device
+// memory: its device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and only that address is
+// passed to the kernels.  The forward's workspace is written before it is
+// read within a call (per-block partials, per-channel tables), so nothing
+// needs clearing between calls.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t kBnScratchBytes = (size_t)8 << 20;
+constexpr int kScratchDevices = 64;
+__device__ __align__(256) unsigned char scratch[kBnScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+}  // namespace
+
+static void* bn_scratch_ptr()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+extern "C" size_t iseg_bn_fwd_noalloc_max_bytes(void) { return kBnScratchBytes; }
+
+extern "C" int iseg_bn_fwd_noalloc(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
+                                   const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
+                                   int8_t* y_out, int32_t* y_exp, void* saved, int32_t* dev_status,
+                                   hipStream_t stream)
+{
+    const size_t need = iseg_bn_fwd_ws(M, C);
+    if (need == 0) return M < 1 || C < 4 ? ISEG_ERR_SHAPE : ISEG_ERR_UNSUPPORTED;
+    if (need > kBnScratchBytes) return ISEG_ERR_WORKSPACE;
+    void* ws = bn_scratch_ptr();
+    if (!ws) return ISEG_ERR_DEVICE;
+    return bn_fwd_impl(x, x_exp, M, C, gamma_q, beta_q, cfg, y_out, y_exp, saved, ws, kBnScratchBytes,
+                       dev_status, stream);
 }
 
 extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,

@@ -87,6 +87,8 @@ _SIGS = {
     "iseg_bn_saved_bytes": ([_I64], _SZ),
     "iseg_bn_fwd_ws": ([_I64, _I64], _SZ),
     "iseg_bn_fwd": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_bn_fwd_noalloc_max_bytes": ([], _SZ),
+    "iseg_bn_fwd_noalloc": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "iseg_bn_bwd_ws": ([_I64, _I64], _SZ),
     "iseg_bn_bwd": ([_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P],
                     C.c_int),
@@ -228,6 +230,12 @@ def iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, ws, stat
                            _ptr(y), _ptr(y_exp), _ptr(saved), *_ws_tuple(ws), _ptr(status),
                            _stream())
     _check(rc, "iseg_bn_fwd")
+
+
+def iseg_bn_fwd_noalloc(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, status=None):
+    rc = lib().iseg_bn_fwd_noalloc(_ptr(x), _ptr(x_exp), M, Cc, _ptr(gamma_q), _ptr(beta_q), C.byref(cfg),
+                                   _ptr(y), _ptr(y_exp), _ptr(saved), _ptr(status), _stream())
+    _check(rc, "iseg_bn_fwd_noalloc")
 
 
 def iseg_bn_bwd(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, dx_exp, dgamma, dbeta, dgamma_exp,
