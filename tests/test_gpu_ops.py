@@ -264,10 +264,10 @@ FULL_CASES = [
     ("fwd", 8, 32, 32, 256, 1024, 1, 1, 0, 1, "dma_two_pass"),    # layer3 conv3
     ("data", 8, 64, 64, 512, 128, 1, 1, 0, 1, "conv_short"),      # layer2.{1-3}.conv1
     ("data", 8, 128, 128, 256, 64, 1, 1, 0, 1, "gemm_short"),     # layer1.{1,2}.conv1
-    ("data", 8, 32, 32, 2048, 256, 3, 1, 6, 6, None),             # ASPP branches
-    ("data", 8, 32, 32, 2048, 256, 3, 1, 12, 12, None),
-    ("data", 8, 32, 32, 2048, 256, 3, 1, 18, 18, None),
-    ("data", 8, 64, 64, 512, 1024, 1, 2, 0, 1, None),              # layer3.0 projection (strided)
+    ("data", 8, 32, 32, 2048, 256, 3, 1, 6, 6, "dma_stage16"),    # ASPP branches
+    ("data", 8, 32, 32, 2048, 256, 3, 1, 12, 12, "dma_stage16"),
+    ("data", 8, 32, 32, 2048, 256, 3, 1, 18, 18, "dma_stage16"),
+    ("data", 8, 64, 64, 512, 1024, 1, 2, 0, 1, "dma_stage16"),     # layer3.0 projection (strided)
 ]
 
 
