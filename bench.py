@@ -162,6 +162,8 @@ def main():
     ap.add_argument("--gq", type=int, default=1, choices=(1, 2),
                     help="weight-gradient quantizer: 1 keeps Scale(G) (Eq. 17), 2 drops it (Eq. 18)")
     ap.add_argument("--no-bn", action="store_true", help="the same network without L1BN")
+    ap.add_argument("--bn-input", default="q8", choices=("q8", "raw"),
+                    help="L1BN on the SQ8 conv output (q8) or on the raw int32 sums (the literal dataflow)")
     ap.add_argument("--copy-kernel-mib", type=int, default=0,
                     help="only run the plain copy kernel used to calibrate the HBM byte counters")
     ap.add_argument("--timed-kernel", default="conv_fwd:aspp.b1",
@@ -187,7 +189,7 @@ def main():
     N = wl["N"]
     inp = synth.workload_inputs(wl)
     widths = dict(k_W=args.k_w, k_U=args.k_u, bn_cfg={"k_A": args.k_a, "k_E2": args.k_e2}, gq=args.gq)
-    net = IntNet(wl, inp, "cuda:0", **widths)
+    net = IntNet(wl, inp, "cuda:0", bn_input=args.bn_input, **widths)
     ops, detail = workload_ops(wl)
     tk = args.timed_kernel
     if args.workload != "deeplabv3" and tk == "conv_fwd:aspp.b1":
@@ -231,7 +233,7 @@ def main():
                convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
                pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
                bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u), gq=args.gq,
-               l1bn=not args.no_bn)
+               l1bn=not args.no_bn, bn_input=args.bn_input)
     status = net.read_status()
     if net.loss is not None:
         cfg["loss"] = float(net.loss.item())

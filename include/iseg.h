@@ -300,6 +300,32 @@ int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
                 int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
                 void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
+/* iseg_bn_fwd_i32 / iseg_bn_bwd_i32 -- the same L1BN forward and backward
+ * (Eq. 12-15, 16) on the raw int32 sums of a convolution (iseg_conv_fwd with
+ * ISEG_OUT_RAW), the literal dataflow of Sec. 3.2.2-3.2.3: BN takes the MAC
+ * output before any activation quantizer, x-hat is quantized to k_xhat bits
+ * because the bit width has grown, and Q_A (Eq. 15) follows BN.  Every
+ * quantity is defined as for iseg_bn_fwd / iseg_bn_bwd; only the input is
+ * wider.
+ *   x [M, C] int32 with exponent s_x in [-40, 0] (ISEG_DEV_RANGE outside),
+ *   M <= 2^22, C % 4 == 0.  saved: iseg_bn_i32_saved_bytes(C) bytes, its own
+ *   layout (int32 hdr[16] = {b, y grid exponent, A exponent, s_x, A's shift},
+ *   then each 256-byte aligned int32 n_mu[C], den[C], mlo[C], mhi[C]: the
+ *   inputs with y > 0 form [mlo, mhi]).  The backward supports the exact E2
+ *   (k_E2 >= 15) only (ISEG_ERR_UNSUPPORTED otherwise). */
+size_t iseg_bn_i32_saved_bytes(int64_t C);
+size_t iseg_bn_fwd_i32_ws(int64_t M, int64_t C);
+int iseg_bn_fwd_i32(const int32_t* x, const int32_t* x_exp, int64_t M, int64_t C,
+                    const int8_t* gamma_q, const int8_t* beta_q, const iseg_bn_cfg* cfg,
+                    int8_t* y_out, int32_t* y_exp, void* saved,
+                    void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+size_t iseg_bn_bwd_i32_ws(int64_t M, int64_t C);
+int iseg_bn_bwd_i32(const int8_t* dy, const int32_t* dy_exp, const int32_t* x, int64_t M, int64_t C,
+                    const int8_t* gamma_q, const iseg_bn_cfg* cfg, const void* saved, int8_t* dx_out,
+                    int32_t* dx_exp, int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp,
+                    int32_t* dbeta_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                    hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Update (Eq. 19) and weight quantizer (Eq. 7-8)                            */
 /* ------------------------------------------------------------------------ */

@@ -358,7 +358,9 @@ void orc_conv_bwd_weight_raw(const int8_t* dy, const int8_t* x, const int64_t* g
 /* ------------------------------------------------------------------------ */
 /* L1 batch normalization, forward (Eq. 12-15).                               */
 /*                                                                            */
-/* Input: int codes q (NHWC flattened to M rows x C channels), exponent s_x.  */
+/* Input: integer codes q (NHWC flattened to M rows x C channels), exponent */
+/* s_x: int8 codes of a requantized conv output, or the conv's raw int32    */
+/* sums (the wide input of the literal dataflow, orc_bn_fwd32).            */
 /* Per channel c over its m = M values:                                       */
 /*   mu     = (1/m) sum x                                     (Eq. 10)        */
 /*   mu_q   = 2 UQ(mu/2, k_mu)        -> code n_mu, value n_mu 2^(2-k_mu)     */
@@ -383,6 +385,9 @@ void orc_conv_bwd_weight_raw(const int8_t* dy, const int8_t* x, const int64_t* g
 /* |xhat| < 2^37 (b <= 37), y on its grid < 2^44, and the backward bracket   */
 /* m^2 f - m sum f - (sum f n_xhat) 2^(b-15) (m s - Z) < 2^96 in __int128.   */
 /* s_x = -40 keeps 2^(e_mu - g) = 2^26 and the sum of |D| likewise in range. */
+/* Raw int32 input (|q| < 2^31): s_x in [-40, 0], so |D| < 2^46, the sum of  */
+/* |D| < 2^68 (held in __int128 here), |xhat| < 2^46 (b <= 46), y < 2^54 on  */
+/* its grid and the backward bracket < 2^106.                               */
 /* ------------------------------------------------------------------------ */
 typedef struct {
     int k_mu, k_sigma, k_xhat, k_gamma, k_beta, k_A, k_E1, k_E2, eps_code, relu;
@@ -394,7 +399,7 @@ typedef struct {
     int g;               /* exponent of the grid on which D = x - mu_q is an integer */
 } orc_bn_chan;
 
-static int bn_channel_stats(const int8_t* x, int32_t s_x, int64_t M, int64_t C, int64_t c,
+static int bn_channel_stats(const int32_t* x, int32_t s_x, int64_t M, int64_t C, int64_t c,
                             const orc_bn_cfg* cf, orc_bn_chan* st)
 {
     int e_mu = 2 - cf->k_mu, e_sig = 2 - cf->k_sigma;
@@ -421,7 +426,7 @@ static int bn_channel_stats(const int8_t* x, int32_t s_x, int64_t M, int64_t C, 
 }
 
 /* D_i = (x_i - mu_q) / 2^g, an exact integer */
-static i128 bn_D(int8_t q, int32_t s_x, const orc_bn_chan* st, int e_mu)
+static i128 bn_D(int32_t q, int32_t s_x, const orc_bn_chan* st, int e_mu)
 {
     return (i128)q * p2(s_x - st->g) - (i128)st->n_mu * p2(e_mu - st->g);
 }
@@ -429,12 +434,12 @@ static i128 bn_D(int8_t q, int32_t s_x, const orc_bn_chan* st, int e_mu)
 /* xhat_i = D_i 2^(g - e_sigma) / den : returns numerator D, the power of two,
  * and den via the channel stats.  The tensor exponent b of Q_xhat:
  * smallest b with max|xhat| < 2^b. */
-static int bn_fwd_core(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
+static int bn_fwd_core(const int32_t* x, int32_t s_x, int wide, int64_t M, int64_t C,
                        const int8_t* gq, const int8_t* bq, const orc_bn_cfg* cf,
                        orc_bn_chan* st, int* b_out, int16_t* nxh /* M*C */,
                        i128* Y /* M*C, pre-ReLU y on grid 2^e_y */, int* e_y_out)
 {
-    if (s_x < -40 || s_x > 16 || M < 1 || M > ((int64_t)1 << 22)) return ORC_ERR_RANGE;
+    if (s_x < -40 || s_x > (wide ? 0 : 16) || M < 1 || M > ((int64_t)1 << 22)) return ORC_ERR_RANGE;
     int e_mu = 2 - cf->k_mu, e_sig = 2 - cf->k_sigma;
     for (int64_t c = 0; c < C; c++) bn_channel_stats(x, s_x, M, C, c, cf, &st[c]);
     /* b = smallest integer with |xhat_i| < 2^b for all i */
@@ -468,10 +473,10 @@ static int bn_fwd_core(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
     return ORC_OK;
 }
 
-int orc_bn_fwd(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
-               const int8_t* gq, const int8_t* bq, const int32_t* cfg_arr,
-               int8_t* out, int32_t* out_exp,
-               int32_t* n_mu, int32_t* n_sigma, int32_t* b_xhat, int16_t* nxh_out)
+static int bn_fwd_any(const int32_t* x, int32_t s_x, int wide, int64_t M, int64_t C,
+                      const int8_t* gq, const int8_t* bq, const int32_t* cfg_arr,
+                      int8_t* out, int32_t* out_exp,
+                      int32_t* n_mu, int32_t* n_sigma, int32_t* b_xhat, int16_t* nxh_out)
 {
     orc_bn_cfg cf = { cfg_arr[0], cfg_arr[1], cfg_arr[2], cfg_arr[3], cfg_arr[4],
                       cfg_arr[5], cfg_arr[6], cfg_arr[7], cfg_arr[8], cfg_arr[9] };
@@ -479,7 +484,7 @@ int orc_bn_fwd(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
     int16_t* nxh = (int16_t*)malloc(sizeof(int16_t) * (size_t)(M * C));
     i128* Y = (i128*)malloc(sizeof(i128) * (size_t)(M * C));
     int b = 0, e_y = 0;
-    int rc = bn_fwd_core(x, s_x, M, C, gq, bq, &cf, st, &b, nxh, Y, &e_y);
+    int rc = bn_fwd_core(x, s_x, wide, M, C, gq, bq, &cf, st, &b, nxh, Y, &e_y);
     if (rc == ORC_OK) {
         /* ReLU, then A = SQ(y, k_A) with one power-of-two scale per tensor */
         i128 Mx = 0;
@@ -504,6 +509,34 @@ int orc_bn_fwd(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
     return rc;
 }
 
+/* int8 codes widened to int32 (exact), for the one core of both inputs */
+static int32_t* widen8(const int8_t* x, int64_t n)
+{
+    int32_t* w = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    for (int64_t i = 0; i < n; i++) w[i] = x[i];
+    return w;
+}
+
+int orc_bn_fwd(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
+               const int8_t* gq, const int8_t* bq, const int32_t* cfg_arr,
+               int8_t* out, int32_t* out_exp,
+               int32_t* n_mu, int32_t* n_sigma, int32_t* b_xhat, int16_t* nxh_out)
+{
+    int32_t* w = widen8(x, M * C);
+    int rc = bn_fwd_any(w, s_x, 0, M, C, gq, bq, cfg_arr, out, out_exp, n_mu, n_sigma, b_xhat, nxh_out);
+    free(w);
+    return rc;
+}
+
+/* the same forward on the raw int32 sums of a convolution */
+int orc_bn_fwd32(const int32_t* x, int32_t s_x, int64_t M, int64_t C,
+                 const int8_t* gq, const int8_t* bq, const int32_t* cfg_arr,
+                 int8_t* out, int32_t* out_exp,
+                 int32_t* n_mu, int32_t* n_sigma, int32_t* b_xhat, int16_t* nxh_out)
+{
+    return bn_fwd_any(x, s_x, 1, M, C, gq, bq, cfg_arr, out, out_exp, n_mu, n_sigma, b_xhat, nxh_out);
+}
+
 /* ------------------------------------------------------------------------ */
 /* L1 batch normalization, backward.  The paper prints no formula; this is    */
 /* the exact derivative of Eq. 12-13 with straight-through estimators across */
@@ -519,12 +552,12 @@ int orc_bn_fwd(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
 /*   d xhat_i/dx_j = [(delta_ij - 1/m) - xhat_i (s_j - mean(s))/m]/(sigma+eps)*/
 /* Optional dx_pre receives the value of dx before E1's quantizer (double).   */
 /* ------------------------------------------------------------------------ */
-int orc_bn_bwd(const int8_t* dA, int32_t s_d, const int8_t* x, int32_t s_x,
-               int64_t M, int64_t C, const int8_t* gq, const int8_t* bq,
-               const int32_t* cfg_arr,
-               int8_t* dx, int32_t* dx_exp,
-               int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
-               double* dx_pre, int64_t* zero_sum_failures)
+static int bn_bwd_any(const int8_t* dA, int32_t s_d, const int32_t* x, int32_t s_x, int wide,
+                      int64_t M, int64_t C, const int8_t* gq, const int8_t* bq,
+                      const int32_t* cfg_arr,
+                      int8_t* dx, int32_t* dx_exp,
+                      int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
+                      double* dx_pre, int64_t* zero_sum_failures)
 {
     orc_bn_cfg cf = { cfg_arr[0], cfg_arr[1], cfg_arr[2], cfg_arr[3], cfg_arr[4],
                       cfg_arr[5], cfg_arr[6], cfg_arr[7], cfg_arr[8], cfg_arr[9] };
@@ -535,7 +568,7 @@ int orc_bn_bwd(const int8_t* dA, int32_t s_d, const int8_t* x, int32_t s_x,
     i128* F = (i128*)malloc(sizeof(i128) * (size_t)(M * C));
     i128* B = (i128*)malloc(sizeof(i128) * (size_t)(M * C));
     int b = 0, e_y = 0;
-    int rc = bn_fwd_core(x, s_x, M, C, gq, bq, &cf, st, &b, nxh, Y, &e_y);
+    int rc = bn_fwd_core(x, s_x, wide, M, C, gq, bq, &cf, st, &b, nxh, Y, &e_y);
     if (rc != ORC_OK) goto done;
     {
         int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
@@ -621,6 +654,32 @@ int orc_bn_bwd(const int8_t* dA, int32_t s_d, const int8_t* x, int32_t s_x,
 done:
     free(st); free(nxh); free(Y); free(F); free(B);
     return rc;
+}
+
+int orc_bn_bwd(const int8_t* dA, int32_t s_d, const int8_t* x, int32_t s_x,
+               int64_t M, int64_t C, const int8_t* gq, const int8_t* bq,
+               const int32_t* cfg_arr,
+               int8_t* dx, int32_t* dx_exp,
+               int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
+               double* dx_pre, int64_t* zero_sum_failures)
+{
+    int32_t* w = widen8(x, M * C);
+    int rc = bn_bwd_any(dA, s_d, w, s_x, 0, M, C, gq, bq, cfg_arr, dx, dx_exp, dgamma, dbeta, dgamma_exp,
+                        dbeta_exp, dx_pre, zero_sum_failures);
+    free(w);
+    return rc;
+}
+
+/* the backward of orc_bn_fwd32 (raw int32 conv sums as the input) */
+int orc_bn_bwd32(const int8_t* dA, int32_t s_d, const int32_t* x, int32_t s_x,
+                 int64_t M, int64_t C, const int8_t* gq, const int8_t* bq,
+                 const int32_t* cfg_arr,
+                 int8_t* dx, int32_t* dx_exp,
+                 int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
+                 double* dx_pre, int64_t* zero_sum_failures)
+{
+    return bn_bwd_any(dA, s_d, x, s_x, 1, M, C, gq, bq, cfg_arr, dx, dx_exp, dgamma, dbeta, dgamma_exp,
+                      dbeta_exp, dx_pre, zero_sum_failures);
 }
 
 /* ------------------------------------------------------------------------ */

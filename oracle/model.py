@@ -31,8 +31,11 @@ import numpy as np
 from . import oracle as O
 
 class OracleNet:
-    def __init__(self, wl, inputs, lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1):
+    def __init__(self, wl, inputs, lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1, bn_input="q8"):
         self.wl = wl
+        # L1BN reads a conv's SQ8 codes ("q8"), or its raw int32 sums ("raw",
+        # the literal dataflow of Sec. 3.2.2-3.2.3: BN on the MAC output)
+        self.bn_raw = bn_input == "raw"
         self.gq = gq                              # 1: Eq. 17 keeps Scale(G); 2: Eq. 18 drops it
         self.lr_shift = lr_shift
         self.k_W, self.k_U = k_W, k_U
@@ -79,8 +82,12 @@ class OracleNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd))
-                z = z.astype(np.int8)
+                if self.bn_raw and nd["bn"]:
+                    # |sum| < 2^31 (the reduction bound), so int32 holds it
+                    z, ze = O.conv_fwd_raw(a, L["w_q"], self._geom(a.shape, nd)).astype(np.int32), ae + self.w_exp
+                else:
+                    z, ze = O.conv_fwd(a, ae, L["w_q"], self.w_exp, self._geom(a.shape, nd))
+                    z = z.astype(np.int8)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
                     b = O.bn_fwd(z, ze, L["g_q"], L["b_q"], self._bn_cfg(nd))

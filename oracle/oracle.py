@@ -51,6 +51,8 @@ def lib():
             getattr(L, f).restype = None
         L.orc_bn_fwd.argtypes = [P, i32, i64, i64, P, P, P, P, P, P, P, P, P]
         L.orc_bn_bwd.argtypes = [P, i32, P, i32, i64, i64, P, P, P, P, P, P, P, P, P, P, P]
+        L.orc_bn_fwd32.argtypes = L.orc_bn_fwd.argtypes
+        L.orc_bn_bwd32.argtypes = L.orc_bn_bwd.argtypes
         L.orc_weight_update.argtypes = [P, i64, P, i32, C.c_int, C.c_int, C.c_int, C.c_int, P]
         L.orc_weight_quant.argtypes = [P, i64, C.c_int, C.c_int, P]
         L.orc_maxpool_fwd.argtypes = [P, i64, i64, i64, i64, i64, i64, i64, P]
@@ -250,10 +252,12 @@ def _bn_cfg(cfg):
 
 
 def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None):
-    """x: int8 [..., C] (NHWC).  Returns dict with A codes (int8), exponent,
-    n_mu, n_sigma (per channel), b (exponent of Q_xhat's scale) and the
-    per-element xhat codes."""
-    x = np.ascontiguousarray(x, dtype=np.int8)
+    """x: int8 codes [..., C] (NHWC), or int32 raw conv sums (the wide input
+    of the literal dataflow, Sec. 3.2.2-3.2.3).  Returns dict with A codes
+    (int8), exponent, n_mu, n_sigma (per channel), b (exponent of Q_xhat's
+    scale) and the per-element xhat codes."""
+    wide = np.asarray(x).dtype == np.int32
+    x = np.ascontiguousarray(x, dtype=np.int32 if wide else np.int8)
     Cc = x.shape[-1]
     M = x.size // Cc
     g = np.ascontiguousarray(gamma_q, dtype=np.int8)
@@ -264,7 +268,8 @@ def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None):
     n_sig = np.zeros(Cc, dtype=np.int32)
     bx = np.zeros(1, dtype=np.int32)
     nxh = np.zeros(x.shape, dtype=np.int16)
-    rc = lib().orc_bn_fwd(_p(x), int(x_exp), M, Cc, _p(g), _p(b), _p(_bn_cfg(cfg)),
+    f = lib().orc_bn_fwd32 if wide else lib().orc_bn_fwd
+    rc = f(_p(x), int(x_exp), M, Cc, _p(g), _p(b), _p(_bn_cfg(cfg)),
                           _p(out), _p(e), _p(n_mu), _p(n_sig), _p(bx), _p(nxh))
     _check(rc, "bn_fwd")
     return dict(y=out, y_exp=int(e[0]), n_mu=n_mu, n_sigma=n_sig, b=int(bx[0]), xhat=nxh)
@@ -274,8 +279,9 @@ def bn_bwd(dA, dA_exp, x, x_exp, gamma_q, beta_q, cfg=None, want_pre=False):
     """Backward of L1BN (+ReLU).  Returns dict with dx codes, exponent, raw
     dgamma/dbeta sums and their exponents; dx_pre (float64 value of dx before
     its quantizer) and the count of channels whose pre-quantizer dx does not
-    sum to exactly zero."""
-    x = np.ascontiguousarray(x, dtype=np.int8)
+    sum to exactly zero.  x int8 codes or int32 raw sums, as in bn_fwd."""
+    wide = np.asarray(x).dtype == np.int32
+    x = np.ascontiguousarray(x, dtype=np.int32 if wide else np.int8)
     dA = np.ascontiguousarray(dA, dtype=np.int8)
     Cc = x.shape[-1]
     M = x.size // Cc
@@ -289,7 +295,8 @@ def bn_bwd(dA, dA_exp, x, x_exp, gamma_q, beta_q, cfg=None, want_pre=False):
     dbe = np.zeros(1, dtype=np.int32)
     pre = np.zeros(x.shape, dtype=np.float64) if want_pre else None
     zf = np.zeros(1, dtype=np.int64)
-    rc = lib().orc_bn_bwd(_p(dA), int(dA_exp), _p(x), int(x_exp), M, Cc, _p(g), _p(b),
+    f = lib().orc_bn_bwd32 if wide else lib().orc_bn_bwd
+    rc = f(_p(dA), int(dA_exp), _p(x), int(x_exp), M, Cc, _p(g), _p(b),
                           _p(_bn_cfg(cfg)), _p(dx), _p(e), _p(dg), _p(db), _p(dge), _p(dbe),
                           _p(pre) if want_pre else None, _p(zf))
     _check(rc, "bn_bwd")

@@ -90,6 +90,12 @@ _SIGS = {
     "iseg_bn_fwd_noalloc_max_bytes": ([], _SZ),
     "iseg_bn_fwd_noalloc": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "iseg_bn_bwd_ws": ([_I64, _I64], _SZ),
+    "iseg_bn_i32_saved_bytes": ([_I64], _SZ),
+    "iseg_bn_fwd_i32_ws": ([_I64, _I64], _SZ),
+    "iseg_bn_fwd_i32": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P], C.c_int),
+    "iseg_bn_bwd_i32_ws": ([_I64, _I64], _SZ),
+    "iseg_bn_bwd_i32": ([_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P],
+                        C.c_int),
     "iseg_bn_bwd": ([_P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P],
                     C.c_int),
     "iseg_weight_update": ([_P, _I64, _P, _P, _I32, _I32, _I32, _I32, _P, _P, _P], C.c_int),
@@ -230,6 +236,20 @@ def iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, ws, stat
                            _ptr(y), _ptr(y_exp), _ptr(saved), *_ws_tuple(ws), _ptr(status),
                            _stream())
     _check(rc, "iseg_bn_fwd")
+
+
+def iseg_bn_fwd_i32(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, ws, status=None):
+    rc = lib().iseg_bn_fwd_i32(_ptr(x), _ptr(x_exp), M, Cc, _ptr(gamma_q), _ptr(beta_q), C.byref(cfg),
+                               _ptr(y), _ptr(y_exp), _ptr(saved), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_bn_fwd_i32")
+
+
+def iseg_bn_bwd_i32(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, dx_exp, dgamma, dbeta, dgamma_exp,
+                    dbeta_exp, ws, status=None):
+    rc = lib().iseg_bn_bwd_i32(_ptr(dy), _ptr(dy_exp), _ptr(x), M, Cc, _ptr(gamma_q), C.byref(cfg),
+                               _ptr(saved), _ptr(dx), _ptr(dx_exp), _ptr(dgamma), _ptr(dbeta),
+                               _ptr(dgamma_exp), _ptr(dbeta_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_bn_bwd_i32")
 
 
 def iseg_bn_fwd_noalloc(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, status=None):
@@ -607,9 +627,18 @@ def conv_bwd_weight(dy, dy_exp, x, x_exp, w_shape, stride=1, pad=0, dil=1, g_mod
 
 
 def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None, saved=None, status=None):
+    """L1BN forward of int8 codes, or of int32 raw conv sums (the wide input)."""
     Cc = x.shape[-1]
     M = x.numel() // Cc
     cfg = cfg or bn_cfg()
+    if x.dtype == torch.int32:
+        y = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+        e = _out_exp(x.device)
+        if saved is None:
+            saved = torch.empty(lib().iseg_bn_i32_saved_bytes(Cc), dtype=torch.uint8, device=x.device)
+        ws = workspace(x.device).get(lib().iseg_bn_fwd_i32_ws(M, Cc))
+        iseg_bn_fwd_i32(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, e, saved, ws, status)
+        return y, e, saved
     y = torch.empty_like(x)
     e = _out_exp(x.device)
     if saved is None:
@@ -625,7 +654,7 @@ def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None, dgb_out=None):
     Cc = x.shape[-1]
     M = x.numel() // Cc
     cfg = cfg or bn_cfg()
-    dx = torch.empty_like(x)
+    dx = torch.empty(x.shape, dtype=torch.int8, device=x.device)
     e = _out_exp(x.device)
     if dgb_out is None:
         dg = torch.empty(Cc, dtype=torch.int64, device=x.device)
@@ -633,6 +662,10 @@ def bn_bwd(dy, dy_exp, x, gamma_q, saved, cfg=None, status=None, dgb_out=None):
         dge, dbe = _out_exp(x.device), _out_exp(x.device)
     else:
         dg, db, dge, dbe = dgb_out
+    if x.dtype == torch.int32:
+        ws = workspace(x.device).get(lib().iseg_bn_bwd_i32_ws(M, Cc))
+        iseg_bn_bwd_i32(dy, dy_exp, x, M, Cc, gamma_q, cfg, saved, dx, e, dg, db, dge, dbe, ws, status)
+        return dx, e, dg, db, dge, dbe
     ws = workspace(x.device, bn=True).get(lib().iseg_bn_bwd_ws(M, Cc))
     for kid in (ISEG_KID_BN_BWD_APPLY, ISEG_KID_BN_BWD_STATS):
         _maybe_arm(kid, (M, Cc))

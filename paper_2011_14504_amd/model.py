@@ -31,9 +31,15 @@ import torch
 from . import iseg
 
 class IntNet:
-    def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1):
+    def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1,
+                 bn_input="q8"):
         if not (2 <= k_W <= 8 and 9 <= k_U <= 31 and gq in (1, 2)):
             raise ValueError("k_W must be in [2, 8], k_U in [9, 31], gq 1 or 2")
+        if bn_input not in ("q8", "raw"):
+            raise ValueError("bn_input is 'q8' (BN on the SQ8 conv output) or 'raw' (on the int32 sums)")
+        # where L1BN reads a conv's output: its SQ8 codes, or the raw int32
+        # sums (the literal dataflow, Sec. 3.2.2-3.2.3)
+        self.bn_raw = bn_input == "raw"
         self.wl = wl
         # weight-gradient quantizer: GQ1 (Eq. 17, the DeepLab setting) keeps
         # Scale(G); GQ2 (Eq. 18, the FCN setting) drops it
@@ -45,6 +51,8 @@ class IntNet:
         self.lr_shift = lr_shift
         self.seed = inputs["seed"]
         self.cfg = dict(iseg.BN_DEFAULT, **(bn_cfg or {}))
+        if self.bn_raw and self.cfg["k_E2"] < 15:
+            raise ValueError("L1BN on the raw sums supports the exact E2 (k_E2 >= 15) only")
         self._cfgs = {r: iseg.bn_cfg(**dict(self.cfg, relu=r)) for r in (0, 1)}
         self.k_A = self.cfg["k_A"]
         self.step_no = 0
@@ -145,7 +153,9 @@ class IntNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
+                raw = self.bn_raw and nd["bn"]
                 z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
+                                      out_mode=iseg.ISEG_OUT_RAW if raw else iseg.ISEG_OUT_Q8,
                                       status=self.status)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:

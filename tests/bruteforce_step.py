@@ -10,7 +10,8 @@ dataflow (Fig. 4 forward, Fig. 5 backward), not interpreted from a graph.
 Readings taken (the same ones the rest of the build takes, restated here so
 that a misreading in the oracle's composition shows up as a mismatch):
   * Scale(x) is the smallest power of two strictly above max|x| (Eq. 3-4);
-  * a conv output is SQ8 of the exact MAC result (Eq. 15 before BN); with BN,
+  * a conv output is SQ8 of the exact MAC result (Eq. 15 before BN), or with
+    bn_input="raw" the exact MAC result itself when BN follows; with BN,
     A = SQ_kA(ReLU?(L1BN(Z))) (Eq. 12-15); without BN, A = SQ_kA(ReLU?(Z)),
     whose backward passes the error where Z > 0;
   * a residual add is SQ_kA(ReLU(a + b)); its backward passes the error where
@@ -233,8 +234,10 @@ class Net:
     """Parameters of a network: per conv layer, the float weights turned
     into masters by Eq. 7, W_q by Eq. 8, and gamma = 1, beta = 0 masters."""
 
-    def __init__(self, wl, inputs, cfg, k_W=8, k_U=24, lr_shift=10, gq=1):
+    def __init__(self, wl, inputs, cfg, k_W=8, k_U=24, lr_shift=10, gq=1, bn_input="q8"):
         self.cfg, self.k_W, self.k_U, self.lr, self.gq = cfg, k_W, k_U, Fr(1, 2 ** lr_shift), gq
+        # "raw": L1BN reads the exact MAC output instead of its SQ8 codes
+        self.bn_raw = bn_input == "raw"
         self.seed = inputs["seed"]
         self.L = {}
         convs = [nd for nd in wl["nodes"] if nd["kind"] == "conv"]
@@ -259,7 +262,11 @@ class Net:
         """Z = SQ8(conv(A, W_q)) (Eq. 15 on the MAC output) and A' of the
         node: with BN, Q_A(ReLU?(L1BN(Z))); without, Q_A(ReLU?(Z))."""
         nd = self.L[name]["nd"]
-        z, z_exp = SQ(conv(a, self.w_q(name), nd["stride"], nd["pad"], nd["dil"]), 8)
+        acc = conv(a, self.w_q(name), nd["stride"], nd["pad"], nd["dil"])
+        if self.bn_raw and nd["bn"]:
+            z, z_exp = acc, None          # the MAC output itself (exponent not compared)
+        else:
+            z, z_exp = SQ(acc, 8)
         cfg = dict(self.cfg, relu=int(nd["relu"]))
         if nd["bn"]:
             g, b = self.gamma_beta(name)

@@ -154,3 +154,21 @@ def test_aspp_head_full_batch_8():
 
 def test_deeplabv3_r50_512px_batch_2():
     _run_both(synth.scaled(synth.DEEPLABV3_R50, 2))
+
+
+# L1BN on the raw int32 conv sums (the literal dataflow, bn_input="raw")
+def test_single_conv_bn_on_raw_sums_two_steps():
+    _run_both(synth.SINGLE_CONV, steps=2, bn_input="raw")
+
+
+def test_resnet50_conv2x_bn_on_raw_sums_two_steps():
+    _run_both(synth.scaled(synth.RESNET50_CONV2X, 2), steps=2, bn_input="raw")
+
+
+def test_deeplabv3_r50_bn_on_raw_sums_ragged_96x80():
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 96, 80), bn_input="raw")
+
+
+def test_resnet50_conv2x_w4a4_bn_on_raw_sums():
+    _run_both(synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28), steps=2, k_W=4, bn_cfg={"k_A": 4},
+              bn_input="raw")

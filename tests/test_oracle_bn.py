@@ -169,3 +169,72 @@ def test_l1bn_range_preconditions(orc):
         orc.bn_fwd(x, 17, [64, 64], [0, 0], CFG)
     with pytest.raises(orc.OracleError):
         orc.bn_fwd(x, -41, [64, 64], [0, 0], CFG)
+
+
+# L1BN on the raw int32 sums of a convolution (the paper's literal dataflow:
+# BN consumes the MAC output before any requantization, Sec. 3.2.2-3.2.3)
+WIDE_CASES = [
+    dict(seed=31, M=6, C=3, x_exp=-14, mag=1 << 20, cfg={}),
+    dict(seed=32, M=5, C=2, x_exp=-20, mag=1 << 30, cfg=dict(relu=0)),
+    dict(seed=33, M=7, C=2, x_exp=0, mag=1 << 30, cfg=dict(eps_code=3)),
+    dict(seed=34, M=4, C=3, x_exp=-40, mag=1 << 12, cfg=dict(k_E2=8)),
+    dict(seed=35, M=8, C=2, x_exp=-9, mag=3000, cfg=dict(relu=0, k_E2=8)),
+]
+
+
+def _wide_case(case):
+    rng = synth.rng(case["seed"])
+    m = case["mag"]
+    x = rng.integers(-m, m + 1, size=(case["M"], case["C"])).astype(np.int32)
+    x[0, 0] = m if case["seed"] % 2 else -m
+    gq = synth.int_codes(case["seed"] + 1, (case["C"],))
+    bq = synth.int_codes(case["seed"] + 2, (case["C"],))
+    return x, gq, bq
+
+
+@pytest.mark.parametrize("case", WIDE_CASES, ids=lambda c: f"seed{c['seed']}")
+def test_l1bn_int32_input_vs_bruteforce(orc, case):
+    cfg = dict(CFG, **case["cfg"])
+    x, gq, bq = _wide_case(case)
+    gam = [Fr(int(v)) * Fr(2) ** (2 - cfg["k_gamma"]) for v in gq]
+    bet = [Fr(int(v)) * Fr(2) ** (2 - cfg["k_beta"]) for v in bq]
+    r = orc.bn_fwd(x, case["x_exp"], gq, bq, cfg)
+    ref = bf.l1bn_forward(_cols(x, case["x_exp"]), gam, bet, cfg)
+    assert [Fr(int(v)) * Fr(2) ** (2 - cfg["k_mu"]) for v in r["n_mu"]] == ref["mu_q"]
+    assert [Fr(int(v)) * Fr(2) ** (2 - cfg["k_sigma"]) for v in r["n_sigma"]] == ref["sigma_q"]
+    assert _cols(r["xhat"], r["b"] - (cfg["k_xhat"] - 1)) == ref["xhat_q"]
+    assert _cols(r["y"], r["y_exp"]) == ref["A"]
+    dA = synth.int_codes(case["seed"] + 50, x.shape)
+    rb = orc.bn_bwd(dA, -20, x, case["x_exp"], gq, bq, cfg)
+    refb = bf.l1bn_backward(_cols(x, case["x_exp"]), _cols(dA, -20), gam, bet, cfg)
+    assert [Fr(int(v)) * Fr(2) ** rb["dbeta_exp"] for v in rb["dbeta"]] == refb["dbeta"]
+    assert [Fr(int(v)) * Fr(2) ** rb["dgamma_exp"] for v in rb["dgamma"]] == refb["dgamma"]
+    assert _cols(rb["dx"], rb["dx_exp"]) == refb["E1"]
+    assert rb["zero_sum_failures"] == 0
+
+
+def test_l1bn_int32_input_equals_int8_path_on_8bit_codes(orc):
+    """Codes that fit 8 bits give the same result through either input type."""
+    x = synth.int_codes(41, (300, 8))
+    gq = synth.int_codes(42, (8,))
+    bq = synth.int_codes(43, (8,))
+    dA = synth.int_codes(44, x.shape)
+    a = orc.bn_fwd(x, -7, gq, bq, CFG)
+    b = orc.bn_fwd(x.astype(np.int32), -7, gq, bq, CFG)
+    for k in ("y", "n_mu", "n_sigma", "xhat"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["y_exp"] == b["y_exp"] and a["b"] == b["b"]
+    ra = orc.bn_bwd(dA, -20, x, -7, gq, bq, CFG)
+    rb = orc.bn_bwd(dA, -20, x.astype(np.int32), -7, gq, bq, CFG)
+    for k in ("dx", "dgamma", "dbeta"):
+        assert np.array_equal(ra[k], rb[k]), k
+    assert ra["dx_exp"] == rb["dx_exp"]
+
+
+def test_l1bn_int32_input_range(orc):
+    x = synth.int_codes(91, (4, 2)).astype(np.int32) * 1000
+    orc.bn_fwd(x, 0, [64, 64], [0, 0], CFG)
+    with pytest.raises(orc.OracleError):
+        orc.bn_fwd(x, 1, [64, 64], [0, 0], CFG)
+    with pytest.raises(orc.OracleError):
+        orc.bn_fwd(x, -41, [64, 64], [0, 0], CFG)

@@ -90,13 +90,14 @@ TINY_STAGE = dict(id=3, name="tiny-stage-8ch-7x6", N=1, H=7, W=6, C=8, input_gra
                   nodes=synth.res_stage("s", "input", 8, 4, 16, 2, stride=2)[0])
 
 
-@pytest.mark.parametrize("variant", ["bn", "bn-w4a4-e2-8", "no-bn-gq2"])
+@pytest.mark.parametrize("variant", ["bn", "bn-w4a4-e2-8", "no-bn-gq2", "bn-raw", "bn-raw-w4a4"])
 def test_residual_stage_two_steps_match_bruteforce(variant):
     """Two bottlenecks (the first strided, with a projection shortcut; the
     second with the identity) on a 1x7x6x8 input with the input gradient:
     every tensor of two training steps against the brute force.  Variants:
     the 8-bit DeepLab setting; W4A4 with E2 at 8 bits (Table 1); the network
-    without BN and Eq. 18's gradient quantizer."""
+    without BN and Eq. 18's gradient quantizer; L1BN on the raw MAC sums (the
+    literal dataflow), at 8 and 4 bits."""
     from oracle.model import OracleNet
     wl = TINY_STAGE
     kw = {}
@@ -105,11 +106,15 @@ def test_residual_stage_two_steps_match_bruteforce(variant):
     if variant == "no-bn-gq2":
         wl = synth.without_bn(wl)
         kw = dict(gq=2)
+    if variant == "bn-raw":
+        kw = dict(bn_input="raw")
+    if variant == "bn-raw-w4a4":
+        kw = dict(k_W=4, k_U=16, bn_cfg={"k_A": 4}, bn_input="raw")
     inp = synth.workload_inputs(wl)
     # random gamma / beta would need another draw; the update moves them off 1 / 0
     onet = OracleNet(wl, inp, **kw)
     bnet = B.Net(wl, inp, dict(onet.cfg), k_W=kw.get("k_W", 8), k_U=kw.get("k_U", 24),
-                 gq=kw.get("gq", 1))
+                 gq=kw.get("gq", 1), bn_input=kw.get("bn_input", "q8"))
     for s in range(2):
         orec = onet.step()
         brec = B.stage_step(bnet, inp["x"], inp["x_exp"], inp["dy"], inp["dy_exp"], "s", 2)
@@ -164,3 +169,42 @@ def test_max_exact_scale_deviation_single_conv():
     for r in report:
         print("  ", r)
     assert len(report) >= 4
+
+
+def test_bn_on_raw_sums_against_the_requantized_reading():
+    """How far L1BN on the raw MAC sums (the literal dataflow) moves the codes
+    from the default reading (BN on the SQ8 conv output), one step of
+    workload 1 and of a ResNet-50 stage at 28x28: the share of activation
+    codes A that differ after each BN, and of the input-error codes.  The
+    counts are printed (recorded with the readings of the paper)."""
+    from oracle.model import OracleNet
+    rows = []
+    for wl in (synth.SINGLE_CONV, synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28)):
+        inp = synth.workload_inputs(wl)
+        ra = OracleNet(wl, inp).step()
+        rb = OracleNet(wl, inp, bn_input="raw").step()
+        for nd in wl["nodes"]:
+            if nd["kind"] != "conv" or not nd["bn"]:
+                continue
+            a, b = ra[nd["name"]], rb[nd["name"]]
+            va = a["a_out"].astype(np.float64) * 2.0 ** a["a_out_exp"]
+            vb = b["a_out"].astype(np.float64) * 2.0 ** b["a_out_exp"]
+            step = 2.0 ** max(a["a_out_exp"], b["a_out_exp"])
+            rows.append((wl["name"][:14], nd["name"], va.size, int((va != vb).sum()),
+                         float(np.abs(va - vb).max() / step), a["a_out_exp"] - b["a_out_exp"]))
+        ea, eb = ra["input"]["e_out"], rb["input"]["e_out"]
+        rows.append((wl["name"][:14], "input error", ea.size,
+                     int((ea.astype(np.int64) * 2.0 ** ra["input"]["e_out_exp"]
+                          != eb.astype(np.int64) * 2.0 ** rb["input"]["e_out_exp"]).sum()), None, None))
+    print("\n[BN on raw sums vs on SQ8 codes] (workload, tensor, elements, values differing, "
+          "max |diff| in steps, exponent difference):")
+    for r in rows:
+        print("  ", r)
+    # a BN whose conv reads the (shared) input differs only through the
+    # rounding of that conv's output: a minority of codes, by at most two
+    # steps; deeper layers also inherit the differences of their inputs
+    first = {("single-conv3x3", "conv"), ("resnet50-conv2", "conv2_x.0.proj"),
+             ("resnet50-conv2", "conv2_x.0.conv1")}
+    for r in rows:
+        if (r[0], r[1]) in first:
+            assert r[3] < 0.5 * r[2] and r[4] <= 2.0, r
