@@ -6,8 +6,11 @@ update) of DeepLabv3-ResNet50 at output stride 16 on a batch of 8 synthetic
 Prints ONE JSON line.  `value` is int8 conv throughput: valid-tap MACs x 2 of
 the forward, backward-data and backward-weight convolutions per step, divided
 by the whole step's wall time (inputs already in HBM); images/s is in
-`config`.  `roofline` reports one kernel timed in place by HIP events that the
-library records around each of its launches inside the timed steps;
+`config`, with the conv throughput over conv time (every conv entry point of
+a few extra steps timed by its own events).  `roofline` reports the step's
+largest kernel by time, the L1BN backward statistics pass, over every one of
+its launches in the timed steps: HIP events that the library records around
+each launch on its stream, algorithmic bytes of each launch's layer;
 `cpu_baseline` is the CPU oracle timed on a bounded sample.
 """
 import argparse
@@ -33,10 +36,11 @@ HBM_PEAK_GBS = 8000.0
 # region's kernels are built from when the counters were taken: a figure whose
 # sources have changed since is reported as null.
 TRAFFIC = {
-    "conv_fwd:aspp.b1": dict(bytes=145803700, src="a993945ca8da308fa45b836fd522f0d654acba28b7da6cd811e00de81046be1e",
-                             profile="profiles/deeplabv3_r50_512_n8_step_kernel_stats.md"),
+    "bn_bwd_stats:*": dict(bytes=23370953, src="46ffa8b258bcef0cbe63941e8d8efafe39011ce25909c9ceb8f5347ae7e96b1a",
+                           profile="profiles/deeplabv3_r50_512_n8_l1bn_hbm_traffic.md"),
 }
-TRAFFIC_SRC = {"conv_fwd": ("conv.hip", "quant.hip", "iseg_common.h")}
+TRAFFIC_SRC = {"conv_fwd": ("conv.hip", "quant.hip", "iseg_common.h"),
+               "bn_bwd_stats": ("bn.hip", "iseg_common.h")}
 
 WORKLOAD_IDS = {"deeplabv3": 5, "aspp": 4, "resnet-stage": 3, "vgg16": 2, "single-conv": 1}
 
@@ -68,29 +72,40 @@ def workload_ops(wl, N=None):
     return total, detail
 
 
+BN_FAMILIES = {
+    # kernel family: (kernel id, algorithmic bytes per element of the layer's
+    # output tensor).  stats1/stats2 read x; apply reads x, writes y; the
+    # backward statistics read x and dy; the backward apply reads x, dy, writes dx
+    "bn_fwd_stats1": ("ISEG_KID_BN_FWD_STATS1", 1), "bn_fwd_stats2": ("ISEG_KID_BN_FWD_STATS2", 1),
+    "bn_fwd_apply": ("ISEG_KID_BN_FWD_APPLY", 2), "bn_bwd_stats": ("ISEG_KID_BN_BWD_STATS", 2),
+    "bn_bwd_apply": ("ISEG_KID_BN_BWD_APPLY", 3),
+}
+CONV_FAMILIES = {"conv_fwd": "ISEG_KID_CONV_FWD", "conv_bwd_data": "ISEG_KID_CONV_BWD_DATA",
+                 "conv_wgrad": "ISEG_KID_CONV_WGRAD"}
+
+
 def timed_kernel_info(name, wl, detail):
-    """Kernel family, layer key and algorithmic work per launch of the kernel
-    timed in place.  Conv kernels: ops of one launch of the named layer.
-    L1BN kernels: bytes of the layer's output tensor moved by the pass."""
+    """Kernel family, layer key (None: every launch of the family) and the
+    algorithmic work of a launch as a function of its layer key.  Conv
+    families: valid-tap ops of the launch's layer.  L1BN families: bytes of
+    the layer's tensor moved by the pass."""
     from paper_2011_14504_amd import iseg, synth
     kind, _, layer = name.partition(":")
-    d = next(x for x in detail if x["name"] == layer)
     shapes = synth.node_shapes(wl)
-    conv_kids = {"conv_fwd": iseg.ISEG_KID_CONV_FWD, "conv_bwd_data": iseg.ISEG_KID_CONV_BWD_DATA,
-                 "conv_wgrad": iseg.ISEG_KID_CONV_WGRAD}
-    if kind in conv_kids:
-        return dict(kid=conv_kids[kind], key=d["key"], bound="mfma", work=2 * d["macs"],
-                    name=f"{kind} of {layer} (N,H,W,C,K,R,stride,pad,dil = {d['key']})")
-    N, P, Q, K = shapes[layer]
-    M = N * P * Q
-    # bytes per element: stats1/stats2 read x; apply reads x, writes y; the
-    # backward statistics read x and dy; the backward apply reads x, dy, writes dx
-    bn = {"bn_fwd_stats1": (iseg.ISEG_KID_BN_FWD_STATS1, 1), "bn_fwd_stats2": (iseg.ISEG_KID_BN_FWD_STATS2, 1),
-          "bn_fwd_apply": (iseg.ISEG_KID_BN_FWD_APPLY, 2), "bn_bwd_stats": (iseg.ISEG_KID_BN_BWD_STATS, 2),
-          "bn_bwd_apply": (iseg.ISEG_KID_BN_BWD_APPLY, 3)}
-    kid, bpe = bn[kind]
-    return dict(kid=kid, key=(M, K), bound="hbm", work=bpe * M * K,
-                name=f"{kind} of the L1BN after {layer} (M = {M}, C = {K})")
+    if kind in CONV_FAMILIES:
+        by_key = {d["key"]: 2 * d["macs"] for d in detail}
+        key = None if layer == "*" else next(d for d in detail if d["name"] == layer)["key"]
+        what = "every launch" if key is None else f"{layer} (N,H,W,C,K,R,stride,pad,dil = {key})"
+        return dict(kid=getattr(iseg, CONV_FAMILIES[kind]), key=key, bound="mfma",
+                    work=lambda k: by_key[tuple(k)], name=f"{kind} entry point, {what}")
+    kid, bpe = BN_FAMILIES[kind]
+    if layer == "*":
+        key, what = None, "every L1BN layer of the step"
+    else:
+        N, P, Q, K = shapes[layer]
+        key, what = (N * P * Q, K), f"the L1BN after {layer} (M = {N * P * Q}, C = {K})"
+    return dict(kid=getattr(iseg, kid), key=key, bound="hbm", work=lambda k: bpe * k[0] * k[1],
+                name=f"{kind} kernel, {what}, {bpe} B per element")
 
 
 def src_digest(files):
@@ -140,7 +155,13 @@ def cpu_baseline(wl, sample_hw, widths=None):
     dt = time.perf_counter() - t0
     ops, _ = workload_ops(small)
     full_ops, _ = workload_ops(wl)
-    return dict(value=ops / dt / 1e12, unit="TOPS", cores=O.num_threads(), kind="oracle",
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu = next(l.split(":", 1)[1].strip() for l in fh if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    return dict(value=ops / dt / 1e12, unit="TOPS", cores=O.num_threads(), cpu=cpu, kind="oracle",
                 sample=f"one full training step (fwd, loss, bwd, update) of the same network on one "
                        f"{sample_hw}x{sample_hw} image: {dt:.2f} s for {ops / 1e9:.1f} G conv ops",
                 images_per_s_est=(ops / full_ops) * wl["N"] / dt)
@@ -166,9 +187,14 @@ def main():
                     help="L1BN on the SQ8 conv output (q8) or on the raw int32 sums (the literal dataflow)")
     ap.add_argument("--copy-kernel-mib", type=int, default=0,
                     help="only run the plain copy kernel used to calibrate the HBM byte counters")
-    ap.add_argument("--timed-kernel", default="conv_fwd:aspp.b1",
-                    help="<family>:<layer>, family one of conv_fwd, conv_bwd_data, conv_wgrad, "
-                         "bn_fwd_stats1, bn_fwd_stats2, bn_fwd_apply, bn_bwd_stats, bn_bwd_apply")
+    ap.add_argument("--timed-kernel", default="bn_bwd_stats:*",
+                    help="<family>:<layer or *>, family one of conv_fwd, conv_bwd_data, conv_wgrad, "
+                         "bn_fwd_stats1, bn_fwd_stats2, bn_fwd_apply, bn_bwd_stats, bn_bwd_apply; * times "
+                         "every launch of the family in the timed steps (the default: the L1BN backward "
+                         "statistics pass, the step's largest kernel by time)")
+    ap.add_argument("--conv-steps", type=int, default=2,
+                    help="extra steps after the timed ones whose conv entry points are timed one by one "
+                         "(conv TOPS over conv time)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
@@ -192,8 +218,8 @@ def main():
     net = IntNet(wl, inp, "cuda:0", bn_input=args.bn_input, **widths)
     ops, detail = workload_ops(wl)
     tk = args.timed_kernel
-    if args.workload != "deeplabv3" and tk == "conv_fwd:aspp.b1":
-        tk = "conv_fwd:" + detail[min(1, len(detail) - 1)]["name"]
+    if args.no_bn and tk.startswith("bn_"):
+        tk = "conv_fwd:*"
     kinfo = timed_kernel_info(tk, wl, detail)
     prof = iseg.KernelTimer(kinfo["kid"], layer_match=kinfo["key"])
 
@@ -210,9 +236,12 @@ def main():
     ms = dt / args.steps * 1e3
     value = ops / (dt / args.steps) / 1e12
 
-    k_ms = prof.mean_ms()
-    per_launch = kinfo["work"]
-    launches = prof.count()
+    # the timed kernel: algorithmic work of each launch over its measured time
+    runs = prof.launches()
+    prof.close()
+    launches = len(runs)
+    k_ms = sum(t for _, _, t in runs) / launches if launches else None
+    per_launch = sum(kinfo["work"](k) for _, k, _ in runs) / launches if launches else None
     if kinfo["bound"] == "mfma":
         ach = per_launch / (k_ms * 1e-3) / 1e12 if k_ms else None
         roof = dict(kernel=kinfo["name"], bound="mfma", achieved=ach, peak=INT8_PEAK_TOPS,
@@ -228,12 +257,28 @@ def main():
     roof["traffic_unit"] = "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)"
     if tk in TRAFFIC:
         roof["profile"] = TRAFFIC[tk]["profile"]
-    prof.close()
+
+    # conv throughput over conv time: every conv entry point of a few more
+    # steps timed by its own events (the weight gradients overlap other work
+    # on their stream, so this sums kernel time, not wall time)
+    conv_tops = None
+    if args.conv_steps > 0:
+        ct = iseg.KernelTimer([iseg.ISEG_KID_CONV_FWD, iseg.ISEG_KID_CONV_BWD_DATA, iseg.ISEG_KID_CONV_WGRAD])
+        iseg.set_kernel_timer(ct)
+        for _ in range(args.conv_steps):
+            net.step()
+        torch.cuda.synchronize()
+        iseg.set_kernel_timer(None)
+        conv_ms = sum(t for _, _, t in ct.launches())
+        ct.close()
+        conv_tops = ops * args.conv_steps / (conv_ms * 1e-3) / 1e12 if conv_ms else None
     cfg = dict(workload=wl["name"], batch=N, image=f"{wl['H']}x{wl['W']}",
                convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
                pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
                bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u), gq=args.gq,
-               l1bn=not args.no_bn, bn_input=args.bn_input)
+               l1bn=not args.no_bn, bn_input=args.bn_input,
+               conv_tops_over_conv_time=conv_tops,
+               conv_pct_int8_peak_over_conv_time=(100.0 * conv_tops / INT8_PEAK_TOPS) if conv_tops else None)
     status = net.read_status()
     if net.loss is not None:
         cfg["loss"] = float(net.loss.item())

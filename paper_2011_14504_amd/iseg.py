@@ -420,35 +420,42 @@ def _hiprt():
 
 
 class KernelTimer:
-    """Times every launch of one kernel family whose layer key matches, with a
-    pair of HIP events that the library records around the launch on its own
-    stream (iseg_profile_arm)."""
+    """Times every launch of one or more kernel families whose layer key
+    matches, with a pair of HIP events that the library records around the
+    launch on its own stream (iseg_profile_arm).  Families timed together
+    must be separate entry-point calls (one arming is held at a time)."""
 
     def __init__(self, kernel_id, layer_match=None):
-        self.kid = kernel_id
+        self.kids = set(kernel_id) if isinstance(kernel_id, (tuple, list, set)) else {kernel_id}
+        self.kid = next(iter(self.kids))
         self.match = tuple(layer_match) if layer_match is not None else None
-        self.pairs = []
+        self.pairs = []                  # (start, stop, kernel id, layer key)
 
     def wants(self, kid, key):
-        return kid == self.kid and (self.match is None or tuple(key) == self.match)
+        return kid in self.kids and (self.match is None or tuple(key) == self.match)
 
-    def arm(self):
+    def arm(self, kid=None, key=None):
         h = _hiprt()
         a, b = C.c_void_p(), C.c_void_p()
         if h.hipEventCreate(C.byref(a)) or h.hipEventCreate(C.byref(b)):
             raise IsegError("hipEventCreate failed")
-        self.pairs.append((a, b))
-        iseg_profile_arm(self.kid, a, b)
+        kid = self.kid if kid is None else kid
+        self.pairs.append((a, b, kid, tuple(key) if key is not None else None))
+        iseg_profile_arm(kid, a, b)
 
-    def times_ms(self):
+    def launches(self):
+        """[(kernel id, layer key, ms)] of every timed launch."""
         h = _hiprt()
         out = []
-        for a, b in self.pairs:
+        for a, b, kid, key in self.pairs:
             h.hipEventSynchronize(b)
             ms = C.c_float()
             if h.hipEventElapsedTime(C.byref(ms), a, b) == 0:
-                out.append(ms.value)
+                out.append((kid, key, ms.value))
         return out
+
+    def times_ms(self):
+        return [t for _, _, t in self.launches()]
 
     def mean_ms(self):
         t = self.times_ms()
@@ -459,7 +466,7 @@ class KernelTimer:
 
     def close(self):
         h = _hiprt()
-        for a, b in self.pairs:
+        for a, b, _, _ in self.pairs:
             h.hipEventDestroy(a)
             h.hipEventDestroy(b)
         self.pairs = []
@@ -478,7 +485,7 @@ def set_kernel_timer(timer):
 
 def _maybe_arm(kid, key):
     if _TIMER is not None and _TIMER.wants(kid, key):
-        _TIMER.arm()
+        _TIMER.arm(kid, key)
 
 
 # --------------------------------------------------------------------------
