@@ -300,6 +300,33 @@ int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t* x,
                 int64_t* dgamma, int64_t* dbeta, int32_t* dgamma_exp, int32_t* dbeta_exp,
                 void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
+/* Inference with frozen statistics.  The paper claims fixed-point inference
+ * (Sec. 1, 6) but gives no rule for running statistics; the reading taken:
+ * a layer's inference state is the state one calibration forward in training
+ * mode (iseg_bn_fwd) saved -- per channel n_mu and the denominator, and the
+ * exponents of its input Z, of Q_xhat (b) and of Q_A -- and later inputs use
+ * it unchanged: every quantizer keeps the calibration's step and clips
+ * (Eq. 2) what falls outside its range.  Under that state L1BN + ReLU + Q_A
+ * (Eq. 12-15) of an int8 code depends on (channel, code) only: the saved
+ * per-(channel, code) A table.
+ *
+ * iseg_bn_infer -- A = table[c][z] for int8 codes z [M, C] whose exponent
+ * must be the calibration's (ISEG_DEV_RANGE otherwise); *a_exp = the
+ * calibration's A exponent.  C % 4 == 0, z and a_out 4-byte aligned.
+ *
+ * iseg_conv_bn_infer -- a conv layer with L1BN + ReLU? + Q_A in inference:
+ * the conv's exact int32 sums (in the workspace), then one pass that puts
+ * them on the calibration's Z grid (clamp(floor(sum 2^(e_x + e_w - e_Z) +
+ * 1/2)) to 8 bits) and applies the A table.  saved: from iseg_bn_fwd on
+ * that conv's output of a calibration batch; the geometry as for
+ * iseg_conv_fwd; a_out [N, P, Q, K] int8. */
+int iseg_bn_infer(const int8_t* z, const int32_t* z_exp, int64_t M, int64_t C, const void* saved,
+                  int8_t* a_out, int32_t* a_exp, int32_t* dev_status, hipStream_t stream);
+size_t iseg_conv_bn_infer_ws(const iseg_conv_geom* g);
+int iseg_conv_bn_infer(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
+                       const iseg_conv_geom* g, const void* saved, int8_t* a_out, int32_t* a_exp,
+                       void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
 /* iseg_bn_fwd_i32 / iseg_bn_bwd_i32 -- the same L1BN forward and backward
  * (Eq. 12-15, 16) on the raw int32 sums of a convolution (iseg_conv_fwd with
  * ISEG_OUT_RAW), the literal dataflow of Sec. 3.2.2-3.2.3: BN takes the MAC

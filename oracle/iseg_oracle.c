@@ -683,6 +683,63 @@ int orc_bn_bwd32(const int8_t* dA, int32_t s_d, const int32_t* x, int32_t s_x,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Inference with frozen statistics (the paper claims fixed-point inference  */
+/* but gives no rule for running statistics).  Reading: a layer's inference  */
+/* state is captured from one calibration forward in training mode -- per   */
+/* channel n_mu and n_sigma, and the exponents of the conv output Z, of     */
+/* Q_xhat's scale (b) and of Q_A -- and every later input uses that state:  */
+/* no batch statistic and no data-dependent scale, so each quantizer is a   */
+/* fixed-step UQ that clips what falls outside its range.                   */
+/* ------------------------------------------------------------------------ */
+
+/* codes = clamp(floor(a 2^(a_exp - out_exp) + 1/2), k bits): a quantizer with
+ * a fixed step 2^out_exp (half-up rounding, Eq. 2's clip) */
+int orc_requant_fixed(const int64_t* in, int64_t n, int32_t in_exp, int32_t out_exp, int k, int64_t* codes)
+{
+    if (k < 2 || k > 31 || n < 0 || in_exp - out_exp > 60 || out_exp - in_exp > 100) return ORC_ERR_ARG;
+    int sh = in_exp - out_exp;
+    for (int64_t i = 0; i < n; i++)
+        codes[i] = (int64_t)clamp_code(round_half_up((i128)in[i], sh, 1), k);
+    return ORC_OK;
+}
+
+/* L1BN + ReLU? + Q_A of int8 codes z (exponent s_x) with the frozen state:
+ * mu_q = n_mu 2^(2-k_mu), sigma_q = n_sigma 2^(2-k_sigma) per channel, x-hat
+ * on the fixed grid 2^(b+1-k_xhat), A on the fixed grid 2^a_exp:
+ *   xhat_q = UQ-like clamp(floor((x - mu_q)/(sigma_q + eps) 2^(k_xhat-1-b) + 1/2))
+ *   y      = gamma_q xhat_q + beta_q, ReLU if cfg->relu
+ *   A      = clamp(floor(y 2^-a_exp + 1/2), k_A bits)                        */
+int orc_bn_infer(const int8_t* x, int32_t s_x, int64_t M, int64_t C,
+                 const int8_t* gq, const int8_t* bq, const int32_t* cfg_arr,
+                 const int32_t* n_mu, const int32_t* n_sigma, int32_t b, int32_t a_exp, int8_t* out)
+{
+    orc_bn_cfg cf = { cfg_arr[0], cfg_arr[1], cfg_arr[2], cfg_arr[3], cfg_arr[4],
+                      cfg_arr[5], cfg_arr[6], cfg_arr[7], cfg_arr[8], cfg_arr[9] };
+    if (s_x < -40 || s_x > 16 || M < 0) return ORC_ERR_RANGE;
+    int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
+    int e_xh = b - (cf.k_xhat - 1);
+    int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
+    int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
+    for (int64_t c = 0; c < C; c++) {
+        orc_bn_chan st;
+        st.n_mu = n_mu[c];
+        st.n_sigma = n_sigma[c];
+        st.den = n_sigma[c] + cf.eps_code;
+        if (st.den < 1) st.den = 1;
+        st.g = s_x < e_mu ? s_x : e_mu;
+        for (int64_t i = 0; i < M; i++) {
+            int64_t j = i * C + c;
+            i128 D = bn_D(x[j], s_x, &st, e_mu);
+            i128 n = clamp_code(round_half_up(D, st.g - e_sig + (cf.k_xhat - 1) - b, st.den), cf.k_xhat);
+            i128 Y = (i128)gq[c] * n * p2(e_g + e_xh - e_y) + (i128)bq[c] * p2(e_b - e_y);
+            if (cf.relu && Y < 0) Y = 0;
+            out[j] = (int8_t)clamp_code(round_half_up(Y, e_y - a_exp, 1), cf.k_A);
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Eq. 19 (Q_U) and Eq. 8 (Q_W): master update and re-quantized weights.     */
 /*   Delta W = UQ(G_q * lr, k_U)  with lr = 2^-lr_shift                       */
 /*   W_m    <- clamp(W_m - Delta W)          (master held at k_U bits)        */

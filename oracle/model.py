@@ -92,6 +92,7 @@ class OracleNet:
                 if nd["bn"]:
                     b = O.bn_fwd(z, ze, L["g_q"], L["b_q"], self._bn_cfg(nd))
                     y, ye = b["y"], b["y_exp"]
+                    r["bn_state"] = O.bn_state(b)
                 elif nd["relu"] or self.k_A < 8:
                     # without BN: A = Q_A(ReLU?(Z)) on the 8-bit conv output
                     y, ye = O.sum_requant([z], [ze], self.k_A, relu=nd["relu"])
@@ -227,6 +228,32 @@ class OracleNet:
                                                      2 - k_U, k_U, cf["k_gamma"])
                 L["b_m"], L["b_q"] = O.weight_update(L["b_m"], r["Gb"], r["Gb_exp"], self.lr_shift,
                                                      2 - k_U, k_U, cf["k_beta"])
+
+    def infer(self, calib, x, x_exp):
+        """Forward of a chain of conv + L1BN (+ReLU) layers and max pooling in
+        inference with the frozen state of a calibration forward `calib` (the
+        record forward() returned): each conv's sums go to the calibration's
+        Z grid (a fixed-step quantizer), then L1BN + ReLU + Q_A with the
+        calibration's statistics and steps.  Returns {node: (codes, exp)}."""
+        act = {"input": (x, x_exp)}
+        out = {}
+        for nd in self.wl["nodes"]:
+            a, ae = act[nd["src"][0]]
+            if nd["kind"] == "conv":
+                if not nd["bn"]:
+                    raise ValueError("inference covers conv layers with L1BN")
+                L, c = self.convs[nd["name"]], calib[nd["name"]]
+                sums = O.conv_fwd_raw(a, L["w_q"], self._geom(a.shape, nd))
+                z = O.requant_fixed(sums, ae + self.w_exp, c["z_exp"], 8)
+                y = O.bn_infer(z, c["z_exp"], L["g_q"], L["b_q"], c["bn_state"], self._bn_cfg(nd))
+                res = (y, c["bn_state"]["a_exp"])
+            elif nd["kind"] == "maxpool":
+                res = (O.maxpool_fwd(a, nd["k"], nd["stride"], nd["pad"]), ae)
+            else:
+                raise ValueError("inference covers chains of conv layers and max pooling")
+            out[nd["name"]] = res
+            act[nd["name"]] = res
+        return out
 
     def step(self):
         rec = self.forward()

@@ -52,6 +52,8 @@ def lib():
         L.orc_bn_fwd.argtypes = [P, i32, i64, i64, P, P, P, P, P, P, P, P, P]
         L.orc_bn_bwd.argtypes = [P, i32, P, i32, i64, i64, P, P, P, P, P, P, P, P, P, P, P]
         L.orc_bn_fwd32.argtypes = L.orc_bn_fwd.argtypes
+        L.orc_requant_fixed.argtypes = [P, i64, i32, i32, C.c_int, P]
+        L.orc_bn_infer.argtypes = [P, i32, i64, i64, P, P, P, P, P, i32, i32, P]
         L.orc_bn_bwd32.argtypes = L.orc_bn_bwd.argtypes
         L.orc_weight_update.argtypes = [P, i64, P, i32, C.c_int, C.c_int, C.c_int, C.c_int, P]
         L.orc_weight_quant.argtypes = [P, i64, C.c_int, C.c_int, P]
@@ -302,6 +304,40 @@ def bn_bwd(dA, dA_exp, x, x_exp, gamma_q, beta_q, cfg=None, want_pre=False):
     _check(rc, "bn_bwd")
     return dict(dx=dx, dx_exp=int(e[0]), dgamma=dg, dbeta=db, dgamma_exp=int(dge[0]),
                 dbeta_exp=int(dbe[0]), dx_pre=pre, zero_sum_failures=int(zf[0]))
+
+
+# --------------------------------------------------------------------------
+# inference with frozen statistics and scales
+# --------------------------------------------------------------------------
+def requant_fixed(acc, acc_exp, out_exp, k=8):
+    """Codes of the integer tensor acc 2^acc_exp on the fixed grid 2^out_exp:
+    clamp(floor(acc 2^(acc_exp - out_exp) + 1/2)) to k bits."""
+    a = np.ascontiguousarray(acc, dtype=np.int64)
+    codes = np.zeros(a.shape, dtype=np.int64)
+    rc = lib().orc_requant_fixed(_p(a), a.size, int(acc_exp), int(out_exp), int(k), _p(codes))
+    _check(rc, "requant_fixed")
+    return codes
+
+
+def bn_state(fwd):
+    """The inference state of a layer from a calibration forward's result
+    (bn_fwd): per-channel n_mu, n_sigma, Q_xhat's exponent b and Q_A's exponent."""
+    return dict(n_mu=np.asarray(fwd["n_mu"], np.int32), n_sigma=np.asarray(fwd["n_sigma"], np.int32),
+                b=int(fwd["b"]), a_exp=int(fwd["y_exp"]))
+
+
+def bn_infer(x, x_exp, gamma_q, beta_q, state, cfg=None):
+    """L1BN (+ReLU) + Q_A of int8 codes with the frozen state of bn_state()."""
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    Cc = x.shape[-1]
+    M = x.size // Cc
+    out = np.zeros(x.shape, dtype=np.int8)
+    rc = lib().orc_bn_infer(_p(x), int(x_exp), M, Cc, _p(np.ascontiguousarray(gamma_q, dtype=np.int8)),
+                            _p(np.ascontiguousarray(beta_q, dtype=np.int8)), _p(_bn_cfg(cfg)),
+                            _p(state["n_mu"]), _p(state["n_sigma"]), int(state["b"]), int(state["a_exp"]),
+                            _p(out))
+    _check(rc, "bn_infer")
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -1569,3 +1569,104 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
                       w, sv, cf.relu);
     return launch_ok();
 }
+
+// ---------------------------------------------------------------------------
+// Inference with the frozen state of a calibration forward (the state that
+// iseg_bn_fwd saved): the per-(channel, code) A table, built from that pass's
+// n_mu, denominator and the fixed steps of Q_xhat and Q_A, is applied to new
+// inputs.  A wide input (the raw int32 sums of a conv) first goes to the
+// calibration's Z grid with a fixed-step quantizer (half-up, clipped to 8
+// bits): the requant, L1BN, ReLU and Q_A of a layer in one pass.
+// ---------------------------------------------------------------------------
+namespace {
+template <bool WIDE>
+__global__ __launch_bounds__(256) void k_bn_infer(const void* __restrict__ in, const int32_t* in_exp,
+                                                  const int32_t* w_exp, int64_t n4, int32_t C, Saved sv,
+                                                  int8_t* __restrict__ out, int32_t* out_exp,
+                                                  int32_t* dev_status)
+{
+    const int32_t ez = sv.hdr[3];
+    const int32_t es = *in_exp + (WIDE ? *w_exp : 0);
+    const int r = ez - es;                 // Z = sums 2^-r on the calibration's grid
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        *out_exp = sv.hdr[2];
+        if (!WIDE && r != 0) set_status(dev_status, ISEG_DEV_RANGE);   // codes on another grid
+    }
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+        const int c0 = (int)((i * 4) % C);
+        int z[4];
+        if (WIDE) {
+            const int4 v = ((const int4*)in)[i];
+            const int s[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                int64_t q;
+                if (r > 0) q = ((int64_t)s[j] + ((int64_t)1 << (r - 1))) >> r;
+                else if (r >= -32) q = (int64_t)s[j] * ((int64_t)1 << -r);
+                else q = s[j] > 0 ? 128 : (s[j] < 0 ? -128 : 0);
+                z[j] = (int)clamp_k(q, 8);
+            }
+        } else {
+            const uint32_t v = ((const uint32_t*)in)[i];
+#pragma unroll
+            for (int j = 0; j < 4; j++) z[j] = (int)(int8_t)(v >> (8 * j));
+        }
+        uint32_t o = 0;
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+            o |= (uint32_t)(uint8_t)sv.acode[(int64_t)(c0 + j) * 256 + z[j] + 128] << (8 * j);
+        ((uint32_t*)out)[i] = o;
+    }
+}
+}  // namespace
+
+extern "C" int iseg_bn_infer(const int8_t* z, const int32_t* z_exp, int64_t M, int64_t C, const void* saved,
+                             int8_t* a_out, int32_t* a_exp, int32_t* dev_status, hipStream_t stream)
+{
+    if (M < 1 || C < 4) return ISEG_ERR_SHAPE;
+    if (!shape_ok(M, C) || C % 4) return ISEG_ERR_UNSUPPORTED;
+    if (!z || !z_exp || !saved || !a_out || !a_exp) return ISEG_ERR_ARG;
+    if (((uintptr_t)z | (uintptr_t)a_out) & 3) return ISEG_ERR_UNSUPPORTED;
+    const Saved sv = saved_map((void*)saved, C);
+    const int64_t n4 = M * C / 4;
+    hipLaunchKernelGGL(k_bn_infer<false>, dim3(grid_for(n4, 256 * 4, 4096)), dim3(256), 0, stream, z, z_exp,
+                       z_exp, n4, (int32_t)C, sv, a_out, a_exp, dev_status);
+    return launch_ok();
+}
+
+extern "C" size_t iseg_conv_bn_infer_ws(const iseg_conv_geom* g)
+{
+    const size_t cw = iseg_conv_fwd_ws(g, ISEG_OUT_RAW);
+    if (!cw || !g) return 0;
+    const int64_t P = (g->H + 2 * g->pad_h - g->dil_h * (g->R - 1) - 1) / g->stride_h + 1;
+    const int64_t Q = (g->W + 2 * g->pad_w - g->dil_w * (g->S - 1) - 1) / g->stride_w + 1;
+    return align256((size_t)(g->N * P * Q * g->K) * 4) + cw;
+}
+
+extern "C" int iseg_conv_bn_infer(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
+                                  const iseg_conv_geom* g, const void* saved, int8_t* a_out, int32_t* a_exp,
+                                  void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    if (!g || !saved || !a_out || !a_exp || !x_exp || !w_exp) return ISEG_ERR_ARG;
+    const size_t need = iseg_conv_bn_infer_ws(g);
+    if (!need) return ISEG_ERR_SHAPE;
+    if (!ws || ws_bytes < need) return ISEG_ERR_WORKSPACE;
+    const int64_t P = (g->H + 2 * g->pad_h - g->dil_h * (g->R - 1) - 1) / g->stride_h + 1;
+    const int64_t Q = (g->W + 2 * g->pad_w - g->dil_w * (g->S - 1) - 1) / g->stride_w + 1;
+    const int64_t M = g->N * P * Q, C = g->K;
+    if (M < 1 || C < 4) return ISEG_ERR_SHAPE;
+    if (!shape_ok(M, C) || C % 4 || ((uintptr_t)a_out & 3)) return ISEG_ERR_UNSUPPORTED;
+    int32_t* sums = (int32_t*)ws;
+    char* cws = (char*)ws + align256((size_t)(M * C) * 4);
+    // the sums' own exponent slot: the conv writes x_exp + w_exp there; the pass reads both inputs' exponents
+    int32_t* sexp = (int32_t*)a_exp;
+    int rc = iseg_conv_fwd(x, x_exp, w, w_exp, g, ISEG_OUT_RAW, sums, sexp, cws, ws_bytes - (cws - (char*)ws),
+                           dev_status, stream);
+    if (rc) return rc;
+    const Saved sv = saved_map((void*)saved, C);
+    const int64_t n4 = M * C / 4;
+    hipLaunchKernelGGL(k_bn_infer<true>, dim3(grid_for(n4, 256 * 4, 4096)), dim3(256), 0, stream, sums, x_exp,
+                       w_exp, n4, (int32_t)C, sv, a_out, a_exp, dev_status);
+    return launch_ok();
+}

@@ -90,6 +90,9 @@ _SIGS = {
     "iseg_bn_fwd_noalloc_max_bytes": ([], _SZ),
     "iseg_bn_fwd_noalloc": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "iseg_bn_bwd_ws": ([_I64, _I64], _SZ),
+    "iseg_bn_infer": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P], C.c_int),
+    "iseg_conv_bn_infer_ws": ([_P], _SZ),
+    "iseg_conv_bn_infer": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P], C.c_int),
     "iseg_bn_i32_saved_bytes": ([_I64], _SZ),
     "iseg_bn_fwd_i32_ws": ([_I64, _I64], _SZ),
     "iseg_bn_fwd_i32": ([_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _SZ, _P, _P], C.c_int),
@@ -236,6 +239,40 @@ def iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, ws, stat
                            _ptr(y), _ptr(y_exp), _ptr(saved), *_ws_tuple(ws), _ptr(status),
                            _stream())
     _check(rc, "iseg_bn_fwd")
+
+
+def iseg_bn_infer(z, z_exp, M, Cc, saved, a, a_exp, status=None):
+    rc = lib().iseg_bn_infer(_ptr(z), _ptr(z_exp), M, Cc, _ptr(saved), _ptr(a), _ptr(a_exp), _ptr(status),
+                             _stream())
+    _check(rc, "iseg_bn_infer")
+
+
+def iseg_conv_bn_infer(x, x_exp, w, w_exp, geom, saved, a, a_exp, ws, status=None):
+    rc = lib().iseg_conv_bn_infer(_ptr(x), _ptr(x_exp), _ptr(w), _ptr(w_exp), C.byref(geom), _ptr(saved),
+                                  _ptr(a), _ptr(a_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_conv_bn_infer")
+
+
+def bn_infer(z, z_exp, saved, status=None):
+    """A codes of int8 codes z through a calibration forward's frozen state."""
+    Cc = z.shape[-1]
+    a = torch.empty_like(z)
+    e = _out_exp(z.device)
+    iseg_bn_infer(z, z_exp, z.numel() // Cc, Cc, saved, a, e, status)
+    return a, e
+
+
+def conv_bn_infer(x, x_exp, w, w_exp, saved, stride=1, pad=0, dil=1, status=None):
+    """Conv + L1BN + ReLU? + Q_A of one layer with a calibration's frozen state."""
+    N, H, W, Cc = x.shape
+    K, R, S, _ = w.shape
+    g = geom(N, H, W, Cc, K, R, S, stride, pad, dil)
+    P, Q = conv_out_hw(g)
+    a = torch.empty((N, P, Q, K), dtype=torch.int8, device=x.device)
+    e = _out_exp(x.device)
+    ws = workspace(x.device).get(lib().iseg_conv_bn_infer_ws(C.byref(g)))
+    iseg_conv_bn_infer(x, x_exp, w, w_exp, g, saved, a, e, ws, status)
+    return a, e
 
 
 def iseg_bn_fwd_i32(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, y_exp, saved, ws, status=None):

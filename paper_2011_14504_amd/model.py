@@ -309,6 +309,29 @@ class IntNet:
                 L = self.convs[nd["name"]]
                 r.update(Gg=L["Gg"], Gb=L["Gb"], Gg_exp=L["Gg_exp"], Gb_exp=L["Gb_exp"])
 
+    def infer(self, calib, x, x_exp):
+        """Forward of a chain of conv + L1BN (+ReLU) layers and max pooling in
+        inference with the frozen state that a calibration forward `calib`
+        (the record forward() returned) saved: one iseg_conv_bn_infer per conv
+        layer.  Returns {node: (codes, exp)}."""
+        act = {"input": (x, x_exp)}
+        out = {}
+        for nd in self.wl["nodes"]:
+            a, ae = act[nd["src"][0]]
+            if nd["kind"] == "conv":
+                if not nd["bn"] or self.bn_raw:
+                    raise ValueError("inference covers conv layers with L1BN on their 8-bit outputs")
+                L = self.convs[nd["name"]]
+                res = iseg.conv_bn_infer(a, ae, L["w_q"], self.w_exp, calib[nd["name"]]["saved"], nd["stride"],
+                                         nd["pad"], nd["dil"], status=self.status)
+            elif nd["kind"] == "maxpool":
+                res = iseg.maxpool_fwd(a, ae, nd["k"], nd["stride"], nd["pad"])
+            else:
+                raise ValueError("inference covers chains of conv layers and max pooling")
+            out[nd["name"]] = res
+            act[nd["name"]] = res
+        return out
+
     def read_status(self):
         """The sticky status word after the work enqueued so far (waits for
         the current stream): 0, or ISEG_DEV_* bits."""

@@ -676,3 +676,49 @@ def test_bn_int32_input_exponent_range(dev):
 def torch_zeros_status(dev):
     import torch
     return torch.zeros(1, dtype=torch.int32, device=dev)
+
+
+# Inference with a calibration forward's frozen state: the A table on new
+# codes, and conv + L1BN + ReLU + Q_A of one layer in one pass over the sums
+@pytest.mark.parametrize("case", [dict(M=4099, C=64, x_exp=-9, cfg={}), dict(M=777, C=20, x_exp=-14, cfg=dict(relu=0)),
+                                  dict(M=2048, C=2048, x_exp=-6, cfg=dict(eps_code=1))], ids=str)
+def test_bn_infer_frozen_state(orc, dev, case):
+    from paper_2011_14504_amd import iseg
+    cfg = dict(orc.BN_DEFAULT, **case["cfg"])
+    cal = synth.int_codes(1100, (case["M"], case["C"]))
+    new = (synth.int_codes(1101, (case["M"], case["C"])).astype(np.int64) * 3 // 4 + 20).astype(np.int8)
+    gq = synth.int_codes(1102, (case["C"],))
+    bq = synth.int_codes(1103, (case["C"],))
+    c = iseg.bn_cfg(**cfg)
+    y, ye, saved = iseg.bn_fwd(T(cal, dev), E(case["x_exp"], dev), T(gq, dev), T(bq, dev), c)
+    st = orc.bn_state(orc.bn_fwd(cal, case["x_exp"], gq, bq, cfg))
+    for x, label in ((cal, "calibration batch"), (new, "new batch")):
+        a, ae = iseg.bn_infer(T(x, dev), E(case["x_exp"], dev), saved)
+        ref = orc.bn_infer(x, case["x_exp"], gq, bq, st, cfg)
+        assert np.array_equal(H(a), ref) and ev(ae) == st["a_exp"], label
+    assert np.array_equal(H(iseg.bn_infer(T(cal, dev), E(case["x_exp"], dev), saved)[0]), H(y))
+
+
+@pytest.mark.parametrize("s", [(8, 32, 32, 64, 64, 3, 1, 1, 1), (8, 32, 32, 256, 64, 1, 1, 0, 1),
+                               (2, 32, 32, 2048, 256, 3, 1, 6, 6), (1, 9, 7, 24, 36, 3, 2, 1, 1)], ids=str)
+def test_conv_bn_infer(orc, dev, s):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    g = _geom(s)
+    cfg = dict(orc.BN_DEFAULT)
+    w = synth.int_codes(1200, (K, R, R, Cc)) // 4
+    gq = synth.int_codes(1201, (K,))
+    bq = synth.int_codes(1202, (K,))
+    cal = synth.int_codes(1203, (N, Hh, W, Cc))
+    new = synth.int_codes(1204, (N, Hh, W, Cc))
+    # calibration: the training forward of the layer (conv -> SQ8 -> L1BN -> ReLU -> Q_A)
+    z, ze = iseg.conv_fwd(T(cal, dev), E(-7, dev), T(w, dev), E(-7, dev), st, pad, d)
+    y, ye, saved = iseg.bn_fwd(z, ze, T(gq, dev), T(bq, dev), iseg.bn_cfg(**cfg))
+    zc, zce = orc.conv_fwd(cal, -7, w, -7, g)
+    state = orc.bn_state(orc.bn_fwd(zc.astype(np.int8), zce, gq, bq, cfg))
+    assert ev(ze) == zce
+    for x in (cal, new):
+        a, ae = iseg.conv_bn_infer(T(x, dev), E(-7, dev), T(w, dev), E(-7, dev), saved, st, pad, d)
+        zz = orc.requant_fixed(orc.conv_fwd_raw(x, w, g), -14, zce, 8)
+        ref = orc.bn_infer(zz, zce, gq, bq, state, cfg)
+        assert np.array_equal(H(a), ref) and ev(ae) == state["a_exp"]

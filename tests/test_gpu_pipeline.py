@@ -172,3 +172,26 @@ def test_deeplabv3_r50_bn_on_raw_sums_ragged_96x80():
 def test_resnet50_conv2x_w4a4_bn_on_raw_sums():
     _run_both(synth.scaled(synth.RESNET50_CONV2X, 1, 28, 28), steps=2, k_W=4, bn_cfg={"k_A": 4},
               bn_input="raw")
+
+
+def test_vgg16_blocks12_inference_with_frozen_state():
+    """Inference of the VGG16 encoder slice (conv + L1BN + ReLU layers and max
+    pooling) on a new batch with the frozen state of a calibration forward."""
+    import torch
+    from oracle.model import OracleNet
+    from paper_2011_14504_amd.model import IntNet
+    wl = synth.scaled(synth.VGG16_BLOCKS12, 2, 112, 96)
+    inp = synth.workload_inputs(wl)
+    gnet = IntNet(wl, inp, "cuda:0")
+    onet = OracleNet(wl, inp)
+    gcal, ocal = gnet.forward(), onet.forward()
+    new = synth.int_codes(1300, inp["x"].shape)
+    for x in (inp["x"], new):
+        gi = gnet.infer(gcal, torch.from_numpy(x).to("cuda:0"), gnet.x_exp)
+        oi = onet.infer(ocal, x, inp["x_exp"])
+        torch.cuda.synchronize()
+        assert gnet.read_status() == 0
+        for nd in wl["nodes"]:
+            (gc, ge), (oc, oe) = gi[nd["name"]], oi[nd["name"]]
+            _cmp(gc, oc, nd["name"])
+            assert _ev(ge) == oe, nd["name"]

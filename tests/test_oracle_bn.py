@@ -238,3 +238,49 @@ def test_l1bn_int32_input_range(orc):
         orc.bn_fwd(x, 1, [64, 64], [0, 0], CFG)
     with pytest.raises(orc.OracleError):
         orc.bn_fwd(x, -41, [64, 64], [0, 0], CFG)
+
+
+# Inference with the frozen state of a calibration forward (the paper gives
+# no running-statistics rule; every quantizer keeps the calibration's step)
+def test_requant_fixed_hand_examples(orc):
+    a = np.array([1000, 1004, 1003, -1004, -1005, 5000, -5000, 0], np.int64)
+    # step 2^3: 125, 125.5 -> 126 (half up), 125.375 -> 125, -125.5 -> -125, -125.625 -> -126, clip
+    assert orc.requant_fixed(a, 0, 3).tolist() == [125, 126, 125, -125, -126, 127, -127, 0]
+    assert orc.requant_fixed(np.array([3, -3], np.int64), -2, -4).tolist() == [12, -12]    # exact left shift
+
+
+def test_bn_infer_on_the_calibration_batch_equals_training_forward(orc):
+    for seed, cfg in ((61, {}), (62, dict(relu=0)), (63, dict(eps_code=2, k_xhat=12))):
+        cfg = dict(CFG, **cfg)
+        x = synth.int_codes(seed, (700, 12))
+        gq = synth.int_codes(seed + 1, (12,))
+        bq = synth.int_codes(seed + 2, (12,))
+        fwd = orc.bn_fwd(x, -9, gq, bq, cfg)
+        assert np.array_equal(orc.bn_infer(x, -9, gq, bq, orc.bn_state(fwd), cfg), fwd["y"])
+
+
+def test_bn_infer_vs_bruteforce(orc):
+    """A new batch through the frozen state, against Eq. 12-15 in Fractions
+    with the calibration's mu_q, sigma_q and the fixed steps of Q_xhat, Q_A."""
+    cfg = dict(CFG)
+    cal = synth.int_codes(71, (9, 3))
+    new = synth.int_codes(72, (7, 3)) // 2 + 40          # shifted: some codes clip
+    gq = synth.int_codes(73, (3,))
+    bq = synth.int_codes(74, (3,))
+    st = orc.bn_state(orc.bn_fwd(cal, -5, gq, bq, cfg))
+    got = orc.bn_infer(new, -5, gq, bq, st, cfg)
+    lsb = Fr(2) ** (2 - cfg["k_sigma"])
+    for c in range(3):
+        mu = Fr(int(st["n_mu"][c])) * Fr(2) ** (2 - cfg["k_mu"])
+        den = max(Fr(int(st["n_sigma"][c])) * lsb + cfg["eps_code"] * lsb, lsb)
+        gam = Fr(int(gq[c])) * Fr(2) ** (2 - cfg["k_gamma"])
+        bet = Fr(int(bq[c])) * Fr(2) ** (2 - cfg["k_beta"])
+        Sx = Fr(2) ** st["b"]
+        for i in range(new.shape[0]):
+            xv = Fr(int(new[i, c])) * Fr(2) ** -5
+            xq = Sx * bf.UQ((xv - mu) / den / Sx, cfg["k_xhat"])          # fixed step, clipped
+            y = gam * xq + bet
+            y = max(y, Fr(0)) if cfg["relu"] else y
+            SA = Fr(2) ** (st["a_exp"] + cfg["k_A"] - 1)
+            want = SA * bf.UQ(y / SA, cfg["k_A"])
+            assert Fr(int(got[i, c])) * Fr(2) ** st["a_exp"] == want, (i, c)

@@ -208,3 +208,18 @@ def test_bn_on_raw_sums_against_the_requantized_reading():
     for r in rows:
         if (r[0], r[1]) in first:
             assert r[3] < 0.5 * r[2] and r[4] <= 2.0, r
+
+
+def test_inference_on_the_calibration_batch_equals_training_forward():
+    """With the frozen state of a calibration forward, inference on the same
+    batch gives the training forward's activations at every layer (the
+    fixed-step quantizers then coincide with the data-dependent ones)."""
+    from oracle.model import OracleNet
+    wl = synth.scaled(synth.VGG16_BLOCKS12, 1, 40, 36)
+    inp = synth.workload_inputs(wl)
+    net = OracleNet(wl, inp)
+    rec = net.forward()
+    inf = net.infer(rec, inp["x"], inp["x_exp"])
+    for nd in wl["nodes"]:
+        codes, e = inf[nd["name"]]
+        assert np.array_equal(codes, rec[nd["name"]]["a_out"]) and e == rec[nd["name"]]["a_out_exp"], nd["name"]
