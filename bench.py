@@ -42,7 +42,7 @@ TRAFFIC = {
 TRAFFIC_SRC = {"conv_fwd": ("conv.hip", "quant.hip", "iseg_common.h"),
                "bn_bwd_stats": ("bn.hip", "iseg_common.h")}
 
-WORKLOAD_IDS = {"deeplabv3": 5, "aspp": 4, "resnet-stage": 3, "vgg16": 2, "single-conv": 1}
+WORKLOAD_IDS = {"deeplabv3": 5, "aspp": 4, "resnet-stage": 3, "vgg16": 2, "single-conv": 1, "fcn8s": 6}
 
 
 def conv_valid_macs(N, H, W, C, K, R, st, pad, dil):
@@ -64,11 +64,17 @@ def workload_ops(wl, N=None):
     total, detail = 0, []
     for nd in synth.conv_nodes(wl):
         n, H, W, cin = shapes[nd["src"][0]]
-        macs = conv_valid_macs(n, H, W, cin, nd["cout"], nd["R"], nd["stride"], nd["pad"], nd["dil"])
+        if nd.get("transposed"):
+            # the conv it is the adjoint of (input of the node's output shape),
+            # the geometry all three of its passes are launched on
+            _, Ho, Wo, cout = shapes[nd["name"]]
+            key = (n, Ho, Wo, cout, cin, nd["R"], nd["stride"], nd["pad"], nd["dil"])
+        else:
+            key = (n, H, W, cin, nd["cout"], nd["R"], nd["stride"], nd["pad"], nd["dil"])
+        macs = conv_valid_macs(*key)
         passes = 3 if (nd["src"][0] != "input" or wl["input_grad"]) else 2
         total += 2 * macs * passes
-        detail.append(dict(name=nd["name"], key=(n, H, W, cin, nd["cout"], nd["R"], nd["stride"],
-                                                 nd["pad"], nd["dil"]), macs=macs))
+        detail.append(dict(name=nd["name"], key=key, macs=macs))
     return total, detail
 
 
@@ -180,8 +186,9 @@ def main():
     ap.add_argument("--k-a", type=int, default=8, help="activation code width k_A")
     ap.add_argument("--k-e2", type=int, default=16, help="BN error width k_E2 (8 or 16)")
     ap.add_argument("--k-u", type=int, default=24, help="master / update width k_U")
-    ap.add_argument("--gq", type=int, default=1, choices=(1, 2),
-                    help="weight-gradient quantizer: 1 keeps Scale(G) (Eq. 17), 2 drops it (Eq. 18)")
+    ap.add_argument("--gq", type=int, default=None, choices=(1, 2),
+                    help="weight-gradient quantizer: 1 keeps Scale(G) (Eq. 17), 2 drops it (Eq. 18); "
+                         "default: the workload's (2 for FCN8s, 1 otherwise)")
     ap.add_argument("--no-bn", action="store_true", help="the same network without L1BN")
     ap.add_argument("--bn-input", default="q8", choices=("q8", "raw"),
                     help="L1BN on the SQ8 conv output (q8) or on the raw int32 sums (the literal dataflow)")
@@ -213,19 +220,27 @@ def main():
     if args.no_bn:
         wl = synth.without_bn(wl)
     N = wl["N"]
+    if args.gq is None:
+        args.gq = wl.get("gq", 1)
     inp = synth.workload_inputs(wl)
     widths = dict(k_W=args.k_w, k_U=args.k_u, bn_cfg={"k_A": args.k_a, "k_E2": args.k_e2}, gq=args.gq)
     net = IntNet(wl, inp, "cuda:0", bn_input=args.bn_input, **widths)
     ops, detail = workload_ops(wl)
     tk = args.timed_kernel
-    if args.no_bn and tk.startswith("bn_"):
+    if tk.startswith("bn_") and (args.no_bn or not any(nd.get("bn") for nd in synth.conv_nodes(wl))):
         tk = "conv_fwd:*"
     kinfo = timed_kernel_info(tk, wl, detail)
     prof = iseg.KernelTimer(kinfo["kid"], layer_match=kinfo["key"])
 
-    for _ in range(args.warmup):
+    # the last warm-up step runs with the timer installed, so the events the
+    # timed steps record are created before the timed region
+    for i in range(args.warmup):
+        if i == args.warmup - 1:
+            iseg.set_kernel_timer(prof)
         net.step()
     torch.cuda.synchronize()
+    iseg.set_kernel_timer(None)
+    prof.reset()
     iseg.set_kernel_timer(prof)
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -276,7 +291,7 @@ def main():
                convs=len(detail), conv_ops_per_step=ops, images_per_s=N / (dt / args.steps),
                pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
                bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u), gq=args.gq,
-               l1bn=not args.no_bn, bn_input=args.bn_input,
+               l1bn=any(nd.get("bn") for nd in synth.conv_nodes(wl)), bn_input=args.bn_input,
                conv_tops_over_conv_time=conv_tops,
                conv_pct_int8_peak_over_conv_time=(100.0 * conv_tops / INT8_PEAK_TOPS) if conv_tops else None)
     status = net.read_status()

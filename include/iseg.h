@@ -157,7 +157,12 @@ int iseg_requant(const void* in, int32_t in_dtype, int64_t n, const int32_t* in_
  * q st_w - pad_w + s dil_w, c] * w[k,r,s,c]; then Q_A = SQ(., 8) (Eq. 15) for
  * ISEG_OUT_Q8 (y int8, y_exp = x_exp + w_exp + r) or the raw sums for
  * ISEG_OUT_RAW (y int32, y_exp = x_exp + w_exp).  The weights are W_q of
- * Eq. 8.  Requires C*R*S <= 131071 so the exact sums fit int32. */
+ * Eq. 8.  ISEG_OUT_RAW requires C*R*S <= 131071 so the exact sums fit
+ * int32.  ISEG_OUT_Q8 also takes longer reductions, cut over C into at most 8
+ * chunks of a multiple of 16 channels with at most 131071 products each (a
+ * 7x7 conv over up to 21376 channels): every chunk's exact int32 sums are
+ * kept in the workspace and the quantizer adds them in int64, so the codes
+ * are those of the exact total; ISEG_ERR_UNSUPPORTED beyond that. */
 size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode);
 int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
                   const iseg_conv_geom* g, int32_t out_mode, void* y, int32_t* y_exp,
@@ -167,7 +172,9 @@ int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t* w, const 
  * dy[n,p,q,k] * w[k,r,s,c] over h = p st_h - pad_h + r dil_h, w = q st_w -
  * pad_w + s dil_w; then Q_E = SQ(., 8) (Eq. 16) for ISEG_OUT_Q8 (dx int8,
  * dx_exp = dy_exp + w_exp + r) or the raw int32 sums.  dy is [N,P,Q,K];
- * dx is [N,H,W,C].  Requires K*R*S <= 131071. */
+ * dx is [N,H,W,C].  ISEG_OUT_RAW requires K*R*S <= 131071; ISEG_OUT_Q8
+ * splits a longer reduction over K as iseg_conv_fwd splits one over C (FCN's
+ * fc6, 7x7 from 4096 channels, takes two chunks). */
 size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mode);
 int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
                        const iseg_conv_geom* g, int32_t out_mode, void* dx, int32_t* dx_exp,
@@ -179,7 +186,8 @@ int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w,
 enum iseg_wt_kind { ISEG_WT_NONE = 0, ISEG_WT_CRSK = 1, ISEG_WT_CRSK_FLIP = 2 };
 
 /* iseg_conv_bwd_data_wt_kind -- the layout iseg_conv_bwd_data builds in its
- * workspace for this geometry (ISEG_WT_NONE for an invalid geometry). */
+ * workspace for this geometry (ISEG_WT_NONE for an invalid geometry, and for
+ * a reduction split over K, whose chunks read w itself). */
 int32_t iseg_conv_bwd_data_wt_kind(const iseg_conv_geom* g);
 
 /* iseg_conv_bwd_data_t -- iseg_conv_bwd_data with the transposed weights
@@ -532,6 +540,19 @@ size_t iseg_softmax_ce_ws(int64_t N, int64_t h, int64_t w, int64_t K, int64_t H,
 int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, const uint8_t* labels,
                     int64_t N, int64_t h, int64_t w, int64_t K, int64_t H, int64_t W, int32_t bits,
                     double* loss, double* grad, int8_t* err, int32_t* err_exp,
+                    void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
+
+/* iseg_mse_onehot -- the MSE loss of the network output against one-hot
+ * labels (the FCN8s loss, Sec. 5.1): loss = mean over the N H W K elements of
+ * (y - t)^2 with t = [k == label] (float64, summed per block and the block
+ * partials in a fixed order), and E1 = SQ(2 (y - t) / (N H W K), bits) (Eq. 4
+ * / 16) decided exactly (err codes, *err_exp).  y [N, H, W, K] int8 with
+ * exponent *y_exp in [-60, 40] (ISEG_DEV_RANGE and a NaN loss outside);
+ * labels [N, H, W] uint8 in [0, K) (otherwise ISEG_DEV_RANGE); loss: one
+ * device double (may be NULL). */
+size_t iseg_mse_onehot_ws(int64_t n);
+int iseg_mse_onehot(const int8_t* y, const int32_t* y_exp, const uint8_t* labels, int64_t N, int64_t H,
+                    int64_t W, int64_t K, int32_t bits, double* loss, int8_t* err, int32_t* err_exp,
                     void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */

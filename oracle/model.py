@@ -67,6 +67,16 @@ class OracleNet:
         return dict(self.cfg, relu=int(nd["relu"]))
 
     @staticmethod
+    def _tgeom(a_shape, nd):
+        """Geometry of the conv a transposed-conv node is the adjoint of: its
+        input has the node's output shape, its output the node's input shape."""
+        N, h, w, cin = a_shape
+        H = (h - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+        W = (w - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+        return (N, H, W, nd["cout"], cin, nd["R"], nd["R"], nd["stride"], nd["stride"], nd["pad"],
+                nd["pad"], nd["dil"], nd["dil"])
+
+    @staticmethod
     def _geom(a_shape, nd):
         N, H, W, C = a_shape
         return (N, H, W, C, nd["cout"], nd["R"], nd["R"], nd["stride"], nd["stride"], nd["pad"],
@@ -82,7 +92,11 @@ class OracleNet:
             r = dict(kind=k, a_in=a, a_in_exp=ae)
             if k == "conv":
                 L = self.convs[name]
-                if self.bn_raw and nd["bn"]:
+                if nd.get("transposed"):
+                    # the adjoint of the conv whose input has this node's output shape
+                    z, ze = O.conv_bwd_data(a, ae, L["w_q"], self.w_exp, self._tgeom(a.shape, nd))
+                    z = z.astype(np.int8)
+                elif self.bn_raw and nd["bn"]:
                     # |sum| < 2^31 (the reduction bound), so int32 holds it
                     z, ze = O.conv_fwd_raw(a, L["w_q"], self._geom(a.shape, nd)).astype(np.int32), ae + self.w_exp
                 else:
@@ -131,6 +145,10 @@ class OracleNet:
         out = rec[self.wl["nodes"][-1]["name"]]
         if self.wl["loss"] == "given":
             return self.dy, self.dy_exp
+        if self.wl["loss"] == "mse":
+            loss, e, ee = O.mse_onehot(out["a_out"], out["a_out_exp"], self.labels)
+            self.loss = loss
+            return e.astype(np.int8), ee
         loss, grad = O.softmax_ce(out["a_out"], out["a_out_exp"], self.labels)
         e, ee = O.quantize_f64(grad, 8)
         self.loss, self.loss_grad = loss, grad
@@ -176,12 +194,25 @@ class OracleNet:
                     dz, dze = O.relu_mask_bwd(e, [r["z"]], [r["z_exp"]]), ee
                 else:
                     dz, dze = e, ee
-                geom = self._geom(r["a_in"].shape, nd)
-                G, Ge = O.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], geom, 8, self.gq == 1,
-                                          self.seed, 16 * L["l"], self.step_no)
+                if nd.get("transposed"):
+                    # the adjoint conv's weight gradient pairs this node's input
+                    # (the conv's output side) with dz (its input side); the
+                    # input error is that conv's forward of dz
+                    geom = self._tgeom(r["a_in"].shape, nd)
+                    G, Ge = O.conv_bwd_weight(r["a_in"], r["a_in_exp"], dz, dze, geom, 8, self.gq == 1,
+                                              self.seed, 16 * L["l"], self.step_no)
+                else:
+                    geom = self._geom(r["a_in"].shape, nd)
+                    G, Ge = O.conv_bwd_weight(dz, dze, r["a_in"], r["a_in_exp"], geom, 8, self.gq == 1,
+                                              self.seed, 16 * L["l"], self.step_no)
                 r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
                 grads.append((nd, r))
-                if need_in:
+                if need_in and nd.get("transposed"):
+                    ei, eie = O.conv_fwd(dz, dze, L["w_q"], self.w_exp, geom)
+                    ei = ei.astype(np.int8)
+                    r.update(e_in=ei, e_in_exp=eie)
+                    send(src, ei, eie)
+                elif need_in:
                     ei, eie = O.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, geom)
                     ei = ei.astype(np.int8)
                     r.update(e_in=ei, e_in_exp=eie)
@@ -193,7 +224,8 @@ class OracleNet:
                     r.update(e_in=ei, e_in_exp=eie)
                     send(src, ei, eie)
             elif k == "add":
-                d = O.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]])
+                d = (O.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]])
+                     if nd["relu"] else e)
                 r.update(e_in=d, e_in_exp=ee)
                 for s in nd["src"]:
                     if s != "input" or want_input:

@@ -530,6 +530,27 @@ def bilinear_matrix(n_in, n_out):
     return A
 
 
+def mse_onehot(y, y_exp, labels, k=8):
+    """MSE loss of the network output against one-hot labels (the FCN8s
+    loss): L = mean over the N H W K elements of (y - t)^2, t = [k ==
+    label], in float64; and E1 = SQ_k of its gradient 2 (y - t) / (N H W K)
+    (Eq. 4 / 16), decided exactly: with g = min(y_exp, 0) every y - t is an
+    integer V on the grid 2^g, and the gradient is V 2^(g+1) / (N H W K).
+    Returns (loss, codes, exponent)."""
+    y = np.asarray(y, dtype=np.int64)
+    N, H, W, K = y.shape
+    lab = np.asarray(labels, dtype=np.int64)
+    if lab.shape != (N, H, W) or lab.min(initial=0) < 0 or lab.max(initial=0) >= K:
+        raise OracleError("mse_onehot: labels must be [N, H, W] in [0, K)")
+    g = min(int(y_exp), 0)
+    t = (np.arange(K)[None, None, None, :] == lab[..., None]).astype(np.int64)
+    V = y * (1 << (int(y_exp) - g)) - t * (1 << (-g))
+    D = N * H * W * K
+    loss = float((V.astype(np.float64) ** 2).sum()) * 2.0 ** (2 * g) / D
+    codes, e = mean_requant(V, g + 1, D, k)
+    return loss, codes, e
+
+
 LOGIT_EXP_MIN, LOGIT_EXP_MAX = -1000, 0
 
 

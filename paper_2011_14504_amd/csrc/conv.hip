@@ -3809,7 +3809,7 @@ size_t conv_pmax_bytes(int64_t rows, int64_t cols, const HaloPlan& hp, int64_t N
     return align256((size_t)nb * 8);
 }
 
-extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
+static size_t conv_fwd_core_ws(const iseg_conv_geom* g, int32_t out_mode)
 {
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
@@ -3835,19 +3835,17 @@ extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
     return s;
 }
 
-extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
-                             const iseg_conv_geom* g, int32_t out_mode, void* y, int32_t* y_exp,
-                             void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+static int conv_fwd_core(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
+                         const iseg_conv_geom* g, int32_t out_mode, void* y, int32_t* y_exp,
+                         void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
 {
-    ProfScope prof_scope(ISEG_KID_CONV_FWD, stream);
-    conv_plan_set("none");
     (void)dev_status;
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
     if (out_mode != ISEG_OUT_Q8 && out_mode != ISEG_OUT_RAW) return ISEG_ERR_ARG;
     if (!x_exp || !w_exp || !y_exp || (g->N > 0 && (!x || !w || !y))) return ISEG_ERR_ARG;
     if (g->C * g->R * g->S > kMaxKred) return ISEG_ERR_UNSUPPORTED;
-    if (!ws || ws_bytes < iseg_conv_fwd_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
+    if (!ws || ws_bytes < conv_fwd_core_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
     // ws: [max][per-block max partials][output staging][padded operands]
     unsigned long long* maxp = (unsigned long long*)ws;
     const int64_t Cp = padded_c(g->C);
@@ -3974,10 +3972,230 @@ extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t
                                 0, 0, 0, ISEG_I8, y, y_exp, nullptr, stream, pmax, nblk);
 }
 
-extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mode)
+// ---------------------------------------------------------------------------
+// Backward-data of a strided conv with few output-gradient channels (K < 64,
+// or K = 64 at stride products >= 4), e.g. the bilinear upsampling layers of
+// FCN (transposed convs of stride 2 and 8 over the class scores), by phase
+// decomposition.  Input pixel h receives only the taps r = ((h + pad) mod
+// stride) + t * stride, from dy row p = floor((h + pad) / stride) - t, so all
+// pixels of one phase ((h + pad) mod stride_h, (w + pad) mod stride_w) share
+// their taps.  A block takes a 16 x 16 tile of one phase's pixels, stages the
+// dy rows they read in LDS (K padded to Kp, a multiple of 8, with zeros) and
+// sums with v_dot4 over 4 dy channels at a time against the weights
+// repacked as [R][S][Cp][Kp] (one address for the whole block: scalar
+// loads); eight output channels per thread, blockIdx.y picks the group.
+// Only the taps that meet real dy entries are computed, where the implicit
+// GEMM multiplies stride_h * stride_w times as many products, most of them
+// with the zeros between the dy rows.
+// ---------------------------------------------------------------------------
+constexpr int kTcTile = 16, kTcCB = 8, kTcMaxTaps = 4, kTcMaxKp = 64;
+
+struct TconvArgs {
+    const int8_t* dy;          // [N][P][Q][K]
+    const int8_t* wp;          // [R][S][Cp][Kp]
+    int32_t* out;              // EPI_RAW: [N][H][W][C] int32
+    int8_t* out8;              // EPI_Q8: [N][H][W][C] codes
+    uint64_t* pmax;            // one max partial per block
+    int64_t npmax;
+    const int32_t* exp_a;
+    const int32_t* exp_b;
+    int32_t* out_exp;
+    int32_t N, H, W, C, K, Kp, Cp, P, Q, R, S, sh, sw, ph, pw;
+    int32_t tiles_h, tiles_w;  // 16 x 16 tiles over ceil(H / sh) x ceil(W / sw) phase pixels
+};
+
+struct TconvPlan {
+    bool ok = false;
+    int32_t Kp = 0, Cp = 0, tiles_h = 0, tiles_w = 0;
+    int64_t gx = 0, gy = 0;
+};
+
+static TconvPlan tconv_plan(const iseg_conv_geom* g)
+{
+    TconvPlan t;
+    if (g->dil_h != 1 || g->dil_w != 1 || (g->stride_h == 1 && g->stride_w == 1)) return t;
+    if (g->K > 64 || (g->K == 64 && g->stride_h * g->stride_w < 4)) return t;
+    if (ceil_div64(g->R, g->stride_h) > kTcMaxTaps || ceil_div64(g->S, g->stride_w) > kTcMaxTaps) return t;
+    t.Kp = (int32_t)((g->K + 7) & ~(int64_t)7);
+    t.Cp = (int32_t)((g->C + kTcCB - 1) / kTcCB * kTcCB);
+    t.tiles_h = (int32_t)ceil_div64(ceil_div64(g->H, g->stride_h), kTcTile);
+    t.tiles_w = (int32_t)ceil_div64(ceil_div64(g->W, g->stride_w), kTcTile);
+    t.gx = g->N * g->stride_h * g->stride_w * t.tiles_h * t.tiles_w;
+    t.gy = t.Cp / kTcCB;
+    t.ok = t.gx >= 1 && t.gx < ((int64_t)1 << 31) && t.gy < 65536 && g->N * g->H * g->W * g->C < ((int64_t)1 << 40);
+    return t;
+}
+
+static size_t tconv_ws_bytes(const iseg_conv_geom* g, const TconvPlan& t)
+{
+    return align256((size_t)(g->R * g->S * t.Cp * t.Kp)) + align256((size_t)(t.gx * t.gy) * 8);
+}
+
+// wp[(r S + s) Cp + c][k] = w[k][r][s][c], zero for k >= K or c >= C
+__global__ __launch_bounds__(256) void k_tconv_pack(const int8_t* __restrict__ w, int8_t* __restrict__ wp,
+                                                    int32_t K, int32_t RS, int32_t C, int32_t Kp, int32_t Cp)
+{
+    const int64_t n = (int64_t)RS * Cp * Kp;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t k = (int32_t)(i % Kp);
+        const int64_t rc = i / Kp;
+        const int32_t c = (int32_t)(rc % Cp), rs = (int32_t)(rc / Cp);
+        wp[i] = (k < K && c < C) ? w[((int64_t)k * RS + rs) * C + c] : (int8_t)0;
+    }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_tconv_phase(TconvArgs a)
+{
+    constexpr int HMAX = kTcTile + kTcMaxTaps - 1;
+    __shared__ __attribute__((aligned(16))) int32_t sdy[HMAX * HMAX * (kTcMaxKp / 4)];
+    const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+    int64_t b = blockIdx.x;
+    const int tw_i = (int)(b % a.tiles_w);
+    b /= a.tiles_w;
+    const int th_i = (int)(b % a.tiles_h);
+    b /= a.tiles_h;
+    const int phw = (int)(b % a.sw);
+    b /= a.sw;
+    const int phh = (int)(b % a.sh);
+    const int n = (int)(b / a.sh);
+    uint64_t gmax = 0;
+    if (EPI == EPI_Q8) gmax = reduce_partials_u64(a.pmax, a.npmax);
+    // taps of this phase and the first phase row / column of the tile
+    const int Th = phh < a.R ? (a.R - phh + a.sh - 1) / a.sh : 0;
+    const int Tw = phw < a.S ? (a.S - phw + a.sw - 1) / a.sw : 0;
+    const int mh0 = (max(0, a.ph - phh) + a.sh - 1) / a.sh + th_i * kTcTile;
+    const int mw0 = (max(0, a.pw - phw) + a.sw - 1) / a.sw + tw_i * kTcTile;
+    const int KW = a.Kp >> 2;
+    const int HR = kTcTile + (Th > 0 ? Th - 1 : 0), HC = kTcTile + (Tw > 0 ? Tw - 1 : 0);
+    const int p0 = mh0 - (Th > 0 ? Th - 1 : 0), q0 = mw0 - (Tw > 0 ? Tw - 1 : 0);
+    int32_t acc[kTcCB];
+#pragma unroll
+    for (int j = 0; j < kTcCB; j++) acc[j] = 0;
+    if (Th > 0 && Tw > 0) {
+        // the dy rows p0 .. p0 + HR - 1, columns q0 .. q0 + HC - 1 (zero outside)
+        const bool words = (a.K & 3) == 0 && ((uintptr_t)a.dy & 3) == 0;
+        const int total = HR * HC * KW;
+        for (int i = tid; i < total; i += 256) {
+            const int kw = i % KW, pix = i / KW;
+            const int p = p0 + pix / HC, q = q0 + pix % HC;
+            int32_t v = 0;
+            if (p >= 0 && p < a.P && q >= 0 && q < a.Q) {
+                const int8_t* src = a.dy + (((int64_t)n * a.P + p) * a.Q + q) * a.K;
+                const int k = kw * 4;
+                if (words) {
+                    if (k < a.K) v = *(const int32_t*)(src + k);
+                } else {
+                    uint32_t u = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        if (k + e < a.K) u |= (uint32_t)(uint8_t)src[k + e] << (8 * e);
+                    v = (int32_t)u;
+                }
+            }
+            sdy[i] = v;
+        }
+        __syncthreads();
+        const int c0 = blockIdx.y * kTcCB;
+        for (int th = 0; th < Th; th++)
+            for (int tw = 0; tw < Tw; tw++) {
+                const int r = phh + th * a.sh, sx = phw + tw * a.sw;
+                const int32_t* wrow = (const int32_t*)(a.wp + (((int64_t)r * a.S + sx) * a.Cp + c0) * a.Kp);
+                const int32_t* srow = sdy + ((ty + Th - 1 - th) * HC + (tx + Tw - 1 - tw)) * KW;
+                for (int kw = 0; kw < KW; kw += 2) {
+                    const int2 v = *(const int2*)(srow + kw);
+#pragma unroll
+                    for (int j = 0; j < kTcCB; j++) {
+                        acc[j] = __builtin_amdgcn_sdot4(v.x, wrow[j * KW + kw], acc[j], false);
+                        acc[j] = __builtin_amdgcn_sdot4(v.y, wrow[j * KW + kw + 1], acc[j], false);
+                    }
+                }
+            }
+    }
+    const int h = (mh0 + ty) * a.sh + phh - a.ph, w = (mw0 + tx) * a.sw + phw - a.pw;
+    const bool valid = h < a.H && w < a.W;            // h, w >= 0 by the choice of mh0, mw0
+    const int c0 = blockIdx.y * kTcCB;
+    const int64_t o = (((int64_t)n * a.H + h) * a.W + w) * a.C + c0;
+    const int nc = a.C - c0 < kTcCB ? a.C - c0 : kTcCB;
+    if (EPI == EPI_RAW) {
+        if (valid)
+#pragma unroll
+            for (int j = 0; j < kTcCB; j++)
+                if (j < nc) a.out[o + j] = acc[j];
+        return;
+    }
+    if (EPI == EPI_MAX) {
+        uint32_t mx = 0;
+#pragma unroll
+        for (int j = 0; j < kTcCB; j++) {
+            const uint32_t av = (valid && j < nc) ? (uint32_t)(acc[j] < 0 ? -acc[j] : acc[j]) : 0u;
+            mx = av > mx ? av : mx;
+        }
+        block_store_max_u64(mx, a.pmax);
+        return;
+    }
+    // EPI_Q8: SQ codes with r = bitlen(global max) - 7 (half-up rounding)
+    const int rq = gmax ? (64 - __builtin_clzll(gmax)) - 7 : 0;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *a.out_exp = *a.exp_a + *a.exp_b + rq;
+    const int rs = rq > 0 ? rq - 1 : 0, ls = rq > 0 ? 0 : -rq;
+    if (valid)
+#pragma unroll
+        for (int j = 0; j < kTcCB; j++) {
+            if (j >= nc) break;
+            int32_t c = rq > 0 ? ((acc[j] >> rs) + 1) >> 1 : acc[j] << ls;
+            c = c > 127 ? 127 : (c < -127 ? -127 : c);
+            a.out8[o + j] = (int8_t)c;
+        }
+}
+
+template <int EPI>
+static int launch_tconv_e(const TconvPlan& t, const TconvArgs& a, hipStream_t s)
+{
+    ISEG_TIMED_LAUNCH(ISEG_KID_CONV_BWD_DATA, s, k_tconv_phase<EPI>, dim3((unsigned)t.gx, (unsigned)t.gy), dim3(256),
+                      0, s, a);
+    return launch_ok();
+}
+
+// the phase path of backward-data: raw sums, or a max pass and a code pass
+// (the sums are recomputed: K * taps products per output are cheaper to redo
+// than an int32 round trip through HBM)
+static int tconv_run(const TconvPlan& t, const iseg_conv_geom* g, int64_t P, int64_t Q, const int8_t* dy,
+                     const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp, int32_t out_mode, void* dx,
+                     int32_t* dx_exp, void* ws, hipStream_t stream)
+{
+    int8_t* wp = (int8_t*)ws;
+    uint64_t* pmax = (uint64_t*)((char*)ws + align256((size_t)(g->R * g->S * t.Cp * t.Kp)));
+    const int64_t npack = g->R * g->S * t.Cp * t.Kp;
+    hipLaunchKernelGGL(k_tconv_pack, dim3(grid_for(npack, 256, 1024)), dim3(256), 0, stream, w, wp, (int32_t)g->K,
+                       (int32_t)(g->R * g->S), (int32_t)g->C, t.Kp, t.Cp);
+    int rc = launch_ok();
+    if (rc) return rc;
+    TconvArgs a{};
+    a.dy = dy; a.wp = wp;
+    a.N = (int32_t)g->N; a.H = (int32_t)g->H; a.W = (int32_t)g->W; a.C = (int32_t)g->C; a.K = (int32_t)g->K;
+    a.Kp = t.Kp; a.Cp = t.Cp; a.P = (int32_t)P; a.Q = (int32_t)Q; a.R = (int32_t)g->R; a.S = (int32_t)g->S;
+    a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
+    a.tiles_h = t.tiles_h; a.tiles_w = t.tiles_w;
+    conv_plan_set("phase");
+    if (out_mode == ISEG_OUT_RAW) {
+        a.out = (int32_t*)dx;
+        if ((rc = launch_tconv_e<EPI_RAW>(t, a, stream))) return rc;
+        hipLaunchKernelGGL(k_exp_sum, dim3(1), dim3(1), 0, stream, dx_exp, dy_exp, w_exp);
+        return launch_ok();
+    }
+    a.pmax = pmax;
+    a.npmax = t.gx * t.gy;
+    if ((rc = launch_tconv_e<EPI_MAX>(t, a, stream))) return rc;
+    a.out8 = (int8_t*)dx; a.exp_a = dy_exp; a.exp_b = w_exp; a.out_exp = dx_exp;
+    return launch_tconv_e<EPI_Q8>(t, a, stream);
+}
+
+static size_t conv_bwd_data_core_ws(const iseg_conv_geom* g, int32_t out_mode)
 {
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
+    const TconvPlan tp = tconv_plan(g);
+    if (tp.ok) return 256 + tconv_ws_bytes(g, tp);
     size_t s = 256 + align256((size_t)(g->K * g->R * g->S * g->C));
     if (out_mode == ISEG_OUT_Q8) {
         size_t big = align256((size_t)(g->N * g->H * g->W * g->C) * 4);
@@ -4000,20 +4218,18 @@ extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mod
 // backward-data with the transposed weights either built here from w (KRSC) or
 // given by the caller (wt_in in layout wt_kind); a given layout that the
 // chosen path does not use is ignored and the path builds its own
-static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
+static int conv_bwd_data_core(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
                               const int8_t* wt_in, int32_t wt_kind, const iseg_conv_geom* g, int32_t out_mode,
                               void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
                               hipStream_t stream)
 {
-    ProfScope prof_scope(ISEG_KID_CONV_BWD_DATA, stream);
-    conv_plan_set("none");
     (void)dev_status;
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
     if (out_mode != ISEG_OUT_Q8 && out_mode != ISEG_OUT_RAW) return ISEG_ERR_ARG;
     if (!dy_exp || !w_exp || !dx_exp || (g->N > 0 && (!dy || !w || !dx))) return ISEG_ERR_ARG;
     if (g->K * g->R * g->S > kMaxKred) return ISEG_ERR_UNSUPPORTED;
-    if (!ws || ws_bytes < iseg_conv_bwd_data_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
+    if (!ws || ws_bytes < conv_bwd_data_core_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
     // ws: [max][transposed weights][per-block max partials][output staging]
     unsigned long long* maxp = (unsigned long long*)ws;
     const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
@@ -4093,6 +4309,9 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
         return halo_q8(hp, h, ISEG_KID_CONV_BWD_DATA, dy_exp, w_exp, (int8_t*)dx, dx_exp, maxp, pmax, rows,
                        stream);
     }
+    const TconvPlan tp = tconv_plan(g);
+    if (tp.ok)
+        return tconv_run(tp, g, P, Q, dy, dy_exp, w, w_exp, out_mode, dx, dx_exp, (char*)ws + 256, stream);
     wt = pick_wt(ISEG_WT_CRSK);
     if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, false, stream))) return rc;
     IgemmArgs a{};
@@ -4117,6 +4336,310 @@ static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int
                                 0, 0, 0, ISEG_I8, dx, dx_exp, nullptr, stream, pmax, nblk);
 }
 
+// ---------------------------------------------------------------------------
+// Reductions longer than the exact-int32 bound (C R S of a forward conv or
+// K R S of a backward-data conv above kMaxKred, e.g. a 7x7 conv from 4096
+// channels): the summed channels are cut into at most kMaxKredSplits chunks of
+// a multiple of 16 channels, each chunk's conv writes its exact int32 sums
+// (one contiguous copy of the chunk's operand columns ahead of it), and the
+// quantizer adds the chunks in int64, so the codes are those of the exact
+// total (|sum| < 127^2 * 8 * 131071 < 2^38).  Final codes only: raw int32 sums
+// of such a reduction need not fit int32.
+// ---------------------------------------------------------------------------
+constexpr int kMaxKredSplits = 8;
+
+struct KredSplit {
+    int splits = 0;        // 0: the reduction cannot be split within the limits
+    int64_t chunk = 0;     // channels per chunk (the last chunk may hold fewer)
+};
+
+static KredSplit kred_split(int64_t ch, int64_t RS)
+{
+    KredSplit ks;
+    const int64_t cmax = (kMaxKred / RS) & ~(int64_t)15;
+    if (cmax < 16) return ks;
+    const int64_t n = ceil_div64(ch, cmax);
+    if (n > kMaxKredSplits) return ks;
+    ks.chunk = (ceil_div64(ch, n) + 15) & ~(int64_t)15;     // <= cmax
+    ks.splits = (int)ceil_div64(ch, ks.chunk);
+    return ks;
+}
+
+// dst[r][c] = src[r][c0 + c] (r < rows, c < cn): a column slice of a
+// row-major [rows][cols] int8 matrix, 16 bytes per lane when all aligned
+__global__ __launch_bounds__(256) void k_gather_cols(const int8_t* __restrict__ src, int64_t rows, int64_t cols,
+                                                     int64_t c0, int64_t cn, int8_t* __restrict__ dst)
+{
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (((cols | c0 | cn) & 15) == 0 && (((uintptr_t)src | (uintptr_t)dst) & 15) == 0) {
+        const int64_t vpr = cn >> 4;
+        for (int64_t i = t0; i < rows * vpr; i += stride) {
+            const int64_t r = i / vpr, v = i - r * vpr;
+            *(int4*)(dst + r * cn + v * 16) = *(const int4*)(src + r * cols + c0 + v * 16);
+        }
+        return;
+    }
+    for (int64_t i = t0; i < rows * cn; i += stride) {
+        const int64_t r = i / cn, c = i - r * cn;
+        dst[i] = src[r * cols + c0 + c];
+    }
+}
+
+static int launch_gather_cols(const int8_t* src, int64_t rows, int64_t cols, int64_t c0, int64_t cn, int8_t* dst,
+                              hipStream_t s)
+{
+    if (rows * cn == 0) return ISEG_OK;
+    const int64_t work = (((cols | c0 | cn) & 15) == 0) ? rows * (cn >> 4) : rows * cn;
+    hipLaunchKernelGGL(k_gather_cols, dim3(grid_for(work, 256, 4096)), dim3(256), 0, s, src, rows, cols, c0, cn, dst);
+    return launch_ok();
+}
+
+// workspace: [max word][operand chunk][weight chunk (forward)][int32 sums of
+// every chunk][max partials][the chunk convs' own workspace]
+struct KredLayout {
+    KredSplit ks;
+    int64_t rows_a = 0, n = 0;
+    size_t a_off = 0, w_off = 0, part_off = 0, pmax_off = 0, sub_off = 0, sub_bytes = 0, total = 0;
+};
+
+// The long reduction on the direct-to-LDS implicit GEMM when its shape
+// allows (64-channel multiples, 16-byte aligned operands): the (tap, 64-channel
+// chunk) steps are split over gridDim.z so that every split sums at most
+// kMaxKred / 64 steps exactly in int32, with more splits (up to
+// kMaxKredSplits) while the output tiles alone leave CUs idle; the int32
+// partials go to the workspace and the quantizer adds them in int64.
+// workspace: [max word][transposed weights (backward-data)][int32 partials of
+// every split][max partials]
+struct KredDma {
+    bool ok = false;
+    DmaPlan p{};
+    size_t wt_off = 0, part_off = 0, pmax_off = 0, total = 0;
+};
+
+static KredDma kred_dma_plan(bool bwd, const iseg_conv_geom* g)
+{
+    KredDma d;
+    int64_t P, Q;
+    if (!geom_ok(g, &P, &Q)) return d;
+    const int64_t Ci = bwd ? g->K : g->C, Nout = bwd ? g->C : g->K;
+    const int64_t Mrows = bwd ? g->N * g->H * g->W : g->N * P * Q;
+    if (Ci % 64 || Nout % 64 || g->R * g->S > 64 || Mrows < 1 || Mrows >= ((int64_t)1 << 31)) return d;
+    const int64_t nk_full = g->R * g->S * (Ci / BK);
+    int S = (int)ceil_div64(nk_full, kMaxKred / BK);
+    if (S > kMaxKredSplits) return d;
+    d.p.two_pass = false;
+    d.p.bm = 128;
+    d.p.bn = Nout % 128 == 0 ? 128 : 64;
+    const int64_t blocks = ceil_div64(Mrows, d.p.bm) * (Nout / d.p.bn);
+    while (S < kMaxKredSplits && blocks * S < ISEG_IGEMM_SPLIT_BLOCKS) S++;
+    d.p.splits = S;
+    size_t o = 256;
+    d.wt_off = o;
+    if (bwd) o += align256((size_t)(g->K * g->R * g->S * g->C));
+    d.part_off = o;
+    o += align256((size_t)(S * Mrows * Nout) * 4);
+    d.pmax_off = o;
+    o += align256(512 * 8);
+    d.total = o;
+    d.ok = true;
+    return d;
+}
+
+static int conv_kred_dma(bool bwd, const KredDma& d, const int8_t* src, const int32_t* a_exp, const int8_t* w,
+                         const int32_t* w_exp, const int8_t* wt_in, int32_t wt_kind, const iseg_conv_geom* g,
+                         int8_t* out, int32_t* out_exp, void* ws, hipStream_t stream)
+{
+    int64_t P, Q;
+    geom_ok(g, &P, &Q);
+    char* base = (char*)ws;
+    int32_t* part = (int32_t*)(base + d.part_off);
+    uint64_t* pmax = (uint64_t*)(base + d.pmax_off);
+    int rc;
+    IgemmArgs a{};
+    if (bwd) {
+        int8_t* wt_ws = (int8_t*)(base + d.wt_off);
+        const bool given = wt_in && wt_kind == ISEG_WT_CRSK && ((uintptr_t)wt_in & 15) == 0;
+        if (!given && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, false, stream))) return rc;
+        a.src = src; a.wmat = given ? wt_in : wt_ws;
+        a.Mrows = g->N * g->H * g->W;
+        a.Nout = (int32_t)g->C; a.Kred = (int32_t)(g->K * g->R * g->S); a.Ci = (int32_t)g->K;
+        a.Hs = (int32_t)P; a.Ws = (int32_t)Q; a.Ho = (int32_t)g->H; a.Wo = (int32_t)g->W;
+    } else {
+        a.src = src; a.wmat = w;
+        a.Mrows = g->N * P * Q;
+        a.Nout = (int32_t)g->K; a.Kred = (int32_t)(g->C * g->R * g->S); a.Ci = (int32_t)g->C;
+        a.Hs = (int32_t)g->H; a.Ws = (int32_t)g->W; a.Ho = (int32_t)P; a.Wo = (int32_t)Q;
+    }
+    a.R = (int32_t)g->R; a.S = (int32_t)g->S;
+    a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
+    a.dh = g->dil_h; a.dw = g->dil_w;
+    a.out = part; a.pmax = nullptr; a.out16 = nullptr; a.tshift = nullptr;
+    if (!igemm_dma_ok(a)) return ISEG_ERR_UNSUPPORTED;
+    a.tap_balance = (bwd ? every_tile_skips<MODE_BWD>(a, d.p.bm) : every_tile_skips<MODE_FWD>(a, d.p.bm)) ? 1 : 0;
+    int64_t nblk = 0;
+    rc = bwd ? launch_igemm_dma<MODE_BWD>(a, d.p, EPI_PART, stream, &nblk)
+             : launch_igemm_dma<MODE_FWD>(a, d.p, EPI_PART, stream, &nblk);
+    if (rc) return rc;
+    conv_plan_set("kred_dma_split");
+    const int64_t n = a.Mrows * a.Nout;
+    int64_t npmax = 0;
+    int qg = 0;
+    if ((rc = launch_wgrad_reduce_qg(part, n, d.p.splits, nullptr, pmax, &npmax, stream, &qg))) return rc;
+    if (qg != d.p.splits) return ISEG_ERR_UNSUPPORTED;     // splits <= 8 and n % 64 == 0 make it fuse
+    return launch_requant_splits(part, d.p.splits, n, a_exp, w_exp, 8, 0, 1, 0, 0, 0, out, out_exp, stream, pmax,
+                                 npmax);
+}
+
+static bool kred_dma_ready(bool bwd, const KredDma& d, const int8_t* src, const int8_t* w)
+{
+    return d.ok && (((uintptr_t)src | (uintptr_t)(bwd ? nullptr : w)) & 15) == 0;
+}
+
+static bool kred_layout(bool bwd, const iseg_conv_geom* g, KredLayout* L)
+{
+    int64_t P, Q;
+    if (!geom_ok(g, &P, &Q)) return false;
+    const int64_t ch = bwd ? g->K : g->C, RS = g->R * g->S;
+    L->ks = kred_split(ch, RS);
+    if (!L->ks.splits) return false;
+    L->rows_a = bwd ? g->N * P * Q : g->N * g->H * g->W;
+    L->n = bwd ? g->N * g->H * g->W * g->C : g->N * P * Q * g->K;
+    if (L->n % 4) return false;
+    size_t o = 256;
+    L->a_off = o;
+    o += align256((size_t)(L->rows_a * L->ks.chunk));
+    L->w_off = o;
+    if (!bwd) o += align256((size_t)(g->K * RS * L->ks.chunk));
+    L->part_off = o;
+    o += align256((size_t)(L->ks.splits * L->n) * 4);
+    L->pmax_off = o;
+    o += align256(512 * 8);
+    size_t sub = 0;
+    const int64_t last = ch - (int64_t)(L->ks.splits - 1) * L->ks.chunk;
+    for (int64_t cn : {L->ks.chunk, last}) {
+        iseg_conv_geom s = *g;
+        (bwd ? s.K : s.C) = cn;
+        const size_t b = bwd ? conv_bwd_data_core_ws(&s, ISEG_OUT_RAW) : conv_fwd_core_ws(&s, ISEG_OUT_RAW);
+        sub = sub > b ? sub : b;
+    }
+    L->sub_off = o;
+    L->sub_bytes = sub;
+    L->total = o + sub;
+    return true;
+}
+
+static size_t kred_ws(bool bwd, const iseg_conv_geom* g)
+{
+    KredLayout L;
+    const size_t gs = kred_layout(bwd, g, &L) ? L.total : 0;
+    const KredDma d = kred_dma_plan(bwd, g);
+    const size_t ds = d.ok ? d.total : 0;
+    return gs > ds ? gs : ds;
+}
+
+static int conv_kred_split(bool bwd, const int8_t* a, const int32_t* a_exp, const int8_t* w, const int32_t* w_exp,
+                           const int8_t* wt_in, int32_t wt_kind, const iseg_conv_geom* g, int8_t* out,
+                           int32_t* out_exp, void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    KredLayout L;
+    if (!kred_layout(bwd, g, &L)) return ISEG_ERR_UNSUPPORTED;
+    if (!ws || ws_bytes < kred_ws(bwd, g)) return ISEG_ERR_WORKSPACE;
+    const KredDma d = kred_dma_plan(bwd, g);
+    if (kred_dma_ready(bwd, d, a, w))
+        return conv_kred_dma(bwd, d, a, a_exp, w, w_exp, wt_in, wt_kind, g, out, out_exp, ws, stream);
+    char* base = (char*)ws;
+    int8_t* ac = (int8_t*)(base + L.a_off);
+    int8_t* wc = (int8_t*)(base + L.w_off);
+    int32_t* part = (int32_t*)(base + L.part_off);
+    uint64_t* pmax = (uint64_t*)(base + L.pmax_off);
+    void* sws = base + L.sub_off;
+    const int64_t ch = bwd ? g->K : g->C, RS = g->R * g->S;
+    int rc;
+    conv_plan_set("kred_split");
+    if (L.n == 0) {     // empty batch: the exponent of an all-zero tensor
+        if ((rc = launch_fill_u32(base, 2, 0, stream))) return rc;
+        return launch_requant_apply(part, ISEG_I32, 0, a_exp, w_exp, 0, 8, 0, 1, 0, 0, 0, ISEG_I8, out, out_exp,
+                                    (const unsigned long long*)base, stream);
+    }
+    for (int i = 0; i < L.ks.splits; i++) {
+        const int64_t c0 = (int64_t)i * L.ks.chunk;
+        const int64_t cn = ch - c0 < L.ks.chunk ? ch - c0 : L.ks.chunk;
+        iseg_conv_geom s = *g;
+        int32_t* pi = part + (int64_t)i * L.n;
+        if ((rc = launch_gather_cols(a, L.rows_a, ch, c0, cn, ac, stream))) return rc;
+        if (bwd) {
+            s.K = cn;
+            rc = conv_bwd_data_core(ac, a_exp, w + c0 * RS * g->C, w_exp, nullptr, ISEG_WT_NONE, &s, ISEG_OUT_RAW,
+                                    pi, out_exp, sws, L.sub_bytes, dev_status, stream);
+        } else {
+            s.C = cn;
+            if ((rc = launch_gather_cols(w, g->K * RS, ch, c0, cn, wc, stream))) return rc;
+            rc = conv_fwd_core(ac, a_exp, wc, w_exp, &s, ISEG_OUT_RAW, pi, out_exp, sws, L.sub_bytes, dev_status,
+                               stream);
+        }
+        if (rc) return rc;
+    }
+    conv_plan_set("kred_split");
+    int64_t npmax = 0;
+    int qg = 0;
+    if ((rc = launch_wgrad_reduce_qg(part, L.n, L.ks.splits, nullptr, pmax, &npmax, stream, &qg))) return rc;
+    if (qg != L.ks.splits) return ISEG_ERR_UNSUPPORTED;     // splits <= 8 and n % 4 == 0 make it fuse
+    return launch_requant_splits(part, L.ks.splits, L.n, a_exp, w_exp, 8, 0, 1, 0, 0, 0, out, out_exp, stream,
+                                 pmax, npmax);
+}
+
+static bool conv_long_kred(bool bwd, const iseg_conv_geom* g)
+{
+    return (bwd ? g->K : g->C) * g->R * g->S > kMaxKred;
+}
+
+extern "C" size_t iseg_conv_fwd_ws(const iseg_conv_geom* g, int32_t out_mode)
+{
+    if (out_mode == ISEG_OUT_Q8 && g && conv_long_kred(false, g)) return kred_ws(false, g);
+    return conv_fwd_core_ws(g, out_mode);
+}
+
+extern "C" int iseg_conv_fwd(const int8_t* x, const int32_t* x_exp, const int8_t* w, const int32_t* w_exp,
+                             const iseg_conv_geom* g, int32_t out_mode, void* y, int32_t* y_exp,
+                             void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    ProfScope prof_scope(ISEG_KID_CONV_FWD, stream);
+    conv_plan_set("none");
+    int64_t P, Q;
+    if (!g || !geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
+    if (out_mode == ISEG_OUT_Q8 && conv_long_kred(false, g)) {
+        if (!x_exp || !w_exp || !y_exp || (g->N > 0 && (!x || !w || !y))) return ISEG_ERR_ARG;
+        return conv_kred_split(false, x, x_exp, w, w_exp, nullptr, ISEG_WT_NONE, g, (int8_t*)y, y_exp, ws, ws_bytes,
+                               dev_status, stream);
+    }
+    return conv_fwd_core(x, x_exp, w, w_exp, g, out_mode, y, y_exp, ws, ws_bytes, dev_status, stream);
+}
+
+extern "C" size_t iseg_conv_bwd_data_ws(const iseg_conv_geom* g, int32_t out_mode)
+{
+    if (out_mode == ISEG_OUT_Q8 && g && conv_long_kred(true, g)) return kred_ws(true, g);
+    return conv_bwd_data_core_ws(g, out_mode);
+}
+
+static int conv_bwd_data_impl(const int8_t* dy, const int32_t* dy_exp, const int8_t* w, const int32_t* w_exp,
+                              const int8_t* wt_in, int32_t wt_kind, const iseg_conv_geom* g, int32_t out_mode,
+                              void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                              hipStream_t stream)
+{
+    ProfScope prof_scope(ISEG_KID_CONV_BWD_DATA, stream);
+    conv_plan_set("none");
+    int64_t P, Q;
+    if (!g || !geom_ok(g, &P, &Q)) return ISEG_ERR_SHAPE;
+    if (out_mode == ISEG_OUT_Q8 && conv_long_kred(true, g)) {
+        if (!dy_exp || !w_exp || !dx_exp || (g->N > 0 && (!dy || !w || !dx))) return ISEG_ERR_ARG;
+        return conv_kred_split(true, dy, dy_exp, w, w_exp, wt_in, wt_kind, g, (int8_t*)dx, dx_exp, ws, ws_bytes,
+                               dev_status, stream);
+    }
+    return conv_bwd_data_core(dy, dy_exp, w, w_exp, wt_in, wt_kind, g, out_mode, dx, dx_exp, ws, ws_bytes,
+                              dev_status, stream);
+}
+
 extern "C" int iseg_conv_bwd_data(const int8_t* dy, const int32_t* dy_exp, const int8_t* w,
                                   const int32_t* w_exp, const iseg_conv_geom* g, int32_t out_mode,
                                   void* dx, int32_t* dx_exp, void* ws, size_t ws_bytes,
@@ -4139,7 +4662,8 @@ extern "C" int iseg_conv_bwd_data_t(const int8_t* dy, const int32_t* dy_exp, con
 extern "C" int32_t iseg_conv_bwd_data_wt_kind(const iseg_conv_geom* g)
 {
     int64_t P, Q;
-    if (!geom_ok(g, &P, &Q)) return ISEG_WT_NONE;
+    if (!geom_ok(g, &P, &Q) || tconv_plan(g).ok) return ISEG_WT_NONE;
+    if (conv_long_kred(true, g)) return kred_dma_plan(true, g).ok ? ISEG_WT_CRSK : ISEG_WT_NONE;
     const M32Plan mp = m32_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,
                                 g->dil_h, g->dil_w);
     const PersistPlan pp = persist_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h,

@@ -513,3 +513,121 @@ extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, c
                        err_exp, loss);
     return launch_ok();
 }
+
+// ---------------------------------------------------------------------------
+// MSE loss against one-hot labels (the FCN8s loss): L = mean over the N H W K
+// elements of (y - t)^2, t = [k == label], and E1 = SQ(2 (y - t) / (N H W K))
+// (Eq. 4 / 16) decided exactly.  With g = min(y_exp, 0), every y - t is an
+// integer V on the grid 2^g: V = c 2^(y_exp - g) - t 2^-g.  The gradient is
+// V 2^(g+1) / D (D = N H W K), its scale 2^u the smallest power of two above
+// max|V| 2^(g+1) / D, and a code floor(V 2^(k-1-ce) / D + 1/2) with ce the
+// smallest e with max|V| < D 2^e (u = ce + g + 1).  The loss is summed per
+// block in float64 and the partials in a fixed order.
+// ---------------------------------------------------------------------------
+namespace {
+struct MseArgs {
+    const int8_t* y;
+    const int32_t* y_exp;
+    const uint8_t* labels;
+    int64_t n;               // N H W K
+    int32_t K;
+    uint64_t* pmax;          // [gridDim.x] max |V|
+    double* psum;            // [gridDim.x] sum V^2
+    int32_t* status;
+};
+
+__device__ __forceinline__ int64_t mse_v(const MseArgs& a, int64_t i, int g, int ye)
+{
+    const int64_t pix = i / a.K;
+    const int k = (int)(i - pix * a.K);
+    const int lab = a.labels[pix];
+    const int64_t t = lab == k ? 1 : 0;
+    return (int64_t)a.y[i] * ((int64_t)1 << (ye - g)) - t * ((int64_t)1 << (-g));
+}
+
+__device__ __forceinline__ bool mse_exp_ok(int32_t e) { return e >= -60 && e <= 40; }
+
+__global__ __launch_bounds__(256) void k_mse_part(MseArgs a)
+{
+    __shared__ double sd[256];
+    const int32_t ye = *a.y_exp;
+    const bool ok = mse_exp_ok(ye);
+    if (!ok && blockIdx.x == 0 && threadIdx.x == 0) set_status(a.status, ISEG_DEV_RANGE);
+    const int g = ye < 0 ? ye : 0;
+    uint64_t m = 0;
+    double s = 0.0;
+    bool bad = false;
+    if (ok)
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.n;
+             i += (int64_t)gridDim.x * blockDim.x) {
+            bad |= a.labels[i / a.K] >= a.K;
+            const int64_t v = mse_v(a, i, g, ye);
+            const uint64_t av = (uint64_t)(v < 0 ? -v : v);
+            m = av > m ? av : m;
+            s += (double)v * (double)v;
+        }
+    if (bad) set_status(a.status, ISEG_DEV_RANGE);
+    block_store_max_u64(m, a.pmax);
+    sd[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sd[threadIdx.x] += sd[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) a.psum[blockIdx.x] = sd[0];
+}
+
+__global__ __launch_bounds__(256) void k_mse_codes(MseArgs a, int nparts, int bits, int8_t* __restrict__ err,
+                                                   int32_t* err_exp, double* loss)
+{
+    const int32_t ye = *a.y_exp;
+    const bool ok = mse_exp_ok(ye);
+    const int g = ye < 0 ? ye : 0;
+    const uint64_t M = reduce_partials_u64(a.pmax, nparts);
+    const i128 D = (i128)a.n;
+    const int ce = M ? ceil_pow2_exp128((i128)M, D) : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        if (M) {
+            *err_exp = ce + g + 2 - bits;
+        } else {
+            int lg = 0;                              // ceil(log2 D)
+            while (((int64_t)1 << lg) < a.n) lg++;
+            *err_exp = g + 1 - lg;
+        }
+        double s = 0.0;
+        for (int b = 0; b < nparts; b++) s += a.psum[b];
+        if (loss) *loss = ok ? ldexp(s, 2 * g) / (double)a.n : __longlong_as_double(0x7ff8000000000000ll);
+    }
+    const int sh = bits - 1 - ce;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int8_t code = 0;
+        if (ok && M) code = (int8_t)clamp_k128(rhu128((i128)mse_v(a, i, g, ye), sh, D), bits);
+        err[i] = code;
+    }
+}
+}  // namespace
+
+extern "C" size_t iseg_mse_onehot_ws(int64_t n) { return n > 0 ? 256 + 2 * align256(2048 * 8) : 0; }
+
+extern "C" int iseg_mse_onehot(const int8_t* y, const int32_t* y_exp, const uint8_t* labels, int64_t N, int64_t H,
+                               int64_t W, int64_t K, int32_t bits, double* loss, int8_t* err, int32_t* err_exp,
+                               void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    if (N < 1 || H < 1 || W < 1 || K < 1 || bits < 2 || bits > 8) return ISEG_ERR_ARG;
+    if (!y || !y_exp || !labels || !err || !err_exp) return ISEG_ERR_ARG;
+    if (K > 256 || N * H * W * K > ((int64_t)1 << 40)) return ISEG_ERR_UNSUPPORTED;
+    const int64_t n = N * H * W * K;
+    if (!ws || ws_bytes < iseg_mse_onehot_ws(n)) return ISEG_ERR_WORKSPACE;
+    MseArgs a{};
+    a.y = y; a.y_exp = y_exp; a.labels = labels; a.n = n; a.K = (int32_t)K; a.status = dev_status;
+    a.pmax = (uint64_t*)((char*)ws + 256);
+    a.psum = (double*)((char*)ws + 256 + align256(2048 * 8));
+    const unsigned grid = grid_for(n, 256 * 8, 2048);
+    hipLaunchKernelGGL(k_mse_part, dim3(grid), dim3(256), 0, stream, a);
+    int rc = launch_ok();
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_mse_codes, dim3(grid_for(n, 256 * 4, 4096)), dim3(256), 0, stream, a, (int)grid,
+                       (int)bits, err, err_exp, loss);
+    return launch_ok();
+}

@@ -122,6 +122,8 @@ _SIGS = {
     "iseg_softmax_ce_ws": ([_I64, _I64, _I64, _I64, _I64, _I64], _SZ),
     "iseg_softmax_ce": ([_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _SZ,
                          _P, _P], C.c_int),
+    "iseg_mse_onehot_ws": ([_I64], _SZ),
+    "iseg_mse_onehot": ([_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _P, _P, _P, _P, _SZ, _P, _P], C.c_int),
     "iseg_update_multi": ([_P, _I32, _I32, _U64, _U32, _I32, _I32, _I32, _P, _P], C.c_int),
     "iseg_philox4x32_10": ([_P, _P, _P], None),
     "iseg_profile_arm": ([_I32, _P, _P], C.c_int),
@@ -404,6 +406,23 @@ def iseg_softmax_ce(logits, logit_exp, labels, N, h, w, K, H, W, bits, loss, gra
     _check(rc, "iseg_softmax_ce")
 
 
+def iseg_mse_onehot(y, y_exp, labels, bits, loss, err, err_exp, ws, status=None):
+    N, H, W, K = y.shape
+    rc = lib().iseg_mse_onehot(_ptr(y), _ptr(y_exp), _ptr(labels), N, H, W, K, bits, _ptr(loss), _ptr(err),
+                               _ptr(err_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_mse_onehot")
+
+
+def mse_onehot(y, y_exp, labels, bits=8, status=None):
+    """(loss, E1 codes, exponent) of the MSE loss against one-hot labels."""
+    loss = torch.zeros(1, dtype=torch.float64, device=y.device)
+    err = torch.empty_like(y)
+    e = _out_exp(y.device)
+    ws = workspace(y.device).get(lib().iseg_mse_onehot_ws(y.numel()))
+    iseg_mse_onehot(y, y_exp, labels, bits, loss, err, e, ws, status)
+    return loss, err, e
+
+
 def iseg_philox4x32_10(ctr, key):
     c = (C.c_uint32 * 4)(*ctr)
     k = (C.c_uint32 * 2)(*key)
@@ -467,18 +486,34 @@ class KernelTimer:
         self.kid = next(iter(self.kids))
         self.match = tuple(layer_match) if layer_match is not None else None
         self.pairs = []                  # (start, stop, kernel id, layer key)
+        self.free = []                   # created events not in use
 
     def wants(self, kid, key):
         return kid in self.kids and (self.match is None or tuple(key) == self.match)
 
-    def arm(self, kid=None, key=None):
-        h = _hiprt()
-        a, b = C.c_void_p(), C.c_void_p()
-        if h.hipEventCreate(C.byref(a)) or h.hipEventCreate(C.byref(b)):
+    def _event(self):
+        if self.free:
+            return self.free.pop()
+        e = C.c_void_p()
+        if _hiprt().hipEventCreate(C.byref(e)):
             raise IsegError("hipEventCreate failed")
+        return e
+
+    def arm(self, kid=None, key=None):
+        a, b = self._event(), self._event()
         kid = self.kid if kid is None else kid
         self.pairs.append((a, b, kid, tuple(key) if key is not None else None))
         iseg_profile_arm(kid, a, b)
+
+    def reset(self):
+        """Forget the timed launches and keep their events for the next ones
+        (an untimed pass with the timer installed creates the events a timed
+        region then reuses, keeping event creation out of it)."""
+        h = _hiprt()
+        for a, b, _, _ in self.pairs:
+            h.hipEventSynchronize(b)
+            self.free += [a, b]
+        self.pairs = []
 
     def launches(self):
         """[(kernel id, layer key, ms)] of every timed launch."""
@@ -506,7 +541,9 @@ class KernelTimer:
         for a, b, _, _ in self.pairs:
             h.hipEventDestroy(a)
             h.hipEventDestroy(b)
-        self.pairs = []
+        for e in self.free:
+            h.hipEventDestroy(e)
+        self.pairs, self.free = [], []
 
 
 _TIMER = None

@@ -134,8 +134,12 @@ class IntNet:
             if nd["kind"] != "conv" or (nd["src"][0] == "input" and not self.wl["input_grad"]):
                 continue
             L = self.convs[nd["name"]]
-            L["wt_kind"] = iseg.wt_kind(rec[nd["name"]]["a_in"].shape, L["w_q"].shape, nd["stride"],
-                                        nd["pad"], nd["dil"])
+            # a transposed conv runs backward-data in its forward, on the
+            # geometry of the conv it is the adjoint of
+            xs = rec[nd["name"]]["a_out"].shape if nd.get("transposed") else rec[nd["name"]]["a_in"].shape
+            L["wt_kind"] = iseg.wt_kind(xs, L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"])
+            if L["wt_kind"] == iseg.ISEG_WT_NONE:
+                continue    # a reduction split over channel chunks reads w itself
             L["w_t"] = torch.empty_like(L["w_q"])
             ents.append((L["w_q"], L["w_t"], L["wt_kind"]))
         self.wt_tab, self.wt_n, self.wt_tiles = iseg.wt_table(ents, self.dev)
@@ -154,9 +158,18 @@ class IntNet:
             if k == "conv":
                 L = self.convs[name]
                 raw = self.bn_raw and nd["bn"]
-                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
-                                      out_mode=iseg.ISEG_OUT_RAW if raw else iseg.ISEG_OUT_Q8,
-                                      status=self.status)
+                if nd.get("transposed"):
+                    # the adjoint of the conv whose input has this node's output shape
+                    N, h, w, _ = a.shape
+                    H = (h - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+                    W = (w - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+                    z, ze = iseg.conv_bwd_data(a, ae, L["w_q"], self.w_exp, (N, H, W, nd["cout"]), nd["stride"],
+                                               nd["pad"], nd["dil"], wt=L.get("w_t"), wt_kind=L.get("wt_kind", 0),
+                                               status=self.status)
+                else:
+                    z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
+                                          out_mode=iseg.ISEG_OUT_RAW if raw else iseg.ISEG_OUT_Q8,
+                                          status=self.status)
                 r.update(z=z, z_exp=ze)
                 if nd["bn"]:
                     y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])],
@@ -194,6 +207,10 @@ class IntNet:
         out = rec[self.wl["nodes"][-1]["name"]]
         if self.wl["loss"] == "given":
             return self.dy, self.dy_exp
+        if self.wl["loss"] == "mse":
+            loss, e, ee = iseg.mse_onehot(out["a_out"], out["a_out_exp"], self.labels, status=self.status)
+            self.loss = loss
+            return e, ee
         loss, grad, e, ee = iseg.softmax_ce(out["a_out"], out["a_out_exp"], self.labels, status=self.status)
         self.loss = loss
         return e, ee
@@ -241,9 +258,16 @@ class IntNet:
                 G, Ge = self._wgrad(nd, L, r, dz, dze)
                 r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
                 grads.append((nd, r))
-                if need_in:
+                if need_in and nd.get("transposed"):
+                    # the input error of a transposed conv is the forward of the
+                    # conv it is the adjoint of
+                    ei, eie = iseg.conv_fwd(dz, dze, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
+                                            status=self.status)
+                    r.update(e_in=ei, e_in_exp=eie)
+                    send(src, ei, eie)
+                elif need_in:
                     ei, eie = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
-                                                 nd["stride"], nd["pad"], nd["dil"], wt=L["w_t"],
+                                                 nd["stride"], nd["pad"], nd["dil"], wt=L.get("w_t"),
                                                  wt_kind=L["wt_kind"], status=self.status)
                     r.update(e_in=ei, e_in_exp=eie)
                     send(src, ei, eie)
@@ -254,8 +278,8 @@ class IntNet:
                     r.update(e_in=ei, e_in_exp=eie)
                     send(src, ei, eie)
             elif k == "add":
-                d = iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]],
-                                       status=self.status)
+                d = (iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]],
+                                        status=self.status) if nd["relu"] else e)
                 r.update(e_in=d, e_in_exp=ee)
                 for s in nd["src"]:
                     if s != "input" or want_input:
@@ -286,8 +310,14 @@ class IntNet:
     def _wgrad(self, nd, L, r, dz, dze):
         """Q_G(backward-weight) of one conv (Eq. 17), on the side stream once
         dz is ready; its inputs are marked as in use there."""
-        args = (dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"],
-                self.g_mode, 8, self.seed, 16 * L["l"], self.step_no)
+        if nd.get("transposed"):
+            # the adjoint conv reads dz and writes this node's input: its
+            # weight gradient pairs the node's input (as the error) with dz
+            args = (r["a_in"], r["a_in_exp"], dz, dze, L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"],
+                    self.g_mode, 8, self.seed, 16 * L["l"], self.step_no)
+        else:
+            args = (dz, dze, r["a_in"], r["a_in_exp"], L["w_q"].shape, nd["stride"], nd["pad"], nd["dil"],
+                    self.g_mode, 8, self.seed, 16 * L["l"], self.step_no)
         if self.side is None:
             return iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]), status=self.status)
         ready = torch.cuda.current_stream(self.dev).record_event()

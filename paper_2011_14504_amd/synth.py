@@ -41,6 +41,22 @@ def he_normal(seed, shape, fan_in):
     return (rng(seed).standard_normal(size=shape) * std).astype(np.float32)
 
 
+def bilinear_filter(R, cin, cout):
+    """The bilinear-upsampling initialisation of a transposed conv (the FCN
+    decoder, Sec. 3.2.1): w[c][r][s][c] = f(r) f(s) on the channel diagonal,
+    f(t) = 1 - |t - centre| / factor with factor = ceil(R / 2) and centre =
+    factor - 1 (R odd) or factor - 1/2 (R even); zero off the diagonal.
+    Layout [cin][R][R][cout]; float32 (every value is a multiple of
+    1/factor^2, exact)."""
+    factor = (R + 1) // 2
+    centre = factor - 1 if R % 2 == 1 else factor - 0.5
+    f = 1.0 - np.abs(np.arange(R) - centre) / factor
+    w = np.zeros((cin, R, R, cout), dtype=np.float32)
+    for c in range(min(cin, cout)):
+        w[c, :, :, c] = np.outer(f, f)
+    return w
+
+
 def gaussian_codes(seed, shape, std, dtype=np.int8):
     """Rounded normal samples clipped to [-127, 127] (for BN statistics tests)."""
     v = np.rint(rng(seed).standard_normal(size=shape) * std)
@@ -77,12 +93,26 @@ def conv(name, src, cin, cout, R, stride=1, pad=0, dil=1, bn=True, relu=True):
                 pad=pad, dil=dil, bn=bn, relu=relu)
 
 
+def deconv(name, src, cin, cout, R, stride, pad, relu=False):
+    """Transposed convolution (a decoder's learned upsampling): the adjoint
+    of a conv whose input is this node's output ([N, (H-1) stride - 2 pad +
+    R, ..., cout]) and whose output is this node's input; its weights are
+    that conv's, [cin][R][R][cout].  No BN (the FCN decoder has none)."""
+    return dict(kind="conv", transposed=True, name=name, src=[src], cin=cin, cout=cout, R=R,
+                stride=stride, pad=pad, dil=1, bn=False, relu=relu)
+
+
 def maxpool(name, src, k, stride, pad=0):
     return dict(kind="maxpool", name=name, src=[src], k=k, stride=stride, pad=pad)
 
 
 def add_relu(name, a, b):
     return dict(kind="add", name=name, src=[a, b], relu=True)
+
+
+def add(name, a, b):
+    """Sum of two maps without a ReLU (the FCN's score fusion)."""
+    return dict(kind="add", name=name, src=[a, b], relu=False)
 
 
 def gap(name, src):
@@ -184,8 +214,42 @@ DEEPLABV3_R50 = dict(id=5, name="deeplabv3-r50-os16-n8-512", N=8, H=512, W=512, 
                      input_grad=False, loss="softmax_ce", classes=150,
                      nodes=_R50[0] + aspp("aspp", _R50[1], 2048, 150)[0])
 
+
+
+def fcn8s(classes, src="input"):
+    """FCN8s on VGG16 (no BN): the five conv blocks with max pooling, the
+    fully convolutional fc6 (7x7, 4096) and fc7 (1x1, 4096) with ReLU, the
+    score convs (1x1, no ReLU) on fc7, pool4 and pool3, and three transposed
+    convs initialised as bilinear upsampling (x2, x2, x8) with the score
+    fusions between them.  Padding is chosen so that each upsampling
+    doubles (or multiplies by 8) the map exactly, so no crop is needed."""
+    nodes, prev, cin = [], src, 3
+    for b, (c, n) in enumerate([(64, 2), (128, 2), (256, 3), (512, 3), (512, 3)], 1):
+        for i in range(1, n + 1):
+            nodes.append(conv(f"conv{b}_{i}", prev, cin, c, 3, 1, 1, bn=False))
+            prev, cin = f"conv{b}_{i}", c
+        nodes.append(maxpool(f"pool{b}", prev, 2, 2, 0))
+        prev = f"pool{b}"
+    nodes += [conv("fc6", "pool5", 512, 4096, 7, 1, 3, bn=False),
+              conv("fc7", "fc6", 4096, 4096, 1, bn=False),
+              conv("score_fr", "fc7", 4096, classes, 1, bn=False, relu=False),
+              deconv("upscore2", "score_fr", classes, classes, 4, 2, 1),
+              conv("score_pool4", "pool4", 512, classes, 1, bn=False, relu=False),
+              add("fuse_pool4", "upscore2", "score_pool4"),
+              deconv("upscore_pool4", "fuse_pool4", classes, classes, 4, 2, 1),
+              conv("score_pool3", "pool3", 256, classes, 1, bn=False, relu=False),
+              add("fuse_pool3", "upscore_pool4", "score_pool3"),
+              deconv("upscore8", "fuse_pool3", classes, classes, 16, 8, 4)]
+    return nodes
+
+
+# FCN8s-VGG16 training step: batch 8 of 3x512x512 images, 21 classes (PASCAL
+# VOC), MSE loss against the one-hot labels, gradients by Eq. 18 (no BN).
+FCN8S_VGG16 = dict(id=6, name="fcn8s-vgg16-n8-512", N=8, H=512, W=512, C=3, input_grad=False,
+                   loss="mse", classes=21, gq=2, nodes=fcn8s(21))
+
 WORKLOADS = {1: SINGLE_CONV, 2: VGG16_BLOCKS12, 3: RESNET50_CONV2X, 4: ASPP_HEAD,
-             5: DEEPLABV3_R50}
+             5: DEEPLABV3_R50, 6: FCN8S_VGG16}
 
 
 def without_bn(wl):
@@ -215,7 +279,11 @@ def node_shapes(wl):
     for nd in wl["nodes"]:
         N, H, W, Cc = shapes[nd["src"][0]]
         k = nd["kind"]
-        if k == "conv":
+        if k == "conv" and nd.get("transposed"):
+            P = (H - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+            Q = (W - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+            shapes[nd["name"]] = (N, P, Q, nd["cout"])
+        elif k == "conv":
             P = (H + 2 * nd["pad"] - nd["dil"] * (nd["R"] - 1) - 1) // nd["stride"] + 1
             Q = (W + 2 * nd["pad"] - nd["dil"] * (nd["R"] - 1) - 1) // nd["stride"] + 1
             shapes[nd["name"]] = (N, P, Q, nd["cout"])
@@ -250,7 +318,10 @@ def workload_inputs(wl, N=None):
     weights = []
     for i, nd in enumerate(conv_nodes(wl)):
         R, cin, cout = nd["R"], nd["cin"], nd["cout"]
-        weights.append(he_normal(seed_for(wl["id"], i + 1), (cout, R, R, cin), cin * R * R))
+        if nd.get("transposed"):
+            weights.append(bilinear_filter(R, cin, cout))
+        else:
+            weights.append(he_normal(seed_for(wl["id"], i + 1), (cout, R, R, cin), cin * R * R))
     out = dict(x=x, x_exp=ACT_EXP, weights=weights, seed=seed_for(wl["id"], 0))
     shp = node_shapes(wl)[wl["nodes"][-1]["name"]]
     if wl["loss"] == "given":
@@ -258,4 +329,6 @@ def workload_inputs(wl, N=None):
         out["dy_exp"] = ERR_EXP
     else:
         out["labels"] = labels(seed_for(wl["id"], 51), (N, wl["H"], wl["W"]), wl["classes"])
+    if wl["loss"] == "mse":
+        out["labels"] = labels(seed_for(wl["id"], 51), shp[:3], wl["classes"])
     return out

@@ -262,7 +262,13 @@ class Net:
         """Z = SQ8(conv(A, W_q)) (Eq. 15 on the MAC output) and A' of the
         node: with BN, Q_A(ReLU?(L1BN(Z))); without, Q_A(ReLU?(Z))."""
         nd = self.L[name]["nd"]
-        acc = conv(a, self.w_q(name), nd["stride"], nd["pad"], nd["dil"])
+        if nd.get("transposed"):
+            # the adjoint of the conv whose input has this node's output shape
+            H = (a.shape[1] - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+            W = (a.shape[2] - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+            acc = conv_data_grad(a, self.w_q(name), H, W, nd["stride"], nd["pad"], nd["dil"])
+        else:
+            acc = conv(a, self.w_q(name), nd["stride"], nd["pad"], nd["dil"])
         if self.bn_raw and nd["bn"]:
             z, z_exp = acc, None          # the MAC output itself (exponent not compared)
         else:
@@ -294,6 +300,14 @@ class Net:
         else:
             dz, dz_exp = e, e_exp
         r["dz"], r["dz_exp"] = dz, dz_exp
+        if nd.get("transposed"):
+            # the adjoint conv reads dz and writes this node's input: its weight
+            # gradient pairs the node's input with dz, its forward gives E1
+            Gsum = conv_weight_grad(r["a_in"], dz, nd["R"], nd["stride"], nd["pad"], nd["dil"])
+            r["G"], r["G_exp"] = RQ(Gsum, 8, self.gq == 1, self.seed, 16 * l, step)
+            if want_input:
+                r["e_in"], r["e_in_exp"] = SQ(conv(dz, self.w_q(name), nd["stride"], nd["pad"], nd["dil"]), 8)
+            return r
         Gsum = conv_weight_grad(dz, r["a_in"], nd["R"], nd["stride"], nd["pad"], nd["dil"])
         r["G"], r["G_exp"] = RQ(Gsum, 8, self.gq == 1, self.seed, 16 * l, step)
         if want_input:
@@ -410,3 +424,45 @@ def stage_step(net, x, x_exp, dy, dy_exp, prefix, blocks):
     recs["input"] = dict(e_out=e, e_out_exp=e_exp)
     net.update({k: v for k, v in recs.items() if k in net.L})
     return recs
+
+
+def mse_error(y, labels, classes):
+    """The MSE loss of y against one-hot labels, mean over every element, and
+    E1 = SQ8 of its gradient 2 (y - t) / (number of elements)."""
+    t = np.zeros(y.shape, dtype=object)
+    for idx in np.ndindex(labels.shape):
+        for k in range(classes):
+            t[idx + (k,)] = Fr(int(labels[idx] == k))
+    D = y.size
+    diff = y - t
+    loss = sum((v * v for v in diff.ravel()), Fr(0)) / D
+    return loss, SQ(diff * Fr(2, D), 8)
+
+
+def decoder_step(net, x, x_exp, labels, classes):
+    """A tiny FCN-style decoder: c1 = ReLU conv 3x3 stride 2 (no BN), s1 = 1x1
+    score conv on c1, up = transposed conv x2 (4x4, stride 2, pad 1) of s1,
+    s0 = 1x1 score conv on the input, fuse = Q_A(up + s0) without ReLU; the
+    MSE loss on fuse; no input gradient."""
+    a = values(x, x_exp)
+    recs = {}
+    recs["c1"] = net.conv_forward("c1", a)
+    recs["s1"] = net.conv_forward("s1", recs["c1"]["a_out"])
+    recs["up"] = net.conv_forward("up", recs["s1"]["a_out"])
+    recs["s0"] = net.conv_forward("s0", a)
+    s = recs["up"]["a_out"] + recs["s0"]["a_out"]
+    out, out_exp = SQ(s, net.cfg["k_A"])
+    recs["fuse"] = dict(a_out=out, a_out_exp=out_exp)
+    loss, (e, e_exp) = mse_error(out, labels, classes)
+    recs["fuse"].update(e_out=e, e_out_exp=e_exp, e_in=e, e_in_exp=e_exp)
+    # the sum passes its error to both inputs unchanged
+    for name in ("up", "s0"):
+        recs[name]["e_out"], recs[name]["e_out_exp"] = e, e_exp
+    net.conv_backward("s0", recs["s0"], e, e_exp, False)
+    net.conv_backward("up", recs["up"], e, e_exp, True)
+    recs["s1"]["e_out"], recs["s1"]["e_out_exp"] = recs["up"]["e_in"], recs["up"]["e_in_exp"]
+    net.conv_backward("s1", recs["s1"], recs["up"]["e_in"], recs["up"]["e_in_exp"], True)
+    recs["c1"]["e_out"], recs["c1"]["e_out_exp"] = recs["s1"]["e_in"], recs["s1"]["e_in_exp"]
+    net.conv_backward("c1", recs["c1"], recs["s1"]["e_in"], recs["s1"]["e_in_exp"], False)
+    net.update({k: v for k, v in recs.items() if k in net.L})
+    return recs, loss

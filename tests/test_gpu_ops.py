@@ -107,7 +107,17 @@ CONV_SHAPES = [
     (2, 9, 10, 320, 64, 1, 1, 0, 1),
     (1, 18, 17, 128, 128, 3, 1, 6, 6),    # atrous 6: 18 steps, padding-only taps
     (1, 11, 13, 64, 128, 3, 1, 3, 3),     # dilation 3: 9 steps
+] + [
+    # strided backward-data with few dy channels (K): the phase path (FCN's
+    # upsampling adjoints at 21 classes among them)
+    (1, 32, 32, 21, 21, 4, 2, 1, 1),
+    (1, 24, 40, 21, 21, 16, 8, 4, 1),
+    (2, 13, 11, 24, 10, 3, 2, 1, 1),
+    (1, 9, 9, 40, 20, 1, 2, 0, 1),        # 1x1 stride 2: half the phases get no tap
+    (1, 15, 17, 8, 33, 5, 3, 2, 1),
+    (1, 10, 12, 9, 64, 3, 2, 1, 1),
 ]
+PHASE_SHAPES = CONV_SHAPES[-6:]
 
 
 def _geom(s):
@@ -147,6 +157,19 @@ def test_conv_bwd_data(orc, dev, s):
     assert np.array_equal(H(dx).astype(np.int64), rc) and ev(dxe) == rce
 
 
+@pytest.mark.parametrize("s", PHASE_SHAPES, ids=str)
+def test_conv_bwd_data_phase_path(dev, s):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, Cc, K, R, st, pad, d = s
+    P = (Hh + 2 * pad - R) // st + 1
+    Q = (W + 2 * pad - R) // st + 1
+    dy = synth.int_codes(23, (N, P, Q, K))
+    w = synth.int_codes(24, (K, R, R, Cc))
+    iseg.conv_bwd_data(T(dy, dev), E(-20, dev), T(w, dev), E(-7, dev), (N, Hh, W, Cc), st, pad, d)
+    assert iseg.iseg_conv_last_plan() == "phase"
+    assert iseg.wt_kind((N, Hh, W, Cc), w.shape, st, pad, d) == iseg.ISEG_WT_NONE
+
+
 def _wt_layout(w, kind):
     """[K, R, S, C] -> [C, R*S, K] (taps reversed for the flipped kind): a plain
     permutation of the weight codes, the layout backward-data reads."""
@@ -168,6 +191,10 @@ def test_conv_bwd_data_pretransposed(orc, dev, s):
     ref = orc.conv_bwd_data_raw(dy, w, _geom(s))
     rc, rce = orc.requant(ref, -27, 8)
     kind = iseg.wt_kind((N, Hh, W, Cc), w.shape, st, pad, d)
+    if kind == iseg.ISEG_WT_NONE:
+        # the phase path (strided, few dy channels) repacks w itself: a
+        # caller's layout of either kind is ignored
+        kind = iseg.ISEG_WT_CRSK
     assert kind in (iseg.ISEG_WT_CRSK, iseg.ISEG_WT_CRSK_FLIP)
     other = iseg.ISEG_WT_CRSK + iseg.ISEG_WT_CRSK_FLIP - kind
     for k in (kind, other):
@@ -247,6 +274,61 @@ def test_conv_bwd_weight_long_reduction(orc, dev):
                                   1, 0, 1, g_mode=iseg.ISEG_G_RAW)
     ref = orc.conv_bwd_weight_raw(dy, x, (3, 220, 220, 4, 4, 1, 1, 1, 1, 0, 0, 1, 1))
     assert np.array_equal(H(raw), ref)
+
+
+# Reductions longer than one exact int32 sum may hold (C R S or K R S above
+# 131071, e.g. FCN's fc6: 7x7 from 4096 channels): the channels are split into
+# chunks whose int32 sums the quantizer adds in int64.  (pass, N, H, W, C, K,
+# R, pad, codes): "max" makes every code 127 so the centre sums pass 2^31.
+LONG_KRED_CASES = [
+    ("fwd", 1, 7, 7, 2740, 32, 7, 3, "max"),       # 2 chunks, C % 16 != 0
+    ("fwd", 1, 3, 3, 6000, 16, 7, 3, "rand"),      # 3 chunks
+    ("fwd", 2, 6, 7, 2752, 64, 7, 3, "rand"),
+    ("bwd", 1, 7, 7, 64, 4096, 7, 3, "max"),       # fc6's backward-data
+    ("bwd", 2, 8, 6, 48, 4100, 7, 3, "rand"),      # K % 16 != 0
+    ("bwd", 1, 4, 4, 512, 4096, 7, 3, "rand"),
+    ("bwd", 2, 16, 16, 512, 4096, 7, 3, "rand"),    # fc6 at 512x512 input, batch 2
+    ("fwd", 1, 7, 7, 2752, 64, 7, 3, "max"),
+    ("bwd", 1, 7, 7, 40, 4100, 7, 3, "max"),
+]
+
+
+@pytest.mark.parametrize("case", LONG_KRED_CASES, ids=lambda c: "-".join(str(v) for v in c))
+def test_conv_long_reduction_split(orc, dev, case):
+    from paper_2011_14504_amd import iseg
+    kind, N, Hh, W, Cc, K, R, pad, codes = case
+    geom = (N, Hh, W, Cc, K, R, R, 1, 1, pad, pad, 1, 1)
+    P, Q = orc.conv_out_hw(geom)
+    a_shape = (N, Hh, W, Cc) if kind == "fwd" else (N, P, Q, K)
+    if codes == "max":
+        a = np.full(a_shape, 127, np.int8)
+        w = np.full((K, R, R, Cc), 127, np.int8)
+    else:
+        a = synth.int_codes(51, a_shape)
+        w = synth.int_codes(52, (K, R, R, Cc))
+    print(f"[long-kred] {case}", flush=True)
+    if kind == "fwd":
+        ref = orc.conv_fwd_raw(a, w, geom)
+        out, oe = iseg.conv_fwd(T(a, dev), E(-7, dev), T(w, dev), E(-6, dev), 1, pad, 1)
+    else:
+        ref = orc.conv_bwd_data_raw(a, w, geom)
+        out, oe = iseg.conv_bwd_data(T(a, dev), E(-7, dev), T(w, dev), E(-6, dev), (N, Hh, W, Cc), 1, pad, 1)
+    # channel multiples of 64: one implicit GEMM split over the reduction;
+    # otherwise channel chunks gathered and run one by one
+    ci, nout = (Cc, K) if kind == "fwd" else (K, Cc)
+    want = "kred_dma_split" if ci % 64 == 0 and nout % 64 == 0 else "kred_split"
+    assert iseg.iseg_conv_last_plan() == want
+    if codes == "max":
+        assert np.abs(ref).max() > 2 ** 31 - 1
+    rc, rce = orc.requant(ref, -13, 8)
+    assert np.array_equal(H(out).astype(np.int64), rc) and ev(oe) == rce
+    # the raw sums of such a reduction need not fit int32: refused
+    with pytest.raises(iseg.IsegError):
+        if kind == "fwd":
+            iseg.conv_fwd(T(a, dev), E(-7, dev), T(w, dev), E(-6, dev), 1, pad, 1, out_mode=iseg.ISEG_OUT_RAW)
+        else:
+            iseg.conv_bwd_data(T(a, dev), E(-7, dev), T(w, dev), E(-6, dev), (N, Hh, W, Cc), 1, pad, 1,
+                               out_mode=iseg.ISEG_OUT_RAW)
 
 
 # Full-size layer shapes of the DeepLabv3-ResNet50 step (batch 8, 512x512),
@@ -722,3 +804,48 @@ def test_conv_bn_infer(orc, dev, s):
         zz = orc.requant_fixed(orc.conv_fwd_raw(x, w, g), -14, zce, 8)
         ref = orc.bn_infer(zz, zce, gq, bq, state, cfg)
         assert np.array_equal(H(a), ref) and ev(ae) == state["a_exp"]
+
+
+# Transposed convolutions of the FCN decoder (the adjoint of a conv): the
+# forward is backward-data, the input error a forward conv, the weight
+# gradient pairs the node's input with its output error; 21 classes
+@pytest.mark.parametrize("s", [(2, 8, 8, 21, 21, 4, 2, 1), (1, 8, 8, 21, 21, 16, 8, 4), (2, 5, 7, 150, 150, 4, 2, 1),
+                               (1, 6, 5, 12, 20, 3, 2, 1)], ids=str)
+def test_transposed_conv(orc, dev, s):
+    from paper_2011_14504_amd import iseg
+    N, h, w, cin, cout, R, st, pad = s
+    H = (h - 1) * st - 2 * pad + R
+    W = (w - 1) * st - 2 * pad + R
+    g = (N, H, W, cout, cin, R, R, st, st, pad, pad, 1, 1)      # the conv it is the adjoint of
+    a = synth.int_codes(1400, (N, h, w, cin))
+    wt = synth.int_codes(1401, (cin, R, R, cout))
+    dz = synth.int_codes(1402, (N, H, W, cout))
+    y, ye = iseg.conv_bwd_data(T(a, dev), E(-5, dev), T(wt, dev), E(-7, dev), (N, H, W, cout), st, pad, 1)
+    ry, rye = orc.conv_bwd_data(a, -5, wt, -7, g)
+    assert np.array_equal(H_(y), ry) and ev(ye) == rye
+    e, ee = iseg.conv_fwd(T(dz, dev), E(-20, dev), T(wt, dev), E(-7, dev), st, pad, 1)
+    re_, ree = orc.conv_fwd(dz, -20, wt, -7, g)
+    assert np.array_equal(H_(e), re_) and ev(ee) == ree
+    G, Ge = iseg.conv_bwd_weight(T(a, dev), E(-5, dev), T(dz, dev), E(-20, dev), (cin, R, R, cout), st, pad, 1,
+                                 g_mode=iseg.ISEG_G_DROP, seed=9, tensor_id=32, step=1)
+    rG, rGe = orc.conv_bwd_weight(a, -5, dz, -20, g, 8, False, 9, 32, 1)
+    assert np.array_equal(H_(G), rG) and ev(Ge) == rGe
+
+
+def H_(t):
+    return t.cpu().numpy().astype(np.int64)
+
+
+@pytest.mark.parametrize("shape", [(1, 6, 5, 3), (2, 64, 48, 21), (1, 128, 128, 150)], ids=str)
+@pytest.mark.parametrize("y_exp", [-6, 1, -30])
+def test_mse_onehot(orc, dev, shape, y_exp):
+    from paper_2011_14504_amd import iseg
+    N, Hh, W, K = shape
+    y = synth.int_codes(1500 + K, shape)
+    lab = synth.labels(1501 + K, (N, Hh, W), K)
+    st = torch_zeros_status(dev)
+    loss, e, ee = iseg.mse_onehot(T(y, dev), E(y_exp, dev), T(lab, dev), status=st)
+    rl, rc, rce = orc.mse_onehot(y, y_exp, lab)
+    assert int(st.item()) == 0
+    assert abs(float(loss.item()) - rl) <= 1e-12 * rl
+    assert np.array_equal(H_(e), rc) and ev(ee) == rce

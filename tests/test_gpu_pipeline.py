@@ -56,7 +56,7 @@ def _run_both(wl, steps=1, **widths):
         if "input" in orec:
             _cmp(grec["input"]["e_out"], orec["input"]["e_out"], f"step {s} input error")
             assert _ev(grec["input"]["e_out_exp"]) == orec["input"]["e_out_exp"]
-        if wl["loss"] == "softmax_ce":
+        if wl["loss"] in ("softmax_ce", "mse"):
             gl = float(gnet.loss.item())
             assert abs(gl - onet.loss) <= 1e-12 * abs(onet.loss), (gl, onet.loss)
         for name in gnet.convs:
@@ -195,3 +195,13 @@ def test_vgg16_blocks12_inference_with_frozen_state():
             (gc, ge), (oc, oe) = gi[nd["name"]], oi[nd["name"]]
             _cmp(gc, oc, nd["name"])
             assert _ev(ge) == oe, nd["name"]
+
+
+# FCN8s-VGG16 (no BN, Eq. 18): transposed convs initialised as bilinear
+# upsampling, score fusions without ReLU, the MSE loss
+def test_fcn8s_vgg16_64px_two_steps():
+    _run_both(synth.scaled(synth.FCN8S_VGG16, 1, 64, 64), steps=2, gq=2)
+
+
+def test_fcn8s_vgg16_ragged_96x160():
+    _run_both(synth.scaled(synth.FCN8S_VGG16, 2, 96, 160), gq=2)

@@ -52,10 +52,19 @@ def test_host_validation_without_device(lib):
     g = iseg.geom(1, 8, 8, 16, 16, 3, 3, 1, 1, 1)
     assert lib.iseg_conv_fwd(None, None, None, None, C.byref(g), 7, None, None, None, 0, None,
                              None) == iseg.ISEG_ERR_ARG
-    big = iseg.geom(1, 8, 8, 20000, 16, 3, 3, 1, 1, 1)   # reduction too long for exact int32
     one = C.c_void_p(1)
-    assert lib.iseg_conv_fwd(one, one, one, one, C.byref(big), 0, one, one, one, 1 << 40, None,
+    # raw int32 sums of a reduction longer than 131071 products: refused; final
+    # codes split it into at most 8 channel chunks, refused beyond that
+    big = iseg.geom(1, 8, 8, 20000, 16, 3, 3, 1, 1, 1)
+    assert lib.iseg_conv_fwd(one, one, one, one, C.byref(big), iseg.ISEG_OUT_RAW, one, one, one, 1 << 40, None,
                              None) == iseg.ISEG_ERR_UNSUPPORTED
+    huge = iseg.geom(1, 8, 8, 120000, 16, 3, 3, 1, 1, 1)
+    assert lib.iseg_conv_fwd(one, one, one, one, C.byref(huge), iseg.ISEG_OUT_Q8, one, one, one, 1 << 40, None,
+                             None) == iseg.ISEG_ERR_UNSUPPORTED
+    assert lib.iseg_conv_bwd_data(one, one, one, one, C.byref(iseg.geom(1, 8, 8, 16, 120000, 3, 3, 1, 1, 1)),
+                                  iseg.ISEG_OUT_Q8, one, one, one, 1 << 40, None, None) == iseg.ISEG_ERR_UNSUPPORTED
+    assert lib.iseg_conv_fwd_ws(C.byref(huge), iseg.ISEG_OUT_Q8) == 0
+    assert lib.iseg_conv_fwd_ws(C.byref(big), iseg.ISEG_OUT_Q8) > 0
     assert lib.iseg_conv_fwd(one, one, one, one, C.byref(g), 0, one, one, one, 16, None,
                              None) == iseg.ISEG_ERR_WORKSPACE
     cfg = iseg.bn_cfg(k_A=9)

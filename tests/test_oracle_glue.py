@@ -247,3 +247,27 @@ def test_softmax_ce_gradient_sums_to_zero_over_classes(orc):
     labels = synth.labels(64, (1, 64, 64), 21)
     _, grad = orc.softmax_ce(logits, -5, labels)
     assert np.max(np.abs(grad.sum(axis=-1))) < 1e-17
+
+
+def test_mse_onehot_loss_and_error(orc):
+    """The MSE loss against one-hot labels: the loss equals torch's float64
+    mse_loss of the same values, its gradient torch's autograd, and the E1
+    codes are SQ8 of the exact gradient 2 (y - t) / D (Fractions)."""
+    import torch
+    import bruteforce as bf
+    from fractions import Fraction as Fr
+    for (N, H, W, K, e) in ((1, 3, 4, 5, -3), (2, 5, 3, 7, 1), (1, 2, 2, 3, -9)):
+        y = synth.int_codes(500 + K, (N, H, W, K))
+        lab = synth.labels(600 + K, (N, H, W), K)
+        loss, codes, ce = orc.mse_onehot(y, e, lab)
+        yt = torch.tensor(y.astype(np.float64) * 2.0 ** e, requires_grad=True)
+        t = torch.nn.functional.one_hot(torch.from_numpy(lab.astype(np.int64)), K).double()
+        ref = torch.nn.functional.mse_loss(yt, t)
+        ref.backward()
+        assert abs(loss - ref.item()) <= 1e-12 * ref.item()
+        D = y.size
+        exact = [(Fr(int(v)) * Fr(2) ** e - int(k == l)) * Fr(2, D)
+                 for v, k, l in zip(y.ravel(), np.tile(np.arange(K), N * H * W), np.repeat(lab.ravel(), K))]
+        assert np.allclose([float(v) for v in exact], yt.grad.numpy().ravel(), rtol=1e-12, atol=0)
+        q = bf.SQ(exact, 8)
+        assert [Fr(int(c)) * Fr(2) ** ce for c in codes.ravel()] == q

@@ -223,3 +223,30 @@ def test_inference_on_the_calibration_batch_equals_training_forward():
     for nd in wl["nodes"]:
         codes, e = inf[nd["name"]]
         assert np.array_equal(codes, rec[nd["name"]]["a_out"]) and e == rec[nd["name"]]["a_out_exp"], nd["name"]
+
+
+TINY_DECODER = dict(id=6, name="tiny-fcn-decoder", N=1, H=6, W=6, C=4, input_grad=False, loss="mse",
+                    classes=3, gq=2,
+                    nodes=[synth.conv("c1", "input", 4, 6, 3, 2, 1, bn=False),
+                           synth.conv("s1", "c1", 6, 3, 1, bn=False, relu=False),
+                           synth.deconv("up", "s1", 3, 3, 4, 2, 1),
+                           synth.conv("s0", "input", 4, 3, 1, bn=False, relu=False),
+                           synth.add("fuse", "up", "s0")])
+
+
+def test_decoder_two_steps_match_bruteforce():
+    """A transposed conv initialised as bilinear upsampling, a score fusion
+    without ReLU, the MSE loss and Eq. 18's gradients: two steps of OracleNet
+    against the brute force, every tensor and master."""
+    from oracle.model import OracleNet
+    wl = TINY_DECODER
+    inp = synth.workload_inputs(wl)
+    onet = OracleNet(wl, inp, gq=2)
+    bnet = B.Net(wl, inp, dict(onet.cfg), gq=2)
+    for s in range(2):
+        orec = onet.step()
+        brec, bloss = B.decoder_step(bnet, inp["x"], inp["x_exp"], inp["labels"], 3)
+        for nd in wl["nodes"]:
+            _compare_node(orec[nd["name"]], brec[nd["name"]], f"step {s} {nd['name']}")
+        assert abs(onet.loss - float(bloss)) <= 1e-12 * float(bloss)
+        _compare_params(onet, bnet, 24, 8, onet.cfg)
