@@ -25,13 +25,13 @@
  * owns all memory.  The library never allocates: scratch space comes from a
  * caller workspace `ws` of at least the size returned by the matching
  * iseg_*_ws() query (256-byte aligned).  Inputs and outputs must not alias.
- * The workspace of iseg_bn_bwd begins with arrival counters
+ * The workspaces of iseg_bn_fwd and iseg_bn_bwd begin with arrival counters
  * (ISEG_BN_WS_ZERO(C) bytes) that must be zero before the first call with
- * that buffer: zero it once when it is allocated.  Every iseg_bn_bwd call
- * leaves them zero again, so a buffer kept for those calls on one stream
- * stays ready; a buffer that other entry points also use must be zeroed again
- * before the next iseg_bn_bwd call, and calls that may run at the same time
- * need buffers of their own.
+ * that buffer: zero it once when it is allocated.  Every iseg_bn_fwd /
+ * iseg_bn_bwd call leaves them zero again, so a buffer kept for those calls
+ * on one stream stays ready; a buffer that other entry points also use must
+ * be zeroed again before the next L1BN call, and calls that may run at the
+ * same time need buffers of their own.
  *
  * Streams.  Every compute call only enqueues work on `stream` (0 = the null
  * stream) and returns; results are ready when the stream reaches that point.
@@ -93,8 +93,8 @@ enum iseg_out_mode { ISEG_OUT_Q8 = 0, ISEG_OUT_RAW = 1 };
  * returns the exact int64 sums */
 enum iseg_g_mode { ISEG_G_KEEP = 0, ISEG_G_DROP = 1, ISEG_G_RAW = 2 };
 
-/* bytes of arrival counters at the head of a BN backward workspace for C
- * channels */
+/* bytes of arrival counters at the head of an L1BN (iseg_bn_fwd /
+ * iseg_bn_bwd) workspace for C channels */
 #define ISEG_BN_WS_ZERO(C) ((((size_t)(C) + 511) / 256) * 256)
 
 /* Convolution geometry.  Input NHWC [N,H,W,C]; weights KRSC [K,R,S,C];
@@ -272,13 +272,14 @@ int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,
 /* iseg_bn_fwd_noalloc -- iseg_bn_fwd for callers that cannot allocate
  * device memory (code under graph capture, serving loops, harnesses that
  * forbid hipMalloc): the same computation and outputs, with the workspace in
- * a static device array of iseg_bn_fwd_noalloc_max_bytes() bytes (8 MiB,
+ * a static device array of iseg_bn_fwd_noalloc_max_bytes() bytes (1 MiB,
  * one per GPU, held until the process ends) instead of a caller buffer.
- * Enough for every C <= 2048 at any M; a shape whose iseg_bn_fwd_ws()
+ * Enough for every C <= 32768 at any M; a shape whose iseg_bn_fwd_ws()
  * exceeds it returns ISEG_ERR_WORKSPACE before anything is enqueued.  Every
  * call on a GPU uses that GPU's one array: calls that overlap on one GPU
  * (other streams, other threads) race and must be serialized by the caller.
- * Nothing has to be cleared between calls.  Allocates nothing (no hipMalloc,
+ * Nothing has to be cleared between calls: the array starts at zero and
+ * every call leaves its arrival counters at zero.  Allocates nothing (no hipMalloc,
  * no library routine that allocates); the array's device address is looked
  * up once per device on the first call there (ISEG_ERR_DEVICE if that
  * fails). */

@@ -10,24 +10,28 @@
 //     written as one partial per block and channel (no global atomics, so no
 //     same-address serialization across blocks);
 //   * finalize steps that reduce the partials and do the exact rational
-//     arithmetic in __int128 once per channel or per table entry: per-channel
-//     kernels (one block per channel) in the forward; in the backward the
-//     per-channel step runs in the tail of the streaming pass, in the last
+//     arithmetic in __int128 once per channel or per table entry.  The
+//     per-channel step runs in the tail of a streaming pass, in the last
 //     block of each channel slice to finish (an arrival counter picks it, no
-//     block waits), and the grid-wide maximum in the last slice to finish.
+//     block waits), and grid-wide maxima in the last slice to finish; the
+//     per-(channel, code) tables take one block per channel.
 // sgn(x - mu_q) and the ReLU mask are monotone in the input code, so the
 // streaming passes get them from two thresholds per channel instead of a
 // table.
 //
-// Forward:  stats1 (sum q, min q, max q) -> finmu -> stats2 (sum |x - mu_q|)
-//           -> finsig (n_sigma, den, max|xhat| exponent) -> fin2 (xhat codes,
-//           y, thresholds, max|y|) -> fin3 (A codes) -> apply (table gather).
+// Forward:  stats1 (sum q, min q, max q | tails: n_mu) -> stats2 (sum
+//           |x - mu_q| | tails: n_sigma, den, the slice's bound on b) -> fin2
+//           (b; xhat codes, y, thresholds, max|y|) -> fin3 (A codes) -> apply
+//           (table gather).
 // Backward: stats (sum delta, sum delta*xhat, sum sgn, per-class extremes of
-//           delta | tails: dgamma, dbeta, then for k_E2 >= 15 E1's exponent)
-//           -> table -> apply (gather).  k_E2 < 15 adds a second streaming
-//           pass: stats tails give max|gamma delta| (E2's scale), stats2 sums
-//           the rounded E2 terms and its tails give E1's exponent.
+//           delta | tails: dgamma, dbeta and, for k_E2 >= 15, each slice's
+//           bound on E1's exponent) -> table (E1's exponent from the slices'
+//           bounds) -> apply (gather).  k_E2 < 15 adds a second streaming
+//           pass: stats tails give each slice's max|gamma delta| (E2's scale
+//           is the largest), stats2 sums the rounded E2 terms and its tails
+//           give the slices' bounds on E1's exponent.
 #include <mutex>
+#include <type_traits>
 
 #include "iseg_common.h"
 
@@ -46,7 +50,7 @@ constexpr int kSentinelLo = -(1 << 30);
 #define ISEG_BNF_STATS_CPL 4     // channels per lane of the forward statistics
 #endif
 #ifndef ISEG_BNB_ROWS
-#define ISEG_BNB_ROWS 8          // row groups per lane that size the backward grid
+#define ISEG_BNB_ROWS 2          // row groups per lane that size the backward statistics grid
 #endif
 constexpr int kMaxBlocks = ISEG_BN_BLOCKS;
 
@@ -109,6 +113,7 @@ int pick_cs(int64_t C, int csmax)
 }
 
 constexpr int kNT = ISEG_BN_NT;
+constexpr int kWaves = kNT / 64;       // waves per streaming block
 
 Stream make_stream(int64_t M, int64_t C, int cs, int cpl, int unroll, int max_blocks)
 {
@@ -244,15 +249,68 @@ struct OpAdd { template <typename T> __device__ T operator()(T a, T b) const { r
 struct OpMin { template <typename T> __device__ T operator()(T a, T b) const { return a < b ? a : b; } };
 struct OpMax { template <typename T> __device__ T operator()(T a, T b) const { return a > b ? a : b; } };
 
-// Lanes of a wave that hold the same channels are G apart.  When G is a power
-// of two dividing 64, fold them with xor-shuffles so that only lanes < G of
-// each wave carry the wave's total into LDS (fewer same-address LDS atomics).
-template <typename T, typename Op>
-__device__ __forceinline__ T group_fold(T v, int G, Op op)
+// v op v[lane ^ O]: for O = 16 or 32 with gfx950's cross-row swaps (VALU, no
+// LDS traffic): v_permlane16_swap / v_permlane32_swap with both operands v
+// leave v and its partner's value in the two results (which is which depends
+// on the lane, so only commutative ops are folded); other O: an xor-shuffle.
+template <int O>
+__device__ __forceinline__ uint32_t lane_x32(uint32_t v, uint32_t* partner)
 {
-    if ((G & (G - 1)) != 0 || G > 64) return v;
-    for (int o = G; o < 64; o <<= 1) v = op(v, (T)__shfl_xor(v, o, 64));
-    return v;
+    if constexpr (O == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        *partner = r[1];
+        return r[0];
+    } else {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        *partner = r[1];
+        return r[0];
+    }
+}
+
+template <int O, typename T, typename Op>
+__device__ __forceinline__ T xor_fold(T v, Op op)
+{
+    if constexpr (O != 16 && O != 32) {
+        return op(v, (T)__shfl_xor(v, O, 64));
+    } else if constexpr (sizeof(T) == 8) {
+        const uint64_t u = (uint64_t)v;
+        uint32_t lp, hp;
+        const uint32_t la = lane_x32<O>((uint32_t)u, &lp);
+        const uint32_t ha = lane_x32<O>((uint32_t)(u >> 32), &hp);
+        return op((T)((uint64_t)la | ((uint64_t)ha << 32)), (T)((uint64_t)lp | ((uint64_t)hp << 32)));
+    } else {
+        uint32_t p;
+        const uint32_t a = lane_x32<O>((uint32_t)v, &p);
+        return op((T)a, (T)p);
+    }
+}
+
+// Lanes of a wave that hold the same channels are G apart (G a power of two
+// dividing 64): fold them so that every lane holds the total over the wave's
+// lanes of its channels (straight-line code for a compile-time G; G = 0 or 64:
+// nothing to fold).  Every lane of the wave must be active.
+template <int G, typename T, typename Op>
+__device__ __forceinline__ T fold_g(T v, Op op)
+{
+    if constexpr (G >= 1 && G < 64) return fold_g<2 * G>(xor_fold<G>(v, op), op);
+    else return v;
+}
+
+// f(std::integral_constant<int, G>) for a slice whose row has G lanes: G
+// itself when it is a power of two up to 64 (compile-time folds), else 0.
+template <typename F>
+__device__ __forceinline__ void with_g(int G, F f)
+{
+    switch (G) {
+    case 1: f(std::integral_constant<int, 1>()); break;
+    case 2: f(std::integral_constant<int, 2>()); break;
+    case 4: f(std::integral_constant<int, 4>()); break;
+    case 8: f(std::integral_constant<int, 8>()); break;
+    case 16: f(std::integral_constant<int, 16>()); break;
+    case 32: f(std::integral_constant<int, 32>()); break;
+    case 64: f(std::integral_constant<int, 64>()); break;
+    default: f(std::integral_constant<int, 0>()); break;
+    }
 }
 
 __device__ __forceinline__ bool group_leader(int G)
@@ -356,23 +414,23 @@ __device__ __forceinline__ T block_max_nt(T v, T* sh)
 }
 
 // ---------------------------------------------------------------------------
-// forward workspace
+// forward workspace.  It starts, like the backward's, with ctr_bytes(C)
+// bytes of arrival counters that each call leaves at zero.
 // ---------------------------------------------------------------------------
 struct FwdWs {
-    int32_t* b_glob;                 // exponent of Q_xhat's scale (written by fin2)
-    unsigned long long* maxY;        // unused (kept for the layout)
-    int32_t *p_s1, *p_min, *p_max;   // [gx][C] partials
+    uint32_t* ctr;                   // arrival counters
+    int32_t* b_glob;                 // exponent of Q_xhat's scale (fin2, block 0)
+    int32_t *p_s1, *p_mm;            // [gx][C] partials: sum q; (min q + 128) | (max q + 128) << 16
     long long* p_abs;                // [gx][C]
-    long long* Y;                    // [C][256] y on the grid 2^e_y (before ReLU)
-    unsigned long long* maxYc;       // [C] max |ReLU(y)| of channel c over its occupied codes
-    int32_t* bcand;                  // [C] channel candidates for b
+    int32_t* sbmax;                  // [slices] largest channel bound on b of each slice (stats2's tails)
+    unsigned long long* maxYc;       // [C] max |ReLU(y)| of channel c over its occupied codes (fin2)
 };
 
 size_t fwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C;
-    return 256 + 3 * align256(pc * 4) + align256(pc * 8) + align256((size_t)st.C * 256 * 8) +
-           align256((size_t)st.C * 8) + align256((size_t)st.C * 4);
+    return ctr_bytes(st.C) + 256 + 2 * align256(pc * 4) + align256(pc * 8) + align256((size_t)st.C) +
+           align256((size_t)st.C * 8);
 }
 
 FwdWs fwd_ws_map(void* base, const Stream& st)
@@ -380,27 +438,47 @@ FwdWs fwd_ws_map(void* base, const Stream& st)
     char* p = (char*)base;
     size_t pc = (size_t)st.gx * st.C;
     FwdWs w;
+    w.ctr = (uint32_t*)p; p += ctr_bytes(st.C);
     w.b_glob = (int32_t*)p;
-    w.maxY = (unsigned long long*)(p + 64);
     p += 256;
     w.p_s1 = (int32_t*)p; p += align256(pc * 4);
-    w.p_min = (int32_t*)p; p += align256(pc * 4);
-    w.p_max = (int32_t*)p; p += align256(pc * 4);
+    w.p_mm = (int32_t*)p; p += align256(pc * 4);
     w.p_abs = (long long*)p; p += align256(pc * 8);
-    w.Y = (long long*)p; p += align256((size_t)st.C * 256 * 8);
-    w.maxYc = (unsigned long long*)p; p += align256((size_t)st.C * 8);
-    w.bcand = (int32_t*)p;
+    w.sbmax = (int32_t*)p; p += align256((size_t)st.C);       // slices <= C / 4
+    w.maxYc = (unsigned long long*)p;
     return w;
 }
 
 // ---------------------------------------------------------------------------
 // forward kernels
+//
+// stats1 | tails: n_mu and the occupied code range of each channel of the slice
+// stats2 | tails: n_sigma, the denominator and each channel's bound on
+//          max|xhat|; the slice's largest bound
+// fin2   (one block per channel, one thread per code): b (Q_xhat's scale) from
+//          the slices' bounds; xhat codes, y, sgn / ReLU thresholds, the
+//          backward's entries and the channel's max|ReLU(y)|
+// fin3   (likewise): Q_A's shift r from the channels' maxima; A codes
+// apply  (table gather)
 // ---------------------------------------------------------------------------
+
+// Partial rows of a slice tail in flight per thread: the thread of channel
+// t % CS in row group t / CS reduces partial rows t / CS + k ng (ng = kNT /
+// CS), kTailU of them per batch, all loads of a batch issued before the first
+// is used (an index past the last row re-reads the group's first row, whose
+// value the reduction ignores).
+constexpr int kTailU = 8;
+
 template <int CPL>
-__global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ x, Stream st, FwdWs w)
+__global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ x, const int32_t* x_exp,
+                                                    Stream st, FwdWs w, Saved sv, BnCfg cf)
 {
     __shared__ int32_t sS[128], sMin[128], sMax[128];
-    if ((int)threadIdx.x < st.CS) { sS[threadIdx.x] = 0; sMin[threadIdx.x] = 1000; sMax[threadIdx.x] = -1000; }
+    __shared__ long long tS[kNT];
+    __shared__ int32_t tMm[kNT];
+    __shared__ int32_t wst[3 * kWaves * 128];      // wave totals [quantity][wave][channel]
+    const bool fold = (st.G & (st.G - 1)) == 0 && st.G <= 64;
+    if (!fold && (int)threadIdx.x < st.CS) { sS[threadIdx.x] = 0; sMin[threadIdx.x] = 1000; sMax[threadIdx.x] = -1000; }
     __syncthreads();
     int g, rsub;
     const bool active = stream_lane(st, g, rsub);
@@ -419,13 +497,41 @@ __global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ 
             }
         });
     }
+    with_g(st.G, [&](auto gc) {
+        constexpr int GG = decltype(gc)::value;
 #pragma unroll
-    for (int i = 0; i < CPL; i++) {
-        s[i] = group_fold(s[i], st.G, OpAdd());
-        mn[i] = group_fold(mn[i], st.G, OpMin());
-        mx[i] = group_fold(mx[i], st.G, OpMax());
-    }
-    if (active && group_leader(st.G)) {
+        for (int i = 0; i < CPL; i++) {
+            s[i] = fold_g<GG>(s[i], OpAdd());
+            mn[i] = fold_g<GG>(mn[i], OpMin());
+            mx[i] = fold_g<GG>(mx[i], OpMax());
+        }
+    });
+    // block totals: the 16 wave totals of each channel staged in LDS and summed
+    // by one thread per channel (see k_bnb_stats); other widths: LDS atomics
+    if (fold) {
+        const int wv = threadIdx.x >> 6;
+        if ((int)(threadIdx.x & 63) < st.G) {
+#pragma unroll
+            for (int i = 0; i < CPL; i++) {
+                const int c = g * CPL + i;
+                wst[wv * 128 + c] = s[i];
+                wst[(kWaves + wv) * 128 + c] = mn[i];
+                wst[(2 * kWaves + wv) * 128 + c] = mx[i];
+            }
+        }
+        __syncthreads();
+        if ((int)threadIdx.x < st.CS) {
+            const int c = threadIdx.x;
+            int bs = 0, bmn = 1000, bmx = -1000;
+#pragma unroll 4
+            for (int v = 0; v < kWaves; v++) {
+                bs += wst[v * 128 + c];
+                bmn = min(bmn, wst[(kWaves + v) * 128 + c]);
+                bmx = max(bmx, wst[(2 * kWaves + v) * 128 + c]);
+            }
+            sS[c] = bs; sMin[c] = bmn; sMax[c] = bmx;
+        }
+    } else if (active && group_leader(st.G)) {
 #pragma unroll
         for (int i = 0; i < CPL; i++) {
             atomicAdd(&sS[g * CPL + i], s[i]);
@@ -434,57 +540,98 @@ __global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ 
         }
     }
     __syncthreads();
+    // every block holds at least one row of the slice, so its extremes are codes
     if ((int)threadIdx.x < st.CS) {
         int64_t o = (int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x;
-        w.p_s1[o] = sS[threadIdx.x];
-        w.p_min[o] = sMin[threadIdx.x];
-        w.p_max[o] = sMax[threadIdx.x];
+        st_x(&w.p_s1[o], sS[threadIdx.x]);
+        st_x(&w.p_mm[o], (sMin[threadIdx.x] + 128) | ((sMax[threadIdx.x] + 128) << 16));
+    }
+    if (!arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) return;
+    // slice tail: sum, min and max of each channel over the slice's partial rows
+    const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
+    const int64_t cb = (int64_t)blockIdx.y * CS;
+    long long sum = 0;
+    int lo = 255, hi = 0;
+    if (grp < ng)
+        for (int b0 = grp; b0 < st.gx; b0 += kTailU * ng) {
+            int32_t vs[kTailU], vm[kTailU];
+#pragma unroll
+            for (int u = 0; u < kTailU; u++) {
+                const int b = b0 + u * ng;
+                const int64_t q = (int64_t)(b < st.gx ? b : b0) * st.C + cb + ch;
+                vs[u] = ld_x(&w.p_s1[q]);
+                vm[u] = ld_x(&w.p_mm[q]);
+            }
+#pragma unroll
+            for (int u = 0; u < kTailU; u++) {
+                if (b0 + u * ng < st.gx) sum += vs[u];
+                lo = min(lo, vm[u] & 0xffff);           // a repeated row changes no extreme
+                hi = max(hi, vm[u] >> 16);
+            }
+        }
+    tS[t] = sum;
+    tMm[t] = lo | (hi << 16);
+    __syncthreads();
+    if (t < CS) {
+        for (int g2 = 1; g2 < ng; g2++) {
+            const int i = g2 * CS + t;
+            sum += tS[i];
+            lo = min(lo, tMm[i] & 0xffff);
+            hi = max(hi, tMm[i] >> 16);
+        }
+        const int32_t s_x = *x_exp;
+        int32_t nm = 0;
+        if (sx_ok(s_x))   // mu/2 = S1 2^(s_x - 1) / M, code floor(mu/2 2^(k_mu-1) + 1/2)
+            nm = (int32_t)clamp_k128(rhu128((i128)sum, s_x - 1 + (cf.k_mu - 1), (i128)st.M), cf.k_mu);
+        const int64_t c = cb + t;
+        sv.n_mu[c] = nm;
+        sv.qmin[c] = lo - 128;
+        sv.qmax[c] = hi - 128;
     }
 }
 
-// per channel: reduce the stats1 partials, n_mu (Eq. 14), occupancy range
-__global__ __launch_bounds__(256) void k_bnf_finmu(const int32_t* x_exp, Stream st, FwdWs w, Saved sv,
-                                                   BnCfg cf)
-{
-    __shared__ long long sh64[256];
-    __shared__ int32_t sh32[256];
-    const int c = blockIdx.x;
-    long long s = 0;
-    int mn = 1000, mx = -1000;
-    for (int b = threadIdx.x; b < st.gx; b += 256) {
-        int64_t o = (int64_t)b * st.C + c;
-        s += w.p_s1[o];
-        mn = w.p_min[o] < mn ? w.p_min[o] : mn;
-        mx = w.p_max[o] > mx ? w.p_max[o] : mx;
-    }
-    s = block_reduce(s, OpAdd(), sh64);
-    mn = block_reduce(mn, OpMin(), sh32);
-    mx = block_reduce(mx, OpMax(), sh32);
-    if (threadIdx.x == 0) {
-        int32_t s_x = *x_exp;
-        int32_t nm = 0;
-        if (sx_ok(s_x))   // mu/2 = S1 2^(s_x - 1) / M, code floor(mu/2 2^(k_mu-1) + 1/2)
-            nm = (int32_t)clamp_k128(rhu128((i128)s, s_x - 1 + (cf.k_mu - 1), (i128)st.M), cf.k_mu);
-        sv.n_mu[c] = nm;
-        sv.qmin[c] = mn;
-        sv.qmax[c] = mx;
-        sv.t0[c] = 128; sv.p0[c] = 128; sv.mlo[c] = 128; sv.mhi[c] = -129;
+// y on the grid 2^e_y of a channel's code q (before ReLU), and x-hat's code
+struct FwdExps {
+    int e_mu, e_sig, gg, e_g, e_b, e_xh, e_y, kx;
+};
 
-    }
+__device__ __forceinline__ FwdExps fwd_exps(int32_t s_x, int b, const BnCfg& cf)
+{
+    FwdExps e;
+    e.e_mu = 2 - cf.k_mu; e.e_sig = 2 - cf.k_sigma;
+    e.gg = s_x < e.e_mu ? s_x : e.e_mu;
+    e.e_g = 2 - cf.k_gamma; e.e_b = 2 - cf.k_beta;
+    e.kx = cf.k_xhat;
+    e.e_xh = b - (cf.k_xhat - 1);
+    e.e_y = (e.e_g + e.e_xh) < e.e_b ? (e.e_g + e.e_xh) : e.e_b;
+    return e;
+}
+
+__device__ __forceinline__ i128 fwd_xcode(int64_t D, int32_t den, int b, const FwdExps& e)
+{
+    return clamp_k128(rhu128((i128)D, e.gg - e.e_sig + (e.kx - 1) - b, (i128)den), e.kx);
+}
+
+__device__ __forceinline__ i128 fwd_y(i128 nx, int gq, int bq, const FwdExps& e)
+{
+    return (i128)gq * nx * pow2_128(e.e_g + e.e_xh - e.e_y) + (i128)bq * pow2_128(e.e_b - e.e_y);
 }
 
 template <int CPL>
 __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ x, const int32_t* x_exp,
-                                                    Stream st, FwdWs w, Saved sv, BnCfg cf,
-                                                    int32_t* dev_status)
+                                                    Stream st, FwdWs w, Saved sv, BnCfg cf, int32_t* dev_status)
 {
     __shared__ unsigned long long sA[128];
+    __shared__ long long tA[kNT];
+    __shared__ int32_t rb[kNT / 64];
+    __shared__ long long wst[kWaves * 128];        // wave totals [wave][channel]
+    const bool fold = (st.G & (st.G - 1)) == 0 && st.G <= 64;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) {
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) set_status(dev_status, ISEG_DEV_RANGE);
         s_x = -14;     // keep shifts defined; outputs are unspecified
     }
-    if ((int)threadIdx.x < st.CS) sA[threadIdx.x] = 0;
+    if (!fold && (int)threadIdx.x < st.CS) sA[threadIdx.x] = 0;
     __syncthreads();
     const int e_mu = 2 - cf.k_mu;
     int g, rsub;
@@ -507,87 +654,119 @@ __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ 
             }
         });
     }
+    with_g(st.G, [&](auto gc) {
+        constexpr int GG = decltype(gc)::value;
 #pragma unroll
-    for (int i = 0; i < CPL; i++) a[i] = group_fold(a[i], st.G, OpAdd());
-    if (active && group_leader(st.G)) {
+        for (int i = 0; i < CPL; i++) a[i] = fold_g<GG>(a[i], OpAdd());
+    });
+    if (fold) {
+        const int wv = threadIdx.x >> 6;
+        if ((int)(threadIdx.x & 63) < st.G) {
+#pragma unroll
+            for (int i = 0; i < CPL; i++) wst[wv * 128 + g * CPL + i] = a[i];
+        }
+        __syncthreads();
+        if ((int)threadIdx.x < st.CS) {
+            long long ba = 0;
+#pragma unroll 4
+            for (int v = 0; v < kWaves; v++) ba += wst[v * 128 + threadIdx.x];
+            sA[threadIdx.x] = (unsigned long long)ba;
+        }
+    } else if (active && group_leader(st.G)) {
 #pragma unroll
         for (int i = 0; i < CPL; i++) atomicAdd(&sA[g * CPL + i], (unsigned long long)a[i]);
     }
     __syncthreads();
     if ((int)threadIdx.x < st.CS)
-        w.p_abs[(int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x] = (long long)sA[threadIdx.x];
-}
-
-// per channel: sigma (Eq. 13-14), denominator, this channel's bound on max|xhat|
-__global__ __launch_bounds__(256) void k_bnf_finsig(const int32_t* x_exp, Stream st, FwdWs w, Saved sv,
-                                                    BnCfg cf)
-{
-    __shared__ long long sh64[256];
-    const int c = blockIdx.x;
-    long long a = 0;
-    for (int b = threadIdx.x; b < st.gx; b += 256) a += w.p_abs[(int64_t)b * st.C + c];
-    a = block_reduce(a, OpAdd(), sh64);
-    if (threadIdx.x != 0) return;
-    w.bcand[c] = kSentinelLo;
-    int32_t s_x = *x_exp;
-    if (!sx_ok(s_x)) return;
-    const int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
+        st_x(&w.p_abs[(int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x], (long long)sA[threadIdx.x]);
+    if (!arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) return;
+    // slice tail: sigma (Eq. 13-14), the denominator and this channel's bound on max|xhat|
+    const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
+    const int64_t cb = (int64_t)blockIdx.y * CS;
+    const int e_sig = 2 - cf.k_sigma;
     const int gg = s_x < e_mu ? s_x : e_mu;
-    // sigma/2 = sumabs 2^(g-1) / M ; n_sigma = floor(sigma/2 2^(k_sigma-1) + 1/2)
-    int32_t ns = (int32_t)clamp_k128(rhu128((i128)a, gg - 1 + (cf.k_sigma - 1), (i128)st.M), cf.k_sigma);
-    int32_t den = ns + cf.eps_code;
-    if (den < 1) den = 1;
-    sv.n_sigma[c] = ns;
-    sv.den[c] = den;
-    int32_t nm = sv.n_mu[c];
-    int best = kSentinelLo;
-    int qs[2] = {sv.qmin[c], sv.qmax[c]};
-    for (int t = 0; t < 2; t++) {          // xhat is linear in q: extremes at qmin / qmax
-        int64_t D = bn_D(qs[t], s_x, nm, e_mu);
-        if (D == 0) continue;
-        int e = ceil_pow2_exp128(abs128((i128)D), (i128)den) + gg - e_sig;
-        best = e > best ? e : best;
+    {
+        long long acc = 0;
+        if (grp < ng)
+            for (int b0 = grp; b0 < st.gx; b0 += kTailU * ng) {
+                long long va[kTailU];
+#pragma unroll
+                for (int u = 0; u < kTailU; u++) {
+                    const int b = b0 + u * ng;
+                    va[u] = ld_x(&w.p_abs[(int64_t)(b < st.gx ? b : b0) * st.C + cb + ch]);
+                }
+#pragma unroll
+                for (int u = 0; u < kTailU; u++)
+                    if (b0 + u * ng < st.gx) acc += va[u];
+            }
+        tA[t] = acc;
+        __syncthreads();
+        if (t < CS) {
+            for (int g2 = 1; g2 < ng; g2++) acc += tA[g2 * CS + t];
+            const int64_t c = cb + t;
+            // sigma/2 = sumabs 2^(g-1) / M ; n_sigma = floor(sigma/2 2^(k_sigma-1) + 1/2)
+            int32_t ns = (int32_t)clamp_k128(rhu128((i128)acc, gg - 1 + (cf.k_sigma - 1), (i128)st.M), cf.k_sigma);
+            int32_t den = ns + cf.eps_code;
+            if (den < 1) den = 1;
+            sv.n_sigma[c] = ns;
+            sv.den[c] = den;
+            const int32_t nm = sv.n_mu[c];
+            int best = kSentinelLo;
+            const int qs[2] = {sv.qmin[c], sv.qmax[c]};
+            for (int k = 0; k < 2; k++) {          // xhat is linear in q: extremes at qmin / qmax
+                const int64_t D = bn_D(qs[k], s_x, nm, e_mu);
+                if (D == 0) continue;
+                const int e = ceil_pow2_exp128(abs128((i128)D), (i128)den) + gg - e_sig;
+                best = e > best ? e : best;
+            }
+            tA[t] = best;                          // slot t is read by thread t only above
+        }
     }
-    w.bcand[c] = best;
+    __syncthreads();
+    int bmax = kSentinelLo;
+    for (int i = t; i < CS; i += kNT) bmax = max(bmax, (int)tA[i]);
+    bmax = block_max_nt(bmax, rb);
+    if (t == 0) w.sbmax[blockIdx.y] = bmax;
 }
 
-// per (channel, code): xhat code, y, flags, thresholds; max |ReLU(y)| over the
-// occurring codes (y is monotone in q, so over qmin and qmax)
-__global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w, Saved sv, BnCfg cf,
+// max of n per-slice values, by every thread of the block (kSentinelLo if n = 0)
+__device__ __forceinline__ int32_t slices_max(const int32_t* a, int n, int32_t* sh)
+{
+    int32_t m = kSentinelLo;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) m = max(m, a[i]);
+    for (int o = 32; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 64));
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = sh[0];
+    for (int k = 1; k < (int)(blockDim.x >> 6); k++) m = max(m, sh[k]);
+    return m;
+}
+
+// per (channel, code): xhat code, y, flags and the backward's entry; per
+// channel: the sgn and ReLU thresholds and max |ReLU(y)| over the occupied
+// codes (y is monotone in q, so over qmin and qmax)
+__global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, int nslices, FwdWs w, Saved sv, BnCfg cf,
                                                   const int8_t* gamma_q, const int8_t* beta_q)
 {
+    __shared__ int32_t rsh[4];
     const int c = blockIdx.x;
     const int q = (int)threadIdx.x - 128;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
-    // b: the largest channel candidate (one block max over C values)
-    int b = kSentinelLo;
-    for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) b = w.bcand[k] > b ? w.bcand[k] : b;
-    {
-        __shared__ int32_t rb[4];
-        for (int o = 32; o > 0; o >>= 1) b = max(b, __shfl_xor(b, o));
-        if ((threadIdx.x & 63) == 0) rb[threadIdx.x >> 6] = b;
-        __syncthreads();
-        b = max(max(rb[0], rb[1]), max(rb[2], rb[3]));
-    }
+    int b = slices_max(w.sbmax, nslices, rsh);
     if (b == kSentinelLo) b = 0;
     if (c == 0 && threadIdx.x == 0) *w.b_glob = b;
-    const int e_mu = 2 - cf.k_mu, e_sig = 2 - cf.k_sigma;
-    const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
-    const int e_xh = b - (cf.k_xhat - 1);
-    const int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
-    const int gg = s_x < e_mu ? s_x : e_mu;
-    int64_t D = bn_D(q, s_x, sv.n_mu[c], e_mu);
-    int32_t den = sv.den[c];
-    i128 nx = clamp_k128(rhu128((i128)D, gg - e_sig + (cf.k_xhat - 1) - b, (i128)den), cf.k_xhat);
-    i128 Y = (i128)gamma_q[c] * nx * pow2_128(e_g + e_xh - e_y) + (i128)beta_q[c] * pow2_128(e_b - e_y);
-    int idx = c * 256 + threadIdx.x;
+    const FwdExps e = fwd_exps(s_x, b, cf);
+    const int64_t D = bn_D(q, s_x, sv.n_mu[c], e.e_mu);
+    const i128 nx = fwd_xcode(D, sv.den[c], b, e);
+    const i128 Y = fwd_y(nx, gamma_q[c], beta_q[c], e);
+    const int idx = c * 256 + threadIdx.x;
     sv.xcode[idx] = (int16_t)nx;
-    int sg = (D > 0) - (D < 0);
+    const int sg = (D > 0) - (D < 0);
     sv.flags[idx] = (uint8_t)((Y > 0 ? 1 : 0) | ((sg + 1) << 1));
     sv.btab[c * 256 + (q & 255)] = ((uint32_t)(uint16_t)(int16_t)nx << 16) | ((uint32_t)(sg & 3) << 8) |
                                    ((uint32_t)(sg != 0) << 10) | (Y > 0 ? 1u : 0u);
-    w.Y[idx] = (long long)Y;
     // thresholds (least code with D >= 0, least with D > 0, code range with y > 0)
     // and the channel's max |ReLU(y)| over its occupied code extremes, by block
     // reductions: same-address atomics would serialize 256 updates per channel
@@ -615,29 +794,28 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, FwdWs w,
     }
 }
 
+// A codes per (channel, code) with Q_A's shift from the channels' maxima
 __global__ __launch_bounds__(256) void k_bnf_fin3(const int32_t* x_exp, FwdWs w, Saved sv, BnCfg cf,
-                                                  int32_t* y_exp)
+                                                  const int8_t* gamma_q, const int8_t* beta_q, int32_t* y_exp)
 {
     const int c = blockIdx.x;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) return;
     const int b = *w.b_glob;
-    const int e_g = 2 - cf.k_gamma, e_b = 2 - cf.k_beta;
-    const int e_xh = b - (cf.k_xhat - 1);
-    const int e_y = (e_g + e_xh) < e_b ? (e_g + e_xh) : e_b;
+    const FwdExps e = fwd_exps(s_x, b, cf);
     uint64_t M = 0;                                  // max over the channels' candidates
     for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) M = w.maxYc[k] > M ? w.maxYc[k] : M;
     M = block_max_u64(M);
-    int r = M ? bitlen_u64(M) - (cf.k_A - 1) : 0;
-    int idx = c * 256 + threadIdx.x;
-    long long Y = w.Y[idx];
+    const int r = M ? bitlen_u64(M) - (cf.k_A - 1) : 0;
+    const int idx = c * 256 + threadIdx.x;
+    i128 Y = fwd_y((i128)sv.xcode[idx], gamma_q[c], beta_q[c], e);
     if (cf.relu && Y < 0) Y = 0;
-    sv.acode[idx] = (int8_t)sq_code(Y, r, cf.k_A);
+    sv.acode[idx] = (int8_t)sq_code((long long)Y, r, cf.k_A);
     if (c == 0 && threadIdx.x == 0) {
-        *y_exp = e_y + r;
+        *y_exp = e.e_y + r;
         sv.hdr[0] = b;
-        sv.hdr[1] = e_y;
-        sv.hdr[2] = e_y + r;
+        sv.hdr[1] = e.e_y;
+        sv.hdr[2] = e.e_y + r;
         sv.hdr[3] = s_x;
     }
 }
@@ -672,22 +850,20 @@ __global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x
 // ---------------------------------------------------------------------------
 struct BwdWs {
     uint32_t* ctr;                   // arrival counters
-    int32_t* bdx;                    // exponent of E1's scale (atomicMax)
-    unsigned long long* maxF;        // max |gamma delta|
-    int32_t *p_sd, *p_z;             // [gx][C] partials
+    int32_t* smax;                   // [slices] bound on E1's exponent over each slice's channels
+    int32_t* smaxF;                  // [slices] max |gamma delta| over each slice's channels (rounding E2)
+    int32_t *p_sd, *p_z, *p_mmA, *p_mmB;   // [gx][C] partials (per-class extremes packed as bytes)
     long long *p_sdn, *p_sf, *p_sfn; // [gx][C]
-    int32_t* p_mm;                   // [6][gx][C]: (min, max) delta for sgn = -1, 0, +1
     long long *sd, *sdn, *sf, *sfn;  // [C] reduced
     int32_t *Z, *mm;                 // [C], [C][6]
     int8_t* lut;                     // [C][3][256] dx codes
-    int32_t* cand;                   // [C] exponent candidates of max|dx|
 };
 
 size_t bwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
-    return ctr_bytes(st.C) + 256 + 2 * align256(pc * 4) + 3 * align256(pc * 8) + align256(pc * 24) +
-           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768) + align256(C * 4);
+    return ctr_bytes(st.C) + 2 * align256(C) + 4 * align256(pc * 4) + 3 * align256(pc * 8) +
+           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768);
 }
 
 BwdWs bwd_ws_map(void* base, const Stream& st)
@@ -696,23 +872,22 @@ BwdWs bwd_ws_map(void* base, const Stream& st)
     size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
     BwdWs w;
     w.ctr = (uint32_t*)p; p += ctr_bytes(st.C);
-    w.bdx = (int32_t*)p;
-    w.maxF = (unsigned long long*)(p + 64);
-    p += 256;
+    w.smax = (int32_t*)p; p += align256(C);          // slices <= C / 4
+    w.smaxF = (int32_t*)p; p += align256(C);
     w.p_sd = (int32_t*)p; p += align256(pc * 4);
     w.p_z = (int32_t*)p; p += align256(pc * 4);
+    w.p_mmA = (int32_t*)p; p += align256(pc * 4);
+    w.p_mmB = (int32_t*)p; p += align256(pc * 4);
     w.p_sdn = (long long*)p; p += align256(pc * 8);
     w.p_sf = (long long*)p; p += align256(pc * 8);
     w.p_sfn = (long long*)p; p += align256(pc * 8);
-    w.p_mm = (int32_t*)p; p += align256(pc * 24);
     w.sd = (long long*)p; p += align256(C * 8);
     w.sdn = (long long*)p; p += align256(C * 8);
     w.sf = (long long*)p; p += align256(C * 8);
     w.sfn = (long long*)p; p += align256(C * 8);
     w.Z = (int32_t*)p; p += align256(C * 4);
     w.mm = (int32_t*)p; p += align256(C * 24);
-    w.lut = (int8_t*)p; p += align256(C * 768);
-    w.cand = (int32_t*)p;
+    w.lut = (int8_t*)p;
     return w;
 }
 
@@ -763,6 +938,24 @@ __device__ __forceinline__ void load_bwd_tab(uint32_t* tab, const uint32_t* src,
     }
 }
 
+// Per-class extremes of the masked delta travel between blocks as bytes:
+// low ends as lo + 128 (255 for an empty class), high ends as hi + 128 (0 for
+// an empty class), so a byte-wise min / max merges them and an empty class
+// still reads lo > hi.  A = (lo, hi) of classes -1 and 0, B = (lo, hi) of +1.
+__device__ __forceinline__ uint32_t pk_lo(int v) { return v > 127 ? 255u : (uint32_t)(v + 128); }
+__device__ __forceinline__ uint32_t pk_hi(int v) { return v < -128 ? 0u : (uint32_t)(v + 128); }
+__device__ __forceinline__ void mm_pack(const int* mm, uint32_t& A, uint32_t& B)
+{
+    A = pk_lo(mm[0]) | pk_hi(mm[1]) << 8 | pk_lo(mm[2]) << 16 | pk_hi(mm[3]) << 24;
+    B = pk_lo(mm[4]) | pk_hi(mm[5]) << 8;
+}
+__device__ __forceinline__ void mm_merge(uint32_t A, uint32_t B, int* lo3, int* hi3)
+{
+    lo3[0] = min(lo3[0], (int)(A & 0xff)); hi3[0] = max(hi3[0], (int)((A >> 8) & 0xff));
+    lo3[1] = min(lo3[1], (int)((A >> 16) & 0xff)); hi3[1] = max(hi3[1], (int)(A >> 24));
+    lo3[2] = min(lo3[2], (int)(B & 0xff)); hi3[2] = max(hi3[2], (int)((B >> 8) & 0xff));
+}
+
 // Pass 1: sum delta, sum delta*xhat, sum sgn and the per-sgn-class extremes of
 // the masked delta d.  The extremes come from four keys per element, d +- 1024 s
 // and d +- 1024 |s| (s = sgn in {-1, 0, 1}, |d| <= 128): the minimum of d + 1024 s
@@ -782,7 +975,14 @@ __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, 
 __device__ __forceinline__ void bnb_round_tail1(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
                                                 const BnCfg& cf, const BnbOut& o);
 
-template <int TAIL>                      // 0: none, 1: exact E2, 2: rounding E2
+// Block totals per channel.  When the G lanes of a row (G = CS / 4) are a
+// power of two, the lanes of a wave that hold the same channels are folded
+// with shuffles and the 16 wave totals of each channel are staged in LDS
+// (the caller's table space, no longer read) and summed by one thread per
+// channel: LDS atomics from every wave onto the same channel slots serialize
+// and cost several microseconds per block.  Other widths use LDS atomics.
+
+template <int TAIL>                      // 1: exact E2, 2: rounding E2
 __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                    Saved sv, BnCfg cf, BnbOut out)
@@ -792,12 +992,12 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
     __shared__ unsigned long long sSdn[64];
     __shared__ int32_t sSd[64], sZ[64], sMM[64 * 6];
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
+    const bool fold = (st.G & (st.G - 1)) == 0 && st.G <= 64;
     load_bwd_tab(tab, sv.btab + cbase * 256, st.CS, relu, false);
-    if ((int)threadIdx.x < st.CS) {
+    if (!fold && (int)threadIdx.x < st.CS) {
         sSdn[threadIdx.x] = 0; sSd[threadIdx.x] = 0; sZ[threadIdx.x] = 0;
         for (int k = 0; k < 3; k++) { sMM[threadIdx.x * 6 + 2 * k] = 1000; sMM[threadIdx.x * 6 + 2 * k + 1] = -1000; }
     }
-    if (!TAIL && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) { *w.maxF = 0; *w.bdx = kSentinelLo; }
     __syncthreads();
     int g, rsub;
     const bool active = stream_lane(st, g, rsub);
@@ -876,64 +1076,103 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
         mm[i][4] = kmn1[i] <= -kKey + 128 ? kmn1[i] + kKey : 1000;     // class +1
         mm[i][5] = kmx0[i] >= kKey - 128 ? kmx0[i] - kKey : -1000;
     }
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-        sd[i] = group_fold(sd[i], st.G, OpAdd());
-        sdn[i] = group_fold(sdn[i], st.G, OpAdd());
-        z[i] = group_fold(z[i], st.G, OpAdd());
-#pragma unroll
-        for (int k = 0; k < 3; k++) {
-            mm[i][2 * k] = group_fold(mm[i][2 * k], st.G, OpMin());
-            mm[i][2 * k + 1] = group_fold(mm[i][2 * k + 1], st.G, OpMax());
-        }
-    }
-    if (active && group_leader(st.G)) {
+    with_g(st.G, [&](auto gc) {
+        constexpr int GG = decltype(gc)::value;
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            int cl = g * 4 + i;
-            atomicAdd(&sSd[cl], sd[i]);
-            atomicAdd(&sSdn[cl], (unsigned long long)sdn[i]);
-            atomicAdd(&sZ[cl], z[i]);
+            sd[i] = fold_g<GG>(sd[i], OpAdd());
+            sdn[i] = fold_g<GG>(sdn[i], OpAdd());
+            z[i] = fold_g<GG>(z[i], OpAdd());
 #pragma unroll
             for (int k = 0; k < 3; k++) {
-                atomicMin(&sMM[cl * 6 + 2 * k], mm[i][2 * k]);
-                atomicMax(&sMM[cl * 6 + 2 * k + 1], mm[i][2 * k + 1]);
+                mm[i][2 * k] = fold_g<GG>(mm[i][2 * k], OpMin());
+                mm[i][2 * k + 1] = fold_g<GG>(mm[i][2 * k + 1], OpMax());
             }
         }
-    }
-    __syncthreads();
-    if ((int)threadIdx.x < st.CS) {
-        const size_t pc = (size_t)st.gx * st.C;
-        int64_t o = (int64_t)blockIdx.x * st.C + cbase + threadIdx.x;
-        if (TAIL) {
-            st_x(&w.p_sd[o], sSd[threadIdx.x]);
-            st_x(&w.p_sdn[o], (long long)sSdn[threadIdx.x]);
-            st_x(&w.p_z[o], sZ[threadIdx.x]);
-            for (int k = 0; k < 6; k++) st_x(&w.p_mm[k * pc + o], sMM[threadIdx.x * 6 + k]);
-        } else {
-            w.p_sd[o] = sSd[threadIdx.x];
-            w.p_sdn[o] = (long long)sSdn[threadIdx.x];
-            w.p_z[o] = sZ[threadIdx.x];
-            for (int k = 0; k < 6; k++) w.p_mm[k * pc + o] = sMM[threadIdx.x * 6 + k];
+    });
+    const int t = threadIdx.x;
+    int32_t bsd = 0, bz = 0;
+    long long bsdn = 0;
+    int bmm[6] = {1000, -1000, 1000, -1000, 1000, -1000};
+    if (fold) {
+        __syncthreads();                                  // every wave is done with the table
+        int32_t* wsd = (int32_t*)tab;                     // [kWaves][64] each
+        int32_t* wz = wsd + kWaves * 64;
+        int32_t* wmm = wz + kWaves * 64;                  // [6][kWaves][64]
+        long long* wsdn = (long long*)(wmm + 6 * kWaves * 64);
+        const int wv = t >> 6;
+        if ((t & 63) < st.G) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int s = wv * 64 + g * 4 + i;
+                wsd[s] = sd[i]; wz[s] = z[i]; wsdn[s] = sdn[i];
+#pragma unroll
+                for (int k = 0; k < 6; k++) wmm[k * kWaves * 64 + s] = mm[i][k];
+            }
+        }
+        __syncthreads();
+        if (t < st.CS) {
+#pragma unroll 4
+            for (int v = 0; v < kWaves; v++) {
+                const int s = v * 64 + t;
+                bsd += wsd[s]; bz += wz[s]; bsdn += wsdn[s];
+#pragma unroll
+                for (int k = 0; k < 6; k++) {
+                    const int m = wmm[k * kWaves * 64 + s];
+                    bmm[k] = (k & 1) ? max(bmm[k], m) : min(bmm[k], m);
+                }
+            }
+        }
+    } else {
+        if (active && group_leader(st.G)) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                int cl = g * 4 + i;
+                atomicAdd(&sSd[cl], sd[i]);
+                atomicAdd(&sSdn[cl], (unsigned long long)sdn[i]);
+                atomicAdd(&sZ[cl], z[i]);
+#pragma unroll
+                for (int k = 0; k < 3; k++) {
+                    atomicMin(&sMM[cl * 6 + 2 * k], mm[i][2 * k]);
+                    atomicMax(&sMM[cl * 6 + 2 * k + 1], mm[i][2 * k + 1]);
+                }
+            }
+        }
+        __syncthreads();
+        if (t < st.CS) {
+            bsd = sSd[t]; bz = sZ[t]; bsdn = (long long)sSdn[t];
+            for (int k = 0; k < 6; k++) bmm[k] = sMM[t * 6 + k];
         }
     }
-    if (TAIL && arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) {
+    if (t < st.CS) {
+        const int64_t o = (int64_t)blockIdx.x * st.C + cbase + t;
+        uint32_t A, B;
+        mm_pack(bmm, A, B);
+        st_x(&w.p_sd[o], bsd);
+        st_x(&w.p_sdn[o], bsdn);
+        st_x(&w.p_z[o], bz);
+        st_x(&w.p_mmA[o], (int32_t)A);
+        st_x(&w.p_mmB[o], (int32_t)B);
+    }
+    if (arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) {
+        __syncthreads();                                  // the staging above may still be read
         if constexpr (TAIL == 1) bnb_exact_tail(tab, st, w, sv, cf, out);
         else bnb_round_tail1(tab, st, w, sv, cf, out);
     }
 }
 
-__device__ __forceinline__ int bnb_r2(const BwdWs& w, const BnCfg& cf)
+
+// E2's requant shift from max |gamma delta| (the slices' maxima)
+__device__ __forceinline__ int bnb_r2_of(int32_t maxF, const BnCfg& cf)
 {
-    uint64_t MF = *w.maxF;
-    return MF ? bitlen_u64(MF) - (cf.k_E2 - 1) : 0;
+    return maxF > 0 ? bitlen_u64((uint64_t)maxF) - (cf.k_E2 - 1) : 0;
 }
 
 __device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st, const BwdWs& w,
-                                                const Saved& sv, const BnCfg& cf, const BnbOut& o);
+                                                const Saved& sv, const BnCfg& cf, const BnbOut& o, int r2);
 
 // pass 2 (only when E2's quantizer rounds): sum f and f*n_xhat; the tails
-// reduce them and give E1's exponent
+// reduce them and give each slice's bound on E1's exponent
 __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ dy,
                                                     const int8_t* __restrict__ x, Stream st, BwdWs w,
                                                     Saved sv, BnCfg cf, BnbOut out)
@@ -943,6 +1182,7 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
     __shared__ int16_t ft[64 * 256];                  // f = SQ(gamma_q d, k_E2) per (channel, d)
     __shared__ Thr thr[64];
     __shared__ unsigned long long sF[64], sFn[64];
+    __shared__ int32_t rsh[kNT / 64];
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
     {
         copy_to_lds<64 * 512 / 16 / kNT>((uint4*)xc, (const uint4*)(sv.xcode + cbase * 256), st.CS * 32);
@@ -952,12 +1192,10 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
         thr[threadIdx.x] = Thr{sv.t0[c], sv.p0[c], cf.relu ? sv.mlo[c] : -1000, cf.relu ? sv.mhi[c] : 1000};
         sF[threadIdx.x] = 0; sFn[threadIdx.x] = 0;
     }
-    {
-        // |f| < 2^(k_E2-1) <= 2^13 on this path
-        const int r2 = bnb_r2(w, cf);
-        for (int e = threadIdx.x; e < st.CS * 256; e += blockDim.x)
-            ft[e] = (int16_t)sq_code((int64_t)gamma_q[cbase + (e >> 8)] * ((e & 255) - 128), r2, cf.k_E2);
-    }
+    // |f| < 2^(k_E2-1) <= 2^13 on this path
+    const int r2 = bnb_r2_of(slices_max(w.smaxF, (int)gridDim.y, rsh), cf);
+    for (int e = threadIdx.x; e < st.CS * 256; e += blockDim.x)
+        ft[e] = (int16_t)sq_code((int64_t)gamma_q[cbase + (e >> 8)] * ((e & 255) - 128), r2, cf.k_E2);
     __syncthreads();
     int g, rsub;
     const bool active = stream_lane(st, g, rsub);
@@ -979,11 +1217,14 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
             }
         });
     }
+    with_g(st.G, [&](auto gc) {
+        constexpr int GG = decltype(gc)::value;
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-        sf[i] = group_fold(sf[i], st.G, OpAdd());
-        sfn[i] = group_fold(sfn[i], st.G, OpAdd());
-    }
+        for (int i = 0; i < 4; i++) {
+            sf[i] = fold_g<GG>(sf[i], OpAdd());
+            sfn[i] = fold_g<GG>(sfn[i], OpAdd());
+        }
+    });
     if (active && group_leader(st.G)) {
 #pragma unroll
         for (int i = 0; i < 4; i++) {
@@ -997,7 +1238,10 @@ __global__ __launch_bounds__(1024) void k_bnb_stats2(const int8_t* __restrict__ 
         st_x(&w.p_sf[o], (long long)sF[threadIdx.x]);
         st_x(&w.p_sfn[o], (long long)sFn[threadIdx.x]);
     }
-    if (arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) bnb_round_tail2((uint32_t*)xc, st, w, sv, cf, out);
+    if (arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) {
+        __syncthreads();
+        bnb_round_tail2((uint32_t*)xc, st, w, sv, cf, out, r2);
+    }
 }
 
 // bracket of the exact dx (times den M^2 / 2^Ebase) for a (f, sgn) pair
@@ -1025,31 +1269,34 @@ __device__ __forceinline__ BnbChan bnb_chan_exps(int r2, int32_t dy_exp, const S
     return ch;
 }
 
-__device__ __forceinline__ BnbChan bnb_chan(int c, const int32_t* dy_exp, const BwdWs& w,
-                                            const Saved& sv, const BnCfg& cf, int gq, bool exact_e2)
+__device__ __forceinline__ void bnb_exps_out(const Saved& sv, const BnCfg& cf, const BnbOut& o)
 {
-    BnbChan ch = bnb_chan_exps(bnb_r2(w, cf), *dy_exp, sv, cf);
-    if (exact_e2) {
-        // E2 exact: f = gamma_q delta 2^-r2 with r2 <= 0
-        ch.Sf = (i128)gq * (i128)w.sd[c] * pow2_128(-ch.r2);
-        ch.T = (i128)gq * (i128)w.sdn[c] * pow2_128(-ch.r2);
-    } else {
-        ch.Sf = (i128)w.sf[c];
-        ch.T = (i128)w.sfn[c];
-    }
-    ch.Z = (i128)w.Z[c];
-    return ch;
+    const int32_t s_d = *o.dy_exp;
+    if (s_d < -60 || s_d > 16) set_status(o.dev_status, ISEG_DEV_RANGE);
+    *o.dbeta_exp = s_d;
+    *o.dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
 }
 
 // dx code table for every (sgn class, masked error code) of a channel
-__global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t Mrows, BwdWs w, Saved sv,
-                                                 BnCfg cf, const int8_t* gamma_q, int exact_e2)
+// (rounding E2): E1's exponent and E2's shift from the slices' maxima
+__global__ __launch_bounds__(256) void k_bnb_lut(int64_t Mrows, int nslices, BwdWs w, Saved sv, BnCfg cf,
+                                                 BnbOut o)
 {
+    __shared__ int32_t rsh[4];
     const int c = blockIdx.x;
     const int d = (int)threadIdx.x - 128;
-    const int gq = gamma_q[c];
-    BnbChan ch = bnb_chan(c, dy_exp, w, sv, cf, gq, exact_e2);
-    const int bdx = *w.bdx;                 // stats2's last tail
+    const int gq = o.gamma_q[c];
+    const int r2 = bnb_r2_of(slices_max(w.smaxF, nslices, rsh), cf);
+    int bdx = slices_max(w.smax, nslices, rsh);
+    if (bdx == kSentinelLo) bdx = 0;
+    if (c == 0 && threadIdx.x == 0) {
+        *o.dx_exp = bdx - (cf.k_E1 - 1);
+        bnb_exps_out(sv, cf, o);
+    }
+    BnbChan ch = bnb_chan_exps(r2, *o.dy_exp, sv, cf);
+    ch.Sf = (i128)w.sf[c];
+    ch.T = (i128)w.sfn[c];
+    ch.Z = (i128)w.Z[c];
     const i128 M = Mrows;
     const i128 Dd = (i128)sv.den[c] * M * M;
     const int64_t f = d < -127 ? 0 : sq_code((int64_t)gq * d, ch.r2, cf.k_E2);
@@ -1067,13 +1314,15 @@ __global__ __launch_bounds__(256) void k_bnb_lut(const int32_t* dy_exp, int64_t 
 // Exact E2 (k_E2 >= 15, |gamma delta| <= 127^2 < 2^(k_E2-1)): E2's requant
 // shift r2 is <= 0 and scales every term of the bracket and the exponent base
 // by inverse powers of two, so dx, its exponent bound and its codes are those
-// of r2 = 0, with f = gamma_q delta; the stats kernel's tails replace fin1 + fin2.
+// of r2 = 0, with f = gamma_q delta; the stats kernel's tails replace a
+// separate per-channel pass.
 // ---------------------------------------------------------------------------
 // stats tail (exact E2).  Slice: the pass-1 sums, dgamma and dbeta of its
 // channels and each channel's bound on max|dx| (|dx| is extreme at a class's
-// extreme deltas: six candidates per channel, one thread each).  Last slice:
-// E1's exponent from the largest bound over all channels.  `lds` is the
-// stats table, no longer read once the block has arrived.
+// extreme deltas: six candidates per channel, one thread each); the largest
+// bound of the slice goes to smax for the table kernel, which takes E1's
+// exponent as the largest over the slices.  `lds` is the stats table, no
+// longer read once the block has arrived.
 struct Tail1Lds {
     int32_t *sd, *z, *mm, *cand;        // [kNT], [kNT], [6][kNT], [6 * CS]
     long long* sdn;                     // [kNT]
@@ -1095,15 +1344,14 @@ __device__ __forceinline__ void bnb_tail_reduce1(uint32_t* lds, const Stream& st
     int32_t* tZ = L.z;
     int32_t* tMM = L.mm;
     long long* tSdn = L.sdn;
-    const size_t pc = (size_t)st.gx * st.C;
     const int64_t cb = (int64_t)blockIdx.y * CS;
     int sd = 0, z = 0;
     long long sdn = 0;
-    int mm[6] = {1000, -1000, 1000, -1000, 1000, -1000};
-    constexpr int U = 4;                    // partial rows whose loads are in flight together
+    int lo3[3] = {255, 255, 255}, hi3[3] = {0, 0, 0};   // byte-coded extremes
+    constexpr int U = 8;                    // partial rows whose loads are in flight together
     if (grp < ng)
         for (int b0 = grp; b0 < st.gx; b0 += U * ng) {
-            int32_t vsd[U], vz[U], vmm[U][6];
+            int32_t vsd[U], vz[U], vA[U], vB[U];
             long long vsdn[U];
 #pragma unroll
             for (int u = 0; u < U; u++) {
@@ -1112,31 +1360,33 @@ __device__ __forceinline__ void bnb_tail_reduce1(uint32_t* lds, const Stream& st
                 vsd[u] = ld_x(&w.p_sd[q]);
                 vsdn[u] = ld_x(&w.p_sdn[q]);
                 vz[u] = ld_x(&w.p_z[q]);
-#pragma unroll
-                for (int k = 0; k < 6; k++) vmm[u][k] = ld_x(&w.p_mm[k * pc + q]);
+                vA[u] = ld_x(&w.p_mmA[q]);
+                vB[u] = ld_x(&w.p_mmB[q]);
             }
 #pragma unroll
             for (int u = 0; u < U; u++) {
+                mm_merge((uint32_t)vA[u], (uint32_t)vB[u], lo3, hi3);   // a repeated row changes nothing
                 if (b0 + u * ng >= st.gx) continue;
                 sd += vsd[u]; sdn += vsdn[u]; z += vz[u];
-#pragma unroll
-                for (int k = 0; k < 6; k++) mm[k] = (k & 1) ? max(mm[k], vmm[u][k]) : min(mm[k], vmm[u][k]);
             }
         }
     tSd[t] = sd; tZ[t] = z; tSdn[t] = sdn;
 #pragma unroll
-    for (int k = 0; k < 6; k++) tMM[k * kNT + t] = mm[k];
+    for (int k = 0; k < 3; k++) { tMM[2 * k * kNT + t] = lo3[k]; tMM[(2 * k + 1) * kNT + t] = hi3[k]; }
     __syncthreads();
     if (t < CS) {
         for (int g2 = 1; g2 < ng; g2++) {
             const int i = g2 * CS + t;
             sd += tSd[i]; z += tZ[i]; sdn += tSdn[i];
 #pragma unroll
-            for (int k = 0; k < 6; k++) {
-                const int v = tMM[k * kNT + i];
-                mm[k] = (k & 1) ? max(mm[k], v) : min(mm[k], v);
+            for (int k = 0; k < 3; k++) {
+                lo3[k] = min(lo3[k], tMM[2 * k * kNT + i]);
+                hi3[k] = max(hi3[k], tMM[(2 * k + 1) * kNT + i]);
             }
         }
+        int mm[6];
+#pragma unroll
+        for (int k = 0; k < 3; k++) { mm[2 * k] = lo3[k] - 128; mm[2 * k + 1] = hi3[k] - 128; }   // empty: lo > hi
         const int64_t c = cb + t;
         w.sd[c] = sd; w.sdn[c] = sdn; w.Z[c] = z;
 #pragma unroll
@@ -1151,12 +1401,14 @@ __device__ __forceinline__ void bnb_tail_reduce1(uint32_t* lds, const Stream& st
     __syncthreads();
 }
 
-__device__ __forceinline__ void bnb_exps_out(const Saved& sv, const BnCfg& cf, const BnbOut& o)
+// largest of the slice's per-channel values in tCand (6 per channel) into
+// *dst (kSentinelLo when none)
+__device__ __forceinline__ void slice_cand_max(const int32_t* tCand, int n, int32_t* dst, int32_t* sh)
 {
-    const int32_t s_d = *o.dy_exp;
-    if (s_d < -60 || s_d > 16) set_status(o.dev_status, ISEG_DEV_RANGE);
-    *o.dbeta_exp = s_d;
-    *o.dgamma_exp = s_d + sv.hdr[0] - (cf.k_xhat - 1);
+    int32_t m = kSentinelLo;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) m = max(m, tCand[i]);
+    m = block_max_nt(m, sh);
+    if (threadIdx.x == 0) *dst = m;
 }
 
 __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
@@ -1170,6 +1422,7 @@ __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, 
     int32_t* tMM = L.mm;
     long long* tSdn = L.sdn;
     int32_t* tCand = L.cand;
+    __shared__ int32_t rb[kNT / 64];
     const int64_t cb = (int64_t)blockIdx.y * CS;
     const int32_t s_d = *o.dy_exp;
     const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
@@ -1191,34 +1444,21 @@ __device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, 
         tCand[t] = best;
     }
     __syncthreads();
-    if (t < CS) {
-        int best = tCand[6 * t];
-        for (int j = 1; j < 6; j++) best = max(best, tCand[6 * t + j]);
-        st_x(&w.cand[cb + t], best);
-    }
-    if (!arrive_last(w.ctr, gridDim.y)) return;
-    __shared__ int32_t rb[kNT / 64];
-    int bdx = kSentinelLo;
-    for (int c = t; c < st.C; c += kNT) bdx = max(bdx, ld_x(&w.cand[c]));
-    bdx = block_max_nt(bdx, rb);
-    if (bdx == kSentinelLo) bdx = 0;
-    if (t == 0) {
-        *w.bdx = bdx;
-        *o.dx_exp = bdx - (cf.k_E1 - 1);
-        bnb_exps_out(sv, cf, o);
-    }
+    slice_cand_max(tCand, 6 * CS, w.smax + blockIdx.y, rb);
 }
 
-// stats tail (rounding E2).  Slice: the pass-1 sums, dgamma, dbeta and each
-// channel's max |gamma_q delta| over its sgn classes.  Last slice: the largest
-// over all channels, the Scale of E2 = SQ(gamma delta, k_E2) read by stats2.
+// stats tail (rounding E2).  Slice: the pass-1 sums, dgamma, dbeta and the
+// largest |gamma_q delta| over its channels' sgn classes, into smaxF; the
+// second pass takes E2's Scale from the largest over the slices.
 __device__ __forceinline__ void bnb_round_tail1(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
                                                 const BnCfg& cf, const BnbOut& o)
 {
     bnb_tail_reduce1(lds, st, w, o);
     const int CS = st.CS, t = threadIdx.x;
     const Tail1Lds L(lds);
+    __shared__ int32_t rb[kNT / 64];
     const int64_t cb = (int64_t)blockIdx.y * CS;
+    int F = 0;
     if (t < CS) {
         int amax = 0;
         for (int k = 0; k < 3; k++) {
@@ -1227,32 +1467,26 @@ __device__ __forceinline__ void bnb_round_tail1(uint32_t* lds, const Stream& st,
             amax = max(amax, max(lo < 0 ? -lo : lo, hi < 0 ? -hi : hi));
         }
         const int gq = o.gamma_q[cb + t];
-        st_x(&w.cand[cb + t], (gq < 0 ? -gq : gq) * amax);      // <= 128 * 128
+        F = (gq < 0 ? -gq : gq) * amax;                // <= 128 * 128
     }
-    if (!arrive_last(w.ctr, gridDim.y)) return;
-    __shared__ int32_t rb[kNT / 64];
-    int F = 0;
-    for (int c = t; c < st.C; c += kNT) F = max(F, ld_x(&w.cand[c]));
     F = block_max_nt(F, rb);
-    if (t == 0) {
-        *w.maxF = (unsigned long long)F;
-        bnb_exps_out(sv, cf, o);
-    }
+    if (t == 0) w.smaxF[blockIdx.y] = F;
 }
 
 // stats2 tail.  Slice: the pass-2 sums (sum f, sum f n_xhat) and each
-// channel's bound on max|dx| (six candidates, as the exact tail); last slice:
-// E1's exponent.  `lds` is stats2's x-hat table, no longer read.
+// channel's bound on max|dx| (six candidates, as the exact tail); the largest
+// goes to smax.  `lds` is stats2's x-hat table, no longer read.
 __device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st, const BwdWs& w,
-                                                const Saved& sv, const BnCfg& cf, const BnbOut& o)
+                                                const Saved& sv, const BnCfg& cf, const BnbOut& o, int r2)
 {
     const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
     long long* tSf = (long long*)lds;                   // [kNT]
     long long* tSfn = tSf + kNT;                        // [kNT]
     int32_t* tCand = (int32_t*)(tSfn + kNT);            // [6 * CS]
+    __shared__ int32_t rb[kNT / 64];
     const int64_t cb = (int64_t)blockIdx.y * CS;
     long long sf = 0, sfn = 0;
-    constexpr int U = 4;                    // partial rows whose loads are in flight together
+    constexpr int U = 8;                    // partial rows whose loads are in flight together
     if (grp < ng)
         for (int b0 = grp; b0 < st.gx; b0 += U * ng) {
             long long vf[U], vn[U];
@@ -1282,7 +1516,7 @@ __device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st,
         int best = kSentinelLo;
         if (lo <= hi) {
             const int gq = o.gamma_q[c];
-            const BnbChan e = bnb_chan_exps(bnb_r2(w, cf), *o.dy_exp, sv, cf);
+            const BnbChan e = bnb_chan_exps(r2, *o.dy_exp, sv, cf);
             const i128 M = st.M;
             const int64_t f = sq_code((int64_t)gq * ((k & 1) ? hi : lo), e.r2, cf.k_E2);
             const i128 B = bnb_bracket(f, (k >> 1) - 1, M, (i128)tSf[cl], (i128)tSfn[cl], (i128)w.Z[c], e.e_xh);
@@ -1291,35 +1525,27 @@ __device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st,
         tCand[t] = best;
     }
     __syncthreads();
-    if (t < CS) {
-        int best = tCand[6 * t];
-        for (int j = 1; j < 6; j++) best = max(best, tCand[6 * t + j]);
-        st_x(&w.cand[cb + t], best);
-    }
-    if (!arrive_last(w.ctr, gridDim.y)) return;
-    __shared__ int32_t rb[kNT / 64];
-    int bdx = kSentinelLo;
-    for (int c = t; c < st.C; c += kNT) bdx = max(bdx, ld_x(&w.cand[c]));
-    bdx = block_max_nt(bdx, rb);
-    if (bdx == kSentinelLo) bdx = 0;
-    if (t == 0) {
-        *w.bdx = bdx;
-        *o.dx_exp = bdx - (cf.k_E1 - 1);
-    }
+    slice_cand_max(tCand, 6 * CS, w.smax + blockIdx.y, rb);
 }
 
 // dx code table of a channel (one thread per masked error code, three sgn
-// classes), with E1's exponent from the stats kernel's last tail
-__global__ __launch_bounds__(256) void k_bnb_lut_exact(const int32_t* dy_exp, int64_t Mrows, BwdWs w, Saved sv,
-                                                       BnCfg cf, const int8_t* gamma_q)
+// classes); E1's exponent is the largest of the slices' bounds
+__global__ __launch_bounds__(256) void k_bnb_lut_exact(int64_t Mrows, int nslices, BwdWs w, Saved sv, BnCfg cf,
+                                                       BnbOut o)
 {
+    __shared__ int32_t rsh[4];
     const int c = blockIdx.x;
-    const int bdx = *w.bdx;                 // the stats kernel's last tail
+    int bdx = slices_max(w.smax, nslices, rsh);
+    if (bdx == kSentinelLo) bdx = 0;
+    if (c == 0 && threadIdx.x == 0) {
+        *o.dx_exp = bdx - (cf.k_E1 - 1);
+        bnb_exps_out(sv, cf, o);
+    }
     const int d = (int)threadIdx.x - 128;
-    const int gq = gamma_q[c];
+    const int gq = o.gamma_q[c];
     const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
     const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
-    const int Ebase = *dy_exp + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
+    const int Ebase = *o.dy_exp + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
     const i128 M = Mrows;
     const i128 Dd = (i128)sv.den[c] * M * M;
     const i128 Sf = (i128)gq * w.sd[c], T = (i128)gq * w.sdn[c], Z = w.Z[c];
@@ -1334,6 +1560,10 @@ __global__ __launch_bounds__(256) void k_bnb_lut_exact(const int32_t* dy_exp, in
     }
 }
 
+// Output pass: dx code = lut[c][sgn class][masked delta].  A per-(channel,
+// code) entry gives the offset of the channel's class row in the block's LDS
+// copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
+// element costs two LDS reads and a handful of ALU operations.
 // Output pass: dx code = lut[c][sgn class][masked delta].  A per-(channel,
 // code) entry gives the offset of the channel's class row in the block's LDS
 // copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
@@ -1451,19 +1681,19 @@ static int bn_fwd_impl(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t
     dim3 sg = stream_grid(st);
     dim3 cb((unsigned)C);
     if (s16)
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<16>, sg, dim3(kNT), 0, stream, x, st, w);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<16>, sg, dim3(kNT), 0, stream, x, x_exp, st,
+                          w, sv, cf);
     else
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<4>, sg, dim3(kNT), 0, stream, x, st, w);
-    hipLaunchKernelGGL(k_bnf_finmu, cb, dim3(256), 0, stream, x_exp, st, w, sv, cf);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<4>, sg, dim3(kNT), 0, stream, x, x_exp, st,
+                          w, sv, cf);
     if (s16)
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2<16>, sg, dim3(kNT), 0, stream, x, x_exp,
                           st, w, sv, cf, dev_status);
     else
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2<4>, sg, dim3(kNT), 0, stream, x, x_exp,
                           st, w, sv, cf, dev_status);
-    hipLaunchKernelGGL(k_bnf_finsig, cb, dim3(256), 0, stream, x_exp, st, w, sv, cf);
-    hipLaunchKernelGGL(k_bnf_fin2, cb, dim3(256), 0, stream, x_exp, w, sv, cf, gamma_q, beta_q);
-    hipLaunchKernelGGL(k_bnf_fin3, cb, dim3(256), 0, stream, x_exp, w, sv, cf, y_exp);
+    hipLaunchKernelGGL(k_bnf_fin2, cb, dim3(256), 0, stream, x_exp, (int)sg.y, w, sv, cf, gamma_q, beta_q);
+    hipLaunchKernelGGL(k_bnf_fin3, cb, dim3(256), 0, stream, x_exp, w, sv, cf, gamma_q, beta_q, y_exp);
     if (v16) {
         Stream a16 = make_stream(M, C, cs, 16, 4, kMaxBlocks);
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply<16>, stream_grid(a16), dim3(kNT), 0,
@@ -1491,12 +1721,13 @@ extern "C" int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int
 // buffer.  In host code `scratch` names a host-side stand-in, not device
 // memory: its device address is looked up once per device with
 // hipGetSymbolAddress (with that device current) and only that address is
-// passed to the kernels.  The forward's workspace is written before it is
-// read within a call (per-block partials, per-channel tables), so nothing
-// needs clearing between calls.
+// passed to the kernels.  The array starts at zero and every call leaves
+// the forward's arrival counters at zero; the rest of the workspace is
+// written before it is read within a call, so nothing needs clearing between
+// calls.
 // ---------------------------------------------------------------------------
 namespace {
-constexpr size_t kBnScratchBytes = (size_t)8 << 20;
+constexpr size_t kBnScratchBytes = (size_t)1 << 20;
 constexpr int kScratchDevices = 64;
 __device__ __align__(256) unsigned char scratch[kBnScratchBytes];
 std::mutex g_scratch_mu;
@@ -1558,15 +1789,17 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     if (exact_e2) {
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<1>, sg, dim3(kNT), 0, stream, dy, x, st, w,
                           sv, cf, out);
-        hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q);
+        hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, M, (int)sg.y, w, sv, cf, out);
     } else {
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<2>, sg, dim3(kNT), 0, stream, dy, x, st,
                           w, sv, cf, out);
         hipLaunchKernelGGL(k_bnb_stats2, sg, dim3(kNT), 0, stream, dy, x, st, w, sv, cf, out);
-        hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, dy_exp, M, w, sv, cf, gamma_q, exact_e2);
+        hipLaunchKernelGGL(k_bnb_lut, cb, dim3(256), 0, stream, M, (int)sg.y, w, sv, cf, out);
     }
-    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, sg, dim3(kNT), 0, stream, dy, x, dx_out, st,
-                      w, sv, cf.relu);
+    // the output pass needs no partials: its grid holds more rows per lane
+    const Stream sa = make_stream(M, C, cs, 4, 8, kMaxBlocks);
+    ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, stream_grid(sa), dim3(kNT), 0, stream, dy, x,
+                      dx_out, sa, w, sv, cf.relu);
     return launch_ok();
 }
 

@@ -568,8 +568,8 @@ def _maybe_arm(kid, key):
 class Workspace:
     """A growable device scratch buffer shared by consecutive calls on one
     stream (stream order keeps the uses apart); each stream has its own.
-    `zeroed` buffers start at zero (the BN backward workspace, whose arrival
-    counters every call leaves at zero)."""
+    `zeroed` buffers start at zero (the BN workspace, whose arrival counters
+    every call leaves at zero)."""
 
     def __init__(self, device="cuda", zeroed=False):
         self.device = device
@@ -588,7 +588,7 @@ _WS = {}
 
 
 def workspace(device, bn=False):
-    """The workspace of the current stream; the BN backward has one of its own."""
+    """The workspace of the current stream; L1BN (int8 input) has one of its own."""
     d = device if isinstance(device, torch.device) else torch.device(device)
     if d.type == "cuda":
         idx = d.index if d.index is not None else _raw_device()
@@ -724,7 +724,7 @@ def bn_fwd(x, x_exp, gamma_q, beta_q, cfg=None, saved=None, status=None):
     e = _out_exp(x.device)
     if saved is None:
         saved = torch.empty(lib().iseg_bn_saved_bytes(Cc), dtype=torch.uint8, device=x.device)
-    ws = workspace(x.device).get(lib().iseg_bn_fwd_ws(M, Cc))
+    ws = workspace(x.device, bn=True).get(lib().iseg_bn_fwd_ws(M, Cc))
     for kid in (ISEG_KID_BN_FWD_APPLY, ISEG_KID_BN_FWD_STATS1, ISEG_KID_BN_FWD_STATS2):
         _maybe_arm(kid, (M, Cc))
     iseg_bn_fwd(x, x_exp, M, Cc, gamma_q, beta_q, cfg, y, e, saved, ws, status)

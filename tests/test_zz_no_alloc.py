@@ -29,7 +29,8 @@ def _run_pair(iseg, torch, dev, M, Cc, relu, seed):
         if noalloc:
             iseg.iseg_bn_fwd_noalloc(x, xe, M, Cc, g, b, cfg, y, ye, sv, st)
         else:
-            ws = torch.empty(iseg.lib().iseg_bn_fwd_ws(M, Cc), dtype=torch.uint8, device=dev)
+            # the workspace starts with arrival counters that must be zero
+            ws = torch.zeros(iseg.lib().iseg_bn_fwd_ws(M, Cc), dtype=torch.uint8, device=dev)
             iseg.iseg_bn_fwd(x, xe, M, Cc, g, b, cfg, y, ye, sv, ws, st)
         torch.cuda.synchronize()
         assert int(st.item()) == 0
@@ -57,7 +58,7 @@ def test_bn_fwd_noalloc_rejects_shapes_beyond_the_array():
         pytest.skip("no GPU")
     from paper_2011_14504_amd import iseg
     L = iseg.lib()
-    M, Cc = 4096, 4096
+    M, Cc = 1024, 65536
     assert L.iseg_bn_fwd_ws(M, Cc) > L.iseg_bn_fwd_noalloc_max_bytes()
     dev = torch.device("cuda", 0)
     x = torch.zeros((M, Cc), dtype=torch.int8, device=dev)
