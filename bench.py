@@ -199,6 +199,8 @@ def main():
                          "bn_fwd_stats1, bn_fwd_stats2, bn_fwd_apply, bn_bwd_stats, bn_bwd_apply; * times "
                          "every launch of the family in the timed steps (the default: the L1BN backward "
                          "statistics pass, the step's largest kernel by time)")
+    ap.add_argument("--no-replay", action="store_true",
+                    help="enqueue every step from Python instead of replaying the recorded last warm-up step")
     ap.add_argument("--conv-steps", type=int, default=2,
                     help="extra steps after the timed ones whose conv entry points are timed one by one "
                          "(conv TOPS over conv time)")
@@ -224,7 +226,12 @@ def main():
         args.gq = wl.get("gq", 1)
     inp = synth.workload_inputs(wl)
     widths = dict(k_W=args.k_w, k_U=args.k_u, bn_cfg={"k_A": args.k_a, "k_E2": args.k_e2}, gq=args.gq)
-    net = IntNet(wl, inp, "cuda:0", bn_input=args.bn_input, **widths)
+    # the last warm-up step is recorded into a step tape and the timed steps
+    # replay it from native code (the same calls, buffers and stream orderings;
+    # the host no longer enqueues each call from Python)
+    replay = not args.no_replay and args.warmup >= 1
+    net = IntNet(wl, inp, "cuda:0", bn_input=args.bn_input, replay_from=args.warmup - 1 if replay else None,
+                 **widths)
     ops, detail = workload_ops(wl)
     tk = args.timed_kernel
     if tk.startswith("bn_") and (args.no_bn or not any(nd.get("bn") for nd in synth.conv_nodes(wl))):
@@ -240,8 +247,20 @@ def main():
         net.step()
     torch.cuda.synchronize()
     iseg.set_kernel_timer(None)
+    armed = [(kid, key) for _, _, kid, key in prof.pairs]
     prof.reset()
-    iseg.set_kernel_timer(prof)
+    if replay:
+        # the recorded step armed the timed kernel's launches: each replay of
+        # the timed region gets its own (start, stop) events for them
+        events = []
+        for _ in range(args.steps):
+            for kid, key in armed:
+                a, b = prof._event(), prof._event()
+                prof.pairs.append((a, b, kid, key))
+                events.append((a.value, b.value))
+        net.tape.set_arm_events(events, args.steps)
+    else:
+        iseg.set_kernel_timer(prof)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         net.step()
@@ -281,7 +300,7 @@ def main():
         ct = iseg.KernelTimer([iseg.ISEG_KID_CONV_FWD, iseg.ISEG_KID_CONV_BWD_DATA, iseg.ISEG_KID_CONV_WGRAD])
         iseg.set_kernel_timer(ct)
         for _ in range(args.conv_steps):
-            net.step()
+            net.step(eager=True)
         torch.cuda.synchronize()
         iseg.set_kernel_timer(None)
         conv_ms = sum(t for _, _, t in ct.launches())
@@ -292,6 +311,7 @@ def main():
                pct_int8_peak=100.0 * value / INT8_PEAK_TOPS,
                bits=dict(W=args.k_w, A=args.k_a, G=8, E1=8, E2=args.k_e2, U=args.k_u), gq=args.gq,
                l1bn=any(nd.get("bn") for nd in synth.conv_nodes(wl)), bn_input=args.bn_input,
+               step_issue="replay of the recorded step tape" if replay else "python",
                conv_tops_over_conv_time=conv_tops,
                conv_pct_int8_peak_over_conv_time=(100.0 * conv_tops / INT8_PEAK_TOPS) if conv_tops else None)
     status = net.read_status()

@@ -619,6 +619,55 @@ int iseg_check_codes(const int8_t* x, int64_t n, int32_t bits, int32_t* dev_stat
 /* Library version string (static storage). */
 const char* iseg_version(void);
 
+/* ------------------------------------------------------------------------ */
+/* Step tape: native replay of a recorded sequence of calls                  */
+/* ------------------------------------------------------------------------ */
+/* A training step is a fixed sequence of the calls above on a few streams,
+ * ordered by events, reading and writing the same buffers every step.  A
+ * tape holds such a sequence, recorded once, and replays it from native code
+ * (no per-call work of the caller's language runtime); it is how a caller
+ * keeps the host side of a step short.  Nothing here is part of the paper's
+ * method: it issues exactly the calls that were recorded.
+ *
+ * iseg_tape_entry -- index of an entry point by name (one of the int-returning
+ *   compute calls above and iseg_profile_arm / iseg_status_clear /
+ *   iseg_check_codes), or -1; iseg_tape_entry_nargs -- its parameter count.
+ * iseg_tape_add_call -- append a call: words[n_words] are its arguments in
+ *   declaration order, each as a 64-bit word (pointers and handles as
+ *   addresses, integers sign- or zero-extended; the declared type is restored
+ *   on replay).  blob (blob_bytes, a multiple of 8, host memory copied into the
+ *   tape) holds the host structures and arrays the call reads through pointer
+ *   arguments; the words listed in blob_words hold byte offsets into it and
+ *   become addresses of the tape's copy.  step_word (-1: none) names the
+ *   argument that carries the step counter of the stochastic rounding: on a
+ *   run with step s it is step_base + s.  A recorded iseg_profile_arm becomes
+ *   an armed slot (see iseg_tape_set_arm_events).
+ * iseg_tape_add_record / iseg_tape_add_wait -- hipEventRecord(slot, stream) /
+ *   hipStreamWaitEvent(stream, slot) on tape-owned events (created on first use).
+ * iseg_tape_set_arm_events -- events[runs][n_arm][2] (start, stop) for the
+ *   armed slots of the next `runs` runs, one set per run; an armed slot of any
+ *   other run does nothing (the recorded events may no longer exist).
+ * iseg_tape_run -- replay every operation in order on its recorded stream;
+ *   stops at the first call that does not return ISEG_OK, returns that code
+ *   and its index in *failed_op (-1 if none).  The caller keeps every buffer,
+ *   stream and workspace the recorded calls use alive and unchanged in size,
+ *   and must not run the same tape from two threads at once.
+ * Memory: the tape itself lives in host memory (iseg_tape_create /
+ *   iseg_tape_destroy, NULL if out of memory); its events are destroyed with it. */
+void* iseg_tape_create(void);
+void iseg_tape_destroy(void* tape);
+int iseg_tape_entry(const char* name);
+int iseg_tape_entry_nargs(int entry);
+int iseg_tape_add_call(void* tape, int entry, const uint64_t* words, int n_words, const void* blob,
+                       size_t blob_bytes, const int32_t* blob_words, int n_blob_words, int32_t step_word,
+                       int64_t step_base);
+int iseg_tape_add_record(void* tape, int32_t slot, hipStream_t stream);
+int iseg_tape_add_wait(void* tape, hipStream_t stream, int32_t slot);
+int iseg_tape_arm_count(const void* tape);
+int iseg_tape_set_arm_events(void* tape, const hipEvent_t* events, int32_t runs);
+int iseg_tape_run(void* tape, uint32_t step, int64_t* failed_op);
+int64_t iseg_tape_size(const void* tape);
+
 #ifdef __cplusplus
 }
 #endif

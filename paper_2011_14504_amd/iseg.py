@@ -132,6 +132,17 @@ _SIGS = {
     "iseg_status_clear": ([_P, _P], C.c_int),
     "iseg_check_codes": ([_P, _I64, _I32, _P, _P], C.c_int),
     "iseg_version": ([], C.c_char_p),
+    "iseg_tape_create": ([], _P),
+    "iseg_tape_destroy": ([_P], None),
+    "iseg_tape_entry": ([C.c_char_p], C.c_int),
+    "iseg_tape_entry_nargs": ([C.c_int], C.c_int),
+    "iseg_tape_add_call": ([_P, C.c_int, _P, C.c_int, _P, _SZ, _P, C.c_int, _I32, _I64], C.c_int),
+    "iseg_tape_add_record": ([_P, _I32, _P], C.c_int),
+    "iseg_tape_add_wait": ([_P, _P, _I32], C.c_int),
+    "iseg_tape_arm_count": ([_P], C.c_int),
+    "iseg_tape_set_arm_events": ([_P, _P, _I32], C.c_int),
+    "iseg_tape_run": ([_P, _U32, _P], C.c_int),
+    "iseg_tape_size": ([_P], _I64),
 }
 
 
@@ -147,11 +158,17 @@ def lib():
             f.argtypes = args
             f.restype = res
         _lib = L
+    if _REC is not None:
+        return _REC.lib
     return _lib
 
 
 def _ptr(t):
-    return None if t is None else C.c_void_p(t.data_ptr())
+    if t is None:
+        return None
+    if _REC is not None:
+        _REC.keep.append(t)          # a recorded call's buffer stays allocated
+    return C.c_void_p(t.data_ptr())
 
 
 _raw_stream = torch._C._cuda_getCurrentRawStream if hasattr(torch._C, "_cuda_getCurrentRawStream") else None
@@ -349,6 +366,8 @@ def iseg_maxpool_bwd(dy, dy_exp, x, k, stride, pad, bits, dx, dx_exp, ws, status
 
 
 def _ptr_array(ts):
+    if _REC is not None:
+        _REC.keep.extend(t for t in ts if t is not None)
     return (C.c_void_p * len(ts))(*[None if t is None else t.data_ptr() for t in ts])
 
 
@@ -415,7 +434,7 @@ def iseg_mse_onehot(y, y_exp, labels, bits, loss, err, err_exp, ws, status=None)
 
 def mse_onehot(y, y_exp, labels, bits=8, status=None):
     """(loss, E1 codes, exponent) of the MSE loss against one-hot labels."""
-    loss = torch.zeros(1, dtype=torch.float64, device=y.device)
+    loss = torch.empty(1, dtype=torch.float64, device=y.device)     # written whole by the kernel
     err = torch.empty_like(y)
     e = _out_exp(y.device)
     ws = workspace(y.device).get(lib().iseg_mse_onehot_ws(y.numel()))
@@ -599,6 +618,183 @@ def workspace(device, bn=False):
     if ws is None:
         ws = _WS[key] = Workspace(torch.device("cuda", idx) if d.type == "cuda" else d, zeroed=bn)
     return ws
+
+
+# --------------------------------------------------------------------------
+# step tape: the calls of one step recorded, then replayed from native code
+# --------------------------------------------------------------------------
+_REC = None
+
+# parameter index of the step counter (stochastic rounding, Eq. 5-6)
+_STEP_ARG = {"iseg_conv_bwd_weight": 9, "iseg_update_multi": 4, "iseg_bn_param_update": 9, "iseg_requant": 9}
+_U64_MASK = (1 << 64) - 1
+
+
+def iseg_tape_create():
+    return C.c_void_p(lib().iseg_tape_create())
+
+
+def iseg_tape_destroy(h):
+    lib().iseg_tape_destroy(h)
+
+
+def iseg_tape_entry(name):
+    return int(lib().iseg_tape_entry(name.encode()))
+
+
+def iseg_tape_entry_nargs(entry):
+    return int(lib().iseg_tape_entry_nargs(entry))
+
+
+def iseg_tape_add_call(h, entry, words, blob, blob_words, step_word, step_base):
+    w = (C.c_uint64 * max(len(words), 1))(*words)
+    bw = (C.c_int32 * max(len(blob_words), 1))(*blob_words)
+    b = (C.c_char * max(len(blob), 1)).from_buffer_copy(bytes(blob) or b"\0")
+    _check(lib().iseg_tape_add_call(h, entry, w, len(words), b, len(blob), bw, len(blob_words), step_word,
+                                    step_base), "iseg_tape_add_call")
+
+
+def iseg_tape_add_record(h, slot, stream_handle):
+    _check(lib().iseg_tape_add_record(h, slot, C.c_void_p(stream_handle)), "iseg_tape_add_record")
+
+
+def iseg_tape_add_wait(h, stream_handle, slot):
+    _check(lib().iseg_tape_add_wait(h, C.c_void_p(stream_handle), slot), "iseg_tape_add_wait")
+
+
+def iseg_tape_arm_count(h):
+    return int(lib().iseg_tape_arm_count(h))
+
+
+def iseg_tape_set_arm_events(h, events, runs):
+    """events: (start, stop) pairs of hipEvent_t handles, runs x armed calls of them."""
+    flat = (C.c_void_p * max(len(events) * 2, 1))(*[e for pair in events for e in pair])
+    _check(lib().iseg_tape_set_arm_events(h, flat, runs), "iseg_tape_set_arm_events")
+
+
+def iseg_tape_run(h, step):
+    failed = C.c_int64(-1)
+    rc = lib().iseg_tape_run(h, int(step) & 0xFFFFFFFF, C.byref(failed))
+    if rc != ISEG_OK:
+        raise IsegError(f"iseg_tape_run: operation {failed.value} returned {_ERRS.get(rc, rc)}")
+
+
+def iseg_tape_size(h):
+    return int(lib().iseg_tape_size(h))
+
+
+class _RecLib:
+    """The library as seen while a tape records: each call of a tape entry
+    point runs, then is appended to the tape."""
+
+    def __init__(self, tape):
+        self._tape = tape
+
+    def __getattr__(self, name):
+        f = getattr(_lib, name)
+        if not name.startswith("iseg_") or name.startswith("iseg_tape_") or name not in self._tape.entries:
+            return f
+        tape = self._tape
+
+        def call(*args):
+            rc = f(*args)
+            if rc == ISEG_OK:
+                tape.add_call(name, args)
+            return rc
+        return call
+
+
+class Tape:
+    """One training step's library calls and stream orderings, recorded while
+    the step runs inside `with tape:` (every call of a tape entry point made
+    then is appended after it returns ISEG_OK), replayed from native code by
+    run(step).  Keeps every buffer the recorded calls use allocated; the
+    caller keeps the streams alive and replays with the same stream setup.""" 
+
+    def __init__(self, step):
+        L = lib()
+        self.h = iseg_tape_create()
+        if not self.h.value:
+            raise IsegError("iseg_tape_create failed")
+        self.step = int(step)
+        self.keep = []
+        self.slots = 0
+        self.arms = []
+        self.entries = {n: L.iseg_tape_entry(n.encode()) for n in _SIGS if n.startswith("iseg_")}
+        self.entries = {n: e for n, e in self.entries.items() if e >= 0}
+        self.lib = _RecLib(self)
+
+    def __enter__(self):
+        global _REC
+        if _REC is not None:
+            raise IsegError("a tape is already recording")
+        _REC = self
+        return self
+
+    def __exit__(self, *exc):
+        global _REC
+        _REC = None
+        return False
+
+    def add_call(self, name, args):
+        argtypes = getattr(_lib, name).argtypes
+        words, blob, blob_words = [], bytearray(), []
+        for i, a in enumerate(args):
+            if a is None:
+                words.append(0)
+            elif isinstance(a, C.c_void_p):
+                words.append(a.value or 0)
+            elif type(a).__name__ == "CArgObject" or isinstance(a, C.Array):
+                obj = a._obj if type(a).__name__ == "CArgObject" else a
+                blob_words.append(i)
+                words.append(len(blob))
+                blob += C.string_at(C.addressof(obj), C.sizeof(obj))
+                blob += bytes(-len(blob) % 8)
+            elif isinstance(a, C._SimpleCData):
+                words.append(int(a.value) & _U64_MASK)
+            elif isinstance(a, int):
+                words.append(a & _U64_MASK)
+            else:
+                raise IsegError(f"{name}: argument {i} of type {type(a).__name__} cannot be recorded")
+            if argtypes[i] is not _P and isinstance(a, C.c_void_p):
+                raise IsegError(f"{name}: argument {i} is a pointer where an integer is declared")
+        sw = _STEP_ARG.get(name, -1)
+        base = int(args[sw].value if isinstance(args[sw], C._SimpleCData) else args[sw]) - self.step if sw >= 0 else 0
+        if name == "iseg_profile_arm":
+            self.arms.append(int(args[0]))
+        iseg_tape_add_call(self.h, self.entries[name], words, blob, blob_words, sw, base)
+
+    def new_slot(self):
+        self.slots += 1
+        return self.slots - 1
+
+    def add_record(self, slot, stream_handle):
+        iseg_tape_add_record(self.h, slot, stream_handle)
+
+    def add_wait(self, stream_handle, slot):
+        iseg_tape_add_wait(self.h, stream_handle, slot)
+
+    def set_arm_events(self, events, runs):
+        """events: runs x (armed calls) (start, stop) pairs of hipEvent_t handles."""
+        iseg_tape_set_arm_events(self.h, events, runs)
+
+    def size(self):
+        return iseg_tape_size(self.h)
+
+    def run(self, step):
+        iseg_tape_run(self.h, step)
+
+    def close(self):
+        if self.h is not None and self.h.value:
+            iseg_tape_destroy(self.h)
+        self.h = None
+        self.keep = []
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def _out_exp(device):

@@ -32,7 +32,7 @@ from . import iseg
 
 class IntNet:
     def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1,
-                 bn_input="q8"):
+                 bn_input="q8", branch_streams=3, replay_from=None):
         if not (2 <= k_W <= 8 and 9 <= k_U <= 31 and gq in (1, 2)):
             raise ValueError("k_W must be in [2, 8], k_U in [9, 31], gq 1 or 2")
         if bn_input not in ("q8", "raw"):
@@ -60,6 +60,20 @@ class IntNet:
         # conv's weight gradient only needs its dz and input, so it overlaps
         # the backward-data / L1BN / merge chain of the layers below
         self.side = torch.cuda.Stream(device=self.dev) if self.dev.type == "cuda" else None
+        # branches of the graph (a projection shortcut, the ASPP branches) run
+        # on streams of their own (default priority) so that their
+        # latency-bound kernels overlap the other branch; forward and
+        # backward of a node use the same stream
+        nb = branch_streams if self.side is not None else 0
+        self.branch = [torch.cuda.Stream(device=self.dev) for _ in range(nb)]
+        self.node_stream = self._plan_streams(wl["nodes"], nb)
+        # nodes with a reader on another stream (an event marks their output)
+        self.cross = {src for nd in wl["nodes"] for src in nd["src"]
+                      if src != "input" and self.node_stream[src] != self.node_stream[nd["name"]]}
+        # nodes whose backward sends errors to a source on another stream (the
+        # input's error is merged on the caller's stream)
+        self.bwd_cross = {nd["name"] for nd in wl["nodes"] for src in nd["src"]
+                          if self.node_stream[src] != self.node_stream[nd["name"]]}
         # one sticky device status word for every call of the step (range
         # violations the kernels detect: merge exponent gaps, BN exponents out
         # of range, bad labels, logits outside the loss region's domain)
@@ -105,6 +119,15 @@ class IntNet:
         self._build_update_table()
         self.wt_tab = None
         self.loss = None
+        # step replay: step number `replay_from` runs and is recorded into a
+        # tape (every library call and stream ordering, the step counter of
+        # the stochastic rounding as a parameter); later steps replay the tape
+        # from native code and return that step's record, whose tensors each
+        # replay rewrites
+        self.replay_from = replay_from if self.side is not None else None
+        self.tape = None
+        self._tape_rec = None
+        self._tape_out = None
 
     def _build_update_table(self):
         """Every parameter tensor of the network for one iseg_update_multi launch."""
@@ -147,61 +170,134 @@ class IntNet:
     def _transpose_weights(self):
         iseg.iseg_weight_transpose_multi(self.wt_tab, self.wt_n, self.wt_tiles)
 
+    @staticmethod
+    def _plan_streams(nodes, nbranch):
+        """Stream index of every node (0: the caller's current stream, k >= 1:
+        branch stream k).  A one-input node that is not the last one-input
+        reader (in node order) of its input opens a branch on the next branch
+        stream (round robin); a one-input node otherwise continues its input's
+        stream; a node with several inputs (a merge) runs on the stream of its
+        input that comes last."""
+        order = {nd["name"]: i for i, nd in enumerate(nodes)}
+        order["input"] = -1
+        readers = {}
+        for nd in nodes:
+            if len(nd["src"]) == 1:
+                readers.setdefault(nd["src"][0], []).append(nd["name"])
+        st, nxt = {"input": 0}, 0
+        for nd in nodes:
+            src = nd["src"]
+            if len(src) > 1:
+                st[nd["name"]] = st[max(src, key=lambda n: order[n])]
+            elif nbranch and readers[src[0]][-1] != nd["name"]:
+                nxt = nxt % nbranch + 1
+                st[nd["name"]] = nxt
+            else:
+                st[nd["name"]] = st[src[0]]
+        return st
+
+    def _streams(self):
+        if self.side is None:
+            return [None]
+        return [torch.cuda.current_stream(self.dev)] + self.branch
+
+    # stream orderings go through these so that a recording tape sees them
+    def _record(self, stream):
+        ev = stream.record_event()
+        slot = None
+        if self._tape_rec is not None:
+            slot = self._tape_rec.new_slot()
+            self._tape_rec.add_record(slot, stream.cuda_stream)
+        return ev, slot
+
+    def _wait(self, stream, tok):
+        stream.wait_event(tok[0])
+        if self._tape_rec is not None:
+            self._tape_rec.add_wait(stream.cuda_stream, tok[1])
+
+    def _join(self, stream, other):
+        """stream waits for the work enqueued on other so far"""
+        self._wait(stream, self._record(other))
+
+    @staticmethod
+    def _on(stream, idx, fn):
+        """fn() with `stream` current (the caller's stream needs no switch)"""
+        if idx == 0:
+            return fn()
+        with torch.cuda.stream(stream):
+            return fn()
+
     # -------------------------------------------------------------------
     def forward(self):
         act = {"input": (self.x, self.x_exp)}
         rec = {}
+        streams = self._streams()
+        for b in self.branch:
+            self._join(b, streams[0])
+        ready = {}
         for nd in self.wl["nodes"]:
-            k, name = nd["kind"], nd["name"]
-            a, ae = act[nd["src"][0]]
-            r = dict(kind=k, a_in=a, a_in_exp=ae)
-            if k == "conv":
-                L = self.convs[name]
-                raw = self.bn_raw and nd["bn"]
-                if nd.get("transposed"):
-                    # the adjoint of the conv whose input has this node's output shape
-                    N, h, w, _ = a.shape
-                    H = (h - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
-                    W = (w - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
-                    z, ze = iseg.conv_bwd_data(a, ae, L["w_q"], self.w_exp, (N, H, W, nd["cout"]), nd["stride"],
-                                               nd["pad"], nd["dil"], wt=L.get("w_t"), wt_kind=L.get("wt_kind", 0),
-                                               status=self.status)
-                else:
-                    z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
-                                          out_mode=iseg.ISEG_OUT_RAW if raw else iseg.ISEG_OUT_Q8,
-                                          status=self.status)
-                r.update(z=z, z_exp=ze)
-                if nd["bn"]:
-                    y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])],
-                                               status=self.status)
-                    r["saved"] = saved
-                elif nd["relu"] or self.k_A < 8:
-                    # without BN: A = Q_A(ReLU?(Z)) on the 8-bit conv output
-                    y, ye = iseg.sum_requant([z], [ze], relu=nd["relu"], bits=self.k_A, status=self.status)
-                else:
-                    y, ye = z, ze
-            elif k == "maxpool":
-                y, ye = iseg.maxpool_fwd(a, ae, nd["k"], nd["stride"], nd["pad"])
-            elif k == "add":
-                b, be = act[nd["src"][1]]
-                y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"], bits=self.k_A,
-                                          status=self.status)
-                r.update(b_in=b, b_in_exp=be)
-            elif k == "gap":
-                y, ye = iseg.gap_fwd(a, ae, bits=self.k_A, status=self.status)
-            elif k == "concat":
-                parts = [act[s] for s in nd["src"]]
-                y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts], bits=self.k_A,
-                                             status=self.status)
-                H, W = y.shape[1], y.shape[2]
-                r.update(widths=[p[0].shape[3] for p in parts],
-                         bcast=[tuple(p[0].shape[1:3]) != (H, W) for p in parts])
-            else:
-                raise ValueError(k)
-            r.update(a_out=y, a_out_exp=ye)
-            rec[name] = r
-            act[name] = (y, ye)
+            si = self.node_stream[nd["name"]]
+            for src in nd["src"]:
+                if src != "input" and self.node_stream[src] != si:   # the input is ready before the branches start
+                    self._wait(streams[si], ready[src])
+                    for t in act[src]:
+                        t.record_stream(streams[si])
+            rec[nd["name"]], act[nd["name"]] = self._on(streams[si], si, lambda: self._fwd_node(nd, act))
+            if nd["name"] in self.cross:
+                ready[nd["name"]] = self._record(streams[si])
+        for b in self.branch:
+            self._join(streams[0], b)
         return rec
+
+    def _fwd_node(self, nd, act):
+        k, name = nd["kind"], nd["name"]
+        a, ae = act[nd["src"][0]]
+        r = dict(kind=k, a_in=a, a_in_exp=ae)
+        if k == "conv":
+            L = self.convs[name]
+            raw = self.bn_raw and nd["bn"]
+            if nd.get("transposed"):
+                # the adjoint of the conv whose input has this node's output shape
+                N, h, w, _ = a.shape
+                H = (h - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+                W = (w - 1) * nd["stride"] - 2 * nd["pad"] + nd["dil"] * (nd["R"] - 1) + 1
+                z, ze = iseg.conv_bwd_data(a, ae, L["w_q"], self.w_exp, (N, H, W, nd["cout"]), nd["stride"],
+                                           nd["pad"], nd["dil"], wt=L.get("w_t"), wt_kind=L.get("wt_kind", 0),
+                                           status=self.status)
+            else:
+                z, ze = iseg.conv_fwd(a, ae, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
+                                      out_mode=iseg.ISEG_OUT_RAW if raw else iseg.ISEG_OUT_Q8,
+                                      status=self.status)
+            r.update(z=z, z_exp=ze)
+            if nd["bn"]:
+                y, ye, saved = iseg.bn_fwd(z, ze, L["g_q"], L["b_q"], self._cfgs[int(nd["relu"])],
+                                           status=self.status)
+                r["saved"] = saved
+            elif nd["relu"] or self.k_A < 8:
+                # without BN: A = Q_A(ReLU?(Z)) on the 8-bit conv output
+                y, ye = iseg.sum_requant([z], [ze], relu=nd["relu"], bits=self.k_A, status=self.status)
+            else:
+                y, ye = z, ze
+        elif k == "maxpool":
+            y, ye = iseg.maxpool_fwd(a, ae, nd["k"], nd["stride"], nd["pad"])
+        elif k == "add":
+            b, be = act[nd["src"][1]]
+            y, ye = iseg.sum_requant([a, b], [ae, be], relu=nd["relu"], bits=self.k_A,
+                                      status=self.status)
+            r.update(b_in=b, b_in_exp=be)
+        elif k == "gap":
+            y, ye = iseg.gap_fwd(a, ae, bits=self.k_A, status=self.status)
+        elif k == "concat":
+            parts = [act[s] for s in nd["src"]]
+            y, ye = iseg.concat_requant([p[0] for p in parts], [p[1] for p in parts], bits=self.k_A,
+                                         status=self.status)
+            H, W = y.shape[1], y.shape[2]
+            r.update(widths=[p[0].shape[3] for p in parts],
+                     bcast=[tuple(p[0].shape[1:3]) != (H, W) for p in parts])
+        else:
+            raise ValueError(k)
+        r.update(a_out=y, a_out_exp=ye)
+        return r, (y, ye)
 
     def loss_error(self, rec):
         out = rec[self.wl["nodes"][-1]["name"]]
@@ -217,12 +313,22 @@ class IntNet:
 
     def backward(self, rec):
         contrib = {}
+        streams = self._streams()
+        for b in self.branch:
+            self._join(b, streams[0])
+        done = {}           # node -> event after its backward, when a source runs on another stream
+        sender = ["loss"]
 
         def send(name, codes, exp, exp_add=0, bcast=0):
-            contrib.setdefault(name, []).append((codes, exp, exp_add, bcast))
+            contrib.setdefault(name, []).append((codes, exp, exp_add, bcast, sender[0]))
 
-        def merged(name):
+        def merged(name, si):
             parts = contrib.pop(name)
+            for p in parts:
+                if p[4] in done and self._stream_of(p[4]) != si:
+                    self._wait(streams[si], done[p[4]])
+                    for t in p[:2]:
+                        t.record_stream(streams[si])
             if len(parts) == 1 and not parts[0][2] and not parts[0][3]:
                 return parts[0][0], parts[0][1]
             return iseg.sum_requant([p[0] for p in parts], [p[1] for p in parts],
@@ -234,78 +340,92 @@ class IntNet:
             self._transpose_weights()
         e, ee = self.loss_error(rec)
         send(self.wl["nodes"][-1]["name"], e, ee)
-        want_input = self.wl["input_grad"]
+        if self.node_stream[self.wl["nodes"][-1]["name"]] != 0:
+            done["loss"] = self._record(streams[0])
         grads = []
         for nd in reversed(self.wl["nodes"]):
-            k, name = nd["kind"], nd["name"]
-            r = rec[name]
-            e, ee = merged(name)
-            r.update(e_out=e, e_out_exp=ee)
-            src = nd["src"][0]
-            need_in = src != "input" or want_input
-            if k == "conv":
-                L = self.convs[name]
-                if nd["bn"]:
-                    dz, dze, dg, db, dge, dbe = iseg.bn_bwd(e, ee, r["z"], L["g_q"], r["saved"],
-                                                            self._cfgs[int(nd["relu"])],
-                                                            status=self.status, dgb_out=(L["dg"], L["db"], L["dg_exp"],
-                                                                     L["db_exp"]))
-                    r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
-                elif nd["relu"]:
-                    dz, dze = iseg.relu_mask_bwd(e, [r["z"]], [r["z_exp"]], status=self.status), ee
-                else:
-                    dz, dze = e, ee
-                G, Ge = self._wgrad(nd, L, r, dz, dze)
-                r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
-                grads.append((nd, r))
-                if need_in and nd.get("transposed"):
-                    # the input error of a transposed conv is the forward of the
-                    # conv it is the adjoint of
-                    ei, eie = iseg.conv_fwd(dz, dze, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
-                                            status=self.status)
-                    r.update(e_in=ei, e_in_exp=eie)
-                    send(src, ei, eie)
-                elif need_in:
-                    ei, eie = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
-                                                 nd["stride"], nd["pad"], nd["dil"], wt=L.get("w_t"),
-                                                 wt_kind=L["wt_kind"], status=self.status)
-                    r.update(e_in=ei, e_in_exp=eie)
-                    send(src, ei, eie)
-            elif k == "maxpool":
-                if need_in:
-                    ei, eie = iseg.maxpool_bwd(e, ee, r["a_in"], nd["k"], nd["stride"], nd["pad"],
-                                               status=self.status)
-                    r.update(e_in=ei, e_in_exp=eie)
-                    send(src, ei, eie)
-            elif k == "add":
-                d = (iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]],
-                                        status=self.status) if nd["relu"] else e)
-                r.update(e_in=d, e_in_exp=ee)
-                for s in nd["src"]:
-                    if s != "input" or want_input:
-                        send(s, d, ee)
-            elif k == "gap":
-                if need_in:
-                    H, W = r["a_in"].shape[1:3]
-                    eg, ege = iseg.gap_bwd(e, ee, H, W, status=self.status)
-                    r.update(e_in=eg, e_in_exp=ege)
-                    send(src, eg, ege, bcast=1)
-            elif k == "concat":
-                parts = iseg.concat_split(e, r["widths"], skip=r["bcast"])
-                c0 = 0
-                for s, p, wdt, bc in zip(nd["src"], parts, r["widths"], r["bcast"]):
-                    if bc:
-                        pe, pee = iseg.spatial_sum(e, ee, 1, c0, wdt, status=self.status)
-                        send(s, pe, pee)
-                    else:
-                        send(s, p, ee)
-                    c0 += wdt
-        if want_input:
-            e, ee = merged("input")
+            si = self.node_stream[nd["name"]]
+            sender[0] = nd["name"]
+            self._on(streams[si], si, lambda: self._bwd_node(nd, rec, merged, send, grads, si))
+            if nd["name"] in self.bwd_cross:
+                done[nd["name"]] = self._record(streams[si])
+        if self.wl["input_grad"]:
+            e, ee = merged("input", 0)
             rec["input"] = dict(kind="input", e_out=e, e_out_exp=ee)
+        for b in self.branch:
+            self._join(streams[0], b)
         if self.side is not None:
-            torch.cuda.current_stream(self.dev).wait_stream(self.side)
+            self._join(streams[0], self.side)
         return grads
+
+    def _stream_of(self, name):
+        return 0 if name == "loss" else self.node_stream[name]
+
+    def _bwd_node(self, nd, rec, merged, send, grads, si):
+        k, name = nd["kind"], nd["name"]
+        want_input = self.wl["input_grad"]
+        r = rec[name]
+        e, ee = merged(name, si)
+        r.update(e_out=e, e_out_exp=ee)
+        src = nd["src"][0]
+        need_in = src != "input" or want_input
+        if k == "conv":
+            L = self.convs[name]
+            if nd["bn"]:
+                dz, dze, dg, db, dge, dbe = iseg.bn_bwd(e, ee, r["z"], L["g_q"], r["saved"],
+                                                        self._cfgs[int(nd["relu"])],
+                                                        status=self.status, dgb_out=(L["dg"], L["db"], L["dg_exp"],
+                                                                 L["db_exp"]))
+                r.update(dgamma=dg, dbeta=db, dgamma_exp=dge, dbeta_exp=dbe)
+            elif nd["relu"]:
+                dz, dze = iseg.relu_mask_bwd(e, [r["z"]], [r["z_exp"]], status=self.status), ee
+            else:
+                dz, dze = e, ee
+            G, Ge = self._wgrad(nd, L, r, dz, dze)
+            r.update(dz=dz, dz_exp=dze, G=G, G_exp=Ge)
+            grads.append((nd, r))
+            if need_in and nd.get("transposed"):
+                # the input error of a transposed conv is the forward of the
+                # conv it is the adjoint of
+                ei, eie = iseg.conv_fwd(dz, dze, L["w_q"], self.w_exp, nd["stride"], nd["pad"], nd["dil"],
+                                        status=self.status)
+                r.update(e_in=ei, e_in_exp=eie)
+                send(src, ei, eie)
+            elif need_in:
+                ei, eie = iseg.conv_bwd_data(dz, dze, L["w_q"], self.w_exp, r["a_in"].shape,
+                                             nd["stride"], nd["pad"], nd["dil"], wt=L.get("w_t"),
+                                             wt_kind=L["wt_kind"], status=self.status)
+                r.update(e_in=ei, e_in_exp=eie)
+                send(src, ei, eie)
+        elif k == "maxpool":
+            if need_in:
+                ei, eie = iseg.maxpool_bwd(e, ee, r["a_in"], nd["k"], nd["stride"], nd["pad"],
+                                           status=self.status)
+                r.update(e_in=ei, e_in_exp=eie)
+                send(src, ei, eie)
+        elif k == "add":
+            d = (iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]],
+                                    status=self.status) if nd["relu"] else e)
+            r.update(e_in=d, e_in_exp=ee)
+            for s in nd["src"]:
+                if s != "input" or want_input:
+                    send(s, d, ee)
+        elif k == "gap":
+            if need_in:
+                H, W = r["a_in"].shape[1:3]
+                eg, ege = iseg.gap_bwd(e, ee, H, W, status=self.status)
+                r.update(e_in=eg, e_in_exp=ege)
+                send(src, eg, ege, bcast=1)
+        elif k == "concat":
+            parts = iseg.concat_split(e, r["widths"], skip=r["bcast"])
+            c0 = 0
+            for s, p, wdt, bc in zip(nd["src"], parts, r["widths"], r["bcast"]):
+                if bc:
+                    pe, pee = iseg.spatial_sum(e, ee, 1, c0, wdt, status=self.status)
+                    send(s, pe, pee)
+                else:
+                    send(s, p, ee)
+                c0 += wdt
 
     def _wgrad(self, nd, L, r, dz, dze):
         """Q_G(backward-weight) of one conv (Eq. 17), on the side stream once
@@ -320,9 +440,9 @@ class IntNet:
                     self.g_mode, 8, self.seed, 16 * L["l"], self.step_no)
         if self.side is None:
             return iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]), status=self.status)
-        ready = torch.cuda.current_stream(self.dev).record_event()
+        ready = self._record(torch.cuda.current_stream(self.dev))
         with torch.cuda.stream(self.side):
-            self.side.wait_event(ready)
+            self._wait(self.side, ready)
             G, Ge = iseg.conv_bwd_weight(*args, out=(L["G"], L["G_exp"]), status=self.status)
         for t in (dz, dze, r["a_in"], r["a_in_exp"]):
             t.record_stream(self.side)
@@ -367,7 +487,25 @@ class IntNet:
         the current stream): 0, or ISEG_DEV_* bits."""
         return iseg.iseg_status_read(self.status)
 
-    def step(self):
+    def step(self, eager=False):
+        """One training step; with a recorded tape a replay unless `eager`."""
+        if self.tape is not None and not eager:
+            self.tape.run(self.step_no)
+            self.step_no += 1
+            return self._tape_out
+        if self.replay_from is not None and self.tape is None and self.step_no >= self.replay_from:
+            tape = iseg.Tape(self.step_no)
+            self._tape_rec = tape
+            try:
+                with tape:
+                    rec = self._step()
+            finally:
+                self._tape_rec = None
+            self.tape, self._tape_out = tape, rec
+            return rec
+        return self._step()
+
+    def _step(self):
         rec = self.forward()
         grads = self.backward(rec)
         self.update(grads)

@@ -23,14 +23,14 @@ CONV_KEYS = ("z", "dz", "G", "Gg", "Gb", "dgamma", "dbeta")
 EXP_KEYS = ("z_exp", "dz_exp", "G_exp", "Gg_exp", "Gb_exp")
 
 
-def _run_both(wl, steps=1, **widths):
+def _run_both(wl, steps=1, replay_from=None, **widths):
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from oracle.model import OracleNet
     from paper_2011_14504_amd.model import IntNet
     inp = synth.workload_inputs(wl)
-    gnet = IntNet(wl, inp, "cuda:0", **widths)
+    gnet = IntNet(wl, inp, "cuda:0", replay_from=replay_from, **widths)
     onet = OracleNet(wl, inp, **widths)
     for s in range(steps):
         print(f"[pipeline] {wl['name']} N={wl['N']} {wl['H']}x{wl['W']} {widths} step {s}", flush=True)
@@ -89,6 +89,17 @@ def test_deeplabv3_r50_128px():
     # the whole DeepLabv3-ResNet50 step at 128x128 (ASPP on a 8x8 map, where
     # rates 12 and 18 leave only the centre tap), softmax loss over 150 classes
     _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 128, 128))
+
+
+def test_deeplabv3_r50_replayed_steps():
+    # step 1 is recorded into a tape, steps 2 and 3 replay it from native code
+    # (the step counter of the stochastic rounding rebased on each replay)
+    _run_both(synth.scaled(synth.DEEPLABV3_R50, 1, 96, 80), steps=4, replay_from=1)
+
+
+def test_resnet50_conv2x_replayed_steps_k_e2_8():
+    # the rounding-E2 backward and the projection branch on its own stream, replayed
+    _run_both(synth.scaled(synth.RESNET50_CONV2X, 2, 28, 28), steps=3, replay_from=1, bn_cfg={"k_E2": 8})
 
 
 def test_deeplabv3_r50_ragged_96x80_two_steps():

@@ -103,3 +103,25 @@ def test_transposed_weight_host_checks(lib):
     assert lib.iseg_weight_transpose_multi(None, 0, 0, None) == iseg.ISEG_OK
     assert lib.iseg_weight_transpose_multi(None, -1, 1, None) == iseg.ISEG_ERR_ARG
     assert lib.iseg_weight_transpose_multi(None, 1, 0, None) == iseg.ISEG_ERR_ARG
+
+
+def test_tape_entries_match_the_binding():
+    """The step tape resolves every call a training step makes, each with the
+    parameter count of its declaration in the binding."""
+    from paper_2011_14504_amd import iseg
+    L = iseg.lib()
+    step_calls = ["iseg_conv_fwd", "iseg_conv_bwd_data", "iseg_conv_bwd_data_t", "iseg_conv_bwd_weight",
+                  "iseg_weight_transpose_multi", "iseg_bn_fwd", "iseg_bn_bwd", "iseg_bn_fwd_i32",
+                  "iseg_bn_bwd_i32", "iseg_update_multi", "iseg_maxpool_fwd", "iseg_maxpool_bwd",
+                  "iseg_sum_requant", "iseg_relu_mask_bwd", "iseg_concat_requant", "iseg_concat_split",
+                  "iseg_spatial_sum", "iseg_softmax_ce", "iseg_mse_onehot", "iseg_profile_arm"]
+    for name in step_calls:
+        assert L.iseg_tape_entry(name.encode()) >= 0, name
+    n = 0
+    for name, (args, res) in iseg._SIGS.items():
+        e = L.iseg_tape_entry(name.encode())
+        if e >= 0:
+            assert L.iseg_tape_entry_nargs(e) == len(args), name
+            n += 1
+    assert n >= len(step_calls)
+    assert L.iseg_tape_entry(b"iseg_nonexistent") == -1
