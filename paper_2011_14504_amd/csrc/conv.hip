@@ -2322,6 +2322,10 @@ DmaPlan dma_plan(int64_t Mrows, int32_t Nout, int32_t Kred, bool q8)
         const int nk = Kred / BK;
         while (p.splits < kMaxSplits && blocks * p.splits < ISEG_IGEMM_SPLIT_BLOCKS && nk / (2 * p.splits) >= 32)
             p.splits *= 2;
+        // a short reduction that leaves the chip under one block per CU takes
+        // 64-column tiles instead (twice the blocks); long reductions split
+        // instead, where 128 x 128 tiles keep their higher MFMA rate
+        if (p.splits == 1 && p.bn == 128 && blocks < 256) p.bn = 64;
     }
     return p;
 }
@@ -2634,6 +2638,30 @@ __device__ __forceinline__ void wt_tile(const int8_t* __restrict__ w, int8_t* __
                                         int32_t RS, int32_t C, bool flip, int32_t k0, int32_t c0, int32_t rs)
 {
     __shared__ int8_t t[64][65];
+    const int rso = flip ? RS - 1 - rs : rs;
+    if (((C | K) & 3) == 0 && ((((uintptr_t)w) | ((uintptr_t)wt)) & 3) == 0) {
+        // dword loads and stores: four channels per lane in, four k per lane out
+        const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int k = k0 + ty + 16 * j, c = c0 + 4 * tx;
+            const uint32_t v = (k < K && c < C) ? *(const uint32_t*)(w + ((uint32_t)k * RS + rs) * (uint32_t)C + c) : 0u;
+#pragma unroll
+            for (int e = 0; e < 4; e++) t[ty + 16 * j][4 * tx + e] = (int8_t)(v >> (8 * e));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int c = c0 + ty + 16 * j, k = k0 + 4 * tx;
+            if (c < C && k < K) {
+                uint32_t v = 0;
+#pragma unroll
+                for (int e = 0; e < 4; e++) v |= (uint32_t)(uint8_t)t[4 * tx + e][ty + 16 * j] << (8 * e);
+                *(uint32_t*)(wt + ((uint32_t)c * RS + rso) * (uint32_t)K + k) = v;
+            }
+        }
+        return;
+    }
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
 #pragma unroll
     for (int j = 0; j < 16; j++) {
@@ -2641,7 +2669,6 @@ __device__ __forceinline__ void wt_tile(const int8_t* __restrict__ w, int8_t* __
         t[ty + 4 * j][tx] = (k < K && c < C) ? w[((uint32_t)k * RS + rs) * (uint32_t)C + c] : (int8_t)0;
     }
     __syncthreads();
-    const int rso = flip ? RS - 1 - rs : rs;
 #pragma unroll
     for (int j = 0; j < 16; j++) {
         const int c = c0 + ty + 4 * j, k = k0 + tx;
@@ -2716,6 +2743,35 @@ static int launch_pad(const int8_t* in, int8_t* out, int64_t npix, int64_t C, in
     hipLaunchKernelGGL(k_pad_channels, dim3(grid_for(npix * Cp, 256, 8192)), dim3(256), 0, s, in, out,
                        npix, (int32_t)C, (int32_t)Cp);
     return launch_ok();
+}
+
+// A 1x1 stride-1 conv whose reduction channels for backward-data (its K,
+// e.g. a classifier's class count) are not a multiple of 64: dy and the
+// transposed weights padded with zero channels to the next multiple of 64 take
+// the direct-to-LDS path (the zero channels add nothing to the sums).
+static int64_t kpad_to(int64_t K) { return ceil_div64(K, 64) * 64; }
+
+static bool kpad_ok(const iseg_conv_geom* g)
+{
+    return g->R == 1 && g->S == 1 && g->stride_h == 1 && g->stride_w == 1 && g->pad_h == 0 && g->pad_w == 0 &&
+           g->K % 64 != 0 && g->C % 64 == 0 && g->N > 0 && g->N * g->H * g->W < ((int64_t)1 << 31);
+}
+
+static size_t kpad_bytes(const iseg_conv_geom* g)
+{
+    if (!kpad_ok(g)) return 0;
+    const int64_t Kp = kpad_to(g->K);
+    return align256((size_t)(g->N * g->H * g->W * Kp)) + align256((size_t)(g->C * Kp));
+}
+
+// wt[c][k] = w[k][c] for k < K, 0 up to Kp (1x1 weights KC -> C x Kp)
+__global__ void k_wt_pad_1x1(const int8_t* __restrict__ w, int8_t* __restrict__ wt, int32_t K, int32_t C, int32_t Kp)
+{
+    const int64_t n = (int64_t)C * Kp;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t c = (int32_t)(i / Kp), k = (int32_t)(i - (int64_t)c * Kp);
+        wt[i] = k < K ? w[(int64_t)k * C + c] : (int8_t)0;
+    }
 }
 
 __global__ void k_exp_sum(int32_t* out, const int32_t* a, const int32_t* b)
@@ -4212,7 +4268,7 @@ static size_t conv_bwd_data_core_ws(const iseg_conv_geom* g, int32_t out_mode)
         }
         s += big + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N, g->H, g->W);
     }
-    return s;
+    return s + kpad_bytes(g);
 }
 
 // backward-data with the transposed weights either built here from w (KRSC) or
@@ -4312,6 +4368,24 @@ static int conv_bwd_data_core(const int8_t* dy, const int32_t* dy_exp, const int
     const TconvPlan tp = tconv_plan(g);
     if (tp.ok)
         return tconv_run(tp, g, P, Q, dy, dy_exp, w, w_exp, out_mode, dx, dx_exp, (char*)ws + 256, stream);
+    if (kpad_ok(g) && (((uintptr_t)dy | (uintptr_t)dx) & 15) == 0) {
+        const int64_t Kp = kpad_to(g->K), M = g->N * g->H * g->W;
+        int8_t* dyp = (int8_t*)ws + (conv_bwd_data_core_ws(g, out_mode) - kpad_bytes(g));
+        int8_t* wtp = dyp + align256((size_t)(M * Kp));
+        if ((rc = launch_pad(dy, dyp, M, g->K, Kp, stream))) return rc;
+        hipLaunchKernelGGL(k_wt_pad_1x1, dim3(grid_for(g->C * Kp, 256, 1024)), dim3(256), 0, stream, w, wtp,
+                           (int32_t)g->K, (int32_t)g->C, (int32_t)Kp);
+        if ((rc = launch_ok())) return rc;
+        IgemmArgs a{};
+        a.src = dyp; a.wmat = wtp; a.out = acc; a.pmax = pmax;
+        a.out16 = nullptr; a.tshift = nullptr;
+        a.Mrows = M;
+        a.Nout = (int32_t)g->C; a.Kred = (int32_t)Kp; a.Ci = (int32_t)Kp;
+        a.Hs = (int32_t)P; a.Ws = (int32_t)Q; a.Ho = (int32_t)g->H; a.Wo = (int32_t)g->W;
+        a.R = 1; a.S = 1; a.sh = 1; a.sw = 1; a.ph = 0; a.pw = 0; a.dh = 1; a.dw = 1;
+        if (igemm_dma_ok(a))
+            return igemm_dma_run<MODE_BWD>(a, out_mode, dy_exp, w_exp, dx, dx_exp, pmax, acc, stream);
+    }
     wt = pick_wt(ISEG_WT_CRSK);
     if (wt != wt_in && (rc = launch_w_transpose(w, wt_ws, g->K, g->R * g->S, g->C, false, stream))) return rc;
     IgemmArgs a{};

@@ -91,6 +91,8 @@ struct CeCellArgs {
     int32_t nry, nrx;
     Run ry[kMaxRuns];
     Run rx[kMaxRuns];
+    int16_t ylo[64], yhi[64];  // per low-res row: first and last row run touching it
+    int16_t xlo[64], xhi[64];  // per low-res column: likewise for column runs
     double* cell;        // [N][nry][nrx][4][K]: corner sums (i0,j0),(i0,j1),(i1,j0),(i1,j1)
     double* cell_loss;   // [N][nry][nrx]
     double* grad;        // [N][h][w][K]
@@ -143,29 +145,186 @@ __device__ __forceinline__ double interp(double a00, double a01, double a10, dou
     return (wy0 * top + wy1 * bot) * scale;
 }
 
-// one block per cell, its rows split over the 4 waves: softmax of every pixel
-// (lanes over classes), the gradient folded into the cell's four low-res
-// corners (x first within a row, then the row weights), the cell's loss; the
-// waves' corner sums are added in wave order
+// One block per cell (three per CU: occupancy hides the latency of each
+// cell's loads and barriers).  A wave takes P = 64 / L rows of the cell at a time, one
+// row per group of L lanes; lane l of a group holds the classes l + L t
+// (t < KT).  Along a row the exps follow the cell's multiplicative recurrence
+// (one multiply per pixel and class), the softmax denominator is a group-wide
+// sum (DPP steps within a row of 16 lanes, no readlane) and one reciprocal per
+// pixel scales the gradient; two pixels of a row are in flight per step.  The
+// cell's per-class constants (the exp at its first pixel, the x- and y-step
+// ratios, the change of the x-step per row) are computed once per block; a
+// row's starting values are integer powers of them.  The one-hot part of the
+// gradient collects in LDS (one region per wave and group, added to by the
+// lane that owns the pixel's label with no-return LDS atomics, so no wait),
+// the corner sums of the groups are added in group order, then those of the
+// waves in wave order.
 constexpr int kCellWaves = 4;
 constexpr int kMaxRunLen = 256;
-constexpr int kLabBuf = 1024;
+constexpr int kLabPre = 4;        // label bytes per lane loaded ahead (a pass of up to 256 pixels)
 
-template <int KT>
-__global__ __launch_bounds__(256) void k_ce_cells(const CeCellArgs a)
+// v + v[lane ^ O] (O = 16, 32) by gfx950's cross-row swaps; the pair comes
+// back in a lane-dependent order, and the sum is the same bits either way
+template <int O>
+__device__ __forceinline__ double swap_sum_f64(double v)
 {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
+    uint32_t l0, l1, h0, h1;
+    if constexpr (O == 16) {
+        const auto rl = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto rh = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        l0 = rl[0]; l1 = rl[1]; h0 = rh[0]; h1 = rh[1];
+    } else {
+        const auto rl = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto rh = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        l0 = rl[0]; l1 = rl[1]; h0 = rh[0]; h1 = rh[1];
+    }
+    const double x = __longlong_as_double((long long)(((uint64_t)h0 << 32) | l0));
+    const double y = __longlong_as_double((long long)(((uint64_t)h1 << 32) | l1));
+    return x + y;
+}
+
+template <int O>
+__device__ __forceinline__ double swap_max_f64(double v)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
+    uint32_t l1, h1;
+    if constexpr (O == 16) {
+        const auto rl = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto rh = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        l1 = rl[0] == lo && rh[0] == hi ? rl[1] : rl[0];
+        h1 = rl[0] == lo && rh[0] == hi ? rh[1] : rh[0];
+    } else {
+        const auto rl = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto rh = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        l1 = rl[0] == lo && rh[0] == hi ? rl[1] : rl[0];
+        h1 = rl[0] == lo && rh[0] == hi ? rh[1] : rh[0];
+    }
+    return fmax(v, __longlong_as_double((long long)(((uint64_t)h1 << 32) | l1)));
+}
+
+// group-wide (L = 16: one DPP row, L = 32: two) sum / max of a double, by
+// steps whose partner pairs are symmetric: every lane of the group ends with
+// the same bits
+template <int L>
+__device__ __forceinline__ double group_sum_f64(double v)
+{
+    v += dpp_f64<0xB1>(v);
+    v += dpp_f64<0x4E>(v);
+    v += dpp_f64<0x141>(v);
+    v += dpp_f64<0x140>(v);
+    if constexpr (L == 32) v = swap_sum_f64<16>(v);
+    return v;
+}
+
+template <int L>
+__device__ __forceinline__ double group_max_f64(double v)
+{
+    v = fmax(v, dpp_f64<0xB1>(v));
+    v = fmax(v, dpp_f64<0x4E>(v));
+    v = fmax(v, dpp_f64<0x141>(v));
+    v = fmax(v, dpp_f64<0x140>(v));
+    if constexpr (L == 32) v = swap_max_f64<16>(v);
+    return v;
+}
+
+// sum of a value over the P groups of a wave (lanes l, l + L, ...), the same
+// bits in every lane: pairs of groups first, then pairs of pairs
+template <int L>
+__device__ __forceinline__ double groups_sum_f64(double v)
+{
+    if constexpr (L == 16) v = swap_sum_f64<16>(v);
+    return swap_sum_f64<32>(v);
+}
+
+// b^e, e >= 0, by squaring
+__device__ __forceinline__ double pow_int(double b, int e)
+{
+    double r = 1.0;
+    while (e) {
+        if (e & 1) r *= b;
+        b *= b;
+        e >>= 1;
+    }
+    return r;
+}
+
+// pairwise sum of KT values
+template <int KT>
+__device__ __forceinline__ double tree_sum(const double* v)
+{
+    double t[KT];
+#pragma unroll
+    for (int i = 0; i < KT; i++) t[i] = v[i];
+#pragma unroll
+    for (int w = 1; w < KT; w *= 2)
+#pragma unroll
+        for (int i = 0; i + w < KT; i += 2 * w) t[i] += t[i + w];
+    return t[0];
+}
+
+// a / s for s > 0 (a normal double, here at least exp(-256)): hardware
+// reciprocal, two Newton steps and one correction of the quotient
+__device__ __forceinline__ double div_pos(double a, double s)
+{
+    double r = __builtin_amdgcn_rcp(s);
+    r = fma(fma(-s, r, 1.0), r, r);
+    r = fma(fma(-s, r, 1.0), r, r);
+    const double q = a * r;
+    return fma(fma(-s, q, a), r, q);
+}
+
+__device__ __forceinline__ void lds_add_f64(double* p, double v)
+{
+    (void)__hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+template <int L, int KT>
+__global__ __launch_bounds__(256, 3) void k_ce_cells(const CeCellArgs a)
+{
+    constexpr int P = 64 / L;
+    static_assert(L == 16 || L == 32, "group width");
     extern __shared__ __align__(16) char smem[];
     __shared__ double wxs[kMaxRunLen];                     // column weight lambda_x per pixel of the run
     __shared__ double wl[kCellWaves];
-    __shared__ uint8_t labs[kCellWaves][kLabBuf];          // each wave's labels, a chunk of rows at a time
+    __shared__ uint8_t labs[kCellWaves][P][kMaxRunLen];    // labels of the rows a wave has in flight
     const int n = blockIdx.z, sy = blockIdx.y, sx = blockIdx.x;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int grp = lane / L, lig = lane % L;
     const int K = a.K, wk = a.w * a.K;
     const Run ry = a.ry[sy], rx = a.rx[sx];
-    const int j0 = rx.i0, j1 = rx.i1;
-    // the four corner columns of both source rows, and the reduction buffer
-    int8_t* C0 = (int8_t*)smem;                            // [4][K]: (i0,j0) (i0,j1) (i1,j0) (i1,j1)
-    double* red = (double*)(smem + ((4 * K + 15) & ~15));  // [waves][4][K]
+    const int j0 = rx.i0, j1 = rx.i1, len = rx.len;
+    // LDS: the four corner columns of both source rows [4][K] (codes), the
+    // per-class constants [4][K], and per wave P one-hot regions [2][K]
+    // (reused for the wave's corner sums [4][K] at the end)
+    int8_t* C0 = (int8_t*)smem;
+    double* cst = (double*)(smem + ((4 * K + 15) & ~15));
+    double* oh = cst + 4 * K;
+    // labels of a pass (rows base .. base + P - 1 of the run): up to kLabPre
+    // bytes per lane through registers, so a pass's loads can be issued early
+    const uint8_t* lab_base = a.labels + ((int64_t)n * a.H + ry.start) * a.W + rx.start;
+    auto lab_load = [&](int base, uint32_t* v) {
+#pragma unroll
+        for (int q = 0; q < kLabPre; q++) {
+            const int t = lane + 64 * q, rr = base + t / len;
+            v[q] = t < P * len && rr < ry.len ? lab_base[(int64_t)rr * a.W + t % len] : 0u;
+        }
+    };
+    auto lab_store = [&](int base, const uint32_t* v) {
+#pragma unroll
+        for (int q = 0; q < kLabPre; q++) {
+            const int t = lane + 64 * q;
+            if (t < P * len) labs[wv][t / len][t % len] = (uint8_t)v[q];
+        }
+        for (int t = lane + 64 * kLabPre; t < P * len; t += 64) {
+            const int rr = base + t / len;
+            labs[wv][t / len][t % len] = rr < ry.len ? lab_base[(int64_t)rr * a.W + t % len] : (uint8_t)0;
+        }
+    };
+    uint32_t lpre[kLabPre];
+    lab_load(wv * P, lpre);
     const int8_t* r0 = a.logits + ((int64_t)n * a.h + ry.i0) * wk;
     const int8_t* r1 = a.logits + ((int64_t)n * a.h + ry.i1) * wk;
     for (int t = threadIdx.x; t < K; t += blockDim.x) {
@@ -174,203 +333,186 @@ __global__ __launch_bounds__(256) void k_ce_cells(const CeCellArgs a)
         C0[2 * K + t] = r1[j0 * K + t];
         C0[3 * K + t] = r1[j1 * K + t];
     }
-    for (int c = threadIdx.x; c < rx.len; c += blockDim.x) {
+    for (int c = threadIdx.x; c < len; c += blockDim.x) {
         int e0, e1;
         bool ecl;
         double lx;
         src_coord_hd(rx.start + c, a.w, a.W, e0, e1, lx, ecl);
         wxs[c] = lx;
     }
+    for (int t = threadIdx.x; t < kCellWaves * P * 2 * K; t += blockDim.x) oh[t] = 0.0;
     __syncthreads();
     // outside the documented range the outputs are discarded (k_ce_quant)
     const double scale = logit_exp_ok(*a.logit_exp) ? ldexp(1.0, *a.logit_exp) : 0.0;
     const double invP = 1.0 / ((double)a.N * (double)a.H * (double)a.W);
 
-    double c00[KT], c01[KT], c10[KT], c11[KT];
+    // the cell's max logit (each group covers every class: the same m everywhere)
     double m = -INFINITY;
 #pragma unroll
     for (int t = 0; t < KT; t++) {
-        const int k = lane + 64 * t;
-        if (k < K) {
-            c00[t] = C0[k];
-            c01[t] = C0[K + k];
-            c10[t] = C0[2 * K + k];
-            c11[t] = C0[3 * K + k];
-            m = fmax(m, fmax(fmax(c00[t], c01[t]), fmax(c10[t], c11[t])) * scale);
-        } else {
-            c00[t] = c01[t] = c10[t] = c11[t] = 0.0;
-        }
+        const int k = lig + L * t;
+        if (k < K) m = fmax(m, fmax(fmax((double)C0[k], (double)C0[K + k]),
+                                    fmax((double)C0[2 * K + k], (double)C0[3 * K + k])) * scale);
     }
-    m = wave_max_f64(m);
+    m = group_max_f64<L>(m);
 
-    // this wave's rows, and the weights at its first two rows / the run's first two columns
-    const int rc = (ry.len + kCellWaves - 1) / kCellWaves;
-    const int rbeg = wv * rc;
-    const int rend = rbeg + rc < ry.len ? rbeg + rc : ry.len;
-    double G00[KT], G01[KT], G10[KT], G11[KT];
-#pragma unroll
-    for (int t = 0; t < KT; t++) G00[t] = G01[t] = G10[t] = G11[t] = 0.0;
-    double lsum = 0.0, luni = 0.0, llab = 0.0, sv = 1.0;
-    int pc = 0;
-    bool bad = false;
-    if (rbeg < rend) {
+    // per class: exp at the first pixel, x-step and y-step ratios, and the
+    // factor by which the x-step changes from row to row
+    {
         int d0, d1;
         bool dcl;
         double ly0, ly1;
-        const double lx0 = wxs[0], lx1 = wxs[rx.len > 1 ? 1 : 0];
-        src_coord_hd(ry.start + rbeg, a.h, a.H, d0, d1, ly0, dcl);
-        src_coord_hd(ry.start + rbeg + (rend - rbeg > 1 ? 1 : 0), a.h, a.H, d0, d1, ly1, dcl);
-        double Er[KT], Rr[KT], Qy[KT], Tx[KT];
-#pragma unroll
-        for (int t = 0; t < KT; t++) {
-            const double l00 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx0, lx0, 1.0 - ly0, ly0, scale);
-            const double l10 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx1, lx1, 1.0 - ly0, ly0, scale);
-            const double l01 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx0, lx0, 1.0 - ly1, ly1, scale);
-            const double l11 = interp(c00[t], c01[t], c10[t], c11[t], 1.0 - lx1, lx1, 1.0 - ly1, ly1, scale);
-            const bool on = lane + 64 * t < K;
-            Er[t] = on ? exp(l00 - m) : 0.0;
-            Rr[t] = exp(l10 - l00);
-            Qy[t] = exp(l01 - l00);
-            Tx[t] = exp((l11 - l01) - (l10 - l00));
-        }
-        const int chunk_rows = kLabBuf / rx.len;
-        for (int r = rbeg; r < rend; r++) {
-            const int y = ry.start + r;
-            if ((r - rbeg) % chunk_rows == 0) {
-                // the labels of the next rows of this wave, loaded in one go
-                const int nr = rend - r < chunk_rows ? rend - r : chunk_rows;
-                for (int t = lane; t < nr * rx.len; t += 64)
-                    labs[wv][t] = a.labels[((int64_t)n * a.H + y + t / rx.len) * a.W + rx.start + t % rx.len];
-                __builtin_amdgcn_wave_barrier();
-            }
-            const uint8_t* lab_row = &labs[wv][((r - rbeg) % chunk_rows) * rx.len];
-            int e0, e1;
-            bool ecl;
-            double ly;
-            src_coord_hd(y, a.h, a.H, e0, e1, ly, ecl);
-            const double wy0 = 1.0 - ly, wy1 = ly;
-            if (r > rbeg) {
-#pragma unroll
-                for (int t = 0; t < KT; t++) {
-                    Er[t] *= Qy[t];
-                    Rr[t] *= Tx[t];
-                }
-            }
-            double E[KT], alo[KT], ahi[KT], olo[KT], ohi[KT];
-#pragma unroll
-            for (int t = 0; t < KT; t++) {
-                E[t] = Er[t];
-                alo[t] = ahi[t] = olo[t] = ohi[t] = 0.0;
-            }
-            for (int c = 0; c < rx.len; c++) {
-                const double lx = wxs[c];
-                const double wx0 = 1.0 - lx, wx1 = lx;
-                if (c > 0) {
-#pragma unroll
-                    for (int t = 0; t < KT; t++) E[t] *= Rr[t];
-                }
-                double s = 0.0;
-#pragma unroll
-                for (int t = 0; t < KT; t++) s += E[t];
-                s = wave_sum_f64(s);
-                const double cp = invP / s;
-                // softmax part of the gradient: E / s / P
-#pragma unroll
-                for (int t = 0; t < KT; t++) {
-                    const double g = E[t] * cp;
-                    alo[t] += wx0 * g;
-                    ahi[t] += wx1 * g;
-                }
-                // one-hot part: the label's lane collects the pixel's column weights
-                const int lab = lab_row[c];
-                bad |= lab >= K;
-                const bool mine = lane == (lab & 63);
-#pragma unroll
-                for (int t = 0; t < KT; t++)
-                    if ((lab >> 6) == t && mine) {
-                        olo[t] += wx0;
-                        ohi[t] += wx1;
-                    }
-                // loss: log(s) + m - l(label); the logs are taken 64 pixels at a time,
-                // the label logits at the end of the row from the one-hot weights
-                luni += m;
-                if ((pc & 63) == lane) sv = s;
-                pc++;
-                if ((pc & 63) == 0) lsum += log(sv);
-            }
-#pragma unroll
-            for (int t = 0; t < KT; t++) {
-                const double glo = alo[t] - olo[t] * invP, ghi = ahi[t] - ohi[t] * invP;
-                G00[t] += wy0 * glo;
-                G01[t] += wy0 * ghi;
-                G10[t] += wy1 * glo;
-                G11[t] += wy1 * ghi;
-                // sum over the row's pixels labelled k of l_k = the corners' bilinear mix
-                llab += (wy0 * (c00[t] * olo[t] + c01[t] * ohi[t]) + wy1 * (c10[t] * olo[t] + c11[t] * ohi[t])) *
-                        scale;
-            }
+        src_coord_hd(ry.start, a.h, a.H, d0, d1, ly0, dcl);
+        src_coord_hd(ry.start + (ry.len > 1 ? 1 : 0), a.h, a.H, d0, d1, ly1, dcl);
+        const double lx0 = wxs[0], lx1 = wxs[len > 1 ? 1 : 0];
+        for (int k = threadIdx.x; k < K; k += blockDim.x) {
+            const double c00 = C0[k], c01 = C0[K + k], c10 = C0[2 * K + k], c11 = C0[3 * K + k];
+            const double l00 = interp(c00, c01, c10, c11, 1.0 - lx0, lx0, 1.0 - ly0, ly0, scale);
+            const double l10 = interp(c00, c01, c10, c11, 1.0 - lx1, lx1, 1.0 - ly0, ly0, scale);
+            const double l01 = interp(c00, c01, c10, c11, 1.0 - lx0, lx0, 1.0 - ly1, ly1, scale);
+            const double l11 = interp(c00, c01, c10, c11, 1.0 - lx1, lx1, 1.0 - ly1, ly1, scale);
+            cst[k] = exp(l00 - m);
+            cst[K + k] = exp(l10 - l00);
+            cst[2 * K + k] = exp(l01 - l00);
+            cst[3 * K + k] = exp((l11 - l01) - (l10 - l00));
         }
     }
-    if (lane < (pc & 63)) lsum += log(sv);
+    lab_store(wv * P, lpre);
+    __syncthreads();
+
+    double G00[KT], G01[KT], G10[KT], G11[KT];
+#pragma unroll
+    for (int t = 0; t < KT; t++) G00[t] = G01[t] = G10[t] = G11[t] = 0.0;
+    double lsum = 0.0, llab = 0.0, sv = 1.0;
+    int pc = 0;
+    bool bad = false;
+    double* ohg = oh + (int64_t)((wv * P + grp) * 2) * K;
+    const uint8_t* lab_row = labs[wv][grp];
+    for (int base = wv * P; base < ry.len; base += kCellWaves * P) {
+        const int row = base + grp;
+        const bool live = row < ry.len;
+        const bool more = base + kCellWaves * P < ry.len;
+        if (more) lab_load(base + kCellWaves * P, lpre);     // the next pass's labels, in flight meanwhile
+        int e0, e1;
+        bool ecl;
+        double ly;
+        src_coord_hd(ry.start + (live ? row : 0), a.h, a.H, e0, e1, ly, ecl);
+        const double wy0 = 1.0 - ly, wy1 = ly;
+        double E[KT], R[KT], alo[KT], ahi[KT];
+#pragma unroll
+        for (int t = 0; t < KT; t++) {
+            const int k = lig + L * t;
+            const bool on = k < K;
+            E[t] = on && live ? cst[k] * pow_int(cst[2 * K + k], row) : 0.0;
+            R[t] = on ? cst[K + k] * pow_int(cst[3 * K + k], live ? row : 0) : 1.0;
+            alo[t] = ahi[t] = 0.0;
+        }
+        // one pixel of the row: softmax part of the gradient E / s / P folded
+        // into the row's two columns; one-hot part by the label's lane; the
+        // loss log(s) + m - l(label), logs taken L pixels at a time and the
+        // label logits at the end of the row from the one-hot weights
+        auto pixel = [&](const double* Ev, double s, double lx, int lab, bool on) {
+            const double cp = on ? div_pos(invP, s) : 0.0;
+            const double c0 = (1.0 - lx) * cp, c1 = lx * cp;
+#pragma unroll
+            for (int t = 0; t < KT; t++) {
+                alo[t] = fma(c0, Ev[t], alo[t]);
+                ahi[t] = fma(c1, Ev[t], ahi[t]);
+            }
+            if (on) {
+                bad |= lab >= K;
+                if (lab < K && lig == lab % L) {
+                    lds_add_f64(&ohg[lab], 1.0 - lx);
+                    lds_add_f64(&ohg[K + lab], lx);
+                }
+                if ((pc % L) == lig) sv = s;
+                pc++;
+                if (pc % L == 0) lsum += log(sv);
+            }
+        };
+        for (int c = 0; c < len; c += 2) {
+            const bool two = c + 1 < len;
+            const double lxa = wxs[c], lxb = wxs[two ? c + 1 : c];
+            const int laba = lab_row[c], labb = lab_row[two ? c + 1 : c];
+            double E1[KT];
+#pragma unroll
+            for (int t = 0; t < KT; t++) E1[t] = E[t] * R[t];
+            const double sa = group_sum_f64<L>(tree_sum<KT>(E));
+            const double sb = group_sum_f64<L>(tree_sum<KT>(E1));
+            pixel(E, sa, lxa, laba, live);
+            pixel(E1, sb, lxb, labb, live && two);
+#pragma unroll
+            for (int t = 0; t < KT; t++) E[t] = E1[t] * R[t];
+        }
+        if (live) {
+#pragma unroll
+            for (int t = 0; t < KT; t++) {
+                const int k = lig + L * t;
+                if (k < K) {
+                    const double olo = ohg[k], ohi = ohg[K + k];
+                    ohg[k] = 0.0;
+                    ohg[K + k] = 0.0;
+                    const double glo = alo[t] - olo * invP, ghi = ahi[t] - ohi * invP;
+                    G00[t] += wy0 * glo;
+                    G01[t] += wy0 * ghi;
+                    G10[t] += wy1 * glo;
+                    G11[t] += wy1 * ghi;
+                    // sum over the row's pixels labelled k of l_k = the corners' bilinear mix
+                    llab += (wy0 * ((double)C0[k] * olo + (double)C0[K + k] * ohi) +
+                             wy1 * ((double)C0[2 * K + k] * olo + (double)C0[3 * K + k] * ohi)) * scale;
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (more) lab_store(base + kCellWaves * P, lpre);
+        __builtin_amdgcn_wave_barrier();
+    }
+    if (lig < (pc % L)) lsum += log(sv);
     lsum = wave_sum_f64(lsum - llab);
+    const bool anybad = __any(bad);
+    // the groups' corner sums, then this wave's into its own LDS region
+    double* red = oh + (int64_t)wv * P * 2 * K;             // [4][K], within the wave's one-hot regions
 #pragma unroll
     for (int t = 0; t < KT; t++) {
-        const int k = lane + 64 * t;
-        if (k < K) {
-            double* o = red + (int64_t)wv * 4 * K;
-            o[k] = G00[t];
-            o[K + k] = G01[t];
-            o[2 * K + k] = G10[t];
-            o[3 * K + k] = G11[t];
+        const double g00 = groups_sum_f64<L>(G00[t]), g01 = groups_sum_f64<L>(G01[t]);
+        const double g10 = groups_sum_f64<L>(G10[t]), g11 = groups_sum_f64<L>(G11[t]);
+        const int k = lig + L * t;
+        if (grp == 0 && k < K) {
+            red[k] = g00;
+            red[K + k] = g01;
+            red[2 * K + k] = g10;
+            red[3 * K + k] = g11;
         }
     }
     if (lane == 0) {
-        wl[wv] = lsum + luni;
-        if (bad) set_status(a.status, ISEG_DEV_RANGE);
+        wl[wv] = lsum;
+        if (anybad) set_status(a.status, ISEG_DEV_RANGE);
     }
     __syncthreads();
     const int64_t cid = ((int64_t)n * a.nry + sy) * a.nrx + sx;
     double* out = a.cell + cid * 4 * K;
+    const int64_t ws = (int64_t)P * 2 * K;
     for (int t = threadIdx.x; t < 4 * K; t += blockDim.x)
-        out[t] = ((red[t] + red[4 * K + t]) + red[8 * K + t]) + red[12 * K + t];
-    if (threadIdx.x == 0) a.cell_loss[cid] = ((wl[0] + wl[1]) + wl[2]) + wl[3];
+        out[t] = ((oh[t] + oh[ws + t]) + oh[2 * ws + t]) + oh[3 * ws + t];
+    if (threadIdx.x == 0)
+        a.cell_loss[cid] = (((wl[0] + wl[1]) + wl[2]) + wl[3]) + m * ((double)ry.len * (double)len);
 }
 
 // grad[n,i,j,k]: sum over the cells with a corner at (i, j), in cell order
-// (row runs, then column runs, then corners); one block per (n, i)
+// (row runs, then column runs, then corners); one thread per element, a block
+// per 256 elements of one low-res row, the runs touching i and j from tables
 __global__ __launch_bounds__(256) void k_ce_combine(const CeCellArgs a)
 {
-    const int n = blockIdx.y, i = blockIdx.x;
-    __shared__ int ys_lo, ys_hi;
-    __shared__ int2 xs[256];             // column run range per low-res column
-    if (threadIdx.x == 0) {
-        int lo = a.nry, hi = -1;
-        for (int s = 0; s < a.nry; s++)
-            if (a.ry[s].i0 == i || a.ry[s].i1 == i) {
-                lo = s < lo ? s : lo;
-                hi = s;
-            }
-        ys_lo = lo;
-        ys_hi = hi;
-    }
-    for (int j = threadIdx.x; j < a.w; j += blockDim.x) {
-        int lo = a.nrx, hi = -1;
-        for (int s = 0; s < a.nrx; s++)
-            if (a.rx[s].i0 == j || a.rx[s].i1 == j) {
-                lo = s < lo ? s : lo;
-                hi = s;
-            }
-        xs[j] = make_int2(lo, hi);
-    }
-    __syncthreads();
+    const int n = blockIdx.z, i = blockIdx.y;
     const int wk = a.w * a.K;
+    const int e = blockIdx.x * 256 + threadIdx.x;
     uint64_t mx = 0;
-    for (int e = threadIdx.x; e < wk; e += blockDim.x) {
-        const int j = e / a.K, k = e % a.K;
+    if (e < wk) {
+        const int j = e / a.K, k = e - j * a.K;
         double acc = 0.0;
-        for (int s = ys_lo; s <= ys_hi; s++) {
+        for (int s = a.ylo[i]; s <= a.yhi[i]; s++) {
             const Run ry = a.ry[s];
-            for (int g = xs[j].x; g <= xs[j].y; g++) {
+            for (int g = a.xlo[j]; g <= a.xhi[j]; g++) {
                 const Run rx = a.rx[g];
                 const double* c = a.cell + (((int64_t)n * a.nry + s) * a.nrx + g) * 4 * a.K + k;
                 if (ry.i0 == i && rx.i0 == j) acc += c[0];
@@ -380,10 +522,10 @@ __global__ __launch_bounds__(256) void k_ce_combine(const CeCellArgs a)
             }
         }
         a.grad[((int64_t)n * a.h + i) * wk + e] = acc;
-        const uint64_t b = (uint64_t)__double_as_longlong(acc) & 0x7fffffffffffffffull;
-        mx = b > mx ? b : mx;
+        mx = (uint64_t)__double_as_longlong(acc) & 0x7fffffffffffffffull;
     }
-    block_store_max_u64(mx, a.part);
+    mx = block_max_u64(mx);
+    if (threadIdx.x == 0) a.part[((int64_t)n * a.h + i) * gridDim.x + blockIdx.x] = mx;
 }
 
 // smallest e with |v| < 2^e for the positive double with bits mb (frexp's exponent)
@@ -440,14 +582,34 @@ __global__ __launch_bounds__(256) void k_ce_quant(const CeCellArgs a, int64_t np
     }
 }
 
-template <int KT>
-int launch_cells(const CeCellArgs& a, size_t lds, hipStream_t s)
+template <int L, int KT>
+int launch_cells(const CeCellArgs& a, hipStream_t s)
 {
-    if (!lds_limit((const void*)k_ce_cells<KT>, lds))
+    const size_t lds = (size_t)((4 * a.K + 15) & ~15) + (size_t)(4 * a.K) * 8 +
+                       (size_t)(kCellWaves * (64 / L) * 2 * a.K) * 8;
+    if (!lds_limit((const void*)k_ce_cells<L, KT>, lds))
         return ISEG_ERR_DEVICE;
-    hipLaunchKernelGGL(k_ce_cells<KT>, dim3((unsigned)a.nrx, (unsigned)a.nry, (unsigned)a.N), dim3(256), lds, s, a);
+    hipLaunchKernelGGL((k_ce_cells<L, KT>), dim3((unsigned)a.nrx, (unsigned)a.nry, (unsigned)a.N), dim3(256), lds,
+                       s, a);
     return launch_ok();
 }
+
+// first and last run touching each low-res index (an empty range: lo > hi)
+void run_ranges(const Run* runs, int nr, int n_low, int16_t* lo, int16_t* hi)
+{
+    for (int i = 0; i < n_low; i++) {
+        lo[i] = (int16_t)nr;
+        hi[i] = -1;
+        for (int s = 0; s < nr; s++)
+            if (runs[s].i0 == i || runs[s].i1 == i) {
+                if (s < lo[i]) lo[i] = (int16_t)s;
+                hi[i] = (int16_t)s;
+            }
+    }
+}
+
+// max |grad| partials: one per combine block
+int64_t ce_nparts(int64_t N, int64_t h, int64_t w, int64_t K) { return N * h * ceil_div64(w * K, 256); }
 
 }  // namespace
 
@@ -466,7 +628,7 @@ extern "C" size_t iseg_softmax_ce_ws(int64_t N, int64_t h, int64_t w, int64_t K,
     if (nry < 0 || nrx < 0) return 0;
     return 256 + ce_cell_bytes(N, nry, nrx, K) +
            align256((size_t)(N * nry * nrx) * 8) + align256((size_t)(N * h * w * K) * 8) +
-           align256((size_t)(N * h) * 8);
+           align256((size_t)ce_nparts(N, h, w, K) * 8);
 }
 
 extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, const uint8_t* labels, int64_t N,
@@ -487,6 +649,8 @@ extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, c
     a.nrx = make_runs((int)w, (int)W, a.rx);
     for (int i = 0; i < a.nrx; i++)
         if (a.rx[i].len > kMaxRunLen) return ISEG_ERR_UNSUPPORTED;
+    run_ranges(a.ry, a.nry, (int)h, a.ylo, a.yhi);
+    run_ranges(a.rx, a.nrx, (int)w, a.xlo, a.xhi);
     a.status = dev_status;
     char* p = (char*)ws;
     p += 256;
@@ -499,18 +663,24 @@ extern "C" int iseg_softmax_ce(const int8_t* logits, const int32_t* logit_exp, c
     a.part = (uint64_t*)p;
     a.grad = grad ? grad : gws;
     int rc;
-    const size_t lds = (size_t)((4 * K + 15) & ~(int64_t)15) + (size_t)(kCellWaves * 4 * K) * 8;
-    const int kt = (int)((K + 63) / 64);
-    rc = kt == 1 ? launch_cells<1>(a, lds, stream)
-       : kt == 2 ? launch_cells<2>(a, lds, stream)
-       : kt == 3 ? launch_cells<3>(a, lds, stream)
-                 : launch_cells<4>(a, lds, stream);
+    // groups of 16 lanes up to 128 classes (KT rounded up to an instantiated
+    // width), else 32: more classes per lane cost occupancy
+    const int kt16 = (int)((K + 15) / 16), kt32 = (int)((K + 31) / 32);
+    rc = kt16 <= 1   ? launch_cells<16, 1>(a, stream)
+       : kt16 <= 2   ? launch_cells<16, 2>(a, stream)
+       : kt16 <= 4   ? launch_cells<16, 4>(a, stream)
+       : kt16 <= 6   ? launch_cells<16, 6>(a, stream)
+       : kt16 <= 8   ? launch_cells<16, 8>(a, stream)
+       : kt32 <= 5   ? launch_cells<32, 5>(a, stream)
+       : kt32 <= 6   ? launch_cells<32, 6>(a, stream)
+                     : launch_cells<32, 8>(a, stream);
     if (rc) return rc;
-    hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)h, (unsigned)N), dim3(256), 0, stream, a);
+    const unsigned cx = (unsigned)ceil_div64(w * K, 256);
+    hipLaunchKernelGGL(k_ce_combine, dim3(cx, (unsigned)h, (unsigned)N), dim3(256), 0, stream, a);
     if ((rc = launch_ok())) return rc;
     const int64_t nlow = N * h * w * K;
-    hipLaunchKernelGGL(k_ce_quant, dim3(grid_for(nlow, 256, 2048)), dim3(256), 0, stream, a, N * h, (int)bits, err,
-                       err_exp, loss);
+    hipLaunchKernelGGL(k_ce_quant, dim3(grid_for(nlow, 256 * 4, 512)), dim3(256), 0, stream, a,
+                       ce_nparts(N, h, w, K), (int)bits, err, err_exp, loss);
     return launch_ok();
 }
 

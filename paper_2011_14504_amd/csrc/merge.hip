@@ -470,6 +470,7 @@ struct SsumArgs {
     int32_t splits;
     int32_t* part;                 // [splits][N][C] int32 partial sums
     int64_t* sums;                 // [N][C] exact sums
+    uint64_t* pmax;                // max |sum| partials, one per reduce block
     const int32_t* x_exp;
     int64_t divisor;
     int32_t bits;
@@ -525,31 +526,54 @@ __global__ __launch_bounds__(256) void k_ssum_part1(SsumArgs a)
     a.part[((int64_t)blockIdx.y * a.N + n) * a.C + c] = s;
 }
 
-// one block: split partials -> exact int64 sums -> max -> SQ of sum / D.
-// With u the smallest integer such that max|sum| < D 2^u, the scale is
-// 2^(x_exp + u) and code = floor(sum 2^(bits-1-u) / D + 1/2), decided exactly.
-__global__ __launch_bounds__(1024) void k_ssum_final(SsumArgs a)
+// exact int64 sum of each (n, c)'s split partials: a block takes 64 elements,
+// its four waves a quarter of the splits each (four loads in flight per lane),
+// the wave sums added through LDS; per-block max |sum| partials
+__global__ __launch_bounds__(256) void k_ssum_reduce(SsumArgs a)
+{
+    __shared__ int64_t red[4][64];
+    const int64_t nc = a.N * a.C;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t j = (int64_t)blockIdx.x * 64 + lane;
+    int64_t s = 0;
+    if (j < nc) {
+        int k = wv;
+        for (; k + 12 < a.splits; k += 16) {
+            const int32_t v0 = a.part[(int64_t)k * nc + j], v1 = a.part[(int64_t)(k + 4) * nc + j];
+            const int32_t v2 = a.part[(int64_t)(k + 8) * nc + j], v3 = a.part[(int64_t)(k + 12) * nc + j];
+            s += ((int64_t)v0 + v1) + ((int64_t)v2 + v3);
+        }
+        for (; k < a.splits; k += 4) s += a.part[(int64_t)k * nc + j];
+    }
+    red[wv][lane] = s;
+    __syncthreads();
+    uint64_t m = 0;
+    if (wv == 0 && j < nc) {
+        const int64_t t = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+        a.sums[j] = t;
+        m = (uint64_t)(t < 0 ? -t : t);
+    }
+    block_store_max_u64(m, a.pmax);
+}
+
+// SQ of sum / D.  With u the smallest integer such that max|sum| < D 2^u
+// (the max from the reduce blocks' partials), the scale is 2^(x_exp + u) and
+// code = floor(sum 2^(bits-1-u) / D + 1/2), decided exactly.
+__global__ __launch_bounds__(256) void k_ssum_code(SsumArgs a, int64_t nparts)
 {
     const int64_t nc = a.N * a.C;
-    uint64_t m = 0;
-    for (int64_t j = threadIdx.x; j < nc; j += blockDim.x) {
-        int64_t s = 0;
-        for (int k = 0; k < a.splits; k++) s += a.part[(int64_t)k * nc + j];
-        a.sums[j] = s;
-        const uint64_t u = (uint64_t)(s < 0 ? -s : s);
-        m = u > m ? u : m;
-    }
-    const uint64_t M = block_max_u64(m);   // its barriers also order the sums above
+    const uint64_t M = nparts ? reduce_partials_u64(a.pmax, nparts) : 0;
     const i128 D = a.divisor;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     if (M == 0) {
-        if (threadIdx.x == 0) *a.out_exp = *a.x_exp - bitlen_u64((uint64_t)(a.divisor - 1));
-        for (int64_t j = threadIdx.x; j < nc; j += blockDim.x) a.out[j] = 0;
+        if (blockIdx.x == 0 && threadIdx.x == 0) *a.out_exp = *a.x_exp - bitlen_u64((uint64_t)(a.divisor - 1));
+        for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nc; j += stride) a.out[j] = 0;
         return;
     }
     const int u = ceil_pow2_exp128((i128)M, D);
     const int sh = a.bits - 1 - u;
-    if (threadIdx.x == 0) *a.out_exp = *a.x_exp + u + 1 - a.bits;
-    for (int64_t j = threadIdx.x; j < nc; j += blockDim.x)
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.out_exp = *a.x_exp + u + 1 - a.bits;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nc; j += stride)
         a.out[j] = (int8_t)clamp_k128(rhu128(a.sums[j], sh, D), a.bits);
 }
 
@@ -700,7 +724,8 @@ static int64_t ssum_splits(int64_t N, int64_t HW, int64_t C)
 extern "C" size_t iseg_spatial_sum_ws(int64_t N, int64_t HW, int64_t C)
 {
     const int64_t s = ssum_splits(N, HW, C);
-    return align256((size_t)(s * N * C) * 4) + align256((size_t)(N * C) * 8);
+    return align256((size_t)(s * N * C) * 4) + align256((size_t)(N * C) * 8) +
+           align256((size_t)ceil_div64(N * C, 64) * 8);
 }
 
 extern "C" int iseg_spatial_sum(const int8_t* x, const int32_t* x_exp, int64_t N, int64_t HW, int64_t ldc,
@@ -721,6 +746,7 @@ extern "C" int iseg_spatial_sum(const int8_t* x, const int32_t* x_exp, int64_t N
     a.splits = (int32_t)ceil_div64(HW, a.rows_per_split);
     a.part = (int32_t*)ws;
     a.sums = (int64_t*)((char*)ws + align256((size_t)(a.splits * N * C) * 4));
+    a.pmax = (uint64_t*)((char*)a.sums + align256((size_t)(N * C) * 8));
     a.x_exp = x_exp; a.divisor = divisor; a.bits = bits; a.out = out; a.out_exp = out_exp;
     if (N > 0) {
         dim3 grid((unsigned)(N * ((C + 255) / 256)), (unsigned)a.splits);
@@ -730,6 +756,12 @@ extern "C" int iseg_spatial_sum(const int8_t* x, const int32_t* x_exp, int64_t N
         int rc = launch_ok();
         if (rc) return rc;
     }
-    hipLaunchKernelGGL(k_ssum_final, dim3(1), dim3(1024), 0, stream, a);
+    const int64_t nred = ceil_div64(N * C, 64);
+    if (nred > 0) {
+        hipLaunchKernelGGL(k_ssum_reduce, dim3((unsigned)nred), dim3(256), 0, stream, a);
+        int rc = launch_ok();
+        if (rc) return rc;
+    }
+    hipLaunchKernelGGL(k_ssum_code, dim3(grid_for(N * C, 256, 256)), dim3(256), 0, stream, a, nred);
     return launch_ok();
 }

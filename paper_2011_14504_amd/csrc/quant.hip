@@ -669,7 +669,27 @@ __global__ __launch_bounds__(256) void k_update_multi(const iseg_update_desc* __
             const int sh = *d.g_exp - u.lr_shift - d.master_exp;      // Delta W code = g 2^sh, rounded
             const int64_t i0 = (int64_t)(ch - first[lo]) * kUpdChunk;
             const int64_t i1 = i0 + kUpdChunk < d.n ? i0 + kUpdChunk : d.n;
-            for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+            // four elements per thread step when the tensors allow 16-byte
+            // master and 4-byte code accesses (chunk starts are multiples of 4)
+            const bool vec = ((((uintptr_t)d.master) & 15) | (((uintptr_t)g) & 3) | (((uintptr_t)d.w_q) & 3)) == 0;
+            const int64_t n4 = vec ? (i1 - i0) >> 2 : 0;
+            for (int64_t q = threadIdx.x; q < n4; q += blockDim.x) {
+                const int64_t i = i0 + 4 * q;
+                const int4 mv = *(const int4*)(d.master + i);
+                const uint32_t gv = *(const uint32_t*)(g + i);
+                int32_t mm[4] = {mv.x, mv.y, mv.z, mv.w};
+                uint32_t wq = 0;
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int64_t m =
+                        clamp_k((int64_t)mm[e] - upd_delta((int8_t)(gv >> (8 * e)), sh, u.k_U, lim), u.k_U);
+                    mm[e] = (int32_t)m;
+                    wq |= (uint32_t)(uint8_t)(int8_t)clamp_k(shr_rhu(m, dq), kw) << (8 * e);
+                }
+                *(int4*)(d.master + i) = make_int4(mm[0], mm[1], mm[2], mm[3]);
+                *(uint32_t*)(d.w_q + i) = wq;
+            }
+            for (int64_t i = i0 + 4 * n4 + threadIdx.x; i < i1; i += blockDim.x) {
                 const int64_t m = clamp_k((int64_t)d.master[i] - upd_delta(g[i], sh, u.k_U, lim), u.k_U);
                 d.master[i] = (int32_t)m;
                 d.w_q[i] = (int8_t)clamp_k(shr_rhu(m, dq), kw);

@@ -107,6 +107,9 @@ CONV_SHAPES = [
     (2, 9, 10, 320, 64, 1, 1, 0, 1),
     (1, 18, 17, 128, 128, 3, 1, 6, 6),    # atrous 6: 18 steps, padding-only taps
     (1, 11, 13, 64, 128, 3, 1, 3, 3),     # dilation 3: 9 steps
+    # 1x1 with a class count as K: backward-data pads K to a multiple of 64
+    (2, 16, 16, 256, 150, 1, 1, 0, 1),
+    (1, 9, 7, 128, 100, 1, 1, 0, 1),
 ] + [
     # strided backward-data with few dy channels (K): the phase path (FCN's
     # upsampling adjoints at 21 classes among them)
