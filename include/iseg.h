@@ -477,6 +477,20 @@ int iseg_sum_requant(int32_t n_in, const int8_t* const* in, const int32_t* const
                      int32_t relu, int32_t bits, int8_t* out, int32_t* out_exp,
                      void* ws, size_t ws_bytes, int32_t* dev_status, hipStream_t stream);
 
+/* iseg_sum_requant_relu_mask -- the sum of the errors a residual add's output
+ * receives (iseg_sum_requant with relu = 0, no broadcast inputs) followed by
+ * the backward of that add's ReLU (iseg_relu_mask_bwd): out = the sum's codes
+ * where sum_i mask_in_i 2^(*mask_exp[i]) > 0, else 0, with the sum's exponent
+ * in *out_exp, bit-identical to the two calls in sequence, in two kernels
+ * instead of three.  mask_in / mask_exp are host arrays of n_mask device
+ * pointers (the add's inputs and their exponents), n_mask in [1, 8]; the
+ * workspace is iseg_sum_requant_ws(N, HW, C).  Sec. 3.1, Eq. 16. */
+int iseg_sum_requant_relu_mask(int32_t n_in, const int8_t* const* in, const int32_t* const* in_exp,
+                               const int32_t* exp_add, int64_t N, int64_t HW, int64_t C, int32_t bits,
+                               int32_t n_mask, const int8_t* const* mask_in, const int32_t* const* mask_exp,
+                               int8_t* out, int32_t* out_exp, void* ws, size_t ws_bytes, int32_t* dev_status,
+                               hipStream_t stream);
+
 /* iseg_relu_mask_bwd -- backward of ReLU(sum_i in_i 2^(e_i + exp_add[i])):
  * dx = dy where the exact sum is > 0, else 0.  The values stay on dy's grid,
  * so dx takes dy's exponent (not written).  All tensors [n] int8, n a

@@ -251,6 +251,64 @@ __global__ __launch_bounds__(256) void k_merge_apply(MergeArgs a, int64_t nparts
     }
 }
 
+// pass 2 of a sum whose codes then go through the backward of a ReLU: the
+// codes of the sum, zeroed where the exact sum of the mask inputs (m) is not
+// positive (the sum's exponent comes from the unmasked max, as when the two
+// steps run apart); 16-byte vectors, two inputs on each side
+__global__ __launch_bounds__(256) void k_merge_apply_mask(MergeArgs a, MergeArgs m, int64_t nparts)
+{
+    int sh[kMaxIn], e0, msh[kMaxIn], me0;
+    merge_shifts(a, sh, &e0);
+    if (!merge_shifts(m, msh, &me0) && blockIdx.x == 0 && threadIdx.x == 0) set_status(a.status, ISEG_DEV_RANGE);
+    const uint64_t M = reduce_partials_u64(a.part, nparts);
+    const int r = M ? bitlen_u64(M) - (a.bits - 1) : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.out_exp = e0 + r;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t nv = a.n / 16;
+    const bool w32 = max_shift(a, sh) <= kW32Shift, mw32 = max_shift(m, msh) <= kW32Shift;
+    for (int64_t v0 = t0; v0 < nv; v0 += stride * kU) {
+        int4 raw[kU][2], mraw[kU][2];
+#pragma unroll
+        for (int u = 0; u < kU; u++) {
+            merge_load16<2>(a, v0 + u * stride, nv, raw[u]);
+            merge_load16<2>(m, v0 + u * stride, nv, mraw[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kU; u++) {
+            const int64_t v = v0 + u * stride;
+            if (v >= nv) break;
+            bool pos[16];
+            if (mw32) {
+                int32_t ms[16];
+                merge_sum16_raw<2>(m, msh, mraw[u], ms);
+#pragma unroll
+                for (int t = 0; t < 16; t++) pos[t] = ms[t] > 0;
+            } else {
+                int64_t ms[16];
+                merge_sum16_raw<2>(m, msh, mraw[u], ms);
+#pragma unroll
+                for (int t = 0; t < 16; t++) pos[t] = ms[t] > 0;
+            }
+            uint32_t w[4] = {0, 0, 0, 0};
+            if (w32) {
+                int32_t s[16];
+                merge_sum16_raw<2>(a, sh, raw[u], s);
+#pragma unroll
+                for (int t = 0; t < 16; t++)
+                    if (pos[t]) w[t >> 2] |= (uint32_t)(uint8_t)sq_code32(s[t], r, a.bits) << (8 * (t & 3));
+            } else {
+                int64_t s[16];
+                merge_sum16_raw<2>(a, sh, raw[u], s);
+#pragma unroll
+                for (int t = 0; t < 16; t++)
+                    if (pos[t]) w[t >> 2] |= (uint32_t)(uint8_t)sq_code(s[t], r, a.bits) << (8 * (t & 3));
+            }
+            *(int4*)(a.out + v * 16) = make_int4((int)w[0], (int)w[1], (int)w[2], (int)w[3]);
+        }
+    }
+}
+
 // ReLU mask of a merged sum: dx = dy where sum_i a_i 2^e_i > 0, else 0
 template <bool VEC, int NIN>
 __global__ __launch_bounds__(256) void k_relu_mask(MergeArgs a, const int8_t* __restrict__ dy)
@@ -631,6 +689,46 @@ extern "C" int iseg_sum_requant(int32_t n_in, const int8_t* const* in, const int
     if (vec && two) hipLaunchKernelGGL((k_merge_apply<true, 2>), dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
     else if (vec) hipLaunchKernelGGL((k_merge_apply<true, 0>), dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
     else hipLaunchKernelGGL((k_merge_apply<false, 0>), dim3(g2), dim3(256), 0, stream, a, (int64_t)g1);
+    return launch_ok();
+}
+
+extern "C" int iseg_sum_requant_relu_mask(int32_t n_in, const int8_t* const* in, const int32_t* const* in_exp,
+                                          const int32_t* exp_add, int64_t N, int64_t HW, int64_t C, int32_t bits,
+                                          int32_t n_mask, const int8_t* const* mask_in,
+                                          const int32_t* const* mask_exp, int8_t* out, int32_t* out_exp, void* ws,
+                                          size_t ws_bytes, int32_t* dev_status, hipStream_t stream)
+{
+    MergeArgs a{}, m{};
+    if (!fill_merge_inputs(a, n_in, in, in_exp, exp_add, nullptr)) return ISEG_ERR_ARG;
+    if (!fill_merge_inputs(m, n_mask, mask_in, mask_exp, nullptr, nullptr)) return ISEG_ERR_ARG;
+    if (N < 0 || HW < 0 || C < 1 || bits < 2 || bits > 8 || !out_exp) return ISEG_ERR_ARG;
+    const int64_t n = N * HW * C;
+    if (n > 0 && !out) return ISEG_ERR_ARG;
+    for (int i = 0; i < n_in; i++)
+        if (n > 0 && !in[i]) return ISEG_ERR_ARG;
+    for (int i = 0; i < n_mask; i++)
+        if (n > 0 && !mask_in[i]) return ISEG_ERR_ARG;
+    if (!ws || ws_bytes < iseg_sum_requant_ws(N, HW, C)) return ISEG_ERR_WORKSPACE;
+    bool vec = n_in == 2 && n_mask == 2 && (C % 16) == 0 && ((uintptr_t)out & 15) == 0;
+    for (int i = 0; i < n_in; i++) vec = vec && (((uintptr_t)in[i]) & 15) == 0;
+    for (int i = 0; i < n_mask; i++) vec = vec && (((uintptr_t)mask_in[i]) & 15) == 0;
+    if (!vec) {
+        // the two steps apart (the mask pass in place on the codes)
+        int rc = iseg_sum_requant(n_in, in, in_exp, exp_add, nullptr, N, HW, C, 0, bits, out, out_exp, ws, ws_bytes,
+                                  dev_status, stream);
+        if (rc) return rc;
+        return iseg_relu_mask_bwd(out, n_mask, mask_in, mask_exp, nullptr, n, C, out, dev_status, stream);
+    }
+    a.n = n; a.HW = HW; a.C = C; a.relu = 0; a.bits = bits;
+    a.part = (uint64_t*)ws; a.out = out; a.out_exp = out_exp; a.status = dev_status;
+    m.n = n; m.HW = HW; m.C = C;
+    const int64_t units = n / 16;
+    const unsigned g1 = grid_for(units, 256 * kU, kMaxPartials);
+    hipLaunchKernelGGL((k_merge_max<true, 2>), dim3(g1), dim3(256), 0, stream, a);
+    int rc = launch_ok();
+    if (rc) return rc;
+    const unsigned g2 = grid_for(units, 256 * kU, 1024);
+    hipLaunchKernelGGL(k_merge_apply_mask, dim3(g2), dim3(256), 0, stream, a, m, (int64_t)g1);
     return launch_ok();
 }
 

@@ -78,6 +78,7 @@ const Entry kEntries[] = {
     ISEG_TAPE_ENTRY(iseg_maxpool_bwd)
     ISEG_TAPE_ENTRY(iseg_sum_requant)
     ISEG_TAPE_ENTRY(iseg_relu_mask_bwd)
+    ISEG_TAPE_ENTRY(iseg_sum_requant_relu_mask)
     ISEG_TAPE_ENTRY(iseg_concat_requant)
     ISEG_TAPE_ENTRY(iseg_concat_split)
     ISEG_TAPE_ENTRY(iseg_spatial_sum)

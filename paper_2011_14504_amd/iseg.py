@@ -113,6 +113,8 @@ _SIGS = {
     "iseg_sum_requant": ([_I32, _P, _P, _P, _P, _I64, _I64, _I64, _I32, _I32, _P, _P, _P, _SZ, _P, _P],
                          C.c_int),
     "iseg_relu_mask_bwd": ([_P, _I32, _P, _P, _P, _I64, _I64, _P, _P, _P], C.c_int),
+    "iseg_sum_requant_relu_mask": ([_I32, _P, _P, _P, _I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _SZ,
+                                    _P, _P], C.c_int),
     "iseg_concat_requant_ws": ([_I32], _SZ),
     "iseg_concat_requant": ([_I32, _P, _P, _P, _P, _I64, _I64, _I32, _P, _P, _P, _SZ, _P, _P], C.c_int),
     "iseg_concat_split": ([_P, _I64, _I32, _P, _P, _P], C.c_int),
@@ -387,6 +389,15 @@ def iseg_sum_requant(ins, in_exps, exp_add, bcast, N, HW, Cc, relu, bits, out, o
                                 N, HW, Cc, relu, bits, _ptr(out), _ptr(out_exp), *_ws_tuple(ws),
                                 _ptr(status), _stream())
     _check(rc, "iseg_sum_requant")
+
+
+def iseg_sum_requant_relu_mask(ins, in_exps, exp_add, N, HW, Cc, bits, masks, mask_exps, out, out_exp, ws,
+                               status=None):
+    n = len(ins)
+    rc = lib().iseg_sum_requant_relu_mask(n, _ptr_array(ins), _ptr_array(in_exps), _i32_array(exp_add or [0] * n),
+                                          N, HW, Cc, bits, len(masks), _ptr_array(masks), _ptr_array(mask_exps),
+                                          _ptr(out), _ptr(out_exp), *_ws_tuple(ws), _ptr(status), _stream())
+    _check(rc, "iseg_sum_requant_relu_mask")
 
 
 def iseg_relu_mask_bwd(dy, ins, in_exps, exp_add, Cc, dx, status=None):
@@ -1011,6 +1022,17 @@ def sum_requant(ins, in_exps, relu=False, exp_add=None, bcast=None, bits=8, stat
     e = _out_exp(ref.device)
     ws = workspace(ref.device).get(lib().iseg_sum_requant_ws(N, H * W, Cc))
     iseg_sum_requant(ins, in_exps, exp_add, bcast, N, H * W, Cc, int(relu), bits, out, e, ws, status)
+    return out, e
+
+
+def sum_requant_relu_mask(ins, in_exps, masks, mask_exps, exp_add=None, bits=8, status=None):
+    """sum_requant (no ReLU, no broadcast) followed by relu_mask_bwd with the
+    mask inputs, in one call: (codes, exponent)."""
+    N, H, W, Cc = ins[0].shape
+    out = torch.empty_like(ins[0])
+    e = _out_exp(ins[0].device)
+    ws = workspace(ins[0].device).get(lib().iseg_sum_requant_ws(N, H * W, Cc))
+    iseg_sum_requant_relu_mask(ins, in_exps, exp_add, N, H * W, Cc, bits, masks, mask_exps, out, e, ws, status)
     return out, e
 
 

@@ -322,7 +322,10 @@ class IntNet:
         def send(name, codes, exp, exp_add=0, bcast=0):
             contrib.setdefault(name, []).append((codes, exp, exp_add, bcast, sender[0]))
 
-        def merged(name, si):
+        def merged(name, si, mask=None):
+            # the summed error of a tensor; with mask (a residual add's inputs
+            # and exponents) a sum of several parts also goes through the add's
+            # ReLU backward in the same call (third result True)
             parts = contrib.pop(name)
             for p in parts:
                 if p[4] in done and self._stream_of(p[4]) != si:
@@ -330,10 +333,15 @@ class IntNet:
                     for t in p[:2]:
                         t.record_stream(streams[si])
             if len(parts) == 1 and not parts[0][2] and not parts[0][3]:
-                return parts[0][0], parts[0][1]
-            return iseg.sum_requant([p[0] for p in parts], [p[1] for p in parts],
-                                    exp_add=[p[2] for p in parts], bcast=[p[3] for p in parts],
-                                    status=self.status)
+                return parts[0][0], parts[0][1], False
+            if mask is not None and not any(p[3] for p in parts):
+                d, de = iseg.sum_requant_relu_mask([p[0] for p in parts], [p[1] for p in parts], mask[0], mask[1],
+                                                   exp_add=[p[2] for p in parts], status=self.status)
+                return d, de, True
+            e, ee = iseg.sum_requant([p[0] for p in parts], [p[1] for p in parts],
+                                     exp_add=[p[2] for p in parts], bcast=[p[3] for p in parts],
+                                     status=self.status)
+            return e, ee, False
 
         if self.wt_tab is None:
             self._build_wt_table(rec)
@@ -350,7 +358,7 @@ class IntNet:
             if nd["name"] in self.bwd_cross:
                 done[nd["name"]] = self._record(streams[si])
         if self.wl["input_grad"]:
-            e, ee = merged("input", 0)
+            e, ee, _ = merged("input", 0)
             rec["input"] = dict(kind="input", e_out=e, e_out_exp=ee)
         for b in self.branch:
             self._join(streams[0], b)
@@ -365,8 +373,9 @@ class IntNet:
         k, name = nd["kind"], nd["name"]
         want_input = self.wl["input_grad"]
         r = rec[name]
-        e, ee = merged(name, si)
-        r.update(e_out=e, e_out_exp=ee)
+        mask = ([r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]]) if k == "add" and nd["relu"] else None
+        e, ee, masked = merged(name, si, mask)
+        r.update(e_out=e, e_out_exp=ee, e_out_masked=masked)
         src = nd["src"][0]
         need_in = src != "input" or want_input
         if k == "conv":
@@ -405,7 +414,7 @@ class IntNet:
                 send(src, ei, eie)
         elif k == "add":
             d = (iseg.relu_mask_bwd(e, [r["a_in"], r["b_in"]], [r["a_in_exp"], r["b_in_exp"]],
-                                    status=self.status) if nd["relu"] else e)
+                                    status=self.status) if nd["relu"] and not masked else e)
             r.update(e_in=d, e_in_exp=ee)
             for s in nd["src"]:
                 if s != "input" or want_input:

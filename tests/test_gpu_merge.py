@@ -106,6 +106,23 @@ def test_relu_mask_bwd(orc, dev, shape, exps):
     assert np.array_equal(H(d), orc.relu_mask_bwd(dy, [a, b], list(exps)))
 
 
+@pytest.mark.parametrize("shape,exps,mexps", [((2, 9, 7, 64), (-8, -7), (-5, -30)),
+                                               ((1, 5, 3, 24), (-8, -11), (-5, -5)),
+                                               ((4, 16, 16, 256), (-30, -9), (-7, -3))], ids=str)
+def test_sum_requant_relu_mask(orc, dev, shape, exps, mexps):
+    """The fused sum + ReLU backward against the oracle's sum then mask."""
+    from paper_2011_14504_amd import iseg
+    e1, e2 = _codes(33, shape), _codes(34, shape)
+    a, b = _codes(35, shape), _codes(36, shape)
+    a[0, 0, :2, :] = 0
+    b[0, 0, :2, :] = 0
+    d, de = iseg.sum_requant_relu_mask([T(e1, dev), T(e2, dev)], [E(exps[0], dev), E(exps[1], dev)],
+                                       [T(a, dev), T(b, dev)], [E(mexps[0], dev), E(mexps[1], dev)])
+    s, se = orc.sum_requant([e1, e2], list(exps), 8, relu=False)
+    assert ev(de) == se
+    assert np.array_equal(H(d).astype(np.int64), orc.relu_mask_bwd(s, [a, b], list(mexps)).astype(np.int64))
+
+
 CAT_CASES = [
     # part widths, exps, spatial of each part (None = full)
     ([256, 256, 256, 256, 256], [-4, -5, -4, -6, -3], [None, None, None, None, (1, 1)]),

@@ -113,7 +113,7 @@ def test_tape_entries_match_the_binding():
     step_calls = ["iseg_conv_fwd", "iseg_conv_bwd_data", "iseg_conv_bwd_data_t", "iseg_conv_bwd_weight",
                   "iseg_weight_transpose_multi", "iseg_bn_fwd", "iseg_bn_bwd", "iseg_bn_fwd_i32",
                   "iseg_bn_bwd_i32", "iseg_update_multi", "iseg_maxpool_fwd", "iseg_maxpool_bwd",
-                  "iseg_sum_requant", "iseg_relu_mask_bwd", "iseg_concat_requant", "iseg_concat_split",
+                  "iseg_sum_requant", "iseg_relu_mask_bwd", "iseg_sum_requant_relu_mask", "iseg_concat_requant", "iseg_concat_split",
                   "iseg_spatial_sum", "iseg_softmax_ce", "iseg_mse_onehot", "iseg_profile_arm"]
     for name in step_calls:
         assert L.iseg_tape_entry(name.encode()) >= 0, name
