@@ -856,14 +856,17 @@ struct BwdWs {
     long long *p_sdn, *p_sf, *p_sfn; // [gx][C]
     long long *sd, *sdn, *sf, *sfn;  // [C] reduced
     int32_t *Z, *mm;                 // [C], [C][6]
-    int8_t* lut;                     // [C][3][256] dx codes
+    int8_t* lut;                     // [C][3][256] dx codes (rounding E2)
+    int32_t* cbnd;                   // [C] each channel's bound on E1's exponent (exact E2)
+    int16_t* lutq;                   // [C][3][256] dx values at the channel's own bound (exact E2)
 };
 
 size_t bwd_ws_bytes(const Stream& st)
 {
     size_t pc = (size_t)st.gx * st.C, C = (size_t)st.C;
     return ctr_bytes(st.C) + 2 * align256(C) + 4 * align256(pc * 4) + 3 * align256(pc * 8) +
-           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768);
+           4 * align256(C * 8) + align256(C * 4) + align256(C * 24) + align256(C * 768) + align256(C * 4) +
+           align256(C * 768 * 2);
 }
 
 BwdWs bwd_ws_map(void* base, const Stream& st)
@@ -887,7 +890,9 @@ BwdWs bwd_ws_map(void* base, const Stream& st)
     w.sfn = (long long*)p; p += align256(C * 8);
     w.Z = (int32_t*)p; p += align256(C * 4);
     w.mm = (int32_t*)p; p += align256(C * 24);
-    w.lut = (int8_t*)p;
+    w.lut = (int8_t*)p; p += align256(C * 768);
+    w.cbnd = (int32_t*)p; p += align256(C * 4);
+    w.lutq = (int16_t*)p;
     return w;
 }
 
@@ -970,8 +975,6 @@ struct BnbOut {
     int32_t *dgamma_exp, *dbeta_exp, *dx_exp, *dev_status;
 };
 
-__device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
-                                               const BnCfg& cf, const BnbOut& o);
 __device__ __forceinline__ void bnb_round_tail1(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
                                                 const BnCfg& cf, const BnbOut& o);
 
@@ -1145,19 +1148,30 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
         }
     }
     if (t < st.CS) {
-        const int64_t o = (int64_t)blockIdx.x * st.C + cbase + t;
         uint32_t A, B;
         mm_pack(bmm, A, B);
-        st_x(&w.p_sd[o], bsd);
-        st_x(&w.p_sdn[o], bsdn);
-        st_x(&w.p_z[o], bz);
-        st_x(&w.p_mmA[o], (int32_t)A);
-        st_x(&w.p_mmB[o], (int32_t)B);
+        if constexpr (TAIL == 1) {
+            // channel-major for the per-channel kernel that follows
+            const int64_t o = (cbase + t) * st.gx + blockIdx.x;
+            w.p_sd[o] = bsd;
+            w.p_sdn[o] = bsdn;
+            w.p_z[o] = bz;
+            w.p_mmA[o] = (int32_t)A;
+            w.p_mmB[o] = (int32_t)B;
+        } else {
+            const int64_t o = (int64_t)blockIdx.x * st.C + cbase + t;
+            st_x(&w.p_sd[o], bsd);
+            st_x(&w.p_sdn[o], bsdn);
+            st_x(&w.p_z[o], bz);
+            st_x(&w.p_mmA[o], (int32_t)A);
+            st_x(&w.p_mmB[o], (int32_t)B);
+        }
     }
-    if (arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) {
-        __syncthreads();                                  // the staging above may still be read
-        if constexpr (TAIL == 1) bnb_exact_tail(tab, st, w, sv, cf, out);
-        else bnb_round_tail1(tab, st, w, sv, cf, out);
+    if constexpr (TAIL == 2) {
+        if (arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) {
+            __syncthreads();                              // the staging above may still be read
+            bnb_round_tail1(tab, st, w, sv, cf, out);
+        }
     }
 }
 
@@ -1411,42 +1425,6 @@ __device__ __forceinline__ void slice_cand_max(const int32_t* tCand, int n, int3
     if (threadIdx.x == 0) *dst = m;
 }
 
-__device__ __forceinline__ void bnb_exact_tail(uint32_t* lds, const Stream& st, const BwdWs& w, const Saved& sv,
-                                               const BnCfg& cf, const BnbOut& o)
-{
-    bnb_tail_reduce1(lds, st, w, o);
-    const int CS = st.CS, t = threadIdx.x;
-    const Tail1Lds L(lds);
-    int32_t* tSd = L.sd;
-    int32_t* tZ = L.z;
-    int32_t* tMM = L.mm;
-    long long* tSdn = L.sdn;
-    int32_t* tCand = L.cand;
-    __shared__ int32_t rb[kNT / 64];
-    const int64_t cb = (int64_t)blockIdx.y * CS;
-    const int32_t s_d = *o.dy_exp;
-    const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
-    const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
-    const int Ebase = s_d + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
-    if (t < 6 * CS) {
-        const int cl = t / 6, k = t % 6;                // channel of the slice; class k / 2, low / high
-        const int64_t c = cb + cl;
-        const int lo = tMM[(k & ~1) * kNT + cl], hi = tMM[(k | 1) * kNT + cl];
-        int best = kSentinelLo;
-        if (lo <= hi) {
-            const int gq = o.gamma_q[c];
-            const i128 M = st.M;
-            const int64_t f = clamp_k((int64_t)gq * ((k & 1) ? hi : lo), cf.k_E2);
-            const i128 B = bnb_bracket(f, (k >> 1) - 1, M, (i128)gq * tSd[cl], (i128)gq * tSdn[cl],
-                                       (i128)tZ[cl], e_xh);
-            if (B != 0) best = ceil_pow2_exp128(abs128(B), (i128)sv.den[c] * M * M) + Ebase;
-        }
-        tCand[t] = best;
-    }
-    __syncthreads();
-    slice_cand_max(tCand, 6 * CS, w.smax + blockIdx.y, rb);
-}
-
 // stats tail (rounding E2).  Slice: the pass-1 sums, dgamma, dbeta and the
 // largest |gamma_q delta| over its channels' sgn classes, into smaxF; the
 // second pass takes E2's Scale from the largest over the slices.
@@ -1528,35 +1506,100 @@ __device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st,
     slice_cand_max(tCand, 6 * CS, w.smax + blockIdx.y, rb);
 }
 
-// dx code table of a channel (one thread per masked error code, three sgn
-// classes); E1's exponent is the largest of the slices' bounds
-__global__ __launch_bounds__(256) void k_bnb_lut_exact(int64_t Mrows, int nslices, BwdWs w, Saved sv, BnCfg cf,
-                                                       BnbOut o)
+// Exact E2 (k_E2 >= 15), one block per channel and one thread per masked
+// error code: the channel's totals from the streaming blocks' partials
+// (dbeta, dgamma), its bound on E1's exponent (the largest over its six
+// per-class extremes; xhat and the bracket are linear in the code, so the
+// extremes bound every code the channel's data holds), and its dx values at
+// that bound: Q = floor(B 2^S / D) with S one more than the shift of the
+// channel's own bound, for the (class, code) pairs inside the channel's
+// per-class ranges (zero elsewhere: the output pass never looks them up).
+// |Q| <= 2^k_E1 + 1 there, so int16 holds it; the output pass rounds Q by
+// the gap between the largest bound and the channel's into the final code
+// (half-up rounding of floor(x) by 2^g + 1 equals that of x).
+__global__ __launch_bounds__(256) void k_bnb_chan_exact(int64_t Mrows, int gx, BwdWs w, Saved sv, BnCfg cf,
+                                                        BnbOut o)
 {
-    __shared__ int32_t rsh[4];
-    const int c = blockIdx.x;
-    int bdx = slices_max(w.smax, nslices, rsh);
-    if (bdx == kSentinelLo) bdx = 0;
-    if (c == 0 && threadIdx.x == 0) {
-        *o.dx_exp = bdx - (cf.k_E1 - 1);
-        bnb_exps_out(sv, cf, o);
+    __shared__ int32_t r_sd[4], r_z[4], r_lo[4][3], r_hi[4][3], r_cand;
+    __shared__ long long r_sdn[4];
+    const int c = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    int sd = 0, z = 0;
+    long long sdn = 0;
+    int lo3[3] = {255, 255, 255}, hi3[3] = {0, 0, 0};       // byte-coded extremes (empty: lo > hi)
+    for (int b = t; b < gx; b += blockDim.x) {
+        const int64_t q = (int64_t)c * gx + b;
+        sd += w.p_sd[q];
+        sdn += w.p_sdn[q];
+        z += w.p_z[q];
+        mm_merge((uint32_t)w.p_mmA[q], (uint32_t)w.p_mmB[q], lo3, hi3);
     }
-    const int d = (int)threadIdx.x - 128;
+    for (int off = 32; off > 0; off >>= 1) {
+        sd += __shfl_xor(sd, off, 64);
+        z += __shfl_xor(z, off, 64);
+        sdn += __shfl_xor(sdn, off, 64);
+#pragma unroll
+        for (int k = 0; k < 3; k++) {
+            lo3[k] = min(lo3[k], __shfl_xor(lo3[k], off, 64));
+            hi3[k] = max(hi3[k], __shfl_xor(hi3[k], off, 64));
+        }
+    }
+    if (lane == 0) {
+        r_sd[wv] = sd; r_z[wv] = z; r_sdn[wv] = sdn;
+#pragma unroll
+        for (int k = 0; k < 3; k++) { r_lo[wv][k] = lo3[k]; r_hi[wv][k] = hi3[k]; }
+    }
+    __syncthreads();
+    sd = (r_sd[0] + r_sd[1]) + (r_sd[2] + r_sd[3]);
+    z = (r_z[0] + r_z[1]) + (r_z[2] + r_z[3]);
+    sdn = (r_sdn[0] + r_sdn[1]) + (r_sdn[2] + r_sdn[3]);
+    int mm[6];
+#pragma unroll
+    for (int k = 0; k < 3; k++) {
+        mm[2 * k] = min(min(r_lo[0][k], r_lo[1][k]), min(r_lo[2][k], r_lo[3][k])) - 128;
+        mm[2 * k + 1] = max(max(r_hi[0][k], r_hi[1][k]), max(r_hi[2][k], r_hi[3][k])) - 128;
+    }
+    if (t == 0) {
+        o.dbeta[c] = sd;
+        o.dgamma[c] = sdn;
+    }
     const int gq = o.gamma_q[c];
     const int e_xh = sv.hdr[0] - (cf.k_xhat - 1);
     const int e_sig = 2 - cf.k_sigma, e_g = 2 - cf.k_gamma;
     const int Ebase = *o.dy_exp + e_g - e_sig + (e_xh < 0 ? e_xh : 0);
     const i128 M = Mrows;
     const i128 Dd = (i128)sv.den[c] * M * M;
-    const i128 Sf = (i128)gq * w.sd[c], T = (i128)gq * w.sdn[c], Z = w.Z[c];
-    const int64_t f = d < -127 ? 0 : clamp_k((int64_t)gq * d, cf.k_E2);
-    for (int k = 0; k < 3; k++) {
-        int8_t code = 0;
-        if (d >= -127) {
-            const i128 B = bnb_bracket(f, k - 1, M, Sf, T, Z, e_xh);
-            code = (int8_t)clamp_k128(rhu128(B, Ebase + (cf.k_E1 - 1) - bdx, Dd), cf.k_E1);
+    const i128 Sf = (i128)gq * sd, T = (i128)gq * sdn, Z = z;
+    // the six per-class candidates (threads 0..5 of wave 0), their max
+    if (wv == 0) {
+        int cand = kSentinelLo;
+        if (t < 6) {
+            const int lo = mm[t & ~1], hi = mm[t | 1];
+            if (lo <= hi) {
+                const int64_t f = clamp_k((int64_t)gq * ((t & 1) ? hi : lo), cf.k_E2);
+                const i128 B = bnb_bracket(f, (t >> 1) - 1, M, Sf, T, Z, e_xh);
+                if (B != 0) cand = ceil_pow2_exp128(abs128(B), Dd) + Ebase;
+            }
         }
-        w.lut[((int64_t)c * 3 + k) * 256 + threadIdx.x] = code;
+        for (int off = 4; off > 0; off >>= 1) cand = max(cand, __shfl_xor(cand, off, 64));
+        if (t == 0) {
+            r_cand = cand;
+            w.cbnd[c] = cand;
+        }
+    }
+    __syncthreads();
+    const int bc = r_cand;
+    const int d = t - 128;
+    const int S = Ebase + (cf.k_E1 - 1) - bc + 1;
+    for (int k = 0; k < 3; k++) {
+        int16_t q = 0;
+        if (bc != kSentinelLo && d >= mm[2 * k] && d <= mm[2 * k + 1] && d >= -127) {
+            const int64_t f = clamp_k((int64_t)gq * d, cf.k_E2);
+            const i128 B = bnb_bracket(f, k - 1, M, Sf, T, Z, e_xh);
+            i128 Q = S >= 0 ? floordiv128(B << S, Dd) : floordiv128(B, Dd << -S);
+            Q = Q > 32767 ? 32767 : (Q < -32767 ? -32767 : Q);
+            q = (int16_t)Q;
+        }
+        w.lutq[((int64_t)c * 3 + k) * 256 + t] = q;
     }
 }
 
@@ -1568,15 +1611,50 @@ __global__ __launch_bounds__(256) void k_bnb_lut_exact(int64_t Mrows, int nslice
 // code) entry gives the offset of the channel's class row in the block's LDS
 // copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
 // element costs two LDS reads and a handful of ALU operations.
+// Exact E2: every block first takes E1's exponent from the channels' bounds
+// (block (0, 0) writes it and the parameter-gradient exponents) and rounds
+// its channels' staged values into the codes.
 __global__ __launch_bounds__(1024) void k_bnb_apply(const int8_t* __restrict__ dy,
                                                    const int8_t* __restrict__ x,
                                                    int8_t* __restrict__ dx, Stream st, BwdWs w,
-                                                   Saved sv, int32_t relu)
+                                                   Saved sv, BnCfg cf, BnbOut o, int32_t exact)
 {
     __shared__ __attribute__((aligned(16))) int8_t lut[64 * 3 * kRowB];
     __shared__ __attribute__((aligned(16))) uint32_t tab[64 * kRowW];
+    __shared__ int32_t rb[kNT / 64];
+    const int relu = cf.relu;
     const int64_t cbase = (int64_t)blockIdx.y * st.CS;
-    copy_rows_to_lds<64 * 3 * 16 / kNT>(lut, w.lut + cbase * 768, st.CS * 3);
+    if (exact) {
+        int bdx = kSentinelLo;
+        for (int i = threadIdx.x; i < st.C; i += kNT) bdx = max(bdx, w.cbnd[i]);
+        bdx = block_max_nt(bdx, rb);
+        if (bdx == kSentinelLo) bdx = 0;
+        if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+            *o.dx_exp = bdx - (cf.k_E1 - 1);
+            bnb_exps_out(sv, cf, o);
+        }
+        const int lim = (1 << (cf.k_E1 - 1)) - 1;
+        const int16_t* src = w.lutq + cbase * 768;
+        for (int v = threadIdx.x; v < st.CS * 96; v += kNT) {      // eight values per step
+            const int i0 = v * 8, row = i0 >> 8, col = i0 & 255;
+            const int bc = w.cbnd[cbase + row / 3];
+            const int sh = bc == kSentinelLo ? 31 : min(bdx - bc, 31);
+            const int4 q = *(const int4*)(src + i0);
+            const uint32_t qw[4] = {(uint32_t)q.x, (uint32_t)q.y, (uint32_t)q.z, (uint32_t)q.w};
+            uint32_t ow[2] = {0, 0};
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+                const int qv = (int)(int16_t)(qw[e >> 1] >> (16 * (e & 1)));
+                int cv = ((qv >> sh) + 1) >> 1;
+                cv = cv > lim ? lim : (cv < -lim ? -lim : cv);
+                ow[e >> 2] |= (uint32_t)(uint8_t)cv << (8 * (e & 3));
+            }
+            *(uint32_t*)(lut + row * kRowB + col) = ow[0];
+            *(uint32_t*)(lut + row * kRowB + col + 4) = ow[1];
+        }
+    } else {
+        copy_rows_to_lds<64 * 3 * 16 / kNT>(lut, w.lut + cbase * 768, st.CS * 3);
+    }
     load_bwd_tab(tab, sv.btab + cbase * 256, st.CS, relu, true);
     __syncthreads();
     int g, rsub;
@@ -1789,7 +1867,7 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     if (exact_e2) {
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<1>, sg, dim3(kNT), 0, stream, dy, x, st, w,
                           sv, cf, out);
-        hipLaunchKernelGGL(k_bnb_lut_exact, cb, dim3(256), 0, stream, M, (int)sg.y, w, sv, cf, out);
+        hipLaunchKernelGGL(k_bnb_chan_exact, cb, dim3(256), 0, stream, M, (int)st.gx, w, sv, cf, out);
     } else {
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<2>, sg, dim3(kNT), 0, stream, dy, x, st,
                           w, sv, cf, out);
@@ -1799,7 +1877,7 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     // the output pass needs no partials: its grid holds more rows per lane
     const Stream sa = make_stream(M, C, cs, 4, 8, kMaxBlocks);
     ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_APPLY, stream, k_bnb_apply, stream_grid(sa), dim3(kNT), 0, stream, dy, x,
-                      dx_out, sa, w, sv, cf.relu);
+                      dx_out, sa, w, sv, cf, out, exact_e2);
     return launch_ok();
 }
 
