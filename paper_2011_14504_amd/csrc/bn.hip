@@ -38,6 +38,7 @@
 namespace {
 
 constexpr int kSentinelLo = -(1 << 30);
+typedef short short2v __attribute__((ext_vector_type(2)));
 
 // launch geometry of the streaming passes (compile-time tuning knobs)
 #ifndef ISEG_BN_NT
@@ -1633,21 +1634,23 @@ __global__ __launch_bounds__(1024) void k_bnb_apply(const int8_t* __restrict__ d
             *o.dx_exp = bdx - (cf.k_E1 - 1);
             bnb_exps_out(sv, cf, o);
         }
-        const int lim = (1 << (cf.k_E1 - 1)) - 1;
+        const short lim = (short)((1 << (cf.k_E1 - 1)) - 1);
         const int16_t* src = w.lutq + cbase * 768;
-        for (int v = threadIdx.x; v < st.CS * 96; v += kNT) {      // eight values per step
+        for (int v = threadIdx.x; v < st.CS * 96; v += kNT) {      // eight values per step, two per op
             const int i0 = v * 8, row = i0 >> 8, col = i0 & 255;
             const int bc = w.cbnd[cbase + row / 3];
-            const int sh = bc == kSentinelLo ? 31 : min(bdx - bc, 31);
+            const short sh = (short)(bc == kSentinelLo ? 15 : min(bdx - bc, 15));
             const int4 q = *(const int4*)(src + i0);
-            const uint32_t qw[4] = {(uint32_t)q.x, (uint32_t)q.y, (uint32_t)q.z, (uint32_t)q.w};
+            const int qw[4] = {q.x, q.y, q.z, q.w};
             uint32_t ow[2] = {0, 0};
 #pragma unroll
-            for (int e = 0; e < 8; e++) {
-                const int qv = (int)(int16_t)(qw[e >> 1] >> (16 * (e & 1)));
-                int cv = ((qv >> sh) + 1) >> 1;
-                cv = cv > lim ? lim : (cv < -lim ? -lim : cv);
-                ow[e >> 2] |= (uint32_t)(uint8_t)cv << (8 * (e & 3));
+            for (int h = 0; h < 4; h++) {
+                short2v qv = __builtin_bit_cast(short2v, qw[h]);
+                qv = ((qv >> sh) + (short)1) >> (short)1;
+                qv = qv > lim ? lim : qv;
+                qv = qv < (short)-lim ? (short)-lim : qv;
+                const uint32_t b = (uint32_t)(uint16_t)qv.x & 0xffu | ((uint32_t)(uint16_t)qv.y & 0xffu) << 8;
+                ow[h >> 1] |= b << (16 * (h & 1));
             }
             *(uint32_t*)(lut + row * kRowB + col) = ow[0];
             *(uint32_t*)(lut + row * kRowB + col + 4) = ow[1];
