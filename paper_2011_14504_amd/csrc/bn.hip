@@ -1152,8 +1152,8 @@ __global__ __launch_bounds__(1024) void k_bnb_stats(const int8_t* __restrict__ d
         uint32_t A, B;
         mm_pack(bmm, A, B);
         if constexpr (TAIL == 1) {
-            // channel-major for the per-channel kernel that follows
-            const int64_t o = (cbase + t) * st.gx + blockIdx.x;
+            // [slice][block][channel of the slice]: one contiguous row per block
+            const int64_t o = ((int64_t)blockIdx.y * st.gx + blockIdx.x) * st.CS + t;
             w.p_sd[o] = bsd;
             w.p_sdn[o] = bsdn;
             w.p_z[o] = bz;
@@ -1518,8 +1518,8 @@ __device__ __forceinline__ void bnb_round_tail2(uint32_t* lds, const Stream& st,
 // |Q| <= 2^k_E1 + 1 there, so int16 holds it; the output pass rounds Q by
 // the gap between the largest bound and the channel's into the final code
 // (half-up rounding of floor(x) by 2^g + 1 equals that of x).
-__global__ __launch_bounds__(256) void k_bnb_chan_exact(int64_t Mrows, int gx, BwdWs w, Saved sv, BnCfg cf,
-                                                        BnbOut o)
+__global__ __launch_bounds__(256) void k_bnb_chan_exact(int64_t Mrows, int gx, int CS, BwdWs w, Saved sv,
+                                                        BnCfg cf, BnbOut o)
 {
     __shared__ int32_t r_sd[4], r_z[4], r_lo[4][3], r_hi[4][3], r_cand;
     __shared__ long long r_sdn[4];
@@ -1527,8 +1527,9 @@ __global__ __launch_bounds__(256) void k_bnb_chan_exact(int64_t Mrows, int gx, B
     int sd = 0, z = 0;
     long long sdn = 0;
     int lo3[3] = {255, 255, 255}, hi3[3] = {0, 0, 0};       // byte-coded extremes (empty: lo > hi)
+    const int sy = c / CS, sc = c - sy * CS;                  // slice, channel within it
     for (int b = t; b < gx; b += blockDim.x) {
-        const int64_t q = (int64_t)c * gx + b;
+        const int64_t q = ((int64_t)sy * gx + b) * CS + sc;
         sd += w.p_sd[q];
         sdn += w.p_sdn[q];
         z += w.p_z[q];
@@ -1870,7 +1871,7 @@ extern "C" int iseg_bn_bwd(const int8_t* dy, const int32_t* dy_exp, const int8_t
     if (exact_e2) {
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<1>, sg, dim3(kNT), 0, stream, dy, x, st, w,
                           sv, cf, out);
-        hipLaunchKernelGGL(k_bnb_chan_exact, cb, dim3(256), 0, stream, M, (int)st.gx, w, sv, cf, out);
+        hipLaunchKernelGGL(k_bnb_chan_exact, cb, dim3(256), 0, stream, M, (int)st.gx, (int)st.CS, w, sv, cf, out);
     } else {
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_BWD_STATS, stream, k_bnb_stats<2>, sg, dim3(kNT), 0, stream, dy, x, st,
                           w, sv, cf, out);

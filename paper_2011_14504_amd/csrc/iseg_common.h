@@ -8,6 +8,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 #include "iseg.h"
@@ -298,18 +299,27 @@ bool lds_limit(const void* f, size_t bytes);
 // *maxp = max over n block partials (one block)
 int launch_reduce_max(const uint64_t* part, int64_t n, unsigned long long* maxp, hipStream_t s);
 
-// measurement hook (iseg_profile_arm): wrap one kernel launch.  prof_begin
-// claims the armed hook for this launch (at most one launch ever claims one
-// arming) and returns the event to record after it, or nullptr.
+// measurement hook (iseg_profile_arm).  prof_claim takes the armed hook for
+// one launch (at most one launch ever claims one arming) and hands out its
+// two events; prof_begin claims it and records the start event, returning the
+// stop event to record after the work, or nullptr.
+bool prof_claim(int kid, hipEvent_t* start, hipEvent_t* stop);
 hipEvent_t prof_begin(int kid, hipStream_t s);
 void prof_end(hipEvent_t stop, hipStream_t s);
 
-#define ISEG_TIMED_LAUNCH(kid, stream, ...)                   \
-    do {                                                      \
-        hipEvent_t iseg_timed_ = prof_begin((kid), (stream)); \
-        hipLaunchKernelGGL(__VA_ARGS__);                      \
-        if (iseg_timed_) prof_end(iseg_timed_, (stream));     \
-    } while (0)
+// One kernel launch under the hook: when armed, the events are attached to
+// the dispatch itself (hipExtLaunchKernelGGL), so they carry the kernel's own
+// start and end times, without the queue markers of separate event records.
+template <typename F, typename... A>
+void timed_launch(int kid, F kernel, const dim3& grid, const dim3& block, uint32_t shmem, hipStream_t s, A... args)
+{
+    hipEvent_t start = nullptr, stop = nullptr;
+    if (prof_claim(kid, &start, &stop))
+        hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, start, stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+}
+#define ISEG_TIMED_LAUNCH(kid, stream, ...) timed_launch((kid), __VA_ARGS__)
 
 // measurement hook around a whole entry-point call (every kernel it enqueues)
 struct ProfScope {

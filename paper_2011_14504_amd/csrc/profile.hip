@@ -42,14 +42,23 @@ __global__ __launch_bounds__(256) void k_check_codes(const int8_t* __restrict__ 
 }
 }  // namespace
 
+bool prof_claim(int kid, hipEvent_t* start, hipEvent_t* stop)
+{
+    if (kid == ISEG_KID_NONE || g_kid.load(std::memory_order_relaxed) != kid) return false;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_kid.load(std::memory_order_relaxed) != kid) return false;
+    g_kid.store(ISEG_KID_NONE, std::memory_order_relaxed);
+    *start = g_start;
+    *stop = g_stop;
+    return true;
+}
+
 hipEvent_t prof_begin(int kid, hipStream_t s)
 {
-    if (kid == ISEG_KID_NONE || g_kid.load(std::memory_order_relaxed) != kid) return nullptr;
-    std::lock_guard<std::mutex> lk(g_mu);
-    if (g_kid.load(std::memory_order_relaxed) != kid) return nullptr;
-    g_kid.store(ISEG_KID_NONE, std::memory_order_relaxed);
-    hipEventRecord(g_start, s);
-    return g_stop;
+    hipEvent_t start, stop;
+    if (!prof_claim(kid, &start, &stop)) return nullptr;
+    hipEventRecord(start, s);
+    return stop;
 }
 
 void prof_end(hipEvent_t stop, hipStream_t s) { hipEventRecord(stop, s); }
