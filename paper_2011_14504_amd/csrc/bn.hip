@@ -19,17 +19,20 @@
 // streaming passes get them from two thresholds per channel instead of a
 // table.
 //
-// Forward:  stats1 (sum q, min q, max q | tails: n_mu) -> stats2 (sum
-//           |x - mu_q| | tails: n_sigma, den, the slice's bound on b) -> fin2
-//           (b; xhat codes, y, thresholds, max|y|) -> fin3 (A codes) -> apply
-//           (table gather).
-// Backward: stats (sum delta, sum delta*xhat, sum sgn, per-class extremes of
-//           delta | tails: dgamma, dbeta and, for k_E2 >= 15, each slice's
-//           bound on E1's exponent) -> table (E1's exponent from the slices'
-//           bounds) -> apply (gather).  k_E2 < 15 adds a second streaming
-//           pass: stats tails give each slice's max|gamma delta| (E2's scale
-//           is the largest), stats2 sums the rounded E2 terms and its tails
-//           give the slices' bounds on E1's exponent.
+// Forward:  stats1 (block partials of sum q, min q, max q) -> stats2 (each
+//           block first forms n_mu and the occupied code range of its slice
+//           from them; sum |x - mu_q| | tails: n_sigma, den, the slice's
+//           bound on b) -> fin2 (b; xhat codes, y, thresholds, max|y|) ->
+//           fin3 (A codes) -> apply (table gather).
+// Backward: exact E2 (k_E2 >= 15): stats (block partials of sum delta, sum
+//           delta*xhat, sum sgn and the per-class extremes of delta) ->
+//           per-channel kernel (dgamma, dbeta, the channel's bound on E1's
+//           exponent, its dx values staged at that bound) -> apply (E1's
+//           exponent from the channels' bounds; staged values rounded into
+//           the gather table).  k_E2 < 15 adds a second streaming pass: stats
+//           tails give each slice's max|gamma delta| (E2's scale is the
+//           largest), stats2 sums the rounded E2 terms and its tails give the
+//           slices' bounds on E1's exponent; a table kernel, then apply.
 #include <mutex>
 #include <type_traits>
 
@@ -421,7 +424,7 @@ __device__ __forceinline__ T block_max_nt(T v, T* sh)
 struct FwdWs {
     uint32_t* ctr;                   // arrival counters
     int32_t* b_glob;                 // exponent of Q_xhat's scale (fin2, block 0)
-    int32_t *p_s1, *p_mm;            // [gx][C] partials: sum q; (min q + 128) | (max q + 128) << 16
+    int32_t *p_s1, *p_mm;            // [slice][gx][CS] partials: sum q; (min q + 128) | (max q + 128) << 16
     long long* p_abs;                // [gx][C]
     int32_t* sbmax;                  // [slices] largest channel bound on b of each slice (stats2's tails)
     unsigned long long* maxYc;       // [C] max |ReLU(y)| of channel c over its occupied codes (fin2)
@@ -471,12 +474,9 @@ FwdWs fwd_ws_map(void* base, const Stream& st)
 constexpr int kTailU = 8;
 
 template <int CPL>
-__global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ x, const int32_t* x_exp,
-                                                    Stream st, FwdWs w, Saved sv, BnCfg cf)
+__global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ x, Stream st, FwdWs w)
 {
     __shared__ int32_t sS[128], sMin[128], sMax[128];
-    __shared__ long long tS[kNT];
-    __shared__ int32_t tMm[kNT];
     __shared__ int32_t wst[3 * kWaves * 128];      // wave totals [quantity][wave][channel]
     const bool fold = (st.G & (st.G - 1)) == 0 && st.G <= 64;
     if (!fold && (int)threadIdx.x < st.CS) { sS[threadIdx.x] = 0; sMin[threadIdx.x] = 1000; sMax[threadIdx.x] = -1000; }
@@ -541,53 +541,13 @@ __global__ __launch_bounds__(1024) void k_bnf_stats1(const int8_t* __restrict__ 
         }
     }
     __syncthreads();
-    // every block holds at least one row of the slice, so its extremes are codes
+    // every block holds at least one row of the slice, so its extremes are
+    // codes; one contiguous row of partials per block, reduced by every block
+    // of the next pass for its slice
     if ((int)threadIdx.x < st.CS) {
-        int64_t o = (int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x;
-        st_x(&w.p_s1[o], sS[threadIdx.x]);
-        st_x(&w.p_mm[o], (sMin[threadIdx.x] + 128) | ((sMax[threadIdx.x] + 128) << 16));
-    }
-    if (!arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) return;
-    // slice tail: sum, min and max of each channel over the slice's partial rows
-    const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
-    const int64_t cb = (int64_t)blockIdx.y * CS;
-    long long sum = 0;
-    int lo = 255, hi = 0;
-    if (grp < ng)
-        for (int b0 = grp; b0 < st.gx; b0 += kTailU * ng) {
-            int32_t vs[kTailU], vm[kTailU];
-#pragma unroll
-            for (int u = 0; u < kTailU; u++) {
-                const int b = b0 + u * ng;
-                const int64_t q = (int64_t)(b < st.gx ? b : b0) * st.C + cb + ch;
-                vs[u] = ld_x(&w.p_s1[q]);
-                vm[u] = ld_x(&w.p_mm[q]);
-            }
-#pragma unroll
-            for (int u = 0; u < kTailU; u++) {
-                if (b0 + u * ng < st.gx) sum += vs[u];
-                lo = min(lo, vm[u] & 0xffff);           // a repeated row changes no extreme
-                hi = max(hi, vm[u] >> 16);
-            }
-        }
-    tS[t] = sum;
-    tMm[t] = lo | (hi << 16);
-    __syncthreads();
-    if (t < CS) {
-        for (int g2 = 1; g2 < ng; g2++) {
-            const int i = g2 * CS + t;
-            sum += tS[i];
-            lo = min(lo, tMm[i] & 0xffff);
-            hi = max(hi, tMm[i] >> 16);
-        }
-        const int32_t s_x = *x_exp;
-        int32_t nm = 0;
-        if (sx_ok(s_x))   // mu/2 = S1 2^(s_x - 1) / M, code floor(mu/2 2^(k_mu-1) + 1/2)
-            nm = (int32_t)clamp_k128(rhu128((i128)sum, s_x - 1 + (cf.k_mu - 1), (i128)st.M), cf.k_mu);
-        const int64_t c = cb + t;
-        sv.n_mu[c] = nm;
-        sv.qmin[c] = lo - 128;
-        sv.qmax[c] = hi - 128;
+        const int64_t o = ((int64_t)blockIdx.y * st.gx + blockIdx.x) * st.CS + threadIdx.x;
+        w.p_s1[o] = sS[threadIdx.x];
+        w.p_mm[o] = (sMin[threadIdx.x] + 128) | ((sMax[threadIdx.x] + 128) << 16);
     }
 }
 
@@ -633,6 +593,50 @@ __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ 
         s_x = -14;     // keep shifts defined; outputs are unspecified
     }
     if (!fold && (int)threadIdx.x < st.CS) sA[threadIdx.x] = 0;
+    // prologue: n_mu (Eq. 12) and the occupied code range of the slice's
+    // channels from stats1's partial rows (every block of the slice forms them;
+    // the slice's last block stores them)
+    __shared__ int32_t sNmu[128], sLo[128], sHi[128];
+    {
+        const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
+        const int32_t* ps = w.p_s1 + (int64_t)blockIdx.y * st.gx * CS;
+        const int32_t* pm = w.p_mm + (int64_t)blockIdx.y * st.gx * CS;
+        long long sum = 0;
+        int lo = 255, hi = 0;
+        if (grp < ng)
+            for (int b0 = grp; b0 < st.gx; b0 += kTailU * ng) {
+                int32_t vs[kTailU], vm[kTailU];
+#pragma unroll
+                for (int u = 0; u < kTailU; u++) {
+                    const int b = b0 + u * ng;
+                    const int64_t q = (int64_t)(b < st.gx ? b : b0) * CS + ch;
+                    vs[u] = ps[q];
+                    vm[u] = pm[q];
+                }
+#pragma unroll
+                for (int u = 0; u < kTailU; u++) {
+                    if (b0 + u * ng < st.gx) sum += vs[u];
+                    lo = min(lo, vm[u] & 0xffff);       // a repeated row changes no extreme
+                    hi = max(hi, vm[u] >> 16);
+                }
+            }
+        tA[t] = sum;
+        __shared__ int32_t tMm[kNT];
+        tMm[t] = lo | (hi << 16);
+        __syncthreads();
+        if (t < CS) {
+            for (int g2 = 1; g2 < ng; g2++) {
+                const int i = g2 * CS + t;
+                sum += tA[i];
+                lo = min(lo, tMm[i] & 0xffff);
+                hi = max(hi, tMm[i] >> 16);
+            }
+            // mu/2 = S1 2^(s_x - 1) / M, code floor(mu/2 2^(k_mu-1) + 1/2)
+            sNmu[t] = (int32_t)clamp_k128(rhu128((i128)sum, s_x - 1 + (cf.k_mu - 1), (i128)st.M), cf.k_mu);
+            sLo[t] = lo - 128;
+            sHi[t] = hi - 128;
+        }
+    }
     __syncthreads();
     const int e_mu = 2 - cf.k_mu;
     int g, rsub;
@@ -646,7 +650,7 @@ __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ 
         const int64_t mulq = (int64_t)1 << (s_x - gg);
         int64_t off[CPL];
 #pragma unroll
-        for (int i = 0; i < CPL; i++) off[i] = (int64_t)sv.n_mu[c0 + i] * ((int64_t)1 << (e_mu - gg));
+        for (int i = 0; i < CPL; i++) off[i] = (int64_t)sNmu[g * CPL + i] * ((int64_t)1 << (e_mu - gg));
         stream_rows<CPL, 4>(st, x, c0, rsub, [&](int64_t, const Vec<CPL>& v) {
 #pragma unroll
             for (int i = 0; i < CPL; i++) {
@@ -711,9 +715,12 @@ __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ 
             if (den < 1) den = 1;
             sv.n_sigma[c] = ns;
             sv.den[c] = den;
-            const int32_t nm = sv.n_mu[c];
+            const int32_t nm = sNmu[t];
+            sv.n_mu[c] = nm;
+            sv.qmin[c] = sLo[t];
+            sv.qmax[c] = sHi[t];
             int best = kSentinelLo;
-            const int qs[2] = {sv.qmin[c], sv.qmax[c]};
+            const int qs[2] = {sLo[t], sHi[t]};
             for (int k = 0; k < 2; k++) {          // xhat is linear in q: extremes at qmin / qmax
                 const int64_t D = bn_D(qs[k], s_x, nm, e_mu);
                 if (D == 0) continue;
@@ -1763,11 +1770,9 @@ static int bn_fwd_impl(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t
     dim3 sg = stream_grid(st);
     dim3 cb((unsigned)C);
     if (s16)
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<16>, sg, dim3(kNT), 0, stream, x, x_exp, st,
-                          w, sv, cf);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<16>, sg, dim3(kNT), 0, stream, x, st, w);
     else
-        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<4>, sg, dim3(kNT), 0, stream, x, x_exp, st,
-                          w, sv, cf);
+        ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS1, stream, k_bnf_stats1<4>, sg, dim3(kNT), 0, stream, x, st, w);
     if (s16)
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2<16>, sg, dim3(kNT), 0, stream, x, x_exp,
                           st, w, sv, cf, dev_status);
