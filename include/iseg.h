@@ -261,7 +261,10 @@ int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, const int8_t* 
  *   input code + 128); uint8 flags[C][256] (bit0: y > 0, bits1-2: sgn(x -
  *   mu_q) + 1); int8 a_code[C][256]; uint32 bwd_entry[C][256] (by the
  *   input code's byte, q & 0xff: bit0 y > 0, bits 8-9 sgn(x - mu_q) as a
- *   two-bit signed field, bit 10 |sgn|, bits 16-31 the xhat code). */
+ *   two-bit signed field, bit 10 |sgn|, bits 16-31 the xhat code); int16
+ *   y_staged[C][256] (by input code + 128: ReLU(y) on the y grid floored by
+ *   2^t_c, t_c = max(0, r_c - 1) with r_c the Q_A shift of channel c's own
+ *   max |ReLU(y)|, clamped to +-32767; the output pass's working copy). */
 size_t iseg_bn_saved_bytes(int64_t C);
 size_t iseg_bn_fwd_ws(int64_t M, int64_t C);
 int iseg_bn_fwd(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t C,

@@ -22,8 +22,9 @@
 // Forward:  stats1 (block partials of sum q, min q, max q) -> stats2 (each
 //           block first forms n_mu and the occupied code range of its slice
 //           from them; sum |x - mu_q| | tails: n_sigma, den, the slice's
-//           bound on b) -> fin2 (b; xhat codes, y, thresholds, max|y|) ->
-//           fin3 (A codes) -> apply (table gather).
+//           bound on b) -> fin2 (b; xhat codes, y, thresholds, max|y|, y
+//           staged at each channel's own Q_A shift) -> apply (Q_A's shift from
+//           the channels' maxima; A codes; table gather).
 // Backward: exact E2 (k_E2 >= 15): stats (block partials of sum delta, sum
 //           delta*xhat, sum sgn and the per-class extremes of delta) ->
 //           per-channel kernel (dgamma, dbeta, the channel's bound on E1's
@@ -69,12 +70,13 @@ struct Saved {
     uint8_t* flags;                  // [C][256]
     int8_t* acode;                   // [C][256]
     uint32_t* btab;                  // [C][256] by q & 0xff: y > 0, sgn, |sgn|, xhat code
+    int16_t* ystg;                   // [C][256] ReLU(y) >> t_c (the output pass's staged A values)
 };
 
 size_t saved_bytes(int64_t C)
 {
     return 256 + 9 * align256((size_t)C * 4) + align256((size_t)C * 512) +
-           2 * align256((size_t)C * 256) + align256((size_t)C * 1024);
+           2 * align256((size_t)C * 256) + align256((size_t)C * 1024) + align256((size_t)C * 512);
 }
 
 Saved saved_map(void* base, int64_t C)
@@ -95,7 +97,8 @@ Saved saved_map(void* base, int64_t C)
     s.xcode = (int16_t*)p; p += align256((size_t)C * 512);
     s.flags = (uint8_t*)p; p += align256((size_t)C * 256);
     s.acode = (int8_t*)p; p += align256((size_t)C * 256);
-    s.btab = (uint32_t*)p;
+    s.btab = (uint32_t*)p; p += align256((size_t)C * 1024);
+    s.ystg = (int16_t*)p;
     return s;
 }
 
@@ -456,14 +459,16 @@ FwdWs fwd_ws_map(void* base, const Stream& st)
 // ---------------------------------------------------------------------------
 // forward kernels
 //
-// stats1 | tails: n_mu and the occupied code range of each channel of the slice
-// stats2 | tails: n_sigma, the denominator and each channel's bound on
-//          max|xhat|; the slice's largest bound
+// stats1 | block partials of sum q, min q, max q
+// stats2 | prologue: n_mu and the occupied code range of the slice's channels
+//          from stats1's partials | tails: n_sigma, the denominator and each
+//          channel's bound on max|xhat|; the slice's largest bound
 // fin2   (one block per channel, one thread per code): b (Q_xhat's scale) from
 //          the slices' bounds; xhat codes, y, sgn / ReLU thresholds, the
-//          backward's entries and the channel's max|ReLU(y)|
-// fin3   (likewise): Q_A's shift r from the channels' maxima; A codes
-// apply  (table gather)
+//          backward's entries, the channel's max|ReLU(y)| and ReLU(y) staged
+//          at the channel's own Q_A shift
+// apply  Q_A's shift r from the channels' maxima; the saved A codes; the
+//          gather table from the staged values; table gather
 // ---------------------------------------------------------------------------
 
 // Partial rows of a slice tail in flight per thread: the thread of channel
@@ -751,6 +756,14 @@ __device__ __forceinline__ int32_t slices_max(const int32_t* a, int n, int32_t* 
     return m;
 }
 
+// shift of a channel's staged A values: max(0, r_c - 1), r_c = bitlen(max) -
+// (k_A - 1) the Q_A shift of the channel's own max |ReLU(y)|
+__device__ __forceinline__ int ystg_shift(uint64_t maxy, int kA)
+{
+    const int rc = maxy ? bitlen_u64(maxy) - (kA - 1) : 0;
+    return rc > 1 ? rc - 1 : 0;
+}
+
 // per (channel, code): xhat code, y, flags and the backward's entry; per
 // channel: the sgn and ReLU thresholds and max |ReLU(y)| over the occupied
 // codes (y is monotone in q, so over qmin and qmax)
@@ -792,6 +805,7 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, int nsli
     const int wv = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) { red[wv][0] = v0; red[wv][1] = v1; red[wv][2] = v2; red[wv][3] = v3; ry[wv] = ay; }
     __syncthreads();
+    __shared__ uint64_t s_ay;
     if (threadIdx.x == 0) {
         for (int k = 1; k < 4; k++) {
             v0 = min(v0, red[k][0]); v1 = min(v1, red[k][1]); v2 = min(v2, red[k][2]); v3 = max(v3, red[k][3]);
@@ -799,41 +813,93 @@ __global__ __launch_bounds__(256) void k_bnf_fin2(const int32_t* x_exp, int nsli
         }
         sv.t0[c] = v0; sv.p0[c] = v1; sv.mlo[c] = v2; sv.mhi[c] = v3;
         w.maxYc[c] = ay;
+        s_ay = ay;
     }
+    __syncthreads();
+    // ReLU(y) floored by 2^t_c, t_c = max(0, r_c - 1) with r_c the Q_A shift
+    // this channel's own maximum would give: below 2^k_A in magnitude for the
+    // occupied codes (clamped elsewhere, where the output pass never looks)
+    const int tc = ystg_shift(s_ay, cf.k_A);
+    i128 z = tc ? (Yr >> tc) : Yr;
+    z = z > 32767 ? 32767 : (z < -32767 ? -32767 : z);
+    sv.ystg[idx] = (int16_t)z;
 }
 
-// A codes per (channel, code) with Q_A's shift from the channels' maxima
-__global__ __launch_bounds__(256) void k_bnf_fin3(const int32_t* x_exp, FwdWs w, Saved sv, BnCfg cf,
-                                                  const int8_t* gamma_q, const int8_t* beta_q, int32_t* y_exp)
+// Output pass.  Every block first takes Q_A's shift r from the channels'
+// maxima (block (0, 0) writes the output exponent and the saved header), then
+//   * writes its share of the saved A codes, exactly from the xhat codes (the
+//     table the inference path applies, every code included);
+//   * builds its channels' gather table from the staged values:
+//     code = ((z >> (r - 1 - t_c)) + 1) >> 1, the half-up rounding of
+//     ReLU(y) by 2^r (half-up rounding of floor(v / 2^t) by 2^(r - t) equals
+//     that of v for t < r), two codes per packed 16-bit operation.
+template <int CPL>
+__global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x, int8_t* __restrict__ y,
+                                                   Stream st, Saved sv, FwdWs w, BnCfg cf, const int32_t* x_exp,
+                                                   const int8_t* gamma_q, const int8_t* beta_q, int32_t* y_exp)
 {
-    const int c = blockIdx.x;
+    __shared__ __attribute__((aligned(16))) int8_t lut[128 * kRowB];
+    __shared__ uint64_t rmax[kNT / 64];
+    uint64_t M = 0;
+    for (int k = threadIdx.x; k < st.C; k += kNT) M = w.maxYc[k] > M ? w.maxYc[k] : M;
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t t = __shfl_xor(M, o);
+        M = t > M ? t : M;
+    }
+    if ((threadIdx.x & 63) == 0) rmax[threadIdx.x >> 6] = M;
+    __syncthreads();
+    M = rmax[0];
+    for (int k = 1; k < kNT / 64; k++) M = rmax[k] > M ? rmax[k] : M;
+    const int r = M ? bitlen_u64(M) - (cf.k_A - 1) : 0;
     int32_t s_x = *x_exp;
-    if (!sx_ok(s_x)) return;
+    const bool ok = sx_ok(s_x);
+    if (!ok) s_x = -14;          // outputs unspecified; keeps the shifts defined
     const int b = *w.b_glob;
     const FwdExps e = fwd_exps(s_x, b, cf);
-    uint64_t M = 0;                                  // max over the channels' candidates
-    for (int k = threadIdx.x; k < (int)gridDim.x; k += blockDim.x) M = w.maxYc[k] > M ? w.maxYc[k] : M;
-    M = block_max_u64(M);
-    const int r = M ? bitlen_u64(M) - (cf.k_A - 1) : 0;
-    const int idx = c * 256 + threadIdx.x;
-    i128 Y = fwd_y((i128)sv.xcode[idx], gamma_q[c], beta_q[c], e);
-    if (cf.relu && Y < 0) Y = 0;
-    sv.acode[idx] = (int8_t)sq_code((long long)Y, r, cf.k_A);
-    if (c == 0 && threadIdx.x == 0) {
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && ok) {
         *y_exp = e.e_y + r;
         sv.hdr[0] = b;
         sv.hdr[1] = e.e_y;
         sv.hdr[2] = e.e_y + r;
         sv.hdr[3] = s_x;
     }
-}
-
-template <int CPL>
-__global__ __launch_bounds__(1024) void k_bnf_apply(const int8_t* __restrict__ x, int8_t* __restrict__ y,
-                                                   Stream st, Saved sv)
-{
-    __shared__ __attribute__((aligned(16))) int8_t lut[128 * kRowB];
-    copy_rows_to_lds<128 * 16 / kNT>(lut, sv.acode + (int64_t)blockIdx.y * st.CS * 256, st.CS);
+    if (ok) {
+        const int64_t nall = (int64_t)st.C * 256, nb = (int64_t)gridDim.x * gridDim.y;
+        const int64_t per = (nall + nb - 1) / nb;
+        const int64_t i0 = ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * per;
+        for (int64_t i = i0 + threadIdx.x; i < i0 + per && i < nall; i += kNT) {
+            const int c = (int)(i >> 8);
+            i128 Yv = fwd_y((i128)sv.xcode[i], gamma_q[c], beta_q[c], e);
+            if (cf.relu && Yv < 0) Yv = 0;
+            sv.acode[i] = (int8_t)sq_code((long long)Yv, r, cf.k_A);
+        }
+    }
+    if (!ok) {
+        for (int i = threadIdx.x; i < st.CS * kRowB; i += kNT) lut[i] = 0;
+    } else {
+        const short lim = (short)((1 << (cf.k_A - 1)) - 1);
+        const int16_t* src = sv.ystg + (int64_t)blockIdx.y * st.CS * 256;
+        for (int v = threadIdx.x; v < st.CS * 32; v += kNT) {       // eight codes per step
+            const int i0 = v * 8, row = i0 >> 8, col = i0 & 255;
+            const int tc = ystg_shift(w.maxYc[blockIdx.y * st.CS + row], cf.k_A);
+            const int4 q = *(const int4*)(src + i0);
+            const int qw[4] = {q.x, q.y, q.z, q.w};
+            uint32_t ow[2] = {0, 0};
+            const short sh = (short)(r > 0 ? min(r - 1 - tc, 15) : 0), up = (short)(r < 0 ? -r : 0);
+#pragma unroll
+            for (int h = 0; h < 4; h++) {
+                short2v zv = __builtin_bit_cast(short2v, qw[h]);
+                if (r > 0) zv = ((zv >> sh) + (short)1) >> (short)1;
+                else zv = zv << up;
+                zv = zv > lim ? lim : zv;
+                zv = zv < (short)-lim ? (short)-lim : zv;
+                const uint32_t bb = ((uint32_t)(uint16_t)zv.x & 0xffu) | (((uint32_t)(uint16_t)zv.y & 0xffu) << 8);
+                ow[h >> 1] |= bb << (16 * (h & 1));
+            }
+            *(uint32_t*)(lut + row * kRowB + col) = ow[0];
+            *(uint32_t*)(lut + row * kRowB + col + 4) = ow[1];
+        }
+    }
     __syncthreads();
     int g, rsub;
     if (!stream_lane(st, g, rsub)) return;
@@ -1780,15 +1846,14 @@ static int bn_fwd_impl(const int8_t* x, const int32_t* x_exp, int64_t M, int64_t
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_STATS2, stream, k_bnf_stats2<4>, sg, dim3(kNT), 0, stream, x, x_exp,
                           st, w, sv, cf, dev_status);
     hipLaunchKernelGGL(k_bnf_fin2, cb, dim3(256), 0, stream, x_exp, (int)sg.y, w, sv, cf, gamma_q, beta_q);
-    hipLaunchKernelGGL(k_bnf_fin3, cb, dim3(256), 0, stream, x_exp, w, sv, cf, gamma_q, beta_q, y_exp);
     if (v16) {
         Stream a16 = make_stream(M, C, cs, 16, 4, kMaxBlocks);
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply<16>, stream_grid(a16), dim3(kNT), 0,
-                          stream, x, y_out, a16, sv);
+                          stream, x, y_out, a16, sv, w, cf, x_exp, gamma_q, beta_q, y_exp);
     } else {
         Stream s4 = make_stream(M, C, cs, 4, 4, kMaxBlocks);
         ISEG_TIMED_LAUNCH(ISEG_KID_BN_FWD_APPLY, stream, k_bnf_apply<4>, stream_grid(s4), dim3(kNT), 0, stream,
-                          x, y_out, s4, sv);
+                          x, y_out, s4, sv, w, cf, x_exp, gamma_q, beta_q, y_exp);
     }
     return launch_ok();
 }
