@@ -4246,12 +4246,65 @@ static int tconv_run(const TconvPlan& t, const iseg_conv_geom* g, int64_t P, int
     return launch_tconv_e<EPI_Q8>(t, a, stream);
 }
 
+// A strided 1x1 conv (a projection shortcut): its dx is zero off the stride
+// grid, and on it the stride-1 1x1 backward-data of dy over the P x Q output
+// pixels.  That GEMM runs on the output grid (a quarter of the rows at stride
+// 2, none of the products with the zeros between dy rows), and a pass writes
+// dx with the zeros interleaved.  The zeros change neither the max nor any
+// code, so the result and its exponent are those of the full backward-data.
+static bool strided_1x1(const iseg_conv_geom* g)
+{
+    return g->R == 1 && g->S == 1 && g->pad_h == 0 && g->pad_w == 0 && (g->stride_h > 1 || g->stride_w > 1) &&
+           g->C % 16 == 0 && g->N > 0;
+}
+
+static iseg_conv_geom strided_1x1_inner(const iseg_conv_geom* g, int64_t P, int64_t Q)
+{
+    iseg_conv_geom s = *g;
+    s.H = P; s.W = Q; s.stride_h = 1; s.stride_w = 1; s.dil_h = 1; s.dil_w = 1;
+    return s;
+}
+
+// dx from the output-grid result: 16-byte pieces of each pixel's row, the
+// stride grid's pixels copied, all others zero
+__global__ __launch_bounds__(256) void k_stride_scatter(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                        int64_t N, int32_t H, int32_t W, int32_t P, int32_t Q,
+                                                        int32_t sh, int32_t sw, int32_t row16)
+{
+    const int64_t n16 = N * H * W * (int64_t)row16;
+    const int64_t hw = (int64_t)H * W;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t pix = i / row16;
+        const int32_t k = (int32_t)(i - pix * row16);
+        const int64_t n = pix / hw;
+        const int32_t rem = (int32_t)(pix - n * hw);
+        const int32_t h = rem / W, w = rem - h * W;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (h % sh == 0 && w % sw == 0 && h / sh < P && w / sw < Q)
+            v = src[((n * P + h / sh) * Q + w / sw) * row16 + k];
+        dst[i] = v;
+    }
+}
+
+static size_t conv_bwd_data_core_ws(const iseg_conv_geom* g, int32_t out_mode);
+
+static size_t strided_1x1_ws(const iseg_conv_geom* g, int32_t out_mode, int64_t P, int64_t Q)
+{
+    const iseg_conv_geom s = strided_1x1_inner(g, P, Q);
+    const size_t es = out_mode == ISEG_OUT_Q8 ? 1 : 4;
+    return align256((size_t)(g->N * P * Q * g->C) * es) + conv_bwd_data_core_ws(&s, out_mode);
+}
+
 static size_t conv_bwd_data_core_ws(const iseg_conv_geom* g, int32_t out_mode)
 {
     int64_t P, Q;
     if (!geom_ok(g, &P, &Q)) return 0;
+    const size_t s1 = strided_1x1(g) ? strided_1x1_ws(g, out_mode, P, Q) : 0;
     const TconvPlan tp = tconv_plan(g);
-    if (tp.ok) return 256 + tconv_ws_bytes(g, tp);
+    if (tp.ok) {
+        const size_t st = 256 + tconv_ws_bytes(g, tp);
+        return st > s1 ? st : s1;
+    }
     size_t s = 256 + align256((size_t)(g->K * g->R * g->S * g->C));
     if (out_mode == ISEG_OUT_Q8) {
         size_t big = align256((size_t)(g->N * g->H * g->W * g->C) * 4);
@@ -4268,7 +4321,8 @@ static size_t conv_bwd_data_core_ws(const iseg_conv_geom* g, int32_t out_mode)
         }
         s += big + conv_pmax_bytes(g->N * g->H * g->W, g->C, hp, g->N, g->H, g->W);
     }
-    return s + kpad_bytes(g);
+    s += kpad_bytes(g);
+    return s > s1 ? s : s1;
 }
 
 // backward-data with the transposed weights either built here from w (KRSC) or
@@ -4286,6 +4340,20 @@ static int conv_bwd_data_core(const int8_t* dy, const int32_t* dy_exp, const int
     if (!dy_exp || !w_exp || !dx_exp || (g->N > 0 && (!dy || !w || !dx))) return ISEG_ERR_ARG;
     if (g->K * g->R * g->S > kMaxKred) return ISEG_ERR_UNSUPPORTED;
     if (!ws || ws_bytes < conv_bwd_data_core_ws(g, out_mode)) return ISEG_ERR_WORKSPACE;
+    if (strided_1x1(g) && ((uintptr_t)dx & 15) == 0) {
+        const iseg_conv_geom s = strided_1x1_inner(g, P, Q);
+        const size_t es = out_mode == ISEG_OUT_Q8 ? 1 : 4;
+        const size_t sub = align256((size_t)(g->N * P * Q * g->C) * es);
+        int rc = conv_bwd_data_core(dy, dy_exp, w, w_exp, wt_in, wt_kind, &s, out_mode, ws, dx_exp,
+                                    (char*)ws + sub, ws_bytes - sub, dev_status, stream);
+        if (rc) return rc;
+        conv_plan_set("strided_1x1");
+        const int32_t row16 = (int32_t)(g->C * (int64_t)es / 16);
+        hipLaunchKernelGGL(k_stride_scatter, dim3(grid_for(g->N * g->H * g->W * row16, 256, 8192)), dim3(256), 0,
+                           stream, (const uint4*)ws, (uint4*)dx, g->N, (int32_t)g->H, (int32_t)g->W, (int32_t)P,
+                           (int32_t)Q, g->stride_h, g->stride_w, row16);
+        return launch_ok();
+    }
     // ws: [max][transposed weights][per-block max partials][output staging]
     unsigned long long* maxp = (unsigned long long*)ws;
     const HaloPlan hp = halo_plan(g->N, g->H, g->W, g->K, g->C, (int)g->R, (int)g->S, g->stride_h, g->stride_w,

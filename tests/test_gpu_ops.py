@@ -110,6 +110,11 @@ CONV_SHAPES = [
     # 1x1 with a class count as K: backward-data pads K to a multiple of 64
     (2, 16, 16, 256, 150, 1, 1, 0, 1),
     (1, 9, 7, 128, 100, 1, 1, 0, 1),
+    # strided 1x1 (projection shortcuts): backward-data on the output grid,
+    # zeros interleaved (even and odd input sizes, stride 3)
+    (2, 10, 12, 32, 64, 1, 2, 0, 1),
+    (1, 9, 7, 64, 128, 1, 2, 0, 1),
+    (1, 11, 10, 16, 32, 1, 3, 0, 1),
 ] + [
     # strided backward-data with few dy channels (K): the phase path (FCN's
     # upsampling adjoints at 21 classes among them)
@@ -352,7 +357,7 @@ FULL_CASES = [
     ("data", 8, 32, 32, 2048, 256, 3, 1, 6, 6, "dma_stage16"),    # ASPP branches
     ("data", 8, 32, 32, 2048, 256, 3, 1, 12, 12, "dma_stage16"),
     ("data", 8, 32, 32, 2048, 256, 3, 1, 18, 18, "dma_stage16"),
-    ("data", 8, 64, 64, 512, 1024, 1, 2, 0, 1, "dma_stage16"),     # layer3.0 projection (strided)
+    ("data", 8, 64, 64, 512, 1024, 1, 2, 0, 1, "strided_1x1"),     # layer3.0 projection (strided)
 ]
 
 
