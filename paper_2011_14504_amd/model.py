@@ -32,7 +32,7 @@ from . import iseg
 
 class IntNet:
     def __init__(self, wl, inputs, device="cuda", lr_shift=10, bn_cfg=None, k_W=8, k_U=24, gq=1,
-                 bn_input="q8", branch_streams=3, replay_from=None):
+                 bn_input="q8", branch_streams=2, replay_from=None):
         if not (2 <= k_W <= 8 and 9 <= k_U <= 31 and gq in (1, 2)):
             raise ValueError("k_W must be in [2, 8], k_U in [9, 31], gq 1 or 2")
         if bn_input not in ("q8", "raw"):
@@ -63,7 +63,10 @@ class IntNet:
         # branches of the graph (a projection shortcut, the ASPP branches) run
         # on streams of their own (default priority) so that their
         # latency-bound kernels overlap the other branch; forward and
-        # backward of a node use the same stream
+        # backward of a node use the same stream.  Two branch streams: with
+        # the caller's stream and the side stream that is one hardware queue
+        # each at HIP's default of four per process (a fifth stream would
+        # share a queue, and serialize, with another)
         nb = branch_streams if self.side is not None else 0
         self.branch = [torch.cuda.Stream(device=self.dev) for _ in range(nb)]
         self.node_stream = self._plan_streams(wl["nodes"], nb)
