@@ -1682,10 +1682,6 @@ __global__ __launch_bounds__(256) void k_bnb_chan_exact(int64_t Mrows, int gx, i
 // code) entry gives the offset of the channel's class row in the block's LDS
 // copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
 // element costs two LDS reads and a handful of ALU operations.
-// Output pass: dx code = lut[c][sgn class][masked delta].  A per-(channel,
-// code) entry gives the offset of the channel's class row in the block's LDS
-// copy of the tables (bits 16..31) and the ReLU mask byte (bits 0..7), so each
-// element costs two LDS reads and a handful of ALU operations.
 // Exact E2: every block first takes E1's exponent from the channels' bounds
 // (block (0, 0) writes it and the parameter-gradient exponents) and rounds
 // its channels' staged values into the codes.
