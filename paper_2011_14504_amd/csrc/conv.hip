@@ -3599,7 +3599,7 @@ int64_t wgrad_splits(int64_t NPQ, int64_t tiles, int64_t* pps_out)
 }
 
 #ifndef ISEG_WGRAD_TAPS_BLOCKS
-#define ISEG_WGRAD_TAPS_BLOCKS 256 // target blocks of the all-taps backward-weight launch
+#define ISEG_WGRAD_TAPS_BLOCKS 128 // target blocks of the all-taps backward-weight launch (it runs beside the main chain: half the chip)
 #endif
 // shapes the all-taps kernel covers (the operand alignment is checked at launch):
 // filters of 9 taps (3x3); one wave per tap keeps a 576-thread block at three
