@@ -587,21 +587,22 @@ template <int CPL>
 __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ x, const int32_t* x_exp,
                                                     Stream st, FwdWs w, Saved sv, BnCfg cf, int32_t* dev_status)
 {
-    __shared__ unsigned long long sA[128];
+    __shared__ int32_t sSg[128], sNg[128];         // block sums of q and counts above each channel's T
     __shared__ long long tA[kNT];
     __shared__ int32_t rb[kNT / 64];
-    __shared__ long long wst[kWaves * 128];        // wave totals [wave][channel]
+    __shared__ int32_t wst[2 * kWaves * 128];      // wave totals [quantity][wave][channel]
     const bool fold = (st.G & (st.G - 1)) == 0 && st.G <= 64;
     int32_t s_x = *x_exp;
     if (!sx_ok(s_x)) {
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) set_status(dev_status, ISEG_DEV_RANGE);
         s_x = -14;     // keep shifts defined; outputs are unspecified
     }
-    if (!fold && (int)threadIdx.x < st.CS) sA[threadIdx.x] = 0;
+    if (!fold && (int)threadIdx.x < st.CS) { sSg[threadIdx.x] = 0; sNg[threadIdx.x] = 0; }
     // prologue: n_mu (Eq. 12) and the occupied code range of the slice's
     // channels from stats1's partial rows (every block of the slice forms them;
     // the slice's last block stores them)
     __shared__ int32_t sNmu[128], sLo[128], sHi[128];
+    __shared__ long long sSum[128];
     {
         const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
         const int32_t* ps = w.p_s1 + (int64_t)blockIdx.y * st.gx * CS;
@@ -638,84 +639,118 @@ __global__ __launch_bounds__(1024) void k_bnf_stats2(const int8_t* __restrict__ 
             }
             // mu/2 = S1 2^(s_x - 1) / M, code floor(mu/2 2^(k_mu-1) + 1/2)
             sNmu[t] = (int32_t)clamp_k128(rhu128((i128)sum, s_x - 1 + (cf.k_mu - 1), (i128)st.M), cf.k_mu);
+            sSum[t] = sum;
             sLo[t] = lo - 128;
             sHi[t] = hi - 128;
         }
     }
     __syncthreads();
+    // Sum |D| over the channel's elements, D = q 2^(s_x - g) - n_mu 2^(e_mu - g)
+    // (g = min(s_x, e_mu)), from int32 sums: with T the largest code whose D is
+    // not positive, sum |D| = 2^(s_x - g) (2 S_gt - S) + n_mu 2^(e_mu - g) (M - 2 N_gt),
+    // S_gt and N_gt the sum and count of the codes above T (the tail forms it)
     const int e_mu = 2 - cf.k_mu;
+    const int gg = s_x < e_mu ? s_x : e_mu;
     int g, rsub;
     const bool active = stream_lane(st, g, rsub);
-    int64_t a[CPL];
+    int32_t sg[CPL], ng[CPL];
 #pragma unroll
-    for (int i = 0; i < CPL; i++) a[i] = 0;
+    for (int i = 0; i < CPL; i++) { sg[i] = 0; ng[i] = 0; }
     if (active) {
         int c0 = blockIdx.y * st.CS + g * CPL;
-        const int gg = s_x < e_mu ? s_x : e_mu;
-        const int64_t mulq = (int64_t)1 << (s_x - gg);
-        int64_t off[CPL];
+        int32_t T[CPL];
 #pragma unroll
-        for (int i = 0; i < CPL; i++) off[i] = (int64_t)sNmu[g * CPL + i] * ((int64_t)1 << (e_mu - gg));
+        for (int i = 0; i < CPL; i++) {
+            const int64_t off = (int64_t)sNmu[g * CPL + i] * ((int64_t)1 << (e_mu - gg));
+            const int64_t t = off >> (s_x - gg);          // floor(off / 2^(s_x - g))
+            T[i] = (int32_t)(t < -129 ? -129 : (t > 127 ? 127 : t));
+        }
         stream_rows<CPL, 4>(st, x, c0, rsub, [&](int64_t, const Vec<CPL>& v) {
 #pragma unroll
             for (int i = 0; i < CPL; i++) {
-                int64_t D = (int64_t)sbyte(v.w[i >> 2], i & 3) * mulq - off[i];
-                a[i] += D < 0 ? -D : D;
+                const int q = sbyte(v.w[i >> 2], i & 3);
+                const bool up = q > T[i];
+                sg[i] += up ? q : 0;
+                ng[i] += up ? 1 : 0;
             }
         });
     }
     with_g(st.G, [&](auto gc) {
         constexpr int GG = decltype(gc)::value;
 #pragma unroll
-        for (int i = 0; i < CPL; i++) a[i] = fold_g<GG>(a[i], OpAdd());
+        for (int i = 0; i < CPL; i++) {
+            sg[i] = fold_g<GG>(sg[i], OpAdd());
+            ng[i] = fold_g<GG>(ng[i], OpAdd());
+        }
     });
     if (fold) {
         const int wv = threadIdx.x >> 6;
         if ((int)(threadIdx.x & 63) < st.G) {
 #pragma unroll
-            for (int i = 0; i < CPL; i++) wst[wv * 128 + g * CPL + i] = a[i];
+            for (int i = 0; i < CPL; i++) {
+                wst[wv * 128 + g * CPL + i] = sg[i];
+                wst[(kWaves + wv) * 128 + g * CPL + i] = ng[i];
+            }
         }
         __syncthreads();
         if ((int)threadIdx.x < st.CS) {
-            long long ba = 0;
+            int32_t bs = 0, bn = 0;
 #pragma unroll 4
-            for (int v = 0; v < kWaves; v++) ba += wst[v * 128 + threadIdx.x];
-            sA[threadIdx.x] = (unsigned long long)ba;
+            for (int v = 0; v < kWaves; v++) {
+                bs += wst[v * 128 + threadIdx.x];
+                bn += wst[(kWaves + v) * 128 + threadIdx.x];
+            }
+            sSg[threadIdx.x] = bs;
+            sNg[threadIdx.x] = bn;
         }
     } else if (active && group_leader(st.G)) {
 #pragma unroll
-        for (int i = 0; i < CPL; i++) atomicAdd(&sA[g * CPL + i], (unsigned long long)a[i]);
+        for (int i = 0; i < CPL; i++) {
+            atomicAdd(&sSg[g * CPL + i], sg[i]);
+            atomicAdd(&sNg[g * CPL + i], ng[i]);
+        }
     }
     __syncthreads();
+    // one 8-byte partial per channel: the sum (low half) and the count (high half)
     if ((int)threadIdx.x < st.CS)
-        st_x(&w.p_abs[(int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x], (long long)sA[threadIdx.x]);
+        st_x(&w.p_abs[(int64_t)blockIdx.x * st.C + blockIdx.y * st.CS + threadIdx.x],
+             (long long)(((uint64_t)(uint32_t)sNg[threadIdx.x] << 32) | (uint32_t)sSg[threadIdx.x]));
     if (!arrive_last(w.ctr + 1 + blockIdx.y, gridDim.x)) return;
     // slice tail: sigma (Eq. 13-14), the denominator and this channel's bound on max|xhat|
-    const int CS = st.CS, ng = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
+    const int CS = st.CS, ngr = kNT / CS, t = threadIdx.x, ch = t % CS, grp = t / CS;
     const int64_t cb = (int64_t)blockIdx.y * CS;
     const int e_sig = 2 - cf.k_sigma;
-    const int gg = s_x < e_mu ? s_x : e_mu;
     {
-        long long acc = 0;
-        if (grp < ng)
-            for (int b0 = grp; b0 < st.gx; b0 += kTailU * ng) {
+        long long acc_s = 0, acc_n = 0;
+        if (grp < ngr)
+            for (int b0 = grp; b0 < st.gx; b0 += kTailU * ngr) {
                 long long va[kTailU];
 #pragma unroll
                 for (int u = 0; u < kTailU; u++) {
-                    const int b = b0 + u * ng;
+                    const int b = b0 + u * ngr;
                     va[u] = ld_x(&w.p_abs[(int64_t)(b < st.gx ? b : b0) * st.C + cb + ch]);
                 }
 #pragma unroll
                 for (int u = 0; u < kTailU; u++)
-                    if (b0 + u * ng < st.gx) acc += va[u];
+                    if (b0 + u * ngr < st.gx) {
+                        acc_s += (int32_t)(uint32_t)((uint64_t)va[u] & 0xffffffffu);
+                        acc_n += (int32_t)(uint32_t)((uint64_t)va[u] >> 32);
+                    }
             }
-        tA[t] = acc;
+        tA[t] = acc_s;
+        __syncthreads();
+        if (t < CS)
+            for (int g2 = 1; g2 < ngr; g2++) acc_s += tA[g2 * CS + t];
+        __syncthreads();
+        tA[t] = acc_n;
         __syncthreads();
         if (t < CS) {
-            for (int g2 = 1; g2 < ng; g2++) acc += tA[g2 * CS + t];
+            for (int g2 = 1; g2 < ngr; g2++) acc_n += tA[g2 * CS + t];
             const int64_t c = cb + t;
+            const i128 mulq = pow2_128(s_x - gg), off = (i128)sNmu[t] * pow2_128(e_mu - gg);
+            const i128 acc = mulq * (2 * (i128)acc_s - (i128)sSum[t]) + off * ((i128)st.M - 2 * (i128)acc_n);
             // sigma/2 = sumabs 2^(g-1) / M ; n_sigma = floor(sigma/2 2^(k_sigma-1) + 1/2)
-            int32_t ns = (int32_t)clamp_k128(rhu128((i128)acc, gg - 1 + (cf.k_sigma - 1), (i128)st.M), cf.k_sigma);
+            int32_t ns = (int32_t)clamp_k128(rhu128(acc, gg - 1 + (cf.k_sigma - 1), (i128)st.M), cf.k_sigma);
             int32_t den = ns + cf.eps_code;
             if (den < 1) den = 1;
             sv.n_sigma[c] = ns;

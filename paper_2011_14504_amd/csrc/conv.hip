@@ -3448,8 +3448,18 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce_fin(const long long* __res
     const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
     uint64_t mx = 0;
     if (e < n) {
+        // eight chunk loads in flight (a loop of dependent single loads waits
+        // for each one: up to ~100 round trips for the stem's chunks)
         long long t = 0;
-        for (int c = 0; c < nchunks; c++) t += out2[(int64_t)c * n + e];
+        int c = 0;
+        for (; c + 8 <= nchunks; c += 8) {
+            long long v[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) v[u] = out2[(int64_t)(c + u) * n + e];
+#pragma unroll
+            for (int u = 0; u < 8; u++) t += v[u];
+        }
+        for (; c < nchunks; c++) t += out2[(int64_t)c * n + e];
         out[e] = t;
         mx = t < 0 ? (uint64_t)(-t) : (uint64_t)t;
     }
