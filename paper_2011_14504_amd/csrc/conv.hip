@@ -3203,25 +3203,76 @@ __global__ __launch_bounds__(256) void k_conv_wgrad_tr(WgradArgs a)
         }
 }
 
-// Backward-weight, all taps in one block (C % 64 == 0, K % 64 == 0, R*S <= 16):
+// Backward-weight, all taps in one block (C % 64 == 0, K % 64 == 0, R*S = 9):
 // wave w owns filter tap w, the block owns 64 output channels (k), one
-// 64-channel chunk of C and a run of output pixels.  Per 64-pixel step the dy
-// tile is staged once and shared by every wave; each wave stages its tap's
-// shifted x tile (neighbouring taps overlap, so those loads mostly hit L1).
-// Operands come from ds_read_b64_tr_b8; loads run two steps ahead.  Each
-// block writes its exact int32 partial tile (no atomics); k_wgrad_reduce adds
-// the splits in int64.
+// 64-channel chunk of C and a run of output pixels, and writes its exact
+// int32 partial tile (no atomics; k_wgrad_reduce adds the splits in int64).
+// Per step (64 output pixels) an LDS stage holds the dy tile (64 pixel rows
+// of 64 output channels), shared by every wave, and one x tile per tap (64
+// rows of 64 input channels, the tap's shifted pixels; zeros come from a zero
+// page for padding and past the split).  The stages are filled by
+// direct-to-LDS loads (global_load_lds, 16 bytes per lane) in a ring of
+// kWgStages, so loads run kWgStages - 1 steps ahead without holding
+// registers.  Rows are 64 bytes, unpadded; the 16-byte part p of row R sits
+// at part p ^ f(R), f(R) = ((R >> 1) ^ (R >> 4)) & 3, so the transposing
+// reads (rows 16 g + i, i < 8, of four lane groups g) spread over the banks
+// two rows per bank.
+constexpr int kWgStages = 3;
+
+__device__ __forceinline__ int wg_sw(int row) { return ((row >> 1) ^ (row >> 4)) & 3; }
+
+// The four 16 x 64 fragments of a tile (columns 0, 16, 32, 48), read with
+// ds_read_b64_tr_b8 in one asm block that ends in its own lgkmcnt wait: the
+// compiler's form of that read carries no LDS alias information, so after
+// direct-to-LDS loads it would wait for every one in flight (vmcnt 0) before
+// the read, and the ring would no longer run ahead.
+__device__ __forceinline__ uint32_t lds_off(const int8_t* p)
+{
+    return (uint32_t)(size_t)(const __attribute__((address_space(3))) int8_t*)p;
+}
+
+__device__ __forceinline__ void tr8_frags_sw(const int8_t* tile, int lane, v4i* f)
+{
+    const int g = lane >> 4, sl = lane & 15;
+    const int i = sl >> 1, h = sl & 1;
+    const int r0 = 16 * g + i, r1 = r0 + 8;
+    uint32_t ad[8];
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+        ad[2 * c] = lds_off(tile + r0 * 64 + ((c ^ wg_sw(r0)) << 4) + 8 * h);
+        ad[2 * c + 1] = lds_off(tile + r1 * 64 + ((c ^ wg_sw(r1)) << 4) + 8 * h);
+    }
+    v2i_t v0, v1, v2, v3, v4, v5, v6, v7;
+    asm volatile("ds_read_b64_tr_b8 %0, %8\n\t"
+                 "ds_read_b64_tr_b8 %1, %9\n\t"
+                 "ds_read_b64_tr_b8 %2, %10\n\t"
+                 "ds_read_b64_tr_b8 %3, %11\n\t"
+                 "ds_read_b64_tr_b8 %4, %12\n\t"
+                 "ds_read_b64_tr_b8 %5, %13\n\t"
+                 "ds_read_b64_tr_b8 %6, %14\n\t"
+                 "ds_read_b64_tr_b8 %7, %15\n\t"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(v0), "=&v"(v1), "=&v"(v2), "=&v"(v3), "=&v"(v4), "=&v"(v5), "=&v"(v6), "=&v"(v7)
+                 : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "v"(ad[4]), "v"(ad[5]), "v"(ad[6]), "v"(ad[7])
+                 : "memory");
+    f[0] = (v4i){v0.x, v0.y, v1.x, v1.y};
+    f[1] = (v4i){v2.x, v2.y, v3.x, v3.y};
+    f[2] = (v4i){v4.x, v4.y, v5.x, v5.y};
+    f[3] = (v4i){v6.x, v6.y, v7.x, v7.y};
+}
+
+size_t wgrad_taps_lds(int RS) { return (size_t)kWgStages * (1 + RS) * BK * 64 + 1024; }
+
 template <int RS>
 __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_t* __restrict__ part_out)
 {
-    constexpr int RA = 80, RB = 80;           // LDS row bytes (64 bytes + 16 pad)
-    constexpr int D = 2;                      // steps of global loads in flight
-    constexpr int nthr = 64 * RS;
-    constexpr int ndy = (256 + nthr - 1) / nthr;   // 16-byte dy pieces per thread
+    constexpr int S = kWgStages;
+    constexpr int TILE = BK * 64;                       // 64 rows of 64 bytes
+    constexpr int STAGE = (1 + RS) * TILE;              // the dy tile, then one x tile per tap
+    constexpr int LPW = 5;                              // loads per wave and step: 4 x rows of 16, 1 dy (or the zero page)
+    static_assert((S - 1) * LPW < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) int8_t smem[];
-    int8_t* As = smem;                                   // [2][64 * RA]
-    int8_t* Bs = smem + 2 * BK * RA;                     // [2][RS][64 * RB]
-    auto Bbuf = [&](int buf, int t) { return Bs + ((size_t)buf * RS + t) * (BK * RB); };
+    int8_t* dummy = smem + S * STAGE;                   // 1 KB sink of the zero-page loads that keep LPW uniform
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;         // wave = tap
@@ -3233,50 +3284,49 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
     if (pend > a.NPQ) pend = a.NPQ;
     const int64_t PQ = (int64_t)a.P * a.Q;
     const int tr = wave / a.S, ts = wave - (wave / a.S) * a.S;
+    const int rin = lane >> 2;                          // row of this lane in a 16-row load
 
-    // x cursors: this lane stages pixels lane/4 + 16 j (j < 4), part lane%4, of its tap
-    const int xpart = lane & 3;
+    // x cursors: pixel 16 j + rin of the step being issued (j < 4)
     int64_t xpix[4];
-    int32_t xn[4], xp[4], xq[4];
+    int32_t xn[4], xp[4], xq[4], xpart[4];
 #pragma unroll
     for (int j = 0; j < 4; j++) {
-        xpix[j] = pbeg + (lane >> 2) + 16 * j;
-        int64_t pp = xpix[j] < a.NPQ ? xpix[j] : 0;
+        xpix[j] = pbeg + 16 * j + rin;
+        const int64_t pp = xpix[j] < a.NPQ ? xpix[j] : 0;
         xn[j] = (int32_t)(pp / PQ);
-        int32_t rem = (int32_t)(pp - (int64_t)xn[j] * PQ);
+        const int32_t rem = (int32_t)(pp - (int64_t)xn[j] * PQ);
         xp[j] = rem / a.Q;
         xq[j] = rem - xp[j] * a.Q;
+        xpart[j] = (lane & 3) ^ wg_sw(16 * j + rin);
     }
-    int4 rx[D][4], rdy[D][ndy];
-    auto load = [&](int slot, int64_t pstep) {
+    const int dpart = (lane & 3) ^ wg_sw(16 * (wave & 3) + rin);
+    const int nsteps = (int)((pend - pbeg + BK - 1) / BK);
+
+    auto issue = [&](int st) {
+        if (st < nsteps) {
+            int8_t* base = smem + (st % S) * STAGE;
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-            int ih = xp[j] * a.sh - a.ph + tr * a.dh, iw = xq[j] * a.sw - a.pw + ts * a.dw;
-            bool v = xpix[j] < pend && ih >= 0 && iw >= 0 && ih < a.H && iw < a.W;
-            rx[slot][j] = v ? *(const int4*)(a.x + (((int64_t)xn[j] * a.H + ih) * a.W + iw) * a.C + c0 + xpart * 16)
-                            : make_int4(0, 0, 0, 0);
-            xpix[j] += BK;
-            xq[j] += BK;
-            while (xq[j] >= a.Q) { xq[j] -= a.Q; if (++xp[j] == a.P) { xp[j] = 0; ++xn[j]; } }
-        }
-#pragma unroll
-        for (int j = 0; j < ndy; j++) {
-            int pc = tid + j * nthr;
-            if (pc < 256) {
-                int64_t pix = pstep + (pc >> 2);
-                rdy[slot][j] = pix < pend ? *(const int4*)(a.dy + pix * a.K + k0 + (pc & 3) * 16)
-                                          : make_int4(0, 0, 0, 0);
+            for (int j = 0; j < 4; j++) {
+                const int ih = xp[j] * a.sh - a.ph + tr * a.dh, iw = xq[j] * a.sw - a.pw + ts * a.dw;
+                const bool v = xpix[j] < pend && ih >= 0 && iw >= 0 && ih < a.H && iw < a.W;
+                const void* g = v ? (const void*)(a.x + (((int64_t)xn[j] * a.H + ih) * a.W + iw) * a.C + c0 +
+                                                  xpart[j] * 16)
+                                  : (const void*)g_conv_zero;
+                dma16(g, base + (1 + wave) * TILE + j * 1024);
+                xpix[j] += BK;
+                xq[j] += BK;
+                while (xq[j] >= a.Q) { xq[j] -= a.Q; if (++xp[j] == a.P) { xp[j] = 0; ++xn[j]; } }
             }
-        }
-    };
-    auto store = [&](int buf, int slot) {
+            if (wave < 4) {
+                const int64_t pix = pbeg + (int64_t)st * BK + 16 * wave + rin;
+                const void* g = pix < pend ? (const void*)(a.dy + pix * a.K + k0 + dpart * 16) : (const void*)g_conv_zero;
+                dma16(g, base + wave * 1024);
+            } else {
+                dma16(g_conv_zero, dummy);
+            }
+        } else {
 #pragma unroll
-        for (int j = 0; j < 4; j++)
-            *(int4*)&Bbuf(buf, wave)[((lane >> 2) + 16 * j) * RB + xpart * 16] = rx[slot][j];
-#pragma unroll
-        for (int j = 0; j < ndy; j++) {
-            int pc = tid + j * nthr;
-            if (pc < 256) *(int4*)&As[(size_t)buf * BK * RA + (pc >> 2) * RA + (pc & 3) * 16] = rdy[slot][j];
+            for (int j = 0; j < LPW; j++) dma16(g_conv_zero, dummy);
         }
     };
 
@@ -3286,35 +3336,27 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
 #pragma unroll
         for (int j = 0; j < 4; j++) acc[i][j] = (v4i){0, 0, 0, 0};
 
-    const int nsteps = (int)((pend - pbeg + BK - 1) / BK);
 #pragma unroll
-    for (int u = 0; u < D; u++)
-        if (u < nsteps) load(u, pbeg + (int64_t)u * BK);
-    store(0, 0);
-    __syncthreads();
-    for (int st0 = 0; st0 < nsteps; st0 += D) {
+    for (int st = 0; st < S - 1; st++) issue(st);
+    for (int st = 0; st < nsteps; st++) {
+        // this wave's loads of step st have landed (those of the next S - 2
+        // steps may still be in flight) and its reads of step st - 1 are done;
+        // after the barrier every wave's are, so step st - 1's stage is free
+        wait_vm_lgkm0<(S - 2) * LPW>();
+        __builtin_amdgcn_s_barrier();
+        issue(st + S - 1);
+        const int8_t* A = smem + (st % S) * STAGE;
+        const int8_t* B = A + (1 + wave) * TILE;
+        v4i fa[4], fb[4];
+        tr8_frags_sw(A, lane, fa);
+        tr8_frags_sw(B, lane, fb);
 #pragma unroll
-        for (int u = 0; u < D; u++) {
-            const int st = st0 + u;
-            if (st < nsteps) {
-                const int8_t* A = As + (size_t)(st & 1) * BK * RA;
-                const int8_t* B = Bbuf(st & 1, wave);
-                v4i fa[4], fb[4];
+        for (int i = 0; i < 4; i++)
 #pragma unroll
-                for (int i = 0; i < 4; i++) fa[i] = tr8_frag(A, RA, i * 16, lane);
-#pragma unroll
-                for (int j = 0; j < 4; j++) fb[j] = tr8_frag(B, RB, j * 16, lane);
-#pragma unroll
-                for (int i = 0; i < 4; i++)
-#pragma unroll
-                    for (int j = 0; j < 4; j++)
-                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
-                if (st + 1 < nsteps) store((st + 1) & 1, (u + 1) % D);
-                if (st + D < nsteps) load(u, pbeg + (int64_t)(st + D) * BK);
-                __syncthreads();
-            }
-        }
+            for (int j = 0; j < 4; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
+    wait_vm<0>();                                       // no load into LDS outlives the block
 
     // exact int32 partial tile of this split: part_out[split][k][tap * C + c]
     int32_t* outp = part_out + (int64_t)blockIdx.y * a.K * a.RSC;
@@ -3720,8 +3762,8 @@ int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax
 {
     const int RS = a.R * a.S;
     int64_t splits = wgrad_taps_splits(a.NPQ, a.K, a.C, &a.pix_per_split);
-    const size_t lds = (size_t)(2 + 2 * RS) * BK * 80;
     if (RS != 9) return ISEG_ERR_UNSUPPORTED;
+    const size_t lds = wgrad_taps_lds(9);
     if (!lds_limit((const void*)k_conv_wgrad_taps<9>, lds))
         return ISEG_ERR_DEVICE;
     dim3 grid((unsigned)((a.C / 64) * (a.K / 64)), (unsigned)splits);
