@@ -3212,12 +3212,13 @@ __global__ __launch_bounds__(256) void k_conv_wgrad_tr(WgradArgs a)
 // rows of 64 input channels, the tap's shifted pixels; zeros come from a zero
 // page for padding and past the split).  The stages are filled by
 // direct-to-LDS loads (global_load_lds, 16 bytes per lane) in a ring of
-// kWgStages, so loads run kWgStages - 1 steps ahead without holding
-// registers.  Rows are 64 bytes, unpadded; the 16-byte part p of row R sits
-// at part p ^ f(R), f(R) = ((R >> 1) ^ (R >> 4)) & 3, so the transposing
-// reads (rows 16 g + i, i < 8, of four lane groups g) spread over the banks
-// two rows per bank.
-constexpr int kWgStages = 3;
+// kWgStages (four stages of 40 KB: the whole LDS), so loads run three steps
+// ahead without holding registers; waves 0-3 also load the dy rows, so the
+// wait counts differ by wave.  Rows are 64 bytes, unpadded; the 16-byte part
+// p of row R sits at part p ^ f(R), f(R) = ((R >> 1) ^ (R >> 4)) & 3, so the
+// transposing reads (rows 16 g + i, i < 8, of four lane groups g) spread
+// over the banks two rows per bank.
+constexpr int kWgStages = 4;
 
 __device__ __forceinline__ int wg_sw(int row) { return ((row >> 1) ^ (row >> 4)) & 3; }
 
@@ -3261,7 +3262,7 @@ __device__ __forceinline__ void tr8_frags_sw(const int8_t* tile, int lane, v4i* 
     f[3] = (v4i){v6.x, v6.y, v7.x, v7.y};
 }
 
-size_t wgrad_taps_lds(int RS) { return (size_t)kWgStages * (1 + RS) * BK * 64 + 1024; }
+size_t wgrad_taps_lds(int RS) { return (size_t)kWgStages * (1 + RS) * BK * 64; }
 
 template <int RS>
 __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_t* __restrict__ part_out)
@@ -3269,10 +3270,8 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
     constexpr int S = kWgStages;
     constexpr int TILE = BK * 64;                       // 64 rows of 64 bytes
     constexpr int STAGE = (1 + RS) * TILE;              // the dy tile, then one x tile per tap
-    constexpr int LPW = 5;                              // loads per wave and step: 4 x rows of 16, 1 dy (or the zero page)
-    static_assert((S - 1) * LPW < 64, "vmcnt range");
+    static_assert((S - 1) * 5 < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) int8_t smem[];
-    int8_t* dummy = smem + S * STAGE;                   // 1 KB sink of the zero-page loads that keep LPW uniform
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;         // wave = tap
@@ -3321,12 +3320,7 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
                 const int64_t pix = pbeg + (int64_t)st * BK + 16 * wave + rin;
                 const void* g = pix < pend ? (const void*)(a.dy + pix * a.K + k0 + dpart * 16) : (const void*)g_conv_zero;
                 dma16(g, base + wave * 1024);
-            } else {
-                dma16(g_conv_zero, dummy);
             }
-        } else {
-#pragma unroll
-            for (int j = 0; j < LPW; j++) dma16(g_conv_zero, dummy);
         }
     };
 
@@ -3342,7 +3336,9 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
         // this wave's loads of step st have landed (those of the next S - 2
         // steps may still be in flight) and its reads of step st - 1 are done;
         // after the barrier every wave's are, so step st - 1's stage is free
-        wait_vm_lgkm0<(S - 2) * LPW>();
+        if (st + S - 2 >= nsteps) wait_vm_lgkm0<0>();       // the last steps: fewer loads behind
+        else if (wave < 4) wait_vm_lgkm0<(S - 2) * 5>();    // x rows and a dy row per step
+        else wait_vm_lgkm0<(S - 2) * 4>();                  // x rows only
         __builtin_amdgcn_s_barrier();
         issue(st + S - 1);
         const int8_t* A = smem + (st % S) * STAGE;
