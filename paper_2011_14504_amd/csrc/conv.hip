@@ -3278,47 +3278,56 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
     const int nch = a.C / 64;
     const int c0 = (blockIdx.x % nch) * 64;
     const int k0 = (blockIdx.x / nch) * 64;
-    const int64_t pbeg = (int64_t)blockIdx.y * a.pix_per_split;
-    int64_t pend = pbeg + a.pix_per_split;
-    if (pend > a.NPQ) pend = a.NPQ;
-    const int64_t PQ = (int64_t)a.P * a.Q;
+    // 32-bit offsets: x and dy are below 2^31 bytes (checked by the caller)
+    const int32_t pbeg = (int32_t)(blockIdx.y * a.pix_per_split);
+    const int32_t pend = (int32_t)(pbeg + a.pix_per_split < a.NPQ ? pbeg + a.pix_per_split : a.NPQ);
+    const int32_t PQ = a.P * a.Q;
     const int tr = wave / a.S, ts = wave - (wave / a.S) * a.S;
     const int rin = lane >> 2;                          // row of this lane in a 16-row load
+    // this wave's tap: input pixel (p sh + dr, q sw + ds) of output pixel (p, q)
+    const int32_t dr = tr * a.dh - a.ph, ds = ts * a.dw - a.pw;
+    // the cursor's advance per step of 64 pixels: dp rows and dq columns
+    const int32_t dp = BK / a.Q, dq = BK - (BK / a.Q) * a.Q;
+    const int32_t HWC = a.H * a.W * a.C, WC = a.W * a.C;
+    const int8_t* zp = g_conv_zero;
 
     // x cursors: pixel 16 j + rin of the step being issued (j < 4)
-    int64_t xpix[4];
-    int32_t xn[4], xp[4], xq[4], xpart[4];
+    int32_t xpix[4], xn[4], xp[4], xq[4], xpart[4];
 #pragma unroll
     for (int j = 0; j < 4; j++) {
         xpix[j] = pbeg + 16 * j + rin;
-        const int64_t pp = xpix[j] < a.NPQ ? xpix[j] : 0;
-        xn[j] = (int32_t)(pp / PQ);
-        const int32_t rem = (int32_t)(pp - (int64_t)xn[j] * PQ);
+        const int32_t pp = xpix[j] < a.NPQ ? xpix[j] : 0;
+        xn[j] = pp / PQ;
+        const int32_t rem = pp - xn[j] * PQ;
         xp[j] = rem / a.Q;
         xq[j] = rem - xp[j] * a.Q;
         xpart[j] = (lane & 3) ^ wg_sw(16 * j + rin);
     }
     const int dpart = (lane & 3) ^ wg_sw(16 * (wave & 3) + rin);
-    const int nsteps = (int)((pend - pbeg + BK - 1) / BK);
+    const int nsteps = (pend - pbeg + BK - 1) / BK;
 
     auto issue = [&](int st) {
         if (st < nsteps) {
             int8_t* base = smem + (st % S) * STAGE;
 #pragma unroll
             for (int j = 0; j < 4; j++) {
-                const int ih = xp[j] * a.sh - a.ph + tr * a.dh, iw = xq[j] * a.sw - a.pw + ts * a.dw;
-                const bool v = xpix[j] < pend && ih >= 0 && iw >= 0 && ih < a.H && iw < a.W;
-                const void* g = v ? (const void*)(a.x + (((int64_t)xn[j] * a.H + ih) * a.W + iw) * a.C + c0 +
-                                                  xpart[j] * 16)
-                                  : (const void*)g_conv_zero;
+                const int32_t ih = xp[j] * a.sh + dr, iw = xq[j] * a.sw + ds;
+                const bool v = xpix[j] < pend && (uint32_t)ih < (uint32_t)a.H && (uint32_t)iw < (uint32_t)a.W;
+                // unsigned (wrapping) arithmetic: a lane outside the image may form an
+                // offset out of range, which the select discards
+                const uint32_t off = (uint32_t)xn[j] * (uint32_t)HWC + (uint32_t)ih * (uint32_t)WC +
+                                     (uint32_t)iw * (uint32_t)a.C + (uint32_t)(c0 + xpart[j] * 16);
+                const int8_t* g = v ? a.x + off : zp;
                 dma16(g, base + (1 + wave) * TILE + j * 1024);
                 xpix[j] += BK;
-                xq[j] += BK;
-                while (xq[j] >= a.Q) { xq[j] -= a.Q; if (++xp[j] == a.P) { xp[j] = 0; ++xn[j]; } }
+                xq[j] += dq;
+                xp[j] += dp;
+                if (xq[j] >= a.Q) { xq[j] -= a.Q; ++xp[j]; }
+                while (xp[j] >= a.P) { xp[j] -= a.P; ++xn[j]; }
             }
             if (wave < 4) {
-                const int64_t pix = pbeg + (int64_t)st * BK + 16 * wave + rin;
-                const void* g = pix < pend ? (const void*)(a.dy + pix * a.K + k0 + dpart * 16) : (const void*)g_conv_zero;
+                const int32_t pix = pbeg + st * BK + 16 * wave + rin;
+                const int8_t* g = pix < pend ? a.dy + ((uint32_t)pix * (uint32_t)a.K + (uint32_t)(k0 + dpart * 16)) : zp;
                 dma16(g, base + wave * 1024);
             }
         }
@@ -4976,7 +4985,8 @@ extern "C" int iseg_conv_bwd_weight(const int8_t* dy, const int32_t* dy_exp, con
     a.RSC = (int32_t)(g->R * g->S * Cp);
     a.sh = g->stride_h; a.sw = g->stride_w; a.ph = g->pad_h; a.pw = g->pad_w;
     a.dh = g->dil_h; a.dw = g->dil_w;
-    if (Cp == g->C && wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) && (((uintptr_t)x | (uintptr_t)dy) & 15) == 0) {
+    if (Cp == g->C && wgrad_taps_shape(NPQ, g->K, Cp, g->R * g->S) && (((uintptr_t)x | (uintptr_t)dy) & 15) == 0 &&
+        g->N * g->H * g->W * Cp < ((int64_t)1 << 31) && NPQ * g->K < ((int64_t)1 << 31)) {
         conv_plan_set("wgrad_taps");
         if ((rc = launch_wgrad_taps(a, part, raw ? nullptr : pmax, &npmax, stream, raw ? nullptr : &qg))) return rc;
         return finish();
