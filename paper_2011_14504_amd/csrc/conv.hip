@@ -3093,46 +3093,54 @@ __global__ __launch_bounds__(256) void k_conv_wgrad_tr(WgradArgs a)
     const int tg = blockIdx.x / nch;
     const int c0 = (blockIdx.x - tg * nch) * 64;
     const int k0 = blockIdx.y * BM;
-    const int64_t pbeg = (int64_t)blockIdx.z * a.pix_per_split;
-    int64_t pend = pbeg + a.pix_per_split;
-    if (pend > a.NPQ) pend = a.NPQ;
+    // 32-bit offsets: x and dy are below 2^31 bytes (wgrad_tr_ok)
+    const int32_t pbeg = (int32_t)(blockIdx.z * a.pix_per_split);
+    const int32_t pend = (int32_t)(pbeg + a.pix_per_split < a.NPQ ? pbeg + a.pix_per_split : a.NPQ);
 
     // this thread stages pixel (step base + tid/4), 16-byte part tid%4
     const int prow = tid >> 2, part = tid & 3;
-    int tr[TAPS], ts[TAPS];
+    int dr[TAPS], ds[TAPS];                   // input pixel (p sh + dr, q sw + ds) of output pixel (p, q)
     bool tok[TAPS];
 #pragma unroll
     for (int t = 0; t < TAPS; t++) {
         int tap = tg * TAPS + t;
         tok[t] = tap < a.R * a.S;
-        tr[t] = tok[t] ? tap / a.S : 0;
-        ts[t] = tok[t] ? tap - tr[t] * a.S : 0;
+        const int tr = tok[t] ? tap / a.S : 0;
+        dr[t] = tr * a.dh - a.ph;
+        ds[t] = (tok[t] ? tap - tr * a.S : 0) * a.dw - a.pw;
     }
-    // load cursor: coordinates of this thread's pixel, advanced 64 pixels per step
-    int64_t pix = pbeg + prow;
-    const int64_t PQ = (int64_t)a.P * a.Q;
-    int32_t pn = (int32_t)(pix / PQ);
-    int32_t rem = (int32_t)(pix - (int64_t)pn * PQ);
+    // load cursor: coordinates of this thread's pixel, advanced 64 pixels (dp
+    // rows and dq columns) per step
+    int32_t pix = pbeg + prow;
+    const int32_t PQ = a.P * a.Q;
+    int32_t pn = pix / PQ;
+    int32_t rem = pix - pn * PQ;
     int32_t pp = rem / a.Q, pq = rem - (rem / a.Q) * a.Q;
+    const int32_t dp = BK / a.Q, dq = BK - (BK / a.Q) * a.Q;
+    const uint32_t HWC = (uint32_t)a.H * a.W * a.C, WC = (uint32_t)a.W * a.C;
 
     int4 ra[D][PA], rb[D][TAPS];
     auto load = [&](int4* pa, int4* pb) {
         const bool ok = pix < pend;
 #pragma unroll
-        for (int j = 0; j < PA; j++) {
-            int kc = k0 + part * 16 + 64 * j;
-            pa[j] = ok && kc < a.K ? *(const int4*)(a.dy + pix * a.K + kc) : make_int4(0, 0, 0, 0);
+        for (int j = 0; j < PA; j++) {          // k0 + part * 16 + 64 j < K: K % BM == 0
+            const uint32_t off = (uint32_t)pix * (uint32_t)a.K + (uint32_t)(k0 + part * 16 + 64 * j);
+            pa[j] = ok ? *(const int4*)(a.dy + off) : make_int4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int t = 0; t < TAPS; t++) {
-            int ih = pp * a.sh - a.ph + tr[t] * a.dh, iw = pq * a.sw - a.pw + ts[t] * a.dw;
-            bool v = ok && tok[t] && ih >= 0 && iw >= 0 && ih < a.H && iw < a.W;
-            pb[t] = v ? *(const int4*)(a.x + (((int64_t)pn * a.H + ih) * a.W + iw) * a.C + c0 + part * 16)
-                      : make_int4(0, 0, 0, 0);
+            const int ih = pp * a.sh + dr[t], iw = pq * a.sw + ds[t];
+            const bool v = ok && tok[t] && (uint32_t)ih < (uint32_t)a.H && (uint32_t)iw < (uint32_t)a.W;
+            // unsigned (wrapping) arithmetic: an offset out of range is never loaded
+            const uint32_t off = (uint32_t)pn * HWC + (uint32_t)ih * WC + (uint32_t)iw * (uint32_t)a.C +
+                                 (uint32_t)(c0 + part * 16);
+            pb[t] = v ? *(const int4*)(a.x + off) : make_int4(0, 0, 0, 0);
         }
         pix += BK;
-        pq += BK;
-        while (pq >= a.Q) { pq -= a.Q; if (++pp == a.P) { pp = 0; ++pn; } }
+        pq += dq;
+        pp += dp;
+        if (pq >= a.Q) { pq -= a.Q; ++pp; }
+        while (pp >= a.P) { pp -= a.P; ++pn; }
     };
     auto store = [&](int buf, const int4* pa, const int4* pb) {
 #pragma unroll
@@ -3783,7 +3791,9 @@ int launch_wgrad_taps(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* npmax
 // K % 64 == 0, 16-byte aligned operands)
 bool wgrad_tr_ok(const WgradArgs& a)
 {
-    return a.NPQ > 0 && a.C % 64 == 0 && a.K % 64 == 0 && (((uintptr_t)a.x | (uintptr_t)a.dy) & 15) == 0;
+    const int64_t nimg = a.P > 0 && a.Q > 0 ? a.NPQ / ((int64_t)a.P * a.Q) : 0;
+    return a.NPQ > 0 && a.C % 64 == 0 && a.K % 64 == 0 && (((uintptr_t)a.x | (uintptr_t)a.dy) & 15) == 0 &&
+           nimg * a.H * a.W * a.C < ((int64_t)1 << 31) && a.NPQ * a.K < ((int64_t)1 << 31);
 }
 
 int64_t wgrad_tr_splits(const WgradArgs& a, int64_t* pps)
@@ -3832,8 +3842,7 @@ int launch_wgrad_tr_split(WgradArgs a, int32_t* part, uint64_t* pmax, int64_t* n
 
 int launch_wgrad(WgradArgs a, hipStream_t s)
 {
-    if (a.NPQ > 0 && a.C % 64 == 0 && a.K % 64 == 0 &&
-        (((uintptr_t)a.x | (uintptr_t)a.dy) & 15) == 0) {
+    if (wgrad_tr_ok(a)) {
         const int BMt = a.K % 128 == 0 ? 128 : 64;
         const int RS = a.R * a.S;
         const int TAPS = RS > 1 ? 2 : 1;
