@@ -3290,28 +3290,40 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
     const int32_t pbeg = (int32_t)(blockIdx.y * a.pix_per_split);
     const int32_t pend = (int32_t)(pbeg + a.pix_per_split < a.NPQ ? pbeg + a.pix_per_split : a.NPQ);
     const int32_t PQ = a.P * a.Q;
-    const int tr = wave / a.S, ts = wave - (wave / a.S) * a.S;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);            // uniform: LDS bases in scalar registers
+    const int tr = wv / a.S, ts = wv - (wv / a.S) * a.S;
     const int rin = lane >> 2;                          // row of this lane in a 16-row load
-    // this wave's tap: input pixel (p sh + dr, q sw + ds) of output pixel (p, q)
-    const int32_t dr = tr * a.dh - a.ph, ds = ts * a.dw - a.pw;
-    // the cursor's advance per step of 64 pixels: dp rows and dq columns
+    // the zero page's address held in scalar registers (not re-derived per load)
+    uint64_t zbits = (uint64_t)(uintptr_t)g_conv_zero;
+    asm volatile("" : "+s"(zbits));
+    const int8_t* zp = (const int8_t*)(uintptr_t)zbits;
+    // Cursor j (pixel 16 j + rin of the step being issued) carries its output
+    // coordinates, the tap's input coordinates (ih, iw) = (p sh + r dh - ph,
+    // q sw + s dw - pw) and the byte offset of that input pixel's 16-byte part
+    // (unsigned, wrapping: meaningful only where (ih, iw) is in the image).
+    // A step of 64 pixels advances dp rows and dq columns.
     const int32_t dp = BK / a.Q, dq = BK - (BK / a.Q) * a.Q;
-    const int32_t HWC = a.H * a.W * a.C, WC = a.W * a.C;
-    const int8_t* zp = g_conv_zero;
-
-    // x cursors: pixel 16 j + rin of the step being issued (j < 4)
-    int32_t xpix[4], xn[4], xp[4], xq[4], xpart[4];
+    const uint32_t C = (uint32_t)a.C, WC = (uint32_t)a.W * C, HWC = (uint32_t)a.H * WC;
+    const uint32_t o_q = (uint32_t)(dq * a.sw) * C + (uint32_t)(dp * a.sh) * WC;   // per step
+    const uint32_t o_row = (uint32_t)a.sh * WC - (uint32_t)(a.Q * a.sw) * C;       // column wrap
+    const uint32_t o_img = HWC - (uint32_t)(a.P * a.sh) * WC;                       // row wrap
+    int32_t xpix[4], xp[4], xq[4], ih[4], iw[4];
+    uint32_t xoff[4];
 #pragma unroll
     for (int j = 0; j < 4; j++) {
         xpix[j] = pbeg + 16 * j + rin;
         const int32_t pp = xpix[j] < a.NPQ ? xpix[j] : 0;
-        xn[j] = pp / PQ;
-        const int32_t rem = pp - xn[j] * PQ;
+        const int32_t n = pp / PQ, rem = pp - n * PQ;
         xp[j] = rem / a.Q;
         xq[j] = rem - xp[j] * a.Q;
-        xpart[j] = (lane & 3) ^ wg_sw(16 * j + rin);
+        ih[j] = xp[j] * a.sh + tr * a.dh - a.ph;
+        iw[j] = xq[j] * a.sw + ts * a.dw - a.pw;
+        const int xpart = (lane & 3) ^ wg_sw(16 * j + rin);
+        xoff[j] = (uint32_t)n * HWC + (uint32_t)ih[j] * WC + (uint32_t)iw[j] * C + (uint32_t)(c0 + xpart * 16);
     }
-    const int dpart = (lane & 3) ^ wg_sw(16 * (wave & 3) + rin);
+    const int dpart = (lane & 3) ^ wg_sw(16 * (wv & 3) + rin);
+    uint32_t doff = (uint32_t)(pbeg + 16 * (wv & 3) + rin) * (uint32_t)a.K + (uint32_t)(k0 + dpart * 16);
+    const uint32_t dstep = (uint32_t)BK * (uint32_t)a.K;
     const int nsteps = (pend - pbeg + BK - 1) / BK;
 
     auto issue = [&](int st) {
@@ -3319,24 +3331,29 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
             int8_t* base = smem + (st % S) * STAGE;
 #pragma unroll
             for (int j = 0; j < 4; j++) {
-                const int32_t ih = xp[j] * a.sh + dr, iw = xq[j] * a.sw + ds;
-                const bool v = xpix[j] < pend && (uint32_t)ih < (uint32_t)a.H && (uint32_t)iw < (uint32_t)a.W;
-                // unsigned (wrapping) arithmetic: a lane outside the image may form an
-                // offset out of range, which the select discards
-                const uint32_t off = (uint32_t)xn[j] * (uint32_t)HWC + (uint32_t)ih * (uint32_t)WC +
-                                     (uint32_t)iw * (uint32_t)a.C + (uint32_t)(c0 + xpart[j] * 16);
-                const int8_t* g = v ? a.x + off : zp;
-                dma16(g, base + (1 + wave) * TILE + j * 1024);
+                const bool v = xpix[j] < pend && (uint32_t)ih[j] < (uint32_t)a.H && (uint32_t)iw[j] < (uint32_t)a.W;
+                dma16(v ? a.x + xoff[j] : zp, base + (1 + wv) * TILE + j * 1024);
                 xpix[j] += BK;
                 xq[j] += dq;
                 xp[j] += dp;
-                if (xq[j] >= a.Q) { xq[j] -= a.Q; ++xp[j]; }
-                while (xp[j] >= a.P) { xp[j] -= a.P; ++xn[j]; }
+                ih[j] += dp * a.sh;
+                iw[j] += dq * a.sw;
+                xoff[j] += o_q;
+                if (xq[j] >= a.Q) {
+                    xq[j] -= a.Q; ++xp[j];
+                    ih[j] += a.sh; iw[j] -= a.Q * a.sw;
+                    xoff[j] += o_row;
+                }
+                while (xp[j] >= a.P) {
+                    xp[j] -= a.P;
+                    ih[j] -= a.P * a.sh;
+                    xoff[j] += o_img;
+                }
             }
-            if (wave < 4) {
-                const int32_t pix = pbeg + st * BK + 16 * wave + rin;
-                const int8_t* g = pix < pend ? a.dy + ((uint32_t)pix * (uint32_t)a.K + (uint32_t)(k0 + dpart * 16)) : zp;
-                dma16(g, base + wave * 1024);
+            if (wv < 4) {
+                const int32_t pix = pbeg + st * BK + 16 * wv + rin;
+                dma16(pix < pend ? a.dy + doff : zp, base + wv * 1024);
+                doff += dstep;
             }
         }
     };
@@ -3354,12 +3371,12 @@ __global__ __launch_bounds__(64 * RS) void k_conv_wgrad_taps(WgradArgs a, int32_
         // steps may still be in flight) and its reads of step st - 1 are done;
         // after the barrier every wave's are, so step st - 1's stage is free
         if (st + S - 2 >= nsteps) wait_vm_lgkm0<0>();       // the last steps: fewer loads behind
-        else if (wave < 4) wait_vm_lgkm0<(S - 2) * 5>();    // x rows and a dy row per step
+        else if (wv < 4) wait_vm_lgkm0<(S - 2) * 5>();      // x rows and a dy row per step
         else wait_vm_lgkm0<(S - 2) * 4>();                  // x rows only
         __builtin_amdgcn_s_barrier();
         issue(st + S - 1);
         const int8_t* A = smem + (st % S) * STAGE;
-        const int8_t* B = A + (1 + wave) * TILE;
+        const int8_t* B = A + (1 + wv) * TILE;
         v4i fa[4], fb[4];
         tr8_frags_sw(A, lane, fa);
         tr8_frags_sw(B, lane, fb);
